@@ -1,0 +1,154 @@
+"""Benchmark: the full TAPS cost-table build on one MI355X.
+
+One step = one pass of the whole hot path on the 96-layer GPT-style graph
+(hidden 12288, 96 heads, seq 2048, batch 64, bf16) on a modeled cluster of
+16 nodes x 8 devices (600 GB/s inside a node, 100 GB/s between nodes):
+enumerate every strategy of every operator, compute the node (intra-op)
+table and the edge (redistribution) table -- 599,136 strategies and
+98,668,128 edge entries, left resident in HBM.  The graph description is
+packed into the C structs once, outside the timed region.
+
+Prints one JSON line.  `value` is edge entries per second of whole steps;
+`roofline` relates the edge-table call (whose kernel dominates the step) to
+MI355X's 8 TB/s HBM: each entry writes 36 bytes (t 8, vol 8, intra 8, inter
+8, meta 4).  `cpu_baseline` times the CPU oracle, single-threaded, on the
+first layers of the same graph.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+BYTES_PER_ENTRY = 36
+
+
+def log(msg: str) -> None:
+    print(msg, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(workload, cluster, layers: int) -> dict:
+    """The oracle as it stands, single-threaded, on the ops and edges of the
+    graph's first `layers` transformer layers."""
+    from oracle import oracle as O
+
+    g = workload.graph
+    ops_per_layer = 14
+    keep = set(range(layers * ops_per_layer))
+    edges = [e for e in g.edges if e.src in keep and e.dst in keep]
+    t0 = time.perf_counter()
+    strats = {k: O.enumerate_strategies(g.ops[k], cluster.devices) for k in sorted(keep)}
+    for k in sorted(keep):
+        O.node_table(g.ops[k], strats[k], cluster)
+    entries = 0
+    for e in edges:
+        tab = O.edge_table(g.ops[e.src], strats[e.src], g.ops[e.dst], e.slot, strats[e.dst],
+                           cluster)
+        entries += tab.size
+    dt = time.perf_counter() - t0
+    return {"value": entries / dt, "unit": "edge entries/s", "cores": 1, "kind": "oracle",
+            "sample": f"first {layers} of 96 layers: {len(keep)} ops, {len(edges)} edges, "
+                      f"{entries} edge entries, enumeration + node + edge tables in {dt:.2f} s"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=5, help="workload 1..5 (default: 5, the largest)")
+    ap.add_argument("--cpu-layers", type=int, default=3,
+                    help="layers of the graph the CPU oracle baseline covers (0 = skip)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: the cost tables of one modeled cluster are built on a "
+              f"single device (asked for --gpus {args.gpus}).", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    from paper_2301_04285_amd import taps, workloads as W
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 1
+    w = W.config(args.config)
+    cname, cl = w.clusters[0]
+    g = taps.pack_graph(w.graph)
+    log(f"[bench] {w.name}/{cname}: {g.n_ops} ops, {g.n_edges} edges")
+
+    stream = torch.cuda.current_stream()
+    tabs = taps.build_tables(g, cl, stream=stream)    # allocates the outputs once
+    torch.cuda.synchronize()
+    entries = int(tabs.edge_offsets[-1])
+    strategies = int(tabs.op_offsets[-1])
+    log(f"[bench] {strategies} strategies, {entries} edge entries")
+
+    def step(ev=None):
+        offs, strat = taps.taps_enumerate_strategies(g, cl, stream=stream, out=tabs.strategies)
+        taps.taps_node_costs(g, cl, strat, offs, out=tabs.node, stream=stream)
+        if ev is not None:
+            ev[0].record(stream)
+        taps.taps_edge_costs(g, cl, strat, offs, out=tabs.edge, stream=stream)
+        if ev is not None:
+            ev[1].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"[bench] warmup {args.warmup} done")
+
+    events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        step(events[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    edge_ms = float(np.mean([a.elapsed_time(b) for a, b in events]))
+    ms_per_step = wall * 1e3 / args.steps
+    log(f"[bench] {args.steps} steps: {ms_per_step:.3f} ms/step, edge call {edge_ms:.3f} ms")
+
+    bytes_per_launch = BYTES_PER_ENTRY * entries
+    achieved = bytes_per_launch / (edge_ms * 1e-3) / 1e9
+    out = {
+        "metric": "edge-cost entries/sec on 1 GPU (full cost-table build: enumerate + node + edge)",
+        "value": entries / (ms_per_step * 1e-3),
+        "unit": "edge entries/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u64",
+        "data": "synthetic",
+        "config": {"workload": f"{w.name}/{cname}", "edge_entries": entries,
+                   "strategies": strategies, "ops": g.n_ops, "edges": g.n_edges,
+                   "modeled_devices": cl.devices, "devices_per_node": cl.devices_per_node,
+                   "bw_intra_GBps": cl.bw_intra / 1e9, "bw_inter_GBps": cl.bw_inter / 1e9},
+        "build_ms": ms_per_step,
+        "edge_call_ms": edge_ms,
+        "edge_entries_per_s": entries / (edge_ms * 1e-3),
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBPS, "traffic": None},
+    }
+    if args.cpu_layers > 0 and args.config == 5:
+        log(f"[bench] CPU oracle baseline on {args.cpu_layers} layers")
+        out["cpu_baseline"] = cpu_baseline(w, cl, args.cpu_layers)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,203 @@
+/*
+ * taps.h -- C ABI of the MI355X TAPS cost-table library.
+ *
+ * TAPS (Liang et al., "TAPS: Topology-Aware Intra-Operator Parallelism
+ * Strategy Searching Algorithm for Deep Neural Networks", arXiv 2301.04285)
+ * chooses one intra-operator sharding strategy per operator of a computation
+ * graph by solving an integer program over an auxiliary graph whose
+ * vertices are (operator, strategy) pairs and whose edges are (producer
+ * strategy, consumer strategy) pairs.  This library builds, on one GPU, the
+ * tables that program consumes:
+ *
+ *   1. taps_enumerate_strategies -- every strategy of every operator
+ *      (GenerateStrategySet, Auxiliary Graph section, Table 3);
+ *   2. taps_node_costs -- the intra-operator communication cost of every
+ *      strategy (Communication Cost Model section: Eq. 5-8, Algorithm 2,
+ *      Eq. 11-12);
+ *   3. taps_edge_costs -- for every graph edge and every (producer strategy,
+ *      consumer strategy) pair the cost of redistributing the edge tensor
+ *      (Table 1 unification, Table 2 / Algorithm 1 sequences, Eq. 9-14,
+ *      Algorithm 3; Algorithm 4 gives the pair loop).
+ *
+ * The inputs follow the paper's problem statement (Overview section): a
+ * computation graph whose operators carry shapes and types, and a device
+ * graph reduced to what the cost model uses -- the device count, the devices
+ * per node and the intra- and inter-node bandwidths.
+ *
+ * Conventions
+ *   - N = nodes * devices_per_node devices, L = devices_per_node; both must be
+ *     powers of two and N <= 2^TAPS_MAX_LEVELS.  Device rank r is mixed-radix
+ *     over the device matrix with its innermost axis fastest and lives on
+ *     node r / L.
+ *   - A strategy splits some partitionable op axes; the degrees are powers of
+ *     two that multiply to N; pos orders the split axes on the device matrix
+ *     (pos 0 innermost = adjacent devices).  A degree must divide its axis.
+ *   - Volumes are unsigned integers in units of bytes x N ("nb"), so every
+ *     per-device volume of the paper's formulas is exact.  Times are seconds.
+ *   - Every record has five fields, stored as five separate arrays (SoA):
+ *       t      double   cost in seconds = intra/(N B_intra) + inter/(N B_inter)
+ *       vol    uint64   communication volume (nb) -- the volume-based model
+ *       intra  uint64   nb carried by intra-node links
+ *       inter  uint64   nb carried by inter-node links, each collective's
+ *                       link volume multiplied by its inter-node group count
+ *       meta   uint32   bits 0-1: chosen sequence (edges; 0 for nodes)
+ *                       bits 2-6: number of collectives
+ *                       bits 7-11: collectives that leave a node
+ *                       bits 12-31: sum of their inter-node group counts
+ *
+ * Memory and streams
+ *   - Graph, cluster and offset arrays are host memory owned by the caller
+ *     and read only during the call.  Strategy and table arrays are device
+ *     memory (HIP) owned by the caller.  The library allocates and frees its
+ *     own device scratch in stream order on the given stream and keeps no
+ *     pointer of the caller after the call returns.
+ *   - Kernels are asynchronous on `stream` (a hipStream_t; NULL = the null
+ *     stream): the tables are complete once that stream has been
+ *     synchronised.  taps_enumerate_strategies synchronises `stream` once to
+ *     read the per-operator counts back.
+ *   - Calls on distinct outputs may run concurrently from several threads.
+ *
+ * Errors
+ *   - Every call returns a taps_status; arguments are validated before any
+ *     GPU work and nothing is written on a validation error.
+ *     taps_last_error() returns a thread-local description of the last
+ *     failure of the calling thread.
+ */
+#ifndef TAPS_H
+#define TAPS_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define TAPS_MAX_AXES 8     /* axes of one operator */
+#define TAPS_MAX_RANK 8     /* dimensions of one tensor */
+#define TAPS_MAX_INPUTS 4   /* activation inputs of one operator */
+#define TAPS_MAX_WEIGHTS 4  /* weights of one operator */
+#define TAPS_MAX_LEVELS 8   /* N <= 2^8 = 256 devices */
+#define TAPS_MAX_TENSOR_BYTES (1ull << 40) /* keeps every volume exact in 64 bits */
+
+typedef enum {
+    TAPS_OK = 0,
+    TAPS_ERR_ARG = 1,         /* NULL pointer, index out of range, malformed operator */
+    TAPS_ERR_TOPOLOGY = 2,    /* nodes or devices per node not a power of two,
+                                 N > 2^TAPS_MAX_LEVELS, a zero bandwidth */
+    TAPS_ERR_SHAPE = 3,       /* an edge's two tensor shapes disagree */
+    TAPS_ERR_NO_STRATEGY = 4, /* an operator has no strategy on N devices */
+    TAPS_ERR_CAPACITY = 5,    /* the output arrays are too small */
+    TAPS_ERR_DEVICE = 6       /* a HIP runtime error */
+} taps_status;
+
+/* The modeled cluster (device graph of the problem statement). */
+typedef struct {
+    uint32_t nodes;
+    uint32_t devices_per_node; /* L */
+    uint64_t bw_intra;         /* bytes per second between devices of one node */
+    uint64_t bw_inter;         /* bytes per second of one node's inter-node link */
+} taps_cluster;
+
+/* A tensor of an operator: dimension d is op axis axis[d]. */
+typedef struct {
+    uint8_t rank;
+    uint8_t axis[TAPS_MAX_RANK];
+} taps_tensor;
+
+/* An operator as an einsum over its axes: `out` is produced, `in` are
+ * activations (edges attach to them), `w` are weights.  Bit a of part_mask
+ * marks axis a as partitionable.  dtype_bytes is the element size of every
+ * tensor of the operator. */
+typedef struct {
+    uint8_t n_axes, part_mask, dtype_bytes, n_in, n_w;
+    int64_t axis_len[TAPS_MAX_AXES];
+    taps_tensor in[TAPS_MAX_INPUTS];
+    taps_tensor w[TAPS_MAX_WEIGHTS];
+    taps_tensor out;
+} taps_op;
+
+/* ops[src_op].out feeds ops[dst_op].in[dst_slot]; both ends must have the
+ * same rank and the same length in every dimension. */
+typedef struct {
+    uint32_t src_op, dst_op, dst_slot;
+} taps_edge;
+
+typedef struct {
+    uint32_t n_ops, n_edges;
+    const taps_op *ops;
+    const taps_edge *edges;
+} taps_graph;
+
+/* One strategy: per op axis, log2 of its degree (0 = not split) and its
+ * device-matrix position (-1 = not split). */
+typedef struct {
+    uint8_t log2_deg[TAPS_MAX_AXES];
+    int8_t pos[TAPS_MAX_AXES];
+} taps_strategy;
+
+/* Device arrays of one table, one element per record. */
+typedef struct {
+    double *t;
+    uint64_t *vol;
+    uint64_t *intra;
+    uint64_t *inter;
+    uint32_t *meta;
+} taps_table;
+
+/* GenerateStrategySet for every operator (Auxiliary Graph section; the
+ * count sum_{i=1}^{min(p,n)} i! C(p,i) C(n-1,i-1) and the example of
+ * Table 3), on N = 2^n devices.
+ *   op_offsets  host, n_ops + 1 entries, written: op k's strategies are
+ *               strategies[op_offsets[k] .. op_offsets[k+1]).
+ *   strategies  device, `capacity` entries, written in canonical order (the
+ *               degree tuple ascending, then the device-map tuple
+ *               descending -- the order of Table 3).  NULL: only op_offsets
+ *               is written (size query).
+ * Strategies whose degree does not divide its axis are left out; with N = 1
+ * the single strategy splits nothing.  TAPS_ERR_NO_STRATEGY if an operator
+ * has none, TAPS_ERR_CAPACITY if op_offsets[n_ops] > capacity. */
+taps_status taps_enumerate_strategies(const taps_graph *graph, const taps_cluster *cluster,
+                                      uint64_t *op_offsets, taps_strategy *strategies,
+                                      uint64_t capacity, void *stream);
+
+/* Intra-operator cost of every strategy (Eq. 5-8 generalised to any
+ * operator: one ring AllReduce per tensor that lacks some split axis -- the
+ * forward partial sum of the output, the backward gradient of an input or
+ * weight -- with volume 2(g-1)/g of its shard; Algorithm 2 gives the
+ * inter-node groups, Eq. 11-12 the cost).
+ *   strategies  device, from taps_enumerate_strategies for the same graph
+ *               and cluster; op_offsets host, as that call returned it.
+ *   out         device arrays of op_offsets[n_ops] records, one per strategy. */
+taps_status taps_node_costs(const taps_graph *graph, const taps_cluster *cluster,
+                            const taps_strategy *strategies, const uint64_t *op_offsets,
+                            taps_table out, void *stream);
+
+/* Redistribution cost of every (producer strategy i, consumer strategy j)
+ * pair of every edge (Algorithm 4's pair loop).  Per pair: the device
+ * matrices and tensor shapes are unified (Table 1); Algorithm 1's sequence,
+ * the same without AllToAll and the "remove" sequence of Table 2 are costed
+ * with Eq. 9-10 volumes and Algorithm 3 / Eq. 14 inter-node groups
+ * (Eq. 11, 13, 14); the record keeps the cheapest in seconds (exact
+ * comparison, ties to the lower index), and vol the smallest volume.
+ *   edge_offsets  host, n_edges + 1 entries, written: edge e's table is
+ *                 entries [edge_offsets[e], edge_offsets[e+1]), row-major,
+ *                 entry edge_offsets[e] + i * S_dst + j.
+ *   out           device arrays of `capacity` records; all five NULL: only
+ *                 edge_offsets is written (size query).
+ * TAPS_ERR_CAPACITY if edge_offsets[n_edges] > capacity. */
+taps_status taps_edge_costs(const taps_graph *graph, const taps_cluster *cluster,
+                            const taps_strategy *strategies, const uint64_t *op_offsets,
+                            uint64_t *edge_offsets, taps_table out, uint64_t capacity,
+                            void *stream);
+
+/* Static name of a status code. */
+const char *taps_status_str(taps_status status);
+
+/* Description of the calling thread's last failure ("" if none). */
+const char *taps_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TAPS_H */

@@ -1,0 +1,391 @@
+// taps_api.hip -- the C ABI: validation, uploads, scratch and launches.
+//
+// Host code only sizes and checks: it validates the graph and cluster,
+// computes table offsets (prefix sums of strategy counts), uploads the
+// caller's structs unchanged and launches the kernels.  Every cost is
+// computed on the GPU.
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <numeric>
+#include <string>
+#include <vector>
+
+#include "taps.h"
+#include "taps_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+taps_status fail(taps_status st, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return st;
+}
+
+taps_status hip_fail(hipError_t err, const char *what) {
+    return fail(TAPS_ERR_DEVICE, "%s: %s", what, hipGetErrorString(err));
+}
+
+bool pow2(uint64_t v) { return v && !(v & (v - 1)); }
+
+uint32_t log2u(uint64_t v) {
+    uint32_t k = 0;
+    while ((1ull << k) < v) ++k;
+    return k;
+}
+
+taps_status check_cluster(const taps_cluster *c, taps_launch *lp) {
+    if (!c) return fail(TAPS_ERR_ARG, "cluster is NULL");
+    if (!pow2(c->nodes) || !pow2(c->devices_per_node))
+        return fail(TAPS_ERR_TOPOLOGY, "nodes (%u) and devices_per_node (%u) must be powers of two",
+                    c->nodes, c->devices_per_node);
+    const uint64_t N = (uint64_t)c->nodes * c->devices_per_node;
+    if (N > (1ull << TAPS_MAX_LEVELS))
+        return fail(TAPS_ERR_TOPOLOGY, "%llu devices exceed the limit of %u", (unsigned long long)N,
+                    1u << TAPS_MAX_LEVELS);
+    if (c->bw_intra == 0 || c->bw_inter == 0)
+        return fail(TAPS_ERR_TOPOLOGY, "bandwidths must be positive");
+    const uint64_t g = std::gcd(c->bw_intra, c->bw_inter);
+    lp->n = log2u(N);
+    lp->lam = log2u(c->devices_per_node);
+    lp->b_inter_red = c->bw_inter / g;
+    lp->b_intra_red = c->bw_intra / g;
+    lp->inv_n_bintra = 1.0 / ((double)N * (double)c->bw_intra);
+    lp->inv_n_binter = 1.0 / ((double)N * (double)c->bw_inter);
+    return TAPS_OK;
+}
+
+taps_status check_tensor(const taps_op &op, const taps_tensor &t, uint32_t k, const char *what,
+                         uint32_t idx) {
+    if (t.rank > TAPS_MAX_RANK)
+        return fail(TAPS_ERR_ARG, "op %u: %s %u has rank %u > %u", k, what, idx, t.rank,
+                    TAPS_MAX_RANK);
+    uint32_t seen = 0;
+    unsigned __int128 bytes = op.dtype_bytes;
+    for (uint32_t d = 0; d < t.rank; ++d) {
+        if (t.axis[d] >= op.n_axes)
+            return fail(TAPS_ERR_ARG, "op %u: %s %u names axis %u of %u", k, what, idx, t.axis[d],
+                        op.n_axes);
+        if (seen & (1u << t.axis[d]))
+            return fail(TAPS_ERR_ARG, "op %u: %s %u names axis %u twice", k, what, idx, t.axis[d]);
+        seen |= 1u << t.axis[d];
+        bytes *= (uint64_t)op.axis_len[t.axis[d]];
+        if (bytes > TAPS_MAX_TENSOR_BYTES)
+            return fail(TAPS_ERR_ARG, "op %u: %s %u exceeds %llu bytes", k, what, idx,
+                        (unsigned long long)TAPS_MAX_TENSOR_BYTES);
+    }
+    return TAPS_OK;
+}
+
+taps_status check_graph(const taps_graph *g, bool with_edges) {
+    if (!g) return fail(TAPS_ERR_ARG, "graph is NULL");
+    if (g->n_ops && !g->ops) return fail(TAPS_ERR_ARG, "graph has %u ops but ops is NULL", g->n_ops);
+    for (uint32_t k = 0; k < g->n_ops; ++k) {
+        const taps_op &op = g->ops[k];
+        if (op.n_axes < 1 || op.n_axes > TAPS_MAX_AXES)
+            return fail(TAPS_ERR_ARG, "op %u: n_axes %u outside 1..%u", k, op.n_axes, TAPS_MAX_AXES);
+        if (op.part_mask >> op.n_axes)
+            return fail(TAPS_ERR_ARG, "op %u: part_mask names axes beyond n_axes", k);
+        if (op.dtype_bytes == 0) return fail(TAPS_ERR_ARG, "op %u: dtype_bytes is 0", k);
+        if (op.n_in > TAPS_MAX_INPUTS || op.n_w > TAPS_MAX_WEIGHTS)
+            return fail(TAPS_ERR_ARG, "op %u: too many inputs or weights", k);
+        for (uint32_t a = 0; a < op.n_axes; ++a)
+            if (op.axis_len[a] < 1)
+                return fail(TAPS_ERR_ARG, "op %u: axis %u has length %lld", k, a,
+                            (long long)op.axis_len[a]);
+        taps_status st = check_tensor(op, op.out, k, "output", 0);
+        for (uint32_t i = 0; st == TAPS_OK && i < op.n_in; ++i)
+            st = check_tensor(op, op.in[i], k, "input", i);
+        for (uint32_t i = 0; st == TAPS_OK && i < op.n_w; ++i)
+            st = check_tensor(op, op.w[i], k, "weight", i);
+        if (st != TAPS_OK) return st;
+    }
+    if (!with_edges) return TAPS_OK;
+    if (g->n_edges && !g->edges)
+        return fail(TAPS_ERR_ARG, "graph has %u edges but edges is NULL", g->n_edges);
+    for (uint32_t e = 0; e < g->n_edges; ++e) {
+        const taps_edge &E = g->edges[e];
+        if (E.src_op >= g->n_ops || E.dst_op >= g->n_ops)
+            return fail(TAPS_ERR_ARG, "edge %u: op index out of range", e);
+        const taps_op &src = g->ops[E.src_op];
+        const taps_op &dst = g->ops[E.dst_op];
+        if (E.dst_slot >= dst.n_in)
+            return fail(TAPS_ERR_ARG, "edge %u: consumer has no input %u", e, E.dst_slot);
+        const taps_tensor &T = src.out, &Tc = dst.in[E.dst_slot];
+        if (T.rank != Tc.rank)
+            return fail(TAPS_ERR_SHAPE, "edge %u: rank %u -> %u", e, T.rank, Tc.rank);
+        for (uint32_t d = 0; d < T.rank; ++d)
+            if (src.axis_len[T.axis[d]] != dst.axis_len[Tc.axis[d]])
+                return fail(TAPS_ERR_SHAPE, "edge %u: dimension %u has length %lld -> %lld", e, d,
+                            (long long)src.axis_len[T.axis[d]], (long long)dst.axis_len[Tc.axis[d]]);
+    }
+    return TAPS_OK;
+}
+
+taps_status check_offsets(const taps_graph *g, const uint64_t *op_offsets) {
+    if (!op_offsets) return fail(TAPS_ERR_ARG, "op_offsets is NULL");
+    if (op_offsets[0] != 0) return fail(TAPS_ERR_ARG, "op_offsets[0] must be 0");
+    for (uint32_t k = 0; k < g->n_ops; ++k)
+        if (op_offsets[k + 1] <= op_offsets[k])
+            return fail(TAPS_ERR_ARG, "op_offsets must increase (op %u)", k);
+    if (op_offsets[g->n_ops] > 0xFFFFFFFFull)
+        return fail(TAPS_ERR_ARG, "more than 2^32 strategies");
+    return TAPS_OK;
+}
+
+// Pinned staging for host-to-device uploads: the next upload waits for the
+// previous copy out of the buffer to finish before overwriting it.
+struct staging {
+    std::mutex mu;
+    char *host = nullptr;
+    size_t cap = 0;
+    hipEvent_t done = nullptr;
+    bool pending = false;
+};
+staging g_stage;
+
+struct chunk {
+    const void *src;
+    size_t bytes;
+    size_t offset;
+};
+
+size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+
+// Uploads the chunks into one stream-ordered device allocation; *dev
+// receives its base (free it with hipFreeAsync on the same stream).
+taps_status upload(std::vector<chunk> &chunks, void **dev, hipStream_t stream) {
+    size_t total = 0;
+    for (chunk &c : chunks) {
+        c.offset = total;
+        total += align256(c.bytes);
+    }
+    if (total == 0) total = 256;
+    hipError_t err = hipMallocAsync(dev, total, stream);
+    if (err != hipSuccess) return hip_fail(err, "hipMallocAsync");
+    std::lock_guard<std::mutex> lock(g_stage.mu);
+    if (g_stage.pending) {
+        err = hipEventSynchronize(g_stage.done);
+        if (err != hipSuccess) return hip_fail(err, "hipEventSynchronize");
+        g_stage.pending = false;
+    }
+    if (!g_stage.done) {
+        err = hipEventCreateWithFlags(&g_stage.done, hipEventDisableTiming);
+        if (err != hipSuccess) return hip_fail(err, "hipEventCreate");
+    }
+    if (g_stage.cap < total) {
+        if (g_stage.host) (void)hipHostFree(g_stage.host);
+        g_stage.host = nullptr;
+        g_stage.cap = 0;
+        err = hipHostMalloc((void **)&g_stage.host, total, hipHostMallocDefault);
+        if (err != hipSuccess) return hip_fail(err, "hipHostMalloc");
+        g_stage.cap = total;
+    }
+    for (const chunk &c : chunks)
+        if (c.bytes) std::memcpy(g_stage.host + c.offset, c.src, c.bytes);
+    err = hipMemcpyAsync(*dev, g_stage.host, total, hipMemcpyHostToDevice, stream);
+    if (err != hipSuccess) return hip_fail(err, "hipMemcpyAsync");
+    err = hipEventRecord(g_stage.done, stream);
+    if (err != hipSuccess) return hip_fail(err, "hipEventRecord");
+    g_stage.pending = true;
+    return TAPS_OK;
+}
+
+template <class T>
+T *at(void *base, const chunk &c) {
+    return reinterpret_cast<T *>(static_cast<char *>(base) + c.offset);
+}
+
+// Stream-ordered scratch that is released on every exit path.
+struct scratch {
+    hipStream_t stream;
+    std::vector<void *> ptrs;
+    explicit scratch(hipStream_t s) : stream(s) {}
+    ~scratch() {
+        for (void *p : ptrs) (void)hipFreeAsync(p, stream);
+    }
+    taps_status alloc(void **p, size_t bytes) {
+        hipError_t err = hipMallocAsync(p, bytes ? bytes : 256, stream);
+        if (err != hipSuccess) return hip_fail(err, "hipMallocAsync");
+        ptrs.push_back(*p);
+        return TAPS_OK;
+    }
+    void adopt(void *p) { ptrs.push_back(p); }
+};
+
+}  // namespace
+
+extern "C" {
+
+const char *taps_status_str(taps_status s) {
+    switch (s) {
+    case TAPS_OK: return "TAPS_OK";
+    case TAPS_ERR_ARG: return "TAPS_ERR_ARG";
+    case TAPS_ERR_TOPOLOGY: return "TAPS_ERR_TOPOLOGY";
+    case TAPS_ERR_SHAPE: return "TAPS_ERR_SHAPE";
+    case TAPS_ERR_NO_STRATEGY: return "TAPS_ERR_NO_STRATEGY";
+    case TAPS_ERR_CAPACITY: return "TAPS_ERR_CAPACITY";
+    case TAPS_ERR_DEVICE: return "TAPS_ERR_DEVICE";
+    }
+    return "TAPS_ERR_UNKNOWN";
+}
+
+const char *taps_last_error(void) { return g_last_error.c_str(); }
+
+taps_status taps_enumerate_strategies(const taps_graph *graph, const taps_cluster *cluster,
+                                      uint64_t *op_offsets, taps_strategy *strategies,
+                                      uint64_t capacity, void *stream_) {
+    g_last_error.clear();
+    taps_launch lp;
+    taps_status st = check_cluster(cluster, &lp);
+    if (st == TAPS_OK) st = check_graph(graph, false);
+    if (st != TAPS_OK) return st;
+    if (!op_offsets) return fail(TAPS_ERR_ARG, "op_offsets is NULL");
+    hipStream_t stream = (hipStream_t)stream_;
+    const uint32_t n_ops = graph->n_ops;
+    if (n_ops == 0) {
+        op_offsets[0] = 0;
+        return TAPS_OK;
+    }
+    scratch sc(stream);
+    std::vector<chunk> ch{{graph->ops, sizeof(taps_op) * n_ops, 0}};
+    void *dev = nullptr;
+    if ((st = upload(ch, &dev, stream)) != TAPS_OK) return st;
+    sc.adopt(dev);
+    const taps_op *d_ops = at<taps_op>(dev, ch[0]);
+    uint32_t *d_counts = nullptr;
+    if ((st = sc.alloc((void **)&d_counts, sizeof(uint32_t) * n_ops)) != TAPS_OK) return st;
+    hipError_t err = taps_launch_enumerate(d_ops, n_ops, lp.n, nullptr, d_counts, nullptr, stream);
+    if (err != hipSuccess) return hip_fail(err, "enumerate (count)");
+    std::vector<uint32_t> counts(n_ops);
+    err = hipMemcpyAsync(counts.data(), d_counts, sizeof(uint32_t) * n_ops, hipMemcpyDeviceToHost,
+                         stream);
+    if (err == hipSuccess) err = hipStreamSynchronize(stream);
+    if (err != hipSuccess) return hip_fail(err, "reading strategy counts");
+    std::vector<uint64_t> offs(n_ops + 1, 0);
+    for (uint32_t k = 0; k < n_ops; ++k) {
+        if (counts[k] == 0)
+            return fail(TAPS_ERR_NO_STRATEGY,
+                        "op %u has no strategy on %u devices (no partitionable axis whose length "
+                        "the degrees divide)",
+                        k, 1u << lp.n);
+        offs[k + 1] = offs[k] + counts[k];
+    }
+    std::memcpy(op_offsets, offs.data(), sizeof(uint64_t) * (n_ops + 1));
+    if (!strategies) return TAPS_OK;
+    if (offs[n_ops] > capacity)
+        return fail(TAPS_ERR_CAPACITY, "%llu strategies, capacity %llu",
+                    (unsigned long long)offs[n_ops], (unsigned long long)capacity);
+    std::vector<chunk> ch2{{offs.data(), sizeof(uint64_t) * (n_ops + 1), 0}};
+    void *dev2 = nullptr;
+    if ((st = upload(ch2, &dev2, stream)) != TAPS_OK) return st;
+    sc.adopt(dev2);
+    err = taps_launch_enumerate(d_ops, n_ops, lp.n, at<uint64_t>(dev2, ch2[0]), nullptr, strategies,
+                                stream);
+    if (err != hipSuccess) return hip_fail(err, "enumerate (emit)");
+    return TAPS_OK;
+}
+
+taps_status taps_node_costs(const taps_graph *graph, const taps_cluster *cluster,
+                            const taps_strategy *strategies, const uint64_t *op_offsets,
+                            taps_table out, void *stream_) {
+    g_last_error.clear();
+    taps_launch lp;
+    taps_status st = check_cluster(cluster, &lp);
+    if (st == TAPS_OK) st = check_graph(graph, false);
+    if (st == TAPS_OK) st = check_offsets(graph, op_offsets);
+    if (st != TAPS_OK) return st;
+    const uint32_t n_ops = graph->n_ops;
+    const uint64_t total = op_offsets[n_ops];
+    if (total == 0) return TAPS_OK;
+    if (!strategies) return fail(TAPS_ERR_ARG, "strategies is NULL");
+    if (!out.t || !out.vol || !out.intra || !out.inter || !out.meta)
+        return fail(TAPS_ERR_ARG, "a table array is NULL");
+    hipStream_t stream = (hipStream_t)stream_;
+    scratch sc(stream);
+    std::vector<chunk> ch{{graph->ops, sizeof(taps_op) * n_ops, 0},
+                          {op_offsets, sizeof(uint64_t) * (n_ops + 1), 0}};
+    void *dev = nullptr;
+    if ((st = upload(ch, &dev, stream)) != TAPS_OK) return st;
+    sc.adopt(dev);
+    taps_desc *d_desc = nullptr;
+    if ((st = sc.alloc((void **)&d_desc, sizeof(taps_desc) * total)) != TAPS_OK) return st;
+    hipError_t err = taps_launch_describe(strategies, total, d_desc, stream);
+    if (err == hipSuccess)
+        err = taps_launch_node_costs(at<taps_op>(dev, ch[0]), n_ops, at<uint64_t>(dev, ch[1]),
+                                     d_desc, total, lp, out, stream);
+    if (err != hipSuccess) return hip_fail(err, "node costs");
+    return TAPS_OK;
+}
+
+taps_status taps_edge_costs(const taps_graph *graph, const taps_cluster *cluster,
+                            const taps_strategy *strategies, const uint64_t *op_offsets,
+                            uint64_t *edge_offsets, taps_table out, uint64_t capacity,
+                            void *stream_) {
+    g_last_error.clear();
+    taps_launch lp;
+    taps_status st = check_cluster(cluster, &lp);
+    if (st == TAPS_OK) st = check_graph(graph, true);
+    if (st == TAPS_OK) st = check_offsets(graph, op_offsets);
+    if (st != TAPS_OK) return st;
+    if (!edge_offsets) return fail(TAPS_ERR_ARG, "edge_offsets is NULL");
+    const uint32_t n_ops = graph->n_ops, n_edges = graph->n_edges;
+    std::vector<uint64_t> eoff(n_edges + 1, 0), tiles(n_edges + 1, 0);
+    for (uint32_t e = 0; e < n_edges; ++e) {
+        const taps_edge &E = graph->edges[e];
+        const uint64_t ns = op_offsets[E.src_op + 1] - op_offsets[E.src_op];
+        const uint64_t nd = op_offsets[E.dst_op + 1] - op_offsets[E.dst_op];
+        eoff[e + 1] = eoff[e] + ns * nd;
+        tiles[e + 1] = tiles[e] + (ns * nd + TAPS_EDGE_TILE - 1) / TAPS_EDGE_TILE;
+    }
+    const bool none = !out.t && !out.vol && !out.intra && !out.inter && !out.meta;
+    const bool all = out.t && out.vol && out.intra && out.inter && out.meta;
+    if (!none && !all) return fail(TAPS_ERR_ARG, "table arrays must be all set or all NULL");
+    if (all && eoff[n_edges] > capacity)
+        return fail(TAPS_ERR_CAPACITY, "%llu entries, capacity %llu",
+                    (unsigned long long)eoff[n_edges], (unsigned long long)capacity);
+    if (all && eoff[n_edges] > 0 && !strategies) return fail(TAPS_ERR_ARG, "strategies is NULL");
+    if (tiles[n_edges] >= 0x7FFFFFFFull)
+        return fail(TAPS_ERR_ARG, "more than 2^31 tiles of %u entries", TAPS_EDGE_TILE);
+    std::memcpy(edge_offsets, eoff.data(), sizeof(uint64_t) * (n_edges + 1));
+    if (none || eoff[n_edges] == 0) return TAPS_OK;
+    hipStream_t stream = (hipStream_t)stream_;
+    scratch sc(stream);
+    const uint64_t total = op_offsets[n_ops];
+    const uint64_t n_tiles = tiles[n_edges];
+    std::vector<chunk> ch{{graph->ops, sizeof(taps_op) * n_ops, 0},
+                          {graph->edges, sizeof(taps_edge) * n_edges, 0},
+                          {op_offsets, sizeof(uint64_t) * (n_ops + 1), 0},
+                          {eoff.data(), sizeof(uint64_t) * (n_edges + 1), 0},
+                          {tiles.data(), sizeof(uint64_t) * (n_edges + 1), 0}};
+    void *dev = nullptr;
+    if ((st = upload(ch, &dev, stream)) != TAPS_OK) return st;
+    sc.adopt(dev);
+    taps_desc *d_desc = nullptr;
+    taps_edge_params *d_params = nullptr;
+    uint32_t *d_tile_edge = nullptr;
+    if ((st = sc.alloc((void **)&d_desc, sizeof(taps_desc) * total)) != TAPS_OK) return st;
+    if ((st = sc.alloc((void **)&d_params, sizeof(taps_edge_params) * n_edges)) != TAPS_OK) return st;
+    if ((st = sc.alloc((void **)&d_tile_edge, sizeof(uint32_t) * n_tiles)) != TAPS_OK) return st;
+    hipError_t err = taps_launch_describe(strategies, total, d_desc, stream);
+    if (err == hipSuccess)
+        err = taps_launch_edge_setup(at<taps_op>(dev, ch[0]), at<taps_edge>(dev, ch[1]), n_edges,
+                                     at<uint64_t>(dev, ch[2]), at<uint64_t>(dev, ch[3]),
+                                     at<uint64_t>(dev, ch[4]), d_params, n_tiles, d_tile_edge,
+                                     stream);
+    if (err == hipSuccess)
+        err = taps_launch_edge_costs(d_params, d_tile_edge, n_tiles, d_desc, lp, out, stream);
+    if (err != hipSuccess) return hip_fail(err, "edge costs");
+    return TAPS_OK;
+}
+
+}  // extern "C"

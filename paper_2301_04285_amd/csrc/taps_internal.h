@@ -1,0 +1,50 @@
+// taps_internal.h -- launch interface between the C ABI and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "taps.h"
+#include "taps_device.h"
+
+// Uniform parameters of a table launch.
+struct taps_launch {
+    uint32_t n;             // log2 N
+    uint32_t lam;           // log2 L
+    uint64_t b_inter_red;   // B_inter / gcd(B_intra, B_inter)
+    uint64_t b_intra_red;   // B_intra / gcd(B_intra, B_inter)
+    double inv_n_bintra;    // 1 / (N B_intra)
+    double inv_n_binter;    // 1 / (N B_inter)
+};
+
+// Per-edge constants of the edge-table kernel (64 bytes).
+struct taps_edge_params {
+    uint64_t out_offset;   // first entry of the edge's table
+    uint64_t tile_begin;   // first tile of the edge
+    uint64_t tbytes;       // elements x dtype bytes of the edge tensor
+    uint32_t src_base;     // first strategy of the producer
+    uint32_t dst_base;     // first strategy of the consumer
+    uint32_t ns, nd;       // strategy counts
+    uint32_t rank;
+    uint32_t paxes;        // nibble d: producer op axis of tensor dimension d
+    uint32_t caxes;        // nibble d: consumer op axis of tensor dimension d
+    uint32_t pad;
+};
+
+#define TAPS_EDGE_TILE 256   // entries (= threads) per edge workgroup
+
+hipError_t taps_launch_enumerate(const taps_op *ops, uint32_t n_ops, uint32_t n,
+                                 const uint64_t *offsets, uint32_t *counts, taps_strategy *out,
+                                 hipStream_t stream);
+hipError_t taps_launch_describe(const taps_strategy *s, uint64_t total, taps_desc *desc,
+                                hipStream_t stream);
+hipError_t taps_launch_node_costs(const taps_op *ops, uint32_t n_ops, const uint64_t *offsets,
+                                  const taps_desc *desc, uint64_t total, const taps_launch &lp,
+                                  taps_table out, hipStream_t stream);
+hipError_t taps_launch_edge_setup(const taps_op *ops, const taps_edge *edges, uint32_t n_edges,
+                                  const uint64_t *op_offsets, const uint64_t *edge_offsets,
+                                  const uint64_t *tile_begin, taps_edge_params *params,
+                                  uint64_t n_tiles, uint32_t *tile_edge, hipStream_t stream);
+hipError_t taps_launch_edge_costs(const taps_edge_params *params, const uint32_t *tile_edge,
+                                  uint64_t n_tiles, const taps_desc *desc, const taps_launch &lp,
+                                  taps_table out, hipStream_t stream);

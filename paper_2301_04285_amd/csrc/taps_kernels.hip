@@ -1,0 +1,271 @@
+// taps_kernels.hip -- gfx950 kernels of the TAPS cost tables.
+//
+//   k_enumerate   one wavefront per operator: GenerateStrategySet in
+//                 canonical order, 64 candidates per step, ballot compaction
+//   k_describe    one thread per strategy: level runs, owners and cuts
+//   k_node_costs  one thread per strategy: the intra-op AllReduces
+//   k_edge_setup  one thread per edge: per-edge constants
+//   k_tile_map    one thread per edge tile: which edge the tile belongs to
+//   k_edge_costs  one 256-thread workgroup per tile of 256 consecutive
+//                 entries of one edge table (row-major, so lanes cover
+//                 consecutive consumer strategies); one entry per lane;
+//                 five coalesced non-temporal SoA stores per entry
+#include "taps_internal.h"
+
+namespace {
+
+constexpr uint32_t kWave = 64;
+
+// Completion counts w(k, s, z) for k, s, z in 0..8 (see taps_completions).
+struct lds_weights {
+    const uint64_t *tab;
+    __device__ uint64_t operator()(uint32_t k, uint32_t s, uint32_t z) const {
+        return tab[(k * 9u + s) * 9u + z];
+    }
+};
+
+__device__ inline uint32_t lanes_below(uint64_t mask) {
+    return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                     __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+}
+
+__global__ __launch_bounds__(kWave) void k_enumerate(const taps_op *__restrict__ ops, uint32_t n,
+                                                     const uint64_t *__restrict__ offsets,
+                                                     uint32_t *__restrict__ counts,
+                                                     taps_strategy *__restrict__ out) {
+    __shared__ uint64_t wtab[9 * 9 * 9];
+    const uint32_t lane = threadIdx.x;
+    for (uint32_t x = lane; x < 9u * 9u * 9u; x += kWave)
+        wtab[x] = taps_completions(x / 81u, (x / 9u) % 9u, x % 9u);
+    __syncthreads();
+    const taps_op &op = ops[blockIdx.x];
+    const uint32_t n_axes = op.n_axes, part = op.part_mask;
+    const lds_weights w{wtab};
+    const uint64_t total = w(taps_popc(part), n, 0);
+    uint64_t base = offsets ? offsets[blockIdx.x] : 0;
+    uint32_t count = 0;
+    for (uint64_t r0 = 0; r0 < total; r0 += kWave) {
+        const uint64_t r = r0 + lane;
+        uint32_t expo[TAPS_D_MAX_AXES];
+        int32_t pos[TAPS_D_MAX_AXES];
+        bool valid = r < total && taps_unrank(n_axes, part, n, r, w, expo, pos);
+        if (valid)
+            for (uint32_t a = 0; a < n_axes; ++a)
+                if (op.axis_len[a] & (((int64_t)1 << expo[a]) - 1)) valid = false;
+        const uint64_t m = __ballot(valid);
+        if (out && valid) {
+            taps_strategy s;
+            for (uint32_t a = 0; a < TAPS_MAX_AXES; ++a) {
+                s.log2_deg[a] = a < n_axes ? (uint8_t)expo[a] : 0;
+                s.pos[a] = a < n_axes ? (int8_t)pos[a] : (int8_t)-1;
+            }
+            out[base + count + lanes_below(m)] = s;
+        }
+        count += (uint32_t)__builtin_popcountll(m);
+    }
+    if (counts && lane == 0) counts[blockIdx.x] = count;
+}
+
+__global__ __launch_bounds__(256) void k_describe(const taps_strategy *__restrict__ s,
+                                                  uint64_t total, taps_desc *__restrict__ desc) {
+    const uint64_t idx = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= total) return;
+    const taps_strategy st = s[idx];
+    uint32_t expo[TAPS_D_MAX_AXES];
+    int32_t pos[TAPS_D_MAX_AXES];
+#pragma unroll
+    for (uint32_t a = 0; a < TAPS_D_MAX_AXES; ++a) {
+        expo[a] = st.log2_deg[a];
+        pos[a] = st.pos[a];
+    }
+    desc[idx] = taps_describe(TAPS_D_MAX_AXES, expo, pos);
+}
+
+// largest k in [0, n) with offsets[k] <= x
+__device__ inline uint32_t find_owner(const uint64_t *offsets, uint32_t n, uint64_t x) {
+    uint32_t lo = 0, hi = n;
+    while (hi - lo > 1) {
+        uint32_t mid = (lo + hi) >> 1;
+        if (offsets[mid] <= x)
+            lo = mid;
+        else
+            hi = mid;
+    }
+    return lo;
+}
+
+__device__ inline void node_tensor(taps_acc &c, const taps_op &op, const taps_tensor &t,
+                                   const taps_desc &D, uint32_t full, uint32_t lam) {
+    uint32_t used = 0;
+    uint64_t bytes = op.dtype_bytes;
+    for (uint32_t d = 0; d < t.rank && d < TAPS_MAX_RANK; ++d) {
+        const uint32_t a = t.axis[d] & 7u;
+        used |= taps_levels(taps_nib(D.lo, a), taps_nib(D.width, a));
+        bytes *= (uint64_t)op.axis_len[a];
+    }
+    taps_allreduce(c, full & ~used, bytes, lam);
+}
+
+__global__ __launch_bounds__(256) void k_node_costs(const taps_op *__restrict__ ops, uint32_t n_ops,
+                                                    const uint64_t *__restrict__ offsets,
+                                                    const taps_desc *__restrict__ desc,
+                                                    uint64_t total, taps_launch lp, taps_table out) {
+    const uint64_t idx = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= total) return;
+    const taps_op &op = ops[find_owner(offsets, n_ops, idx)];
+    const taps_desc D = desc[idx];
+    const uint32_t full = taps_low_mask(lp.n);
+    taps_acc c;
+    taps_acc_zero(c);
+    node_tensor(c, op, op.out, D, full, lp.lam);
+    for (uint32_t k = 0; k < op.n_in && k < TAPS_MAX_INPUTS; ++k)
+        node_tensor(c, op, op.in[k], D, full, lp.lam);
+    for (uint32_t k = 0; k < op.n_w && k < TAPS_MAX_WEIGHTS; ++k)
+        node_tensor(c, op, op.w[k], D, full, lp.lam);
+    out.t[idx] = (double)c.intra * lp.inv_n_bintra + (double)c.inter * lp.inv_n_binter;
+    out.vol[idx] = c.vol;
+    out.intra[idx] = c.intra;
+    out.inter[idx] = c.inter;
+    out.meta[idx] = taps_meta(0, c);
+}
+
+__global__ __launch_bounds__(256) void k_edge_setup(const taps_op *__restrict__ ops,
+                                                    const taps_edge *__restrict__ edges,
+                                                    uint32_t n_edges,
+                                                    const uint64_t *__restrict__ op_offsets,
+                                                    const uint64_t *__restrict__ edge_offsets,
+                                                    const uint64_t *__restrict__ tile_begin,
+                                                    taps_edge_params *__restrict__ params) {
+    const uint32_t e = blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= n_edges) return;
+    const taps_edge E = edges[e];
+    const taps_op &src = ops[E.src_op];
+    const taps_op &dst = ops[E.dst_op];
+    const taps_tensor &T = src.out;
+    const taps_tensor &Tc = dst.in[E.dst_slot];
+    taps_edge_params p;
+    p.out_offset = edge_offsets[e];
+    p.tile_begin = tile_begin[e];
+    uint64_t bytes = src.dtype_bytes;
+    uint32_t pa = 0, ca = 0;
+    for (uint32_t d = 0; d < T.rank && d < TAPS_MAX_RANK; ++d) {
+        bytes *= (uint64_t)src.axis_len[T.axis[d] & 7u];
+        pa |= (uint32_t)(T.axis[d] & 7u) << (4u * d);
+        ca |= (uint32_t)(Tc.axis[d] & 7u) << (4u * d);
+    }
+    p.tbytes = bytes;
+    p.src_base = (uint32_t)op_offsets[E.src_op];
+    p.dst_base = (uint32_t)op_offsets[E.dst_op];
+    p.ns = (uint32_t)(op_offsets[E.src_op + 1] - op_offsets[E.src_op]);
+    p.nd = (uint32_t)(op_offsets[E.dst_op + 1] - op_offsets[E.dst_op]);
+    p.rank = T.rank;
+    p.paxes = pa;
+    p.caxes = ca;
+    p.pad = 0;
+    params[e] = p;
+}
+
+__global__ __launch_bounds__(256) void k_tile_map(const uint64_t *__restrict__ tile_begin,
+                                                  uint32_t n_edges, uint64_t n_tiles,
+                                                  uint32_t *__restrict__ tile_edge) {
+    const uint64_t t = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= n_tiles) return;
+    tile_edge[t] = find_owner(tile_begin, n_edges, t);
+}
+
+__global__ __launch_bounds__(TAPS_EDGE_TILE) void k_edge_costs(
+    const taps_edge_params *__restrict__ params, const uint32_t *__restrict__ tile_edge,
+    const taps_desc *__restrict__ desc, taps_launch lp, taps_table out) {
+    const uint32_t e = tile_edge[blockIdx.x];
+    const taps_edge_params E = params[e];
+    const uint64_t local = (uint64_t)(blockIdx.x - E.tile_begin) * TAPS_EDGE_TILE + threadIdx.x;
+    const uint64_t entries = (uint64_t)E.ns * E.nd;
+    if (local >= entries) return;
+    uint64_t i, j;
+    if (entries <= 0xFFFFFFFFull) {
+        const uint32_t l32 = (uint32_t)local;
+        i = l32 / E.nd;
+        j = l32 - (uint32_t)i * E.nd;
+    } else {
+        i = local / E.nd;
+        j = local - i * E.nd;
+    }
+    const taps_desc Dp = desc[E.src_base + i];
+    const taps_desc Dc = desc[E.dst_base + j];
+    taps_edge_problem p;
+    p.rank = E.rank;
+    p.n = lp.n;
+    p.lam = lp.lam;
+    p.tbytes = E.tbytes;
+    p.pcuts = Dp.cuts;
+    p.ccuts = Dc.cuts;
+#pragma unroll
+    for (uint32_t d = 0; d < TAPS_D_MAX_RANK; ++d) {
+        const uint32_t ap = taps_nib(E.paxes, d), ac = taps_nib(E.caxes, d);
+        p.plo[d] = taps_nib(Dp.lo, ap);
+        p.pw[d] = d < E.rank ? taps_nib(Dp.width, ap) : 0u;
+        p.clo[d] = taps_nib(Dc.lo, ac);
+        p.cw[d] = d < E.rank ? taps_nib(Dc.width, ac) : 0u;
+    }
+    const taps_entry_out o =
+        taps_edge_entry(p, lp.b_inter_red, lp.b_intra_red, lp.inv_n_bintra, lp.inv_n_binter);
+    const uint64_t g = E.out_offset + local;
+    __builtin_nontemporal_store(o.t, out.t + g);
+    __builtin_nontemporal_store(o.vol, out.vol + g);
+    __builtin_nontemporal_store(o.intra, out.intra + g);
+    __builtin_nontemporal_store(o.inter, out.inter + g);
+    __builtin_nontemporal_store(o.ok ? o.meta : 0xFFFFFFFFu, out.meta + g);
+}
+
+inline uint32_t blocks_for(uint64_t n, uint32_t per) { return (uint32_t)((n + per - 1) / per); }
+
+}  // namespace
+
+hipError_t taps_launch_enumerate(const taps_op *ops, uint32_t n_ops, uint32_t n,
+                                 const uint64_t *offsets, uint32_t *counts, taps_strategy *out,
+                                 hipStream_t stream) {
+    if (n_ops == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_enumerate, dim3(n_ops), dim3(kWave), 0, stream, ops, n, offsets, counts,
+                       out);
+    return hipGetLastError();
+}
+
+hipError_t taps_launch_describe(const taps_strategy *s, uint64_t total, taps_desc *desc,
+                                hipStream_t stream) {
+    if (total == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_describe, dim3(blocks_for(total, 256)), dim3(256), 0, stream, s, total,
+                       desc);
+    return hipGetLastError();
+}
+
+hipError_t taps_launch_node_costs(const taps_op *ops, uint32_t n_ops, const uint64_t *offsets,
+                                  const taps_desc *desc, uint64_t total, const taps_launch &lp,
+                                  taps_table out, hipStream_t stream) {
+    if (total == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_node_costs, dim3(blocks_for(total, 256)), dim3(256), 0, stream, ops,
+                       n_ops, offsets, desc, total, lp, out);
+    return hipGetLastError();
+}
+
+hipError_t taps_launch_edge_setup(const taps_op *ops, const taps_edge *edges, uint32_t n_edges,
+                                  const uint64_t *op_offsets, const uint64_t *edge_offsets,
+                                  const uint64_t *tile_begin, taps_edge_params *params,
+                                  uint64_t n_tiles, uint32_t *tile_edge, hipStream_t stream) {
+    if (n_edges == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_edge_setup, dim3(blocks_for(n_edges, 256)), dim3(256), 0, stream, ops,
+                       edges, n_edges, op_offsets, edge_offsets, tile_begin, params);
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess || n_tiles == 0) return err;
+    hipLaunchKernelGGL(k_tile_map, dim3(blocks_for(n_tiles, 256)), dim3(256), 0, stream,
+                       tile_begin, n_edges, n_tiles, tile_edge);
+    return hipGetLastError();
+}
+
+hipError_t taps_launch_edge_costs(const taps_edge_params *params, const uint32_t *tile_edge,
+                                  uint64_t n_tiles, const taps_desc *desc, const taps_launch &lp,
+                                  taps_table out, hipStream_t stream) {
+    if (n_tiles == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_edge_costs, dim3((uint32_t)n_tiles), dim3(TAPS_EDGE_TILE), 0, stream,
+                       params, tile_edge, desc, lp, out);
+    return hipGetLastError();
+}

@@ -1,0 +1,297 @@
+"""Python binding of the C ABI in ``include/taps.h`` (ctypes).
+
+Argument marshalling only: graph descriptions become the ABI's structs,
+torch provides device memory and the current HIP stream, and every step of
+the cost tables runs in ``libtaps.so``.  If the library is missing the calls
+raise -- there is no other implementation to fall back to.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import re
+from dataclasses import dataclass
+from typing import Dict, List, Optional, Tuple
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libtaps.so")
+HEADER = os.path.join(os.path.dirname(HERE), "include", "taps.h")
+
+MAX_AXES = 8
+MAX_RANK = 8
+MAX_INPUTS = 4
+MAX_WEIGHTS = 4
+
+OK, ERR_ARG, ERR_TOPOLOGY, ERR_SHAPE, ERR_NO_STRATEGY, ERR_CAPACITY, ERR_DEVICE = range(7)
+
+
+class TapsError(RuntimeError):
+    def __init__(self, status: int, call: str, detail: str):
+        self.status = status
+        super().__init__(f"{call} failed: {status_str(status)}: {detail}")
+
+
+class Cluster(C.Structure):
+    _fields_ = [("nodes", C.c_uint32), ("devices_per_node", C.c_uint32),
+                ("bw_intra", C.c_uint64), ("bw_inter", C.c_uint64)]
+
+
+class Tensor(C.Structure):
+    _fields_ = [("rank", C.c_uint8), ("axis", C.c_uint8 * MAX_RANK)]
+
+
+class Op(C.Structure):
+    _fields_ = [("n_axes", C.c_uint8), ("part_mask", C.c_uint8), ("dtype_bytes", C.c_uint8),
+                ("n_in", C.c_uint8), ("n_w", C.c_uint8),
+                ("axis_len", C.c_int64 * MAX_AXES),
+                ("ins", Tensor * MAX_INPUTS), ("ws", Tensor * MAX_WEIGHTS), ("out", Tensor)]
+
+
+class EdgeS(C.Structure):
+    _fields_ = [("src_op", C.c_uint32), ("dst_op", C.c_uint32), ("dst_slot", C.c_uint32)]
+
+
+class GraphS(C.Structure):
+    _fields_ = [("n_ops", C.c_uint32), ("n_edges", C.c_uint32),
+                ("ops", C.POINTER(Op)), ("edges", C.POINTER(EdgeS))]
+
+
+class Table(C.Structure):
+    _fields_ = [("t", C.c_void_p), ("vol", C.c_void_p), ("intra", C.c_void_p),
+                ("inter", C.c_void_p), ("meta", C.c_void_p)]
+
+
+STRATEGY_BYTES = 16   # sizeof(taps_strategy): log2_deg[8] uint8, pos[8] int8
+
+_lib = None
+
+
+def load():
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2301_04285_amd.build`")
+        L = C.CDLL(LIB_PATH)
+        P = C.POINTER
+        L.taps_enumerate_strategies.restype = C.c_int
+        L.taps_enumerate_strategies.argtypes = [P(GraphS), P(Cluster), P(C.c_uint64), C.c_void_p,
+                                                C.c_uint64, C.c_void_p]
+        L.taps_node_costs.restype = C.c_int
+        L.taps_node_costs.argtypes = [P(GraphS), P(Cluster), C.c_void_p, P(C.c_uint64), Table,
+                                      C.c_void_p]
+        L.taps_edge_costs.restype = C.c_int
+        L.taps_edge_costs.argtypes = [P(GraphS), P(Cluster), C.c_void_p, P(C.c_uint64),
+                                      P(C.c_uint64), Table, C.c_uint64, C.c_void_p]
+        L.taps_status_str.restype = C.c_char_p
+        L.taps_status_str.argtypes = [C.c_int]
+        L.taps_last_error.restype = C.c_char_p
+        L.taps_last_error.argtypes = []
+        _lib = L
+    return _lib
+
+
+def declared_symbols() -> List[str]:
+    """Entry points declared in include/taps.h."""
+    with open(HEADER) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"^\s*(?:taps_status|const char \*)\s*(taps_\w+)\s*\(", text,
+                                 flags=re.M)))
+
+
+def status_str(status: int) -> str:
+    return load().taps_status_str(status).decode()
+
+
+def last_error() -> str:
+    return load().taps_last_error().decode()
+
+
+def _check(status: int, call: str) -> None:
+    if status != OK:
+        raise TapsError(status, call, last_error())
+
+
+# ---------------------------------------------------------------------------
+# marshalling
+# ---------------------------------------------------------------------------
+
+def _tensor(axes) -> Tensor:
+    t = Tensor()
+    t.rank = len(axes)
+    for d, a in enumerate(axes):
+        t.axis[d] = a
+    return t
+
+
+@dataclass
+class PackedGraph:
+    struct: GraphS
+    ops: object
+    edges: object
+    n_ops: int
+    n_edges: int
+    edge_list: List[Tuple[int, int, int]]
+
+
+def pack_graph(graph) -> PackedGraph:
+    """``graph`` has ``ops`` (with axis_len, partitionable, dtype_bytes, ins,
+    ws, out) and ``edges`` (with src, dst, slot), as ``workloads.Graph``."""
+    n_ops, n_edges = len(graph.ops), len(graph.edges)
+    ops = (Op * max(n_ops, 1))()
+    for k, op in enumerate(graph.ops):
+        o = ops[k]
+        o.n_axes = len(op.axis_len)
+        o.part_mask = sum(1 << a for a, p in enumerate(op.partitionable) if p)
+        o.dtype_bytes = op.dtype_bytes
+        o.n_in = len(op.ins)
+        o.n_w = len(op.ws)
+        for a, n in enumerate(op.axis_len):
+            o.axis_len[a] = n
+        for i, t in enumerate(op.ins):
+            o.ins[i] = _tensor(t)
+        for i, t in enumerate(op.ws):
+            o.ws[i] = _tensor(t)
+        o.out = _tensor(op.out)
+    edges = (EdgeS * max(n_edges, 1))()
+    for k, e in enumerate(graph.edges):
+        edges[k].src_op, edges[k].dst_op, edges[k].dst_slot = e.src, e.dst, e.slot
+    g = GraphS(n_ops, n_edges, C.cast(ops, C.POINTER(Op)) if n_ops else None,
+               C.cast(edges, C.POINTER(EdgeS)) if n_edges else None)
+    return PackedGraph(g, ops, edges, n_ops, n_edges,
+                       [(e.src, e.dst, e.slot) for e in graph.edges])
+
+
+def pack_cluster(cluster) -> Cluster:
+    return Cluster(cluster.nodes, cluster.devices_per_node, cluster.bw_intra, cluster.bw_inter)
+
+
+def _stream(stream) -> C.c_void_p:
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return C.c_void_p(stream.cuda_stream)
+
+
+def _graph(graph) -> PackedGraph:
+    return graph if isinstance(graph, PackedGraph) else pack_graph(graph)
+
+
+def _u64_array(a: np.ndarray):
+    return a.ctypes.data_as(C.POINTER(C.c_uint64))
+
+
+# ---------------------------------------------------------------------------
+# the three calls
+# ---------------------------------------------------------------------------
+
+def taps_enumerate_strategies(graph, cluster, device="cuda", stream=None, size_only=False,
+                              out=None):
+    """(op_offsets as numpy uint64 [n_ops+1], strategies as a device uint8
+    tensor [S, 16]: log2 degrees then device-map positions as int8).
+    ``out``: a preallocated device uint8 tensor [capacity, 16] to fill in one
+    call; otherwise a size query runs first."""
+    import torch
+    g = _graph(graph)
+    cl = pack_cluster(cluster)
+    offs = np.zeros(g.n_ops + 1, dtype=np.uint64)
+    L = load()
+    if out is None:
+        st = L.taps_enumerate_strategies(C.byref(g.struct), C.byref(cl), _u64_array(offs), None,
+                                         0, _stream(stream))
+        _check(st, "taps_enumerate_strategies")
+        if size_only:
+            return offs, None
+        out = torch.empty((max(int(offs[-1]), 1), STRATEGY_BYTES), dtype=torch.uint8,
+                          device=device)
+    st = L.taps_enumerate_strategies(C.byref(g.struct), C.byref(cl), _u64_array(offs),
+                                     C.c_void_p(out.data_ptr()), int(out.shape[0]),
+                                     _stream(stream))
+    _check(st, "taps_enumerate_strategies")
+    return offs, out[:int(offs[-1])]
+
+
+def alloc_table(n: int, device="cuda") -> Dict[str, "torch.Tensor"]:
+    import torch
+    n = max(int(n), 1)
+    return {"t": torch.empty(n, dtype=torch.float64, device=device),
+            "vol": torch.empty(n, dtype=torch.uint64, device=device),
+            "intra": torch.empty(n, dtype=torch.uint64, device=device),
+            "inter": torch.empty(n, dtype=torch.uint64, device=device),
+            "meta": torch.empty(n, dtype=torch.uint32, device=device)}
+
+
+def _table(tab) -> Table:
+    if tab is None:
+        return Table(None, None, None, None, None)
+    return Table(*(C.c_void_p(tab[k].data_ptr()) for k in ("t", "vol", "intra", "inter", "meta")))
+
+
+def taps_node_costs(graph, cluster, strategies, op_offsets, out=None, stream=None):
+    """Node table (dict of device tensors, one record per strategy)."""
+    g = _graph(graph)
+    cl = pack_cluster(cluster)
+    offs = np.ascontiguousarray(op_offsets, dtype=np.uint64)
+    total = int(offs[-1])
+    if out is None:
+        out = alloc_table(total, device=strategies.device)
+    st = load().taps_node_costs(C.byref(g.struct), C.byref(cl), C.c_void_p(strategies.data_ptr()),
+                                _u64_array(offs), _table(out), _stream(stream))
+    _check(st, "taps_node_costs")
+    return {k: v[:total] for k, v in out.items()}
+
+
+def taps_edge_costs(graph, cluster, strategies, op_offsets, out=None, stream=None,
+                    size_only=False):
+    """(edge_offsets numpy uint64 [n_edges+1], edge table dict of device
+    tensors or None for a size query)."""
+    g = _graph(graph)
+    cl = pack_cluster(cluster)
+    offs = np.ascontiguousarray(op_offsets, dtype=np.uint64)
+    eoffs = np.zeros(g.n_edges + 1, dtype=np.uint64)
+    L = load()
+    sptr = C.c_void_p(strategies.data_ptr()) if strategies is not None else None
+    st = L.taps_edge_costs(C.byref(g.struct), C.byref(cl), sptr, _u64_array(offs),
+                           _u64_array(eoffs), _table(None), 0, _stream(stream))
+    _check(st, "taps_edge_costs")
+    if size_only:
+        return eoffs, None
+    total = int(eoffs[-1])
+    if out is None:
+        out = alloc_table(total, device=strategies.device)
+    cap = min(int(v.numel()) for v in out.values())
+    st = L.taps_edge_costs(C.byref(g.struct), C.byref(cl), sptr, _u64_array(offs),
+                           _u64_array(eoffs), _table(out), cap, _stream(stream))
+    _check(st, "taps_edge_costs")
+    return eoffs, {k: v[:total] for k, v in out.items()}
+
+
+@dataclass
+class Tables:
+    op_offsets: np.ndarray
+    strategies: "torch.Tensor"
+    node: Dict[str, "torch.Tensor"]
+    edge_offsets: np.ndarray
+    edge: Dict[str, "torch.Tensor"]
+
+
+def build_tables(graph, cluster, device="cuda", stream=None, out: Optional[Tables] = None) -> Tables:
+    """Enumeration, node table and edge table of one graph on one cluster.
+    ``out``: tables of an earlier build of the same graph to fill again."""
+    g = _graph(graph)
+    offs, strat = taps_enumerate_strategies(g, cluster, device=device, stream=stream,
+                                            out=out.strategies if out is not None else None)
+    node = taps_node_costs(g, cluster, strat, offs, stream=stream,
+                           out=out.node if out is not None else None)
+    eoffs, edge = taps_edge_costs(g, cluster, strat, offs, stream=stream,
+                                  out=out.edge if out is not None else None)
+    return Tables(offs, strat, node, eoffs, edge)
+
+
+def strategies_to_numpy(strategies) -> Tuple[np.ndarray, np.ndarray]:
+    """(log2 degrees uint8 [S, 8], positions int8 [S, 8]) on the host."""
+    a = strategies.cpu().numpy()
+    return a[:, :MAX_AXES].copy(), a[:, MAX_AXES:].view(np.int8).copy()

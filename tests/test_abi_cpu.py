@@ -1,0 +1,167 @@
+"""The C-ABI library on the host: it loads, exports what include/taps.h
+declares, validates its arguments before touching the GPU, and sizes tables
+(no compute call here -- those need a GPU)."""
+import ctypes as C
+import subprocess
+
+import numpy as np
+import pytest
+
+from paper_2301_04285_amd import taps as T
+from paper_2301_04285_amd import workloads as W
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return T.load()
+
+
+def test_exports_every_declared_symbol(lib):
+    declared = T.declared_symbols()
+    assert declared == sorted(["taps_enumerate_strategies", "taps_node_costs", "taps_edge_costs",
+                               "taps_status_str", "taps_last_error"])
+    out = subprocess.run(["nm", "-D", "--defined-only", T.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = {line.split()[-1] for line in out.splitlines() if line.strip()}
+    for name in declared:
+        assert name in exported
+        assert getattr(lib, name) is not None
+
+
+def test_status_strings(lib):
+    names = [T.status_str(s) for s in range(7)]
+    assert names == ["TAPS_OK", "TAPS_ERR_ARG", "TAPS_ERR_TOPOLOGY", "TAPS_ERR_SHAPE",
+                     "TAPS_ERR_NO_STRATEGY", "TAPS_ERR_CAPACITY", "TAPS_ERR_DEVICE"]
+
+
+def _enum(lib, graph, cluster, offs=None):
+    g = T.pack_graph(graph)
+    cl = T.pack_cluster(cluster) if cluster is not None else None
+    if offs is None:
+        offs = np.zeros(len(graph.ops) + 1, np.uint64)
+    return lib.taps_enumerate_strategies(C.byref(g.struct), C.byref(cl) if cl else None,
+                                         T._u64_array(offs), None, 0, None)
+
+
+@pytest.mark.parametrize("cluster,status", [
+    (W.Cluster(3, 2, 10, 1), T.ERR_TOPOLOGY),
+    (W.Cluster(2, 6, 10, 1), T.ERR_TOPOLOGY),
+    (W.Cluster(0, 2, 10, 1), T.ERR_TOPOLOGY),
+    (W.Cluster(64, 8, 10, 1), T.ERR_TOPOLOGY),     # 512 devices > 2^8
+    (W.Cluster(2, 2, 0, 1), T.ERR_TOPOLOGY),
+    (W.Cluster(2, 2, 10, 0), T.ERR_TOPOLOGY),
+])
+def test_cluster_validation(lib, cluster, status):
+    assert _enum(lib, W.mlp2(), cluster) == status
+    assert T.last_error() != ""
+
+
+def test_null_arguments(lib):
+    g = T.pack_graph(W.mlp2())
+    cl = T.pack_cluster(W.Cluster(2, 2, 10, 1))
+    offs = np.zeros(4, np.uint64)
+    assert lib.taps_enumerate_strategies(None, C.byref(cl), T._u64_array(offs), None, 0, None) \
+        == T.ERR_ARG
+    assert lib.taps_enumerate_strategies(C.byref(g.struct), None, T._u64_array(offs), None, 0,
+                                         None) == T.ERR_ARG
+    assert lib.taps_enumerate_strategies(C.byref(g.struct), C.byref(cl), None, None, 0, None) \
+        == T.ERR_ARG
+    eo = np.zeros(3, np.uint64)
+    good = np.array([0, 9, 13, 22], np.uint64)
+    assert lib.taps_edge_costs(C.byref(g.struct), C.byref(cl), None, None, T._u64_array(eo),
+                               T._table(None), 0, None) == T.ERR_ARG
+    assert lib.taps_edge_costs(C.byref(g.struct), C.byref(cl), None, T._u64_array(good), None,
+                               T._table(None), 0, None) == T.ERR_ARG
+    assert lib.taps_node_costs(C.byref(g.struct), C.byref(cl), None, T._u64_array(good),
+                               T.Table(1, 1, 1, 1, 1), None) == T.ERR_ARG
+
+
+def _op(**kw):
+    base = dict(name="x", kind="x", axis_names=("a", "b"), axis_len=(8, 8),
+                partitionable=(True, True), dtype_bytes=2, ins=((0, 1),), ws=(), out=(0, 1))
+    base.update(kw)
+    return W.Op(**base)
+
+
+@pytest.mark.parametrize("op", [
+    _op(out=(0, 2)),                          # axis out of range
+    _op(out=(0, 0)),                          # axis named twice
+    _op(axis_len=(8, 0)),                     # zero length
+    _op(dtype_bytes=0),
+    _op(axis_len=(1 << 30, 1 << 30)),         # 2^61 bytes: volumes would not stay exact
+])
+def test_operator_validation(lib, op):
+    g = W.Graph()
+    object.__setattr__(op, "check", lambda: None)
+    g.ops.append(op)
+    assert _enum(lib, g, W.Cluster(2, 2, 10, 1)) == T.ERR_ARG
+
+
+def _size_query(lib, graph, offs, cluster=W.Cluster(2, 2, 10, 1)):
+    g = T.pack_graph(graph)
+    cl = T.pack_cluster(cluster)
+    eo = np.zeros(len(graph.edges) + 1, np.uint64)
+    st = lib.taps_edge_costs(C.byref(g.struct), C.byref(cl), None,
+                             T._u64_array(np.asarray(offs, np.uint64)), T._u64_array(eo),
+                             T._table(None), 0, None)
+    return st, eo
+
+
+def test_edge_shape_mismatch(lib):
+    g = W.mlp2()
+    bad = W.Graph(list(g.ops), [W.Edge(0, 2, 0)])   # (64, 1024) into (64, 1024)? mm2.X is (64,1024)
+    st, _ = _size_query(lib, bad, [0, 9, 13, 22])
+    assert st == T.OK
+    bad = W.Graph(list(g.ops), [W.Edge(2, 0, 0)])   # (64, 256) into mm1.X (64, 256): fine
+    assert _size_query(lib, bad, [0, 9, 13, 22])[0] == T.OK
+    bad = W.Graph(list(g.ops), [W.Edge(1, 0, 0)])   # (64, 1024) into (64, 256)
+    assert _size_query(lib, bad, [0, 9, 13, 22])[0] == T.ERR_SHAPE
+    bad = W.Graph(list(g.ops), [W.Edge(0, 1, 1)])   # gelu has one input
+    assert _size_query(lib, bad, [0, 9, 13, 22])[0] == T.ERR_ARG
+    bad = W.Graph(list(g.ops), [W.Edge(0, 5, 0)])
+    assert _size_query(lib, bad, [0, 9, 13, 22])[0] == T.ERR_ARG
+
+
+def test_edge_size_query_offsets(lib):
+    g = W.gpt(2, 64, 4, 32, 4, 2)
+    rng = np.random.default_rng(0)
+    counts = rng.integers(1, 50, len(g.ops))
+    offs = np.concatenate([[0], np.cumsum(counts)]).astype(np.uint64)
+    st, eo = _size_query(lib, g, offs)
+    assert st == T.OK
+    want = np.concatenate([[0], np.cumsum([counts[e.src] * counts[e.dst] for e in g.edges])])
+    assert np.array_equal(eo, want.astype(np.uint64))
+    assert len(g.edges) == 18 * 2 - 2
+
+
+def test_offsets_must_increase(lib):
+    st, _ = _size_query(lib, W.mlp2(), [0, 9, 9, 18])
+    assert st == T.ERR_ARG
+    st, _ = _size_query(lib, W.mlp2(), [1, 9, 13, 22])
+    assert st == T.ERR_ARG
+
+
+def test_capacity_and_partial_tables(lib):
+    g = T.pack_graph(W.mlp2())
+    cl = T.pack_cluster(W.Cluster(2, 2, 10, 1))
+    offs = np.array([0, 9, 13, 22], np.uint64)
+    eo = np.zeros(3, np.uint64)
+    fake = T.Table(256, 256, 256, 256, 256)   # never dereferenced: the checks fail first
+    assert lib.taps_edge_costs(C.byref(g.struct), C.byref(cl), C.c_void_p(256),
+                               T._u64_array(offs), T._u64_array(eo), fake, 71, None) \
+        == T.ERR_CAPACITY
+    assert np.all(eo == 0)   # nothing written on error
+    partial = T.Table(256, None, 256, 256, 256)
+    assert lib.taps_edge_costs(C.byref(g.struct), C.byref(cl), C.c_void_p(256),
+                               T._u64_array(offs), T._u64_array(eo), partial, 72, None) \
+        == T.ERR_ARG
+
+
+def test_device_errors_are_reported(lib):
+    """Without a usable device every compute call returns TAPS_ERR_DEVICE
+    (on a GPU machine this test is skipped)."""
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present")
+    assert _enum(lib, W.mlp2(), W.Cluster(2, 2, 10, 1)) == T.ERR_DEVICE
+    assert "hip" in T.last_error().lower()

@@ -1,0 +1,256 @@
+"""GPU tables against the CPU oracle, through the C ABI.
+
+Integers (vol, intra, inter, meta) must be identical; t within 1e-9
+relative.  Small configurations are compared entry by entry in full; the
+96-layer configuration (9.9e7 edge entries) is built in full on the GPU in
+the same launch configuration the benchmark times and compared on seeded
+samples the oracle computes one by one, plus properties checked over every
+entry.
+"""
+import random
+import sys
+
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2301_04285_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+RTOL = 1e-9
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def T():
+    import torch
+    from paper_2301_04285_amd import taps
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    taps.load()
+    return taps
+
+
+def _np(t):
+    import torch
+    if t.dtype == torch.uint64:
+        return t.view(torch.int64).cpu().numpy().view(np.uint64)
+    if t.dtype == torch.uint32:
+        return t.view(torch.int32).cpu().numpy().view(np.uint32)
+    return t.cpu().numpy()
+
+
+def _signed(t):
+    import torch
+    return {torch.uint64: lambda: t.view(torch.int64),
+            torch.uint32: lambda: t.view(torch.int32)}.get(t.dtype, lambda: t)()
+
+
+def _host(tab):
+    return {k: _np(v) for k, v in tab.items()}
+
+
+def assert_records(got, ref, where=""):
+    """got: dict of numpy arrays; ref: oracle RECORD_DTYPE array (same order)."""
+    ref = ref.ravel()
+    for f in ("vol", "intra", "inter", "meta"):
+        bad = np.flatnonzero(got[f] != ref[f])
+        assert bad.size == 0, (f"{where}: {f} differs at {bad[:5]}: "
+                               f"gpu {got[f][bad[:5]]} oracle {ref[f][bad[:5]]}")
+    denom = np.maximum(np.abs(ref["t"]), np.finfo(np.float64).tiny)
+    rel = np.abs(got["t"] - ref["t"]) / denom
+    bad = np.flatnonzero(rel > RTOL)
+    assert bad.size == 0, f"{where}: t differs at {bad[:5]}: {got['t'][bad[:5]]} vs {ref['t'][bad[:5]]}"
+
+
+def check_strategies(T, graph, cluster, offs, strat):
+    lg, pos = T.strategies_to_numpy(strat)
+    for k, op in enumerate(graph.ops):
+        ref = O.enumerate_strategies(op, cluster.devices)
+        a, b = int(offs[k]), int(offs[k + 1])
+        assert b - a == len(ref), op.name
+        deg = np.where(pos[a:b, :op.n_axes] >= 0, 1 << lg[a:b, :op.n_axes].astype(np.int64), 1)
+        assert np.array_equal(deg, ref["degree"][:, :op.n_axes]), op.name
+        assert np.array_equal(pos[a:b, :op.n_axes], ref["pos"][:, :op.n_axes]), op.name
+        assert np.all(lg[a:b, op.n_axes:] == 0) and np.all(pos[a:b, op.n_axes:] == -1)
+    return [O.enumerate_strategies(op, cluster.devices) for op in graph.ops]
+
+
+def full_check(T, graph, cluster, name):
+    import torch
+    say(f"[gpu] build {name}")
+    tabs = T.build_tables(graph, cluster)
+    torch.cuda.synchronize()
+    say(f"[gpu] built {name}: {int(tabs.edge_offsets[-1])} edge entries")
+    ref_strats = check_strategies(T, graph, cluster, tabs.op_offsets, tabs.strategies)
+    node = _host(tabs.node)
+    edge = _host(tabs.edge)
+    for k, op in enumerate(graph.ops):
+        a, b = int(tabs.op_offsets[k]), int(tabs.op_offsets[k + 1])
+        ref = O.node_table(op, ref_strats[k], cluster)
+        assert_records({f: v[a:b] for f, v in node.items()}, ref, f"{name} node {k} {op.name}")
+    for x, e in enumerate(graph.edges):
+        a, b = int(tabs.edge_offsets[x]), int(tabs.edge_offsets[x + 1])
+        ref = O.edge_table(graph.ops[e.src], ref_strats[e.src], graph.ops[e.dst], e.slot,
+                           ref_strats[e.dst], cluster)
+        assert_records({f: v[a:b] for f, v in edge.items()}, ref, f"{name} edge {x}")
+    return tabs
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 4])
+def test_full_tables_small_configs(T, cfg):
+    w = W.config(cfg)
+    for name, cl in w.clusters:
+        full_check(T, w.graph, cl, f"{w.name}/{name}")
+
+
+def test_full_tables_config3_both_views(T):
+    w = W.config(3)
+    for name, cl in w.clusters:
+        full_check(T, w.graph, cl, f"{w.name}/{name}")
+
+
+def test_largest_config_sampled(T):
+    """The 96-layer GPT on 16 x 8 devices, built whole in HBM."""
+    import torch
+    w = W.config(5)
+    name, cl = w.clusters[0]
+    g = w.graph
+    say(f"[gpu] build {w.name}/{name}")
+    tabs = T.build_tables(g, cl)
+    torch.cuda.synchronize()
+    total = int(tabs.edge_offsets[-1])
+    say(f"[gpu] built {total} edge entries")
+    assert total == 98_668_128
+    ref_strats = check_strategies(T, g, cl, tabs.op_offsets, tabs.strategies)
+    # node tables in full
+    node = _host(tabs.node)
+    for k, op in enumerate(g.ops):
+        a, b = int(tabs.op_offsets[k]), int(tabs.op_offsets[k + 1])
+        assert_records({f: v[a:b] for f, v in node.items()},
+                       O.node_table(op, ref_strats[k], cl), f"node {k}")
+    # properties over every entry
+    meta = tabs.edge["meta"].view(torch.int32)
+    assert int((meta == -1).sum()) == 0, "an entry's sequence did not settle"
+    assert int(((meta & 3) == 3).sum()) == 0
+    vol = tabs.edge["vol"].view(torch.int64).double()
+    t = tabs.edge["t"]
+    assert bool((t >= vol / (cl.devices * cl.bw_intra) * (1 - 1e-12)).all())
+    # seeded samples: every edge's first, last and a tile-boundary entry,
+    # plus random entries of 64 random edges
+    rng = random.Random(96)
+    edge = tabs.edge
+    deep = set(rng.sample(range(len(g.edges)), 64))
+    picks = []
+    for x, e in enumerate(g.edges):
+        ns, nd = len(ref_strats[e.src]), len(ref_strats[e.dst])
+        cand = {0, ns * nd - 1, min(ns * nd - 1, 255), min(ns * nd - 1, 256)}
+        if x in deep:
+            cand |= {rng.randrange(ns * nd) for _ in range(1500)}
+        picks.append(sorted(cand))
+    checked = 0
+    for x, e in enumerate(g.edges):
+        nd = len(ref_strats[e.dst])
+        loc = np.array(picks[x], dtype=np.int64)
+        glob = torch.from_numpy(loc + int(tabs.edge_offsets[x])).to(t.device)
+        got = {f: _np(_signed(v).index_select(0, glob).view(v.dtype)) for f, v in edge.items()}
+        ref = O.edge_entries(g.ops[e.src], ref_strats[e.src], g.ops[e.dst], e.slot,
+                             ref_strats[e.dst], loc // nd, loc % nd, cl)
+        assert_records(got, ref, f"edge {x}")
+        checked += len(loc)
+    say(f"[gpu] checked {checked} sampled entries")
+    assert checked > 90_000
+
+
+def _entries(g, N):
+    counts = [len(O.enumerate_strategies(op, N)) for op in g.ops]
+    return sum(counts[e.src] * counts[e.dst] for e in g.edges)
+
+
+def _random_cases(seed, count, max_entries=400_000):
+    """Seeded random graphs on random meshes (N = 1..256), each small enough
+    for the oracle to check in full."""
+    rng = random.Random(seed)
+    made = 0
+    while made < count:
+        g = W.random_graph(rng, rng.randint(2, 7), max_axes=6, max_rank=5, len_pow_range=(0, 9))
+        n = rng.randint(0, 8)
+        L = 1 << rng.randint(0, n)
+        N = 1 << n
+        if _entries(g, N) > max_entries:
+            continue
+        made += 1
+        yield g, W.Cluster(N // L, L, rng.choice([600, 400, 200, 25]) * W.GB,
+                           int(rng.choice([100, 50, 12.5, 6]) * W.GB))
+
+
+def test_random_graphs_and_meshes(T):
+    from paper_2301_04285_amd.taps import TapsError
+    done = 0
+    for k, (g, cl) in enumerate(_random_cases(2301, 40)):
+        try:
+            full_check(T, g, cl, f"random {k} N={cl.devices} L={cl.devices_per_node}")
+        except TapsError as ex:
+            assert ex.status == T.ERR_NO_STRATEGY
+            assert any(len(O.enumerate_strategies(op, cl.devices)) == 0 for op in g.ops)
+            continue
+        done += 1
+    assert done >= 20
+
+
+def test_degenerate_clusters(T):
+    g = W.gpt(1, 64, 4, 32, 4, 2)
+    for cl in (W.Cluster(1, 1, 10, 1),        # one device: one whole strategy per op
+               W.Cluster(16, 1, 300, 7),      # one device per node
+               W.Cluster(1, 16, 300, 7)):     # a single node
+        full_check(T, g, cl, f"gpt1 N={cl.devices} L={cl.devices_per_node}")
+    # 256 devices, the largest mesh: batch x sequence must split 256 ways
+    g = W.gpt(1, 64, 2, 128, 2, 2)
+    for cl in (W.Cluster(2, 128, 300, 7), W.Cluster(32, 8, 300, 7), W.Cluster(256, 1, 300, 7)):
+        full_check(T, g, cl, f"gpt1-s128 N={cl.devices} L={cl.devices_per_node}")
+
+
+def test_empty_graph_and_no_edges(T):
+    cl = W.Cluster(2, 2, 10, 1)
+    tabs = T.build_tables(W.Graph(), cl)
+    assert list(tabs.op_offsets) == [0] and list(tabs.edge_offsets) == [0]
+    g = W.Graph([W.matmul("a", 8, 8, 8, 2)], [])
+    tabs = full_check(T, g, cl, "one op")
+    assert list(tabs.edge_offsets) == [0]
+
+
+def test_capacity_error_on_device(T):
+    import torch
+    w = W.config(1)
+    cl = w.clusters[0][1]
+    offs, _ = T.taps_enumerate_strategies(w.graph, cl, size_only=True)
+    small = torch.empty((int(offs[-1]) - 1, 16), dtype=torch.uint8, device="cuda")
+    import ctypes as C
+    g = T.pack_graph(w.graph)
+    c = T.pack_cluster(cl)
+    st = T.load().taps_enumerate_strategies(C.byref(g.struct), C.byref(c), T._u64_array(offs),
+                                            C.c_void_p(small.data_ptr()), int(offs[-1]) - 1, None)
+    assert st == T.ERR_CAPACITY
+
+
+def test_no_strategy_error(T):
+    g = W.Graph([W.Op("odd", "x", ("a",), (3,), (True,), 2, ins=((0,),), ws=(), out=(0,))], [])
+    with pytest.raises(T.TapsError) as ex:
+        T.taps_enumerate_strategies(g, W.Cluster(2, 2, 10, 1))
+    assert ex.value.status == T.ERR_NO_STRATEGY
+
+
+def test_repeatable_bitwise(T):
+    import torch
+    w = W.config(2)
+    cl = w.clusters[0][1]
+    a = T.build_tables(w.graph, cl)
+    b = T.build_tables(w.graph, cl)
+    torch.cuda.synchronize()
+    for f in ("t", "vol", "intra", "inter", "meta"):
+        assert np.array_equal(_np(a.edge[f]), _np(b.edge[f]))
+        assert np.array_equal(_np(a.node[f]), _np(b.node[f]))
