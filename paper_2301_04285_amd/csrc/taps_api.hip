@@ -61,6 +61,7 @@ taps_status check_cluster(const taps_cluster *c, taps_launch *lp) {
     lp->b_intra_red = c->bw_intra / g;
     lp->inv_n_bintra = 1.0 / ((double)N * (double)c->bw_intra);
     lp->inv_n_binter = 1.0 / ((double)N * (double)c->bw_inter);
+    lp->narrow = (lp->b_inter_red >> 32) == 0 && (lp->b_intra_red >> 32) == 0;
     return TAPS_OK;
 }
 
@@ -345,7 +346,7 @@ taps_status taps_edge_costs(const taps_graph *graph, const taps_cluster *cluster
         const uint64_t ns = op_offsets[E.src_op + 1] - op_offsets[E.src_op];
         const uint64_t nd = op_offsets[E.dst_op + 1] - op_offsets[E.dst_op];
         eoff[e + 1] = eoff[e] + ns * nd;
-        tiles[e + 1] = tiles[e] + (ns * nd + TAPS_EDGE_TILE - 1) / TAPS_EDGE_TILE;
+        tiles[e + 1] = tiles[e] + ns * ((nd + TAPS_TILE_COLS - 1) / TAPS_TILE_COLS);
     }
     const bool none = !out.t && !out.vol && !out.intra && !out.inter && !out.meta;
     const bool all = out.t && out.vol && out.intra && out.inter && out.meta;
@@ -354,8 +355,11 @@ taps_status taps_edge_costs(const taps_graph *graph, const taps_cluster *cluster
         return fail(TAPS_ERR_CAPACITY, "%llu entries, capacity %llu",
                     (unsigned long long)eoff[n_edges], (unsigned long long)capacity);
     if (all && eoff[n_edges] > 0 && !strategies) return fail(TAPS_ERR_ARG, "strategies is NULL");
-    if (tiles[n_edges] >= 0x7FFFFFFFull)
-        return fail(TAPS_ERR_ARG, "more than 2^31 tiles of %u entries", TAPS_EDGE_TILE);
+    for (uint32_t e = 0; e < n_edges; ++e)
+        if (tiles[e + 1] - tiles[e] > 0xFFFFFFFFull)
+            return fail(TAPS_ERR_ARG, "edge %u has more than 2^32 tiles", e);
+    if (tiles[n_edges] / TAPS_TILES_PER_BLOCK >= 0x7FFFFFFFull)
+        return fail(TAPS_ERR_ARG, "more than 2^31 workgroups of %u tiles", TAPS_TILES_PER_BLOCK);
     std::memcpy(edge_offsets, eoff.data(), sizeof(uint64_t) * (n_edges + 1));
     if (none || eoff[n_edges] == 0) return TAPS_OK;
     hipStream_t stream = (hipStream_t)stream_;

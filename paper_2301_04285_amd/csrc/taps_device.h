@@ -51,6 +51,11 @@ __host__ __device__ inline uint32_t taps_ctz(uint32_t v) { return (uint32_t)__bu
 
 __host__ __device__ inline uint32_t taps_low_mask(uint32_t k) { return k >= 32u ? ~0u : ((1u << k) - 1u); }
 
+// Levels lo .. lo+w-1.
+__host__ __device__ inline uint32_t taps_levels(uint32_t lo, uint32_t w) {
+    return taps_low_mask(lo + w) & ~taps_low_mask(lo);
+}
+
 // ---------------------------------------------------------------------------
 // GenerateStrategySet in canonical order (Auxiliary Graph section, Table 3).
 //
@@ -199,245 +204,289 @@ __host__ __device__ inline void taps_allreduce(taps_acc &c, uint32_t missing, ui
 }
 
 // ---------------------------------------------------------------------------
-// A collective of the redistribution along the unified axis [lo, lo + w):
-// an AllGather (Eq. 9) or an AllToAll (Eq. 10, Eq. 14), with ct from the
-// levels no tensor dimension uses at that point (Algorithm 3): groups that
-// hold the same data inside a node share one inter-node transfer.
-// S = per-device data size before the collective, in nb.
+// Edge entries.
+//
+// The edge tensor T (rank R) leaves its producer under strategy P and enters
+// its consumer under strategy Q.  Dimension d of T occupies the run of levels
+// of its producer axis, mask pr[d] with top phi[d]-1 (0 if whole), and on the
+// consumer side cr[d] with top chi[d]-1.
+//
+// Positions.  In the unified tensor, the sub-dimension that starts at bit t
+// of dimension d is held, on the producer side, by the unified axis whose top
+// level is phi[d]-1-t, and on the consumer side by the one whose top is
+// chi[d]-1-t.  So one position corresponds to producer top l and consumer
+// top l + dl[d] with dl[d] = chi[d] - phi[d]: every relation between the two
+// tensor maps that Algorithm 1 needs is a per-dimension shift of an 8-bit
+// level mask.  A unified axis is named by its top level; sets of axes are
+// masks of tops.
+//
+// Volumes.  The producer's per-device shard is S = tbytes * 2^e nb with
+// e = n - (levels the current map uses), and every volume of Eq. 9, 10 and
+// 14 is tbytes times a power of two times a small integer.  Candidates are
+// therefore accumulated as 32-bit integers in units of tbytes/256 ("factor"
+// units) and scaled by tbytes once, exactly, at the end; comparing two
+// candidates of one entry does not need tbytes at all.
 // ---------------------------------------------------------------------------
-__host__ __device__ inline void taps_collective(taps_acc &c, bool a2a, uint32_t lo, uint32_t w,
-                                                uint64_t S, uint32_t unused, uint32_t lam) {
-    uint64_t V = a2a ? S - (S >> w) : (S << w) - S;
-    c.vol += V;
-    c.n_coll += 1;
-    if (lo + w <= lam) {
-        c.intra += V;
-        return;
-    }
-    uint32_t m = lo < lam ? lo : lam;
-    uint32_t lct = m - taps_popc(unused & taps_low_mask(m));
-    uint64_t link = V;
-    if (a2a) {
-        uint32_t kap = lam > lo ? lam - lo : 0u;   // log2 of group members inside a node
-        link = ((S >> w) << kap) * (uint64_t)((1u << w) - (1u << kap));
-    }
-    c.inter += link << lct;
-    c.n_inter += 1;
-    c.sum_ct += 1u << lct;
+
+// m shifted towards higher levels by d (d may be negative; d in [-8, 8]).
+__host__ __device__ inline uint32_t taps_shift(uint32_t m, int32_t d) {
+    return (m << 16) >> (16 - d);
 }
 
-// ---------------------------------------------------------------------------
-// One edge entry: the tensor of rank R leaves its producer under strategy P
-// and enters its consumer under strategy C.
-//
-// Inputs per tensor dimension d: the level run [plo[d], plo[d]+pw[d]) of its
-// producer axis and [clo[d], clo[d]+cw[d]) of its consumer axis (width 0 =
-// whole).  pcuts / ccuts: the strategies' cut masks.  tbytes = |T| x dtype.
-// ---------------------------------------------------------------------------
+__host__ __device__ inline uint32_t taps_msb(uint32_t v) { return 31u - (uint32_t)__builtin_clz(v); }
 
-struct taps_edge_problem {
-    uint32_t rank, n, lam;
-    uint32_t plo[TAPS_D_MAX_RANK], pw[TAPS_D_MAX_RANK];
-    uint32_t clo[TAPS_D_MAX_RANK], cw[TAPS_D_MAX_RANK];
-    uint32_t pcuts, ccuts;
-    uint64_t tbytes;
+// Producer side of one table row (uniform across a wavefront).
+struct taps_row {
+    uint32_t rank, n, lam, full;
+    uint32_t pr[TAPS_D_MAX_RANK];   // level run of dimension d (0 if whole)
+    uint32_t phi[TAPS_D_MAX_RANK];  // top level + 1 of that run
+    uint32_t pw[TAPS_D_MAX_RANK];   // its width
+    uint32_t pcuts;                 // cut mask of the producer strategy
+    uint32_t pru;                   // levels the producer map uses
+    uint32_t e0;                    // n - |pru|
 };
 
-// Per unified axis (indexed by its lowest level) after unification.
-struct taps_axes {
-    uint32_t start;                      // bit l: a unified axis starts at level l
-    uint32_t has_src, has_dst, home;     // axis sets (bit = its start level)
-    uint32_t width[TAPS_D_MAX_LEVELS];
-    uint32_t skey[TAPS_D_MAX_LEVELS];    // producer position dim*8+bit, or NONE
-    uint32_t dkey[TAPS_D_MAX_LEVELS];    // consumer position, or NONE
-    uint64_t tgt;                        // positions the consumer map uses
-    uint64_t occ0;                       // positions the producer map uses
-    uint32_t used0;                      // levels the producer map uses
-    uint64_t S0;                         // producer shard, nb
+// Consumer side of one table column.
+struct taps_col {
+    uint32_t cr[TAPS_D_MAX_RANK], chi[TAPS_D_MAX_RANK], cw[TAPS_D_MAX_RANK];
+    uint32_t ccuts;
 };
 
-__host__ __device__ inline uint64_t taps_bit64(uint32_t k) { return (uint64_t)1 << k; }
+// The unified problem of one entry.
+struct taps_lv {
+    uint32_t tp;            // tops of the unified axes
+    uint32_t p1, p2, p4;    // "same axis as the level above" masks for taps_fill
+    uint32_t src, dst;      // axes the producer / consumer maps use
+    uint32_t home;          // axes at the same position in both maps
+    uint32_t tgtsrc;        // producer positions the consumer map also uses
+    int32_t dl[TAPS_D_MAX_RANK];
+};
 
-// Unification (Table 1) as a least fixpoint over cuts, then the position of
-// every unified axis in the unified producer and consumer tensor maps.
-__host__ __device__ inline void taps_unify(const taps_edge_problem &p, taps_axes &ax) {
-    const uint32_t inner = taps_low_mask(p.n) & ~1u;   // valid cut bits 1..n-1
-    uint32_t C = (p.pcuts | p.ccuts) & inner;
+// One candidate sequence, in factor units.
+struct taps_fac {
+    uint32_t vol, intra, inter;
+    uint32_t n_coll, n_inter, sum_ct;
+};
+
+__host__ __device__ inline void taps_fac_zero(taps_fac &c) {
+    c.vol = c.intra = c.inter = 0;
+    c.n_coll = c.n_inter = c.sum_ct = 0;
+}
+
+// All levels of the axes whose tops are in x.
+__host__ __device__ inline uint32_t taps_fill(const taps_lv &L, uint32_t x) {
+    x |= (x >> 1) & L.p1;
+    x |= (x >> 2) & L.p2;
+    x |= (x >> 4) & L.p4;
+    return x;
+}
+
+// Unification (Table 1) as a least fixpoint over cuts: a cut inside the part
+// of a dimension both maps split forces the cut at the same bit of that
+// dimension on the other side.  Then the axes and their positions.
+__host__ __device__ inline void taps_unify(const taps_row &P, const taps_col &Q, taps_lv &L) {
+    uint32_t pwin[TAPS_D_MAX_RANK], cwin[TAPS_D_MAX_RANK];
+    uint32_t cru = 0, home = 0, tgt = 0;
+#pragma unroll
+    for (uint32_t d = 0; d < TAPS_D_MAX_RANK; ++d) {
+        pwin[d] = cwin[d] = 0;
+        L.dl[d] = 0;
+        if (d >= P.rank) continue;
+        const bool both = P.pw[d] && Q.cw[d];
+        const int32_t dl = both ? (int32_t)Q.chi[d] - (int32_t)P.phi[d] : 0;
+        L.dl[d] = dl;
+        const uint32_t m = P.pw[d] < Q.cw[d] ? P.pw[d] : Q.cw[d];
+        if (m >= 2) {
+            const uint32_t win = taps_low_mask(m - 1);
+            pwin[d] = win << (P.phi[d] - m + 1);
+            cwin[d] = win << (Q.chi[d] - m + 1);
+        }
+        cru |= Q.cr[d];
+        if (both && dl == 0) home |= P.pr[d] & Q.cr[d];
+        if (both) tgt |= P.pr[d] & taps_shift(Q.cr[d], -dl);
+    }
+    uint32_t C = (P.pcuts | Q.ccuts) & P.full & ~1u;
     for (uint32_t it = 0; it < TAPS_D_MAX_LEVELS; ++it) {
-        uint32_t before = C;
+        const uint32_t before = C;
 #pragma unroll
         for (uint32_t d = 0; d < TAPS_D_MAX_RANK; ++d) {
-            if (d >= p.rank) break;
-            uint32_t m = p.pw[d] < p.cw[d] ? p.pw[d] : p.cw[d];
-            if (m < 2) continue;
-            uint32_t phi = p.plo[d] + p.pw[d], chi = p.clo[d] + p.cw[d];
-            uint32_t win = taps_low_mask(m - 1);
-            uint32_t pwin = win << (phi - m + 1), cwin = win << (chi - m + 1);
-            if (chi >= phi) {
-                uint32_t sh = chi - phi;
-                C |= ((C & pwin) << sh) | ((C & cwin) >> sh);
-            } else {
-                uint32_t sh = phi - chi;
-                C |= ((C & pwin) >> sh) | ((C & cwin) << sh);
-            }
+            if (d >= P.rank) break;
+            C |= taps_shift(C & pwin[d], L.dl[d]) | taps_shift(C & cwin[d], -L.dl[d]);
         }
         if (C == before) break;
     }
-    ax.start = (C | 1u) & taps_low_mask(p.n);
-    if (p.n == 0) ax.start = 0;
-    ax.has_src = ax.has_dst = ax.home = 0;
-    ax.tgt = ax.occ0 = 0;
-    ax.used0 = 0;
-    uint32_t usedw = 0;
+    const uint32_t starts = (C | 1u) & P.full;
+    L.tp = P.n ? ((starts >> 1) | (1u << (P.n - 1))) & P.full : 0u;
+    L.p1 = ~(starts >> 1) & P.full;
+    L.p2 = L.p1 & (L.p1 >> 1);
+    L.p4 = L.p2 & (L.p2 >> 2);
+    L.src = L.tp & P.pru;
+    L.dst = L.tp & cru;
+    L.home = L.tp & home;
+    L.tgtsrc = L.tp & tgt;
+}
+
+// Consumer tops whose target position an axis in ats (producer tops) holds.
+__host__ __device__ inline uint32_t taps_blocked(const taps_row &P, const taps_col &Q,
+                                                 const taps_lv &L, uint32_t ats) {
+    uint32_t b = 0;
 #pragma unroll
-    for (uint32_t l = 0; l < TAPS_D_MAX_LEVELS; ++l) {
-        ax.skey[l] = TAPS_D_NONE;
-        ax.dkey[l] = TAPS_D_NONE;
-        ax.width[l] = 0;
-        if (!((ax.start >> l) & 1u)) continue;
-        uint32_t above = ax.start & ~taps_low_mask(l + 1);
-        uint32_t hi = above ? taps_ctz(above) : p.n;
-        ax.width[l] = hi - l;
-#pragma unroll
-        for (uint32_t d = 0; d < TAPS_D_MAX_RANK; ++d) {
-            if (d >= p.rank) break;
-            if (p.pw[d] && l >= p.plo[d] && l < p.plo[d] + p.pw[d])
-                ax.skey[l] = d * 8u + (p.plo[d] + p.pw[d] - hi);
-            if (p.cw[d] && l >= p.clo[d] && l < p.clo[d] + p.cw[d])
-                ax.dkey[l] = d * 8u + (p.clo[d] + p.cw[d] - hi);
-        }
-        if (ax.skey[l] != TAPS_D_NONE) {
-            ax.has_src |= 1u << l;
-            ax.occ0 |= taps_bit64(ax.skey[l]);
-            ax.used0 |= taps_low_mask(hi) & ~taps_low_mask(l);
-        }
-        if (ax.dkey[l] != TAPS_D_NONE) {
-            ax.has_dst |= 1u << l;
-            ax.tgt |= taps_bit64(ax.dkey[l]);
-        }
-        if (ax.skey[l] != TAPS_D_NONE && ax.skey[l] == ax.dkey[l]) ax.home |= 1u << l;
+    for (uint32_t d = 0; d < TAPS_D_MAX_RANK; ++d) {
+        if (d >= P.rank) break;
+        b |= taps_shift(ats & P.pr[d], L.dl[d]) & Q.cr[d];
     }
+    return b;
+}
+
+// The axis of x at the lowest producer position: lowest dimension, then its
+// highest level.
+__host__ __device__ inline uint32_t taps_first_src(const taps_row &P, uint32_t x) {
+    uint32_t r = TAPS_D_NONE;
 #pragma unroll
-    for (uint32_t d = 0; d < TAPS_D_MAX_RANK; ++d)
-        if (d < p.rank) usedw += p.pw[d];
-    ax.S0 = p.tbytes << (p.n - usedw);
+    for (uint32_t d = 0; d < TAPS_D_MAX_RANK; ++d) {
+        if (d >= P.rank) break;
+        const uint32_t y = x & P.pr[d];
+        if (r == TAPS_D_NONE && y) r = taps_msb(y);
+    }
+    return r;
 }
 
-__host__ __device__ inline uint32_t taps_levels(uint32_t lo, uint32_t w) {
-    return taps_low_mask(lo + w) & ~taps_low_mask(lo);
+// An AllGather (Eq. 9) or AllToAll (Eq. 10, Eq. 14) of the axis with top
+// level `top`, shard tbytes * 2^e, with the inter-node group count of
+// Algorithm 3: groups holding the same data inside a node (replicas along
+// levels no dimension uses) share one inter-node transfer.
+__host__ __device__ inline void taps_cost(taps_fac &c, bool a2a, uint32_t top, const taps_lv &L,
+                                          uint32_t lam, uint32_t e, uint32_t unused) {
+    const uint32_t below = L.tp & taps_low_mask(top);
+    const uint32_t lo = below ? taps_msb(below) + 1u : 0u;
+    const uint32_t w = top + 1u - lo;
+    const uint32_t sh = e + 8u;
+    const uint32_t V = a2a ? (1u << sh) - (1u << (sh - w)) : ((1u << w) - 1u) << sh;
+    const bool in_node = top < lam;   // the whole group inside one node
+    const uint32_t m = lo < lam ? lo : lam;
+    const uint32_t lct = m - taps_popc(unused & taps_low_mask(m));
+    const uint32_t kap = lam > lo ? lam - lo : 0u;   // log2 of group members per node
+    const uint32_t link = a2a ? ((1u << w) - (1u << kap)) << (kap + sh - w) : V;
+    c.vol += V;
+    c.n_coll += 1;
+    c.intra += in_node ? V : 0u;
+    c.inter += in_node ? 0u : link << lct;
+    c.n_inter += in_node ? 0u : 1u;
+    c.sum_ct += in_node ? 0u : 1u << lct;
 }
 
-// Algorithm 1 (use_a2a) or its variant without AllToAll ("rearrange").
-// Returns the number of AllToAlls issued; *ok = false if the loop did not
-// settle (cannot happen for a unified problem).
-__host__ __device__ inline uint32_t taps_alg1(const taps_axes &ax, uint32_t lam, bool use_a2a,
-                                              taps_acc &c, bool *ok) {
-    uint32_t at_src = ax.has_src & ~ax.home;    // mapped by the producer, not at its target
-    uint32_t at_dst = ax.home;                  // at its target position
-    uint64_t occ = ax.occ0;
-    uint32_t unused = ~ax.used0;
-    uint64_t S = ax.S0;
+struct taps_run {
+    taps_fac c;
+    uint32_t n_a2a;   // AllToAlls issued
+    bool ok;          // false if the loop did not settle (cannot happen)
+};
+
+// Algorithm 1 (use_a2a) or the same without AllToAll ("rearrange").
+__host__ __device__ inline taps_run taps_alg1(const taps_row &P, const taps_col &Q,
+                                              const taps_lv &L, bool use_a2a) {
+    taps_fac c;
+    taps_fac_zero(c);
+    uint32_t ats = L.src & ~L.home;   // held at a producer position that is not its target
+    uint32_t atd = L.home;            // at its target position
+    uint32_t unused = P.full & ~P.pru;
+    uint32_t e = P.e0;
     uint32_t n_a2a = 0;
-    *ok = true;
+    bool ok = true;
     for (uint32_t guard = 0;; ++guard) {
-        if (at_src == 0 && at_dst == ax.has_dst) break;
+        if (ats == 0 && atd == L.dst) break;
         if (guard > 4 * TAPS_D_MAX_LEVELS) {
-            *ok = false;
+            ok = false;
             break;
         }
-        bool sliced;
+        uint32_t sl;
         do {
-            // InferSlice: every target position that is free and whose axis
-            // no dimension uses yet
-            uint32_t sl = 0;
-#pragma unroll
-            for (uint32_t l = 0; l < TAPS_D_MAX_LEVELS; ++l) {
-                uint32_t b = 1u << l;
-                if ((ax.has_dst & b) && !((at_src | at_dst) & b) && !((occ >> ax.dkey[l]) & 1u))
-                    sl |= b;
+            // InferSlice: free target positions whose axes no dimension uses
+            sl = L.dst & ~(ats | atd) & ~taps_blocked(P, Q, L, ats);
+            if (sl) {
+                const uint32_t lv = taps_fill(L, sl);
+                atd |= sl;
+                unused &= ~lv;
+                e -= taps_popc(lv);
             }
-#pragma unroll
-            for (uint32_t l = 0; l < TAPS_D_MAX_LEVELS; ++l) {
-                if (!((sl >> l) & 1u)) continue;
-                occ |= taps_bit64(ax.dkey[l]);
-                S >>= ax.width[l];
-                unused &= ~taps_levels(l, ax.width[l]);
-            }
-            at_dst |= sl;
-            sliced = sl != 0;
-            // InferAll2All until none: an axis held elsewhere moves to its
-            // target position once that position is free
+            // InferAll2All until none: held axes move to free targets
             while (use_a2a) {
-                uint32_t mv = 0;
-#pragma unroll
-                for (uint32_t l = 0; l < TAPS_D_MAX_LEVELS; ++l) {
-                    uint32_t b = 1u << l;
-                    if ((at_src & ax.has_dst & b) && !((occ >> ax.dkey[l]) & 1u)) mv |= b;
-                }
+                const uint32_t mv = L.dst & ats & ~taps_blocked(P, Q, L, ats);
                 if (!mv) break;
-#pragma unroll
-                for (uint32_t l = 0; l < TAPS_D_MAX_LEVELS; ++l) {
-                    if (!((mv >> l) & 1u)) continue;
-                    taps_collective(c, true, l, ax.width[l], S, unused, lam);
-                    occ ^= taps_bit64(ax.skey[l]) | taps_bit64(ax.dkey[l]);
+                uint32_t m = mv;
+                while (m) {
+                    const uint32_t top = taps_msb(m);
+                    m &= ~(1u << top);
+                    taps_cost(c, true, top, L, P.lam, e, unused);
                     ++n_a2a;
                 }
-                at_src &= ~mv;
-                at_dst |= mv;
+                ats &= ~mv;
+                atd |= mv;
             }
-        } while (sliced);
-        // InferAllGather: the lowest producer position the consumer does not
-        // use; else AllGatherFirstUndoneDim: the lowest one not yet right
-        // key = position << 8 | level << 4 | width keeps the choice in registers
-        uint32_t best = 0xFFFFFu, best_any = 0xFFFFFu;
-#pragma unroll
-        for (uint32_t l = 0; l < TAPS_D_MAX_LEVELS; ++l) {
-            if (!((at_src >> l) & 1u)) continue;
-            uint32_t key = (ax.skey[l] << 8) | (l << 4) | ax.width[l];
-            if (!((ax.tgt >> ax.skey[l]) & 1u) && key < best) best = key;
-            if (key < best_any) best_any = key;
-        }
-        if (best == 0xFFFFFu) best = best_any;
-        if (best != 0xFFFFFu) {
-            uint32_t l = (best >> 4) & 15u, w = best & 15u;
-            taps_collective(c, false, l, w, S, unused, lam);
-            occ &= ~taps_bit64(best >> 8);
-            at_src &= ~(1u << l);
-            S <<= w;
-            unused |= taps_levels(l, w);
+        } while (sl);
+        // InferAllGather: lowest held position the consumer does not use;
+        // else AllGatherFirstUndoneDim: lowest held position
+        const uint32_t ug = ats & ~L.tgtsrc;
+        const uint32_t x = ug ? ug : ats;
+        if (x) {
+            const uint32_t top = taps_first_src(P, x);
+            taps_cost(c, false, top, L, P.lam, e, unused);
+            const uint32_t lv = taps_fill(L, 1u << top);
+            ats &= ~(1u << top);
+            unused |= lv;
+            e += taps_popc(lv);
         }
     }
-    return n_a2a;
+    taps_run r;
+    r.c = c;
+    r.n_a2a = n_a2a;
+    r.ok = ok;
+    return r;
 }
 
-// "remove" (Table 2): gather every producer-mapped axis that is not at its
-// target, lowest position first, then slice (free).
-__host__ __device__ inline void taps_remove(const taps_axes &ax, uint32_t lam, taps_acc &c) {
-    uint32_t todo = ax.has_src & ~ax.home;
-    uint32_t unused = ~ax.used0;
-    uint64_t S = ax.S0;
-    while (todo) {
-        uint32_t best = 0xFFFFFu;
-#pragma unroll
-        for (uint32_t l = 0; l < TAPS_D_MAX_LEVELS; ++l) {
-            if (!((todo >> l) & 1u)) continue;
-            uint32_t key = (ax.skey[l] << 8) | (l << 4) | ax.width[l];
-            if (key < best) best = key;
-        }
-        uint32_t l = (best >> 4) & 15u, w = best & 15u;
-        taps_collective(c, false, l, w, S, unused, lam);
-        todo &= ~(1u << l);
-        S <<= w;
-        unused |= taps_levels(l, w);
+// "remove" (Table 2): gather every held axis not at its target, lowest
+// position first; the slices that follow are free.
+__host__ __device__ inline taps_fac taps_remove(const taps_row &P, const taps_lv &L) {
+    taps_fac c;
+    taps_fac_zero(c);
+    uint32_t x = L.src & ~L.home;
+    uint32_t unused = P.full & ~P.pru;
+    uint32_t e = P.e0;
+    while (x) {
+        const uint32_t top = taps_first_src(P, x);
+        taps_cost(c, false, top, L, P.lam, e, unused);
+        const uint32_t lv = taps_fill(L, 1u << top);
+        x &= ~(1u << top);
+        unused |= lv;
+        e += taps_popc(lv);
     }
+    return c;
 }
 
-// Exact comparison of intra/(N B_intra) + inter/(N B_inter) between two
-// candidates: compare intra * bi + inter * ba with bi = B_inter / g,
-// ba = B_intra / g (g = gcd of the two bandwidths), in 128 bits.
-__host__ __device__ inline unsigned __int128 taps_key(const taps_acc &c, uint64_t b_inter_red,
-                                                      uint64_t b_intra_red) {
-    return (unsigned __int128)c.intra * b_inter_red + (unsigned __int128)c.inter * b_intra_red;
+// tbytes * f / 256, exact (the result is an integer volume in nb < 2^64).
+__host__ __device__ inline uint64_t taps_scale(uint64_t tbytes, uint32_t f) {
+    return (((tbytes & 0xFFFFFFFFull) * f) >> 8) + (((tbytes >> 32) * f) << 24);
+}
+
+// Exact order of intra/(N B_intra) + inter/(N B_inter) between candidates:
+// intra * bi + inter * ba with bi = B_inter / g, ba = B_intra / g
+// (g = gcd of the two).  Both products fit 64 bits when bi, ba < 2^32.
+struct taps_keys {
+    uint64_t b_inter_red, b_intra_red;
+    bool narrow;   // both reduced bandwidths below 2^32
+};
+
+__host__ __device__ inline bool taps_less(const taps_fac &a, const taps_fac &b,
+                                          const taps_keys &K) {
+    if (K.narrow) {
+        const uint64_t ka = (uint64_t)a.intra * K.b_inter_red + (uint64_t)a.inter * K.b_intra_red;
+        const uint64_t kb = (uint64_t)b.intra * K.b_inter_red + (uint64_t)b.inter * K.b_intra_red;
+        return ka < kb;
+    }
+    const unsigned __int128 ka =
+        (unsigned __int128)a.intra * K.b_inter_red + (unsigned __int128)a.inter * K.b_intra_red;
+    const unsigned __int128 kb =
+        (unsigned __int128)b.intra * K.b_inter_red + (unsigned __int128)b.inter * K.b_intra_red;
+    return ka < kb;
 }
 
 struct taps_entry_out {
@@ -448,48 +497,73 @@ struct taps_entry_out {
 };
 
 // The cheapest of Algorithm 1, Algorithm 1 without AllToAll, and "remove"
-// (the naive sequence gathers a superset of what "remove" gathers, in the
-// same order, so it is never cheaper in either model and never wins a tie);
-// vol is the smallest volume among them.
-__host__ __device__ inline taps_entry_out taps_edge_entry(const taps_edge_problem &p,
-                                                          uint64_t b_inter_red,
-                                                          uint64_t b_intra_red, double inv_n_bintra,
+// (the naive sequence of Table 2 gathers a superset of what "remove"
+// gathers, in the same order, so it is never cheaper in either model and
+// never wins a tie); vol is the smallest volume among them.
+__host__ __device__ inline taps_entry_out taps_edge_entry(const taps_row &P, const taps_col &Q,
+                                                          uint64_t tbytes, const taps_keys &K,
+                                                          double inv_n_bintra,
                                                           double inv_n_binter) {
-    taps_axes ax;
-    taps_unify(p, ax);
-    taps_acc c0, c1, c2;
-    taps_acc_zero(c0);
-    taps_acc_zero(c1);
-    taps_acc_zero(c2);
-    bool ok0 = true, ok1 = true;
-    uint32_t n_a2a = taps_alg1(ax, p.lam, true, c0, &ok0);
-    if (n_a2a)
-        taps_alg1(ax, p.lam, false, c1, &ok1);
-    else
-        c1 = c0;
-    taps_remove(ax, p.lam, c2);
-    unsigned __int128 k0 = taps_key(c0, b_inter_red, b_intra_red);
-    unsigned __int128 k1 = taps_key(c1, b_inter_red, b_intra_red);
-    unsigned __int128 k2 = taps_key(c2, b_inter_red, b_intra_red);
-    taps_acc best = c0;
+    taps_lv L;
+    taps_unify(P, Q, L);
+    const taps_run r0 = taps_alg1(P, Q, L, true);
+    const taps_run r1 = r0.n_a2a ? taps_alg1(P, Q, L, false) : r0;
+    const taps_fac c0 = r0.c, c1 = r1.c, c2 = taps_remove(P, L);
+    taps_fac best = c0;
     uint32_t cand = 0;
-    unsigned __int128 kb = k0;
-    if (k1 < kb) {
+    if (taps_less(c1, best, K)) {
         best = c1;
         cand = 1;
-        kb = k1;
     }
-    if (k2 < kb) {
+    if (taps_less(c2, best, K)) {
         best = c2;
         cand = 2;
     }
+    uint32_t vmin = c0.vol < c1.vol ? c0.vol : c1.vol;
+    vmin = vmin < c2.vol ? vmin : c2.vol;
     taps_entry_out o;
-    uint64_t v = c0.vol < c1.vol ? c0.vol : c1.vol;
-    o.vol = v < c2.vol ? v : c2.vol;
-    o.intra = best.intra;
-    o.inter = best.inter;
-    o.t = (double)best.intra * inv_n_bintra + (double)best.inter * inv_n_binter;
-    o.meta = taps_meta(cand, best);
-    o.ok = ok0 && ok1;
+    o.vol = taps_scale(tbytes, vmin);
+    o.intra = taps_scale(tbytes, best.intra);
+    o.inter = taps_scale(tbytes, best.inter);
+    o.t = (double)o.intra * inv_n_bintra + (double)o.inter * inv_n_binter;
+    o.meta = cand | (best.n_coll << 2) | (best.n_inter << 7) | (best.sum_ct << 12);
+    o.ok = r0.ok && r1.ok;
     return o;
+}
+
+// Producer side of a row from a strategy descriptor and the tensor's axes
+// (nibble d of `axes` = op axis of dimension d).
+__host__ __device__ inline void taps_make_row(taps_row &P, const taps_desc &D, uint32_t axes,
+                                              uint32_t rank, uint32_t n, uint32_t lam) {
+    P.rank = rank;
+    P.n = n;
+    P.lam = lam;
+    P.full = taps_low_mask(n);
+    P.pcuts = D.cuts;
+    P.pru = 0;
+    uint32_t used = 0;
+#pragma unroll
+    for (uint32_t d = 0; d < TAPS_D_MAX_RANK; ++d) {
+        const uint32_t a = taps_nib(axes, d);
+        const uint32_t lo = taps_nib(D.lo, a), w = d < rank ? taps_nib(D.width, a) : 0u;
+        P.pw[d] = w;
+        P.phi[d] = lo + w;
+        P.pr[d] = taps_levels(lo, w);
+        P.pru |= P.pr[d];
+        used += w;
+    }
+    P.e0 = n - used;
+}
+
+__host__ __device__ inline void taps_make_col(taps_col &Q, const taps_desc &D, uint32_t axes,
+                                              uint32_t rank) {
+    Q.ccuts = D.cuts;
+#pragma unroll
+    for (uint32_t d = 0; d < TAPS_D_MAX_RANK; ++d) {
+        const uint32_t a = taps_nib(axes, d);
+        const uint32_t lo = taps_nib(D.lo, a), w = d < rank ? taps_nib(D.width, a) : 0u;
+        Q.cw[d] = w;
+        Q.chi[d] = lo + w;
+        Q.cr[d] = taps_levels(lo, w);
+    }
 }

@@ -15,6 +15,7 @@ struct taps_launch {
     uint64_t b_intra_red;   // B_intra / gcd(B_intra, B_inter)
     double inv_n_bintra;    // 1 / (N B_intra)
     double inv_n_binter;    // 1 / (N B_inter)
+    uint32_t narrow;        // both reduced bandwidths below 2^32
 };
 
 // Per-edge constants of the edge-table kernel (64 bytes).
@@ -31,7 +32,10 @@ struct taps_edge_params {
     uint32_t pad;
 };
 
-#define TAPS_EDGE_TILE 256   // entries (= threads) per edge workgroup
+// An edge tile is one table row (producer strategy) times 64 consecutive
+// columns (consumer strategies): one wavefront.  A workgroup runs four.
+#define TAPS_TILE_COLS 64
+#define TAPS_TILES_PER_BLOCK 4
 
 hipError_t taps_launch_enumerate(const taps_op *ops, uint32_t n_ops, uint32_t n,
                                  const uint64_t *offsets, uint32_t *counts, taps_strategy *out,

@@ -6,9 +6,9 @@
 //   k_node_costs  one thread per strategy: the intra-op AllReduces
 //   k_edge_setup  one thread per edge: per-edge constants
 //   k_tile_map    one thread per edge tile: which edge the tile belongs to
-//   k_edge_costs  one 256-thread workgroup per tile of 256 consecutive
-//                 entries of one edge table (row-major, so lanes cover
-//                 consecutive consumer strategies); one entry per lane;
+//   k_edge_costs  one wavefront per tile = one table row (producer strategy,
+//                 uniform: its descriptor sits in scalar registers) x 64
+//                 consecutive columns (consumer strategies, one per lane);
 //                 five coalesced non-temporal SoA stores per entry
 #include "taps_internal.h"
 
@@ -173,43 +173,31 @@ __global__ __launch_bounds__(256) void k_tile_map(const uint64_t *__restrict__ t
     tile_edge[t] = find_owner(tile_begin, n_edges, t);
 }
 
-__global__ __launch_bounds__(TAPS_EDGE_TILE) void k_edge_costs(
+__global__ __launch_bounds__(TAPS_TILE_COLS * TAPS_TILES_PER_BLOCK) void k_edge_costs(
     const taps_edge_params *__restrict__ params, const uint32_t *__restrict__ tile_edge,
-    const taps_desc *__restrict__ desc, taps_launch lp, taps_table out) {
-    const uint32_t e = tile_edge[blockIdx.x];
+    uint64_t n_tiles, const taps_desc *__restrict__ desc, taps_launch lp, taps_table out) {
+    // everything up to the column index is uniform across the wavefront
+    const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x / TAPS_TILE_COLS);
+    const uint32_t lane = threadIdx.x % TAPS_TILE_COLS;
+    const uint64_t tile = (uint64_t)blockIdx.x * TAPS_TILES_PER_BLOCK + wave;
+    if (tile >= n_tiles) return;
+    const uint32_t e = __builtin_amdgcn_readfirstlane(tile_edge[tile]);
     const taps_edge_params E = params[e];
-    const uint64_t local = (uint64_t)(blockIdx.x - E.tile_begin) * TAPS_EDGE_TILE + threadIdx.x;
-    const uint64_t entries = (uint64_t)E.ns * E.nd;
-    if (local >= entries) return;
-    uint64_t i, j;
-    if (entries <= 0xFFFFFFFFull) {
-        const uint32_t l32 = (uint32_t)local;
-        i = l32 / E.nd;
-        j = l32 - (uint32_t)i * E.nd;
-    } else {
-        i = local / E.nd;
-        j = local - i * E.nd;
-    }
-    const taps_desc Dp = desc[E.src_base + i];
-    const taps_desc Dc = desc[E.dst_base + j];
-    taps_edge_problem p;
-    p.rank = E.rank;
-    p.n = lp.n;
-    p.lam = lp.lam;
-    p.tbytes = E.tbytes;
-    p.pcuts = Dp.cuts;
-    p.ccuts = Dc.cuts;
-#pragma unroll
-    for (uint32_t d = 0; d < TAPS_D_MAX_RANK; ++d) {
-        const uint32_t ap = taps_nib(E.paxes, d), ac = taps_nib(E.caxes, d);
-        p.plo[d] = taps_nib(Dp.lo, ap);
-        p.pw[d] = d < E.rank ? taps_nib(Dp.width, ap) : 0u;
-        p.clo[d] = taps_nib(Dc.lo, ac);
-        p.cw[d] = d < E.rank ? taps_nib(Dc.width, ac) : 0u;
-    }
-    const taps_entry_out o =
-        taps_edge_entry(p, lp.b_inter_red, lp.b_intra_red, lp.inv_n_bintra, lp.inv_n_binter);
-    const uint64_t g = E.out_offset + local;
+    const uint32_t row_tiles = (E.nd + TAPS_TILE_COLS - 1) / TAPS_TILE_COLS;
+    const uint32_t lt = (uint32_t)(tile - E.tile_begin);
+    const uint32_t i = __builtin_amdgcn_readfirstlane(lt / row_tiles);
+    const uint32_t j = (lt - i * row_tiles) * TAPS_TILE_COLS + lane;
+    if (j >= E.nd) return;
+    taps_row P;
+    taps_make_row(P, desc[E.src_base + i], E.paxes, E.rank, lp.n, lp.lam);
+    taps_col Q;
+    taps_make_col(Q, desc[E.dst_base + j], E.caxes, E.rank);
+    taps_keys K;
+    K.b_inter_red = lp.b_inter_red;
+    K.b_intra_red = lp.b_intra_red;
+    K.narrow = lp.narrow != 0;
+    const taps_entry_out o = taps_edge_entry(P, Q, E.tbytes, K, lp.inv_n_bintra, lp.inv_n_binter);
+    const uint64_t g = E.out_offset + (uint64_t)i * E.nd + j;
     __builtin_nontemporal_store(o.t, out.t + g);
     __builtin_nontemporal_store(o.vol, out.vol + g);
     __builtin_nontemporal_store(o.intra, out.intra + g);
@@ -265,7 +253,8 @@ hipError_t taps_launch_edge_costs(const taps_edge_params *params, const uint32_t
                                   uint64_t n_tiles, const taps_desc *desc, const taps_launch &lp,
                                   taps_table out, hipStream_t stream) {
     if (n_tiles == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_edge_costs, dim3((uint32_t)n_tiles), dim3(TAPS_EDGE_TILE), 0, stream,
-                       params, tile_edge, desc, lp, out);
+    hipLaunchKernelGGL(k_edge_costs, dim3(blocks_for(n_tiles, TAPS_TILES_PER_BLOCK)),
+                       dim3(TAPS_TILE_COLS * TAPS_TILES_PER_BLOCK), 0, stream, params, tile_edge,
+                       n_tiles, desc, lp, out);
     return hipGetLastError();
 }
