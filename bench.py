@@ -66,7 +66,19 @@ def main() -> int:
     ap.add_argument("--config", type=int, default=5, help="workload 1..5 (default: 5, the largest)")
     ap.add_argument("--cpu-layers", type=int, default=3,
                     help="layers of the graph the CPU oracle baseline covers (0 = skip)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="only run a plain device-to-device copy of BYTES bytes (to scale HBM "
+                         "traffic counters), then exit")
     args = ap.parse_args()
+    if args.copy_calibration:
+        import torch
+        src = torch.ones(args.copy_calibration // 4, dtype=torch.int32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": src.numel() * 4, "launches": 3}))
+        return 0
     if args.gpus != 1:
         print(f"bench.py measures one GPU: the cost tables of one modeled cluster are built on a "
               f"single device (asked for --gpus {args.gpus}).", file=sys.stderr)

@@ -51,9 +51,12 @@ __host__ __device__ inline uint32_t taps_ctz(uint32_t v) { return (uint32_t)__bu
 
 __host__ __device__ inline uint32_t taps_low_mask(uint32_t k) { return k >= 32u ? ~0u : ((1u << k) - 1u); }
 
-// Levels lo .. lo+w-1.
+// Bits 0..k-1 for k < 32.
+__host__ __device__ inline uint32_t taps_below(uint32_t k) { return (1u << k) - 1u; }
+
+// Levels lo .. lo+w-1 (lo + w <= 8).
 __host__ __device__ inline uint32_t taps_levels(uint32_t lo, uint32_t w) {
-    return taps_low_mask(lo + w) & ~taps_low_mask(lo);
+    return taps_below(lo + w) & ~taps_below(lo);
 }
 
 // ---------------------------------------------------------------------------
@@ -244,6 +247,11 @@ struct taps_row {
     uint32_t pcuts;                 // cut mask of the producer strategy
     uint32_t pru;                   // levels the producer map uses
     uint32_t e0;                    // n - |pru|
+    // Producer positions in order (dimension ascending, then bit ascending,
+    // i.e. level descending): rank r holds level nibble r of `order`;
+    // to_rank[x] is the level mask x with level l moved to bit rank(l).
+    uint32_t order;
+    const uint8_t *to_rank;
 };
 
 // Consumer side of one table column.
@@ -265,12 +273,12 @@ struct taps_lv {
 // One candidate sequence, in factor units.
 struct taps_fac {
     uint32_t vol, intra, inter;
-    uint32_t n_coll, n_inter, sum_ct;
+    uint32_t counts;   // collectives | inter-node collectives << 8 | sum of ct << 16
 };
 
 __host__ __device__ inline void taps_fac_zero(taps_fac &c) {
     c.vol = c.intra = c.inter = 0;
-    c.n_coll = c.n_inter = c.sum_ct = 0;
+    c.counts = 0;
 }
 
 // All levels of the axes whose tops are in x.
@@ -338,17 +346,14 @@ __host__ __device__ inline uint32_t taps_blocked(const taps_row &P, const taps_c
     return b;
 }
 
-// The axis of x at the lowest producer position: lowest dimension, then its
-// highest level.
+// The level holding producer-order rank k.
+__host__ __device__ inline uint32_t taps_rank_level(const taps_row &P, uint32_t k) {
+    return (P.order >> (4u * k)) & 15u;
+}
+
+// The axis of x (non-empty, producer levels) at the lowest producer position.
 __host__ __device__ inline uint32_t taps_first_src(const taps_row &P, uint32_t x) {
-    uint32_t r = TAPS_D_NONE;
-#pragma unroll
-    for (uint32_t d = 0; d < TAPS_D_MAX_RANK; ++d) {
-        if (d >= P.rank) break;
-        const uint32_t y = x & P.pr[d];
-        if (r == TAPS_D_NONE && y) r = taps_msb(y);
-    }
-    return r;
+    return taps_rank_level(P, taps_ctz(P.to_rank[x]));
 }
 
 // An AllGather (Eq. 9) or AllToAll (Eq. 10, Eq. 14) of the axis with top
@@ -357,114 +362,21 @@ __host__ __device__ inline uint32_t taps_first_src(const taps_row &P, uint32_t x
 // levels no dimension uses) share one inter-node transfer.
 __host__ __device__ inline void taps_cost(taps_fac &c, bool a2a, uint32_t top, const taps_lv &L,
                                           uint32_t lam, uint32_t e, uint32_t unused) {
-    const uint32_t below = L.tp & taps_low_mask(top);
-    const uint32_t lo = below ? taps_msb(below) + 1u : 0u;
+    // lowest level of the axis: one above the next lower top (0 if none)
+    const uint32_t lo = taps_msb(((L.tp & taps_below(top)) << 1) | 1u);
     const uint32_t w = top + 1u - lo;
     const uint32_t sh = e + 8u;
     const uint32_t V = a2a ? (1u << sh) - (1u << (sh - w)) : ((1u << w) - 1u) << sh;
     const bool in_node = top < lam;   // the whole group inside one node
     const uint32_t m = lo < lam ? lo : lam;
-    const uint32_t lct = m - taps_popc(unused & taps_low_mask(m));
+    const uint32_t lct = m - taps_popc(unused & taps_below(m));
     const uint32_t kap = lam > lo ? lam - lo : 0u;   // log2 of group members per node
     const uint32_t link = a2a ? ((1u << w) - (1u << kap)) << (kap + sh - w) : V;
     c.vol += V;
-    c.n_coll += 1;
     c.intra += in_node ? V : 0u;
     c.inter += in_node ? 0u : link << lct;
-    c.n_inter += in_node ? 0u : 1u;
-    c.sum_ct += in_node ? 0u : 1u << lct;
-}
-
-struct taps_run {
-    taps_fac c;
-    uint32_t n_a2a;   // AllToAlls issued
-    bool ok;          // false if the loop did not settle (cannot happen)
-};
-
-// Algorithm 1 (use_a2a) or the same without AllToAll ("rearrange").
-__host__ __device__ inline taps_run taps_alg1(const taps_row &P, const taps_col &Q,
-                                              const taps_lv &L, bool use_a2a) {
-    taps_fac c;
-    taps_fac_zero(c);
-    uint32_t ats = L.src & ~L.home;   // held at a producer position that is not its target
-    uint32_t atd = L.home;            // at its target position
-    uint32_t unused = P.full & ~P.pru;
-    uint32_t e = P.e0;
-    uint32_t n_a2a = 0;
-    bool ok = true;
-    for (uint32_t guard = 0;; ++guard) {
-        if (ats == 0 && atd == L.dst) break;
-        if (guard > 4 * TAPS_D_MAX_LEVELS) {
-            ok = false;
-            break;
-        }
-        uint32_t sl;
-        do {
-            // InferSlice: free target positions whose axes no dimension uses
-            sl = L.dst & ~(ats | atd) & ~taps_blocked(P, Q, L, ats);
-            if (sl) {
-                const uint32_t lv = taps_fill(L, sl);
-                atd |= sl;
-                unused &= ~lv;
-                e -= taps_popc(lv);
-            }
-            // InferAll2All until none: held axes move to free targets
-            while (use_a2a) {
-                const uint32_t mv = L.dst & ats & ~taps_blocked(P, Q, L, ats);
-                if (!mv) break;
-                uint32_t m = mv;
-                while (m) {
-                    const uint32_t top = taps_msb(m);
-                    m &= ~(1u << top);
-                    taps_cost(c, true, top, L, P.lam, e, unused);
-                    ++n_a2a;
-                }
-                ats &= ~mv;
-                atd |= mv;
-            }
-        } while (sl);
-        // InferAllGather: lowest held position the consumer does not use;
-        // else AllGatherFirstUndoneDim: lowest held position
-        const uint32_t ug = ats & ~L.tgtsrc;
-        const uint32_t x = ug ? ug : ats;
-        if (x) {
-            const uint32_t top = taps_first_src(P, x);
-            taps_cost(c, false, top, L, P.lam, e, unused);
-            const uint32_t lv = taps_fill(L, 1u << top);
-            ats &= ~(1u << top);
-            unused |= lv;
-            e += taps_popc(lv);
-        }
-    }
-    taps_run r;
-    r.c = c;
-    r.n_a2a = n_a2a;
-    r.ok = ok;
-    return r;
-}
-
-// "remove" (Table 2): gather every held axis not at its target, lowest
-// position first; the slices that follow are free.
-__host__ __device__ inline taps_fac taps_remove(const taps_row &P, const taps_lv &L) {
-    taps_fac c;
-    taps_fac_zero(c);
-    uint32_t x = L.src & ~L.home;
-    uint32_t unused = P.full & ~P.pru;
-    uint32_t e = P.e0;
-    while (x) {
-        const uint32_t top = taps_first_src(P, x);
-        taps_cost(c, false, top, L, P.lam, e, unused);
-        const uint32_t lv = taps_fill(L, 1u << top);
-        x &= ~(1u << top);
-        unused |= lv;
-        e += taps_popc(lv);
-    }
-    return c;
-}
-
-// tbytes * f / 256, exact (the result is an integer volume in nb < 2^64).
-__host__ __device__ inline uint64_t taps_scale(uint64_t tbytes, uint32_t f) {
-    return (((tbytes & 0xFFFFFFFFull) * f) >> 8) + (((tbytes >> 32) * f) << 24);
+    // collectives (bits 0-7), inter-node ones (8-15), sum of their ct (16-31)
+    c.counts += in_node ? 1u : 0x101u + ((1u << lct) << 16);
 }
 
 // Exact order of intra/(N B_intra) + inter/(N B_inter) between candidates:
@@ -475,18 +387,179 @@ struct taps_keys {
     bool narrow;   // both reduced bandwidths below 2^32
 };
 
+__host__ __device__ inline uint64_t taps_key64(const taps_fac &a, const taps_keys &K) {
+    return (uint64_t)a.intra * (uint32_t)K.b_inter_red + (uint64_t)a.inter * (uint32_t)K.b_intra_red;
+}
+
 __host__ __device__ inline bool taps_less(const taps_fac &a, const taps_fac &b,
                                           const taps_keys &K) {
-    if (K.narrow) {
-        const uint64_t ka = (uint64_t)a.intra * K.b_inter_red + (uint64_t)a.inter * K.b_intra_red;
-        const uint64_t kb = (uint64_t)b.intra * K.b_inter_red + (uint64_t)b.inter * K.b_intra_red;
-        return ka < kb;
-    }
+    if (K.narrow) return taps_key64(a, K) < taps_key64(b, K);
     const unsigned __int128 ka =
         (unsigned __int128)a.intra * K.b_inter_red + (unsigned __int128)a.inter * K.b_intra_red;
     const unsigned __int128 kb =
         (unsigned __int128)b.intra * K.b_inter_red + (unsigned __int128)b.inter * K.b_intra_red;
     return ka < kb;
+}
+
+// A later candidate can stop early: every collective adds to both its key
+// and its volume, so once the running key reaches the best key so far and
+// the running volume reaches the smallest volume so far it can neither be
+// chosen (ties go to the earlier candidate) nor lower the volume.
+struct taps_limit {
+    bool on;
+    uint64_t key;
+    uint32_t vol;
+};
+
+__host__ __device__ inline bool taps_hopeless(const taps_fac &c, const taps_limit &lim,
+                                              const taps_keys &K) {
+    return lim.on && c.vol >= lim.vol && taps_key64(c, K) >= lim.key;
+}
+
+struct taps_run {
+    taps_fac c;
+    uint32_t n_a2a;   // AllToAlls issued
+    bool ok;          // false if the loop did not settle (cannot happen)
+    bool stopped;     // stopped early: cannot beat the limit it was given
+};
+
+// Running state of one sequence: axes held at their producer position (ats)
+// and at their target (atd), consumer tops whose target an at-src axis holds
+// (blk), free levels (unused) and the shard exponent e (shard = tbytes 2^e).
+struct taps_state {
+    uint32_t ats, atd, blk, unused, e;
+};
+
+__host__ __device__ inline void taps_gather(const taps_row &P, const taps_lv &L, taps_state &s,
+                                            taps_fac &c, uint32_t top) {
+    taps_cost(c, false, top, L, P.lam, s.e, s.unused);
+    const uint32_t lv = taps_fill(L, 1u << top);
+    s.ats &= ~(1u << top);
+    s.unused |= lv;
+    s.e += taps_popc(lv);
+}
+
+// Every free target position whose axis no dimension uses is sliced.
+__host__ __device__ inline uint32_t taps_slice(const taps_lv &L, taps_state &s) {
+    const uint32_t sl = L.dst & ~(s.ats | s.atd) & ~s.blk;
+    if (sl) {
+        const uint32_t lv = taps_fill(L, sl);
+        s.atd |= sl;
+        s.unused &= ~lv;
+        s.e -= taps_popc(lv);
+    }
+    return sl;
+}
+
+// Algorithm 1 (use_a2a) or the same without AllToAll ("rearrange").
+//
+// Equivalent schedule of the printed loop:
+//   * one pass of the inner loop is InferSlice, then InferAll2All until
+//     nothing moves; a slice never frees a position, so a second pass can
+//     only slice (targets the AllToAlls freed) and a third finds nothing;
+//   * an AllGather of an axis whose producer position no consumer axis
+//     targets frees no position, so the next inner loop can only slice that
+//     same axis into its target (possible without AllToAll: with AllToAll a
+//     mover with a free target has already moved); such gathers therefore
+//     run back to back, lowest position first, until one leaves a slice
+//     pending (or one was pending from the last AllToAlls).
+__host__ __device__ inline taps_run taps_alg1(const taps_row &P, const taps_col &Q,
+                                              const taps_lv &L, bool use_a2a,
+                                              const taps_limit &lim, const taps_keys &K) {
+    taps_fac c;
+    taps_fac_zero(c);
+    taps_state s;
+    s.ats = L.src & ~L.home;
+    s.atd = L.home;
+    s.blk = taps_blocked(P, Q, L, s.ats);
+    s.unused = P.full & ~P.pru;
+    s.e = P.e0;
+    uint32_t n_a2a = 0;
+    bool ok = true, stopped = false;
+    for (uint32_t guard = 0;; ++guard) {
+        if (guard > 4 * TAPS_D_MAX_LEVELS) {
+            ok = false;
+            break;
+        }
+        if (taps_hopeless(c, lim, K)) {
+            stopped = true;
+            break;
+        }
+        // inner loop
+        const uint32_t sl = taps_slice(L, s);
+        while (use_a2a) {
+            const uint32_t mv = L.dst & s.ats & ~s.blk;
+            if (!mv) break;
+            uint32_t m = mv;
+            while (m) {
+                const uint32_t top = taps_msb(m);
+                m &= ~(1u << top);
+                taps_cost(c, true, top, L, P.lam, s.e, s.unused);
+                ++n_a2a;
+            }
+            s.blk &= ~taps_blocked(P, Q, L, mv);
+            s.ats &= ~mv;
+            s.atd |= mv;
+        }
+        if (sl) taps_slice(L, s);
+        if (s.ats == 0 && s.atd == L.dst) break;
+        // InferAllGather / AllGatherFirstUndoneDim
+        uint32_t ug = s.ats & ~L.tgtsrc;
+        if (ug) {
+            bool pending = (L.dst & ~(s.ats | s.atd) & ~s.blk) != 0;
+            do {
+                const uint32_t top = taps_first_src(P, ug);
+                taps_gather(P, L, s, c, top);
+                ug &= ~(1u << top);
+                // without AllToAll the gathered axis may now slice into its target
+                pending = pending || (L.dst & (1u << top) & ~s.blk) != 0;
+            } while (ug && !pending && !taps_hopeless(c, lim, K));
+        } else if (s.ats) {
+            const uint32_t top = taps_first_src(P, s.ats);
+            s.blk &= ~taps_blocked(P, Q, L, 1u << top);
+            taps_gather(P, L, s, c, top);
+        }
+    }
+    taps_run r;
+    r.c = c;
+    r.n_a2a = n_a2a;
+    r.ok = ok;
+    r.stopped = stopped;
+    return r;
+}
+
+// "remove" (Table 2): gather every held axis not at its target, lowest
+// position first; the slices that follow are free.
+__host__ __device__ inline taps_run taps_remove(const taps_row &P, const taps_lv &L,
+                                               const taps_limit &lim, const taps_keys &K) {
+    taps_fac c;
+    taps_fac_zero(c);
+    taps_state s;
+    s.ats = L.src & ~L.home;
+    s.unused = P.full & ~P.pru;
+    s.e = P.e0;
+    uint32_t x = P.to_rank[s.ats];   // in producer order
+    bool stopped = false;
+    while (x) {
+        if (taps_hopeless(c, lim, K)) {
+            stopped = true;
+            break;
+        }
+        const uint32_t top = taps_rank_level(P, taps_ctz(x));
+        x &= x - 1u;
+        taps_gather(P, L, s, c, top);
+    }
+    taps_run r;
+    r.c = c;
+    r.n_a2a = 0;
+    r.ok = true;
+    r.stopped = stopped;
+    return r;
+}
+
+// tbytes * f / 256, exact (the result is an integer volume in nb < 2^64).
+__host__ __device__ inline uint64_t taps_scale(uint64_t tbytes, uint32_t f) {
+    return (((tbytes & 0xFFFFFFFFull) * f) >> 8) + (((tbytes >> 32) * f) << 24);
 }
 
 struct taps_entry_out {
@@ -499,35 +572,54 @@ struct taps_entry_out {
 // The cheapest of Algorithm 1, Algorithm 1 without AllToAll, and "remove"
 // (the naive sequence of Table 2 gathers a superset of what "remove"
 // gathers, in the same order, so it is never cheaper in either model and
-// never wins a tie); vol is the smallest volume among them.
+// never wins a tie); vol is the smallest volume among them.  The second and
+// third candidates stop as soon as they cannot change the record.
 __host__ __device__ inline taps_entry_out taps_edge_entry(const taps_row &P, const taps_col &Q,
                                                           uint64_t tbytes, const taps_keys &K,
                                                           double inv_n_bintra,
                                                           double inv_n_binter) {
     taps_lv L;
     taps_unify(P, Q, L);
-    const taps_run r0 = taps_alg1(P, Q, L, true);
-    const taps_run r1 = r0.n_a2a ? taps_alg1(P, Q, L, false) : r0;
-    const taps_fac c0 = r0.c, c1 = r1.c, c2 = taps_remove(P, L);
-    taps_fac best = c0;
-    uint32_t cand = 0;
-    if (taps_less(c1, best, K)) {
-        best = c1;
-        cand = 1;
+    taps_limit lim;
+    lim.on = false;
+    lim.key = 0;
+    lim.vol = 0;
+    const taps_run r0 = taps_alg1(P, Q, L, true, lim, K);
+    taps_fac best = r0.c;
+    uint32_t cand = 0, vmin = r0.c.vol;
+    lim.on = K.narrow;
+    lim.key = taps_key64(best, K);
+    lim.vol = vmin;
+    bool ok = r0.ok;
+    if (r0.n_a2a) {   // without AllToAll the sequence would be the same
+        const taps_run r1 = taps_alg1(P, Q, L, false, lim, K);
+        ok = ok && r1.ok;
+        if (!r1.stopped) {
+            if (taps_less(r1.c, best, K)) {
+                best = r1.c;
+                cand = 1;
+            }
+            vmin = r1.c.vol < vmin ? r1.c.vol : vmin;
+        }
     }
-    if (taps_less(c2, best, K)) {
-        best = c2;
-        cand = 2;
+    lim.key = taps_key64(best, K);
+    lim.vol = vmin;
+    const taps_run r2 = taps_remove(P, L, lim, K);
+    if (!r2.stopped) {
+        if (taps_less(r2.c, best, K)) {
+            best = r2.c;
+            cand = 2;
+        }
+        vmin = r2.c.vol < vmin ? r2.c.vol : vmin;
     }
-    uint32_t vmin = c0.vol < c1.vol ? c0.vol : c1.vol;
-    vmin = vmin < c2.vol ? vmin : c2.vol;
     taps_entry_out o;
     o.vol = taps_scale(tbytes, vmin);
     o.intra = taps_scale(tbytes, best.intra);
     o.inter = taps_scale(tbytes, best.inter);
     o.t = (double)o.intra * inv_n_bintra + (double)o.inter * inv_n_binter;
-    o.meta = cand | (best.n_coll << 2) | (best.n_inter << 7) | (best.sum_ct << 12);
-    o.ok = r0.ok && r1.ok;
+    o.meta = cand | ((best.counts & 0xFFu) << 2) | (((best.counts >> 8) & 0xFFu) << 7) |
+             ((best.counts >> 16) << 12);
+    o.ok = ok;
     return o;
 }
 
@@ -553,6 +645,33 @@ __host__ __device__ inline void taps_make_row(taps_row &P, const taps_desc &D, u
         used += w;
     }
     P.e0 = n - used;
+    // producer order: dimensions ascending, each from its top level down
+    P.order = 0;
+    uint32_t k = 0;
+#pragma unroll
+    for (uint32_t d = 0; d < TAPS_D_MAX_RANK; ++d)
+        for (uint32_t t = 0; t < P.pw[d]; ++t) P.order |= (P.phi[d] - 1u - t) << (4u * k++);
+    P.to_rank = nullptr;
+}
+
+// to_rank table of a row: tab[x] = level mask x permuted into producer order.
+// Entries x = first, first + step, ... < 256.
+__host__ __device__ inline void taps_fill_rank_table(const taps_row &P, uint8_t *tab, uint32_t first,
+                                                     uint32_t step) {
+    // nibble l: producer-order rank of level l (8 = not a producer level)
+    uint32_t rank_of = 0x88888888u;
+    const uint32_t used = taps_popc(P.pru);
+    for (uint32_t k = 0; k < used; ++k) {
+        const uint32_t l = taps_rank_level(P, k);
+        rank_of = (rank_of & ~(15u << (4u * l))) | (k << (4u * l));
+    }
+    for (uint32_t x = first; x < 256u; x += step) {
+        uint32_t y = 0;
+#pragma unroll
+        for (uint32_t l = 0; l < TAPS_D_MAX_LEVELS; ++l)
+            if ((x >> l) & 1u) y |= (1u << ((rank_of >> (4u * l)) & 15u)) & 0xFFu;
+        tab[x] = (uint8_t)y;
+    }
 }
 
 __host__ __device__ inline void taps_make_col(taps_col &Q, const taps_desc &D, uint32_t axes,

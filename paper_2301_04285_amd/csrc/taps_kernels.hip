@@ -176,20 +176,24 @@ __global__ __launch_bounds__(256) void k_tile_map(const uint64_t *__restrict__ t
 __global__ __launch_bounds__(TAPS_TILE_COLS * TAPS_TILES_PER_BLOCK) void k_edge_costs(
     const taps_edge_params *__restrict__ params, const uint32_t *__restrict__ tile_edge,
     uint64_t n_tiles, const taps_desc *__restrict__ desc, taps_launch lp, taps_table out) {
+    __shared__ uint8_t rank_tab[TAPS_TILES_PER_BLOCK][256];
     // everything up to the column index is uniform across the wavefront
     const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x / TAPS_TILE_COLS);
     const uint32_t lane = threadIdx.x % TAPS_TILE_COLS;
     const uint64_t tile = (uint64_t)blockIdx.x * TAPS_TILES_PER_BLOCK + wave;
-    if (tile >= n_tiles) return;
-    const uint32_t e = __builtin_amdgcn_readfirstlane(tile_edge[tile]);
+    const bool live = tile < n_tiles;
+    const uint32_t e = __builtin_amdgcn_readfirstlane(live ? tile_edge[tile] : 0u);
     const taps_edge_params E = params[e];
     const uint32_t row_tiles = (E.nd + TAPS_TILE_COLS - 1) / TAPS_TILE_COLS;
-    const uint32_t lt = (uint32_t)(tile - E.tile_begin);
+    const uint32_t lt = live ? (uint32_t)(tile - E.tile_begin) : 0u;
     const uint32_t i = __builtin_amdgcn_readfirstlane(lt / row_tiles);
-    const uint32_t j = (lt - i * row_tiles) * TAPS_TILE_COLS + lane;
-    if (j >= E.nd) return;
     taps_row P;
     taps_make_row(P, desc[E.src_base + i], E.paxes, E.rank, lp.n, lp.lam);
+    taps_fill_rank_table(P, rank_tab[wave], lane, TAPS_TILE_COLS);
+    __syncthreads();
+    P.to_rank = rank_tab[wave];
+    const uint32_t j = (lt - i * row_tiles) * TAPS_TILE_COLS + lane;
+    if (!live || j >= E.nd) return;
     taps_col Q;
     taps_make_col(Q, desc[E.dst_base + j], E.caxes, E.rank);
     taps_keys K;
