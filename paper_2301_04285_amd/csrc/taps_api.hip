@@ -37,6 +37,24 @@ taps_status hip_fail(hipError_t err, const char *what) {
 
 bool pow2(uint64_t v) { return v && !(v & (v - 1)); }
 
+// Strategies of an operator with p partitionable axes on 2^n devices before
+// the divisibility filter: sum_{i=1}^{min(p,n)} i! C(p,i) C(n-1,i-1); one
+// (nothing split) for n = 0.  Sizes the enumeration grid.
+uint64_t candidate_count(uint32_t p, uint32_t n) {
+    if (n == 0) return 1;
+    auto binom = [](uint64_t a, uint64_t b) {
+        uint64_t r = 1;
+        for (uint64_t x = 1; x <= b; ++x) r = r * (a - b + x) / x;
+        return b > a ? 0 : r;
+    };
+    uint64_t tot = 0, fact = 1;
+    for (uint32_t i = 1; i <= p && i <= n; ++i) {
+        fact *= i;
+        tot += fact * binom(p, i) * binom(n - 1, i - 1);
+    }
+    return tot;
+}
+
 uint32_t log2u(uint64_t v) {
     uint32_t k = 0;
     while ((1ull << k) < v) ++k;
@@ -257,41 +275,68 @@ taps_status taps_enumerate_strategies(const taps_graph *graph, const taps_cluste
         op_offsets[0] = 0;
         return TAPS_OK;
     }
+    // launch geometry: the operator's candidates before the divisibility
+    // filter (the closed-form count) cut into chunks of one wavefront
+    std::vector<uint32_t> chunk_op, chunk_first;
+    std::vector<uint32_t> first_chunk(n_ops + 1, 0);
+    for (uint32_t k = 0; k < n_ops; ++k) {
+        const uint64_t cand = candidate_count(__builtin_popcount(graph->ops[k].part_mask), lp.n);
+        first_chunk[k] = (uint32_t)chunk_op.size();
+        for (uint64_t f = 0; f < cand; f += TAPS_ENUM_CHUNK) {
+            chunk_op.push_back(k);
+            chunk_first.push_back((uint32_t)f);
+        }
+    }
+    first_chunk[n_ops] = (uint32_t)chunk_op.size();
+    const uint32_t n_chunks = (uint32_t)chunk_op.size();
     scratch sc(stream);
-    std::vector<chunk> ch{{graph->ops, sizeof(taps_op) * n_ops, 0}};
+    std::vector<chunk> ch{{graph->ops, sizeof(taps_op) * n_ops, 0},
+                          {chunk_op.data(), sizeof(uint32_t) * n_chunks, 0},
+                          {chunk_first.data(), sizeof(uint32_t) * n_chunks, 0}};
     void *dev = nullptr;
     if ((st = upload(ch, &dev, stream)) != TAPS_OK) return st;
     sc.adopt(dev);
     const taps_op *d_ops = at<taps_op>(dev, ch[0]);
     uint32_t *d_counts = nullptr;
-    if ((st = sc.alloc((void **)&d_counts, sizeof(uint32_t) * n_ops)) != TAPS_OK) return st;
-    hipError_t err = taps_launch_enumerate(d_ops, n_ops, lp.n, nullptr, d_counts, nullptr, stream);
+    if ((st = sc.alloc((void **)&d_counts, sizeof(uint32_t) * (n_chunks ? n_chunks : 1))) != TAPS_OK)
+        return st;
+    hipError_t err = taps_launch_enumerate(d_ops, lp.n, n_chunks, at<uint32_t>(dev, ch[1]),
+                                           at<uint32_t>(dev, ch[2]), nullptr, d_counts, nullptr,
+                                           stream);
     if (err != hipSuccess) return hip_fail(err, "enumerate (count)");
-    std::vector<uint32_t> counts(n_ops);
-    err = hipMemcpyAsync(counts.data(), d_counts, sizeof(uint32_t) * n_ops, hipMemcpyDeviceToHost,
-                         stream);
-    if (err == hipSuccess) err = hipStreamSynchronize(stream);
-    if (err != hipSuccess) return hip_fail(err, "reading strategy counts");
-    std::vector<uint64_t> offs(n_ops + 1, 0);
+    std::vector<uint32_t> counts(n_chunks);
+    if (n_chunks) {
+        err = hipMemcpyAsync(counts.data(), d_counts, sizeof(uint32_t) * n_chunks,
+                             hipMemcpyDeviceToHost, stream);
+        if (err == hipSuccess) err = hipStreamSynchronize(stream);
+        if (err != hipSuccess) return hip_fail(err, "reading strategy counts");
+    }
+    std::vector<uint64_t> offs(n_ops + 1, 0), base(n_chunks ? n_chunks : 1, 0);
     for (uint32_t k = 0; k < n_ops; ++k) {
-        if (counts[k] == 0)
+        uint64_t at_k = offs[k];
+        for (uint32_t c = first_chunk[k]; c < first_chunk[k + 1]; ++c) {
+            base[c] = at_k;
+            at_k += counts[c];
+        }
+        if (at_k == offs[k])
             return fail(TAPS_ERR_NO_STRATEGY,
                         "op %u has no strategy on %u devices (no partitionable axis whose length "
                         "the degrees divide)",
                         k, 1u << lp.n);
-        offs[k + 1] = offs[k] + counts[k];
+        offs[k + 1] = at_k;
     }
     std::memcpy(op_offsets, offs.data(), sizeof(uint64_t) * (n_ops + 1));
     if (!strategies) return TAPS_OK;
     if (offs[n_ops] > capacity)
         return fail(TAPS_ERR_CAPACITY, "%llu strategies, capacity %llu",
                     (unsigned long long)offs[n_ops], (unsigned long long)capacity);
-    std::vector<chunk> ch2{{offs.data(), sizeof(uint64_t) * (n_ops + 1), 0}};
+    std::vector<chunk> ch2{{base.data(), sizeof(uint64_t) * n_chunks, 0}};
     void *dev2 = nullptr;
     if ((st = upload(ch2, &dev2, stream)) != TAPS_OK) return st;
     sc.adopt(dev2);
-    err = taps_launch_enumerate(d_ops, n_ops, lp.n, at<uint64_t>(dev2, ch2[0]), nullptr, strategies,
-                                stream);
+    err = taps_launch_enumerate(d_ops, lp.n, n_chunks, at<uint32_t>(dev, ch[1]),
+                                at<uint32_t>(dev, ch[2]), at<uint64_t>(dev2, ch2[0]), nullptr,
+                                strategies, stream);
     if (err != hipSuccess) return hip_fail(err, "enumerate (emit)");
     return TAPS_OK;
 }

@@ -71,44 +71,57 @@ __host__ __device__ inline uint32_t taps_levels(uint32_t lo, uint32_t w) {
 // z = 0 this is the paper's count sum_i i! C(p,i) C(n-1,i-1).
 // ---------------------------------------------------------------------------
 
-__host__ __device__ inline uint64_t taps_binom(uint32_t a, uint32_t b) {
+__host__ __device__ constexpr uint32_t taps_binom(uint32_t a, uint32_t b) {
     if (b > a) return 0;
-    uint64_t r = 1;
+    uint32_t r = 1;
     for (uint32_t x = 1; x <= b; ++x) r = r * (a - b + x) / x;
     return r;
 }
 
-__host__ __device__ inline uint64_t taps_fact(uint32_t a) {
-    uint64_t r = 1;
+__host__ __device__ constexpr uint32_t taps_fact(uint32_t a) {
+    uint32_t r = 1;
     for (uint32_t x = 2; x <= a; ++x) r *= x;
     return r;
 }
 
-__host__ __device__ inline uint64_t taps_completions(uint32_t k, uint32_t s, uint32_t z) {
+// w(k, s, z); only states with z + s <= 8 occur (each split axis takes at
+// least one level), where every term has z + j <= 8 and the sum stays below
+// 2^32; other entries are never read.
+__host__ __device__ constexpr uint32_t taps_completions(uint32_t k, uint32_t s, uint32_t z) {
+    if (z + s > TAPS_D_MAX_LEVELS) return 0;
     if (s == 0) return taps_fact(z);
-    uint64_t tot = 0;
-    uint32_t jmax = k < s ? k : s;
+    uint32_t tot = 0;
+    const uint32_t jmax = k < s ? k : s;
     for (uint32_t j = 1; j <= jmax; ++j)
         tot += taps_binom(k, j) * taps_binom(s - 1, j - 1) * taps_fact(z + j);
     return tot;
 }
 
-// Decodes candidate r (0 <= r < taps_completions(p, n, 0)) into per-axis
-// exponents and device-map positions.  part: partitionable-axis mask.
-// Returns false if r is out of range.
-template <class W>
-__host__ __device__ inline bool taps_unrank(uint32_t n_axes, uint32_t part, uint32_t n, uint64_t r,
-                                            const W &w, uint32_t *expo, int32_t *pos) {
+struct taps_completion_table {
+    uint32_t v[9 * 9 * 9];   // index (k * 9 + s) * 9 + z
+};
+
+__host__ __device__ constexpr taps_completion_table taps_make_completions() {
+    taps_completion_table t{};
+    for (uint32_t x = 0; x < 9u * 9u * 9u; ++x) t.v[x] = taps_completions(x / 81u, (x / 9u) % 9u, x % 9u);
+    return t;
+}
+
+// Decodes candidate r (0 <= r < w(p, n, 0)) into per-axis exponents and
+// device-map positions.  part: partitionable-axis mask; W: the completion
+// table.  Returns false if r is out of range.
+__host__ __device__ inline bool taps_unrank(uint32_t n_axes, uint32_t part, uint32_t n, uint32_t r,
+                                            const uint32_t *W, uint32_t *expo, int32_t *pos) {
     uint32_t s = n, z = 0;
     for (uint32_t a = 0; a < n_axes; ++a) {
         expo[a] = 0;
         pos[a] = -1;
         if (!((part >> a) & 1u)) continue;
-        uint32_t k = taps_popc(part >> (a + 1));
+        const uint32_t k = taps_popc(part >> (a + 1));
         bool placed = false;
         for (uint32_t e = 0; e <= s; ++e) {
-            uint32_t z2 = z + (e > 0 ? 1u : 0u);
-            uint64_t c = w(k, s - e, z2);
+            const uint32_t z2 = z + (e > 0 ? 1u : 0u);
+            const uint32_t c = W[(k * 9u + (s - e)) * 9u + z2];
             if (r < c) {
                 expo[a] = e;
                 s -= e;
@@ -123,17 +136,17 @@ __host__ __device__ inline bool taps_unrank(uint32_t n_axes, uint32_t part, uint
     if (s != 0) return false;
     // r is now the rank of the position tuple among the z! orderings, in
     // descending order; decode the (z! - 1 - r)-th ascending permutation.
-    uint64_t q = taps_fact(z) - 1 - r;
+    uint32_t q = taps_fact(z) - 1u - r;
     uint32_t free_pos = taps_low_mask(z);
     uint32_t t = 0;
     for (uint32_t a = 0; a < n_axes; ++a) {
         if (expo[a] == 0) continue;
-        uint64_t f = taps_fact(z - 1 - t);
-        uint32_t idx = (uint32_t)(q / f);
-        q -= (uint64_t)idx * f;
+        const uint32_t f = taps_fact(z - 1u - t);
+        const uint32_t idx = q / f;
+        q -= idx * f;
         uint32_t m = free_pos;
-        for (uint32_t x = 0; x < idx; ++x) m &= m - 1;   // drop the idx lowest free positions
-        uint32_t p = taps_ctz(m);
+        for (uint32_t x = 0; x < idx; ++x) m &= m - 1u;   // drop the idx lowest free positions
+        const uint32_t p = taps_ctz(m);
         free_pos &= ~(1u << p);
         pos[a] = (int32_t)p;
         ++t;

@@ -37,8 +37,11 @@ struct taps_edge_params {
 #define TAPS_TILE_COLS 64
 #define TAPS_TILES_PER_BLOCK 4
 
-hipError_t taps_launch_enumerate(const taps_op *ops, uint32_t n_ops, uint32_t n,
-                                 const uint64_t *offsets, uint32_t *counts, taps_strategy *out,
+#define TAPS_ENUM_CHUNK 64   // candidates per enumeration wavefront
+
+hipError_t taps_launch_enumerate(const taps_op *ops, uint32_t n, uint32_t n_chunks,
+                                 const uint32_t *chunk_op, const uint32_t *chunk_first,
+                                 const uint64_t *base, uint32_t *counts, taps_strategy *out,
                                  hipStream_t stream);
 hipError_t taps_launch_describe(const taps_strategy *s, uint64_t total, taps_desc *desc,
                                 hipStream_t stream);

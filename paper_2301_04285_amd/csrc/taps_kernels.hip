@@ -1,7 +1,7 @@
 // taps_kernels.hip -- gfx950 kernels of the TAPS cost tables.
 //
-//   k_enumerate   one wavefront per operator: GenerateStrategySet in
-//                 canonical order, 64 candidates per step, ballot compaction
+//   k_enumerate   one wavefront per 64 candidates of one operator:
+//                 GenerateStrategySet in canonical order, ballot compaction
 //   k_describe    one thread per strategy: level runs, owners and cuts
 //   k_node_costs  one thread per strategy: the intra-op AllReduces
 //   k_edge_setup  one thread per edge: per-edge constants
@@ -16,54 +16,50 @@ namespace {
 
 constexpr uint32_t kWave = 64;
 
-// Completion counts w(k, s, z) for k, s, z in 0..8 (see taps_completions).
-struct lds_weights {
-    const uint64_t *tab;
-    __device__ uint64_t operator()(uint32_t k, uint32_t s, uint32_t z) const {
-        return tab[(k * 9u + s) * 9u + z];
-    }
-};
+// Completion counts w(k, s, z) for k, s, z in 0..8 (see taps_completions),
+// evaluated by the compiler.
+__constant__ taps_completion_table kCompletions = taps_make_completions();
 
 __device__ inline uint32_t lanes_below(uint64_t mask) {
     return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
                                      __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
 }
 
+// One wavefront per chunk of 64 consecutive candidates of one operator.
+// chunk_op[c] / chunk_first[c]: operator and first candidate of chunk c.
+// Count pass (out == nullptr): counts[c] = valid candidates of the chunk.
+// Emit pass: valid candidates go to out[base[c] + rank among the chunk's].
 __global__ __launch_bounds__(kWave) void k_enumerate(const taps_op *__restrict__ ops, uint32_t n,
-                                                     const uint64_t *__restrict__ offsets,
+                                                     const uint32_t *__restrict__ chunk_op,
+                                                     const uint32_t *__restrict__ chunk_first,
+                                                     const uint64_t *__restrict__ base,
                                                      uint32_t *__restrict__ counts,
                                                      taps_strategy *__restrict__ out) {
-    __shared__ uint64_t wtab[9 * 9 * 9];
+    __shared__ uint32_t W[9 * 9 * 9];
     const uint32_t lane = threadIdx.x;
-    for (uint32_t x = lane; x < 9u * 9u * 9u; x += kWave)
-        wtab[x] = taps_completions(x / 81u, (x / 9u) % 9u, x % 9u);
+    for (uint32_t x = lane; x < 9u * 9u * 9u; x += kWave) W[x] = kCompletions.v[x];
     __syncthreads();
-    const taps_op &op = ops[blockIdx.x];
+    const uint32_t c = blockIdx.x;
+    const taps_op &op = ops[chunk_op[c]];
     const uint32_t n_axes = op.n_axes, part = op.part_mask;
-    const lds_weights w{wtab};
-    const uint64_t total = w(taps_popc(part), n, 0);
-    uint64_t base = offsets ? offsets[blockIdx.x] : 0;
-    uint32_t count = 0;
-    for (uint64_t r0 = 0; r0 < total; r0 += kWave) {
-        const uint64_t r = r0 + lane;
-        uint32_t expo[TAPS_D_MAX_AXES];
-        int32_t pos[TAPS_D_MAX_AXES];
-        bool valid = r < total && taps_unrank(n_axes, part, n, r, w, expo, pos);
-        if (valid)
-            for (uint32_t a = 0; a < n_axes; ++a)
-                if (op.axis_len[a] & (((int64_t)1 << expo[a]) - 1)) valid = false;
-        const uint64_t m = __ballot(valid);
-        if (out && valid) {
-            taps_strategy s;
-            for (uint32_t a = 0; a < TAPS_MAX_AXES; ++a) {
-                s.log2_deg[a] = a < n_axes ? (uint8_t)expo[a] : 0;
-                s.pos[a] = a < n_axes ? (int8_t)pos[a] : (int8_t)-1;
-            }
-            out[base + count + lanes_below(m)] = s;
+    const uint32_t total = W[(taps_popc(part) * 9u + n) * 9u];
+    const uint32_t r = chunk_first[c] + lane;
+    uint32_t expo[TAPS_D_MAX_AXES];
+    int32_t pos[TAPS_D_MAX_AXES];
+    bool valid = r < total && taps_unrank(n_axes, part, n, r, W, expo, pos);
+    if (valid)
+        for (uint32_t a = 0; a < n_axes; ++a)
+            if (op.axis_len[a] & (((int64_t)1 << expo[a]) - 1)) valid = false;
+    const uint64_t m = __ballot(valid);
+    if (counts && lane == 0) counts[c] = (uint32_t)__builtin_popcountll(m);
+    if (out && valid) {
+        taps_strategy st;
+        for (uint32_t a = 0; a < TAPS_MAX_AXES; ++a) {
+            st.log2_deg[a] = a < n_axes ? (uint8_t)expo[a] : 0;
+            st.pos[a] = a < n_axes ? (int8_t)pos[a] : (int8_t)-1;
         }
-        count += (uint32_t)__builtin_popcountll(m);
+        out[base[c] + lanes_below(m)] = st;
     }
-    if (counts && lane == 0) counts[blockIdx.x] = count;
 }
 
 __global__ __launch_bounds__(256) void k_describe(const taps_strategy *__restrict__ s,
@@ -213,12 +209,13 @@ inline uint32_t blocks_for(uint64_t n, uint32_t per) { return (uint32_t)((n + pe
 
 }  // namespace
 
-hipError_t taps_launch_enumerate(const taps_op *ops, uint32_t n_ops, uint32_t n,
-                                 const uint64_t *offsets, uint32_t *counts, taps_strategy *out,
+hipError_t taps_launch_enumerate(const taps_op *ops, uint32_t n, uint32_t n_chunks,
+                                 const uint32_t *chunk_op, const uint32_t *chunk_first,
+                                 const uint64_t *base, uint32_t *counts, taps_strategy *out,
                                  hipStream_t stream) {
-    if (n_ops == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_enumerate, dim3(n_ops), dim3(kWave), 0, stream, ops, n, offsets, counts,
-                       out);
+    if (n_chunks == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_enumerate, dim3(n_chunks), dim3(kWave), 0, stream, ops, n, chunk_op,
+                       chunk_first, base, counts, out);
     return hipGetLastError();
 }
 
