@@ -452,6 +452,48 @@ __host__ __device__ inline void taps_gather(const taps_row &P, const taps_lv &L,
     s.e += taps_popc(lv);
 }
 
+// Gathers, back to back in producer order, every axis whose top is in x (x
+// within producer levels), with no other event between them.  Within one
+// dimension the axes go from the top level down, so their volumes telescope:
+// the axes wholly above the node boundary (levels >= lam) cost
+// (2^W_A - 1) S together and share one inter-node group count (they do not
+// change which levels below lam are free); at most one axis straddles the
+// boundary; the axes below it are intra-node and cost (2^W_B - 1) S' together.
+__host__ __device__ inline void taps_gather_run(const taps_row &P, const taps_lv &L, taps_state &s,
+                                                taps_fac &c, uint32_t x) {
+    const uint32_t lam = P.lam;
+    const uint32_t low = taps_below(lam);
+#pragma unroll
+    for (uint32_t d = 0; d < TAPS_D_MAX_RANK; ++d) {
+        if (d >= P.rank) break;
+        const uint32_t xd = x & P.pr[d];
+        const uint32_t G = taps_fill(L, xd);
+        const uint32_t hi = G & ~low, lo = G & low;
+        // the axis through levels lam-1 and lam (no top at lam-1)
+        const bool st = lam >= 1u && ((G >> lam) & 1u) && ((G >> (lam - 1u)) & 1u) &&
+                        !((L.tp >> (lam - 1u)) & 1u);
+        const uint32_t t_s = taps_ctz((L.tp & hi) | 0x100u);
+        const uint32_t lo_s = taps_msb(((L.tp & low) << 1) | 1u);
+        const uint32_t ws_hi = st ? t_s + 1u - lam : 0u, ws_lo = st ? lam - lo_s : 0u;
+        const uint32_t nS = st ? 1u : 0u;
+        const uint32_t nA = taps_popc(L.tp & hi) - nS, nB = taps_popc(L.tp & lo);
+        const uint32_t WA = taps_popc(hi) - ws_hi, WB = taps_popc(lo) - ws_lo, WS = ws_hi + ws_lo;
+        const uint32_t sh = s.e + 8u;
+        const uint32_t VA = ((1u << WA) - 1u) << sh;
+        const uint32_t VS = ((1u << WS) - 1u) << (sh + WA);
+        const uint32_t VB = ((1u << WB) - 1u) << (sh + WA + WS);
+        const uint32_t lctA = lam - taps_popc(s.unused & low);
+        const uint32_t lctS = st ? lo_s - taps_popc(s.unused & taps_below(lo_s)) : 0u;
+        c.vol += VA + VS + VB;
+        c.intra += VB;
+        c.inter += (VA << lctA) + (VS << lctS);
+        c.counts += (nA + nS + nB) + ((nA + nS) << 8) + (((nA << lctA) + (nS << lctS)) << 16);
+        s.e += taps_popc(G);
+        s.unused |= G;
+        s.ats &= ~xd;
+    }
+}
+
 // Every free target position whose axis no dimension uses is sliced.
 __host__ __device__ inline uint32_t taps_slice(const taps_lv &L, taps_state &s) {
     const uint32_t sl = L.dst & ~(s.ats | s.atd) & ~s.blk;
@@ -464,21 +506,20 @@ __host__ __device__ inline uint32_t taps_slice(const taps_lv &L, taps_state &s) 
     return sl;
 }
 
-// Algorithm 1 (use_a2a) or the same without AllToAll ("rearrange").
+// Algorithm 1 ("replace" in Table 2).
 //
 // Equivalent schedule of the printed loop:
 //   * one pass of the inner loop is InferSlice, then InferAll2All until
 //     nothing moves; a slice never frees a position, so a second pass can
 //     only slice (targets the AllToAlls freed) and a third finds nothing;
 //   * an AllGather of an axis whose producer position no consumer axis
-//     targets frees no position, so the next inner loop can only slice that
-//     same axis into its target (possible without AllToAll: with AllToAll a
-//     mover with a free target has already moved); such gathers therefore
-//     run back to back, lowest position first, until one leaves a slice
-//     pending (or one was pending from the last AllToAlls).
+//     targets frees no position anyone wants, and the axis itself cannot be
+//     sliced (a held axis with a free target has already moved), so the
+//     next inner loop does nothing: such gathers run back to back, lowest
+//     position first, unless the last AllToAlls left a slice pending, in
+//     which case only the first runs before it.
 __host__ __device__ inline taps_run taps_alg1(const taps_row &P, const taps_col &Q,
-                                              const taps_lv &L, bool use_a2a,
-                                              const taps_limit &lim, const taps_keys &K) {
+                                              const taps_lv &L) {
     taps_fac c;
     taps_fac_zero(c);
     taps_state s;
@@ -488,19 +529,14 @@ __host__ __device__ inline taps_run taps_alg1(const taps_row &P, const taps_col 
     s.unused = P.full & ~P.pru;
     s.e = P.e0;
     uint32_t n_a2a = 0;
-    bool ok = true, stopped = false;
+    bool ok = true;
     for (uint32_t guard = 0;; ++guard) {
         if (guard > 4 * TAPS_D_MAX_LEVELS) {
             ok = false;
             break;
         }
-        if (taps_hopeless(c, lim, K)) {
-            stopped = true;
-            break;
-        }
-        // inner loop
         const uint32_t sl = taps_slice(L, s);
-        while (use_a2a) {
+        for (;;) {
             const uint32_t mv = L.dst & s.ats & ~s.blk;
             if (!mv) break;
             uint32_t m = mv;
@@ -519,14 +555,13 @@ __host__ __device__ inline taps_run taps_alg1(const taps_row &P, const taps_col 
         // InferAllGather / AllGatherFirstUndoneDim
         uint32_t ug = s.ats & ~L.tgtsrc;
         if (ug) {
-            bool pending = (L.dst & ~(s.ats | s.atd) & ~s.blk) != 0;
-            do {
-                const uint32_t top = taps_first_src(P, ug);
+            if (L.dst & ~(s.ats | s.atd) & ~s.blk) ug = 1u << taps_first_src(P, ug);
+            uint32_t x = P.to_rank[ug];
+            while (x) {
+                const uint32_t top = taps_rank_level(P, taps_ctz(x));
+                x &= x - 1u;
                 taps_gather(P, L, s, c, top);
-                ug &= ~(1u << top);
-                // without AllToAll the gathered axis may now slice into its target
-                pending = pending || (L.dst & (1u << top) & ~s.blk) != 0;
-            } while (ug && !pending && !taps_hopeless(c, lim, K));
+            }
         } else if (s.ats) {
             const uint32_t top = taps_first_src(P, s.ats);
             s.blk &= ~taps_blocked(P, Q, L, 1u << top);
@@ -537,22 +572,39 @@ __host__ __device__ inline taps_run taps_alg1(const taps_row &P, const taps_col 
     r.c = c;
     r.n_a2a = n_a2a;
     r.ok = ok;
-    r.stopped = stopped;
+    r.stopped = false;
     return r;
 }
 
-// "remove" (Table 2): gather every held axis not at its target, lowest
-// position first; the slices that follow are free.
-__host__ __device__ inline taps_run taps_remove(const taps_row &P, const taps_lv &L,
-                                               const taps_limit &lim, const taps_keys &K) {
+// Algorithm 1 without AllToAll ("rearrange" in Table 2).  Without AllToAll
+// the printed loop reduces to:
+//   1. InferSlice once (a second pass finds nothing: no AllToAll frees a
+//      position);
+//   2. every held axis whose position no consumer axis targets is gathered,
+//      lowest position first; one whose own target is free is sliced back
+//      right away (the slice undoes the gather's change of shard and free
+//      levels), the others stay whole;
+//   3. the remaining held axes (all at targeted positions) are gathered,
+//      lowest position first; after each, the axis itself is sliced back if
+//      its target is free, and the axis targeting the freed position is
+//      sliced if no dimension uses it.
+__host__ __device__ inline taps_run taps_rearrange(const taps_row &P, const taps_col &Q,
+                                                   const taps_lv &L, const taps_limit &lim,
+                                                   const taps_keys &K) {
     taps_fac c;
     taps_fac_zero(c);
     taps_state s;
     s.ats = L.src & ~L.home;
+    s.atd = L.home;
+    s.blk = taps_blocked(P, Q, L, s.ats);
     s.unused = P.full & ~P.pru;
     s.e = P.e0;
-    uint32_t x = P.to_rank[s.ats];   // in producer order
     bool stopped = false;
+    taps_slice(L, s);
+    // 2. untargeted positions
+    const uint32_t ug = s.ats & ~L.tgtsrc;
+    const uint32_t bounce = ug & L.dst & ~s.blk;
+    uint32_t x = P.to_rank[ug];
     while (x) {
         if (taps_hopeless(c, lim, K)) {
             stopped = true;
@@ -560,7 +612,42 @@ __host__ __device__ inline taps_run taps_remove(const taps_row &P, const taps_lv
         }
         const uint32_t top = taps_rank_level(P, taps_ctz(x));
         x &= x - 1u;
-        taps_gather(P, L, s, c, top);
+        const uint32_t b = 1u << top;
+        taps_cost(c, false, top, L, P.lam, s.e, s.unused);
+        s.ats &= ~b;
+        if (bounce & b) {
+            s.atd |= b;
+        } else {
+            const uint32_t lv = taps_fill(L, b);
+            s.unused |= lv;
+            s.e += taps_popc(lv);
+        }
+    }
+    // 3. targeted positions
+    x = stopped ? 0u : P.to_rank[s.ats];
+    while (x) {
+        if (taps_hopeless(c, lim, K)) {
+            stopped = true;
+            break;
+        }
+        const uint32_t top = taps_rank_level(P, taps_ctz(x));
+        x &= x - 1u;
+        const uint32_t b = 1u << top;
+        taps_cost(c, false, top, L, P.lam, s.e, s.unused);
+        const uint32_t freed_for = taps_blocked(P, Q, L, b);   // the axis targeting that position
+        s.ats &= ~b;
+        s.blk &= ~freed_for;
+        uint32_t lv = taps_fill(L, b);
+        s.unused |= lv;
+        s.e += taps_popc(lv);
+        uint32_t sl = L.dst & b & ~s.blk;                  // back into its own target
+        sl |= freed_for & ~(s.ats | s.atd);                // into the freed position
+        if (sl) {
+            lv = taps_fill(L, sl);
+            s.atd |= sl;
+            s.unused &= ~lv;
+            s.e -= taps_popc(lv);
+        }
     }
     taps_run r;
     r.c = c;
@@ -568,6 +655,21 @@ __host__ __device__ inline taps_run taps_remove(const taps_row &P, const taps_lv
     r.ok = true;
     r.stopped = stopped;
     return r;
+}
+
+// "remove" (Table 2): gather every held axis not at its target, lowest
+// position first; the slices that follow are free.  One uninterrupted run.
+__host__ __device__ inline taps_fac taps_remove(const taps_row &P, const taps_lv &L) {
+    taps_fac c;
+    taps_fac_zero(c);
+    taps_state s;
+    s.ats = L.src & ~L.home;
+    s.atd = 0;
+    s.blk = 0;
+    s.unused = P.full & ~P.pru;
+    s.e = P.e0;
+    taps_gather_run(P, L, s, c, s.ats);
+    return c;
 }
 
 // tbytes * f / 256, exact (the result is an integer volume in nb < 2^64).
@@ -593,19 +695,16 @@ __host__ __device__ inline taps_entry_out taps_edge_entry(const taps_row &P, con
                                                           double inv_n_binter) {
     taps_lv L;
     taps_unify(P, Q, L);
-    taps_limit lim;
-    lim.on = false;
-    lim.key = 0;
-    lim.vol = 0;
-    const taps_run r0 = taps_alg1(P, Q, L, true, lim, K);
+    const taps_run r0 = taps_alg1(P, Q, L);
     taps_fac best = r0.c;
     uint32_t cand = 0, vmin = r0.c.vol;
+    taps_limit lim;
     lim.on = K.narrow;
     lim.key = taps_key64(best, K);
     lim.vol = vmin;
     bool ok = r0.ok;
     if (r0.n_a2a) {   // without AllToAll the sequence would be the same
-        const taps_run r1 = taps_alg1(P, Q, L, false, lim, K);
+        const taps_run r1 = taps_rearrange(P, Q, L, lim, K);
         ok = ok && r1.ok;
         if (!r1.stopped) {
             if (taps_less(r1.c, best, K)) {
@@ -615,16 +714,12 @@ __host__ __device__ inline taps_entry_out taps_edge_entry(const taps_row &P, con
             vmin = r1.c.vol < vmin ? r1.c.vol : vmin;
         }
     }
-    lim.key = taps_key64(best, K);
-    lim.vol = vmin;
-    const taps_run r2 = taps_remove(P, L, lim, K);
-    if (!r2.stopped) {
-        if (taps_less(r2.c, best, K)) {
-            best = r2.c;
-            cand = 2;
-        }
-        vmin = r2.c.vol < vmin ? r2.c.vol : vmin;
+    const taps_fac c2 = taps_remove(P, L);
+    if (taps_less(c2, best, K)) {
+        best = c2;
+        cand = 2;
     }
+    vmin = c2.vol < vmin ? c2.vol : vmin;
     taps_entry_out o;
     o.vol = taps_scale(tbytes, vmin);
     o.intra = taps_scale(tbytes, best.intra);
