@@ -385,13 +385,13 @@ taps_status taps_edge_costs(const taps_graph *graph, const taps_cluster *cluster
     if (st != TAPS_OK) return st;
     if (!edge_offsets) return fail(TAPS_ERR_ARG, "edge_offsets is NULL");
     const uint32_t n_ops = graph->n_ops, n_edges = graph->n_edges;
-    std::vector<uint64_t> eoff(n_edges + 1, 0), tiles(n_edges + 1, 0);
+    std::vector<uint64_t> eoff(n_edges + 1, 0), rows(n_edges + 1, 0);
     for (uint32_t e = 0; e < n_edges; ++e) {
         const taps_edge &E = graph->edges[e];
         const uint64_t ns = op_offsets[E.src_op + 1] - op_offsets[E.src_op];
         const uint64_t nd = op_offsets[E.dst_op + 1] - op_offsets[E.dst_op];
         eoff[e + 1] = eoff[e] + ns * nd;
-        tiles[e + 1] = tiles[e] + ns * ((nd + TAPS_TILE_COLS - 1) / TAPS_TILE_COLS);
+        rows[e + 1] = rows[e] + ns;
     }
     const bool none = !out.t && !out.vol && !out.intra && !out.inter && !out.meta;
     const bool all = out.t && out.vol && out.intra && out.inter && out.meta;
@@ -400,39 +400,36 @@ taps_status taps_edge_costs(const taps_graph *graph, const taps_cluster *cluster
         return fail(TAPS_ERR_CAPACITY, "%llu entries, capacity %llu",
                     (unsigned long long)eoff[n_edges], (unsigned long long)capacity);
     if (all && eoff[n_edges] > 0 && !strategies) return fail(TAPS_ERR_ARG, "strategies is NULL");
-    for (uint32_t e = 0; e < n_edges; ++e)
-        if (tiles[e + 1] - tiles[e] > 0xFFFFFFFFull)
-            return fail(TAPS_ERR_ARG, "edge %u has more than 2^32 tiles", e);
-    if (tiles[n_edges] / TAPS_TILES_PER_BLOCK >= 0x7FFFFFFFull)
-        return fail(TAPS_ERR_ARG, "more than 2^31 workgroups of %u tiles", TAPS_TILES_PER_BLOCK);
+    if (rows[n_edges] >= 0x7FFFFFFFull)
+        return fail(TAPS_ERR_ARG, "more than 2^31 table rows");
     std::memcpy(edge_offsets, eoff.data(), sizeof(uint64_t) * (n_edges + 1));
     if (none || eoff[n_edges] == 0) return TAPS_OK;
     hipStream_t stream = (hipStream_t)stream_;
     scratch sc(stream);
     const uint64_t total = op_offsets[n_ops];
-    const uint64_t n_tiles = tiles[n_edges];
+    const uint64_t n_rows = rows[n_edges];
     std::vector<chunk> ch{{graph->ops, sizeof(taps_op) * n_ops, 0},
                           {graph->edges, sizeof(taps_edge) * n_edges, 0},
                           {op_offsets, sizeof(uint64_t) * (n_ops + 1), 0},
                           {eoff.data(), sizeof(uint64_t) * (n_edges + 1), 0},
-                          {tiles.data(), sizeof(uint64_t) * (n_edges + 1), 0}};
+                          {rows.data(), sizeof(uint64_t) * (n_edges + 1), 0}};
     void *dev = nullptr;
     if ((st = upload(ch, &dev, stream)) != TAPS_OK) return st;
     sc.adopt(dev);
     taps_desc *d_desc = nullptr;
     taps_edge_params *d_params = nullptr;
-    uint32_t *d_tile_edge = nullptr;
+    taps_row_ref *d_rows = nullptr;
     if ((st = sc.alloc((void **)&d_desc, sizeof(taps_desc) * total)) != TAPS_OK) return st;
     if ((st = sc.alloc((void **)&d_params, sizeof(taps_edge_params) * n_edges)) != TAPS_OK) return st;
-    if ((st = sc.alloc((void **)&d_tile_edge, sizeof(uint32_t) * n_tiles)) != TAPS_OK) return st;
+    if ((st = sc.alloc((void **)&d_rows, sizeof(taps_row_ref) * n_rows)) != TAPS_OK) return st;
     hipError_t err = taps_launch_describe(strategies, total, d_desc, stream);
     if (err == hipSuccess)
         err = taps_launch_edge_setup(at<taps_op>(dev, ch[0]), at<taps_edge>(dev, ch[1]), n_edges,
                                      at<uint64_t>(dev, ch[2]), at<uint64_t>(dev, ch[3]),
-                                     at<uint64_t>(dev, ch[4]), d_params, n_tiles, d_tile_edge,
+                                     at<uint64_t>(dev, ch[4]), lp, d_params, n_rows, d_rows,
                                      stream);
     if (err == hipSuccess)
-        err = taps_launch_edge_costs(d_params, d_tile_edge, n_tiles, d_desc, lp, out, stream);
+        err = taps_launch_edge_costs(d_params, d_rows, n_rows, d_desc, lp, out, stream);
     if (err != hipSuccess) return hip_fail(err, "edge costs");
     return TAPS_OK;
 }

@@ -260,6 +260,7 @@ struct taps_row {
     uint32_t pcuts;                 // cut mask of the producer strategy
     uint32_t pru;                   // levels the producer map uses
     uint32_t e0;                    // n - |pru|
+    uint32_t dstr;                  // dimension whose run holds levels lam - 1 and lam (8: none)
     // Producer positions in order (dimension ascending, then bit ascending,
     // i.e. level descending): rank r holds level nibble r of `order`;
     // to_rank[x] is the level mask x with level l moved to bit rank(l).
@@ -280,6 +281,8 @@ struct taps_lv {
     uint32_t src, dst;      // axes the producer / consumer maps use
     uint32_t home;          // axes at the same position in both maps
     uint32_t tgtsrc;        // producer positions the consumer map also uses
+    uint32_t st;            // top of the axis holding levels lam - 1 and lam (0 if none)
+    uint32_t lo_s;          // its lowest level
     int32_t dl[TAPS_D_MAX_RANK];
 };
 
@@ -345,6 +348,11 @@ __host__ __device__ inline void taps_unify(const taps_row &P, const taps_col &Q,
     L.dst = L.tp & cru;
     L.home = L.tp & home;
     L.tgtsrc = L.tp & tgt;
+    const uint32_t lam = P.lam;
+    const uint32_t low = taps_below(lam);
+    L.lo_s = taps_msb(((L.tp & low) << 1) | 1u);
+    const bool st = lam >= 1u && lam < P.n && !((L.tp >> (lam - 1u)) & 1u);
+    L.st = st ? 1u << taps_ctz((L.tp & ~low) | 0x100u) : 0u;
 }
 
 // Consumer tops whose target position an axis in ats (producer tops) holds.
@@ -369,27 +377,62 @@ __host__ __device__ inline uint32_t taps_first_src(const taps_row &P, uint32_t x
     return taps_rank_level(P, taps_ctz(P.to_rank[x]));
 }
 
-// An AllGather (Eq. 9) or AllToAll (Eq. 10, Eq. 14) of the axis with top
-// level `top`, shard tbytes * 2^e, with the inter-node group count of
-// Algorithm 3: groups holding the same data inside a node (replicas along
-// levels no dimension uses) share one inter-node transfer.
-__host__ __device__ inline void taps_cost(taps_fac &c, bool a2a, uint32_t top, const taps_lv &L,
+// An AllGather (Eq. 9) of the axis with top level `top`, shard tbytes * 2^e,
+// with the inter-node group count of Algorithm 3: groups holding the same
+// data inside a node (replicas along levels no dimension uses) share one
+// inter-node transfer.
+__host__ __device__ inline void taps_cost(taps_fac &c, uint32_t top, const taps_lv &L,
                                           uint32_t lam, uint32_t e, uint32_t unused) {
     // lowest level of the axis: one above the next lower top (0 if none)
     const uint32_t lo = taps_msb(((L.tp & taps_below(top)) << 1) | 1u);
     const uint32_t w = top + 1u - lo;
-    const uint32_t sh = e + 8u;
-    const uint32_t V = a2a ? (1u << sh) - (1u << (sh - w)) : ((1u << w) - 1u) << sh;
+    const uint32_t V = ((1u << w) - 1u) << (e + 8u);
     const bool in_node = top < lam;   // the whole group inside one node
     const uint32_t m = lo < lam ? lo : lam;
     const uint32_t lct = m - taps_popc(unused & taps_below(m));
-    const uint32_t kap = lam > lo ? lam - lo : 0u;   // log2 of group members per node
-    const uint32_t link = a2a ? ((1u << w) - (1u << kap)) << (kap + sh - w) : V;
     c.vol += V;
     c.intra += in_node ? V : 0u;
-    c.inter += in_node ? 0u : link << lct;
+    c.inter += in_node ? 0u : V << lct;
     // collectives (bits 0-7), inter-node ones (8-15), sum of their ct (16-31)
     c.counts += in_node ? 1u : 0x101u + ((1u << lct) << 16);
+}
+
+// AllToAlls (Eq. 10, Eq. 14) of every axis whose top is in x, all issued at
+// one state (shard tbytes * 2^e, free levels `unused`): an AllToAll changes
+// neither, so the axes of one closure are costed together.  An axis wholly
+// above the node boundary sends V over the inter-node link with the group
+// count of Algorithm 3 that all such axes share; an in-node axis costs V
+// inside the node; the straddling axis (at most one) keeps its group
+// members inside a node out of the inter-node link.
+__host__ __device__ inline void taps_a2a_batch(taps_fac &c, uint32_t x, const taps_lv &L,
+                                               uint32_t lam, uint32_t e, uint32_t unused) {
+    const uint32_t sh = e + 8u;
+    const uint32_t low = taps_below(lam);
+    const uint32_t whole = 1u << sh;
+    uint32_t sum_in = 0, sum_out = 0;
+    for (uint32_t m = x & ~L.st; m; m &= m - 1u) {
+        const uint32_t t = taps_ctz(m);
+        const uint32_t lo = taps_msb(((L.tp & taps_below(t)) << 1) | 1u);
+        const uint32_t V = whole - (1u << (sh + lo - t - 1u));   // width t + 1 - lo
+        sum_in += t < lam ? V : 0u;
+        sum_out += t < lam ? 0u : V;
+    }
+    const uint32_t n_in = taps_popc(x & low), n_out = taps_popc(x & ~low & ~L.st);
+    const uint32_t lct = lam - taps_popc(unused & low);
+    c.vol += sum_in + sum_out;
+    c.intra += sum_in;
+    c.inter += sum_out << lct;
+    c.counts += n_in + (n_out << 8) + n_out + ((n_out << lct) << 16);
+    if (x & L.st) {
+        const uint32_t t = taps_ctz(L.st), lo = L.lo_s;
+        const uint32_t w = t + 1u - lo, kap = lam - lo;
+        const uint32_t V = whole - (1u << (sh - w));
+        const uint32_t link = ((1u << w) - (1u << kap)) << (kap + sh - w);
+        const uint32_t lcts = lo - taps_popc(unused & taps_below(lo));
+        c.vol += V;
+        c.inter += link << lcts;
+        c.counts += 0x101u + ((1u << lcts) << 16);
+    }
 }
 
 // Exact order of intra/(N B_intra) + inter/(N B_inter) between candidates:
@@ -445,53 +488,11 @@ struct taps_state {
 
 __host__ __device__ inline void taps_gather(const taps_row &P, const taps_lv &L, taps_state &s,
                                             taps_fac &c, uint32_t top) {
-    taps_cost(c, false, top, L, P.lam, s.e, s.unused);
+    taps_cost(c, top, L, P.lam, s.e, s.unused);
     const uint32_t lv = taps_fill(L, 1u << top);
     s.ats &= ~(1u << top);
     s.unused |= lv;
     s.e += taps_popc(lv);
-}
-
-// Gathers, back to back in producer order, every axis whose top is in x (x
-// within producer levels), with no other event between them.  Within one
-// dimension the axes go from the top level down, so their volumes telescope:
-// the axes wholly above the node boundary (levels >= lam) cost
-// (2^W_A - 1) S together and share one inter-node group count (they do not
-// change which levels below lam are free); at most one axis straddles the
-// boundary; the axes below it are intra-node and cost (2^W_B - 1) S' together.
-__host__ __device__ inline void taps_gather_run(const taps_row &P, const taps_lv &L, taps_state &s,
-                                                taps_fac &c, uint32_t x) {
-    const uint32_t lam = P.lam;
-    const uint32_t low = taps_below(lam);
-#pragma unroll
-    for (uint32_t d = 0; d < TAPS_D_MAX_RANK; ++d) {
-        if (d >= P.rank) break;
-        const uint32_t xd = x & P.pr[d];
-        const uint32_t G = taps_fill(L, xd);
-        const uint32_t hi = G & ~low, lo = G & low;
-        // the axis through levels lam-1 and lam (no top at lam-1)
-        const bool st = lam >= 1u && ((G >> lam) & 1u) && ((G >> (lam - 1u)) & 1u) &&
-                        !((L.tp >> (lam - 1u)) & 1u);
-        const uint32_t t_s = taps_ctz((L.tp & hi) | 0x100u);
-        const uint32_t lo_s = taps_msb(((L.tp & low) << 1) | 1u);
-        const uint32_t ws_hi = st ? t_s + 1u - lam : 0u, ws_lo = st ? lam - lo_s : 0u;
-        const uint32_t nS = st ? 1u : 0u;
-        const uint32_t nA = taps_popc(L.tp & hi) - nS, nB = taps_popc(L.tp & lo);
-        const uint32_t WA = taps_popc(hi) - ws_hi, WB = taps_popc(lo) - ws_lo, WS = ws_hi + ws_lo;
-        const uint32_t sh = s.e + 8u;
-        const uint32_t VA = ((1u << WA) - 1u) << sh;
-        const uint32_t VS = ((1u << WS) - 1u) << (sh + WA);
-        const uint32_t VB = ((1u << WB) - 1u) << (sh + WA + WS);
-        const uint32_t lctA = lam - taps_popc(s.unused & low);
-        const uint32_t lctS = st ? lo_s - taps_popc(s.unused & taps_below(lo_s)) : 0u;
-        c.vol += VA + VS + VB;
-        c.intra += VB;
-        c.inter += (VA << lctA) + (VS << lctS);
-        c.counts += (nA + nS + nB) + ((nA + nS) << 8) + (((nA << lctA) + (nS << lctS)) << 16);
-        s.e += taps_popc(G);
-        s.unused |= G;
-        s.ats &= ~xd;
-    }
 }
 
 // Every free target position whose axis no dimension uses is sliced.
@@ -536,19 +537,18 @@ __host__ __device__ inline taps_run taps_alg1(const taps_row &P, const taps_col 
             break;
         }
         const uint32_t sl = taps_slice(L, s);
+        uint32_t moved = 0;
         for (;;) {
             const uint32_t mv = L.dst & s.ats & ~s.blk;
             if (!mv) break;
-            uint32_t m = mv;
-            while (m) {
-                const uint32_t top = taps_msb(m);
-                m &= ~(1u << top);
-                taps_cost(c, true, top, L, P.lam, s.e, s.unused);
-                ++n_a2a;
-            }
+            moved |= mv;
             s.blk &= ~taps_blocked(P, Q, L, mv);
             s.ats &= ~mv;
-            s.atd |= mv;
+        }
+        if (moved) {
+            s.atd |= moved;
+            n_a2a += taps_popc(moved);
+            taps_a2a_batch(c, moved, L, P.lam, s.e, s.unused);
         }
         if (sl) taps_slice(L, s);
         if (s.ats == 0 && s.atd == L.dst) break;
@@ -613,7 +613,7 @@ __host__ __device__ inline taps_run taps_rearrange(const taps_row &P, const taps
         const uint32_t top = taps_rank_level(P, taps_ctz(x));
         x &= x - 1u;
         const uint32_t b = 1u << top;
-        taps_cost(c, false, top, L, P.lam, s.e, s.unused);
+        taps_cost(c, top, L, P.lam, s.e, s.unused);
         s.ats &= ~b;
         if (bounce & b) {
             s.atd |= b;
@@ -633,7 +633,7 @@ __host__ __device__ inline taps_run taps_rearrange(const taps_row &P, const taps
         const uint32_t top = taps_rank_level(P, taps_ctz(x));
         x &= x - 1u;
         const uint32_t b = 1u << top;
-        taps_cost(c, false, top, L, P.lam, s.e, s.unused);
+        taps_cost(c, top, L, P.lam, s.e, s.unused);
         const uint32_t freed_for = taps_blocked(P, Q, L, b);   // the axis targeting that position
         s.ats &= ~b;
         s.blk &= ~freed_for;
@@ -658,24 +658,96 @@ __host__ __device__ inline taps_run taps_rearrange(const taps_row &P, const taps
 }
 
 // "remove" (Table 2): gather every held axis not at its target, lowest
-// position first; the slices that follow are free.  One uninterrupted run.
+// position first (dimensions ascending, each from its top level down); the
+// slices that follow are free.  The run is uninterrupted, so it has a
+// closed form:
+//   * each gather multiplies the shard by 2^w, so all volumes together
+//     telescope to (2^W - 1) S0 with W the gathered levels;
+//   * inside one dimension the axes wholly above the node boundary come
+//     first; they leave the free levels below lam alone, so they share one
+//     inter-node group count (Algorithm 3) and cost (2^W_A - 1) S together;
+//   * at most one unified axis straddles the boundary (the one holding
+//     levels lam - 1 and lam), and it lies in the producer dimension whose
+//     run holds those levels;
+//   * the in-node axes come last and cost (2^W_B - 1) S' together.
 __host__ __device__ inline taps_fac taps_remove(const taps_row &P, const taps_lv &L) {
+    const uint32_t lam = P.lam;
+    const uint32_t low = taps_below(lam);
+    const uint32_t G = taps_fill(L, L.src & ~L.home);
+    // the straddling axis (levels lo_s .. its top); only dimension P.dstr can hold it
+    const uint32_t lo_s = L.lo_s;
+    const uint32_t S = L.st && P.dstr < TAPS_D_MAX_RANK ? taps_fill(L, L.st) : 0u;
+    const uint32_t GA = G & ~low & ~S, GB = G & low & ~S;
+    const uint32_t TA = L.tp & GA, TB = L.tp & GB;
     taps_fac c;
-    taps_fac_zero(c);
-    taps_state s;
-    s.ats = L.src & ~L.home;
-    s.atd = 0;
-    s.blk = 0;
-    s.unused = P.full & ~P.pru;
-    s.e = P.e0;
-    taps_gather_run(P, L, s, c, s.ats);
+    c.vol = ((1u << taps_popc(G)) - 1u) << (P.e0 + 8u);
+    c.intra = c.inter = 0;
+    c.counts = 0;
+    uint32_t sh = P.e0 + 8u;
+    uint32_t unused = P.full & ~P.pru;
+#pragma unroll
+    for (uint32_t d = 0; d < TAPS_D_MAX_RANK; ++d) {
+        if (d >= P.rank) break;
+        const uint32_t pd = P.pr[d];
+        const uint32_t WA = taps_popc(GA & pd), WB = taps_popc(GB & pd);
+        const uint32_t nA = taps_popc(TA & pd), nB = taps_popc(TB & pd);
+        const uint32_t lctA = lam - taps_popc(unused & low);
+        uint32_t WS = 0;
+        if (d == P.dstr) {   // uniform: the only dimension that can hold the straddler
+            WS = taps_popc(G & S);
+            if (WS) {
+                const uint32_t lctS = lo_s - taps_popc(unused & taps_below(lo_s));
+                const uint32_t VS = ((1u << WS) - 1u) << (sh + WA);
+                c.inter += VS << lctS;
+                c.counts += 0x101u + ((1u << lctS) << 16);
+            }
+        }
+        const uint32_t VA = ((1u << WA) - 1u) << sh;
+        const uint32_t VB = ((1u << WB) - 1u) << (sh + WA + WS);
+        c.intra += VB;
+        c.inter += VA << lctA;
+        c.counts += (nA + nB) + (nA << 8) + ((nA << lctA) << 16);
+        const uint32_t Gd = G & pd;
+        sh += taps_popc(Gd);
+        unused |= Gd;
+    }
     return c;
 }
 
-// tbytes * f / 256, exact (the result is an integer volume in nb < 2^64).
-__host__ __device__ inline uint64_t taps_scale(uint64_t tbytes, uint32_t f) {
-    return (((tbytes & 0xFFFFFFFFull) * f) >> 8) + (((tbytes >> 32) * f) << 24);
+// How the factor-unit sums of one edge become record numbers (uniform over
+// the edge): volumes are tbytes * f / 256 nb, exact; t uses the per-unit
+// seconds a = tbytes / 256 / (N B).
+struct taps_scaler {
+    uint64_t tbytes;
+    uint32_t q;         // tbytes / 256 when that is exact and below 2^32, else 0
+    double a_intra;     // tbytes / 256 / (N B_intra)
+    double a_inter;     // tbytes / 256 / (N B_inter)
+};
+
+__host__ __device__ inline taps_scaler taps_make_scaler(uint64_t tbytes, double inv_n_bintra,
+                                                        double inv_n_binter) {
+    taps_scaler S;
+    S.tbytes = tbytes;
+    S.q = (tbytes & 255u) == 0 && (tbytes >> 40) == 0 ? (uint32_t)(tbytes >> 8) : 0u;
+    const double unit = (double)tbytes * (1.0 / 256.0);   // exact: tbytes < 2^53
+    S.a_intra = unit * inv_n_bintra;
+    S.a_inter = unit * inv_n_binter;
+    return S;
 }
+
+// tbytes * f / 256, exact (the result is an integer volume in nb < 2^64).
+__host__ __device__ inline uint64_t taps_scale(const taps_scaler &S, uint32_t f) {
+    if (S.q) return (uint64_t)S.q * f;
+    return (((S.tbytes & 0xFFFFFFFFull) * f) >> 8) + (((S.tbytes >> 32) * f) << 24);
+}
+
+// The chosen candidate of one entry, in factor units.
+struct taps_pick {
+    taps_fac best;
+    uint32_t vmin;   // smallest volume among the candidates
+    uint32_t cand;   // 0 Algorithm 1, 1 without AllToAll, 2 remove
+    bool ok;
+};
 
 struct taps_entry_out {
     double t;
@@ -687,48 +759,59 @@ struct taps_entry_out {
 // The cheapest of Algorithm 1, Algorithm 1 without AllToAll, and "remove"
 // (the naive sequence of Table 2 gathers a superset of what "remove"
 // gathers, in the same order, so it is never cheaper in either model and
-// never wins a tie); vol is the smallest volume among them.  The second and
-// third candidates stop as soon as they cannot change the record.
-__host__ __device__ inline taps_entry_out taps_edge_entry(const taps_row &P, const taps_col &Q,
-                                                          uint64_t tbytes, const taps_keys &K,
-                                                          double inv_n_bintra,
-                                                          double inv_n_binter) {
+// never wins a tie); vol is the smallest volume among them.  The second
+// candidate stops as soon as it cannot change the record.
+__host__ __device__ inline taps_pick taps_edge_select(const taps_row &P, const taps_col &Q,
+                                                      const taps_keys &K) {
     taps_lv L;
     taps_unify(P, Q, L);
     const taps_run r0 = taps_alg1(P, Q, L);
-    taps_fac best = r0.c;
-    uint32_t cand = 0, vmin = r0.c.vol;
+    taps_pick k;
+    k.best = r0.c;
+    k.cand = 0;
+    k.vmin = r0.c.vol;
+    k.ok = r0.ok;
     taps_limit lim;
     lim.on = K.narrow;
-    lim.key = taps_key64(best, K);
-    lim.vol = vmin;
-    bool ok = r0.ok;
+    lim.key = taps_key64(k.best, K);
+    lim.vol = k.vmin;
     if (r0.n_a2a) {   // without AllToAll the sequence would be the same
         const taps_run r1 = taps_rearrange(P, Q, L, lim, K);
-        ok = ok && r1.ok;
+        k.ok = k.ok && r1.ok;
         if (!r1.stopped) {
-            if (taps_less(r1.c, best, K)) {
-                best = r1.c;
-                cand = 1;
+            if (taps_less(r1.c, k.best, K)) {
+                k.best = r1.c;
+                k.cand = 1;
             }
-            vmin = r1.c.vol < vmin ? r1.c.vol : vmin;
+            k.vmin = r1.c.vol < k.vmin ? r1.c.vol : k.vmin;
         }
     }
     const taps_fac c2 = taps_remove(P, L);
-    if (taps_less(c2, best, K)) {
-        best = c2;
-        cand = 2;
+    if (taps_less(c2, k.best, K)) {
+        k.best = c2;
+        k.cand = 2;
     }
-    vmin = c2.vol < vmin ? c2.vol : vmin;
+    k.vmin = c2.vol < k.vmin ? c2.vol : k.vmin;
+    return k;
+}
+
+__host__ __device__ inline taps_entry_out taps_entry_finish(const taps_pick &k,
+                                                            const taps_scaler &S) {
     taps_entry_out o;
-    o.vol = taps_scale(tbytes, vmin);
-    o.intra = taps_scale(tbytes, best.intra);
-    o.inter = taps_scale(tbytes, best.inter);
-    o.t = (double)o.intra * inv_n_bintra + (double)o.inter * inv_n_binter;
-    o.meta = cand | ((best.counts & 0xFFu) << 2) | (((best.counts >> 8) & 0xFFu) << 7) |
-             ((best.counts >> 16) << 12);
-    o.ok = ok;
+    o.vol = taps_scale(S, k.vmin);
+    o.intra = taps_scale(S, k.best.intra);
+    o.inter = taps_scale(S, k.best.inter);
+    o.t = (double)k.best.intra * S.a_intra + (double)k.best.inter * S.a_inter;
+    const uint32_t n = k.best.counts;
+    o.meta = k.cand | ((n & 0xFFu) << 2) | (((n >> 8) & 0xFFu) << 7) | ((n >> 16) << 12);
+    o.ok = k.ok;
     return o;
+}
+
+__host__ __device__ inline taps_entry_out taps_edge_entry(const taps_row &P, const taps_col &Q,
+                                                          const taps_scaler &S,
+                                                          const taps_keys &K) {
+    return taps_entry_finish(taps_edge_select(P, Q, K), S);
 }
 
 // Producer side of a row from a strategy descriptor and the tensor's axes
@@ -753,6 +836,13 @@ __host__ __device__ inline void taps_make_row(taps_row &P, const taps_desc &D, u
         used += w;
     }
     P.e0 = n - used;
+    P.dstr = TAPS_D_MAX_RANK;
+    if (lam >= 1u && lam < n) {
+        const uint32_t two = 3u << (lam - 1u);
+#pragma unroll
+        for (uint32_t d = 0; d < TAPS_D_MAX_RANK; ++d)
+            if ((P.pr[d] & two) == two) P.dstr = d;
+    }
     // producer order: dimensions ascending, each from its top level down
     P.order = 0;
     uint32_t k = 0;

@@ -18,11 +18,11 @@ struct taps_launch {
     uint32_t narrow;        // both reduced bandwidths below 2^32
 };
 
-// Per-edge constants of the edge-table kernel (64 bytes).
+// Per-edge constants of the edge-table kernel.
 struct taps_edge_params {
     uint64_t out_offset;   // first entry of the edge's table
-    uint64_t tile_begin;   // first tile of the edge
-    uint64_t tbytes;       // elements x dtype bytes of the edge tensor
+    uint64_t row_begin;    // first table row of the edge (rows of all edges, in order)
+    taps_scaler scale;     // tbytes and the per-unit seconds of the edge tensor
     uint32_t src_base;     // first strategy of the producer
     uint32_t dst_base;     // first strategy of the consumer
     uint32_t ns, nd;       // strategy counts
@@ -32,10 +32,18 @@ struct taps_edge_params {
     uint32_t pad;
 };
 
-// An edge tile is one table row (producer strategy) times 64 consecutive
-// columns (consumer strategies): one wavefront.  A workgroup runs four.
+// One wavefront per table row (producer strategy i of one edge); it walks
+// the row's consumer strategies 64 at a time.  A workgroup holds
+// TAPS_ROWS_PER_BLOCK rows.
 #define TAPS_TILE_COLS 64
-#define TAPS_TILES_PER_BLOCK 4
+#define TAPS_ROWS_PER_BLOCK 4
+
+// Row r of the flat row list: its edge and the global index of its producer
+// strategy.
+struct taps_row_ref {
+    uint32_t edge;
+    uint32_t strategy;
+};
 
 #define TAPS_ENUM_CHUNK 64   // candidates per enumeration wavefront
 
@@ -50,8 +58,9 @@ hipError_t taps_launch_node_costs(const taps_op *ops, uint32_t n_ops, const uint
                                   taps_table out, hipStream_t stream);
 hipError_t taps_launch_edge_setup(const taps_op *ops, const taps_edge *edges, uint32_t n_edges,
                                   const uint64_t *op_offsets, const uint64_t *edge_offsets,
-                                  const uint64_t *tile_begin, taps_edge_params *params,
-                                  uint64_t n_tiles, uint32_t *tile_edge, hipStream_t stream);
-hipError_t taps_launch_edge_costs(const taps_edge_params *params, const uint32_t *tile_edge,
-                                  uint64_t n_tiles, const taps_desc *desc, const taps_launch &lp,
+                                  const uint64_t *row_begin, const taps_launch &lp,
+                                  taps_edge_params *params, uint64_t n_rows, taps_row_ref *rows,
+                                  hipStream_t stream);
+hipError_t taps_launch_edge_costs(const taps_edge_params *params, const taps_row_ref *rows,
+                                  uint64_t n_rows, const taps_desc *desc, const taps_launch &lp,
                                   taps_table out, hipStream_t stream);

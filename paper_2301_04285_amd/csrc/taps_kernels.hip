@@ -5,11 +5,12 @@
 //   k_describe    one thread per strategy: level runs, owners and cuts
 //   k_node_costs  one thread per strategy: the intra-op AllReduces
 //   k_edge_setup  one thread per edge: per-edge constants
-//   k_tile_map    one thread per edge tile: which edge the tile belongs to
-//   k_edge_costs  one wavefront per tile = one table row (producer strategy,
-//                 uniform: its descriptor sits in scalar registers) x 64
-//                 consecutive columns (consumer strategies, one per lane);
-//                 five coalesced non-temporal SoA stores per entry
+//   k_row_map     one thread per table row: its edge and producer strategy
+//   k_edge_costs  one wavefront per table row (producer strategy, uniform:
+//                 its descriptor sits in scalar registers), four rows per
+//                 workgroup, walking the row's consumer strategies 64 at a
+//                 time (one per lane, the next 64 prefetched); five
+//                 coalesced non-temporal SoA stores per entry
 #include "taps_internal.h"
 
 namespace {
@@ -19,6 +20,11 @@ constexpr uint32_t kWave = 64;
 // Completion counts w(k, s, z) for k, s, z in 0..8 (see taps_completions),
 // evaluated by the compiler.
 __constant__ taps_completion_table kCompletions = taps_make_completions();
+
+template <typename T>
+__device__ inline T *at_byte(T *base, uint32_t offset) {
+    return (T *)((char *)base + offset);
+}
 
 __device__ inline uint32_t lanes_below(uint64_t mask) {
     return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
@@ -130,7 +136,8 @@ __global__ __launch_bounds__(256) void k_edge_setup(const taps_op *__restrict__ 
                                                     uint32_t n_edges,
                                                     const uint64_t *__restrict__ op_offsets,
                                                     const uint64_t *__restrict__ edge_offsets,
-                                                    const uint64_t *__restrict__ tile_begin,
+                                                    const uint64_t *__restrict__ row_begin,
+                                                    taps_launch lp,
                                                     taps_edge_params *__restrict__ params) {
     const uint32_t e = blockIdx.x * blockDim.x + threadIdx.x;
     if (e >= n_edges) return;
@@ -141,7 +148,7 @@ __global__ __launch_bounds__(256) void k_edge_setup(const taps_op *__restrict__ 
     const taps_tensor &Tc = dst.in[E.dst_slot];
     taps_edge_params p;
     p.out_offset = edge_offsets[e];
-    p.tile_begin = tile_begin[e];
+    p.row_begin = row_begin[e];
     uint64_t bytes = src.dtype_bytes;
     uint32_t pa = 0, ca = 0;
     for (uint32_t d = 0; d < T.rank && d < TAPS_MAX_RANK; ++d) {
@@ -149,7 +156,7 @@ __global__ __launch_bounds__(256) void k_edge_setup(const taps_op *__restrict__ 
         pa |= (uint32_t)(T.axis[d] & 7u) << (4u * d);
         ca |= (uint32_t)(Tc.axis[d] & 7u) << (4u * d);
     }
-    p.tbytes = bytes;
+    p.scale = taps_make_scaler(bytes, lp.inv_n_bintra, lp.inv_n_binter);
     p.src_base = (uint32_t)op_offsets[E.src_op];
     p.dst_base = (uint32_t)op_offsets[E.dst_op];
     p.ns = (uint32_t)(op_offsets[E.src_op + 1] - op_offsets[E.src_op]);
@@ -161,48 +168,71 @@ __global__ __launch_bounds__(256) void k_edge_setup(const taps_op *__restrict__ 
     params[e] = p;
 }
 
-__global__ __launch_bounds__(256) void k_tile_map(const uint64_t *__restrict__ tile_begin,
-                                                  uint32_t n_edges, uint64_t n_tiles,
-                                                  uint32_t *__restrict__ tile_edge) {
-    const uint64_t t = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (t >= n_tiles) return;
-    tile_edge[t] = find_owner(tile_begin, n_edges, t);
+__global__ __launch_bounds__(256) void k_row_map(const uint64_t *__restrict__ row_begin,
+                                                 const uint64_t *__restrict__ op_offsets,
+                                                 const taps_edge *__restrict__ edges,
+                                                 uint32_t n_edges, uint64_t n_rows,
+                                                 taps_row_ref *__restrict__ rows) {
+    const uint64_t r = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (r >= n_rows) return;
+    const uint32_t e = find_owner(row_begin, n_edges, r);
+    taps_row_ref ref;
+    ref.edge = e;
+    ref.strategy = (uint32_t)(op_offsets[edges[e].src_op] + (r - row_begin[e]));
+    rows[r] = ref;
 }
 
-__global__ __launch_bounds__(TAPS_TILE_COLS * TAPS_TILES_PER_BLOCK) void k_edge_costs(
-    const taps_edge_params *__restrict__ params, const uint32_t *__restrict__ tile_edge,
-    uint64_t n_tiles, const taps_desc *__restrict__ desc, taps_launch lp, taps_table out) {
-    __shared__ uint8_t rank_tab[TAPS_TILES_PER_BLOCK][256];
-    // everything up to the column index is uniform across the wavefront
-    const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x / TAPS_TILE_COLS);
+__global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_costs(
+    const taps_edge_params *__restrict__ params, const taps_row_ref *__restrict__ rows,
+    uint32_t n_rows, const taps_desc *__restrict__ desc, taps_launch lp, taps_table out) {
+    __shared__ uint8_t rank_tab[TAPS_ROWS_PER_BLOCK][256];
     const uint32_t lane = threadIdx.x % TAPS_TILE_COLS;
-    const uint64_t tile = (uint64_t)blockIdx.x * TAPS_TILES_PER_BLOCK + wave;
-    const bool live = tile < n_tiles;
-    const uint32_t e = __builtin_amdgcn_readfirstlane(live ? tile_edge[tile] : 0u);
-    const taps_edge_params E = params[e];
-    const uint32_t row_tiles = (E.nd + TAPS_TILE_COLS - 1) / TAPS_TILE_COLS;
-    const uint32_t lt = live ? (uint32_t)(tile - E.tile_begin) : 0u;
-    const uint32_t i = __builtin_amdgcn_readfirstlane(lt / row_tiles);
+    const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x / TAPS_TILE_COLS);
+    const uint32_t r = blockIdx.x * TAPS_ROWS_PER_BLOCK + wave;
+    const bool live = r < n_rows;
+    const taps_row_ref ref = rows[live ? r : 0u];
+    const taps_edge_params E = params[ref.edge];
+    const taps_desc Dp = desc[ref.strategy];
+    const uint32_t i = ref.strategy - E.src_base;
     taps_row P;
-    taps_make_row(P, desc[E.src_base + i], E.paxes, E.rank, lp.n, lp.lam);
+    taps_make_row(P, Dp, E.paxes, E.rank, lp.n, lp.lam);
     taps_fill_rank_table(P, rank_tab[wave], lane, TAPS_TILE_COLS);
     __syncthreads();
+    if (!live) return;
     P.to_rank = rank_tab[wave];
-    const uint32_t j = (lt - i * row_tiles) * TAPS_TILE_COLS + lane;
-    if (!live || j >= E.nd) return;
-    taps_col Q;
-    taps_make_col(Q, desc[E.dst_base + j], E.caxes, E.rank);
     taps_keys K;
     K.b_inter_red = lp.b_inter_red;
     K.b_intra_red = lp.b_intra_red;
     K.narrow = lp.narrow != 0;
-    const taps_entry_out o = taps_edge_entry(P, Q, E.tbytes, K, lp.inv_n_bintra, lp.inv_n_binter);
-    const uint64_t g = E.out_offset + (uint64_t)i * E.nd + j;
-    __builtin_nontemporal_store(o.t, out.t + g);
-    __builtin_nontemporal_store(o.vol, out.vol + g);
-    __builtin_nontemporal_store(o.intra, out.intra + g);
-    __builtin_nontemporal_store(o.inter, out.inter + g);
-    __builtin_nontemporal_store(o.ok ? o.meta : 0xFFFFFFFFu, out.meta + g);
+    // the row's records start here; lane j writes entry j
+    const uint64_t row_out = E.out_offset + (uint64_t)i * E.nd;
+    double *const t_row = out.t + row_out;
+    uint64_t *const vol_row = out.vol + row_out;
+    uint64_t *const intra_row = out.intra + row_out;
+    uint64_t *const inter_row = out.inter + row_out;
+    uint32_t *const meta_row = out.meta + row_out;
+    const taps_desc *col = desc + E.dst_base;
+    // consumer descriptors one tile ahead
+    taps_desc next = col[lane < E.nd ? lane : 0u];
+    for (uint32_t j0 = 0; j0 < E.nd; j0 += TAPS_TILE_COLS) {
+        const taps_desc cur = next;
+        const uint32_t j = j0 + lane;
+        const uint32_t jn = j + TAPS_TILE_COLS;
+        if (jn < E.nd) next = col[jn];
+        if (j < E.nd) {
+            taps_col Q;
+            taps_make_col(Q, cur, E.caxes, E.rank);
+            const taps_entry_out o = taps_entry_finish(taps_edge_select(P, Q, K), E.scale);
+            // 32-bit byte offsets from the uniform row bases: j < 2^21 (8 axes on
+            // 8 levels give at most 1,047,376 strategies per operator)
+            const uint32_t o8 = j * 8u, o4 = j * 4u;
+            __builtin_nontemporal_store(o.t, at_byte(t_row, o8));
+            __builtin_nontemporal_store(o.vol, at_byte(vol_row, o8));
+            __builtin_nontemporal_store(o.intra, at_byte(intra_row, o8));
+            __builtin_nontemporal_store(o.inter, at_byte(inter_row, o8));
+            __builtin_nontemporal_store(o.ok ? o.meta : 0xFFFFFFFFu, at_byte(meta_row, o4));
+        }
+    }
 }
 
 inline uint32_t blocks_for(uint64_t n, uint32_t per) { return (uint32_t)((n + per - 1) / per); }
@@ -238,24 +268,25 @@ hipError_t taps_launch_node_costs(const taps_op *ops, uint32_t n_ops, const uint
 
 hipError_t taps_launch_edge_setup(const taps_op *ops, const taps_edge *edges, uint32_t n_edges,
                                   const uint64_t *op_offsets, const uint64_t *edge_offsets,
-                                  const uint64_t *tile_begin, taps_edge_params *params,
-                                  uint64_t n_tiles, uint32_t *tile_edge, hipStream_t stream) {
+                                  const uint64_t *row_begin, const taps_launch &lp,
+                                  taps_edge_params *params, uint64_t n_rows, taps_row_ref *rows,
+                                  hipStream_t stream) {
     if (n_edges == 0) return hipSuccess;
     hipLaunchKernelGGL(k_edge_setup, dim3(blocks_for(n_edges, 256)), dim3(256), 0, stream, ops,
-                       edges, n_edges, op_offsets, edge_offsets, tile_begin, params);
+                       edges, n_edges, op_offsets, edge_offsets, row_begin, lp, params);
     hipError_t err = hipGetLastError();
-    if (err != hipSuccess || n_tiles == 0) return err;
-    hipLaunchKernelGGL(k_tile_map, dim3(blocks_for(n_tiles, 256)), dim3(256), 0, stream,
-                       tile_begin, n_edges, n_tiles, tile_edge);
+    if (err != hipSuccess || n_rows == 0) return err;
+    hipLaunchKernelGGL(k_row_map, dim3(blocks_for(n_rows, 256)), dim3(256), 0, stream, row_begin,
+                       op_offsets, edges, n_edges, n_rows, rows);
     return hipGetLastError();
 }
 
-hipError_t taps_launch_edge_costs(const taps_edge_params *params, const uint32_t *tile_edge,
-                                  uint64_t n_tiles, const taps_desc *desc, const taps_launch &lp,
+hipError_t taps_launch_edge_costs(const taps_edge_params *params, const taps_row_ref *rows,
+                                  uint64_t n_rows, const taps_desc *desc, const taps_launch &lp,
                                   taps_table out, hipStream_t stream) {
-    if (n_tiles == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_edge_costs, dim3(blocks_for(n_tiles, TAPS_TILES_PER_BLOCK)),
-                       dim3(TAPS_TILE_COLS * TAPS_TILES_PER_BLOCK), 0, stream, params, tile_edge,
-                       n_tiles, desc, lp, out);
+    if (n_rows == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_edge_costs, dim3(blocks_for(n_rows, TAPS_ROWS_PER_BLOCK)),
+                       dim3(TAPS_TILE_COLS * TAPS_ROWS_PER_BLOCK), 0, stream, params, rows,
+                       (uint32_t)n_rows, desc, lp, out);
     return hipGetLastError();
 }
