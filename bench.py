@@ -9,10 +9,13 @@ table and the edge (redistribution) table -- 599,136 strategies and
 packed into the C structs once, outside the timed region.
 
 Prints one JSON line.  `value` is edge entries per second of whole steps;
-`roofline` relates the edge-table call (whose kernel dominates the step) to
-MI355X's 8 TB/s HBM: each entry writes 36 bytes (t 8, vol 8, intra 8, inter
-8, meta 4).  `cpu_baseline` times the CPU oracle, single-threaded, on the
-first layers of the same graph.
+`roofline` relates the edge-table kernel (which dominates the step), timed
+with HIP events the library records right around its launch on the same
+stream, to MI355X's 8 TB/s HBM: each entry writes 36 bytes (t 8, vol 8,
+intra 8, inter 8, meta 4).  `cpu_baseline` times the CPU oracle, single-threaded, on the
+first layers of the same graph.  `roofline.traffic` is the edge kernel's HBM
+bytes per launch from the committed rocprofv3 counter summary (null once the
+kernel sources differ from the ones the counters were taken with).
 """
 from __future__ import annotations
 
@@ -28,10 +31,35 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBPS = 8000.0
 BYTES_PER_ENTRY = 36
+# rocprofv3 counter summary of the edge kernel on the 96-layer workload: HBM bytes
+# per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated) and a hash of the kernel
+# sources they were taken with
+COUNTERS = os.path.join(ROOT, "profiles", "edge_costs_gpt96L_16x8_counters.md")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2301_04285_amd", "csrc", f)
+                  for f in ("taps_device.h", "taps_kernels.hip", "taps_internal.h")]
 
 
 def log(msg: str) -> None:
     print(msg, file=sys.stderr, flush=True)
+
+
+def measured_traffic():
+    """HBM bytes per launch of the edge kernel from the committed counter summary,
+    or None when the kernel sources changed since the counters were taken."""
+    import hashlib
+    try:
+        text = open(COUNTERS).read()
+    except OSError:
+        return None
+    fields = dict(line.split(": ", 1) for line in text.splitlines()
+                  if line.startswith(("traffic_bytes_per_launch: ", "kernel_sources_sha256: ")))
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    if fields.get("kernel_sources_sha256", "").strip() != h.hexdigest():
+        return None
+    return int(fields["traffic_bytes_per_launch"])
 
 
 def cpu_baseline(workload, cluster, layers: int) -> dict:
@@ -109,6 +137,7 @@ def main() -> int:
         taps.taps_node_costs(g, cl, strat, offs, out=tabs.node, stream=stream)
         if ev is not None:
             ev[0].record(stream)
+            taps.taps_set_edge_kernel_events(ev[2], ev[3])
         taps.taps_edge_costs(g, cl, strat, offs, out=tabs.edge, stream=stream)
         if ev is not None:
             ev[1].record(stream)
@@ -118,20 +147,27 @@ def main() -> int:
     torch.cuda.synchronize()
     log(f"[bench] warmup {args.warmup} done")
 
-    events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+    # per step: the whole edge call, and the edge-table kernel alone (recorded by the
+    # library on the same stream right around that launch)
+    events = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(4))
               for _ in range(args.steps)]
+    for ev in events:
+        for e in ev:
+            e.record(stream)   # creates the event before the library records it again
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(args.steps):
         step(events[k])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    edge_ms = float(np.mean([a.elapsed_time(b) for a, b in events]))
+    edge_ms = float(np.mean([ev[0].elapsed_time(ev[1]) for ev in events]))
+    kernel_ms = float(np.mean([ev[2].elapsed_time(ev[3]) for ev in events]))
     ms_per_step = wall * 1e3 / args.steps
-    log(f"[bench] {args.steps} steps: {ms_per_step:.3f} ms/step, edge call {edge_ms:.3f} ms")
+    log(f"[bench] {args.steps} steps: {ms_per_step:.3f} ms/step, edge call {edge_ms:.3f} ms, "
+        f"edge kernel {kernel_ms:.3f} ms")
 
     bytes_per_launch = BYTES_PER_ENTRY * entries
-    achieved = bytes_per_launch / (edge_ms * 1e-3) / 1e9
+    achieved = bytes_per_launch / (kernel_ms * 1e-3) / 1e9
     out = {
         "metric": "edge-cost entries/sec on 1 GPU (full cost-table build: enumerate + node + edge)",
         "value": entries / (ms_per_step * 1e-3),
@@ -151,9 +187,11 @@ def main() -> int:
                    "bw_intra_GBps": cl.bw_intra / 1e9, "bw_inter_GBps": cl.bw_inter / 1e9},
         "build_ms": ms_per_step,
         "edge_call_ms": edge_ms,
+        "edge_kernel_ms": kernel_ms,
         "edge_entries_per_s": entries / (edge_ms * 1e-3),
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBPS, "traffic": None},
+                     "frac": achieved / HBM_PEAK_GBPS,
+                     "traffic": measured_traffic() if args.config == 5 else None},
     }
     if args.cpu_layers > 0 and args.config == 5:
         log(f"[bench] CPU oracle baseline on {args.cpu_layers} layers")

@@ -190,6 +190,15 @@ taps_status taps_edge_costs(const taps_graph *graph, const taps_cluster *cluster
                             uint64_t *edge_offsets, taps_table out, uint64_t capacity,
                             void *stream);
 
+/* Profiling aid, not part of the method: `before` and `after` are HIP events
+ * (hipEvent_t, created by the caller, passed as plain pointers) that the
+ * calling thread's next taps_edge_costs call that launches the edge-table
+ * kernel records on its stream immediately before and after that kernel, so
+ * that the caller can time the kernel alone.  The setting is thread-local,
+ * used once and then cleared; two NULLs clear it.  The events stay owned by
+ * the caller.  TAPS_ERR_ARG if exactly one of them is NULL. */
+taps_status taps_set_edge_kernel_events(void *before, void *after);
+
 /* Static name of a status code. */
 const char *taps_status_str(taps_status status);
 

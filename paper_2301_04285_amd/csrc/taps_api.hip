@@ -20,6 +20,8 @@
 namespace {
 
 thread_local std::string g_last_error;
+// events to record around the next edge-table kernel (taps_set_edge_kernel_events)
+thread_local hipEvent_t g_kernel_before = nullptr, g_kernel_after = nullptr;
 
 taps_status fail(taps_status st, const char *fmt, ...) {
     char buf[512];
@@ -260,6 +262,15 @@ const char *taps_status_str(taps_status s) {
 
 const char *taps_last_error(void) { return g_last_error.c_str(); }
 
+taps_status taps_set_edge_kernel_events(void *before, void *after) {
+    g_last_error.clear();
+    if ((before == nullptr) != (after == nullptr))
+        return fail(TAPS_ERR_ARG, "both kernel events or neither");
+    g_kernel_before = (hipEvent_t)before;
+    g_kernel_after = (hipEvent_t)after;
+    return TAPS_OK;
+}
+
 taps_status taps_enumerate_strategies(const taps_graph *graph, const taps_cluster *cluster,
                                       uint64_t *op_offsets, taps_strategy *strategies,
                                       uint64_t capacity, void *stream_) {
@@ -428,8 +439,13 @@ taps_status taps_edge_costs(const taps_graph *graph, const taps_cluster *cluster
                                      at<uint64_t>(dev, ch[2]), at<uint64_t>(dev, ch[3]),
                                      at<uint64_t>(dev, ch[4]), lp, d_params, n_rows, d_rows,
                                      stream);
+    // the edge-table kernel launches (entries > 0): use the events, if any, once
+    const hipEvent_t before = g_kernel_before, after = g_kernel_after;
+    g_kernel_before = g_kernel_after = nullptr;
+    if (err == hipSuccess && before) err = hipEventRecord(before, stream);
     if (err == hipSuccess)
         err = taps_launch_edge_costs(d_params, d_rows, n_rows, d_desc, lp, out, stream);
+    if (err == hipSuccess && after) err = hipEventRecord(after, stream);
     if (err != hipSuccess) return hip_fail(err, "edge costs");
     return TAPS_OK;
 }

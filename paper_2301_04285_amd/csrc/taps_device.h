@@ -377,18 +377,29 @@ __host__ __device__ inline uint32_t taps_first_src(const taps_row &P, uint32_t x
     return taps_rank_level(P, taps_ctz(P.to_rank[x]));
 }
 
+// The unified axis with top level `top`: lowest level (one above the next
+// lower top, 0 if none), width and level mask.
+struct taps_ax {
+    uint32_t lo, w, lv;
+};
+
+__host__ __device__ inline taps_ax taps_axis(const taps_lv &L, uint32_t top) {
+    taps_ax a;
+    a.lo = taps_msb(((L.tp & taps_below(top)) << 1) | 1u);
+    a.w = top + 1u - a.lo;
+    a.lv = taps_below(top + 1u) & ~taps_below(a.lo);
+    return a;
+}
+
 // An AllGather (Eq. 9) of the axis with top level `top`, shard tbytes * 2^e,
 // with the inter-node group count of Algorithm 3: groups holding the same
 // data inside a node (replicas along levels no dimension uses) share one
 // inter-node transfer.
-__host__ __device__ inline void taps_cost(taps_fac &c, uint32_t top, const taps_lv &L,
+__host__ __device__ inline void taps_cost(taps_fac &c, uint32_t top, const taps_ax &a,
                                           uint32_t lam, uint32_t e, uint32_t unused) {
-    // lowest level of the axis: one above the next lower top (0 if none)
-    const uint32_t lo = taps_msb(((L.tp & taps_below(top)) << 1) | 1u);
-    const uint32_t w = top + 1u - lo;
-    const uint32_t V = ((1u << w) - 1u) << (e + 8u);
+    const uint32_t V = ((1u << a.w) - 1u) << (e + 8u);
     const bool in_node = top < lam;   // the whole group inside one node
-    const uint32_t m = lo < lam ? lo : lam;
+    const uint32_t m = a.lo < lam ? a.lo : lam;
     const uint32_t lct = m - taps_popc(unused & taps_below(m));
     c.vol += V;
     c.intra += in_node ? V : 0u;
@@ -488,11 +499,11 @@ struct taps_state {
 
 __host__ __device__ inline void taps_gather(const taps_row &P, const taps_lv &L, taps_state &s,
                                             taps_fac &c, uint32_t top) {
-    taps_cost(c, top, L, P.lam, s.e, s.unused);
-    const uint32_t lv = taps_fill(L, 1u << top);
+    const taps_ax a = taps_axis(L, top);
+    taps_cost(c, top, a, P.lam, s.e, s.unused);
     s.ats &= ~(1u << top);
-    s.unused |= lv;
-    s.e += taps_popc(lv);
+    s.unused |= a.lv;
+    s.e += a.w;
 }
 
 // Every free target position whose axis no dimension uses is sliced.
@@ -613,14 +624,14 @@ __host__ __device__ inline taps_run taps_rearrange(const taps_row &P, const taps
         const uint32_t top = taps_rank_level(P, taps_ctz(x));
         x &= x - 1u;
         const uint32_t b = 1u << top;
-        taps_cost(c, top, L, P.lam, s.e, s.unused);
+        const taps_ax a = taps_axis(L, top);
+        taps_cost(c, top, a, P.lam, s.e, s.unused);
         s.ats &= ~b;
         if (bounce & b) {
             s.atd |= b;
         } else {
-            const uint32_t lv = taps_fill(L, b);
-            s.unused |= lv;
-            s.e += taps_popc(lv);
+            s.unused |= a.lv;
+            s.e += a.w;
         }
     }
     // 3. targeted positions
@@ -633,18 +644,21 @@ __host__ __device__ inline taps_run taps_rearrange(const taps_row &P, const taps
         const uint32_t top = taps_rank_level(P, taps_ctz(x));
         x &= x - 1u;
         const uint32_t b = 1u << top;
-        taps_cost(c, top, L, P.lam, s.e, s.unused);
+        const taps_ax a = taps_axis(L, top);
+        taps_cost(c, top, a, P.lam, s.e, s.unused);
         const uint32_t freed_for = taps_blocked(P, Q, L, b);   // the axis targeting that position
         s.ats &= ~b;
         s.blk &= ~freed_for;
-        uint32_t lv = taps_fill(L, b);
-        s.unused |= lv;
-        s.e += taps_popc(lv);
-        uint32_t sl = L.dst & b & ~s.blk;                  // back into its own target
-        sl |= freed_for & ~(s.ats | s.atd);                // into the freed position
-        if (sl) {
-            lv = taps_fill(L, sl);
-            s.atd |= sl;
+        if (L.dst & b & ~s.blk) {
+            s.atd |= b;   // sliced back into its own target: shard and free levels as before
+        } else {
+            s.unused |= a.lv;
+            s.e += a.w;
+        }
+        const uint32_t sf = freed_for & ~(s.ats | s.atd);   // sliced into the freed position
+        if (sf) {
+            const uint32_t lv = taps_fill(L, sf);
+            s.atd |= sf;
             s.unused &= ~lv;
             s.e -= taps_popc(lv);
         }

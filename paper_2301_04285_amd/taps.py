@@ -86,6 +86,8 @@ def load():
         L.taps_edge_costs.restype = C.c_int
         L.taps_edge_costs.argtypes = [P(GraphS), P(Cluster), C.c_void_p, P(C.c_uint64),
                                       P(C.c_uint64), Table, C.c_uint64, C.c_void_p]
+        L.taps_set_edge_kernel_events.restype = C.c_int
+        L.taps_set_edge_kernel_events.argtypes = [C.c_void_p, C.c_void_p]
         L.taps_status_str.restype = C.c_char_p
         L.taps_status_str.argtypes = [C.c_int]
         L.taps_last_error.restype = C.c_char_p
@@ -267,6 +269,19 @@ def taps_edge_costs(graph, cluster, strategies, op_offsets, out=None, stream=Non
                            _u64_array(eoffs), _table(out), cap, _stream(stream))
     _check(st, "taps_edge_costs")
     return eoffs, {k: v[:total] for k, v in out.items()}
+
+
+def taps_set_edge_kernel_events(before, after) -> None:
+    """Have this thread's next edge-table kernel recorded between two
+    ``torch.cuda.Event``s (each recorded once already, so that it exists), or
+    clear the setting with two Nones."""
+    handles = []
+    for ev in (before, after):
+        h = 0 if ev is None else int(ev.cuda_event)
+        if ev is not None and h == 0:
+            raise ValueError("record the event once before passing it")
+        handles.append(C.c_void_p(h) if h else None)
+    _check(load().taps_set_edge_kernel_events(*handles), "taps_set_edge_kernel_events")
 
 
 @dataclass

@@ -19,13 +19,22 @@ def lib():
 def test_exports_every_declared_symbol(lib):
     declared = T.declared_symbols()
     assert declared == sorted(["taps_enumerate_strategies", "taps_node_costs", "taps_edge_costs",
-                               "taps_status_str", "taps_last_error"])
+                               "taps_set_edge_kernel_events", "taps_status_str",
+                               "taps_last_error"])
     out = subprocess.run(["nm", "-D", "--defined-only", T.LIB_PATH], capture_output=True,
                          text=True, check=True).stdout
     exported = {line.split()[-1] for line in out.splitlines() if line.strip()}
     for name in declared:
         assert name in exported
         assert getattr(lib, name) is not None
+
+
+def test_kernel_events_need_both_or_neither(lib):
+    import ctypes as C
+    assert lib.taps_set_edge_kernel_events(C.c_void_p(0x1000), None) == T.ERR_ARG
+    assert "both" in T.last_error()
+    assert lib.taps_set_edge_kernel_events(None, C.c_void_p(0x1000)) == T.ERR_ARG
+    assert lib.taps_set_edge_kernel_events(None, None) == 0
 
 
 def test_status_strings(lib):

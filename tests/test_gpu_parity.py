@@ -254,3 +254,29 @@ def test_repeatable_bitwise(T):
     for f in ("t", "vol", "intra", "inter", "meta"):
         assert np.array_equal(_np(a.edge[f]), _np(b.edge[f]))
         assert np.array_equal(_np(a.node[f]), _np(b.node[f]))
+
+
+@pytest.mark.gpu
+def test_edge_kernel_events(T):
+    """The events given to taps_set_edge_kernel_events bracket the edge-table
+    kernel inside the edge call, and are used once."""
+    import torch
+    w = W.config(2)
+    cl = w.clusters[0][1]
+    tabs = T.build_tables(w.graph, cl)
+    stream = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    for e in ev:
+        e.record(stream)
+    torch.cuda.synchronize()
+    ev[0].record(stream)
+    T.taps_set_edge_kernel_events(ev[2], ev[3])
+    T.taps_edge_costs(w.graph, cl, tabs.strategies, tabs.op_offsets, out=tabs.edge, stream=stream)
+    ev[1].record(stream)
+    torch.cuda.synchronize()
+    call_ms, kernel_ms = ev[0].elapsed_time(ev[1]), ev[2].elapsed_time(ev[3])
+    assert 0.0 < kernel_ms <= call_ms
+    # used once: a second call leaves the kernel events where they were
+    T.taps_edge_costs(w.graph, cl, tabs.strategies, tabs.op_offsets, out=tabs.edge, stream=stream)
+    torch.cuda.synchronize()
+    assert ev[2].elapsed_time(ev[3]) == kernel_ms
