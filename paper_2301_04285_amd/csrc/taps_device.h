@@ -529,7 +529,10 @@ __host__ __device__ inline uint32_t taps_slice(const taps_lv &L, taps_state &s) 
 //     sliced (a held axis with a free target has already moved), so the
 //     next inner loop does nothing: such gathers run back to back, lowest
 //     position first, unless the last AllToAlls left a slice pending, in
-//     which case only the first runs before it.
+//     which case only the first runs before it;
+//   * once no axis is held at a producer position only slices remain (no
+//     held axis blocks a target), and slices cost nothing: the sequence's
+//     cost is final there.
 __host__ __device__ inline taps_run taps_alg1(const taps_row &P, const taps_col &Q,
                                               const taps_lv &L) {
     taps_fac c;
@@ -562,7 +565,8 @@ __host__ __device__ inline taps_run taps_alg1(const taps_row &P, const taps_col 
             taps_a2a_batch(c, moved, L, P.lam, s.e, s.unused);
         }
         if (sl) taps_slice(L, s);
-        if (s.ats == 0 && s.atd == L.dst) break;
+        // nothing held at a producer position: only slices remain, and they cost nothing
+        if (s.ats == 0) break;
         // InferAllGather / AllGatherFirstUndoneDim
         uint32_t ug = s.ats & ~L.tgtsrc;
         if (ug) {
@@ -573,11 +577,12 @@ __host__ __device__ inline taps_run taps_alg1(const taps_row &P, const taps_col 
                 x &= x - 1u;
                 taps_gather(P, L, s, c, top);
             }
-        } else if (s.ats) {
+        } else {
             const uint32_t top = taps_first_src(P, s.ats);
             s.blk &= ~taps_blocked(P, Q, L, 1u << top);
             taps_gather(P, L, s, c, top);
         }
+        if (s.ats == 0) break;
     }
     taps_run r;
     r.c = c;

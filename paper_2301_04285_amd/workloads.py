@@ -256,6 +256,13 @@ def mlp_stack(layers: int = 64, batch: int = 1024, dtype_bytes: int = 2,
     return g
 
 
+def leading_ops(graph: Graph, n_ops: int) -> Graph:
+    """The first `n_ops` operators of a graph and the edges among them (one transformer
+    layer of `gpt` is its first 14 operators)."""
+    return Graph(list(graph.ops[:n_ops]),
+                 [e for e in graph.edges if e.src < n_ops and e.dst < n_ops])
+
+
 # --------------------------------------------------------------------------
 # The five measured configurations
 # --------------------------------------------------------------------------

@@ -280,3 +280,23 @@ def test_edge_kernel_events(T):
     T.taps_edge_costs(w.graph, cl, tabs.strategies, tabs.op_offsets, out=tabs.edge, stream=stream)
     torch.cuda.synchronize()
     assert ev[2].elapsed_time(ev[3]) == kernel_ms
+
+
+@pytest.mark.gpu
+def test_search_on_gpu_tables_matches_oracle_tables(T, oracle_lib):
+    """The host search reaches the same optima on the library's tables as on the
+    oracle's (configuration 1 and one GPT layer on 2 x 8 devices)."""
+    import torch
+    from paper_2301_04285_amd import search as S
+    cases = [(W.config(1).graph, W.config(1).clusters[0][1]),
+             (W.leading_ops(W.config(2).graph, 14), W.config(2).clusters[0][1])]
+    for g, cl in cases:
+        tabs = T.build_tables(g, cl)
+        torch.cuda.synchronize()
+        ref = oracle_lib.build_tables(g, cl)
+        for f in ("t", "vol"):
+            node, edge = S.host_tables(g, tabs, f)
+            rnode = [np.asarray(v[f], np.float64) for v in ref.node]
+            redge = [np.asarray(m[f], np.float64) for m in ref.edge]
+            a, b = S.solve(g, node, edge), S.solve(g, rnode, redge)
+            assert abs(a.objective - b.objective) <= 1e-9 * abs(b.objective)
