@@ -13,7 +13,10 @@ Prints one JSON line.  `value` is edge entries per second of whole steps;
 with HIP events the library records right around its launch on the same
 stream, to MI355X's 8 TB/s HBM: each entry writes 36 bytes (t 8, vol 8,
 intra 8, inter 8, meta 4).  `cpu_baseline` times the CPU oracle, single-threaded, on the
-first layers of the same graph.  `roofline.traffic` is the edge kernel's HBM
+first layers of the same graph.  `shared_tables` times the same build with
+identical edge tables computed once (the paper searches one layer of a stack
+of identical layers) and checks the result equal to the full evaluation;
+`value` and `roofline` always come from the full evaluation.  `roofline.traffic` is the edge kernel's HBM
 bytes per launch from the committed rocprofv3 counter summary (null once the
 kernel sources differ from the ones the counters were taken with).
 """
@@ -94,6 +97,9 @@ def main() -> int:
     ap.add_argument("--config", type=int, default=5, help="workload 1..5 (default: 5, the largest)")
     ap.add_argument("--cpu-layers", type=int, default=3,
                     help="layers of the graph the CPU oracle baseline covers (0 = skip)")
+    ap.add_argument("--shared", type=int, default=1,
+                    help="also time taps_edge_costs_shared (identical tables computed once) "
+                         "and report it under shared_tables (0 = skip)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES bytes (to scale HBM "
                          "traffic counters), then exit")
@@ -132,37 +138,39 @@ def main() -> int:
     strategies = int(tabs.op_offsets[-1])
     log(f"[bench] {strategies} strategies, {entries} edge entries")
 
-    def step(ev=None):
+    def step(ev=None, shared=False, edge_out=None):
         offs, strat = taps.taps_enumerate_strategies(g, cl, stream=stream, out=tabs.strategies)
         taps.taps_node_costs(g, cl, strat, offs, out=tabs.node, stream=stream)
         if ev is not None:
             ev[0].record(stream)
             taps.taps_set_edge_kernel_events(ev[2], ev[3])
-        taps.taps_edge_costs(g, cl, strat, offs, out=tabs.edge, stream=stream)
+        taps.taps_edge_costs(g, cl, strat, offs, out=edge_out or tabs.edge, stream=stream,
+                             shared=shared)
         if ev is not None:
             ev[1].record(stream)
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    log(f"[bench] warmup {args.warmup} done")
+    def timed(shared=False, edge_out=None):
+        for _ in range(args.warmup):
+            step(shared=shared, edge_out=edge_out)
+        torch.cuda.synchronize()
+        # per step: the whole edge call, and the edge-table kernel alone (recorded by
+        # the library on the same stream right around that launch)
+        events = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(4))
+                  for _ in range(args.steps)]
+        for ev in events:
+            for e in ev:
+                e.record(stream)   # creates the event before the library records it again
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for k in range(args.steps):
+            step(events[k], shared=shared, edge_out=edge_out)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        edge_ms = float(np.mean([ev[0].elapsed_time(ev[1]) for ev in events]))
+        kernel_ms = float(np.mean([ev[2].elapsed_time(ev[3]) for ev in events]))
+        return wall * 1e3 / args.steps, edge_ms, kernel_ms
 
-    # per step: the whole edge call, and the edge-table kernel alone (recorded by the
-    # library on the same stream right around that launch)
-    events = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(4))
-              for _ in range(args.steps)]
-    for ev in events:
-        for e in ev:
-            e.record(stream)   # creates the event before the library records it again
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for k in range(args.steps):
-        step(events[k])
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    edge_ms = float(np.mean([ev[0].elapsed_time(ev[1]) for ev in events]))
-    kernel_ms = float(np.mean([ev[2].elapsed_time(ev[3]) for ev in events]))
-    ms_per_step = wall * 1e3 / args.steps
+    ms_per_step, edge_ms, kernel_ms = timed()
     log(f"[bench] {args.steps} steps: {ms_per_step:.3f} ms/step, edge call {edge_ms:.3f} ms, "
         f"edge kernel {kernel_ms:.3f} ms")
 
@@ -193,6 +201,21 @@ def main() -> int:
                      "frac": achieved / HBM_PEAK_GBPS,
                      "traffic": measured_traffic() if args.config == 5 else None},
     }
+    if args.shared:
+        # identical edge tables computed once (taps_edge_costs_shared), into a second
+        # set of tables, checked equal to the full evaluation
+        other = taps.alloc_table(entries, device="cuda")
+        s_step, s_edge, s_kernel = timed(shared=True, edge_out=other)
+        equal = all(torch.equal(tabs.edge[f][:entries], other[f][:entries])
+                    for f in ("t", "vol", "intra", "inter", "meta"))
+        log(f"[bench] shared tables: {s_step:.3f} ms/step, edge call {s_edge:.3f} ms, "
+            f"edge kernel {s_kernel:.3f} ms, equal to the full evaluation: {equal}")
+        out["shared_tables"] = {
+            "ms_per_step": s_step, "edge_call_ms": s_edge, "edge_kernel_ms": s_kernel,
+            "edge_entries_per_s": entries / (s_step * 1e-3),
+            "hbm_write_frac": bytes_per_launch / (s_kernel * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+            "equal_to_full_evaluation": equal}
+        del other
     if args.cpu_layers > 0 and args.config == 5:
         log(f"[bench] CPU oracle baseline on {args.cpu_layers} layers")
         out["cpu_baseline"] = cpu_baseline(w, cl, args.cpu_layers)

@@ -190,11 +190,29 @@ taps_status taps_edge_costs(const taps_graph *graph, const taps_cluster *cluster
                             uint64_t *edge_offsets, taps_table out, uint64_t capacity,
                             void *stream);
 
+/* The same tables as taps_edge_costs, written with each distinct table
+ * computed once.  Edges with the same producer (axes, lengths, partitionable
+ * axes, element size, output tensor) and the same consumer (axes, lengths,
+ * partitionable axes, the input tensor the edge feeds) have the same table
+ * whenever their operators' strategy ranges are equal -- which holds for the
+ * strategies taps_enumerate_strategies writes and is checked on the device
+ * for any others.  The paper relies on the same fact when it searches one
+ * layer of a stack of identical transformer layers (searching runtime
+ * subsection).  Each group's first edge is computed and every other member's
+ * range is copied from it.  Unlike taps_edge_costs this call synchronises the
+ * stream once (to read back the strategy comparison) when some edges share.
+ * Arguments, layout and errors as taps_edge_costs. */
+taps_status taps_edge_costs_shared(const taps_graph *graph, const taps_cluster *cluster,
+                                   const taps_strategy *strategies, const uint64_t *op_offsets,
+                                   uint64_t *edge_offsets, taps_table out, uint64_t capacity,
+                                   void *stream);
+
 /* Profiling aid, not part of the method: `before` and `after` are HIP events
  * (hipEvent_t, created by the caller, passed as plain pointers) that the
- * calling thread's next taps_edge_costs call that launches the edge-table
- * kernel records on its stream immediately before and after that kernel, so
- * that the caller can time the kernel alone.  The setting is thread-local,
+ * calling thread's next taps_edge_costs or taps_edge_costs_shared call that
+ * launches the edge-table kernel records on its stream immediately before and
+ * after that kernel (and, for shared tables, the copies after it), so that
+ * the caller can time the kernel alone.  The setting is thread-local,
  * used once and then cleared; two NULLs clear it.  The events stay owned by
  * the caller.  TAPS_ERR_ARG if exactly one of them is NULL. */
 taps_status taps_set_edge_kernel_events(void *before, void *after);

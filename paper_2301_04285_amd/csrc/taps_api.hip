@@ -9,6 +9,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <map>
 #include <mutex>
 #include <numeric>
 #include <string>
@@ -243,6 +244,190 @@ struct scratch {
     void adopt(void *p) { ptrs.push_back(p); }
 };
 
+// Edges whose tables are identical: the same producer description (axes,
+// lengths, partitionable axes, element size, output tensor), the same
+// consumer description (axes, lengths, partitionable axes, the input tensor
+// the edge feeds) -- and, checked on the device, the same strategies.
+std::vector<int64_t> edge_key(const taps_graph *g, uint32_t e) {
+    const taps_edge &E = g->edges[e];
+    const taps_op &s = g->ops[E.src_op], &d = g->ops[E.dst_op];
+    std::vector<int64_t> k{s.n_axes, s.part_mask, s.dtype_bytes, s.out.rank,
+                           d.n_axes, d.part_mask, d.in[E.dst_slot].rank};
+    for (uint32_t a = 0; a < s.n_axes; ++a) k.push_back(s.axis_len[a]);
+    for (uint32_t a = 0; a < d.n_axes; ++a) k.push_back(d.axis_len[a]);
+    for (uint32_t r = 0; r < s.out.rank; ++r) k.push_back(s.out.axis[r]);
+    for (uint32_t r = 0; r < d.in[E.dst_slot].rank; ++r) k.push_back(d.in[E.dst_slot].axis[r]);
+    return k;
+}
+
+// rep[e]: the edge whose table edge e shares (itself if none).  One
+// synchronisation reads back the device comparison of strategy ranges.
+taps_status share_edges(const taps_graph *g, const uint64_t *op_offsets,
+                        const taps_strategy *strategies, hipStream_t stream,
+                        std::vector<uint32_t> &rep) {
+    const uint32_t n_edges = g->n_edges;
+    std::map<std::vector<int64_t>, uint32_t> first;
+    std::map<std::pair<uint32_t, uint32_t>, uint32_t> pair_index;   // (op, rep op) -> pair
+    std::vector<uint64_t> pairs;
+    auto count = [&](uint32_t op) { return op_offsets[op + 1] - op_offsets[op]; };
+    auto want = [&](uint32_t a, uint32_t b) -> int64_t {   // pair index, -1 if counts differ
+        if (a == b) return -2;
+        if (count(a) != count(b)) return -1;
+        auto it = pair_index.find({a, b});
+        if (it != pair_index.end()) return it->second;
+        const uint32_t k = (uint32_t)(pairs.size() / 3);
+        pairs.insert(pairs.end(), {op_offsets[a], op_offsets[b], count(a)});
+        pair_index[{a, b}] = k;
+        return k;
+    };
+    std::vector<int64_t> src_pair(n_edges, -2), dst_pair(n_edges, -2);
+    for (uint32_t e = 0; e < n_edges; ++e) {
+        auto it = first.emplace(edge_key(g, e), e).first;
+        rep[e] = it->second;
+        if (rep[e] == e) continue;
+        const taps_edge &E = g->edges[e], &R = g->edges[rep[e]];
+        src_pair[e] = want(E.src_op, R.src_op);
+        dst_pair[e] = want(E.dst_op, R.dst_op);
+    }
+    std::vector<uint32_t> flags(pairs.size() / 3, 0);
+    if (!flags.empty()) {
+        scratch sc(stream);
+        uint64_t *d_pairs = nullptr;
+        uint32_t *d_flags = nullptr;
+        taps_status st;
+        if ((st = sc.alloc((void **)&d_pairs, sizeof(uint64_t) * pairs.size())) != TAPS_OK) return st;
+        if ((st = sc.alloc((void **)&d_flags, sizeof(uint32_t) * flags.size())) != TAPS_OK) return st;
+        hipError_t err = hipMemcpyAsync(d_pairs, pairs.data(), sizeof(uint64_t) * pairs.size(),
+                                        hipMemcpyHostToDevice, stream);
+        if (err == hipSuccess)
+            err = taps_launch_same_ranges(strategies, d_pairs, (uint32_t)flags.size(), d_flags,
+                                          stream);
+        if (err == hipSuccess)
+            err = hipMemcpyAsync(flags.data(), d_flags, sizeof(uint32_t) * flags.size(),
+                                 hipMemcpyDeviceToHost, stream);
+        if (err == hipSuccess) err = hipStreamSynchronize(stream);
+        if (err != hipSuccess) return hip_fail(err, "strategy comparison");
+    }
+    auto same = [&](int64_t p) { return p == -2 || (p >= 0 && flags[p] == 0); };
+    for (uint32_t e = 0; e < n_edges; ++e)
+        if (rep[e] != e && !(same(src_pair[e]) && same(dst_pair[e]))) rep[e] = e;
+    return TAPS_OK;
+}
+
+taps_status edge_costs(const taps_graph *graph, const taps_cluster *cluster,
+                       const taps_strategy *strategies, const uint64_t *op_offsets,
+                       uint64_t *edge_offsets, taps_table out, uint64_t capacity, void *stream_,
+                       bool share) {
+    g_last_error.clear();
+    taps_launch lp;
+    taps_status st = check_cluster(cluster, &lp);
+    if (st == TAPS_OK) st = check_graph(graph, true);
+    if (st == TAPS_OK) st = check_offsets(graph, op_offsets);
+    if (st != TAPS_OK) return st;
+    if (!edge_offsets) return fail(TAPS_ERR_ARG, "edge_offsets is NULL");
+    const uint32_t n_ops = graph->n_ops, n_edges = graph->n_edges;
+    std::vector<uint64_t> eoff(n_edges + 1, 0);
+    uint64_t all_segs = 0;   // row segments without sharing (an upper bound)
+    for (uint32_t e = 0; e < n_edges; ++e) {
+        const taps_edge &E = graph->edges[e];
+        const uint64_t ns = op_offsets[E.src_op + 1] - op_offsets[E.src_op];
+        const uint64_t nd = op_offsets[E.dst_op + 1] - op_offsets[E.dst_op];
+        eoff[e + 1] = eoff[e] + ns * nd;
+        all_segs += ns * ((nd + TAPS_TILE_COLS * TAPS_SEG_TILES - 1) /
+                          (TAPS_TILE_COLS * TAPS_SEG_TILES));
+    }
+    const bool none = !out.t && !out.vol && !out.intra && !out.inter && !out.meta;
+    const bool all = out.t && out.vol && out.intra && out.inter && out.meta;
+    if (!none && !all) return fail(TAPS_ERR_ARG, "table arrays must be all set or all NULL");
+    if (all && eoff[n_edges] > capacity)
+        return fail(TAPS_ERR_CAPACITY, "%llu entries, capacity %llu",
+                    (unsigned long long)eoff[n_edges], (unsigned long long)capacity);
+    if (all && eoff[n_edges] > 0 && !strategies) return fail(TAPS_ERR_ARG, "strategies is NULL");
+    if (all_segs >= 0x7FFFFFFFull) return fail(TAPS_ERR_ARG, "more than 2^31 row segments");
+    std::memcpy(edge_offsets, eoff.data(), sizeof(uint64_t) * (n_edges + 1));
+    if (none || eoff[n_edges] == 0) return TAPS_OK;
+    hipStream_t stream = (hipStream_t)stream_;
+    // shared tables: every group computes its representative's rows once
+    std::vector<uint32_t> rep(n_edges);
+    std::iota(rep.begin(), rep.end(), 0u);
+    if (share && (st = share_edges(graph, op_offsets, strategies, stream, rep)) != TAPS_OK)
+        return st;
+    // row segments of every computed table (shared tables: the first of each group)
+    std::vector<uint64_t> segs(n_edges + 1, 0);
+    for (uint32_t e = 0; e < n_edges; ++e) {
+        const taps_edge &E = graph->edges[e];
+        const uint64_t ns = op_offsets[E.src_op + 1] - op_offsets[E.src_op];
+        const uint64_t nd = op_offsets[E.dst_op + 1] - op_offsets[E.dst_op];
+        const uint64_t per_row = (nd + TAPS_TILE_COLS * TAPS_SEG_TILES - 1) /
+                                 (TAPS_TILE_COLS * TAPS_SEG_TILES);
+        segs[e + 1] = segs[e] + (rep[e] == e ? ns * per_row : 0);
+    }
+    // shared tables: every chunk of a computed table is stored into each table sharing it
+    std::vector<uint64_t> dst_list;
+    std::vector<taps_copy_task> copies;
+    {
+        std::vector<std::vector<uint32_t>> members(n_edges);
+        for (uint32_t e = 0; e < n_edges; ++e)
+            if (rep[e] != e) members[rep[e]].push_back(e);
+        for (uint32_t r = 0; r < n_edges; ++r) {
+            if (members[r].empty()) continue;
+            const uint32_t begin = (uint32_t)dst_list.size();
+            for (uint32_t m : members[r]) dst_list.push_back(eoff[m]);
+            const uint64_t size = eoff[r + 1] - eoff[r];
+            const uint32_t n_dst = (uint32_t)members[r].size();
+            for (uint64_t k = 0; k < size; k += TAPS_COPY_CHUNK)
+                for (uint32_t m = 0; m < n_dst; m += TAPS_COPY_DSTS) {
+                    taps_copy_task c;
+                    c.src = eoff[r] + k;
+                    c.offset = k;
+                    c.count = (uint32_t)(size - k < TAPS_COPY_CHUNK ? size - k : TAPS_COPY_CHUNK);
+                    c.dst_begin = begin + m;
+                    c.n_dst = n_dst - m < TAPS_COPY_DSTS ? n_dst - m : TAPS_COPY_DSTS;
+                    c.pad = 0;
+                    copies.push_back(c);
+                }
+        }
+    }
+    if (copies.size() > 0x7FFFFFFFull) return fail(TAPS_ERR_ARG, "too many table copies");
+    scratch sc(stream);
+    const uint64_t total = op_offsets[n_ops];
+    const uint64_t n_segs = segs[n_edges];
+    std::vector<chunk> ch{{graph->ops, sizeof(taps_op) * n_ops, 0},
+                          {graph->edges, sizeof(taps_edge) * n_edges, 0},
+                          {op_offsets, sizeof(uint64_t) * (n_ops + 1), 0},
+                          {eoff.data(), sizeof(uint64_t) * (n_edges + 1), 0},
+                          {segs.data(), sizeof(uint64_t) * (n_edges + 1), 0},
+                          {copies.data(), sizeof(taps_copy_task) * copies.size(), 0},
+                          {dst_list.data(), sizeof(uint64_t) * dst_list.size(), 0}};
+    void *dev = nullptr;
+    if ((st = upload(ch, &dev, stream)) != TAPS_OK) return st;
+    sc.adopt(dev);
+    taps_desc *d_desc = nullptr;
+    taps_edge_params *d_params = nullptr;
+    taps_row_ref *d_segs = nullptr;
+    if ((st = sc.alloc((void **)&d_desc, sizeof(taps_desc) * total)) != TAPS_OK) return st;
+    if ((st = sc.alloc((void **)&d_params, sizeof(taps_edge_params) * n_edges)) != TAPS_OK) return st;
+    if ((st = sc.alloc((void **)&d_segs, sizeof(taps_row_ref) * n_segs)) != TAPS_OK) return st;
+    hipError_t err = taps_launch_describe(strategies, total, d_desc, stream);
+    if (err == hipSuccess)
+        err = taps_launch_edge_setup(at<taps_op>(dev, ch[0]), at<taps_edge>(dev, ch[1]), n_edges,
+                                     at<uint64_t>(dev, ch[2]), at<uint64_t>(dev, ch[3]),
+                                     at<uint64_t>(dev, ch[4]), lp, d_params, n_segs, d_segs,
+                                     stream);
+    // the edge-table kernel launches (entries > 0): use the events, if any, once
+    const hipEvent_t before = g_kernel_before, after = g_kernel_after;
+    g_kernel_before = g_kernel_after = nullptr;
+    if (err == hipSuccess && before) err = hipEventRecord(before, stream);
+    if (err == hipSuccess)
+        err = taps_launch_edge_costs(d_params, d_segs, n_segs, d_desc, lp, out, stream);
+    if (err == hipSuccess)
+        err = taps_launch_copy_tables(at<taps_copy_task>(dev, ch[5]), (uint32_t)copies.size(),
+                                      at<uint64_t>(dev, ch[6]), out, stream);
+    if (err == hipSuccess && after) err = hipEventRecord(after, stream);
+    if (err != hipSuccess) return hip_fail(err, "edge costs");
+    return TAPS_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -387,67 +572,17 @@ taps_status taps_node_costs(const taps_graph *graph, const taps_cluster *cluster
 taps_status taps_edge_costs(const taps_graph *graph, const taps_cluster *cluster,
                             const taps_strategy *strategies, const uint64_t *op_offsets,
                             uint64_t *edge_offsets, taps_table out, uint64_t capacity,
-                            void *stream_) {
-    g_last_error.clear();
-    taps_launch lp;
-    taps_status st = check_cluster(cluster, &lp);
-    if (st == TAPS_OK) st = check_graph(graph, true);
-    if (st == TAPS_OK) st = check_offsets(graph, op_offsets);
-    if (st != TAPS_OK) return st;
-    if (!edge_offsets) return fail(TAPS_ERR_ARG, "edge_offsets is NULL");
-    const uint32_t n_ops = graph->n_ops, n_edges = graph->n_edges;
-    std::vector<uint64_t> eoff(n_edges + 1, 0), rows(n_edges + 1, 0);
-    for (uint32_t e = 0; e < n_edges; ++e) {
-        const taps_edge &E = graph->edges[e];
-        const uint64_t ns = op_offsets[E.src_op + 1] - op_offsets[E.src_op];
-        const uint64_t nd = op_offsets[E.dst_op + 1] - op_offsets[E.dst_op];
-        eoff[e + 1] = eoff[e] + ns * nd;
-        rows[e + 1] = rows[e] + ns;
-    }
-    const bool none = !out.t && !out.vol && !out.intra && !out.inter && !out.meta;
-    const bool all = out.t && out.vol && out.intra && out.inter && out.meta;
-    if (!none && !all) return fail(TAPS_ERR_ARG, "table arrays must be all set or all NULL");
-    if (all && eoff[n_edges] > capacity)
-        return fail(TAPS_ERR_CAPACITY, "%llu entries, capacity %llu",
-                    (unsigned long long)eoff[n_edges], (unsigned long long)capacity);
-    if (all && eoff[n_edges] > 0 && !strategies) return fail(TAPS_ERR_ARG, "strategies is NULL");
-    if (rows[n_edges] >= 0x7FFFFFFFull)
-        return fail(TAPS_ERR_ARG, "more than 2^31 table rows");
-    std::memcpy(edge_offsets, eoff.data(), sizeof(uint64_t) * (n_edges + 1));
-    if (none || eoff[n_edges] == 0) return TAPS_OK;
-    hipStream_t stream = (hipStream_t)stream_;
-    scratch sc(stream);
-    const uint64_t total = op_offsets[n_ops];
-    const uint64_t n_rows = rows[n_edges];
-    std::vector<chunk> ch{{graph->ops, sizeof(taps_op) * n_ops, 0},
-                          {graph->edges, sizeof(taps_edge) * n_edges, 0},
-                          {op_offsets, sizeof(uint64_t) * (n_ops + 1), 0},
-                          {eoff.data(), sizeof(uint64_t) * (n_edges + 1), 0},
-                          {rows.data(), sizeof(uint64_t) * (n_edges + 1), 0}};
-    void *dev = nullptr;
-    if ((st = upload(ch, &dev, stream)) != TAPS_OK) return st;
-    sc.adopt(dev);
-    taps_desc *d_desc = nullptr;
-    taps_edge_params *d_params = nullptr;
-    taps_row_ref *d_rows = nullptr;
-    if ((st = sc.alloc((void **)&d_desc, sizeof(taps_desc) * total)) != TAPS_OK) return st;
-    if ((st = sc.alloc((void **)&d_params, sizeof(taps_edge_params) * n_edges)) != TAPS_OK) return st;
-    if ((st = sc.alloc((void **)&d_rows, sizeof(taps_row_ref) * n_rows)) != TAPS_OK) return st;
-    hipError_t err = taps_launch_describe(strategies, total, d_desc, stream);
-    if (err == hipSuccess)
-        err = taps_launch_edge_setup(at<taps_op>(dev, ch[0]), at<taps_edge>(dev, ch[1]), n_edges,
-                                     at<uint64_t>(dev, ch[2]), at<uint64_t>(dev, ch[3]),
-                                     at<uint64_t>(dev, ch[4]), lp, d_params, n_rows, d_rows,
-                                     stream);
-    // the edge-table kernel launches (entries > 0): use the events, if any, once
-    const hipEvent_t before = g_kernel_before, after = g_kernel_after;
-    g_kernel_before = g_kernel_after = nullptr;
-    if (err == hipSuccess && before) err = hipEventRecord(before, stream);
-    if (err == hipSuccess)
-        err = taps_launch_edge_costs(d_params, d_rows, n_rows, d_desc, lp, out, stream);
-    if (err == hipSuccess && after) err = hipEventRecord(after, stream);
-    if (err != hipSuccess) return hip_fail(err, "edge costs");
-    return TAPS_OK;
+                            void *stream) {
+    return edge_costs(graph, cluster, strategies, op_offsets, edge_offsets, out, capacity, stream,
+                      false);
+}
+
+taps_status taps_edge_costs_shared(const taps_graph *graph, const taps_cluster *cluster,
+                                   const taps_strategy *strategies, const uint64_t *op_offsets,
+                                   uint64_t *edge_offsets, taps_table out, uint64_t capacity,
+                                   void *stream) {
+    return edge_costs(graph, cluster, strategies, op_offsets, edge_offsets, out, capacity, stream,
+                      true);
 }
 
 }  // extern "C"

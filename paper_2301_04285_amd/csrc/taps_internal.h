@@ -21,7 +21,7 @@ struct taps_launch {
 // Per-edge constants of the edge-table kernel.
 struct taps_edge_params {
     uint64_t out_offset;   // first entry of the edge's table
-    uint64_t row_begin;    // first table row of the edge (rows of all edges, in order)
+    uint64_t seg_begin;    // first row segment of the edge (segments of all edges, in order)
     taps_scaler scale;     // tbytes and the per-unit seconds of the edge tensor
     uint32_t src_base;     // first strategy of the producer
     uint32_t dst_base;     // first strategy of the consumer
@@ -32,17 +32,30 @@ struct taps_edge_params {
     uint32_t pad;
 };
 
-// One wavefront per table row (producer strategy i of one edge); it walks
-// the row's consumer strategies 64 at a time.  A workgroup holds
-// TAPS_ROWS_PER_BLOCK rows.
+// Shared tables: entries [src, src + count) of every array are copied to
+// [dst[k] + offset, dst[k] + offset + count) for the n_dst table starts
+// dst[k] = dst_list[dst_begin + k].
+struct taps_copy_task {
+    uint64_t src, offset;
+    uint32_t count, dst_begin, n_dst, pad;
+};
+#define TAPS_COPY_CHUNK 2048    // entries per copy task (8 per thread of 256)
+#define TAPS_COPY_DSTS 16       // tables one copy task writes
+
+// One wavefront per row segment: producer strategy i of one edge and up to
+// TAPS_SEG_TILES tiles of 64 consecutive consumer strategies, walked 64 at a
+// time.  A workgroup holds TAPS_ROWS_PER_BLOCK segments.
 #define TAPS_TILE_COLS 64
+#define TAPS_SEG_TILES 4
 #define TAPS_ROWS_PER_BLOCK 4
 
-// Row r of the flat row list: its edge and the global index of its producer
-// strategy.
+// Segment r of the flat segment list: its edge, the global index of its
+// producer strategy and its first consumer strategy.
 struct taps_row_ref {
     uint32_t edge;
     uint32_t strategy;
+    uint32_t first_col;
+    uint32_t pad;
 };
 
 #define TAPS_ENUM_CHUNK 64   // candidates per enumeration wavefront
@@ -58,9 +71,16 @@ hipError_t taps_launch_node_costs(const taps_op *ops, uint32_t n_ops, const uint
                                   taps_table out, hipStream_t stream);
 hipError_t taps_launch_edge_setup(const taps_op *ops, const taps_edge *edges, uint32_t n_edges,
                                   const uint64_t *op_offsets, const uint64_t *edge_offsets,
-                                  const uint64_t *row_begin, const taps_launch &lp,
-                                  taps_edge_params *params, uint64_t n_rows, taps_row_ref *rows,
+                                  const uint64_t *seg_begin, const taps_launch &lp,
+                                  taps_edge_params *params, uint64_t n_segs, taps_row_ref *segs,
                                   hipStream_t stream);
 hipError_t taps_launch_edge_costs(const taps_edge_params *params, const taps_row_ref *rows,
                                   uint64_t n_rows, const taps_desc *desc, const taps_launch &lp,
                                   taps_table out, hipStream_t stream);
+hipError_t taps_launch_copy_tables(const taps_copy_task *tasks, uint32_t n_tasks,
+                                   const uint64_t *dst_list, taps_table out, hipStream_t stream);
+// For each pair p: flags[p] = 0 if strategies[first_a .. +count) equals
+// strategies[first_b .. +count), else 1.  pairs: (first_a, first_b, count) as
+// three uint64 each.
+hipError_t taps_launch_same_ranges(const taps_strategy *strategies, const uint64_t *pairs,
+                                   uint32_t n_pairs, uint32_t *flags, hipStream_t stream);

@@ -5,12 +5,15 @@
 //   k_describe    one thread per strategy: level runs, owners and cuts
 //   k_node_costs  one thread per strategy: the intra-op AllReduces
 //   k_edge_setup  one thread per edge: per-edge constants
-//   k_row_map     one thread per table row: its edge and producer strategy
-//   k_edge_costs  one wavefront per table row (producer strategy, uniform:
-//                 its descriptor sits in scalar registers), four rows per
-//                 workgroup, walking the row's consumer strategies 64 at a
-//                 time (one per lane, the next 64 prefetched); five
+//   k_row_map     one thread per row segment: its edge, producer strategy
+//                 and first consumer strategy
+//   k_edge_costs  one wavefront per row segment (one producer strategy,
+//                 uniform: its descriptor sits in scalar registers; up to
+//                 four tiles of 64 consumer strategies, one per lane, the
+//                 next 64 prefetched), four segments per workgroup; five
 //                 coalesced non-temporal SoA stores per entry
+//   k_copy_tables shared tables: one workgroup per chunk of a computed
+//                 table, written to every table that shares it
 #include "taps_internal.h"
 
 namespace {
@@ -24,6 +27,19 @@ __constant__ taps_completion_table kCompletions = taps_make_completions();
 template <typename T>
 __device__ inline T *at_byte(T *base, uint32_t offset) {
     return (T *)((char *)base + offset);
+}
+
+// Entry j of a row whose records start at `row` (uniform): 32-bit byte offsets
+// from the uniform row bases, j < 2^21 (8 axes on 8 levels give at most
+// 1,047,376 strategies per operator); five non-temporal stores.
+__device__ inline void store_entry(const taps_table &out, uint64_t row, uint32_t j,
+                                   const taps_entry_out &o, uint32_t meta) {
+    const uint32_t o8 = j * 8u, o4 = j * 4u;
+    __builtin_nontemporal_store(o.t, at_byte(out.t + row, o8));
+    __builtin_nontemporal_store(o.vol, at_byte(out.vol + row, o8));
+    __builtin_nontemporal_store(o.intra, at_byte(out.intra + row, o8));
+    __builtin_nontemporal_store(o.inter, at_byte(out.inter + row, o8));
+    __builtin_nontemporal_store(meta, at_byte(out.meta + row, o4));
 }
 
 __device__ inline uint32_t lanes_below(uint64_t mask) {
@@ -136,7 +152,7 @@ __global__ __launch_bounds__(256) void k_edge_setup(const taps_op *__restrict__ 
                                                     uint32_t n_edges,
                                                     const uint64_t *__restrict__ op_offsets,
                                                     const uint64_t *__restrict__ edge_offsets,
-                                                    const uint64_t *__restrict__ row_begin,
+                                                    const uint64_t *__restrict__ seg_begin,
                                                     taps_launch lp,
                                                     taps_edge_params *__restrict__ params) {
     const uint32_t e = blockIdx.x * blockDim.x + threadIdx.x;
@@ -148,7 +164,7 @@ __global__ __launch_bounds__(256) void k_edge_setup(const taps_op *__restrict__ 
     const taps_tensor &Tc = dst.in[E.dst_slot];
     taps_edge_params p;
     p.out_offset = edge_offsets[e];
-    p.row_begin = row_begin[e];
+    p.seg_begin = seg_begin[e];
     uint64_t bytes = src.dtype_bytes;
     uint32_t pa = 0, ca = 0;
     for (uint32_t d = 0; d < T.rank && d < TAPS_MAX_RANK; ++d) {
@@ -168,28 +184,34 @@ __global__ __launch_bounds__(256) void k_edge_setup(const taps_op *__restrict__ 
     params[e] = p;
 }
 
-__global__ __launch_bounds__(256) void k_row_map(const uint64_t *__restrict__ row_begin,
+__global__ __launch_bounds__(256) void k_row_map(const uint64_t *__restrict__ seg_begin,
                                                  const uint64_t *__restrict__ op_offsets,
                                                  const taps_edge *__restrict__ edges,
-                                                 uint32_t n_edges, uint64_t n_rows,
-                                                 taps_row_ref *__restrict__ rows) {
+                                                 const taps_edge_params *__restrict__ params,
+                                                 uint32_t n_edges, uint64_t n_segs,
+                                                 taps_row_ref *__restrict__ segs) {
     const uint64_t r = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (r >= n_rows) return;
-    const uint32_t e = find_owner(row_begin, n_edges, r);
+    if (r >= n_segs) return;
+    const uint32_t e = find_owner(seg_begin, n_edges, r);
+    const uint32_t nd = params[e].nd;
+    const uint64_t per_row = (nd + TAPS_TILE_COLS * TAPS_SEG_TILES - 1) / (TAPS_TILE_COLS * TAPS_SEG_TILES);
+    const uint64_t k = r - seg_begin[e];
     taps_row_ref ref;
     ref.edge = e;
-    ref.strategy = (uint32_t)(op_offsets[edges[e].src_op] + (r - row_begin[e]));
-    rows[r] = ref;
+    ref.strategy = (uint32_t)(op_offsets[edges[e].src_op] + k / per_row);
+    ref.first_col = (uint32_t)(k % per_row) * (TAPS_TILE_COLS * TAPS_SEG_TILES);
+    ref.pad = 0;
+    segs[r] = ref;
 }
 
 __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_costs(
     const taps_edge_params *__restrict__ params, const taps_row_ref *__restrict__ rows,
-    uint32_t n_rows, const taps_desc *__restrict__ desc, taps_launch lp, taps_table out) {
+    uint32_t n_segs, const taps_desc *__restrict__ desc, taps_launch lp, taps_table out) {
     __shared__ uint8_t rank_tab[TAPS_ROWS_PER_BLOCK][256];
     const uint32_t lane = threadIdx.x % TAPS_TILE_COLS;
     const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x / TAPS_TILE_COLS);
     const uint32_t r = blockIdx.x * TAPS_ROWS_PER_BLOCK + wave;
-    const bool live = r < n_rows;
+    const bool live = r < n_segs;
     const taps_row_ref ref = rows[live ? r : 0u];
     const taps_edge_params E = params[ref.edge];
     const taps_desc Dp = desc[ref.strategy];
@@ -206,33 +228,78 @@ __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_co
     K.narrow = lp.narrow != 0;
     // the row's records start here; lane j writes entry j
     const uint64_t row_out = E.out_offset + (uint64_t)i * E.nd;
-    double *const t_row = out.t + row_out;
-    uint64_t *const vol_row = out.vol + row_out;
-    uint64_t *const intra_row = out.intra + row_out;
-    uint64_t *const inter_row = out.inter + row_out;
-    uint32_t *const meta_row = out.meta + row_out;
     const taps_desc *col = desc + E.dst_base;
+    const uint32_t c0 = ref.first_col;
+    const uint32_t c1 = E.nd - c0 < TAPS_TILE_COLS * TAPS_SEG_TILES ? E.nd
+                                                                       : c0 + TAPS_TILE_COLS * TAPS_SEG_TILES;
     // consumer descriptors one tile ahead
-    taps_desc next = col[lane < E.nd ? lane : 0u];
-    for (uint32_t j0 = 0; j0 < E.nd; j0 += TAPS_TILE_COLS) {
+    taps_desc next = col[c0 + lane < c1 ? c0 + lane : c0];
+    for (uint32_t j0 = c0; j0 < c1; j0 += TAPS_TILE_COLS) {
         const taps_desc cur = next;
         const uint32_t j = j0 + lane;
         const uint32_t jn = j + TAPS_TILE_COLS;
-        if (jn < E.nd) next = col[jn];
-        if (j < E.nd) {
+        if (jn < c1) next = col[jn];
+        if (j < c1) {
             taps_col Q;
             taps_make_col(Q, cur, E.caxes, E.rank);
             const taps_entry_out o = taps_entry_finish(taps_edge_select(P, Q, K), E.scale);
-            // 32-bit byte offsets from the uniform row bases: j < 2^21 (8 axes on
-            // 8 levels give at most 1,047,376 strategies per operator)
-            const uint32_t o8 = j * 8u, o4 = j * 4u;
-            __builtin_nontemporal_store(o.t, at_byte(t_row, o8));
-            __builtin_nontemporal_store(o.vol, at_byte(vol_row, o8));
-            __builtin_nontemporal_store(o.intra, at_byte(intra_row, o8));
-            __builtin_nontemporal_store(o.inter, at_byte(inter_row, o8));
-            __builtin_nontemporal_store(o.ok ? o.meta : 0xFFFFFFFFu, at_byte(meta_row, o4));
+            store_entry(out, row_out, j, o, o.ok ? o.meta : 0xFFFFFFFFu);
         }
     }
+}
+
+// Shared tables: each task holds `count` (<= TAPS_COPY_CHUNK) consecutive
+// entries of a computed table, loaded once (8 per thread, consecutive
+// threads on consecutive entries) and stored into every table that shares it,
+// at the same offset; blockIdx.y picks the array.
+template <typename T>
+__device__ inline void copy_range(T *base, const taps_copy_task &c,
+                                  const uint64_t *__restrict__ dst_list) {
+    constexpr uint32_t kPer = TAPS_COPY_CHUNK / 256;
+    const T *s = base + c.src;
+    T v[kPer];
+#pragma unroll
+    for (uint32_t u = 0; u < kPer; ++u) {
+        const uint32_t x = threadIdx.x + u * 256u;
+        if (x < c.count) v[u] = s[x];
+    }
+    for (uint32_t k = 0; k < c.n_dst; ++k) {
+        T *d = base + dst_list[c.dst_begin + k] + c.offset;
+#pragma unroll
+        for (uint32_t u = 0; u < kPer; ++u) {
+            const uint32_t x = threadIdx.x + u * 256u;
+            if (x < c.count) d[x] = v[u];   // cached: L2 merges the partial lines at the ends
+        }
+    }
+}
+
+__global__ __launch_bounds__(256) void k_copy_tables(const taps_copy_task *__restrict__ tasks,
+                                                     const uint64_t *__restrict__ dst_list,
+                                                     taps_table out) {
+    const taps_copy_task c = tasks[blockIdx.x];
+    switch (blockIdx.y) {
+    case 0: copy_range(out.t, c, dst_list); break;
+    case 1: copy_range(out.vol, c, dst_list); break;
+    case 2: copy_range(out.intra, c, dst_list); break;
+    case 3: copy_range(out.inter, c, dst_list); break;
+    default: copy_range(out.meta, c, dst_list); break;
+    }
+}
+
+// One workgroup per pair of strategy ranges; flags[p] = any entry differs.
+__global__ __launch_bounds__(256) void k_same_ranges(const taps_strategy *__restrict__ s,
+                                                     const uint64_t *__restrict__ pairs,
+                                                     uint32_t *__restrict__ flags) {
+    const uint64_t a = pairs[3 * blockIdx.x], b = pairs[3 * blockIdx.x + 1];
+    const uint64_t count = pairs[3 * blockIdx.x + 2];
+    int differ = 0;
+    for (uint64_t k = threadIdx.x; k < count; k += blockDim.x) {
+        const taps_strategy x = s[a + k], y = s[b + k];
+        for (uint32_t q = 0; q < TAPS_MAX_AXES; ++q)
+            differ |= (x.log2_deg[q] != y.log2_deg[q]) | (x.pos[q] != y.pos[q]);
+    }
+    differ = __syncthreads_or(differ);
+    if (threadIdx.x == 0) flags[blockIdx.x] = differ ? 1u : 0u;
 }
 
 inline uint32_t blocks_for(uint64_t n, uint32_t per) { return (uint32_t)((n + per - 1) / per); }
@@ -268,25 +335,41 @@ hipError_t taps_launch_node_costs(const taps_op *ops, uint32_t n_ops, const uint
 
 hipError_t taps_launch_edge_setup(const taps_op *ops, const taps_edge *edges, uint32_t n_edges,
                                   const uint64_t *op_offsets, const uint64_t *edge_offsets,
-                                  const uint64_t *row_begin, const taps_launch &lp,
-                                  taps_edge_params *params, uint64_t n_rows, taps_row_ref *rows,
+                                  const uint64_t *seg_begin, const taps_launch &lp,
+                                  taps_edge_params *params, uint64_t n_segs, taps_row_ref *segs,
                                   hipStream_t stream) {
     if (n_edges == 0) return hipSuccess;
     hipLaunchKernelGGL(k_edge_setup, dim3(blocks_for(n_edges, 256)), dim3(256), 0, stream, ops,
-                       edges, n_edges, op_offsets, edge_offsets, row_begin, lp, params);
+                       edges, n_edges, op_offsets, edge_offsets, seg_begin, lp, params);
     hipError_t err = hipGetLastError();
-    if (err != hipSuccess || n_rows == 0) return err;
-    hipLaunchKernelGGL(k_row_map, dim3(blocks_for(n_rows, 256)), dim3(256), 0, stream, row_begin,
-                       op_offsets, edges, n_edges, n_rows, rows);
+    if (err != hipSuccess || n_segs == 0) return err;
+    hipLaunchKernelGGL(k_row_map, dim3(blocks_for(n_segs, 256)), dim3(256), 0, stream, seg_begin,
+                       op_offsets, edges, params, n_edges, n_segs, segs);
     return hipGetLastError();
 }
 
-hipError_t taps_launch_edge_costs(const taps_edge_params *params, const taps_row_ref *rows,
-                                  uint64_t n_rows, const taps_desc *desc, const taps_launch &lp,
+hipError_t taps_launch_edge_costs(const taps_edge_params *params, const taps_row_ref *segs,
+                                  uint64_t n_segs, const taps_desc *desc, const taps_launch &lp,
                                   taps_table out, hipStream_t stream) {
-    if (n_rows == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_edge_costs, dim3(blocks_for(n_rows, TAPS_ROWS_PER_BLOCK)),
-                       dim3(TAPS_TILE_COLS * TAPS_ROWS_PER_BLOCK), 0, stream, params, rows,
-                       (uint32_t)n_rows, desc, lp, out);
+    if (n_segs == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_edge_costs, dim3(blocks_for(n_segs, TAPS_ROWS_PER_BLOCK)),
+                       dim3(TAPS_TILE_COLS * TAPS_ROWS_PER_BLOCK), 0, stream, params, segs,
+                       (uint32_t)n_segs, desc, lp, out);
+    return hipGetLastError();
+}
+
+hipError_t taps_launch_copy_tables(const taps_copy_task *tasks, uint32_t n_tasks,
+                                   const uint64_t *dst_list, taps_table out, hipStream_t stream) {
+    if (n_tasks == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_copy_tables, dim3(n_tasks, 5), dim3(256), 0, stream, tasks, dst_list,
+                       out);
+    return hipGetLastError();
+}
+
+hipError_t taps_launch_same_ranges(const taps_strategy *strategies, const uint64_t *pairs,
+                                   uint32_t n_pairs, uint32_t *flags, hipStream_t stream) {
+    if (n_pairs == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_same_ranges, dim3(n_pairs), dim3(256), 0, stream, strategies, pairs,
+                       flags);
     return hipGetLastError();
 }

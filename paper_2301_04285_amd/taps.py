@@ -86,6 +86,8 @@ def load():
         L.taps_edge_costs.restype = C.c_int
         L.taps_edge_costs.argtypes = [P(GraphS), P(Cluster), C.c_void_p, P(C.c_uint64),
                                       P(C.c_uint64), Table, C.c_uint64, C.c_void_p]
+        L.taps_edge_costs_shared.restype = C.c_int
+        L.taps_edge_costs_shared.argtypes = L.taps_edge_costs.argtypes
         L.taps_set_edge_kernel_events.restype = C.c_int
         L.taps_set_edge_kernel_events.argtypes = [C.c_void_p, C.c_void_p]
         L.taps_status_str.restype = C.c_char_p
@@ -247,9 +249,10 @@ def taps_node_costs(graph, cluster, strategies, op_offsets, out=None, stream=Non
 
 
 def taps_edge_costs(graph, cluster, strategies, op_offsets, out=None, stream=None,
-                    size_only=False):
+                    size_only=False, shared=False):
     """(edge_offsets numpy uint64 [n_edges+1], edge table dict of device
-    tensors or None for a size query)."""
+    tensors or None for a size query).  ``shared``: taps_edge_costs_shared
+    (identical tables computed once)."""
     g = _graph(graph)
     cl = pack_cluster(cluster)
     offs = np.ascontiguousarray(op_offsets, dtype=np.uint64)
@@ -265,9 +268,10 @@ def taps_edge_costs(graph, cluster, strategies, op_offsets, out=None, stream=Non
     if out is None:
         out = alloc_table(total, device=strategies.device)
     cap = min(int(v.numel()) for v in out.values())
-    st = L.taps_edge_costs(C.byref(g.struct), C.byref(cl), sptr, _u64_array(offs),
-                           _u64_array(eoffs), _table(out), cap, _stream(stream))
-    _check(st, "taps_edge_costs")
+    fn = L.taps_edge_costs_shared if shared else L.taps_edge_costs
+    st = fn(C.byref(g.struct), C.byref(cl), sptr, _u64_array(offs), _u64_array(eoffs),
+            _table(out), cap, _stream(stream))
+    _check(st, "taps_edge_costs_shared" if shared else "taps_edge_costs")
     return eoffs, {k: v[:total] for k, v in out.items()}
 
 
@@ -293,16 +297,18 @@ class Tables:
     edge: Dict[str, "torch.Tensor"]
 
 
-def build_tables(graph, cluster, device="cuda", stream=None, out: Optional[Tables] = None) -> Tables:
+def build_tables(graph, cluster, device="cuda", stream=None, out: Optional[Tables] = None,
+                 shared: bool = False) -> Tables:
     """Enumeration, node table and edge table of one graph on one cluster.
-    ``out``: tables of an earlier build of the same graph to fill again."""
+    ``out``: tables of an earlier build of the same graph to fill again;
+    ``shared``: identical edge tables computed once (taps_edge_costs_shared)."""
     g = _graph(graph)
     offs, strat = taps_enumerate_strategies(g, cluster, device=device, stream=stream,
                                             out=out.strategies if out is not None else None)
     node = taps_node_costs(g, cluster, strat, offs, stream=stream,
                            out=out.node if out is not None else None)
     eoffs, edge = taps_edge_costs(g, cluster, strat, offs, stream=stream,
-                                  out=out.edge if out is not None else None)
+                                  out=out.edge if out is not None else None, shared=shared)
     return Tables(offs, strat, node, eoffs, edge)
 
 

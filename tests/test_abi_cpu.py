@@ -19,8 +19,8 @@ def lib():
 def test_exports_every_declared_symbol(lib):
     declared = T.declared_symbols()
     assert declared == sorted(["taps_enumerate_strategies", "taps_node_costs", "taps_edge_costs",
-                               "taps_set_edge_kernel_events", "taps_status_str",
-                               "taps_last_error"])
+                               "taps_edge_costs_shared", "taps_set_edge_kernel_events",
+                               "taps_status_str", "taps_last_error"])
     out = subprocess.run(["nm", "-D", "--defined-only", T.LIB_PATH], capture_output=True,
                          text=True, check=True).stdout
     exported = {line.split()[-1] for line in out.splitlines() if line.strip()}
@@ -156,14 +156,27 @@ def test_capacity_and_partial_tables(lib):
     offs = np.array([0, 9, 13, 22], np.uint64)
     eo = np.zeros(3, np.uint64)
     fake = T.Table(256, 256, 256, 256, 256)   # never dereferenced: the checks fail first
-    assert lib.taps_edge_costs(C.byref(g.struct), C.byref(cl), C.c_void_p(256),
-                               T._u64_array(offs), T._u64_array(eo), fake, 71, None) \
-        == T.ERR_CAPACITY
-    assert np.all(eo == 0)   # nothing written on error
     partial = T.Table(256, None, 256, 256, 256)
-    assert lib.taps_edge_costs(C.byref(g.struct), C.byref(cl), C.c_void_p(256),
-                               T._u64_array(offs), T._u64_array(eo), partial, 72, None) \
-        == T.ERR_ARG
+    for fn in (lib.taps_edge_costs, lib.taps_edge_costs_shared):
+        assert fn(C.byref(g.struct), C.byref(cl), C.c_void_p(256), T._u64_array(offs),
+                  T._u64_array(eo), fake, 71, None) == T.ERR_CAPACITY
+        assert np.all(eo == 0)   # nothing written on error
+        assert fn(C.byref(g.struct), C.byref(cl), C.c_void_p(256), T._u64_array(offs),
+                  T._u64_array(eo), partial, 72, None) == T.ERR_ARG
+
+
+def test_shared_size_query_matches(lib):
+    g = T.pack_graph(W.gpt(2, 64, 4, 32, 4, 2))
+    cl = T.pack_cluster(W.Cluster(2, 2, 10, 1))
+    counts = np.random.default_rng(1).integers(1, 50, g.n_ops)
+    offs = np.concatenate([[0], np.cumsum(counts)]).astype(np.uint64)
+    a, b = np.zeros(g.n_edges + 1, np.uint64), np.zeros(g.n_edges + 1, np.uint64)
+    none = T.Table(None, None, None, None, None)
+    assert lib.taps_edge_costs(C.byref(g.struct), C.byref(cl), None, T._u64_array(offs),
+                               T._u64_array(a), none, 0, None) == T.OK
+    assert lib.taps_edge_costs_shared(C.byref(g.struct), C.byref(cl), None, T._u64_array(offs),
+                                      T._u64_array(b), none, 0, None) == T.OK
+    assert np.array_equal(a, b)
 
 
 def test_device_errors_are_reported(lib):

@@ -300,3 +300,73 @@ def test_search_on_gpu_tables_matches_oracle_tables(T, oracle_lib):
             redge = [np.asarray(m[f], np.float64) for m in ref.edge]
             a, b = S.solve(g, node, edge), S.solve(g, rnode, redge)
             assert abs(a.objective - b.objective) <= 1e-9 * abs(b.objective)
+
+
+def _same_tables(a, b):
+    import torch
+    return all(torch.equal(a[f], b[f]) for f in ("t", "vol", "intra", "inter", "meta"))
+
+
+@pytest.mark.gpu
+def test_shared_tables_equal_full_evaluation(T):
+    """taps_edge_costs_shared writes exactly the tables of taps_edge_costs."""
+    import torch
+    cases = [(W.config(2).graph, W.config(2).clusters[0][1]),
+             (W.config(4).graph, W.config(4).clusters[0][1]),
+             (W.gpt(3, 64, 2, 128, 2, 2), W.Cluster(2, 2, 200 * W.GB, 25 * W.GB))]
+    rng = random.Random(77)
+    for _ in range(6):
+        g = W.random_graph(rng, rng.randint(2, 5), max_axes=4, max_rank=3, len_pow_range=(2, 7))
+        # three disjoint copies of the graph, so that every edge repeats
+        rep = W.Graph()
+        for k in range(3):
+            base = len(rep.ops)
+            for op in g.ops:
+                rep.ops.append(op)
+            for e in g.edges:
+                rep.connect(base + e.src, base + e.dst, e.slot)
+        try:
+            T.taps_enumerate_strategies(rep, W.Cluster(2, 4, 600 * W.GB, 50 * W.GB), size_only=True)
+        except T.TapsError:
+            continue
+        cases.append((rep, W.Cluster(2, 4, 600 * W.GB, 50 * W.GB)))
+    assert len(cases) >= 6
+    for g, cl in cases:
+        a = T.build_tables(g, cl)
+        b = T.build_tables(g, cl, shared=True)
+        torch.cuda.synchronize()
+        assert np.array_equal(a.edge_offsets, b.edge_offsets)
+        assert _same_tables(a.edge, b.edge)
+
+
+@pytest.mark.gpu
+def test_shared_tables_checks_the_strategies(T):
+    """With caller strategies that differ between two identically described
+    operators (one range reversed), sharing is refused for their edges and the
+    tables still equal the full evaluation."""
+    import torch
+    w = W.config(2)
+    cl = w.clusters[0][1]
+    offs, strat = T.taps_enumerate_strategies(w.graph, cl)
+    strat = strat.clone()
+    k = 14 + 1   # layer 1's query projection, described like layer 0's
+    a0, a1 = int(offs[k]), int(offs[k + 1])
+    strat[a0:a1] = strat[a0:a1].flip(0)
+    _, full = T.taps_edge_costs(w.graph, cl, strat, offs)
+    _, shared = T.taps_edge_costs(w.graph, cl, strat, offs, shared=True)
+    torch.cuda.synchronize()
+    assert _same_tables(full, shared)
+
+
+@pytest.mark.gpu
+def test_shared_tables_largest_config(T):
+    import torch
+    w = W.config(5)
+    cl = w.clusters[0][1]
+    a = T.build_tables(w.graph, cl)
+    b = T.build_tables(w.graph, cl, shared=True)
+    torch.cuda.synchronize()
+    assert int(b.edge_offsets[-1]) == 98668128
+    assert _same_tables(a.edge, b.edge)
+    del a, b
+    torch.cuda.empty_cache()
