@@ -46,8 +46,8 @@ struct taps_copy_task {
 // TAPS_SEG_TILES tiles of 64 consecutive consumer strategies, walked 64 at a
 // time.  A workgroup holds TAPS_ROWS_PER_BLOCK segments.
 #define TAPS_TILE_COLS 64
-#define TAPS_SEG_TILES 4
-#define TAPS_ROWS_PER_BLOCK 4
+#define TAPS_SEG_TILES 2
+#define TAPS_ROWS_PER_BLOCK 2
 
 // Segment r of the flat segment list: its edge, the global index of its
 // producer strategy and its first consumer strategy.

@@ -9,8 +9,8 @@
 //                 and first consumer strategy
 //   k_edge_costs  one wavefront per row segment (one producer strategy,
 //                 uniform: its descriptor sits in scalar registers; up to
-//                 four tiles of 64 consumer strategies, one per lane, the
-//                 next 64 prefetched), four segments per workgroup; five
+//                 TAPS_SEG_TILES tiles of 64 consumer strategies, one per lane, the
+//                 next 64 prefetched), TAPS_ROWS_PER_BLOCK segments per workgroup; five
 //                 coalesced non-temporal SoA stores per entry
 //   k_copy_tables shared tables: one workgroup per chunk of a computed
 //                 table, written to every table that shares it
