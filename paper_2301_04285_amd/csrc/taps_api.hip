@@ -92,7 +92,7 @@ taps_status check_tensor(const taps_op &op, const taps_tensor &t, uint32_t k, co
         return fail(TAPS_ERR_ARG, "op %u: %s %u has rank %u > %u", k, what, idx, t.rank,
                     TAPS_MAX_RANK);
     uint32_t seen = 0;
-    unsigned __int128 bytes = op.dtype_bytes;
+    uint64_t bytes = op.dtype_bytes;   // stays <= 2^40 or the check below fails first
     for (uint32_t d = 0; d < t.rank; ++d) {
         if (t.axis[d] >= op.n_axes)
             return fail(TAPS_ERR_ARG, "op %u: %s %u names axis %u of %u", k, what, idx, t.axis[d],
@@ -100,8 +100,8 @@ taps_status check_tensor(const taps_op &op, const taps_tensor &t, uint32_t k, co
         if (seen & (1u << t.axis[d]))
             return fail(TAPS_ERR_ARG, "op %u: %s %u names axis %u twice", k, what, idx, t.axis[d]);
         seen |= 1u << t.axis[d];
-        bytes *= (uint64_t)op.axis_len[t.axis[d]];
-        if (bytes > TAPS_MAX_TENSOR_BYTES)
+        if (__builtin_mul_overflow(bytes, (uint64_t)op.axis_len[t.axis[d]], &bytes) ||
+            bytes > TAPS_MAX_TENSOR_BYTES)
             return fail(TAPS_ERR_ARG, "op %u: %s %u exceeds %llu bytes", k, what, idx,
                         (unsigned long long)TAPS_MAX_TENSOR_BYTES);
     }
@@ -183,6 +183,34 @@ struct chunk {
 
 size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
+// Waits for the stream by polling: the calls that must read a result back wait
+// for a few tens of microseconds of queued work, where a blocking wait adds
+// its own wake-up latency.
+hipError_t wait_stream(hipStream_t stream) {
+    for (;;) {
+        const hipError_t err = hipStreamQuery(stream);
+        if (err != hipErrorNotReady) return err;
+    }
+}
+
+// The stream-ordered pool of the current device keeps freed scratch for the
+// next call instead of handing it back to the driver: a fresh reservation of
+// the tens of MB an edge call needs costs hundreds of microseconds.
+void retain_pool() {
+    static std::mutex mu;
+    static bool done[64] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return;
+    std::lock_guard<std::mutex> lock(mu);
+    if (done[dev]) return;
+    hipMemPool_t pool;
+    if (hipDeviceGetDefaultMemPool(&pool, dev) == hipSuccess) {
+        uint64_t threshold = UINT64_MAX;
+        (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &threshold);
+    }
+    done[dev] = true;
+}
+
 // Uploads the chunks into one stream-ordered device allocation; *dev
 // receives its base (free it with hipFreeAsync on the same stream).
 taps_status upload(std::vector<chunk> &chunks, void **dev, hipStream_t stream) {
@@ -192,6 +220,7 @@ taps_status upload(std::vector<chunk> &chunks, void **dev, hipStream_t stream) {
         total += align256(c.bytes);
     }
     if (total == 0) total = 256;
+    retain_pool();
     hipError_t err = hipMallocAsync(dev, total, stream);
     if (err != hipSuccess) return hip_fail(err, "hipMallocAsync");
     std::lock_guard<std::mutex> lock(g_stage.mu);
@@ -305,7 +334,7 @@ taps_status share_edges(const taps_graph *g, const uint64_t *op_offsets,
         if (err == hipSuccess)
             err = hipMemcpyAsync(flags.data(), d_flags, sizeof(uint32_t) * flags.size(),
                                  hipMemcpyDeviceToHost, stream);
-        if (err == hipSuccess) err = hipStreamSynchronize(stream);
+        if (err == hipSuccess) err = wait_stream(stream);
         if (err != hipSuccess) return hip_fail(err, "strategy comparison");
     }
     auto same = [&](int64_t p) { return p == -2 || (p >= 0 && flags[p] == 0); };
@@ -473,67 +502,58 @@ taps_status taps_enumerate_strategies(const taps_graph *graph, const taps_cluste
     }
     // launch geometry: the operator's candidates before the divisibility
     // filter (the closed-form count) cut into chunks of one wavefront
-    std::vector<uint32_t> chunk_op, chunk_first;
     std::vector<uint32_t> first_chunk(n_ops + 1, 0);
+    uint64_t n_chunks64 = 0;
     for (uint32_t k = 0; k < n_ops; ++k) {
         const uint64_t cand = candidate_count(__builtin_popcount(graph->ops[k].part_mask), lp.n);
-        first_chunk[k] = (uint32_t)chunk_op.size();
-        for (uint64_t f = 0; f < cand; f += TAPS_ENUM_CHUNK) {
-            chunk_op.push_back(k);
-            chunk_first.push_back((uint32_t)f);
-        }
+        first_chunk[k] = (uint32_t)n_chunks64;
+        n_chunks64 += (cand + TAPS_ENUM_CHUNK - 1) / TAPS_ENUM_CHUNK;
+        if (n_chunks64 > 0x7FFFFFFFull) return fail(TAPS_ERR_ARG, "too many candidates");
     }
-    first_chunk[n_ops] = (uint32_t)chunk_op.size();
-    const uint32_t n_chunks = (uint32_t)chunk_op.size();
+    first_chunk[n_ops] = (uint32_t)n_chunks64;
+    const uint32_t n_chunks = (uint32_t)n_chunks64;
     scratch sc(stream);
     std::vector<chunk> ch{{graph->ops, sizeof(taps_op) * n_ops, 0},
-                          {chunk_op.data(), sizeof(uint32_t) * n_chunks, 0},
-                          {chunk_first.data(), sizeof(uint32_t) * n_chunks, 0}};
+                          {first_chunk.data(), sizeof(uint32_t) * (n_ops + 1), 0}};
     void *dev = nullptr;
     if ((st = upload(ch, &dev, stream)) != TAPS_OK) return st;
     sc.adopt(dev);
     const taps_op *d_ops = at<taps_op>(dev, ch[0]);
     uint32_t *d_counts = nullptr;
+    uint64_t *d_base = nullptr, *d_scan = nullptr;
     if ((st = sc.alloc((void **)&d_counts, sizeof(uint32_t) * (n_chunks ? n_chunks : 1))) != TAPS_OK)
         return st;
-    hipError_t err = taps_launch_enumerate(d_ops, lp.n, n_chunks, at<uint32_t>(dev, ch[1]),
-                                           at<uint32_t>(dev, ch[2]), nullptr, d_counts, nullptr,
-                                           stream);
-    if (err != hipSuccess) return hip_fail(err, "enumerate (count)");
-    std::vector<uint32_t> counts(n_chunks);
-    if (n_chunks) {
-        err = hipMemcpyAsync(counts.data(), d_counts, sizeof(uint32_t) * n_chunks,
+    if ((st = sc.alloc((void **)&d_base, sizeof(uint64_t) * (n_chunks ? n_chunks : 1))) != TAPS_OK)
+        return st;
+    if ((st = sc.alloc((void **)&d_scan, sizeof(uint64_t) * (n_ops + 2))) != TAPS_OK) return st;
+    // count pass, prefix sums and (for a real call) the emit pass back to back on the
+    // device; the emit pass writes nothing unless every operator has a strategy and
+    // they fit the capacity.  One read-back returns the offsets.
+    const uint32_t *d_first = at<uint32_t>(dev, ch[1]);
+    hipError_t err = taps_launch_enumerate(d_ops, lp.n, n_ops, n_chunks, d_first, d_base,
+                                           d_scan + n_ops + 1, d_counts, nullptr, stream);
+    if (err == hipSuccess)
+        err = taps_launch_chunk_scan(d_counts, n_chunks, d_first, n_ops,
+                                     strategies ? capacity : UINT64_MAX, d_base, d_scan, stream);
+    if (err == hipSuccess && strategies)
+        err = taps_launch_enumerate(d_ops, lp.n, n_ops, n_chunks, d_first, d_base,
+                                    d_scan + n_ops + 1, nullptr, strategies, stream);
+    std::vector<uint64_t> offs(n_ops + 2, 0);
+    if (err == hipSuccess)
+        err = hipMemcpyAsync(offs.data(), d_scan, sizeof(uint64_t) * (n_ops + 2),
                              hipMemcpyDeviceToHost, stream);
-        if (err == hipSuccess) err = hipStreamSynchronize(stream);
-        if (err != hipSuccess) return hip_fail(err, "reading strategy counts");
-    }
-    std::vector<uint64_t> offs(n_ops + 1, 0), base(n_chunks ? n_chunks : 1, 0);
-    for (uint32_t k = 0; k < n_ops; ++k) {
-        uint64_t at_k = offs[k];
-        for (uint32_t c = first_chunk[k]; c < first_chunk[k + 1]; ++c) {
-            base[c] = at_k;
-            at_k += counts[c];
-        }
-        if (at_k == offs[k])
+    if (err == hipSuccess) err = wait_stream(stream);
+    if (err != hipSuccess) return hip_fail(err, "enumerate");
+    for (uint32_t k = 0; k < n_ops; ++k)
+        if (offs[k + 1] == offs[k])
             return fail(TAPS_ERR_NO_STRATEGY,
                         "op %u has no strategy on %u devices (no partitionable axis whose length "
                         "the degrees divide)",
                         k, 1u << lp.n);
-        offs[k + 1] = at_k;
-    }
     std::memcpy(op_offsets, offs.data(), sizeof(uint64_t) * (n_ops + 1));
-    if (!strategies) return TAPS_OK;
-    if (offs[n_ops] > capacity)
+    if (strategies && offs[n_ops] > capacity)
         return fail(TAPS_ERR_CAPACITY, "%llu strategies, capacity %llu",
                     (unsigned long long)offs[n_ops], (unsigned long long)capacity);
-    std::vector<chunk> ch2{{base.data(), sizeof(uint64_t) * n_chunks, 0}};
-    void *dev2 = nullptr;
-    if ((st = upload(ch2, &dev2, stream)) != TAPS_OK) return st;
-    sc.adopt(dev2);
-    err = taps_launch_enumerate(d_ops, lp.n, n_chunks, at<uint32_t>(dev, ch[1]),
-                                at<uint32_t>(dev, ch[2]), at<uint64_t>(dev2, ch2[0]), nullptr,
-                                strategies, stream);
-    if (err != hipSuccess) return hip_fail(err, "enumerate (emit)");
     return TAPS_OK;
 }
 

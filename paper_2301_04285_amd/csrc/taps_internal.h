@@ -60,10 +60,15 @@ struct taps_row_ref {
 
 #define TAPS_ENUM_CHUNK 64   // candidates per enumeration wavefront
 
-hipError_t taps_launch_enumerate(const taps_op *ops, uint32_t n, uint32_t n_chunks,
-                                 const uint32_t *chunk_op, const uint32_t *chunk_first,
-                                 const uint64_t *base, uint32_t *counts, taps_strategy *out,
-                                 hipStream_t stream);
+// first_chunk: n_ops + 1 entries, operator k owns chunks [first_chunk[k], first_chunk[k+1]).
+hipError_t taps_launch_enumerate(const taps_op *ops, uint32_t n, uint32_t n_ops,
+                                 uint32_t n_chunks, const uint32_t *first_chunk,
+                                 const uint64_t *base, const uint64_t *valid_flag,
+                                 uint32_t *counts, taps_strategy *out, hipStream_t stream);
+// scan: n_ops + 2 entries (operator offsets, total, valid flag); base: n_chunks.
+hipError_t taps_launch_chunk_scan(const uint32_t *counts, uint32_t n_chunks,
+                                  const uint32_t *first_chunk, uint32_t n_ops, uint64_t capacity,
+                                  uint64_t *base, uint64_t *scan, hipStream_t stream);
 hipError_t taps_launch_describe(const taps_strategy *s, uint64_t total, taps_desc *desc,
                                 hipStream_t stream);
 hipError_t taps_launch_node_costs(const taps_op *ops, uint32_t n_ops, const uint64_t *offsets,

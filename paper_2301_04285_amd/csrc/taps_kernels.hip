@@ -19,6 +19,7 @@
 namespace {
 
 constexpr uint32_t kWave = 64;
+static_assert(TAPS_ENUM_CHUNK == kWave, "one enumeration chunk per wavefront");
 
 // Completion counts w(k, s, z) for k, s, z in 0..8 (see taps_completions),
 // evaluated by the compiler.
@@ -47,25 +48,45 @@ __device__ inline uint32_t lanes_below(uint64_t mask) {
                                      __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
 }
 
+// The operator owning chunk c: largest k < n_ops with first_chunk[k] <= c
+// (operators without chunks share their successor's first chunk).
+__device__ inline uint32_t find_chunk_owner(const uint32_t *first_chunk, uint32_t n_ops,
+                                            uint32_t c) {
+    uint32_t lo = 0, hi = n_ops;
+    while (hi - lo > 1) {
+        const uint32_t mid = (lo + hi) >> 1;
+        if (first_chunk[mid] <= c)
+            lo = mid;
+        else
+            hi = mid;
+    }
+    return lo;
+}
+
 // One wavefront per chunk of 64 consecutive candidates of one operator.
-// chunk_op[c] / chunk_first[c]: operator and first candidate of chunk c.
+// Operator k owns chunks first_chunk[k] .. first_chunk[k+1]-1, its candidates
+// in order, 64 per chunk.
 // Count pass (out == nullptr): counts[c] = valid candidates of the chunk.
-// Emit pass: valid candidates go to out[base[c] + rank among the chunk's].
+// Emit pass: valid candidates go to out[base[c] + rank among the chunk's],
+// only if the scan found the enumeration valid (scan[n_ops + 1] == 1).
 __global__ __launch_bounds__(kWave) void k_enumerate(const taps_op *__restrict__ ops, uint32_t n,
-                                                     const uint32_t *__restrict__ chunk_op,
-                                                     const uint32_t *__restrict__ chunk_first,
+                                                     uint32_t n_ops,
+                                                     const uint32_t *__restrict__ first_chunk,
                                                      const uint64_t *__restrict__ base,
+                                                     const uint64_t *__restrict__ valid_flag,
                                                      uint32_t *__restrict__ counts,
                                                      taps_strategy *__restrict__ out) {
     __shared__ uint32_t W[9 * 9 * 9];
+    if (out && *valid_flag != 1u) return;   // uniform: nothing is written on an error
     const uint32_t lane = threadIdx.x;
     for (uint32_t x = lane; x < 9u * 9u * 9u; x += kWave) W[x] = kCompletions.v[x];
     __syncthreads();
     const uint32_t c = blockIdx.x;
-    const taps_op &op = ops[chunk_op[c]];
+    const uint32_t k = find_chunk_owner(first_chunk, n_ops, c);
+    const taps_op &op = ops[k];
     const uint32_t n_axes = op.n_axes, part = op.part_mask;
     const uint32_t total = W[(taps_popc(part) * 9u + n) * 9u];
-    const uint32_t r = chunk_first[c] + lane;
+    const uint32_t r = (c - first_chunk[k]) * kWave + lane;
     uint32_t expo[TAPS_D_MAX_AXES];
     int32_t pos[TAPS_D_MAX_AXES];
     bool valid = r < total && taps_unrank(n_axes, part, n, r, W, expo, pos);
@@ -81,6 +102,66 @@ __global__ __launch_bounds__(kWave) void k_enumerate(const taps_op *__restrict__
             st.pos[a] = a < n_axes ? (int8_t)pos[a] : (int8_t)-1;
         }
         out[base[c] + lanes_below(m)] = st;
+    }
+}
+
+// One workgroup: exclusive prefix sums of the chunk counts (base[c], the
+// first strategy of chunk c), the operator offsets scan[k] = base of the
+// operator's first chunk (scan[n_ops] = total), and scan[n_ops + 1] = 1 if
+// every operator has a strategy and the total fits `capacity`, else 0.
+__global__ __launch_bounds__(1024) void k_chunk_scan(const uint32_t *__restrict__ counts,
+                                                     uint32_t n_chunks,
+                                                     const uint32_t *__restrict__ first_chunk,
+                                                     uint32_t n_ops, uint64_t capacity,
+                                                     uint64_t *__restrict__ base,
+                                                     uint64_t *__restrict__ scan) {
+    __shared__ uint32_t wsum[16];
+    __shared__ uint32_t bad;
+    const uint32_t t = threadIdx.x, lane = t % kWave, wave = t / kWave;
+    if (t == 0) bad = 0;
+    uint64_t carry = 0;
+    // tiles of 1024 consecutive chunks: wavefront scans, then a scan of the 16
+    // wavefront sums
+    for (uint32_t tile = 0; tile < n_chunks; tile += 1024u) {
+        const uint32_t c = tile + t;
+        const uint32_t own = c < n_chunks ? counts[c] : 0u;
+        uint32_t v = own;
+#pragma unroll
+        for (uint32_t d = 1; d < kWave; d <<= 1) {
+            const uint32_t y = __shfl_up(v, d, kWave);
+            if (lane >= d) v += y;
+        }
+        if (lane == kWave - 1) wsum[wave] = v;
+        __syncthreads();
+        if (wave == 0) {
+            uint32_t w = lane < 16u ? wsum[lane] : 0u;
+#pragma unroll
+            for (uint32_t d = 1; d < 16u; d <<= 1) {
+                const uint32_t y = __shfl_up(w, d, kWave);
+                if (lane >= d) w += y;
+            }
+            if (lane < 16u) wsum[lane] = w;
+        }
+        __syncthreads();
+        const uint32_t before = wave ? wsum[wave - 1] : 0u;
+        if (c < n_chunks) base[c] = carry + before + v - own;
+        carry += wsum[15];
+        __syncthreads();   // wsum is rewritten by the next tile
+    }
+    __threadfence_block();
+    __syncthreads();
+    const uint64_t total = carry;
+    for (uint32_t k = t; k < n_ops; k += 1024u) {
+        const uint32_t f = first_chunk[k], f1 = first_chunk[k + 1];
+        const uint64_t start = f < n_chunks ? base[f] : total;
+        const uint64_t end = f1 < n_chunks ? base[f1] : total;
+        scan[k] = start;
+        if (end == start) bad = 1;   // an operator without a strategy
+    }
+    __syncthreads();
+    if (t == 0) {
+        scan[n_ops] = total;
+        scan[n_ops + 1] = (!bad && total <= capacity) ? 1u : 0u;
     }
 }
 
@@ -306,13 +387,21 @@ inline uint32_t blocks_for(uint64_t n, uint32_t per) { return (uint32_t)((n + pe
 
 }  // namespace
 
-hipError_t taps_launch_enumerate(const taps_op *ops, uint32_t n, uint32_t n_chunks,
-                                 const uint32_t *chunk_op, const uint32_t *chunk_first,
-                                 const uint64_t *base, uint32_t *counts, taps_strategy *out,
-                                 hipStream_t stream) {
+hipError_t taps_launch_enumerate(const taps_op *ops, uint32_t n, uint32_t n_ops,
+                                 uint32_t n_chunks, const uint32_t *first_chunk,
+                                 const uint64_t *base, const uint64_t *valid_flag,
+                                 uint32_t *counts, taps_strategy *out, hipStream_t stream) {
     if (n_chunks == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_enumerate, dim3(n_chunks), dim3(kWave), 0, stream, ops, n, chunk_op,
-                       chunk_first, base, counts, out);
+    hipLaunchKernelGGL(k_enumerate, dim3(n_chunks), dim3(kWave), 0, stream, ops, n, n_ops,
+                       first_chunk, base, valid_flag, counts, out);
+    return hipGetLastError();
+}
+
+hipError_t taps_launch_chunk_scan(const uint32_t *counts, uint32_t n_chunks,
+                                  const uint32_t *first_chunk, uint32_t n_ops, uint64_t capacity,
+                                  uint64_t *base, uint64_t *scan, hipStream_t stream) {
+    hipLaunchKernelGGL(k_chunk_scan, dim3(1), dim3(1024), 0, stream, counts, n_chunks,
+                       first_chunk, n_ops, capacity, base, scan);
     return hipGetLastError();
 }
 

@@ -259,19 +259,19 @@ def taps_edge_costs(graph, cluster, strategies, op_offsets, out=None, stream=Non
     eoffs = np.zeros(g.n_edges + 1, dtype=np.uint64)
     L = load()
     sptr = C.c_void_p(strategies.data_ptr()) if strategies is not None else None
-    st = L.taps_edge_costs(C.byref(g.struct), C.byref(cl), sptr, _u64_array(offs),
-                           _u64_array(eoffs), _table(None), 0, _stream(stream))
-    _check(st, "taps_edge_costs")
-    if size_only:
-        return eoffs, None
-    total = int(eoffs[-1])
-    if out is None:
-        out = alloc_table(total, device=strategies.device)
+    if out is None or size_only:   # size query first
+        st = L.taps_edge_costs(C.byref(g.struct), C.byref(cl), sptr, _u64_array(offs),
+                               _u64_array(eoffs), _table(None), 0, _stream(stream))
+        _check(st, "taps_edge_costs")
+        if size_only:
+            return eoffs, None
+        out = alloc_table(int(eoffs[-1]), device=strategies.device)
     cap = min(int(v.numel()) for v in out.values())
     fn = L.taps_edge_costs_shared if shared else L.taps_edge_costs
     st = fn(C.byref(g.struct), C.byref(cl), sptr, _u64_array(offs), _u64_array(eoffs),
             _table(out), cap, _stream(stream))
     _check(st, "taps_edge_costs_shared" if shared else "taps_edge_costs")
+    total = int(eoffs[-1])
     return eoffs, {k: v[:total] for k, v in out.items()}
 
 
