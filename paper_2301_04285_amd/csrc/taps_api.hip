@@ -6,6 +6,7 @@
 // computed on the GPU.
 #include <hip/hip_runtime.h>
 
+#include <chrono>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -183,14 +184,18 @@ struct chunk {
 
 size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
-// Waits for the stream by polling: the calls that must read a result back wait
+// Waits for the stream: the calls that must read a result back usually wait
 // for a few tens of microseconds of queued work, where a blocking wait adds
-// its own wake-up latency.
+// its own wake-up latency, so the stream is polled for up to 200 us before
+// the wait blocks (a caller's long work already queued on the stream then
+// does not keep a core spinning).
 hipError_t wait_stream(hipStream_t stream) {
-    for (;;) {
+    const auto until = std::chrono::steady_clock::now() + std::chrono::microseconds(200);
+    while (std::chrono::steady_clock::now() < until) {
         const hipError_t err = hipStreamQuery(stream);
         if (err != hipErrorNotReady) return err;
     }
+    return hipStreamSynchronize(stream);
 }
 
 // The stream-ordered pool of the current device keeps freed scratch for the
