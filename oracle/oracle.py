@@ -115,6 +115,11 @@ def lib():
         L.or_edge_cost.restype = C.c_int
         L.or_edge_cost.argtypes = [P(OrOp), P(OrStrategy), P(OrOp), C.c_int, P(OrStrategy),
                                    i64, i64, u64, u64, P(OrRecord)]
+        L.or_edge_cost_reverse.restype = C.c_int
+        L.or_edge_cost_reverse.argtypes = L.or_edge_cost.argtypes
+        L.or_edge_table_reverse.restype = i64
+        L.or_edge_table_reverse.argtypes = [P(OrOp), P(OrStrategy), i64, P(OrOp), C.c_int,
+                                            P(OrStrategy), i64, i64, i64, u64, u64, P(OrRecord)]
         L.or_edge_table.restype = i64
         L.or_edge_table.argtypes = [P(OrOp), P(OrStrategy), i64, P(OrOp), C.c_int,
                                     P(OrStrategy), i64, i64, i64, u64, u64, P(OrRecord)]
@@ -201,6 +206,34 @@ def edge_table(src_op, src_strats: np.ndarray, dst_op, slot: int, dst_strats: np
                             cluster.devices_per_node, cluster.bw_intra, cluster.bw_inter, _rp(out))
     assert n == out.size, "oracle failed on this edge"
     return out.reshape(len(src_strats), len(dst_strats))
+
+
+def edge_table_reverse(src_op, src_strats: np.ndarray, dst_op, slot: int, dst_strats: np.ndarray,
+                       cluster) -> np.ndarray:
+    """Backward table of one edge (the gradient from the consumer's map back to the
+    producer's), consumer-major: shape (len(dst_strats), len(src_strats))."""
+    a, b = make_op(src_op), make_op(dst_op)
+    out = np.zeros(len(src_strats) * len(dst_strats), dtype=RECORD_DTYPE)
+    n = lib().or_edge_table_reverse(C.byref(a), _sp(src_strats), len(src_strats), C.byref(b),
+                                    slot, _sp(dst_strats), len(dst_strats), cluster.devices,
+                                    cluster.devices_per_node, cluster.bw_intra, cluster.bw_inter,
+                                    _rp(out))
+    assert n == out.size, "oracle failed on this edge"
+    return out.reshape(len(dst_strats), len(src_strats))
+
+
+def edge_cost_reverse(src_op, si, dst_op, slot, sj, cluster):
+    """Backward cost of one pair (the gradient from consumer strategy sj back to
+    producer strategy si)."""
+    a, b = make_op(src_op), make_op(dst_op)
+    rec = OrRecord()
+    s1 = np.ascontiguousarray(si, dtype=STRATEGY_DTYPE).reshape(1)
+    s2 = np.ascontiguousarray(sj, dtype=STRATEGY_DTYPE).reshape(1)
+    rc = lib().or_edge_cost_reverse(C.byref(a), _sp(s1), C.byref(b), slot, _sp(s2),
+                                    cluster.devices, cluster.devices_per_node, cluster.bw_intra,
+                                    cluster.bw_inter, C.byref(rec))
+    assert rc == 0
+    return (rec.t, rec.vol, rec.intra, rec.inter, rec.meta)
 
 
 def edge_entries(src_op, src_strats, dst_op, slot, dst_strats, ii, jj, cluster) -> np.ndarray:

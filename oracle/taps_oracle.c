@@ -766,10 +766,14 @@ static seq_cost cost_sequence(const int64_t *D, int h, const int32_t *Mfrom, int
 
 /* ---------------------------------------------------------------------------
  * One auxiliary edge (Algorithm 4): the tensor src.out feeds dst.in[slot];
- * strategy si of the producer, sj of the consumer.
+ * strategy si of the producer, sj of the consumer.  Forward: the tensor
+ * moves from the producer's map to the consumer's.  Reverse (the gradient of
+ * the same tensor in the backward pass): from the consumer's map back to the
+ * producer's; same shape and element size.
  * ------------------------------------------------------------------------- */
-static int edge_problem(const or_op *src, const or_strategy *si, const or_op *dst, int slot,
-                        const or_strategy *sj, int64_t N, or_unified *u, uint64_t *shard0_nb) {
+static int edge_problem_dir(const or_op *src, const or_strategy *si, const or_op *dst, int slot,
+                            const or_strategy *sj, int64_t N, int reverse, or_unified *u,
+                            uint64_t *shard0_nb) {
     const or_tensor *T = &src->out, *Tc = &dst->in[slot];
     int64_t Dp[OR_MAX_DEV], Dc[OR_MAX_DEV], shape[OR_MAX_RANK];
     int32_t Mp[OR_MAX_RANK], Mc[OR_MAX_RANK];
@@ -781,12 +785,19 @@ static int edge_problem(const or_op *src, const or_strategy *si, const or_op *ds
         shape[d] = src->axis_len[T->axis[d]];
         elems *= (uint64_t)shape[d];
     }
-    if (or_unify(N, Dp, hp, Mp, Dc, hc, Mc, T->rank, shape, u)) return -1;
+    if (reverse ? or_unify(N, Dc, hc, Mc, Dp, hp, Mp, T->rank, shape, u)
+                : or_unify(N, Dp, hp, Mp, Dc, hc, Mc, T->rank, shape, u))
+        return -1;
     uint64_t used = 1;
     for (int d = 0; d < u->r; ++d)
         if (u->m_from[d] >= 0) used *= (uint64_t)u->D[u->m_from[d]];
     *shard0_nb = elems * (uint64_t)src->dtype_bytes * (uint64_t)N / used;
     return 0;
+}
+
+static int edge_problem(const or_op *src, const or_strategy *si, const or_op *dst, int slot,
+                        const or_strategy *sj, int64_t N, or_unified *u, uint64_t *shard0_nb) {
+    return edge_problem_dir(src, si, dst, slot, sj, N, 0, u, shard0_nb);
 }
 
 /* Exposes one candidate's unified problem and operator sequence with the
@@ -818,13 +829,13 @@ int or_sequence_cost(const int64_t *D, int h, const int32_t *Mfrom, const int32_
 
 /* Reading R-h: the cheapest of the four candidates by exact comparison of
  * intra/(N B_intra) + inter/(N B_inter), ties to the lower candidate index. */
-int or_edge_cost(const or_op *src, const or_strategy *si, const or_op *dst, int slot,
-                 const or_strategy *sj, int64_t N, int64_t L, uint64_t Bintra, uint64_t Binter,
-                 or_record *rec) {
+static int edge_cost_dir(const or_op *src, const or_strategy *si, const or_op *dst, int slot,
+                         const or_strategy *sj, int64_t N, int64_t L, uint64_t Bintra,
+                         uint64_t Binter, int reverse, or_record *rec) {
     or_unified u;
     uint64_t shard0;
     memset(rec, 0, sizeof *rec);
-    if (edge_problem(src, si, dst, slot, sj, N, &u, &shard0)) return -1;
+    if (edge_problem_dir(src, si, dst, slot, sj, N, reverse, &u, &shard0)) return -1;
     or_redop seq[OR_MAX_SEQ];
     seq_cost best;
     memset(&best, 0, sizeof best);
@@ -851,6 +862,33 @@ int or_edge_cost(const or_op *src, const or_strategy *si, const or_op *dst, int 
     rec->inter = best.inter;
     rec->meta = (uint32_t)best_c | (best.n_coll << 2) | (best.n_inter << 7) | (best.sum_ct << 12);
     return 0;
+}
+
+int or_edge_cost(const or_op *src, const or_strategy *si, const or_op *dst, int slot,
+                 const or_strategy *sj, int64_t N, int64_t L, uint64_t Bintra, uint64_t Binter,
+                 or_record *rec) {
+    return edge_cost_dir(src, si, dst, slot, sj, N, L, Bintra, Binter, 0, rec);
+}
+
+/* The backward direction of the same pair: the gradient moves from the
+ * consumer's map (strategy sj) back to the producer's (strategy si). */
+int or_edge_cost_reverse(const or_op *src, const or_strategy *si, const or_op *dst, int slot,
+                         const or_strategy *sj, int64_t N, int64_t L, uint64_t Bintra,
+                         uint64_t Binter, or_record *rec) {
+    return edge_cost_dir(src, si, dst, slot, sj, N, L, Bintra, Binter, 1, rec);
+}
+
+/* Backward table of one edge, consumer-major: out[j * ns + i]. */
+int64_t or_edge_table_reverse(const or_op *src, const or_strategy *ss, int64_t ns,
+                              const or_op *dst, int slot, const or_strategy *sd, int64_t nd,
+                              int64_t N, int64_t L, uint64_t Bintra, uint64_t Binter,
+                              or_record *out) {
+    for (int64_t j = 0; j < nd; ++j)
+        for (int64_t i = 0; i < ns; ++i)
+            if (or_edge_cost_reverse(src, &ss[i], dst, slot, &sd[j], N, L, Bintra, Binter,
+                                     &out[j * ns + i]))
+                return -1;
+    return ns * nd;
 }
 
 /* Row-major table of one edge: out[i * nd + j]. */

@@ -325,3 +325,72 @@ def test_tables_are_deterministic(oracle_lib):
     b = oracle_lib.build_tables(w.graph, cl)
     for x, y in zip(a.edge + a.node, b.edge + b.node):
         assert x.tobytes() == y.tobytes()
+
+
+# ---------------------------------------------------------------------------
+# Backward direction: the gradient of an edge tensor moves from the consumer's
+# map back to the producer's.
+# ---------------------------------------------------------------------------
+
+def _reversed_edge(src, dst, slot):
+    """A virtual edge running the other way: the consumer, producing the tensor in
+    its input map, feeds the producer, reading it in its output map."""
+    import dataclasses
+    a = dataclasses.replace(dst, out=dst.ins[slot], dtype_bytes=src.dtype_bytes)
+    b = dataclasses.replace(src, ins=(src.out,))
+    return a, b
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_reverse_table_equals_forward_table_of_the_reversed_edge(oracle_lib, seed):
+    rng = random.Random(500 + seed)
+    g = W.random_graph(rng, 3, max_axes=4, max_rank=3, len_pow_range=(2, 6))
+    cl = W.Cluster(2, 4, 600 * W.GB, 50 * W.GB)
+    strats = [oracle_lib.enumerate_strategies(op, cl.devices) for op in g.ops]
+    for e in g.edges:
+        if not len(strats[e.src]) or not len(strats[e.dst]):
+            continue
+        src, dst = g.ops[e.src], g.ops[e.dst]
+        rev = oracle_lib.edge_table_reverse(src, strats[e.src], dst, e.slot, strats[e.dst], cl)
+        a, b = _reversed_edge(src, dst, e.slot)
+        fwd = oracle_lib.edge_table(a, strats[e.dst], b, 0, strats[e.src], cl)
+        assert rev.shape == fwd.shape == (len(strats[e.dst]), len(strats[e.src]))
+        for f in ("vol", "intra", "inter", "meta"):
+            assert np.array_equal(rev[f], fwd[f])
+        assert np.allclose(rev["t"], fwd["t"], rtol=1e-12, atol=0)
+
+
+def test_reverse_table_of_a_self_similar_edge_is_the_forward_table(oracle_lib):
+    """Between two alike element-wise operators the strategy lists and tensor maps
+    coincide, so moving layout j to layout i costs the same in both tables."""
+    op = W.elementwise("x", "gelu", ("b", "s", "h"), (64, 512, 1024), 1, 2)
+    g = W.Graph()
+    g.add(op)
+    g.add(W.elementwise("y", "gelu", ("b", "s", "h"), (64, 512, 1024), 1, 2))
+    g.connect(0, 1, 0)
+    cl = W.Cluster(4, 4, 600 * W.GB, 50 * W.GB)
+    s = oracle_lib.enumerate_strategies(g.ops[0], cl.devices)
+    fwd = oracle_lib.edge_table(g.ops[0], s, g.ops[1], 0, s, cl)
+    rev = oracle_lib.edge_table_reverse(g.ops[0], s, g.ops[1], 0, s, cl)
+    assert fwd.shape == rev.shape and fwd.shape[0] > 10
+    for f in ("t", "vol", "intra", "inter", "meta"):
+        assert np.array_equal(fwd[f], rev[f])
+    # and the direction matters elsewhere: a matmul output into a transposing consumer
+    assert not np.array_equal(fwd["vol"], fwd["vol"].T) or fwd.shape[0] == 1
+
+
+def test_reverse_tables_of_a_transformer_layer(oracle_lib):
+    """Every edge of one GPT layer (16 edges, transposing and non-transposing maps)."""
+    g = W.gpt(1, 64, 4, 128, 4, 2)
+    cl = W.Cluster(2, 4, 600 * W.GB, 50 * W.GB)
+    strats = [oracle_lib.enumerate_strategies(op, cl.devices) for op in g.ops]
+    checked = 0
+    for e in g.edges:
+        src, dst = g.ops[e.src], g.ops[e.dst]
+        rev = oracle_lib.edge_table_reverse(src, strats[e.src], dst, e.slot, strats[e.dst], cl)
+        a, b = _reversed_edge(src, dst, e.slot)
+        fwd = oracle_lib.edge_table(a, strats[e.dst], b, 0, strats[e.src], cl)
+        for f in ("vol", "intra", "inter", "meta"):
+            assert np.array_equal(rev[f], fwd[f])
+        checked += rev.size
+    assert len(g.edges) == 16 and checked > 10000
