@@ -207,10 +207,28 @@ taps_status taps_edge_costs_shared(const taps_graph *graph, const taps_cluster *
                                    uint64_t *edge_offsets, taps_table out, uint64_t capacity,
                                    void *stream);
 
+/* The backward direction of every edge: in the backward pass the gradient of
+ * the edge tensor leaves the consumer in the consumer's input map (fully
+ * reduced: its AllReduce is in the consumer's node cost) and must reach the
+ * producer in the producer's output map.  The same candidates and selection
+ * as taps_edge_costs, with the roles of the two maps swapped; same shape and
+ * element size.  The paper costs only the forward direction (the edge-weight
+ * paragraph after Algorithm 4); a search that also charges the backward
+ * redistribution adds these tables.
+ *   edge_offsets  as taps_edge_costs (S_src * S_dst entries per edge);
+ *                 edge e's table is consumer-major: entry
+ *                 edge_offsets[e] + j * S_src + i for producer strategy i and
+ *                 consumer strategy j.
+ * Other arguments and errors as taps_edge_costs. */
+taps_status taps_edge_costs_backward(const taps_graph *graph, const taps_cluster *cluster,
+                                     const taps_strategy *strategies, const uint64_t *op_offsets,
+                                     uint64_t *edge_offsets, taps_table out, uint64_t capacity,
+                                     void *stream);
+
 /* Profiling aid, not part of the method: `before` and `after` are HIP events
  * (hipEvent_t, created by the caller, passed as plain pointers) that the
- * calling thread's next taps_edge_costs or taps_edge_costs_shared call that
- * launches the edge-table kernel records on its stream immediately before and
+ * calling thread's next taps_edge_costs, taps_edge_costs_shared or
+ * taps_edge_costs_backward call that launches the edge-table kernel records on its stream immediately before and
  * after that kernel (and, for shared tables, the copies after it), so that
  * the caller can time the kernel alone.  The setting is thread-local,
  * used once and then cleared; two NULLs clear it.  The events stay owned by

@@ -351,7 +351,7 @@ taps_status share_edges(const taps_graph *g, const uint64_t *op_offsets,
 taps_status edge_costs(const taps_graph *graph, const taps_cluster *cluster,
                        const taps_strategy *strategies, const uint64_t *op_offsets,
                        uint64_t *edge_offsets, taps_table out, uint64_t capacity, void *stream_,
-                       bool share) {
+                       bool share, bool reverse) {
     g_last_error.clear();
     taps_launch lp;
     taps_status st = check_cluster(cluster, &lp);
@@ -364,8 +364,9 @@ taps_status edge_costs(const taps_graph *graph, const taps_cluster *cluster,
     uint64_t all_segs = 0;   // row segments without sharing (an upper bound)
     for (uint32_t e = 0; e < n_edges; ++e) {
         const taps_edge &E = graph->edges[e];
-        const uint64_t ns = op_offsets[E.src_op + 1] - op_offsets[E.src_op];
-        const uint64_t nd = op_offsets[E.dst_op + 1] - op_offsets[E.dst_op];
+        const uint64_t np = op_offsets[E.src_op + 1] - op_offsets[E.src_op];
+        const uint64_t nc = op_offsets[E.dst_op + 1] - op_offsets[E.dst_op];
+        const uint64_t ns = reverse ? nc : np, nd = reverse ? np : nc;   // rows, columns
         eoff[e + 1] = eoff[e] + ns * nd;
         all_segs += ns * ((nd + TAPS_TILE_COLS * TAPS_SEG_TILES - 1) /
                           (TAPS_TILE_COLS * TAPS_SEG_TILES));
@@ -390,8 +391,9 @@ taps_status edge_costs(const taps_graph *graph, const taps_cluster *cluster,
     std::vector<uint64_t> segs(n_edges + 1, 0);
     for (uint32_t e = 0; e < n_edges; ++e) {
         const taps_edge &E = graph->edges[e];
-        const uint64_t ns = op_offsets[E.src_op + 1] - op_offsets[E.src_op];
-        const uint64_t nd = op_offsets[E.dst_op + 1] - op_offsets[E.dst_op];
+        const uint64_t np = op_offsets[E.src_op + 1] - op_offsets[E.src_op];
+        const uint64_t nc = op_offsets[E.dst_op + 1] - op_offsets[E.dst_op];
+        const uint64_t ns = reverse ? nc : np, nd = reverse ? np : nc;
         const uint64_t per_row = (nd + TAPS_TILE_COLS * TAPS_SEG_TILES - 1) /
                                  (TAPS_TILE_COLS * TAPS_SEG_TILES);
         segs[e + 1] = segs[e] + (rep[e] == e ? ns * per_row : 0);
@@ -446,8 +448,8 @@ taps_status edge_costs(const taps_graph *graph, const taps_cluster *cluster,
     if (err == hipSuccess)
         err = taps_launch_edge_setup(at<taps_op>(dev, ch[0]), at<taps_edge>(dev, ch[1]), n_edges,
                                      at<uint64_t>(dev, ch[2]), at<uint64_t>(dev, ch[3]),
-                                     at<uint64_t>(dev, ch[4]), lp, d_params, n_segs, d_segs,
-                                     stream);
+                                     at<uint64_t>(dev, ch[4]), lp, reverse, d_params, n_segs,
+                                     d_segs, stream);
     // the edge-table kernel launches (entries > 0): use the events, if any, once
     const hipEvent_t before = g_kernel_before, after = g_kernel_after;
     g_kernel_before = g_kernel_after = nullptr;
@@ -599,7 +601,7 @@ taps_status taps_edge_costs(const taps_graph *graph, const taps_cluster *cluster
                             uint64_t *edge_offsets, taps_table out, uint64_t capacity,
                             void *stream) {
     return edge_costs(graph, cluster, strategies, op_offsets, edge_offsets, out, capacity, stream,
-                      false);
+                      false, false);
 }
 
 taps_status taps_edge_costs_shared(const taps_graph *graph, const taps_cluster *cluster,
@@ -607,7 +609,15 @@ taps_status taps_edge_costs_shared(const taps_graph *graph, const taps_cluster *
                                    uint64_t *edge_offsets, taps_table out, uint64_t capacity,
                                    void *stream) {
     return edge_costs(graph, cluster, strategies, op_offsets, edge_offsets, out, capacity, stream,
-                      true);
+                      true, false);
+}
+
+taps_status taps_edge_costs_backward(const taps_graph *graph, const taps_cluster *cluster,
+                                     const taps_strategy *strategies, const uint64_t *op_offsets,
+                                     uint64_t *edge_offsets, taps_table out, uint64_t capacity,
+                                     void *stream) {
+    return edge_costs(graph, cluster, strategies, op_offsets, edge_offsets, out, capacity, stream,
+                      false, true);
 }
 
 }  // extern "C"

@@ -23,12 +23,12 @@ struct taps_edge_params {
     uint64_t out_offset;   // first entry of the edge's table
     uint64_t seg_begin;    // first row segment of the edge (segments of all edges, in order)
     taps_scaler scale;     // tbytes and the per-unit seconds of the edge tensor
-    uint32_t src_base;     // first strategy of the producer
-    uint32_t dst_base;     // first strategy of the consumer
-    uint32_t ns, nd;       // strategy counts
+    uint32_t src_base;     // first strategy of the source side (producer; consumer for
+    uint32_t dst_base;     //   the backward tables) and of the target side
+    uint32_t ns, nd;       // their strategy counts
     uint32_t rank;
-    uint32_t paxes;        // nibble d: producer op axis of tensor dimension d
-    uint32_t caxes;        // nibble d: consumer op axis of tensor dimension d
+    uint32_t paxes;        // nibble d: source op axis of tensor dimension d
+    uint32_t caxes;        // nibble d: target op axis of tensor dimension d
     uint32_t pad;
 };
 
@@ -74,11 +74,12 @@ hipError_t taps_launch_describe(const taps_strategy *s, uint64_t total, taps_des
 hipError_t taps_launch_node_costs(const taps_op *ops, uint32_t n_ops, const uint64_t *offsets,
                                   const taps_desc *desc, uint64_t total, const taps_launch &lp,
                                   taps_table out, hipStream_t stream);
+// reverse: the backward tables (source side = the consumer's input map).
 hipError_t taps_launch_edge_setup(const taps_op *ops, const taps_edge *edges, uint32_t n_edges,
                                   const uint64_t *op_offsets, const uint64_t *edge_offsets,
                                   const uint64_t *seg_begin, const taps_launch &lp,
-                                  taps_edge_params *params, uint64_t n_segs, taps_row_ref *segs,
-                                  hipStream_t stream);
+                                  bool reverse, taps_edge_params *params, uint64_t n_segs,
+                                  taps_row_ref *segs, hipStream_t stream);
 hipError_t taps_launch_edge_costs(const taps_edge_params *params, const taps_row_ref *rows,
                                   uint64_t n_rows, const taps_desc *desc, const taps_launch &lp,
                                   taps_table out, hipStream_t stream);

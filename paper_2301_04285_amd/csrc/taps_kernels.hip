@@ -234,7 +234,7 @@ __global__ __launch_bounds__(256) void k_edge_setup(const taps_op *__restrict__ 
                                                     const uint64_t *__restrict__ op_offsets,
                                                     const uint64_t *__restrict__ edge_offsets,
                                                     const uint64_t *__restrict__ seg_begin,
-                                                    taps_launch lp,
+                                                    taps_launch lp, uint32_t reverse,
                                                     taps_edge_params *__restrict__ params) {
     const uint32_t e = blockIdx.x * blockDim.x + threadIdx.x;
     if (e >= n_edges) return;
@@ -254,13 +254,16 @@ __global__ __launch_bounds__(256) void k_edge_setup(const taps_op *__restrict__ 
         ca |= (uint32_t)(Tc.axis[d] & 7u) << (4u * d);
     }
     p.scale = taps_make_scaler(bytes, lp.inv_n_bintra, lp.inv_n_binter);
-    p.src_base = (uint32_t)op_offsets[E.src_op];
-    p.dst_base = (uint32_t)op_offsets[E.dst_op];
-    p.ns = (uint32_t)(op_offsets[E.src_op + 1] - op_offsets[E.src_op]);
-    p.nd = (uint32_t)(op_offsets[E.dst_op + 1] - op_offsets[E.dst_op]);
+    // the source side of the redistribution: the producer's output map, or for
+    // the backward tables the consumer's input map (the gradient moves back)
+    const uint32_t from = reverse ? E.dst_op : E.src_op, to = reverse ? E.src_op : E.dst_op;
+    p.src_base = (uint32_t)op_offsets[from];
+    p.dst_base = (uint32_t)op_offsets[to];
+    p.ns = (uint32_t)(op_offsets[from + 1] - op_offsets[from]);
+    p.nd = (uint32_t)(op_offsets[to + 1] - op_offsets[to]);
     p.rank = T.rank;
-    p.paxes = pa;
-    p.caxes = ca;
+    p.paxes = reverse ? ca : pa;
+    p.caxes = reverse ? pa : ca;
     p.pad = 0;
     params[e] = p;
 }
@@ -279,7 +282,7 @@ __global__ __launch_bounds__(256) void k_row_map(const uint64_t *__restrict__ se
     const uint64_t k = r - seg_begin[e];
     taps_row_ref ref;
     ref.edge = e;
-    ref.strategy = (uint32_t)(op_offsets[edges[e].src_op] + k / per_row);
+    ref.strategy = (uint32_t)(params[e].src_base + k / per_row);
     ref.first_col = (uint32_t)(k % per_row) * (TAPS_TILE_COLS * TAPS_SEG_TILES);
     ref.pad = 0;
     segs[r] = ref;
@@ -425,11 +428,12 @@ hipError_t taps_launch_node_costs(const taps_op *ops, uint32_t n_ops, const uint
 hipError_t taps_launch_edge_setup(const taps_op *ops, const taps_edge *edges, uint32_t n_edges,
                                   const uint64_t *op_offsets, const uint64_t *edge_offsets,
                                   const uint64_t *seg_begin, const taps_launch &lp,
-                                  taps_edge_params *params, uint64_t n_segs, taps_row_ref *segs,
-                                  hipStream_t stream) {
+                                  bool reverse, taps_edge_params *params, uint64_t n_segs,
+                                  taps_row_ref *segs, hipStream_t stream) {
     if (n_edges == 0) return hipSuccess;
     hipLaunchKernelGGL(k_edge_setup, dim3(blocks_for(n_edges, 256)), dim3(256), 0, stream, ops,
-                       edges, n_edges, op_offsets, edge_offsets, seg_begin, lp, params);
+                       edges, n_edges, op_offsets, edge_offsets, seg_begin, lp,
+                       reverse ? 1u : 0u, params);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess || n_segs == 0) return err;
     hipLaunchKernelGGL(k_row_map, dim3(blocks_for(n_segs, 256)), dim3(256), 0, stream, seg_begin,

@@ -75,6 +75,19 @@ def _scale(node, edge):
                [float(np.max(np.abs(m))) for m in edge if m.size] + [1e-300])
 
 
+def add_backward(graph, tables_edge, backward, offsets, field: str):
+    """Per-edge (S_src, S_dst) matrices with each pair's backward cost added: the
+    backward table of edge e is consumer-major (S_dst, S_src)."""
+    offs = np.asarray(offsets, dtype=np.int64)
+    b_all = backward[field].cpu().numpy().astype(np.float64)
+    out, pos = [], 0
+    for x, e in enumerate(graph.edges):
+        ns, nd = offs[e.src + 1] - offs[e.src], offs[e.dst + 1] - offs[e.dst]
+        out.append(tables_edge[x] + b_all[pos:pos + ns * nd].reshape(nd, ns).T)
+        pos += ns * nd
+    return out
+
+
 def solve(graph, node: Sequence[np.ndarray], edge: Sequence[np.ndarray],
           time_limit: float = 600.0, within=None, maximise: bool = False) -> Plan:
     """Cheapest plan: one strategy per operator minimising node plus edge costs.
@@ -235,6 +248,8 @@ def main() -> int:
     ap.add_argument("--time-limit", type=float, default=300.0, help="seconds per ILP")
     ap.add_argument("--range-time-limit", type=float, default=60.0,
                     help="seconds per solve of the volume-optimal range")
+    ap.add_argument("--with-backward", action="store_true",
+                    help="charge each edge in both directions (forward + backward tables)")
     args = ap.parse_args()
 
     import torch
@@ -250,10 +265,16 @@ def main() -> int:
         torch.cuda.synchronize()
         nt, et = host_tables(g, tabs, "t")
         nv, ev = host_tables(g, tabs, "vol")
+        if args.with_backward:
+            _, back = taps.taps_edge_costs(g, cl, tabs.strategies, tabs.op_offsets, backward=True)
+            et = add_backward(g, et, back, tabs.op_offsets, "t")
+            ev = add_backward(g, ev, back, tabs.op_offsets, "vol")
+            del back
         r = compare(g, nt, et, nv, ev, args.time_limit, args.range_time_limit)
         r.pop("topology_plan")
         r.pop("volume_plans")
-        print(json.dumps({"workload": name, **r}), flush=True)
+        print(json.dumps({"workload": name, "directions": "forward+backward" if
+                          args.with_backward else "forward", **r}), flush=True)
     return 0
 
 

@@ -88,6 +88,8 @@ def load():
                                       P(C.c_uint64), Table, C.c_uint64, C.c_void_p]
         L.taps_edge_costs_shared.restype = C.c_int
         L.taps_edge_costs_shared.argtypes = L.taps_edge_costs.argtypes
+        L.taps_edge_costs_backward.restype = C.c_int
+        L.taps_edge_costs_backward.argtypes = L.taps_edge_costs.argtypes
         L.taps_set_edge_kernel_events.restype = C.c_int
         L.taps_set_edge_kernel_events.argtypes = [C.c_void_p, C.c_void_p]
         L.taps_status_str.restype = C.c_char_p
@@ -249,10 +251,13 @@ def taps_node_costs(graph, cluster, strategies, op_offsets, out=None, stream=Non
 
 
 def taps_edge_costs(graph, cluster, strategies, op_offsets, out=None, stream=None,
-                    size_only=False, shared=False):
+                    size_only=False, shared=False, backward=False):
     """(edge_offsets numpy uint64 [n_edges+1], edge table dict of device
     tensors or None for a size query).  ``shared``: taps_edge_costs_shared
-    (identical tables computed once)."""
+    (identical tables computed once); ``backward``: taps_edge_costs_backward
+    (the gradient's direction, tables consumer-major)."""
+    if shared and backward:
+        raise ValueError("shared tables are computed for the forward direction only")
     g = _graph(graph)
     cl = pack_cluster(cluster)
     offs = np.ascontiguousarray(op_offsets, dtype=np.uint64)
@@ -267,10 +272,11 @@ def taps_edge_costs(graph, cluster, strategies, op_offsets, out=None, stream=Non
             return eoffs, None
         out = alloc_table(int(eoffs[-1]), device=strategies.device)
     cap = min(int(v.numel()) for v in out.values())
-    fn = L.taps_edge_costs_shared if shared else L.taps_edge_costs
-    st = fn(C.byref(g.struct), C.byref(cl), sptr, _u64_array(offs), _u64_array(eoffs),
-            _table(out), cap, _stream(stream))
-    _check(st, "taps_edge_costs_shared" if shared else "taps_edge_costs")
+    name = ("taps_edge_costs_shared" if shared else
+            "taps_edge_costs_backward" if backward else "taps_edge_costs")
+    st = getattr(L, name)(C.byref(g.struct), C.byref(cl), sptr, _u64_array(offs),
+                          _u64_array(eoffs), _table(out), cap, _stream(stream))
+    _check(st, name)
     total = int(eoffs[-1])
     return eoffs, {k: v[:total] for k, v in out.items()}
 

@@ -19,8 +19,9 @@ def lib():
 def test_exports_every_declared_symbol(lib):
     declared = T.declared_symbols()
     assert declared == sorted(["taps_enumerate_strategies", "taps_node_costs", "taps_edge_costs",
-                               "taps_edge_costs_shared", "taps_set_edge_kernel_events",
-                               "taps_status_str", "taps_last_error"])
+                               "taps_edge_costs_shared", "taps_edge_costs_backward",
+                               "taps_set_edge_kernel_events", "taps_status_str",
+                               "taps_last_error"])
     out = subprocess.run(["nm", "-D", "--defined-only", T.LIB_PATH], capture_output=True,
                          text=True, check=True).stdout
     exported = {line.split()[-1] for line in out.splitlines() if line.strip()}
@@ -157,7 +158,7 @@ def test_capacity_and_partial_tables(lib):
     eo = np.zeros(3, np.uint64)
     fake = T.Table(256, 256, 256, 256, 256)   # never dereferenced: the checks fail first
     partial = T.Table(256, None, 256, 256, 256)
-    for fn in (lib.taps_edge_costs, lib.taps_edge_costs_shared):
+    for fn in (lib.taps_edge_costs, lib.taps_edge_costs_shared, lib.taps_edge_costs_backward):
         assert fn(C.byref(g.struct), C.byref(cl), C.c_void_p(256), T._u64_array(offs),
                   T._u64_array(eo), fake, 71, None) == T.ERR_CAPACITY
         assert np.all(eo == 0)   # nothing written on error

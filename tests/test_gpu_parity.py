@@ -370,3 +370,52 @@ def test_shared_tables_largest_config(T):
     assert _same_tables(a.edge, b.edge)
     del a, b
     torch.cuda.empty_cache()
+
+
+def backward_check(T, graph, cluster, name, edges=None):
+    """taps_edge_costs_backward against the oracle's backward tables, entry by entry."""
+    import torch
+    offs, strat = T.taps_enumerate_strategies(graph, cluster)
+    eoffs, tab = T.taps_edge_costs(graph, cluster, strat, offs, backward=True)
+    torch.cuda.synchronize()
+    say(f"[gpu] backward {name}: {int(eoffs[-1])} entries")
+    ref_strats = [O.enumerate_strategies(op, cluster.devices) for op in graph.ops]
+    got = _host(tab)
+    for x, e in enumerate(graph.edges):
+        if edges is not None and x not in edges:
+            continue
+        a, b = int(eoffs[x]), int(eoffs[x + 1])
+        ref = O.edge_table_reverse(graph.ops[e.src], ref_strats[e.src], graph.ops[e.dst], e.slot,
+                                   ref_strats[e.dst], cluster)
+        assert_records({f: v[a:b] for f, v in got.items()}, ref, f"{name} backward edge {x}")
+
+
+@pytest.mark.gpu
+def test_backward_tables(T):
+    for cfg in (1, 2, 4):
+        w = W.config(cfg)
+        name, cl = w.clusters[0]
+        backward_check(T, w.graph, cl, f"{w.name}/{name}")
+    w = W.config(3)
+    for name, cl in w.clusters:
+        backward_check(T, W.leading_ops(w.graph, 28), cl, f"{w.name}/{name} (two layers)")
+    rng = random.Random(4242)
+    n = 0
+    while n < 12:
+        g = W.random_graph(rng, rng.randint(2, 6), max_axes=5, max_rank=4, len_pow_range=(1, 8))
+        k = rng.randint(0, 7)
+        N = 1 << k
+        L = 1 << rng.randint(0, k)
+        cl = W.Cluster(N // L, L, 600 * W.GB, rng.choice([12, 25, 100]) * W.GB)
+        try:
+            backward_check(T, g, cl, f"random {n}")
+        except T.TapsError:
+            continue
+        n += 1
+
+
+@pytest.mark.gpu
+def test_backward_tables_largest_config_one_layer(T):
+    w = W.config(5)
+    name, cl = w.clusters[0]
+    backward_check(T, W.leading_ops(w.graph, 14), cl, f"{w.name}/{name} (one layer)")

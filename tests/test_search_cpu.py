@@ -140,3 +140,26 @@ def test_volume_baseline_range_brackets_every_volume_optimal_plan(oracle_lib):
         assert _close(r["t_volume_plans_s"][0], min(ts))
         assert _close(r["t_volume_plans_s"][1], max(ts))
         assert _close(r["t_topology_plan_s"], min(S.plan_cost(g, nt, et, p) for p in plans))
+
+
+def test_backward_tables_add_pairwise(oracle_lib):
+    """add_backward lines the consumer-major backward table up with the forward pairs."""
+    import torch
+    w = W.config(1)
+    g, cl = w.graph, w.clusters[0][1]
+    strats = [oracle_lib.enumerate_strategies(op, cl.devices) for op in g.ops]
+    offs = np.concatenate([[0], np.cumsum([len(s) for s in strats])])
+    fwd = [np.asarray(oracle_lib.edge_table(g.ops[e.src], strats[e.src], g.ops[e.dst], e.slot,
+                                            strats[e.dst], cl)["t"], np.float64) for e in g.edges]
+    rev = [oracle_lib.edge_table_reverse(g.ops[e.src], strats[e.src], g.ops[e.dst], e.slot,
+                                         strats[e.dst], cl)["t"] for e in g.edges]
+    flat = {"t": torch.from_numpy(np.concatenate([r.ravel() for r in rev]))}
+    both = S.add_backward(g, fwd, flat, offs, "t")
+    for x, e in enumerate(g.edges):
+        for i in range(len(strats[e.src])):
+            for j in range(len(strats[e.dst])):
+                c = oracle_lib.edge_cost(g.ops[e.src], strats[e.src][i], g.ops[e.dst], e.slot,
+                                         strats[e.dst][j], cl)[0]
+                b = oracle_lib.edge_cost_reverse(g.ops[e.src], strats[e.src][i], g.ops[e.dst],
+                                                 e.slot, strats[e.dst][j], cl)[0]
+                assert abs(both[x][i, j] - (c + b)) <= 1e-15 * max(1.0, c + b)
