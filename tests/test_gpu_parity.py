@@ -232,16 +232,38 @@ def test_capacity_error_on_device(T):
     import ctypes as C
     g = T.pack_graph(w.graph)
     c = T.pack_cluster(cl)
+    small.fill_(0xAB)
     st = T.load().taps_enumerate_strategies(C.byref(g.struct), C.byref(c), T._u64_array(offs),
                                             C.c_void_p(small.data_ptr()), int(offs[-1]) - 1, None)
     assert st == T.ERR_CAPACITY
+    torch.cuda.synchronize()
+    assert bool((small == 0xAB).all()), "nothing is written on a capacity error"
 
 
 def test_no_strategy_error(T):
+    import torch
     g = W.Graph([W.Op("odd", "x", ("a",), (3,), (True,), 2, ins=((0,),), ws=(), out=(0,))], [])
     with pytest.raises(T.TapsError) as ex:
         T.taps_enumerate_strategies(g, W.Cluster(2, 2, 10, 1))
     assert ex.value.status == T.ERR_NO_STRATEGY
+    # with a caller buffer: nothing is written either
+    ok = W.matmul("ok", 8, 8, 8, 2)
+    g2 = W.Graph([ok, g.ops[0]], [])
+    buf = torch.full((64, 16), 0xAB, dtype=torch.uint8, device="cuda")
+    with pytest.raises(T.TapsError) as ex:
+        T.taps_enumerate_strategies(g2, W.Cluster(2, 2, 10, 1), out=buf)
+    assert ex.value.status == T.ERR_NO_STRATEGY
+    torch.cuda.synchronize()
+    assert bool((buf == 0xAB).all())
+
+
+def test_shared_and_backward_on_empty_graphs(T):
+    cl = W.Cluster(2, 2, 10, 1)
+    for g in (W.Graph(), W.Graph([W.matmul("a", 8, 8, 8, 2)], [])):
+        offs, strat = T.taps_enumerate_strategies(g, cl)
+        for kw in ({"shared": True}, {"backward": True}):
+            eoffs, tab = T.taps_edge_costs(g, cl, strat, offs, **kw)
+            assert list(eoffs) == [0]
 
 
 def test_repeatable_bitwise(T):
