@@ -604,6 +604,9 @@ __host__ __device__ inline taps_run taps_alg1(const taps_row &P, const taps_col 
 //      lowest position first; after each, the axis itself is sliced back if
 //      its target is free, and the axis targeting the freed position is
 //      sliced if no dimension uses it.
+// Step 2 is step 3 on positions no consumer axis targets (nothing is freed
+// for anyone there), so both run as one loop over the held axes: the
+// untargeted ones in producer order, then the targeted ones.
 __host__ __device__ inline taps_run taps_rearrange(const taps_row &P, const taps_col &Q,
                                                    const taps_lv &L, const taps_limit &lim,
                                                    const taps_keys &K) {
@@ -617,36 +620,15 @@ __host__ __device__ inline taps_run taps_rearrange(const taps_row &P, const taps
     s.e = P.e0;
     bool stopped = false;
     taps_slice(L, s);
-    // 2. untargeted positions
-    const uint32_t ug = s.ats & ~L.tgtsrc;
-    const uint32_t bounce = ug & L.dst & ~s.blk;
-    uint32_t x = P.to_rank[ug];
+    // producer ranks of the untargeted held axes in bits 0-7, of the targeted ones in bits 8-15
+    uint32_t x = (uint32_t)P.to_rank[s.ats & ~L.tgtsrc] |
+                 ((uint32_t)P.to_rank[s.ats & L.tgtsrc] << 8);
     while (x) {
         if (taps_hopeless(c, lim, K)) {
             stopped = true;
             break;
         }
-        const uint32_t top = taps_rank_level(P, taps_ctz(x));
-        x &= x - 1u;
-        const uint32_t b = 1u << top;
-        const taps_ax a = taps_axis(L, top);
-        taps_cost(c, top, a, P.lam, s.e, s.unused);
-        s.ats &= ~b;
-        if (bounce & b) {
-            s.atd |= b;
-        } else {
-            s.unused |= a.lv;
-            s.e += a.w;
-        }
-    }
-    // 3. targeted positions
-    x = stopped ? 0u : P.to_rank[s.ats];
-    while (x) {
-        if (taps_hopeless(c, lim, K)) {
-            stopped = true;
-            break;
-        }
-        const uint32_t top = taps_rank_level(P, taps_ctz(x));
+        const uint32_t top = taps_rank_level(P, taps_ctz(x) & 7u);
         x &= x - 1u;
         const uint32_t b = 1u << top;
         const taps_ax a = taps_axis(L, top);
