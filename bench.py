@@ -12,13 +12,16 @@ Prints one JSON line.  `value` is edge entries per second of whole steps;
 `roofline` relates the edge-table kernel (which dominates the step), timed
 with HIP events the library records right around its launch on the same
 stream, to MI355X's 8 TB/s HBM: each entry writes 36 bytes (t 8, vol 8,
-intra 8, inter 8, meta 4).  `cpu_baseline` times the CPU oracle, single-threaded, on the
-first layers of the same graph.  `shared_tables` times the same build with
+intra 8, inter 8, meta 4).  `cpu_baseline` times the CPU oracle,
+single-threaded, on the first layers of the same graph.  `shared_tables` times the same build with
 identical edge tables computed once (the paper searches one layer of a stack
 of identical layers) and checks the result equal to the full evaluation;
-`value` and `roofline` always come from the full evaluation.  `roofline.traffic` is the edge kernel's HBM
-bytes per launch from the committed rocprofv3 counter summary (null once the
-kernel sources differ from the ones the counters were taken with).
+`bandwidth_sweep` builds the tables at four inter-node bandwidths in
+one pass (candidates costed once per entry, one selection and store per
+point); `value` and `roofline` always come from the full evaluation.
+`roofline.traffic` is the edge kernel's HBM bytes per launch from the
+committed rocprofv3 counter summary (null once the kernel sources differ from
+the ones the counters were taken with).
 """
 from __future__ import annotations
 
@@ -100,6 +103,10 @@ def main() -> int:
     ap.add_argument("--shared", type=int, default=1,
                     help="also time taps_edge_costs_shared (identical tables computed once) "
                          "and report it under shared_tables (0 = skip)")
+    ap.add_argument("--sweep", type=int, default=4, choices=range(5),
+                    help="also time taps_edge_costs_sweep at this many inter-node bandwidths "
+                         "(the wide-MLP workload's 12.5-100 GB/s points, the benchmark's cluster "
+                         "last) and report it under bandwidth_sweep (0 = skip)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES bytes (to scale HBM "
                          "traffic counters), then exit")
@@ -138,20 +145,23 @@ def main() -> int:
     strategies = int(tabs.op_offsets[-1])
     log(f"[bench] {strategies} strategies, {entries} edge entries")
 
-    def step(ev=None, shared=False, edge_out=None):
+    def step(ev=None, shared=False, edge_out=None, points=None):
         offs, strat = taps.taps_enumerate_strategies(g, cl, stream=stream, out=tabs.strategies)
         taps.taps_node_costs(g, cl, strat, offs, out=tabs.node, stream=stream)
         if ev is not None:
             ev[0].record(stream)
             taps.taps_set_edge_kernel_events(ev[2], ev[3])
-        taps.taps_edge_costs(g, cl, strat, offs, out=edge_out or tabs.edge, stream=stream,
-                             shared=shared)
+        if points:
+            taps.taps_edge_costs_sweep(g, points, strat, offs, out=edge_out, stream=stream)
+        else:
+            taps.taps_edge_costs(g, cl, strat, offs, out=edge_out or tabs.edge, stream=stream,
+                                 shared=shared)
         if ev is not None:
             ev[1].record(stream)
 
-    def timed(shared=False, edge_out=None):
+    def timed(shared=False, edge_out=None, points=None):
         for _ in range(args.warmup):
-            step(shared=shared, edge_out=edge_out)
+            step(shared=shared, edge_out=edge_out, points=points)
         torch.cuda.synchronize()
         # per step: the whole edge call, and the edge-table kernel alone (recorded by
         # the library on the same stream right around that launch)
@@ -163,7 +173,7 @@ def main() -> int:
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         for k in range(args.steps):
-            step(events[k], shared=shared, edge_out=edge_out)
+            step(events[k], shared=shared, edge_out=edge_out, points=points)
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
         edge_ms = float(np.mean([ev[0].elapsed_time(ev[1]) for ev in events]))
@@ -216,6 +226,28 @@ def main() -> int:
             "hbm_write_frac": bytes_per_launch / (s_kernel * 1e-3) / 1e9 / HBM_PEAK_GBPS,
             "equal_to_full_evaluation": equal}
         del other
+    if args.sweep:
+        # the same graph at several inter-node bandwidths in one pass
+        # (taps_edge_costs_sweep); the point equal to the benchmark's cluster is
+        # checked equal to the full evaluation above
+        inter = [12.5e9, 25e9, 50e9, 100e9][-args.sweep:]
+        points = [W.Cluster(cl.nodes, cl.devices_per_node, cl.bw_intra, int(b)) for b in inter]
+        points[-1] = cl
+        outs = [taps.alloc_table(entries, device="cuda") for _ in points]
+        w_step, w_edge, w_kernel = timed(edge_out=outs, points=points)
+        equal = all(torch.equal(tabs.edge[f][:entries], outs[-1][f][:entries])
+                    for f in ("t", "vol", "intra", "inter", "meta"))
+        k = len(points)
+        log(f"[bench] bandwidth sweep, {k} points: {w_step:.3f} ms/step, edge call "
+            f"{w_edge:.3f} ms, edge kernel {w_kernel:.3f} ms, last point equal to the full "
+            f"evaluation: {equal}")
+        out["bandwidth_sweep"] = {
+            "inter_GBps": [p.bw_inter / 1e9 for p in points], "ms_per_step": w_step,
+            "edge_call_ms": w_edge, "edge_kernel_ms": w_kernel,
+            "edge_entries_per_s": k * entries / (w_step * 1e-3),
+            "hbm_write_frac": k * bytes_per_launch / (w_kernel * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+            "equal_to_single_point": equal}
+        del outs
     if args.cpu_layers > 0 and args.config == 5:
         log(f"[bench] CPU oracle baseline on {args.cpu_layers} layers")
         out["cpu_baseline"] = cpu_baseline(w, cl, args.cpu_layers)

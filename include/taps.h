@@ -77,6 +77,7 @@ extern "C" {
 #define TAPS_MAX_INPUTS 4   /* activation inputs of one operator */
 #define TAPS_MAX_WEIGHTS 4  /* weights of one operator */
 #define TAPS_MAX_LEVELS 8   /* N <= 2^8 = 256 devices */
+#define TAPS_MAX_SWEEP 8    /* bandwidth points of one taps_edge_costs_sweep call */
 #define TAPS_MAX_TENSOR_BYTES (1ull << 40) /* keeps every volume exact in 64 bits */
 
 typedef enum {
@@ -225,11 +226,34 @@ taps_status taps_edge_costs_backward(const taps_graph *graph, const taps_cluster
                                      uint64_t *edge_offsets, taps_table out, uint64_t capacity,
                                      void *stream);
 
+/* The tables of taps_edge_costs at several bandwidth points in one pass:
+ * clusters[k] (k < n_points <= TAPS_MAX_SWEEP) must have the same nodes and
+ * devices_per_node and may differ in bw_intra and bw_inter.  The candidate
+ * sequences of an entry (Table 2) and their volumes, intra- and inter-node
+ * bytes and collective counts do not depend on the bandwidths; only the
+ * choice among them (Eq. 9, 10, 14 times) and t do.  So each entry's
+ * candidates are costed once and the choice, scaling and store are made once
+ * per point -- the bandwidth sweep of the evaluation (the wide-MLP workload
+ * is costed at several inter-node bandwidths).  out[k] receives the table of
+ * clusters[k], bit for bit what taps_edge_costs(graph, &clusters[k], ...)
+ * writes.
+ *   out           host array of n_points tables (device arrays of `capacity`
+ *                 records each, same layout as taps_edge_costs); out NULL or
+ *                 every array of every table NULL: size query.
+ * TAPS_ERR_ARG if n_points is 0 or above TAPS_MAX_SWEEP, if the points differ
+ * in nodes or devices_per_node, or if some but not all arrays are NULL; other
+ * arguments and errors as taps_edge_costs. */
+taps_status taps_edge_costs_sweep(const taps_graph *graph, const taps_cluster *clusters,
+                                  uint32_t n_points, const taps_strategy *strategies,
+                                  const uint64_t *op_offsets, uint64_t *edge_offsets,
+                                  const taps_table *out, uint64_t capacity, void *stream);
+
 /* Profiling aid, not part of the method: `before` and `after` are HIP events
  * (hipEvent_t, created by the caller, passed as plain pointers) that the
- * calling thread's next taps_edge_costs, taps_edge_costs_shared or
- * taps_edge_costs_backward call that launches the edge-table kernel records on its stream immediately before and
- * after that kernel (and, for shared tables, the copies after it), so that
+ * calling thread's next taps_edge_costs, taps_edge_costs_shared,
+ * taps_edge_costs_backward or taps_edge_costs_sweep call that launches the
+ * edge-table kernel records on its stream immediately before and after that
+ * kernel (and, for shared tables, the copies after it), so that
  * the caller can time the kernel alone.  The setting is thread-local,
  * used once and then cleared; two NULLs clear it.  The events stay owned by
  * the caller.  TAPS_ERR_ARG if exactly one of them is NULL. */

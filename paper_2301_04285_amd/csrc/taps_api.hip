@@ -348,13 +348,29 @@ taps_status share_edges(const taps_graph *g, const uint64_t *op_offsets,
     return TAPS_OK;
 }
 
-taps_status edge_costs(const taps_graph *graph, const taps_cluster *cluster,
+// Edge tables of one graph at n_points bandwidth points (clusters that differ
+// only in their bandwidths), table k in outs[k]; outs NULL or every table's
+// arrays NULL: size query.
+taps_status edge_costs(const taps_graph *graph, const taps_cluster *clusters, uint32_t n_points,
                        const taps_strategy *strategies, const uint64_t *op_offsets,
-                       uint64_t *edge_offsets, taps_table out, uint64_t capacity, void *stream_,
-                       bool share, bool reverse) {
+                       uint64_t *edge_offsets, const taps_table *outs, uint64_t capacity,
+                       void *stream_, bool share, bool reverse) {
     g_last_error.clear();
-    taps_launch lp;
-    taps_status st = check_cluster(cluster, &lp);
+    if (!clusters) return fail(TAPS_ERR_ARG, "cluster is NULL");
+    if (n_points == 0 || n_points > TAPS_MAX_SWEEP)
+        return fail(TAPS_ERR_ARG, "%u bandwidth points, 1 to %u allowed", n_points,
+                    (unsigned)TAPS_MAX_SWEEP);
+    taps_launch lps[TAPS_MAX_SWEEP];
+    taps_status st = TAPS_OK;
+    for (uint32_t k = 0; k < n_points && st == TAPS_OK; ++k) {
+        st = check_cluster(&clusters[k], &lps[k]);
+        if (st == TAPS_OK && (clusters[k].nodes != clusters[0].nodes ||
+                              clusters[k].devices_per_node != clusters[0].devices_per_node))
+            st = fail(TAPS_ERR_ARG, "bandwidth point %u: %u x %u devices, point 0 has %u x %u", k,
+                      clusters[k].nodes, clusters[k].devices_per_node, clusters[0].nodes,
+                      clusters[0].devices_per_node);
+    }
+    const taps_launch &lp = lps[0];
     if (st == TAPS_OK) st = check_graph(graph, true);
     if (st == TAPS_OK) st = check_offsets(graph, op_offsets);
     if (st != TAPS_OK) return st;
@@ -371,9 +387,14 @@ taps_status edge_costs(const taps_graph *graph, const taps_cluster *cluster,
         all_segs += ns * ((nd + TAPS_TILE_COLS * TAPS_SEG_TILES - 1) /
                           (TAPS_TILE_COLS * TAPS_SEG_TILES));
     }
-    const bool none = !out.t && !out.vol && !out.intra && !out.inter && !out.meta;
-    const bool all = out.t && out.vol && out.intra && out.inter && out.meta;
-    if (!none && !all) return fail(TAPS_ERR_ARG, "table arrays must be all set or all NULL");
+    bool none = true, all = outs != nullptr;
+    for (uint32_t k = 0; outs && k < n_points; ++k) {
+        const taps_table &o = outs[k];
+        none = none && !o.t && !o.vol && !o.intra && !o.inter && !o.meta;
+        all = all && o.t && o.vol && o.intra && o.inter && o.meta;
+    }
+    if (!none && !all)
+        return fail(TAPS_ERR_ARG, "table arrays must be all set or all NULL (every point)");
     if (all && eoff[n_edges] > capacity)
         return fail(TAPS_ERR_CAPACITY, "%llu entries, capacity %llu",
                     (unsigned long long)eoff[n_edges], (unsigned long long)capacity);
@@ -454,11 +475,25 @@ taps_status edge_costs(const taps_graph *graph, const taps_cluster *cluster,
     const hipEvent_t before = g_kernel_before, after = g_kernel_after;
     g_kernel_before = g_kernel_after = nullptr;
     if (err == hipSuccess && before) err = hipEventRecord(before, stream);
-    if (err == hipSuccess)
-        err = taps_launch_edge_costs(d_params, d_segs, n_segs, d_desc, lp, out, stream);
-    if (err == hipSuccess)
+    if (err == hipSuccess && n_points == 1) {
+        err = taps_launch_edge_costs(d_params, d_segs, n_segs, d_desc, lp, outs[0], stream);
+    } else if (err == hipSuccess) {
+        taps_sweep sw;
+        std::memset(&sw, 0, sizeof(sw));
+        sw.count = n_points;
+        for (uint32_t k = 0; k < n_points; ++k) {
+            sw.narrow[k] = lps[k].narrow;
+            sw.b_inter_red[k] = lps[k].b_inter_red;
+            sw.b_intra_red[k] = lps[k].b_intra_red;
+            sw.inv_n_bintra[k] = lps[k].inv_n_bintra;
+            sw.inv_n_binter[k] = lps[k].inv_n_binter;
+            sw.out[k] = outs[k];
+        }
+        err = taps_launch_edge_costs_sweep(d_params, d_segs, n_segs, d_desc, lp, sw, stream);
+    }
+    for (uint32_t k = 0; k < n_points && err == hipSuccess; ++k)
         err = taps_launch_copy_tables(at<taps_copy_task>(dev, ch[5]), (uint32_t)copies.size(),
-                                      at<uint64_t>(dev, ch[6]), out, stream);
+                                      at<uint64_t>(dev, ch[6]), outs[k], stream);
     if (err == hipSuccess && after) err = hipEventRecord(after, stream);
     if (err != hipSuccess) return hip_fail(err, "edge costs");
     return TAPS_OK;
@@ -600,24 +635,32 @@ taps_status taps_edge_costs(const taps_graph *graph, const taps_cluster *cluster
                             const taps_strategy *strategies, const uint64_t *op_offsets,
                             uint64_t *edge_offsets, taps_table out, uint64_t capacity,
                             void *stream) {
-    return edge_costs(graph, cluster, strategies, op_offsets, edge_offsets, out, capacity, stream,
-                      false, false);
+    return edge_costs(graph, cluster, 1, strategies, op_offsets, edge_offsets, &out, capacity,
+                      stream, false, false);
 }
 
 taps_status taps_edge_costs_shared(const taps_graph *graph, const taps_cluster *cluster,
                                    const taps_strategy *strategies, const uint64_t *op_offsets,
                                    uint64_t *edge_offsets, taps_table out, uint64_t capacity,
                                    void *stream) {
-    return edge_costs(graph, cluster, strategies, op_offsets, edge_offsets, out, capacity, stream,
-                      true, false);
+    return edge_costs(graph, cluster, 1, strategies, op_offsets, edge_offsets, &out, capacity,
+                      stream, true, false);
 }
 
 taps_status taps_edge_costs_backward(const taps_graph *graph, const taps_cluster *cluster,
                                      const taps_strategy *strategies, const uint64_t *op_offsets,
                                      uint64_t *edge_offsets, taps_table out, uint64_t capacity,
                                      void *stream) {
-    return edge_costs(graph, cluster, strategies, op_offsets, edge_offsets, out, capacity, stream,
-                      false, true);
+    return edge_costs(graph, cluster, 1, strategies, op_offsets, edge_offsets, &out, capacity,
+                      stream, false, true);
+}
+
+taps_status taps_edge_costs_sweep(const taps_graph *graph, const taps_cluster *clusters,
+                                  uint32_t n_points, const taps_strategy *strategies,
+                                  const uint64_t *op_offsets, uint64_t *edge_offsets,
+                                  const taps_table *out, uint64_t capacity, void *stream) {
+    return edge_costs(graph, clusters, n_points, strategies, op_offsets, edge_offsets, out,
+                      capacity, stream, false, false);
 }
 
 }  // extern "C"

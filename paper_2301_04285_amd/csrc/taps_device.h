@@ -472,14 +472,20 @@ __host__ __device__ inline bool taps_less(const taps_fac &a, const taps_fac &b,
 // and its volume, so once the running key reaches the best key so far and
 // the running volume reaches the smallest volume so far it can neither be
 // chosen (ties go to the earlier candidate) nor lower the volume.
+// Without a single key (several bandwidth points) a candidate is hopeless
+// once its intra- and inter-node bytes both reach the first candidate's:
+// then its key is at least as large under every pair of bandwidths.
 struct taps_limit {
-    bool on;
+    bool on;          // compare keys
+    bool dominated;   // compare intra and inter
     uint64_t key;
-    uint32_t vol;
+    uint32_t vol, intra, inter;
 };
 
 __host__ __device__ inline bool taps_hopeless(const taps_fac &c, const taps_limit &lim,
                                               const taps_keys &K) {
+    if (lim.dominated)
+        return c.vol >= lim.vol && c.intra >= lim.intra && c.inter >= lim.inter;
     return lim.on && c.vol >= lim.vol && taps_key64(c, K) >= lim.key;
 }
 
@@ -774,8 +780,10 @@ __host__ __device__ inline taps_pick taps_edge_select(const taps_row &P, const t
     k.ok = r0.ok;
     taps_limit lim;
     lim.on = K.narrow;
+    lim.dominated = false;
     lim.key = taps_key64(k.best, K);
     lim.vol = k.vmin;
+    lim.intra = lim.inter = 0;
     if (r0.n_a2a) {   // without AllToAll the sequence would be the same
         const taps_run r1 = taps_rearrange(P, Q, L, lim, K);
         k.ok = k.ok && r1.ok;
@@ -794,6 +802,86 @@ __host__ __device__ inline taps_pick taps_edge_select(const taps_row &P, const t
     }
     k.vmin = c2.vol < k.vmin ? c2.vol : k.vmin;
     return k;
+}
+
+// The candidates of one entry costed once for several bandwidth points: the
+// factor integers of a sequence do not depend on the bandwidths, only the
+// order of two candidates does.  The rearrange candidate stops early only
+// once it can neither be chosen at any point (its intra- and inter-node
+// bytes have reached the first candidate's; ties go to the first) nor lower
+// the volume, so every selection below equals taps_edge_select under its
+// own keys.
+struct taps_cands {
+    taps_fac c[3];   // replace, rearrange, remove
+    uint32_t vmin;   // smallest volume among them
+    bool has_rearrange;
+    bool ok;
+};
+
+__host__ __device__ inline taps_cands taps_edge_candidates(const taps_row &P, const taps_col &Q,
+                                                           const taps_keys &any) {
+    taps_lv L;
+    taps_unify(P, Q, L);
+    const taps_run r0 = taps_alg1(P, Q, L);
+    taps_cands k;
+    k.c[0] = r0.c;
+    k.ok = r0.ok;
+    k.vmin = r0.c.vol;
+    k.has_rearrange = r0.n_a2a != 0;   // without AllToAll the sequence would be the same
+    taps_fac_zero(k.c[1]);
+    if (k.has_rearrange) {
+        taps_limit lim;
+        lim.on = false;
+        lim.dominated = true;
+        lim.key = 0;
+        lim.vol = r0.c.vol;
+        lim.intra = r0.c.intra;
+        lim.inter = r0.c.inter;
+        const taps_run r1 = taps_rearrange(P, Q, L, lim, any);
+        k.ok = k.ok && r1.ok;
+        if (r1.stopped) {
+            k.has_rearrange = false;
+        } else {
+            k.c[1] = r1.c;
+            k.vmin = r1.c.vol < k.vmin ? r1.c.vol : k.vmin;
+        }
+    }
+    k.c[2] = taps_remove(P, L);
+    k.vmin = k.c[2].vol < k.vmin ? k.c[2].vol : k.vmin;
+    return k;
+}
+
+// Selection of taps_edge_select among precomputed candidates, under the
+// keys of one bandwidth point (ties go to the earlier candidate).
+__host__ __device__ inline taps_pick taps_pick_for(const taps_cands &k, const taps_keys &K) {
+    taps_pick p;
+    p.best = k.c[0];
+    p.cand = 0;
+    if (K.narrow) {   // each candidate's key once
+        uint64_t best = taps_key64(k.c[0], K);
+        const uint64_t k1 = taps_key64(k.c[1], K), k2 = taps_key64(k.c[2], K);
+        if (k.has_rearrange && k1 < best) {
+            p.best = k.c[1];
+            p.cand = 1;
+            best = k1;
+        }
+        if (k2 < best) {
+            p.best = k.c[2];
+            p.cand = 2;
+        }
+    } else {
+        if (k.has_rearrange && taps_less(k.c[1], p.best, K)) {
+            p.best = k.c[1];
+            p.cand = 1;
+        }
+        if (taps_less(k.c[2], p.best, K)) {
+            p.best = k.c[2];
+            p.cand = 2;
+        }
+    }
+    p.vmin = k.vmin;
+    p.ok = k.ok;
+    return p;
 }
 
 __host__ __device__ inline taps_entry_out taps_entry_finish(const taps_pick &k,

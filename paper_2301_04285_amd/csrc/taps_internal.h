@@ -83,6 +83,21 @@ hipError_t taps_launch_edge_setup(const taps_op *ops, const taps_edge *edges, ui
 hipError_t taps_launch_edge_costs(const taps_edge_params *params, const taps_row_ref *rows,
                                   uint64_t n_rows, const taps_desc *desc, const taps_launch &lp,
                                   taps_table out, hipStream_t stream);
+// Bandwidth points of one sweep: the keys and per-unit seconds of each, and
+// the table each writes.
+struct taps_sweep {
+    uint32_t count;
+    uint32_t narrow[TAPS_MAX_SWEEP];
+    uint64_t b_inter_red[TAPS_MAX_SWEEP];
+    uint64_t b_intra_red[TAPS_MAX_SWEEP];
+    double inv_n_bintra[TAPS_MAX_SWEEP];
+    double inv_n_binter[TAPS_MAX_SWEEP];
+    taps_table out[TAPS_MAX_SWEEP];
+};
+hipError_t taps_launch_edge_costs_sweep(const taps_edge_params *params, const taps_row_ref *rows,
+                                        uint64_t n_rows, const taps_desc *desc,
+                                        const taps_launch &lp, const taps_sweep &sw,
+                                        hipStream_t stream);
 hipError_t taps_launch_copy_tables(const taps_copy_task *tasks, uint32_t n_tasks,
                                    const uint64_t *dst_list, taps_table out, hipStream_t stream);
 // For each pair p: flags[p] = 0 if strategies[first_a .. +count) equals

@@ -12,6 +12,8 @@
 //                 TAPS_SEG_TILES tiles of 64 consumer strategies, one per lane, the
 //                 next 64 prefetched), TAPS_ROWS_PER_BLOCK segments per workgroup; five
 //                 coalesced non-temporal SoA stores per entry
+//   k_edge_costs_sweep  as k_edge_costs for several bandwidth points: the
+//                 candidates once per entry, one selection and store per point
 //   k_copy_tables shared tables: one workgroup per chunk of a computed
 //                 table, written to every table that shares it
 #include "taps_internal.h"
@@ -332,6 +334,59 @@ __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_co
     }
 }
 
+// Several bandwidth points: the candidates of each entry are costed once and
+// selected, scaled and stored once per point.
+__global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_costs_sweep(
+    const taps_edge_params *__restrict__ params, const taps_row_ref *__restrict__ rows,
+    uint32_t n_segs, const taps_desc *__restrict__ desc, taps_launch lp, taps_sweep sw) {
+    __shared__ uint8_t rank_tab[TAPS_ROWS_PER_BLOCK][256];
+    const uint32_t lane = threadIdx.x % TAPS_TILE_COLS;
+    const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x / TAPS_TILE_COLS);
+    const uint32_t r = blockIdx.x * TAPS_ROWS_PER_BLOCK + wave;
+    const bool live = r < n_segs;
+    const taps_row_ref ref = rows[live ? r : 0u];
+    const taps_edge_params E = params[ref.edge];
+    const taps_desc Dp = desc[ref.strategy];
+    const uint32_t i = ref.strategy - E.src_base;
+    taps_row P;
+    taps_make_row(P, Dp, E.paxes, E.rank, lp.n, lp.lam);
+    taps_fill_rank_table(P, rank_tab[wave], lane, TAPS_TILE_COLS);
+    __syncthreads();
+    if (!live) return;
+    P.to_rank = rank_tab[wave];
+    taps_keys any;
+    any.b_inter_red = sw.b_inter_red[0];
+    any.b_intra_red = sw.b_intra_red[0];
+    any.narrow = sw.narrow[0] != 0;
+    const uint64_t row_out = E.out_offset + (uint64_t)i * E.nd;
+    const taps_desc *col = desc + E.dst_base;
+    const uint32_t c0 = ref.first_col;
+    const uint32_t c1 = E.nd - c0 < TAPS_TILE_COLS * TAPS_SEG_TILES ? E.nd
+                                                                       : c0 + TAPS_TILE_COLS * TAPS_SEG_TILES;
+    taps_desc next = col[c0 + lane < c1 ? c0 + lane : c0];
+    for (uint32_t j0 = c0; j0 < c1; j0 += TAPS_TILE_COLS) {
+        const taps_desc cur = next;
+        const uint32_t j = j0 + lane;
+        const uint32_t jn = j + TAPS_TILE_COLS;
+        if (jn < c1) next = col[jn];
+        if (j < c1) {
+            taps_col Q;
+            taps_make_col(Q, cur, E.caxes, E.rank);
+            const taps_cands cands = taps_edge_candidates(P, Q, any);
+            for (uint32_t k = 0; k < sw.count; ++k) {
+                taps_keys K;
+                K.b_inter_red = sw.b_inter_red[k];
+                K.b_intra_red = sw.b_intra_red[k];
+                K.narrow = sw.narrow[k] != 0;
+                const taps_scaler S = taps_make_scaler(E.scale.tbytes, sw.inv_n_bintra[k],
+                                                       sw.inv_n_binter[k]);
+                const taps_entry_out o = taps_entry_finish(taps_pick_for(cands, K), S);
+                store_entry(sw.out[k], row_out, j, o, o.ok ? o.meta : 0xFFFFFFFFu);
+            }
+        }
+    }
+}
+
 // Shared tables: each task holds `count` (<= TAPS_COPY_CHUNK) consecutive
 // entries of a computed table, loaded once (8 per thread, consecutive
 // threads on consecutive entries) and stored into every table that shares it,
@@ -448,6 +503,17 @@ hipError_t taps_launch_edge_costs(const taps_edge_params *params, const taps_row
     hipLaunchKernelGGL(k_edge_costs, dim3(blocks_for(n_segs, TAPS_ROWS_PER_BLOCK)),
                        dim3(TAPS_TILE_COLS * TAPS_ROWS_PER_BLOCK), 0, stream, params, segs,
                        (uint32_t)n_segs, desc, lp, out);
+    return hipGetLastError();
+}
+
+hipError_t taps_launch_edge_costs_sweep(const taps_edge_params *params, const taps_row_ref *segs,
+                                        uint64_t n_segs, const taps_desc *desc,
+                                        const taps_launch &lp, const taps_sweep &sw,
+                                        hipStream_t stream) {
+    if (n_segs == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_edge_costs_sweep, dim3(blocks_for(n_segs, TAPS_ROWS_PER_BLOCK)),
+                       dim3(TAPS_TILE_COLS * TAPS_ROWS_PER_BLOCK), 0, stream, params, segs,
+                       (uint32_t)n_segs, desc, lp, sw);
     return hipGetLastError();
 }
 

@@ -90,6 +90,10 @@ def load():
         L.taps_edge_costs_shared.argtypes = L.taps_edge_costs.argtypes
         L.taps_edge_costs_backward.restype = C.c_int
         L.taps_edge_costs_backward.argtypes = L.taps_edge_costs.argtypes
+        L.taps_edge_costs_sweep.restype = C.c_int
+        L.taps_edge_costs_sweep.argtypes = [P(GraphS), P(Cluster), C.c_uint32, C.c_void_p,
+                                            P(C.c_uint64), P(C.c_uint64), P(Table), C.c_uint64,
+                                            C.c_void_p]
         L.taps_set_edge_kernel_events.restype = C.c_int
         L.taps_set_edge_kernel_events.argtypes = [C.c_void_p, C.c_void_p]
         L.taps_status_str.restype = C.c_char_p
@@ -279,6 +283,36 @@ def taps_edge_costs(graph, cluster, strategies, op_offsets, out=None, stream=Non
     _check(st, name)
     total = int(eoffs[-1])
     return eoffs, {k: v[:total] for k, v in out.items()}
+
+
+def taps_edge_costs_sweep(graph, clusters, strategies, op_offsets, out=None, stream=None,
+                          size_only=False):
+    """(edge_offsets numpy uint64 [n_edges+1], list of edge table dicts, one per
+    cluster, or None for a size query).  The clusters differ only in their
+    bandwidths; table k equals taps_edge_costs on clusters[k]."""
+    g = _graph(graph)
+    cls = list(clusters)
+    arr = (Cluster * max(len(cls), 1))(*[pack_cluster(c) for c in cls])
+    offs = np.ascontiguousarray(op_offsets, dtype=np.uint64)
+    eoffs = np.zeros(g.n_edges + 1, dtype=np.uint64)
+    L = load()
+    sptr = C.c_void_p(strategies.data_ptr()) if strategies is not None else None
+    if out is None or size_only:   # size query first
+        st = L.taps_edge_costs_sweep(C.byref(g.struct), arr, len(cls), sptr, _u64_array(offs),
+                                     _u64_array(eoffs), None, 0, _stream(stream))
+        _check(st, "taps_edge_costs_sweep")
+        if size_only:
+            return eoffs, None
+        out = [alloc_table(int(eoffs[-1]), device=strategies.device) for _ in cls]
+    if len(out) != len(cls):
+        raise ValueError(f"{len(out)} tables for {len(cls)} bandwidth points")
+    cap = min(int(v.numel()) for o in out for v in o.values())
+    tabs = (Table * len(out))(*[_table(o) for o in out])
+    st = L.taps_edge_costs_sweep(C.byref(g.struct), arr, len(cls), sptr, _u64_array(offs),
+                                 _u64_array(eoffs), tabs, cap, _stream(stream))
+    _check(st, "taps_edge_costs_sweep")
+    total = int(eoffs[-1])
+    return eoffs, [{k: v[:total] for k, v in o.items()} for o in out]
 
 
 def taps_set_edge_kernel_events(before, after) -> None:

@@ -20,7 +20,7 @@ def test_exports_every_declared_symbol(lib):
     declared = T.declared_symbols()
     assert declared == sorted(["taps_enumerate_strategies", "taps_node_costs", "taps_edge_costs",
                                "taps_edge_costs_shared", "taps_edge_costs_backward",
-                               "taps_set_edge_kernel_events", "taps_status_str",
+                               "taps_edge_costs_sweep", "taps_set_edge_kernel_events", "taps_status_str",
                                "taps_last_error"])
     out = subprocess.run(["nm", "-D", "--defined-only", T.LIB_PATH], capture_output=True,
                          text=True, check=True).stdout
@@ -178,6 +178,48 @@ def test_shared_size_query_matches(lib):
     assert lib.taps_edge_costs_shared(C.byref(g.struct), C.byref(cl), None, T._u64_array(offs),
                                       T._u64_array(b), none, 0, None) == T.OK
     assert np.array_equal(a, b)
+
+
+def _sweep(lib, clusters, n=None, tables=None, capacity=0, graph=None, offs=None):
+    g = T.pack_graph(graph or W.mlp2())
+    offs = np.asarray(offs if offs is not None else [0, 9, 13, 22], np.uint64)
+    arr = (T.Cluster * max(len(clusters), 1))(*[T.pack_cluster(c) for c in clusters])
+    eo = np.zeros(g.n_edges + 1, np.uint64)
+    tabs = None if tables is None else (T.Table * len(tables))(*tables)
+    st = lib.taps_edge_costs_sweep(C.byref(g.struct), arr, len(clusters) if n is None else n,
+                                   C.c_void_p(256), T._u64_array(offs), T._u64_array(eo), tabs,
+                                   capacity, None)
+    return st, eo
+
+
+def test_sweep_size_query_matches_single_point(lib):
+    g = W.gpt(2, 64, 4, 32, 4, 2)
+    counts = np.random.default_rng(2).integers(1, 50, len(g.ops))
+    offs = np.concatenate([[0], np.cumsum(counts)]).astype(np.uint64)
+    pts = [W.Cluster(2, 2, 100 * W.GB, b * W.GB) for b in (12, 25, 50, 100)]
+    st, eo = _sweep(lib, pts, graph=g, offs=offs)
+    assert st == T.OK
+    st1, eo1 = _size_query(lib, g, offs, pts[0])
+    assert st1 == T.OK and np.array_equal(eo, eo1)
+    none = T.Table(None, None, None, None, None)
+    st, eo2 = _sweep(lib, pts, tables=[none] * 4, graph=g, offs=offs)
+    assert st == T.OK and np.array_equal(eo2, eo1)
+
+
+def test_sweep_argument_checks(lib):
+    a, b = W.Cluster(2, 2, 10, 1), W.Cluster(2, 2, 20, 3)
+    fake = T.Table(256, 256, 256, 256, 256)
+    assert _sweep(lib, [a, b], n=0)[0] == T.ERR_ARG
+    assert _sweep(lib, [a] * 9)[0] == T.ERR_ARG
+    assert "bandwidth points" in T.last_error()
+    st, eo = _sweep(lib, [a, W.Cluster(4, 1, 10, 1)], tables=[fake, fake], capacity=72)
+    assert st == T.ERR_ARG and "point 1" in T.last_error() and np.all(eo == 0)
+    assert _sweep(lib, [a, W.Cluster(2, 2, 0, 1)])[0] == T.ERR_TOPOLOGY
+    none = T.Table(None, None, None, None, None)
+    st, eo = _sweep(lib, [a, b], tables=[fake, none], capacity=72)
+    assert st == T.ERR_ARG and np.all(eo == 0)
+    st, eo = _sweep(lib, [a, b], tables=[fake, fake], capacity=71)
+    assert st == T.ERR_CAPACITY and np.all(eo == 0)
 
 
 def test_device_errors_are_reported(lib):

@@ -441,3 +441,71 @@ def test_backward_tables_largest_config_one_layer(T):
     w = W.config(5)
     name, cl = w.clusters[0]
     backward_check(T, W.leading_ops(w.graph, 14), cl, f"{w.name}/{name} (one layer)")
+
+
+def sweep_check(T, graph, points, name, oracle=True):
+    """taps_edge_costs_sweep: table k equals taps_edge_costs on points[k] bit
+    for bit and, with `oracle`, the oracle's tables at that point."""
+    import torch
+    offs, strat = T.taps_enumerate_strategies(graph, points[0])
+    eoffs, tabs = T.taps_edge_costs_sweep(graph, points, strat, offs)
+    torch.cuda.synchronize()
+    say(f"[gpu] sweep {name}: {len(points)} points, {int(eoffs[-1])} entries each")
+    ref_strats = [O.enumerate_strategies(op, points[0].devices) for op in graph.ops] if oracle else None
+    for k, cl in enumerate(points):
+        e1, single = T.taps_edge_costs(graph, cl, strat, offs)
+        torch.cuda.synchronize()
+        assert np.array_equal(e1, eoffs)
+        assert _same_tables(single, tabs[k]), f"{name} point {k}"
+        if not oracle:
+            continue
+        got = _host(tabs[k])
+        for x, e in enumerate(graph.edges):
+            a, b = int(eoffs[x]), int(eoffs[x + 1])
+            ref = O.edge_table(graph.ops[e.src], ref_strats[e.src], graph.ops[e.dst], e.slot,
+                               ref_strats[e.dst], cl)
+            assert_records({f: v[a:b] for f, v in got.items()}, ref, f"{name} point {k} edge {x}")
+    return tabs
+
+
+@pytest.mark.gpu
+def test_sweep_tables(T):
+    w = W.config(1)
+    sweep_check(T, w.graph, [W.Cluster(2, 2, 200 * W.GB, 25 * W.GB),
+                             W.Cluster(2, 2, 25 * W.GB, 200 * W.GB),
+                             W.Cluster(2, 2, 100 * W.GB, 100 * W.GB)], w.name)
+    w = W.config(4)   # the wide MLP at its inter-node bandwidth points
+    sweep_check(T, w.graph, [cl for _, cl in w.clusters], w.name)
+    w = W.config(2)
+    sweep_check(T, w.graph, [W.Cluster(2, 8, 400 * W.GB, b * W.GB) for b in (50, 6, 400)], w.name)
+    rng = random.Random(5151)
+    n = 0
+    while n < 10:
+        g = W.random_graph(rng, rng.randint(2, 5), max_axes=5, max_rank=4, len_pow_range=(1, 8))
+        k = rng.randint(0, 7)
+        N = 1 << k
+        L = 1 << rng.randint(0, k)
+        # the last point has reduced bandwidths above 2^32 (the 128-bit order)
+        pts = [W.Cluster(N // L, L, rng.choice([100, 200, 600]) * W.GB,
+                         rng.choice([6, 12, 25, 100]) * W.GB) for _ in range(rng.randint(1, 7))]
+        pts.append(W.Cluster(N // L, L, (1 << 40) + 1, 3))
+        try:
+            sweep_check(T, g, pts, f"random {n}")
+        except T.TapsError:
+            continue
+        n += 1
+
+
+@pytest.mark.gpu
+def test_sweep_tables_largest_config(T):
+    """The 96-layer GPT at four inter-node bandwidths: each table equals the
+    single-point evaluation over all 98,668,128 entries."""
+    import torch
+    w = W.config(5)
+    cl = w.clusters[0][1]
+    pts = [W.Cluster(cl.nodes, cl.devices_per_node, cl.bw_intra, b * W.GB // 2)
+           for b in (25, 50, 100, 200)]
+    tabs = sweep_check(T, w.graph, pts, w.name, oracle=False)
+    assert int(tabs[0]["t"].numel()) == 98668128
+    del tabs
+    torch.cuda.empty_cache()
