@@ -226,6 +226,23 @@ taps_status taps_edge_costs_backward(const taps_graph *graph, const taps_cluster
                                      uint64_t *edge_offsets, taps_table out, uint64_t capacity,
                                      void *stream);
 
+/* Per-device memory of every strategy: the memory cost that the ILP's
+ * device-memory constraint (Eq. 18) sums, which the paper names but never
+ * defines.  Reading used here: a strategy keeps on each device one shard of
+ * each of the operator's weights and one shard of its output (an input is
+ * another operator's output and is counted there); a tensor dimension on op
+ * axis a is cut into 2^log2_deg[a] equal parts when the strategy splits a
+ * (pos[a] >= 0), so a shard holds prod_d (axis_len / 2^log2_deg) elements of
+ * dtype_bytes bytes.  Exact for strategies whose degrees divide their axes
+ * (every strategy taps_enumerate_strategies writes); for others each
+ * dimension's length is divided with the remainder dropped.
+ *   strategies  device, op_offsets[n_ops] entries; op_offsets host.
+ *   memory      device, op_offsets[n_ops] bytes per device, one per strategy.
+ * TAPS_ERR_ARG on NULL arguments (strategies and memory may be NULL when
+ * there are no strategies); TAPS_ERR_DEVICE if the launch fails. */
+taps_status taps_memory_costs(const taps_graph *graph, const taps_strategy *strategies,
+                              const uint64_t *op_offsets, uint64_t *memory, void *stream);
+
 /* The tables of taps_edge_costs at several bandwidth points in one pass:
  * clusters[k] (k < n_points <= TAPS_MAX_SWEEP) must have the same nodes and
  * devices_per_node and may differ in bw_intra and bw_inter.  The candidate

@@ -196,6 +196,22 @@ def node_table(op, strategies: np.ndarray, cluster) -> np.ndarray:
     return out
 
 
+def memory_table(op, strategies: np.ndarray) -> np.ndarray:
+    """Per-device bytes of each strategy (uint64): one shard of every weight
+    and of the output.  Eq. 18 bounds the sum of the selected memory costs by
+    the device memory but the paper does not define the cost itself; this is
+    the reading used here.  A tensor dimension on op axis a is cut into
+    degree[a] equal parts, so a shard has prod_d (len_d // degree_d) elements."""
+    deg = strategies["degree"].astype(np.int64) if len(strategies) else np.ones((0, 8), np.int64)
+    out = np.zeros(len(strategies), dtype=np.uint64)
+    for t in (*op.ws, op.out):
+        elems = np.ones(len(strategies), dtype=np.int64)
+        for a in t:
+            elems = elems * (op.axis_len[a] // deg[:, a])
+        out += (elems * op.dtype_bytes).astype(np.uint64)
+    return out
+
+
 def edge_table(src_op, src_strats: np.ndarray, dst_op, slot: int, dst_strats: np.ndarray,
                cluster) -> np.ndarray:
     """Row-major (len(src_strats), len(dst_strats)) table of one edge."""

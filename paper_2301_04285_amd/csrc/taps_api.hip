@@ -631,6 +631,31 @@ taps_status taps_node_costs(const taps_graph *graph, const taps_cluster *cluster
     return TAPS_OK;
 }
 
+taps_status taps_memory_costs(const taps_graph *graph, const taps_strategy *strategies,
+                              const uint64_t *op_offsets, uint64_t *memory, void *stream_) {
+    g_last_error.clear();
+    taps_status st = check_graph(graph, false);
+    if (st == TAPS_OK) st = check_offsets(graph, op_offsets);
+    if (st != TAPS_OK) return st;
+    const uint32_t n_ops = graph->n_ops;
+    const uint64_t total = op_offsets[n_ops];
+    if (total == 0) return TAPS_OK;
+    if (!strategies) return fail(TAPS_ERR_ARG, "strategies is NULL");
+    if (!memory) return fail(TAPS_ERR_ARG, "memory is NULL");
+    hipStream_t stream = (hipStream_t)stream_;
+    scratch sc(stream);
+    std::vector<chunk> ch{{graph->ops, sizeof(taps_op) * n_ops, 0},
+                          {op_offsets, sizeof(uint64_t) * (n_ops + 1), 0}};
+    void *dev = nullptr;
+    if ((st = upload(ch, &dev, stream)) != TAPS_OK) return st;
+    sc.adopt(dev);
+    const hipError_t err = taps_launch_memory_costs(at<taps_op>(dev, ch[0]), n_ops,
+                                                    at<uint64_t>(dev, ch[1]), strategies, total,
+                                                    memory, stream);
+    if (err != hipSuccess) return hip_fail(err, "memory costs");
+    return TAPS_OK;
+}
+
 taps_status taps_edge_costs(const taps_graph *graph, const taps_cluster *cluster,
                             const taps_strategy *strategies, const uint64_t *op_offsets,
                             uint64_t *edge_offsets, taps_table out, uint64_t capacity,

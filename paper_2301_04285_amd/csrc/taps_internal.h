@@ -83,6 +83,9 @@ hipError_t taps_launch_edge_setup(const taps_op *ops, const taps_edge *edges, ui
 hipError_t taps_launch_edge_costs(const taps_edge_params *params, const taps_row_ref *rows,
                                   uint64_t n_rows, const taps_desc *desc, const taps_launch &lp,
                                   taps_table out, hipStream_t stream);
+hipError_t taps_launch_memory_costs(const taps_op *ops, uint32_t n_ops, const uint64_t *offsets,
+                                   const taps_strategy *s, uint64_t total, uint64_t *memory,
+                                   hipStream_t stream);
 // Bandwidth points of one sweep: the keys and per-unit seconds of each, and
 // the table each writes.
 struct taps_sweep {

@@ -4,6 +4,7 @@
 //                 GenerateStrategySet in canonical order, ballot compaction
 //   k_describe    one thread per strategy: level runs, owners and cuts
 //   k_node_costs  one thread per strategy: the intra-op AllReduces
+//   k_memory_costs one thread per strategy: weight and output shard bytes
 //   k_edge_setup  one thread per edge: per-edge constants
 //   k_row_map     one thread per row segment: its edge, producer strategy
 //                 and first consumer strategy
@@ -230,6 +231,33 @@ __global__ __launch_bounds__(256) void k_node_costs(const taps_op *__restrict__ 
     out.intra[idx] = c.intra;
     out.inter[idx] = c.inter;
     out.meta[idx] = taps_meta(0, c);
+}
+
+// Bytes of one shard of tensor t under strategy s: each dimension's length
+// divided by its split degree, times the element size.
+__device__ inline uint64_t shard_bytes(const taps_op &op, const taps_tensor &t,
+                                       const taps_strategy &s) {
+    uint64_t b = op.dtype_bytes;
+    for (uint32_t d = 0; d < t.rank && d < TAPS_MAX_RANK; ++d) {
+        const uint32_t a = t.axis[d] & 7u;
+        const uint32_t e = s.pos[a] >= 0 ? (s.log2_deg[a] & 15u) : 0u;
+        b *= (uint64_t)op.axis_len[a] >> e;
+    }
+    return b;
+}
+
+__global__ __launch_bounds__(256) void k_memory_costs(const taps_op *__restrict__ ops,
+                                                      uint32_t n_ops,
+                                                      const uint64_t *__restrict__ offsets,
+                                                      const taps_strategy *__restrict__ strategies,
+                                                      uint64_t total, uint64_t *__restrict__ memory) {
+    const uint64_t idx = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= total) return;
+    const taps_op &op = ops[find_owner(offsets, n_ops, idx)];
+    const taps_strategy s = strategies[idx];
+    uint64_t m = shard_bytes(op, op.out, s);
+    for (uint32_t k = 0; k < op.n_w && k < TAPS_MAX_WEIGHTS; ++k) m += shard_bytes(op, op.w[k], s);
+    memory[idx] = m;
 }
 
 __global__ __launch_bounds__(256) void k_edge_setup(const taps_op *__restrict__ ops,
@@ -479,6 +507,15 @@ hipError_t taps_launch_node_costs(const taps_op *ops, uint32_t n_ops, const uint
     if (total == 0) return hipSuccess;
     hipLaunchKernelGGL(k_node_costs, dim3(blocks_for(total, 256)), dim3(256), 0, stream, ops,
                        n_ops, offsets, desc, total, lp, out);
+    return hipGetLastError();
+}
+
+hipError_t taps_launch_memory_costs(const taps_op *ops, uint32_t n_ops, const uint64_t *offsets,
+                                   const taps_strategy *s, uint64_t total, uint64_t *memory,
+                                   hipStream_t stream) {
+    if (total == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_memory_costs, dim3(blocks_for(total, 256)), dim3(256), 0, stream, ops,
+                       n_ops, offsets, s, total, memory);
     return hipGetLastError();
 }
 

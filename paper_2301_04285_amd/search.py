@@ -30,7 +30,7 @@ from __future__ import annotations
 
 import time
 from dataclasses import dataclass
-from typing import Dict, List, Sequence
+from typing import Dict, List, Optional, Sequence
 
 import numpy as np
 
@@ -89,12 +89,16 @@ def add_backward(graph, tables_edge, backward, offsets, field: str):
 
 
 def solve(graph, node: Sequence[np.ndarray], edge: Sequence[np.ndarray],
-          time_limit: float = 600.0, within=None, maximise: bool = False) -> Plan:
+          time_limit: float = 600.0, within=None, maximise: bool = False,
+          memory: Optional[Sequence[np.ndarray]] = None, budget: Optional[float] = None) -> Plan:
     """Cheapest plan: one strategy per operator minimising node plus edge costs.
 
     ``within=(node2, edge2, bound)`` keeps only plans whose cost in a second field is
     at most ``bound`` (a lexicographic second stage); ``maximise`` asks for the
-    dearest such plan instead of the cheapest."""
+    dearest such plan instead of the cheapest.  ``memory`` (per operator, the bytes
+    per device of each strategy, as taps_memory_costs returns them) with ``budget``
+    adds the device-memory constraint (Eq. 18): the chosen strategies' memory sums to
+    at most ``budget`` bytes."""
     from scipy.optimize import LinearConstraint, milp
     from scipy.sparse import coo_matrix
 
@@ -145,6 +149,13 @@ def solve(graph, node: Sequence[np.ndarray], edge: Sequence[np.ndarray],
         s2 = _scale(node2, edge2)
         c2 = _cost_vector(node2, edge2, n_var, xoff, boff, s2)
         constraints.append(LinearConstraint(c2.reshape(1, -1), -np.inf, bound / s2))
+    if memory is not None:
+        if budget is None or budget <= 0:
+            raise ValueError("a memory constraint needs a positive budget")
+        mrow = np.zeros(n_var)
+        for k in range(n_ops):
+            mrow[xoff[k]:xoff[k + 1]] = np.asarray(memory[k], dtype=np.float64) / budget
+        constraints.append(LinearConstraint(mrow.reshape(1, -1), -np.inf, 1.0))
     integrality = np.zeros(n_var)
     integrality[:n_x] = 1
     t0 = time.perf_counter()
@@ -157,6 +168,11 @@ def solve(graph, node: Sequence[np.ndarray], edge: Sequence[np.ndarray],
     return Plan(choice, plan_cost(graph, node, edge, choice), dt, n_x, int(pair_sizes.sum()))
 
 
+def plan_memory(memory: Sequence[np.ndarray], choice: Sequence[int]) -> int:
+    """Bytes per device of the chosen strategies (the left side of Eq. 18)."""
+    return sum(int(memory[k][c]) for k, c in enumerate(choice))
+
+
 def plan_cost(graph, node: Sequence[np.ndarray], edge: Sequence[np.ndarray],
               choice: Sequence[int]) -> float:
     """Node cost of every chosen strategy plus edge cost of every chosen pair."""
@@ -166,7 +182,7 @@ def plan_cost(graph, node: Sequence[np.ndarray], edge: Sequence[np.ndarray],
 
 
 def compare(graph, node_t, edge_t, node_vol, edge_vol, time_limit: float = 600.0,
-            range_time_limit: float = 60.0) -> Dict:
+            range_time_limit: float = 60.0, memory=None, budget=None) -> Dict:
     """TAPS (search on t) against the volume-based search (on vol), plans priced with
     the topology-aware time t.
 
@@ -177,15 +193,17 @@ def compare(graph, node_t, edge_t, node_vol, edge_vol, time_limit: float = 600.0
     volume equals the optimum.  When such a solve finds no plan within
     ``range_time_limit`` seconds, or returns one whose exact volume exceeds the
     optimum (solver tolerance), that end falls back to the plan of the plain volume
-    search and ``range_exact`` says so."""
-    topo = solve(graph, node_t, edge_t, time_limit)
-    vol = solve(graph, node_vol, edge_vol, time_limit)
+    search and ``range_exact`` says so.  ``memory`` and ``budget`` (see solve) bound
+    every search by the device memory."""
+    mem = dict(memory=memory, budget=budget)
+    topo = solve(graph, node_t, edge_t, time_limit, **mem)
+    vol = solve(graph, node_vol, edge_vol, time_limit, **mem)
     vmin = vol.objective
     ends, exact = {}, []
     for key, maximise in (("best", False), ("worst", True)):
         try:
             p = solve(graph, node_t, edge_t, range_time_limit,
-                      within=(node_vol, edge_vol, vmin), maximise=maximise)
+                      within=(node_vol, edge_vol, vmin), maximise=maximise, **mem)
             ok = plan_cost(graph, node_vol, edge_vol, p.choice) <= vmin
         except RuntimeError:
             ok = False
@@ -197,7 +215,12 @@ def compare(graph, node_t, edge_t, node_vol, edge_vol, time_limit: float = 600.0
     t_best = plan_cost(graph, node_t, edge_t, ends["best"].choice)
     t_worst = plan_cost(graph, node_t, edge_t, ends["worst"].choice)
     red = lambda t: 1.0 - t_topo / t if t > 0 else 0.0
+    out = {}
+    if memory is not None:
+        out["memory_bytes"] = [plan_memory(memory, p.choice)
+                               for p in (topo, ends["best"], ends["worst"])]
     return {
+        **out,
         "t_topology_plan_s": t_topo,
         "t_volume_plans_s": [t_best, t_worst],
         "reduction": [red(t_best), red(t_worst)],
@@ -250,6 +273,9 @@ def main() -> int:
                     help="seconds per solve of the volume-optimal range")
     ap.add_argument("--with-backward", action="store_true",
                     help="charge each edge in both directions (forward + backward tables)")
+    ap.add_argument("--memory-budget-gb", type=float, default=0.0,
+                    help="device-memory constraint (Eq. 18) in GB: the chosen strategies' weight "
+                         "and output shards per device (taps_memory_costs) must fit (0 = none)")
     args = ap.parse_args()
 
     import torch
@@ -270,11 +296,18 @@ def main() -> int:
             et = add_backward(g, et, back, tabs.op_offsets, "t")
             ev = add_backward(g, ev, back, tabs.op_offsets, "vol")
             del back
-        r = compare(g, nt, et, nv, ev, args.time_limit, args.range_time_limit)
+        mem = budget = None
+        if args.memory_budget_gb > 0:
+            m = taps.taps_memory_costs(g, tabs.strategies, tabs.op_offsets)
+            flat = m.view(torch.int64).cpu().numpy()
+            mem = [flat[int(tabs.op_offsets[k]):int(tabs.op_offsets[k + 1])] for k in range(len(g.ops))]
+            budget = args.memory_budget_gb * 1e9
+        r = compare(g, nt, et, nv, ev, args.time_limit, args.range_time_limit, mem, budget)
         r.pop("topology_plan")
         r.pop("volume_plans")
         print(json.dumps({"workload": name, "directions": "forward+backward" if
-                          args.with_backward else "forward", **r}), flush=True)
+                          args.with_backward else "forward",
+                          "memory_budget_gb": args.memory_budget_gb or None, **r}), flush=True)
     return 0
 
 

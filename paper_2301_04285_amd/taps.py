@@ -94,6 +94,9 @@ def load():
         L.taps_edge_costs_sweep.argtypes = [P(GraphS), P(Cluster), C.c_uint32, C.c_void_p,
                                             P(C.c_uint64), P(C.c_uint64), P(Table), C.c_uint64,
                                             C.c_void_p]
+        L.taps_memory_costs.restype = C.c_int
+        L.taps_memory_costs.argtypes = [P(GraphS), C.c_void_p, P(C.c_uint64), C.c_void_p,
+                                        C.c_void_p]
         L.taps_set_edge_kernel_events.restype = C.c_int
         L.taps_set_edge_kernel_events.argtypes = [C.c_void_p, C.c_void_p]
         L.taps_status_str.restype = C.c_char_p
@@ -283,6 +286,23 @@ def taps_edge_costs(graph, cluster, strategies, op_offsets, out=None, stream=Non
     _check(st, name)
     total = int(eoffs[-1])
     return eoffs, {k: v[:total] for k, v in out.items()}
+
+
+def taps_memory_costs(graph, strategies, op_offsets, out=None, stream=None):
+    """Per-device bytes of every strategy (device uint64 tensor, one per strategy)."""
+    import torch
+    g = _graph(graph)
+    offs = np.ascontiguousarray(op_offsets, dtype=np.uint64)
+    total = int(offs[-1])
+    if out is None:
+        out = torch.empty(max(total, 1), dtype=torch.uint64, device=strategies.device)
+    if int(out.numel()) < total:
+        raise ValueError(f"memory output holds {out.numel()} entries, {total} needed")
+    st = load().taps_memory_costs(C.byref(g.struct),
+                                  C.c_void_p(strategies.data_ptr()) if strategies is not None else None,
+                                  _u64_array(offs), C.c_void_p(out.data_ptr()), _stream(stream))
+    _check(st, "taps_memory_costs")
+    return out[:total]
 
 
 def taps_edge_costs_sweep(graph, clusters, strategies, op_offsets, out=None, stream=None,

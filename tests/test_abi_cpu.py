@@ -20,7 +20,8 @@ def test_exports_every_declared_symbol(lib):
     declared = T.declared_symbols()
     assert declared == sorted(["taps_enumerate_strategies", "taps_node_costs", "taps_edge_costs",
                                "taps_edge_costs_shared", "taps_edge_costs_backward",
-                               "taps_edge_costs_sweep", "taps_set_edge_kernel_events", "taps_status_str",
+                               "taps_edge_costs_sweep", "taps_memory_costs",
+                               "taps_set_edge_kernel_events", "taps_status_str",
                                "taps_last_error"])
     out = subprocess.run(["nm", "-D", "--defined-only", T.LIB_PATH], capture_output=True,
                          text=True, check=True).stdout
@@ -220,6 +221,24 @@ def test_sweep_argument_checks(lib):
     assert st == T.ERR_ARG and np.all(eo == 0)
     st, eo = _sweep(lib, [a, b], tables=[fake, fake], capacity=71)
     assert st == T.ERR_CAPACITY and np.all(eo == 0)
+
+
+def test_memory_costs_argument_checks(lib):
+    g = T.pack_graph(W.mlp2())
+    offs = np.array([0, 9, 13, 22], np.uint64)
+    assert lib.taps_memory_costs(C.byref(g.struct), C.c_void_p(256), T._u64_array(offs), None,
+                                 None) == T.ERR_ARG
+    assert "memory" in T.last_error()
+    assert lib.taps_memory_costs(C.byref(g.struct), None, T._u64_array(offs), C.c_void_p(256),
+                                 None) == T.ERR_ARG
+    assert lib.taps_memory_costs(C.byref(g.struct), C.c_void_p(256),
+                                 T._u64_array(np.array([0, 9, 9, 18], np.uint64)),
+                                 C.c_void_p(256), None) == T.ERR_ARG
+    assert lib.taps_memory_costs(None, C.c_void_p(256), T._u64_array(offs), C.c_void_p(256),
+                                 None) == T.ERR_ARG
+    empty = T.pack_graph(W.Graph())   # no strategies: nothing to do, NULL buffers allowed
+    assert lib.taps_memory_costs(C.byref(empty.struct), None, T._u64_array(np.zeros(1, np.uint64)),
+                                 None, None) == T.OK
 
 
 def test_device_errors_are_reported(lib):

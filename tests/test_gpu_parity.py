@@ -509,3 +509,29 @@ def test_sweep_tables_largest_config(T):
     assert int(tabs[0]["t"].numel()) == 98668128
     del tabs
     torch.cuda.empty_cache()
+
+
+@pytest.mark.gpu
+def test_memory_costs(T):
+    """taps_memory_costs against the oracle, every strategy of every operator."""
+    import torch
+    cases = [(W.config(c).graph, W.config(c).clusters[0][1]) for c in (1, 2, 3, 4, 5)]
+    rng = random.Random(6161)
+    while len(cases) < 13:
+        g = W.random_graph(rng, rng.randint(1, 6), max_axes=6, max_rank=4, len_pow_range=(1, 9))
+        k = rng.randint(0, 8)
+        cl = W.Cluster(1 << rng.randint(0, k), 1, 10, 1)
+        cl = W.Cluster(cl.nodes, (1 << k) // cl.nodes, 10, 1)
+        try:
+            T.taps_enumerate_strategies(g, cl, size_only=True)
+        except T.TapsError:
+            continue
+        cases.append((g, cl))
+    for g, cl in cases:
+        offs, strat = T.taps_enumerate_strategies(g, cl)
+        mem = _np(T.taps_memory_costs(g, strat, offs))
+        torch.cuda.synchronize()
+        for k, op in enumerate(g.ops):
+            ref = O.memory_table(op, O.enumerate_strategies(op, cl.devices))
+            a, b = int(offs[k]), int(offs[k + 1])
+            assert np.array_equal(mem[a:b], ref), (k, op.name)

@@ -163,3 +163,48 @@ def test_backward_tables_add_pairwise(oracle_lib):
                 b = oracle_lib.edge_cost_reverse(g.ops[e.src], strats[e.src][i], g.ops[e.dst],
                                                  e.slot, strats[e.dst][j], cl)[0]
                 assert abs(both[x][i, j] - (c + b)) <= 1e-15 * max(1.0, c + b)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_memory_constraint_matches_exhaustive_search(oracle_lib, seed):
+    """With the device-memory constraint (Eq. 18) the ILP finds the cheapest plan among
+    those whose strategies' memory fits the budget (exhaustive check), for budgets
+    between the smallest and the largest plan memory."""
+    from oracle import oracle as O
+    rng = random.Random(3000 + seed)
+    cl = W.Cluster(2, 4, 200 * W.GB, 25 * W.GB)
+    while True:   # a graph whose plans differ in memory (with no weights, often they do not)
+        g = W.random_graph(rng, 4, max_axes=3, max_rank=3, len_pow_range=(3, 7))
+        node, edge = _fields(oracle_lib, g, cl)["t"]
+        mem = [O.memory_table(op, O.enumerate_strategies(op, cl.devices)).astype(np.int64)
+               for op in g.ops]
+        plans = list(itertools.product(*[range(len(v)) for v in node]))
+        pm = np.array([S.plan_memory(mem, p) for p in plans])
+        levels = np.unique(pm)
+        if len(levels) >= 3 and len(plans) <= 200_000:
+            break
+    pc = np.array([S.plan_cost(g, node, edge, p) for p in plans])
+    for q in (0.05, 0.3, 0.6):
+        k = int(q * (len(levels) - 1))
+        budget = (levels[k] + levels[k + 1]) / 2   # between two plan memories: no tie at the bound
+        best = pc[pm <= budget].min()
+        plan = S.solve(g, node, edge, memory=mem, budget=budget)
+        assert S.plan_memory(mem, plan.choice) <= budget
+        assert _close(plan.objective, best)
+    with pytest.raises(RuntimeError):
+        S.solve(g, node, edge, memory=mem, budget=levels[0] / 2)
+
+
+def test_compare_under_a_memory_budget(oracle_lib):
+    """Both searches respect the budget; the reported plan memories fit it."""
+    from oracle import oracle as O
+    w = W.config(1)
+    cl = w.clusters[0][1]
+    tabs = _fields(oracle_lib, w.graph, cl)
+    mem = [O.memory_table(op, O.enumerate_strategies(op, cl.devices)).astype(np.int64)
+           for op in w.graph.ops]
+    free = S.compare(w.graph, *tabs["t"], *tabs["vol"], memory=mem, budget=1e18)
+    tight = min(free["memory_bytes"]) - 1
+    r = S.compare(w.graph, *tabs["t"], *tabs["vol"], memory=mem, budget=tight)
+    assert all(m <= tight for m in r["memory_bytes"])
+    assert r["t_topology_plan_s"] >= free["t_topology_plan_s"] - 1e-15
