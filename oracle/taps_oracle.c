@@ -214,7 +214,7 @@ int64_t or_enumerate(const or_op *op, int64_t N, int filter, or_strategy *out, i
         return -1;
     }
     g_sort_axes = op->n_axes;
-    qsort(v.buf, (size_t)v.len, sizeof(or_strategy), strategy_order);
+    if (v.len > 1) qsort(v.buf, (size_t)v.len, sizeof(or_strategy), strategy_order);
     for (int64_t k = 0; k < v.len && k < cap; ++k) out[k] = v.buf[k];
     int64_t n = v.len;
     free(v.buf);
