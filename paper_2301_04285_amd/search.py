@@ -273,6 +273,10 @@ def main() -> int:
                     help="seconds per solve of the volume-optimal range")
     ap.add_argument("--with-backward", action="store_true",
                     help="charge each edge in both directions (forward + backward tables)")
+    ap.add_argument("--workload-json", default="",
+                    help="search this workload (JSON written by workloads.workload_to_json, "
+                         "e.g. `python -m paper_2301_04285_amd.workloads 2 w.json`) instead of "
+                         "the built-in ones")
     ap.add_argument("--memory-budget-gb", type=float, default=0.0,
                     help="device-memory constraint (Eq. 18) in GB: the chosen strategies' weight "
                          "and output shards per device (taps_memory_costs) must fit (0 = none)")
@@ -284,7 +288,14 @@ def main() -> int:
     if not torch.cuda.is_available():
         print("the tables are built on a GPU", file=sys.stderr)
         return 1
-    for name, g, cl in experiment_workloads():
+    if args.workload_json:
+        from . import workloads as W
+        with open(args.workload_json) as f:
+            w = W.workload_from_json(f.read())
+        runs = [(f"{w.name} / {n}", w.graph, cl) for n, cl in w.clusters]
+    else:
+        runs = experiment_workloads()
+    for name, g, cl in runs:
         if args.only not in name:
             continue
         tabs = taps.build_tables(g, cl)

@@ -357,6 +357,44 @@ class Tables:
     edge: Dict[str, "torch.Tensor"]
 
 
+TABLE_FIELDS = ("t", "vol", "intra", "inter", "meta")
+
+
+def save_tables(path: str, tabs: Tables) -> None:
+    """Write a table set to one .npz file (plain arrays, no pickled objects)."""
+    arrays = {"op_offsets": np.asarray(tabs.op_offsets, dtype=np.uint64),
+              "edge_offsets": np.asarray(tabs.edge_offsets, dtype=np.uint64),
+              "strategies": tabs.strategies.cpu().numpy()}
+    n_str, n_edge = int(tabs.op_offsets[-1]), int(tabs.edge_offsets[-1])
+    for prefix, tab, n in (("node_", tabs.node, n_str), ("edge_", tabs.edge, n_edge)):
+        for f in TABLE_FIELDS:
+            v = tab[f][:n]
+            arrays[prefix + f] = {8: lambda: v.view(_torch().int64).cpu().numpy().view(np.uint64),
+                                  4: lambda: v.view(_torch().int32).cpu().numpy().view(np.uint32)}[
+                v.element_size()]() if f != "t" else v.cpu().numpy()
+    np.savez(path, **arrays)
+
+
+def load_tables(path: str, device="cuda") -> Tables:
+    """A table set written by save_tables, on `device`."""
+    torch = _torch()
+    with np.load(path, allow_pickle=False) as z:
+        def dev(a):
+            if a.dtype == np.uint64:
+                return torch.from_numpy(a.view(np.int64).copy()).to(device).view(torch.uint64)
+            if a.dtype == np.uint32:
+                return torch.from_numpy(a.view(np.int32).copy()).to(device).view(torch.uint32)
+            return torch.from_numpy(a.copy()).to(device)
+        return Tables(z["op_offsets"].copy(), dev(z["strategies"]),
+                      {f: dev(z["node_" + f]) for f in TABLE_FIELDS}, z["edge_offsets"].copy(),
+                      {f: dev(z["edge_" + f]) for f in TABLE_FIELDS})
+
+
+def _torch():
+    import torch
+    return torch
+
+
 def build_tables(graph, cluster, device="cuda", stream=None, out: Optional[Tables] = None,
                  shared: bool = False) -> Tables:
     """Enumeration, node table and edge table of one graph on one cluster.

@@ -20,6 +20,7 @@ tensor, ``ins`` are activations (edge consumers attach to them by slot) and
 """
 from __future__ import annotations
 
+import json
 import random
 from dataclasses import dataclass, field
 from typing import List, Sequence, Tuple
@@ -336,3 +337,68 @@ def random_graph(rng: random.Random, n_ops: int, max_axes: int = 5, max_rank: in
                        tuple(part), so.dtype_bytes, ins=(tensor_axes,), ws=ws, out=out))
         g.connect(src, dst, 0)
     return g
+
+
+# --------------------------------------------------------------------------
+# JSON descriptions (graphs and clusters as plain data, integer bytes/s)
+# --------------------------------------------------------------------------
+
+def graph_to_dict(graph: Graph) -> dict:
+    return {"ops": [{"name": op.name, "kind": op.kind, "axes": list(op.axis_names),
+                     "lengths": list(op.axis_len), "partitionable": list(op.partitionable),
+                     "dtype_bytes": op.dtype_bytes, "inputs": [list(t) for t in op.ins],
+                     "weights": [list(t) for t in op.ws], "output": list(op.out)}
+                    for op in graph.ops],
+            "edges": [{"src": e.src, "dst": e.dst, "slot": e.slot} for e in graph.edges]}
+
+
+def graph_from_dict(d: dict) -> Graph:
+    g = Graph()
+    for o in d["ops"]:
+        g.add(Op(str(o["name"]), str(o["kind"]), tuple(o["axes"]),
+                 tuple(int(x) for x in o["lengths"]), tuple(bool(x) for x in o["partitionable"]),
+                 int(o["dtype_bytes"]), ins=tuple(tuple(int(a) for a in t) for t in o["inputs"]),
+                 ws=tuple(tuple(int(a) for a in t) for t in o["weights"]),
+                 out=tuple(int(a) for a in o["output"])))
+    for e in d["edges"]:
+        src, dst, slot = int(e["src"]), int(e["dst"]), int(e["slot"])
+        if not (0 <= src < len(g.ops) and 0 <= dst < len(g.ops)):
+            raise ValueError(f"edge {e} names an operator that does not exist")
+        g.connect(src, dst, slot)
+    return g
+
+
+def cluster_to_dict(cluster: Cluster) -> dict:
+    return {"nodes": cluster.nodes, "devices_per_node": cluster.devices_per_node,
+            "bw_intra": cluster.bw_intra, "bw_inter": cluster.bw_inter}
+
+
+def cluster_from_dict(d: dict) -> Cluster:
+    return Cluster(int(d["nodes"]), int(d["devices_per_node"]), int(d["bw_intra"]),
+                   int(d["bw_inter"]))
+
+
+def workload_to_json(w: Workload) -> str:
+    return json.dumps({"name": w.name, "graph": graph_to_dict(w.graph),
+                       "clusters": [{"name": n, **cluster_to_dict(c)} for n, c in w.clusters]})
+
+
+def workload_from_json(text: str) -> Workload:
+    d = json.loads(text)
+    return Workload(str(d["name"]), graph_from_dict(d["graph"]),
+                    [(str(c["name"]), cluster_from_dict(c)) for c in d["clusters"]])
+
+
+def main() -> int:
+    import argparse
+    ap = argparse.ArgumentParser(description="write a measured configuration as JSON")
+    ap.add_argument("config", type=int, help="1..5")
+    ap.add_argument("out", help="output file")
+    args = ap.parse_args()
+    with open(args.out, "w") as f:
+        f.write(workload_to_json(config(args.config)))
+    return 0
+
+
+if __name__ == "__main__":
+    raise SystemExit(main())
