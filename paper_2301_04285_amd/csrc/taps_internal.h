@@ -40,7 +40,7 @@ struct taps_copy_task {
     uint32_t count, dst_begin, n_dst, pad;
 };
 #define TAPS_COPY_CHUNK 2048    // entries per copy task (8 per thread of 256)
-#define TAPS_COPY_DSTS 16       // tables one copy task writes
+#define TAPS_COPY_DSTS 6        // tables one copy task writes (4-6 measured best, 16 is 20 % slower)
 
 // One wavefront per row segment: producer strategy i of one edge and up to
 // TAPS_SEG_TILES tiles of 64 consecutive consumer strategies, walked 64 at a

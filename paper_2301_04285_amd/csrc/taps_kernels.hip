@@ -418,40 +418,51 @@ __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_co
 }
 
 // Shared tables: each task holds `count` (<= TAPS_COPY_CHUNK) consecutive
-// entries of a computed table, loaded once (8 per thread, consecutive
-// threads on consecutive entries) and stored into every table that shares it,
-// at the same offset; blockIdx.y picks the array.
+// entries of a computed table, staged once in LDS and stored into every table
+// that shares it, at the same offset; blockIdx.y picks the array.  The tables
+// start at arbitrary entries, so each destination is written with 16-byte
+// stores aligned to its own 16-byte boundaries (LDS absorbs the difference in
+// alignment between source and destination), plus single-entry stores for the
+// head and tail.
+struct alignas(16) vec16 {
+    uint32_t w[4];
+};
+
 template <typename T>
 __device__ inline void copy_range(T *base, const taps_copy_task &c,
-                                  const uint64_t *__restrict__ dst_list) {
-    constexpr uint32_t kPer = TAPS_COPY_CHUNK / 256;
+                                  const uint64_t *__restrict__ dst_list, T *stage) {
+    constexpr uint32_t kV = 16 / sizeof(T);   // entries per 16-byte store
     const T *s = base + c.src;
-    T v[kPer];
-#pragma unroll
-    for (uint32_t u = 0; u < kPer; ++u) {
-        const uint32_t x = threadIdx.x + u * 256u;
-        if (x < c.count) v[u] = s[x];
-    }
+    for (uint32_t x = threadIdx.x; x < c.count; x += blockDim.x) stage[x] = s[x];
+    __syncthreads();
     for (uint32_t k = 0; k < c.n_dst; ++k) {
         T *d = base + dst_list[c.dst_begin + k] + c.offset;
-#pragma unroll
-        for (uint32_t u = 0; u < kPer; ++u) {
-            const uint32_t x = threadIdx.x + u * 256u;
-            if (x < c.count) d[x] = v[u];   // cached: L2 merges the partial lines at the ends
+        const uint32_t mis = (uint32_t)(((uintptr_t)d & 15u) / sizeof(T));
+        const uint32_t head = mis ? (kV - mis < c.count ? kV - mis : c.count) : 0u;
+        const uint32_t n_vec = (c.count - head) / kV;
+        const uint32_t tail = head + n_vec * kV;
+        if (threadIdx.x < head) d[threadIdx.x] = stage[threadIdx.x];
+        vec16 *dv = (vec16 *)(d + head);
+        for (uint32_t v = threadIdx.x; v < n_vec; v += blockDim.x) {
+            vec16 val;
+            __builtin_memcpy(&val, stage + head + v * kV, 16);
+            dv[v] = val;
         }
+        if (tail + threadIdx.x < c.count) d[tail + threadIdx.x] = stage[tail + threadIdx.x];
     }
 }
 
 __global__ __launch_bounds__(256) void k_copy_tables(const taps_copy_task *__restrict__ tasks,
                                                      const uint64_t *__restrict__ dst_list,
                                                      taps_table out) {
+    __shared__ uint64_t stage[TAPS_COPY_CHUNK];
     const taps_copy_task c = tasks[blockIdx.x];
     switch (blockIdx.y) {
-    case 0: copy_range(out.t, c, dst_list); break;
-    case 1: copy_range(out.vol, c, dst_list); break;
-    case 2: copy_range(out.intra, c, dst_list); break;
-    case 3: copy_range(out.inter, c, dst_list); break;
-    default: copy_range(out.meta, c, dst_list); break;
+    case 0: copy_range(out.t, c, dst_list, (double *)stage); break;
+    case 1: copy_range(out.vol, c, dst_list, stage); break;
+    case 2: copy_range(out.intra, c, dst_list, stage); break;
+    case 3: copy_range(out.inter, c, dst_list, stage); break;
+    default: copy_range(out.meta, c, dst_list, (uint32_t *)stage); break;
     }
 }
 
