@@ -94,6 +94,8 @@ def lib():
         P = C.POINTER
         L.or_enumerate.restype = i64
         L.or_enumerate.argtypes = [P(OrOp), i64, C.c_int, P(OrStrategy), i64]
+        L.or_enumerate_mesh.restype = i64
+        L.or_enumerate_mesh.argtypes = [P(OrOp), P(i64), C.c_int, C.c_int, P(OrStrategy), i64]
         L.or_node_cost.restype = None
         L.or_node_cost.argtypes = [P(OrOp), P(OrStrategy), i64, i64, u64, u64, P(OrRecord)]
         L.or_node_table.restype = i64
@@ -175,6 +177,24 @@ def enumerate_strategies(op, n_devices: int, filter_divisible: bool = True) -> n
     if n:
         got = L.or_enumerate(C.byref(o), n_devices, int(filter_divisible),
                              arr.ctypes.data_as(C.POINTER(OrStrategy)), n)
+        assert got == n
+    return arr
+
+
+def enumerate_strategies_mesh(op, mesh: Sequence[int], filter_divisible: bool = True) -> np.ndarray:
+    """The strategies of `enumerate_strategies` on prod(mesh) devices whose device
+    matrix groups whole, consecutive dimensions of the fixed mesh `mesh`
+    (innermost first), in the same order.  A fixed-mesh strategy space is an
+    extension: the paper's device matrices are free."""
+    o = make_op(op)
+    L = lib()
+    m = (C.c_int64 * max(1, len(mesh)))(*mesh)
+    n = L.or_enumerate_mesh(C.byref(o), m, len(mesh), int(filter_divisible), None, 0)
+    assert n >= 0
+    arr = np.zeros(n, dtype=STRATEGY_DTYPE)
+    if n:
+        got = L.or_enumerate_mesh(C.byref(o), m, len(mesh), int(filter_divisible),
+                                  arr.ctypes.data_as(C.POINTER(OrStrategy)), n)
         assert got == n
     return arr
 

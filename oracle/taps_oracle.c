@@ -234,6 +234,54 @@ static int device_matrix(const or_op *op, const or_strategy *s, int64_t *D) {
     return h;
 }
 
+/* ---------------------------------------------------------------------------
+ * Fixed-mesh strategy spaces (an extension; the paper's device matrix is
+ * free).
+ *
+ * A search over a fixed physical mesh [m_0, m_1, ..., m_{k-1}] (m_0 innermost,
+ * the product is N) shards an operator axis over whole mesh dimensions only:
+ * the strategy's device matrix D = [d_{h-1}, ..., d_0] must group consecutive
+ * mesh dimensions, i.e. every prefix product d_0 ... d_j is a prefix product
+ * m_0 ... m_i of the mesh.  The candidates before the divisibility filter are
+ * then counted by the paper's formula with n replaced by k: a strategy picks i
+ * axes, an ordering, and a composition of the k mesh dimensions into i runs.
+ * ------------------------------------------------------------------------- */
+
+static int on_mesh(const or_op *op, const or_strategy *s, const int64_t *mesh, int k) {
+    int64_t D[OR_MAX_DEV];
+    const int h = device_matrix(op, s, D);
+    int i = 0;
+    int64_t mp = 1, dp = 1;
+    for (int j = 0; j < h; ++j) {
+        dp *= D[j];
+        while (i < k && mp < dp) mp *= mesh[i++];
+        if (mp != dp) return 0;
+    }
+    return 1;
+}
+
+/* The strategies of or_enumerate on N = prod(mesh) devices that lie on the
+ * mesh, in the same (canonical) order; returns how many (-1 on allocation
+ * failure). */
+int64_t or_enumerate_mesh(const or_op *op, const int64_t *mesh, int k, int filter,
+                          or_strategy *out, int64_t cap) {
+    int64_t N = 1;
+    for (int i = 0; i < k; ++i) N *= mesh[i];
+    const int64_t all = or_enumerate(op, N, filter, NULL, 0);
+    if (all < 0) return -1;
+    or_strategy *buf = (or_strategy *)malloc((size_t)(all ? all : 1) * sizeof(or_strategy));
+    if (!buf) return -1;
+    or_enumerate(op, N, filter, buf, all);
+    int64_t n = 0;
+    for (int64_t x = 0; x < all; ++x) {
+        if (!on_mesh(op, &buf[x], mesh, k)) continue;
+        if (n < cap) out[n] = buf[x];
+        ++n;
+    }
+    free(buf);
+    return n;
+}
+
 static void tensor_map(const or_tensor *t, const or_strategy *s, int32_t *M) {
     for (int d = 0; d < t->rank; ++d) {
         int a = t->axis[d];
