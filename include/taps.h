@@ -10,7 +10,8 @@
  * tables that program consumes:
  *
  *   1. taps_enumerate_strategies -- every strategy of every operator
- *      (GenerateStrategySet, Auxiliary Graph section, Table 3);
+ *      (GenerateStrategySet, Auxiliary Graph section, Table 3), or with
+ *      taps_enumerate_strategies_mesh those a fixed device mesh expresses;
  *   2. taps_node_costs -- the intra-operator communication cost of every
  *      strategy (Communication Cost Model section: Eq. 5-8, Algorithm 2,
  *      Eq. 11-12);
@@ -136,6 +137,14 @@ typedef struct {
     int8_t pos[TAPS_MAX_AXES];
 } taps_strategy;
 
+/* A fixed device mesh: dims[0] (innermost) x dims[1] x ... x dims[n_dims - 1]
+ * devices, each size a power of two >= 2, the product N = nodes * L.  N = 1
+ * takes n_dims = 0. */
+typedef struct {
+    uint32_t n_dims;
+    uint32_t dims[TAPS_MAX_LEVELS];
+} taps_mesh;
+
 /* Device arrays of one table, one element per record. */
 typedef struct {
     double *t;
@@ -160,6 +169,23 @@ typedef struct {
 taps_status taps_enumerate_strategies(const taps_graph *graph, const taps_cluster *cluster,
                                       uint64_t *op_offsets, taps_strategy *strategies,
                                       uint64_t capacity, void *stream);
+
+/* The strategies of taps_enumerate_strategies that a search over a fixed
+ * device mesh can express (an extension: the paper's device matrices are
+ * free, Auxiliary Graph section): every split axis is sharded over whole,
+ * consecutive mesh dimensions, i.e. each prefix product of the strategy's
+ * device matrix (innermost first) is a prefix product of the mesh.  Same
+ * canonical order, a subsequence of the unrestricted set; before the
+ * divisibility filter the count is the paper's formula with n replaced by
+ * mesh->n_dims.  The tables of taps_node_costs, taps_edge_costs and the
+ * other calls take these strategies as they take any others.
+ *   mesh  host; TAPS_ERR_TOPOLOGY if a size is not a power of two >= 2, the
+ *         product differs from N, or n_dims > TAPS_MAX_LEVELS.
+ * Other arguments, outputs and errors as taps_enumerate_strategies. */
+taps_status taps_enumerate_strategies_mesh(const taps_graph *graph, const taps_cluster *cluster,
+                                           const taps_mesh *mesh, uint64_t *op_offsets,
+                                           taps_strategy *strategies, uint64_t capacity,
+                                           void *stream);
 
 /* Intra-operator cost of every strategy (Eq. 5-8 generalised to any
  * operator: one ring AllReduce per tensor that lacks some split axis -- the

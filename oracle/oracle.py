@@ -414,9 +414,12 @@ class Tables:
     edge: List[Optional[np.ndarray]]  # per edge, (S_src, S_dst) RECORD_DTYPE, or None if skipped
 
 
-def build_tables(graph, cluster, edges: Optional[Sequence[int]] = None) -> Tables:
-    """Every table of ``graph`` on ``cluster`` (only the listed edges if given)."""
-    strats = [enumerate_strategies(op, cluster.devices) for op in graph.ops]
+def build_tables(graph, cluster, edges: Optional[Sequence[int]] = None,
+                 mesh: Optional[Sequence[int]] = None) -> Tables:
+    """Every table of ``graph`` on ``cluster`` (only the listed edges if given;
+    over the strategies of the fixed mesh ``mesh`` if given)."""
+    strats = [enumerate_strategies(op, cluster.devices) if mesh is None
+              else enumerate_strategies_mesh(op, mesh) for op in graph.ops]
     node = [node_table(op, s, cluster) for op, s in zip(graph.ops, strats)]
     want = set(range(len(graph.edges))) if edges is None else set(edges)
     edge = []

@@ -499,43 +499,12 @@ taps_status edge_costs(const taps_graph *graph, const taps_cluster *clusters, ui
     return TAPS_OK;
 }
 
-}  // namespace
-
-extern "C" {
-
-const char *taps_status_str(taps_status s) {
-    switch (s) {
-    case TAPS_OK: return "TAPS_OK";
-    case TAPS_ERR_ARG: return "TAPS_ERR_ARG";
-    case TAPS_ERR_TOPOLOGY: return "TAPS_ERR_TOPOLOGY";
-    case TAPS_ERR_SHAPE: return "TAPS_ERR_SHAPE";
-    case TAPS_ERR_NO_STRATEGY: return "TAPS_ERR_NO_STRATEGY";
-    case TAPS_ERR_CAPACITY: return "TAPS_ERR_CAPACITY";
-    case TAPS_ERR_DEVICE: return "TAPS_ERR_DEVICE";
-    }
-    return "TAPS_ERR_UNKNOWN";
-}
-
-const char *taps_last_error(void) { return g_last_error.c_str(); }
-
-taps_status taps_set_edge_kernel_events(void *before, void *after) {
-    g_last_error.clear();
-    if ((before == nullptr) != (after == nullptr))
-        return fail(TAPS_ERR_ARG, "both kernel events or neither");
-    g_kernel_before = (hipEvent_t)before;
-    g_kernel_after = (hipEvent_t)after;
-    return TAPS_OK;
-}
-
-taps_status taps_enumerate_strategies(const taps_graph *graph, const taps_cluster *cluster,
-                                      uint64_t *op_offsets, taps_strategy *strategies,
-                                      uint64_t capacity, void *stream_) {
-    g_last_error.clear();
-    taps_launch lp;
-    taps_status st = check_cluster(cluster, &lp);
-    if (st == TAPS_OK) st = check_graph(graph, false);
-    if (st != TAPS_OK) return st;
-    if (!op_offsets) return fail(TAPS_ERR_ARG, "op_offsets is NULL");
+// GenerateStrategySet on the device; allowed_cuts: the level boundaries a
+// strategy's axis runs may meet (all of them unless a fixed mesh is given).
+taps_status enumerate(const taps_graph *graph, const taps_launch &lp, uint32_t allowed_cuts,
+                      uint64_t *op_offsets, taps_strategy *strategies, uint64_t capacity,
+                      void *stream_) {
+    taps_status st = TAPS_OK;
     hipStream_t stream = (hipStream_t)stream_;
     const uint32_t n_ops = graph->n_ops;
     if (n_ops == 0) {
@@ -573,13 +542,13 @@ taps_status taps_enumerate_strategies(const taps_graph *graph, const taps_cluste
     // they fit the capacity.  One read-back returns the offsets.
     const uint32_t *d_first = at<uint32_t>(dev, ch[1]);
     hipError_t err = taps_launch_enumerate(d_ops, lp.n, n_ops, n_chunks, d_first, d_base,
-                                           d_scan + n_ops + 1, d_counts, nullptr, stream);
+                                           d_scan + n_ops + 1, allowed_cuts, d_counts, nullptr, stream);
     if (err == hipSuccess)
         err = taps_launch_chunk_scan(d_counts, n_chunks, d_first, n_ops,
                                      strategies ? capacity : UINT64_MAX, d_base, d_scan, stream);
     if (err == hipSuccess && strategies)
         err = taps_launch_enumerate(d_ops, lp.n, n_ops, n_chunks, d_first, d_base,
-                                    d_scan + n_ops + 1, nullptr, strategies, stream);
+                                    d_scan + n_ops + 1, allowed_cuts, nullptr, strategies, stream);
     std::vector<uint64_t> offs(n_ops + 2, 0);
     if (err == hipSuccess)
         err = hipMemcpyAsync(offs.data(), d_scan, sizeof(uint64_t) * (n_ops + 2),
@@ -597,6 +566,84 @@ taps_status taps_enumerate_strategies(const taps_graph *graph, const taps_cluste
         return fail(TAPS_ERR_CAPACITY, "%llu strategies, capacity %llu",
                     (unsigned long long)offs[n_ops], (unsigned long long)capacity);
     return TAPS_OK;
+}
+
+// The level boundaries of a fixed mesh (bit c: between levels c-1 and c), or
+// TAPS_ERR_TOPOLOGY unless its sizes are powers of two >= 2 multiplying to 2^n.
+taps_status mesh_cuts(const taps_mesh *mesh, uint32_t n, uint32_t *allowed) {
+    if (!mesh) return fail(TAPS_ERR_ARG, "mesh is NULL");
+    if (mesh->n_dims > TAPS_MAX_LEVELS)
+        return fail(TAPS_ERR_TOPOLOGY, "a mesh has at most %u dimensions (got %u)",
+                    TAPS_MAX_LEVELS, mesh->n_dims);
+    uint32_t level = 0, cuts = 0;
+    for (uint32_t k = 0; k < mesh->n_dims; ++k) {
+        const uint32_t m = mesh->dims[k];
+        if (m < 2 || !pow2(m))
+            return fail(TAPS_ERR_TOPOLOGY, "mesh dimension %u has size %u (not a power of two >= 2)",
+                        k, m);
+        if (level) cuts |= 1u << level;
+        level += log2u(m);
+        if (level > n) break;
+    }
+    if (level != n)
+        return fail(TAPS_ERR_TOPOLOGY, "the mesh does not have 2^%u devices", n);
+    *allowed = cuts;
+    return TAPS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *taps_status_str(taps_status s) {
+    switch (s) {
+    case TAPS_OK: return "TAPS_OK";
+    case TAPS_ERR_ARG: return "TAPS_ERR_ARG";
+    case TAPS_ERR_TOPOLOGY: return "TAPS_ERR_TOPOLOGY";
+    case TAPS_ERR_SHAPE: return "TAPS_ERR_SHAPE";
+    case TAPS_ERR_NO_STRATEGY: return "TAPS_ERR_NO_STRATEGY";
+    case TAPS_ERR_CAPACITY: return "TAPS_ERR_CAPACITY";
+    case TAPS_ERR_DEVICE: return "TAPS_ERR_DEVICE";
+    }
+    return "TAPS_ERR_UNKNOWN";
+}
+
+const char *taps_last_error(void) { return g_last_error.c_str(); }
+
+taps_status taps_set_edge_kernel_events(void *before, void *after) {
+    g_last_error.clear();
+    if ((before == nullptr) != (after == nullptr))
+        return fail(TAPS_ERR_ARG, "both kernel events or neither");
+    g_kernel_before = (hipEvent_t)before;
+    g_kernel_after = (hipEvent_t)after;
+    return TAPS_OK;
+}
+
+taps_status taps_enumerate_strategies(const taps_graph *graph, const taps_cluster *cluster,
+                                      uint64_t *op_offsets, taps_strategy *strategies,
+                                      uint64_t capacity, void *stream) {
+    g_last_error.clear();
+    taps_launch lp;
+    taps_status st = check_cluster(cluster, &lp);
+    if (st == TAPS_OK) st = check_graph(graph, false);
+    if (st != TAPS_OK) return st;
+    if (!op_offsets) return fail(TAPS_ERR_ARG, "op_offsets is NULL");
+    return enumerate(graph, lp, 0xFFu, op_offsets, strategies, capacity, stream);
+}
+
+taps_status taps_enumerate_strategies_mesh(const taps_graph *graph, const taps_cluster *cluster,
+                                           const taps_mesh *mesh, uint64_t *op_offsets,
+                                           taps_strategy *strategies, uint64_t capacity,
+                                           void *stream) {
+    g_last_error.clear();
+    taps_launch lp;
+    taps_status st = check_cluster(cluster, &lp);
+    if (st == TAPS_OK) st = check_graph(graph, false);
+    if (st != TAPS_OK) return st;
+    if (!op_offsets) return fail(TAPS_ERR_ARG, "op_offsets is NULL");
+    uint32_t allowed = 0;
+    if ((st = mesh_cuts(mesh, lp.n, &allowed)) != TAPS_OK) return st;
+    return enumerate(graph, lp, allowed, op_offsets, strategies, capacity, stream);
 }
 
 taps_status taps_node_costs(const taps_graph *graph, const taps_cluster *cluster,

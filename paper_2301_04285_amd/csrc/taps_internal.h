@@ -64,7 +64,8 @@ struct taps_row_ref {
 hipError_t taps_launch_enumerate(const taps_op *ops, uint32_t n, uint32_t n_ops,
                                  uint32_t n_chunks, const uint32_t *first_chunk,
                                  const uint64_t *base, const uint64_t *valid_flag,
-                                 uint32_t *counts, taps_strategy *out, hipStream_t stream);
+                                 uint32_t allowed_cuts, uint32_t *counts, taps_strategy *out,
+                                 hipStream_t stream);
 // scan: n_ops + 2 entries (operator offsets, total, valid flag); base: n_chunks.
 hipError_t taps_launch_chunk_scan(const uint32_t *counts, uint32_t n_chunks,
                                   const uint32_t *first_chunk, uint32_t n_ops, uint64_t capacity,

@@ -74,11 +74,14 @@ __device__ inline uint32_t find_chunk_owner(const uint32_t *first_chunk, uint32_
 // Count pass (out == nullptr): counts[c] = valid candidates of the chunk.
 // Emit pass: valid candidates go to out[base[c] + rank among the chunk's],
 // only if the scan found the enumeration valid (scan[n_ops + 1] == 1).
+// allowed_cuts: level boundaries a strategy's axis runs may meet (bit c: the
+// boundary between levels c-1 and c); all of them without a fixed mesh.
 __global__ __launch_bounds__(kWave) void k_enumerate(const taps_op *__restrict__ ops, uint32_t n,
                                                      uint32_t n_ops,
                                                      const uint32_t *__restrict__ first_chunk,
                                                      const uint64_t *__restrict__ base,
                                                      const uint64_t *__restrict__ valid_flag,
+                                                     uint32_t allowed_cuts,
                                                      uint32_t *__restrict__ counts,
                                                      taps_strategy *__restrict__ out) {
     __shared__ uint32_t W[9 * 9 * 9];
@@ -98,6 +101,8 @@ __global__ __launch_bounds__(kWave) void k_enumerate(const taps_op *__restrict__
     if (valid)
         for (uint32_t a = 0; a < n_axes; ++a)
             if (op.axis_len[a] & (((int64_t)1 << expo[a]) - 1)) valid = false;
+    // a fixed mesh admits only boundaries between axis runs that are mesh boundaries
+    if (valid && (taps_describe(n_axes, expo, pos).cuts & ~allowed_cuts)) valid = false;
     const uint64_t m = __ballot(valid);
     if (counts && lane == 0) counts[c] = (uint32_t)__builtin_popcountll(m);
     if (out && valid) {
@@ -489,10 +494,11 @@ inline uint32_t blocks_for(uint64_t n, uint32_t per) { return (uint32_t)((n + pe
 hipError_t taps_launch_enumerate(const taps_op *ops, uint32_t n, uint32_t n_ops,
                                  uint32_t n_chunks, const uint32_t *first_chunk,
                                  const uint64_t *base, const uint64_t *valid_flag,
-                                 uint32_t *counts, taps_strategy *out, hipStream_t stream) {
+                                 uint32_t allowed_cuts, uint32_t *counts, taps_strategy *out,
+                                 hipStream_t stream) {
     if (n_chunks == 0) return hipSuccess;
     hipLaunchKernelGGL(k_enumerate, dim3(n_chunks), dim3(kWave), 0, stream, ops, n, n_ops,
-                       first_chunk, base, valid_flag, counts, out);
+                       first_chunk, base, valid_flag, allowed_cuts, counts, out);
     return hipGetLastError();
 }
 

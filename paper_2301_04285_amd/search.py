@@ -17,8 +17,9 @@ Formulation, read per original edge:
 The paper writes the degree constraints summed over all auxiliary edges of an auxiliary
 vertex; the per-edge form implies them and keeps exactly one pair per original edge.
 Once X is integral the pair variables are forced to 0 or 1, so they stay continuous.
-The memory constraint (Eq. 18) needs a memory cost the paper does not define and is
-left out. Node costs enter once per operator (the paper folds the consumer's
+The memory constraint (Eq. 18) needs a memory cost M_ij the paper does not define;
+with ``memory`` and ``budget`` (per-strategy bytes per device from taps_memory_costs)
+the chosen strategies must fit the budget, counted once per operator. Node costs enter once per operator (the paper folds the consumer's
 intra-operator cost into the weight of each of its in-edges, which counts an operator
 with several inputs several times and one with none never).
 
@@ -34,7 +35,7 @@ from typing import Dict, List, Optional, Sequence
 
 import numpy as np
 
-__all__ = ["Plan", "solve", "plan_cost", "compare", "host_tables"]
+__all__ = ["Plan", "solve", "plan_cost", "compare", "compare_mesh", "host_tables"]
 
 
 @dataclass
@@ -241,6 +242,28 @@ def compare(graph, node_t, edge_t, node_vol, edge_vol, time_limit: float = 600.0
 # by the library on the GPU, both searches on the host.
 # ---------------------------------------------------------------------------
 
+def compare_mesh(graph, cluster, mesh, time_limit: float = 600.0, device="cuda") -> Dict:
+    """TAPS over every device matrix against TAPS restricted to the strategies a
+    fixed device mesh expresses (each operator axis sharded over whole,
+    consecutive mesh dimensions, as a mesh-based search would), both searched and
+    priced with the topology-aware time t.  The restricted space is a subset, so
+    its best plan is never cheaper."""
+    import torch
+    from . import taps
+    out = {}
+    for key, m in (("free", None), ("mesh", mesh)):
+        tabs = taps.build_tables(graph, cluster, device=device, mesh=m)
+        torch.cuda.synchronize()
+        nt, et = host_tables(graph, tabs, "t")
+        plan = solve(graph, nt, et, time_limit)
+        out[key] = {"t_s": plan_cost(graph, nt, et, plan.choice), "binaries": plan.n_binaries,
+                    "pairs": plan.n_pairs, "solve_s": plan.solve_s}
+        del tabs
+    out["mesh"] = {**out["mesh"], "dims": list(mesh)}
+    out["mesh_over_free"] = out["mesh"]["t_s"] / out["free"]["t_s"] if out["free"]["t_s"] else 1.0
+    return out
+
+
 def experiment_workloads():
     """(name, graph, cluster) of every comparison: the five configurations (the
     transformer ones cut to one layer, as the paper searches one layer of a stack of
@@ -253,10 +276,10 @@ def experiment_workloads():
         g = W.leading_ops(w.graph, 14) if k in (3, 5) else w.graph
         tag = w.name + (" (one layer)" if k in (3, 5) else "")
         for cname, cl in w.clusters:
-            out.append((f"{tag} / {cname}", g, cl))
+            out.append((f"{tag} / {cname}", g, cl, W.physical_mesh(k, cl)))
     paper = W.Cluster(2, 8, 60 * W.GB, 6 * W.GB)
-    out.append(("gpt-4L-h1024-fp16 / 2x8 at 60/6 GB/s", W.config(2).graph, paper))
-    out.append(("mlp64-fp16 / 2x8 at 60/6 GB/s", W.config(4).graph, paper))
+    out.append(("gpt-4L-h1024-fp16 / 2x8 at 60/6 GB/s", W.config(2).graph, paper, (8, 2)))
+    out.append(("mlp64-fp16 / 2x8 at 60/6 GB/s", W.config(4).graph, paper, (8, 2)))
     return out
 
 
@@ -277,6 +300,9 @@ def main() -> int:
                     help="search this workload (JSON written by workloads.workload_to_json, "
                          "e.g. `python -m paper_2301_04285_amd.workloads 2 w.json`) instead of "
                          "the built-in ones")
+    ap.add_argument("--mesh-space", action="store_true",
+                    help="instead: TAPS over every device matrix against TAPS over the strategies "
+                         "of the workload's fixed physical mesh (taps_enumerate_strategies_mesh)")
     ap.add_argument("--memory-budget-gb", type=float, default=0.0,
                     help="device-memory constraint (Eq. 18) in GB: the chosen strategies' weight "
                          "and output shards per device (taps_memory_costs) must fit (0 = none)")
@@ -292,11 +318,17 @@ def main() -> int:
         from . import workloads as W
         with open(args.workload_json) as f:
             w = W.workload_from_json(f.read())
-        runs = [(f"{w.name} / {n}", w.graph, cl) for n, cl in w.clusters]
+        runs = [(f"{w.name} / {n}", w.graph, cl,
+                 tuple(m for m in (cl.devices_per_node, cl.nodes) if m > 1))
+                for n, cl in w.clusters]
     else:
         runs = experiment_workloads()
-    for name, g, cl in runs:
+    for name, g, cl, mesh in runs:
         if args.only not in name:
+            continue
+        if args.mesh_space:
+            r = compare_mesh(g, cl, mesh, args.time_limit)
+            print(json.dumps({"workload": name, **r}), flush=True)
             continue
         tabs = taps.build_tables(g, cl)
         torch.cuda.synchronize()

@@ -38,6 +38,13 @@ class Cluster(C.Structure):
                 ("bw_intra", C.c_uint64), ("bw_inter", C.c_uint64)]
 
 
+MAX_LEVELS = 8
+
+
+class Mesh(C.Structure):
+    _fields_ = [("n_dims", C.c_uint32), ("dims", C.c_uint32 * MAX_LEVELS)]
+
+
 class Tensor(C.Structure):
     _fields_ = [("rank", C.c_uint8), ("axis", C.c_uint8 * MAX_RANK)]
 
@@ -80,6 +87,9 @@ def load():
         L.taps_enumerate_strategies.restype = C.c_int
         L.taps_enumerate_strategies.argtypes = [P(GraphS), P(Cluster), P(C.c_uint64), C.c_void_p,
                                                 C.c_uint64, C.c_void_p]
+        L.taps_enumerate_strategies_mesh.restype = C.c_int
+        L.taps_enumerate_strategies_mesh.argtypes = [P(GraphS), P(Cluster), P(Mesh), P(C.c_uint64),
+                                                     C.c_void_p, C.c_uint64, C.c_void_p]
         L.taps_node_costs.restype = C.c_int
         L.taps_node_costs.argtypes = [P(GraphS), P(Cluster), C.c_void_p, P(C.c_uint64), Table,
                                       C.c_void_p]
@@ -201,29 +211,47 @@ def _u64_array(a: np.ndarray):
 # the three calls
 # ---------------------------------------------------------------------------
 
+def pack_mesh(mesh) -> Mesh:
+    """A fixed device mesh, innermost dimension first."""
+    dims = [int(m) for m in mesh]
+    if len(dims) > MAX_LEVELS:
+        raise ValueError(f"a mesh has at most {MAX_LEVELS} dimensions")
+    return Mesh(len(dims), (C.c_uint32 * MAX_LEVELS)(*dims))
+
+
 def taps_enumerate_strategies(graph, cluster, device="cuda", stream=None, size_only=False,
-                              out=None):
+                              out=None, mesh=None):
     """(op_offsets as numpy uint64 [n_ops+1], strategies as a device uint8
     tensor [S, 16]: log2 degrees then device-map positions as int8).
     ``out``: a preallocated device uint8 tensor [capacity, 16] to fill in one
-    call; otherwise a size query runs first."""
+    call; otherwise a size query runs first.  ``mesh`` (sizes, innermost
+    first): only the strategies a fixed device mesh expresses
+    (taps_enumerate_strategies_mesh)."""
     import torch
     g = _graph(graph)
     cl = pack_cluster(cluster)
     offs = np.zeros(g.n_ops + 1, dtype=np.uint64)
     L = load()
+    if mesh is None:
+        name = "taps_enumerate_strategies"
+
+        def call(ptr, cap):
+            return L.taps_enumerate_strategies(C.byref(g.struct), C.byref(cl), _u64_array(offs),
+                                               ptr, cap, _stream(stream))
+    else:
+        name = "taps_enumerate_strategies_mesh"
+        ms = pack_mesh(mesh)
+
+        def call(ptr, cap):
+            return L.taps_enumerate_strategies_mesh(C.byref(g.struct), C.byref(cl), C.byref(ms),
+                                                    _u64_array(offs), ptr, cap, _stream(stream))
     if out is None:
-        st = L.taps_enumerate_strategies(C.byref(g.struct), C.byref(cl), _u64_array(offs), None,
-                                         0, _stream(stream))
-        _check(st, "taps_enumerate_strategies")
+        _check(call(None, 0), name)
         if size_only:
             return offs, None
         out = torch.empty((max(int(offs[-1]), 1), STRATEGY_BYTES), dtype=torch.uint8,
                           device=device)
-    st = L.taps_enumerate_strategies(C.byref(g.struct), C.byref(cl), _u64_array(offs),
-                                     C.c_void_p(out.data_ptr()), int(out.shape[0]),
-                                     _stream(stream))
-    _check(st, "taps_enumerate_strategies")
+    _check(call(C.c_void_p(out.data_ptr()), int(out.shape[0])), name)
     return offs, out[:int(offs[-1])]
 
 
@@ -396,13 +424,16 @@ def _torch():
 
 
 def build_tables(graph, cluster, device="cuda", stream=None, out: Optional[Tables] = None,
-                 shared: bool = False) -> Tables:
+                 shared: bool = False, mesh=None) -> Tables:
     """Enumeration, node table and edge table of one graph on one cluster.
     ``out``: tables of an earlier build of the same graph to fill again;
-    ``shared``: identical edge tables computed once (taps_edge_costs_shared)."""
+    ``shared``: identical edge tables computed once (taps_edge_costs_shared);
+    ``mesh``: the strategy space of a fixed device mesh (sizes, innermost
+    first) instead of every device matrix."""
     g = _graph(graph)
     offs, strat = taps_enumerate_strategies(g, cluster, device=device, stream=stream,
-                                            out=out.strategies if out is not None else None)
+                                            out=out.strategies if out is not None else None,
+                                            mesh=mesh)
     node = taps_node_costs(g, cluster, strat, offs, stream=stream,
                            out=out.node if out is not None else None)
     eoffs, edge = taps_edge_costs(g, cluster, strat, offs, stream=stream,

@@ -292,6 +292,25 @@ def config(index: int) -> Workload:
 
 ALL_CONFIGS = (1, 2, 3, 4, 5)
 
+# Physical meshes of the configurations that name one (innermost dimension
+# first: the 8 devices of a node, then the node grid).
+CONFIG_MESHES = {4: (8, 4, 2), 5: (8, 4, 4)}
+
+
+def physical_mesh(index: int, cluster: Cluster) -> Tuple[int, ...]:
+    """The fixed device mesh of a configuration's cluster: the one the
+    configuration names, else (devices per node, nodes) without sizes of 1."""
+    if index in CONFIG_MESHES and math_prod(CONFIG_MESHES[index]) == cluster.devices:
+        return CONFIG_MESHES[index]
+    return tuple(m for m in (cluster.devices_per_node, cluster.nodes) if m > 1)
+
+
+def math_prod(xs: Sequence[int]) -> int:
+    out = 1
+    for x in xs:
+        out *= x
+    return out
+
 
 def random_graph(rng: random.Random, n_ops: int, max_axes: int = 5, max_rank: int = 4,
                  dtype_choices: Sequence[int] = (2, 4), len_pow_range=(0, 7)) -> Graph:

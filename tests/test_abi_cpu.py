@@ -18,7 +18,8 @@ def lib():
 
 def test_exports_every_declared_symbol(lib):
     declared = T.declared_symbols()
-    assert declared == sorted(["taps_enumerate_strategies", "taps_node_costs", "taps_edge_costs",
+    assert declared == sorted(["taps_enumerate_strategies", "taps_enumerate_strategies_mesh",
+                               "taps_node_costs", "taps_edge_costs",
                                "taps_edge_costs_shared", "taps_edge_costs_backward",
                                "taps_edge_costs_sweep", "taps_memory_costs",
                                "taps_set_edge_kernel_events", "taps_status_str",
@@ -85,6 +86,29 @@ def test_null_arguments(lib):
                                T._table(None), 0, None) == T.ERR_ARG
     assert lib.taps_node_costs(C.byref(g.struct), C.byref(cl), None, T._u64_array(good),
                                T.Table(1, 1, 1, 1, 1), None) == T.ERR_ARG
+
+
+@pytest.mark.parametrize("mesh", [
+    [4, 2],            # 8 devices on a 16-device cluster
+    [8, 2, 2],         # 32 devices
+    [3, 4, 4],         # not a power of two
+    [1, 16],           # size 1
+    [16, 0],
+    [2] * 9,           # more dimensions than levels
+])
+def test_mesh_validation(lib, mesh):
+    g = T.pack_graph(W.mlp2())
+    cl = T.pack_cluster(W.Cluster(2, 8, 10, 1))
+    offs = np.full(4, 7, np.uint64)
+    m = T.Mesh(min(len(mesh), 8), (C.c_uint32 * 8)(*mesh[:8]))
+    if len(mesh) > 8:
+        m.n_dims = len(mesh)
+    st = lib.taps_enumerate_strategies_mesh(C.byref(g.struct), C.byref(cl), C.byref(m),
+                                            T._u64_array(offs), None, 0, None)
+    assert st == T.ERR_TOPOLOGY and T.last_error() != ""
+    assert (offs == 7).all()   # nothing written
+    assert lib.taps_enumerate_strategies_mesh(C.byref(g.struct), C.byref(cl), None,
+                                              T._u64_array(offs), None, 0, None) == T.ERR_ARG
 
 
 def _op(**kw):

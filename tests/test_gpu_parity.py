@@ -67,26 +67,32 @@ def assert_records(got, ref, where=""):
     assert bad.size == 0, f"{where}: t differs at {bad[:5]}: {got['t'][bad[:5]]} vs {ref['t'][bad[:5]]}"
 
 
-def check_strategies(T, graph, cluster, offs, strat):
+def _oracle_strategies(op, cluster, mesh=None):
+    if mesh is None:
+        return O.enumerate_strategies(op, cluster.devices)
+    return O.enumerate_strategies_mesh(op, mesh)
+
+
+def check_strategies(T, graph, cluster, offs, strat, mesh=None):
     lg, pos = T.strategies_to_numpy(strat)
     for k, op in enumerate(graph.ops):
-        ref = O.enumerate_strategies(op, cluster.devices)
+        ref = _oracle_strategies(op, cluster, mesh)
         a, b = int(offs[k]), int(offs[k + 1])
         assert b - a == len(ref), op.name
         deg = np.where(pos[a:b, :op.n_axes] >= 0, 1 << lg[a:b, :op.n_axes].astype(np.int64), 1)
         assert np.array_equal(deg, ref["degree"][:, :op.n_axes]), op.name
         assert np.array_equal(pos[a:b, :op.n_axes], ref["pos"][:, :op.n_axes]), op.name
         assert np.all(lg[a:b, op.n_axes:] == 0) and np.all(pos[a:b, op.n_axes:] == -1)
-    return [O.enumerate_strategies(op, cluster.devices) for op in graph.ops]
+    return [_oracle_strategies(op, cluster, mesh) for op in graph.ops]
 
 
-def full_check(T, graph, cluster, name):
+def full_check(T, graph, cluster, name, mesh=None):
     import torch
     say(f"[gpu] build {name}")
-    tabs = T.build_tables(graph, cluster)
+    tabs = T.build_tables(graph, cluster, mesh=mesh)
     torch.cuda.synchronize()
     say(f"[gpu] built {name}: {int(tabs.edge_offsets[-1])} edge entries")
-    ref_strats = check_strategies(T, graph, cluster, tabs.op_offsets, tabs.strategies)
+    ref_strats = check_strategies(T, graph, cluster, tabs.op_offsets, tabs.strategies, mesh)
     node = _host(tabs.node)
     edge = _host(tabs.edge)
     for k, op in enumerate(graph.ops):
@@ -212,6 +218,43 @@ def test_degenerate_clusters(T):
     g = W.gpt(1, 64, 2, 128, 2, 2)
     for cl in (W.Cluster(2, 128, 300, 7), W.Cluster(32, 8, 300, 7), W.Cluster(256, 1, 300, 7)):
         full_check(T, g, cl, f"gpt1-s128 N={cl.devices} L={cl.devices_per_node}")
+
+
+def _random_mesh(rng, n):
+    dims, left = [], n
+    while left:
+        e = rng.randint(1, min(3, left))
+        dims.append(1 << e)
+        left -= e
+    return dims
+
+
+def test_fixed_mesh_spaces(T):
+    """taps_enumerate_strategies_mesh and the tables over its strategies: the
+    workloads on their meshes (the 4 x 4 x 8 and 2 x 4 x 8 meshes with the node's
+    8 devices innermost), the 2 x 2 and 4 meshes of Table 3, and random graphs on
+    random meshes."""
+    cases = [(W.config(1).graph, W.config(1).clusters[0][1], [2, 2]),
+             (W.config(1).graph, W.config(1).clusters[0][1], [4]),
+             (W.config(2).graph, W.config(2).clusters[0][1], [8, 2]),
+             (W.config(3).graph, W.config(3).clusters[0][1], [8, 4]),
+             (W.config(3).graph, W.config(3).clusters[1][1], [16, 2]),
+             (W.config(4).graph, W.config(4).clusters[0][1], [8, 4, 2]),
+             (W.config(5).graph, W.config(5).clusters[0][1], [8, 4, 4])]
+    for g, cl, mesh in cases:
+        full_check(T, g, cl, f"{len(g.ops)} ops N={cl.devices} mesh={mesh}", mesh=mesh)
+    rng = random.Random(4488)
+    done = 0
+    for k, (g, cl) in enumerate(_random_cases(4488, 16)):
+        mesh = _random_mesh(rng, cl.devices.bit_length() - 1)
+        try:
+            full_check(T, g, cl, f"random {k} N={cl.devices} mesh={mesh}", mesh=mesh)
+        except T.TapsError as ex:
+            assert ex.status == T.ERR_NO_STRATEGY
+            assert any(len(O.enumerate_strategies_mesh(op, mesh)) == 0 for op in g.ops)
+            continue
+        done += 1
+    assert done >= 8
 
 
 def test_empty_graph_and_no_edges(T):

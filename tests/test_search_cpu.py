@@ -14,8 +14,8 @@ from paper_2301_04285_amd import search as S
 from paper_2301_04285_amd import workloads as W
 
 
-def _fields(oracle_lib, graph, cluster):
-    tab = oracle_lib.build_tables(graph, cluster)
+def _fields(oracle_lib, graph, cluster, mesh=None):
+    tab = oracle_lib.build_tables(graph, cluster, mesh=mesh)
     out = {}
     for f in ("t", "vol"):
         node = [np.asarray(v[f], dtype=np.float64) for v in tab.node]
@@ -208,3 +208,20 @@ def test_compare_under_a_memory_budget(oracle_lib):
     r = S.compare(w.graph, *tabs["t"], *tabs["vol"], memory=mem, budget=tight)
     assert all(m <= tight for m in r["memory_bytes"])
     assert r["t_topology_plan_s"] >= free["t_topology_plan_s"] - 1e-15
+
+
+def test_fixed_mesh_space_search(oracle_lib):
+    """On a fixed mesh the search runs over a subset of the strategies: the ILP
+    finds that subset's exhaustive optimum, which is never below the optimum over
+    every device matrix (the 2-layer MLP on a 1-D mesh of 4 and on 2 x 2, whose
+    mesh dimensions are the binary levels, so nothing is lost)."""
+    w = W.config(1)
+    cl = w.clusters[0][1]
+    free = _fields(oracle_lib, w.graph, cl)["t"]
+    t_free = S.solve(w.graph, *free).objective
+    for mesh, same in (([4], False), ([2, 2], True)):
+        node, edge = _fields(oracle_lib, w.graph, cl, mesh)["t"]
+        plan = S.solve(w.graph, node, edge)
+        assert _close(plan.objective, _exhaustive(w.graph, node, edge))
+        assert plan.objective >= t_free * (1 - 1e-12)
+        assert _close(plan.objective, t_free) == same
