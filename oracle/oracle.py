@@ -64,6 +64,21 @@ class OrUnified(C.Structure):
                 ("m_from", C.c_int32 * MAX_SUB), ("m_to", C.c_int32 * MAX_SUB)]
 
 
+MAX_CLASSES = 4
+
+
+class OrTopology(C.Structure):
+    _fields_ = [("n_classes", C.c_int32), ("pad_", C.c_int32),
+                ("domain", C.c_int64 * MAX_CLASSES), ("bw", C.c_uint64 * MAX_CLASSES)]
+
+
+def make_topology(topo) -> OrTopology:
+    """workloads.Topology -> the oracle's struct."""
+    assert 1 <= len(topo.domains) == len(topo.bw) <= MAX_CLASSES
+    return OrTopology(len(topo.domains), 0, (C.c_int64 * MAX_CLASSES)(*topo.domains),
+                      (C.c_uint64 * MAX_CLASSES)(*topo.bw))
+
+
 RECORD_DTYPE = np.dtype([("t", "<f8"), ("vol", "<u8"), ("intra", "<u8"), ("inter", "<u8"),
                          ("meta", "<u4"), ("pad_", "<u4")])
 assert RECORD_DTYPE.itemsize == C.sizeof(OrRecord)
@@ -96,6 +111,21 @@ def lib():
         L.or_enumerate.argtypes = [P(OrOp), i64, C.c_int, P(OrStrategy), i64]
         L.or_enumerate_mesh.restype = i64
         L.or_enumerate_mesh.argtypes = [P(OrOp), P(i64), C.c_int, C.c_int, P(OrStrategy), i64]
+        L.or_node_cost_topo.restype = None
+        L.or_node_cost_topo.argtypes = [P(OrOp), P(OrStrategy), i64, P(OrTopology), P(OrRecord)]
+        L.or_node_table_topo.restype = i64
+        L.or_node_table_topo.argtypes = [P(OrOp), P(OrStrategy), i64, i64, P(OrTopology),
+                                         P(OrRecord)]
+        L.or_edge_cost_topo.restype = C.c_int
+        L.or_edge_cost_topo.argtypes = [P(OrOp), P(OrStrategy), P(OrOp), C.c_int, P(OrStrategy),
+                                        i64, P(OrTopology), P(OrRecord)]
+        L.or_edge_table_topo.restype = i64
+        L.or_edge_table_topo.argtypes = [P(OrOp), P(OrStrategy), i64, P(OrOp), C.c_int,
+                                         P(OrStrategy), i64, i64, P(OrTopology), P(OrRecord)]
+        L.or_edge_entries_topo.restype = i64
+        L.or_edge_entries_topo.argtypes = [P(OrOp), P(OrStrategy), P(OrOp), C.c_int,
+                                           P(OrStrategy), P(i64), P(i64), i64, i64,
+                                           P(OrTopology), P(OrRecord)]
         L.or_node_cost.restype = None
         L.or_node_cost.argtypes = [P(OrOp), P(OrStrategy), i64, i64, u64, u64, P(OrRecord)]
         L.or_node_table.restype = i64
@@ -404,6 +434,62 @@ def node_cost(op, s, cluster):
 
 
 # ---------------------------------------------------------------------------
+# several link classes (workloads.Topology)
+# ---------------------------------------------------------------------------
+
+def node_cost_topo(op, s, topo):
+    o, t = make_op(op), make_topology(topo)
+    rec = OrRecord()
+    s1 = np.ascontiguousarray(s, dtype=STRATEGY_DTYPE).reshape(1)
+    lib().or_node_cost_topo(C.byref(o), _sp(s1), topo.devices, C.byref(t), C.byref(rec))
+    return (rec.t, rec.vol, rec.intra, rec.inter, rec.meta)
+
+
+def node_table_topo(op, strategies: np.ndarray, topo) -> np.ndarray:
+    o, t = make_op(op), make_topology(topo)
+    out = np.zeros(len(strategies), dtype=RECORD_DTYPE)
+    n = lib().or_node_table_topo(C.byref(o), _sp(strategies), len(strategies), topo.devices,
+                                 C.byref(t), _rp(out))
+    assert n == len(strategies)
+    return out
+
+
+def edge_cost_topo(src_op, si, dst_op, slot, sj, topo):
+    a, b, t = make_op(src_op), make_op(dst_op), make_topology(topo)
+    rec = OrRecord()
+    s1 = np.ascontiguousarray(si, dtype=STRATEGY_DTYPE).reshape(1)
+    s2 = np.ascontiguousarray(sj, dtype=STRATEGY_DTYPE).reshape(1)
+    rc = lib().or_edge_cost_topo(C.byref(a), _sp(s1), C.byref(b), slot, _sp(s2), topo.devices,
+                                 C.byref(t), C.byref(rec))
+    assert rc == 0
+    return (rec.t, rec.vol, rec.intra, rec.inter, rec.meta)
+
+
+def edge_table_topo(src_op, src_strats: np.ndarray, dst_op, slot: int, dst_strats: np.ndarray,
+                    topo) -> np.ndarray:
+    a, b, t = make_op(src_op), make_op(dst_op), make_topology(topo)
+    out = np.zeros(len(src_strats) * len(dst_strats), dtype=RECORD_DTYPE)
+    n = lib().or_edge_table_topo(C.byref(a), _sp(src_strats), len(src_strats), C.byref(b), slot,
+                                 _sp(dst_strats), len(dst_strats), topo.devices, C.byref(t),
+                                 _rp(out))
+    assert n == out.size, "oracle failed on this edge"
+    return out.reshape(len(src_strats), len(dst_strats))
+
+
+def edge_entries_topo(src_op, src_strats, dst_op, slot, dst_strats, ii, jj, topo) -> np.ndarray:
+    a, b, t = make_op(src_op), make_op(dst_op), make_topology(topo)
+    ii = np.ascontiguousarray(ii, dtype=np.int64)
+    jj = np.ascontiguousarray(jj, dtype=np.int64)
+    out = np.zeros(len(ii), dtype=RECORD_DTYPE)
+    n = lib().or_edge_entries_topo(C.byref(a), _sp(src_strats), C.byref(b), slot, _sp(dst_strats),
+                                   ii.ctypes.data_as(C.POINTER(C.c_int64)),
+                                   jj.ctypes.data_as(C.POINTER(C.c_int64)), len(ii), topo.devices,
+                                   C.byref(t), _rp(out))
+    assert n == len(ii)
+    return out
+
+
+# ---------------------------------------------------------------------------
 # whole graphs
 # ---------------------------------------------------------------------------
 
@@ -415,11 +501,22 @@ class Tables:
 
 
 def build_tables(graph, cluster, edges: Optional[Sequence[int]] = None,
-                 mesh: Optional[Sequence[int]] = None) -> Tables:
+                 mesh: Optional[Sequence[int]] = None, topology=None) -> Tables:
     """Every table of ``graph`` on ``cluster`` (only the listed edges if given;
-    over the strategies of the fixed mesh ``mesh`` if given)."""
+    over the strategies of the fixed mesh ``mesh`` if given; with the link
+    classes of ``topology`` (a workloads.Topology of cluster.devices devices)
+    in place of the cluster's two if given)."""
     strats = [enumerate_strategies(op, cluster.devices) if mesh is None
               else enumerate_strategies_mesh(op, mesh) for op in graph.ops]
+    if topology is not None:
+        assert topology.devices == cluster.devices
+        node = [node_table_topo(op, s, topology) for op, s in zip(graph.ops, strats)]
+        edge = []
+        for k, e in enumerate(graph.edges):
+            edge.append(edge_table_topo(graph.ops[e.src], strats[e.src], graph.ops[e.dst], e.slot,
+                                        strats[e.dst], topology)
+                        if edges is None or k in edges else None)
+        return Tables(strats, node, edge)
     node = [node_table(op, s, cluster) for op, s in zip(graph.ops, strats)]
     want = set(range(len(graph.edges))) if edges is None else set(edges)
     edge = []

@@ -52,7 +52,13 @@
  *        AllToAll, remove, naive), ties to the first; the volume table takes
  *        the smallest volume of the four;
  *   R-i  partial sums of the producer are resolved inside the producer's own
- *        intra-op cost, so the edge sees those axes as replicated.
+ *        intra-op cost, so the edge sees those axes as replicated;
+ *   R-j  (an extension) a hierarchy of link classes: blocks of domain[0] <=
+ *        domain[1] <= ... <= domain[C-1] = N consecutive ranks; a collective
+ *        belongs to the smallest domain whose Algorithm 2 / 3 count is zero
+ *        (its group fits inside one block), takes that class's bandwidth and
+ *        the count of the next smaller domain as its ct; with the domains
+ *        (L, N) this is the paper's two-class model.
  */
 #include <stdint.h>
 #include <stdlib.h>
@@ -105,6 +111,30 @@ typedef struct {
     uint64_t link_nb;                       /* volume carried by the link class (Eq. 14 for AllToAll) */
     double cost;                            /* seconds */
 } or_redop;
+
+/* Link classes (reading R-j).  Class 0: links inside one block of domain[0]
+ * consecutive ranks (a node); class c >= 1: links between the domain[c-1]
+ * blocks of one domain[c] block, bw[c] bytes/s each.  domain[] is
+ * non-decreasing, domain[n_classes - 1] = N.  The paper's cluster is
+ * {2, {L, N}, {B_intra, B_inter}}. */
+#define OR_MAX_CLASSES 4
+typedef struct {
+    int32_t n_classes;
+    int32_t pad_;
+    int64_t domain[OR_MAX_CLASSES];
+    uint64_t bw[OR_MAX_CLASSES];
+} or_topology;
+
+static or_topology two_class(int64_t N, int64_t L, uint64_t Bintra, uint64_t Binter) {
+    or_topology t;
+    memset(&t, 0, sizeof t);
+    t.n_classes = 2;
+    t.domain[0] = L;
+    t.domain[1] = N;
+    t.bw[0] = Bintra;
+    t.bw[1] = Binter;
+    return t;
+}
 
 typedef struct {
     int32_t h;                  /* depth of the unified device matrix */
@@ -371,8 +401,8 @@ int64_t or_gather_ct(const int64_t *D, int h, const int32_t *M, int r, int g, in
  * V / B_e (Eq. 11, Eq. 12) with ct from Algorithm 2.
  * ------------------------------------------------------------------------- */
 static void allreduce_tensor(const or_op *op, const or_tensor *t, const int64_t *D, int h,
-                             const or_strategy *s, int64_t N, int64_t L, uint64_t Bintra,
-                             uint64_t Binter, or_record *rec, uint32_t *n_coll, uint32_t *n_inter,
+                             const or_strategy *s, int64_t N, const or_topology *topo,
+                             or_record *rec, uint32_t *n_coll, uint32_t *n_inter,
                              uint32_t *sum_ct) {
     int32_t M[OR_MAX_RANK];
     tensor_map(t, s, M);
@@ -384,35 +414,49 @@ static void allreduce_tensor(const or_op *op, const or_tensor *t, const int64_t 
     uint64_t data_nb = (uint64_t)tensor_elems(op, t) * (uint64_t)op->dtype_bytes * (uint64_t)N /
                        (uint64_t)used;
     uint64_t V = 2 * (uint64_t)(g - 1) * data_nb / (uint64_t)g;
-    int64_t ct = or_allreduce_ct(D, h, M, t->rank, L);
+    /* reading R-j: the smallest domain that holds the group, ct of the next smaller one */
+    int cls = 0;
+    while (cls < topo->n_classes - 1 && or_allreduce_ct(D, h, M, t->rank, topo->domain[cls]) != 0)
+        ++cls;
+    int64_t ct = cls ? or_allreduce_ct(D, h, M, t->rank, topo->domain[cls - 1]) : 0;
     rec->vol += V;
     *n_coll += 1;
     if (ct == 0) {
         rec->intra += V;
-        rec->t += ((double)V / (double)N) / (double)Bintra;
+        rec->t += ((double)V / (double)N) / (double)topo->bw[0];
     } else {
         rec->inter += V * (uint64_t)ct;
-        double Be = (double)Binter / (double)ct;
+        double Be = (double)topo->bw[cls] / (double)ct;
         rec->t += ((double)V / (double)N) / Be;
         *n_inter += 1;
         *sum_ct += (uint32_t)ct;
     }
 }
 
-void or_node_cost(const or_op *op, const or_strategy *s, int64_t N, int64_t L, uint64_t Bintra,
-                  uint64_t Binter, or_record *rec) {
+void or_node_cost_topo(const or_op *op, const or_strategy *s, int64_t N, const or_topology *topo,
+                       or_record *rec) {
     int64_t D[OR_MAX_DEV];
     int h = device_matrix(op, s, D);
     uint32_t n_coll = 0, n_inter = 0, sum_ct = 0;
     memset(rec, 0, sizeof *rec);
-    allreduce_tensor(op, &op->out, D, h, s, N, L, Bintra, Binter, rec, &n_coll, &n_inter, &sum_ct);
+    allreduce_tensor(op, &op->out, D, h, s, N, topo, rec, &n_coll, &n_inter, &sum_ct);
     for (int k = 0; k < op->n_in; ++k)
-        allreduce_tensor(op, &op->in[k], D, h, s, N, L, Bintra, Binter, rec, &n_coll, &n_inter,
-                         &sum_ct);
+        allreduce_tensor(op, &op->in[k], D, h, s, N, topo, rec, &n_coll, &n_inter, &sum_ct);
     for (int k = 0; k < op->n_w; ++k)
-        allreduce_tensor(op, &op->w[k], D, h, s, N, L, Bintra, Binter, rec, &n_coll, &n_inter,
-                         &sum_ct);
+        allreduce_tensor(op, &op->w[k], D, h, s, N, topo, rec, &n_coll, &n_inter, &sum_ct);
     rec->meta = (n_coll << 2) | (n_inter << 7) | (sum_ct << 12);
+}
+
+void or_node_cost(const or_op *op, const or_strategy *s, int64_t N, int64_t L, uint64_t Bintra,
+                  uint64_t Binter, or_record *rec) {
+    const or_topology topo = two_class(N, L, Bintra, Binter);
+    or_node_cost_topo(op, s, N, &topo, rec);
+}
+
+int64_t or_node_table_topo(const or_op *op, const or_strategy *s, int64_t count, int64_t N,
+                           const or_topology *topo, or_record *out) {
+    for (int64_t k = 0; k < count; ++k) or_node_cost_topo(op, &s[k], N, topo, &out[k]);
+    return count;
 }
 
 int64_t or_node_table(const or_op *op, const or_strategy *s, int64_t count, int64_t N, int64_t L,
@@ -749,12 +793,13 @@ int or_sequence(const int32_t *Mfrom, const int32_t *Mto, int r, int cand, or_re
 typedef struct {
     double t;
     uint64_t vol, intra, inter;
+    uint64_t x[OR_MAX_CLASSES];   /* per link class: link volume x ct (x[0] = intra) */
     uint32_t n_coll, n_inter, sum_ct;
 } seq_cost;
 
 static seq_cost cost_sequence(const int64_t *D, int h, const int32_t *Mfrom, int r,
-                              or_redop *seq, int len, uint64_t shard0_nb, int64_t N, int64_t L,
-                              uint64_t Bintra, uint64_t Binter) {
+                              or_redop *seq, int len, uint64_t shard0_nb, int64_t N,
+                              const or_topology *topo) {
     seq_cost c;
     memset(&c, 0, sizeof c);
     int32_t M[OR_MAX_SUB];
@@ -769,8 +814,19 @@ static seq_cost cost_sequence(const int64_t *D, int h, const int32_t *Mfrom, int
             shard /= (uint64_t)p;
             continue;
         }
+        /* reading R-j: the smallest domain that holds the group, ct (and the
+         * members per block, k) of the next smaller one */
         int64_t k_in = 0;
-        int64_t ct = or_gather_ct(D, h, M, r, op->axis, L, &k_in);
+        int cls = 0;
+        while (cls < topo->n_classes - 1 &&
+               or_gather_ct(D, h, M, r, op->axis, topo->domain[cls], &k_in) != 0)
+            ++cls;
+        int64_t ct = 0;
+        if (cls)
+            ct = or_gather_ct(D, h, M, r, op->axis, topo->domain[cls - 1], &k_in);
+        else
+            or_gather_ct(D, h, M, r, op->axis, topo->domain[0], &k_in);
+        const double Bintra = (double)topo->bw[0], Bcls = (double)topo->bw[cls];
         op->ct = (int32_t)ct;
         op->k_in = (int32_t)k_in;
         uint64_t V, link;
@@ -778,19 +834,19 @@ static seq_cost cost_sequence(const int64_t *D, int h, const int32_t *Mfrom, int
         if (op->kind == OR_ALLGATHER) {
             V = (uint64_t)(p - 1) * shard;                  /* Eq. 9 */
             link = V;
-            cost = ct == 0 ? ((double)V / (double)N) / (double)Bintra
-                           : ((double)V / (double)N) / ((double)Binter / (double)ct);
+            cost = ct == 0 ? ((double)V / (double)N) / Bintra
+                           : ((double)V / (double)N) / (Bcls / (double)ct);
             M[op->from_dim] = -1;
             shard *= (uint64_t)p;
         } else {
             V = (uint64_t)(p - 1) * shard / (uint64_t)p;     /* Eq. 10 */
             if (ct == 0) {
                 link = V;
-                cost = ((double)V / (double)N) / (double)Bintra;
+                cost = ((double)V / (double)N) / Bintra;
             } else {                                          /* Eq. 14, p > k */
                 link = (uint64_t)k_in * (uint64_t)(p - k_in) * shard / (uint64_t)p;
                 double factor = (double)(k_in * (p - k_in)) / (double)(p - 1);
-                cost = factor * ((double)V / (double)N) / ((double)Binter / (double)ct);
+                cost = factor * ((double)V / (double)N) / (Bcls / (double)ct);
             }
             M[op->from_dim] = -1;
             M[op->to_dim] = op->axis;
@@ -803,8 +859,10 @@ static seq_cost cost_sequence(const int64_t *D, int h, const int32_t *Mfrom, int
         c.n_coll += 1;
         if (ct == 0) {
             c.intra += link;
+            c.x[0] += link;
         } else {
             c.inter += link * (uint64_t)ct;
+            c.x[cls] += link * (uint64_t)ct;
             c.n_inter += 1;
             c.sum_ct += (uint32_t)ct;
         }
@@ -856,7 +914,8 @@ int or_edge_detail(const or_op *src, const or_strategy *si, const or_op *dst, in
     if (edge_problem(src, si, dst, slot, sj, N, u, shard0_nb)) return -1;
     int len = or_sequence(u->m_from, u->m_to, u->r, cand, seq);
     if (len < 0) return -1;
-    cost_sequence(u->D, u->h, u->m_from, u->r, seq, len, *shard0_nb, N, L, Bintra, Binter);
+    const or_topology topo = two_class(N, L, Bintra, Binter);
+    cost_sequence(u->D, u->h, u->m_from, u->r, seq, len, *shard0_nb, N, &topo);
     return len;
 }
 
@@ -866,7 +925,8 @@ int or_sequence_cost(const int64_t *D, int h, const int32_t *Mfrom, const int32_
                      uint64_t Binter, or_redop *seq, or_record *rec) {
     int len = or_sequence(Mfrom, Mto, r, cand, seq);
     if (len < 0) return -1;
-    seq_cost c = cost_sequence(D, h, Mfrom, r, seq, len, shard0_nb, N, L, Bintra, Binter);
+    const or_topology topo = two_class(N, L, Bintra, Binter);
+    seq_cost c = cost_sequence(D, h, Mfrom, r, seq, len, shard0_nb, N, &topo);
     rec->t = c.t;
     rec->vol = c.vol;
     rec->intra = c.intra;
@@ -875,14 +935,58 @@ int or_sequence_cost(const int64_t *D, int h, const int32_t *Mfrom, const int32_
     return len;
 }
 
+static uint64_t gcd_u64(uint64_t a, uint64_t b) {
+    while (b) {
+        uint64_t t = a % b;
+        a = b;
+        b = t;
+    }
+    return a;
+}
+
+/* Exact order of sum_c x[c] / bw[c] (reading R-j) as integer keys: with two
+ * classes x[0] bw[1] + x[1] bw[0] (reading R-h's intra/(N B_intra) +
+ * inter/(N B_inter)); with more, sum_c x[c] w[c] with w[c] = lcm(bw) / bw[c],
+ * which must stay below 2^32 (returns -1 otherwise). */
+static int class_weights(const or_topology *topo, uint64_t *w) {
+    if (topo->n_classes == 2) {
+        w[0] = topo->bw[1];
+        w[1] = topo->bw[0];
+        return 0;
+    }
+    unsigned __int128 lcm = 1;
+    for (int c = 0; c < topo->n_classes; ++c) {
+        if (topo->bw[c] == 0) return -1;
+        const uint64_t g = gcd_u64((uint64_t)(lcm % topo->bw[c]), topo->bw[c]);
+        const unsigned __int128 q = lcm / g;
+        if (q >> 64) return -1;
+        lcm = q * topo->bw[c];
+    }
+    for (int c = 0; c < topo->n_classes; ++c) {
+        unsigned __int128 q = lcm / topo->bw[c];
+        if (q >> 32) return -1;
+        w[c] = (uint64_t)q;
+    }
+    return 0;
+}
+
+static unsigned __int128 class_key(const seq_cost *sc, const or_topology *topo, const uint64_t *w) {
+    unsigned __int128 key = 0;
+    for (int c = 0; c < topo->n_classes; ++c) key += (unsigned __int128)sc->x[c] * w[c];
+    return key;
+}
+
 /* Reading R-h: the cheapest of the four candidates by exact comparison of
- * intra/(N B_intra) + inter/(N B_inter), ties to the lower candidate index. */
+ * intra/(N B_intra) + inter/(N B_inter) (per link class under R-j), ties to
+ * the lower candidate index. */
 static int edge_cost_dir(const or_op *src, const or_strategy *si, const or_op *dst, int slot,
-                         const or_strategy *sj, int64_t N, int64_t L, uint64_t Bintra,
-                         uint64_t Binter, int reverse, or_record *rec) {
+                         const or_strategy *sj, int64_t N, const or_topology *topo, int reverse,
+                         or_record *rec) {
     or_unified u;
     uint64_t shard0;
+    uint64_t w[OR_MAX_CLASSES];
     memset(rec, 0, sizeof *rec);
+    if (class_weights(topo, w)) return -1;
     if (edge_problem_dir(src, si, dst, slot, sj, N, reverse, &u, &shard0)) return -1;
     or_redop seq[OR_MAX_SEQ];
     seq_cost best;
@@ -893,10 +997,8 @@ static int edge_cost_dir(const or_op *src, const or_strategy *si, const or_op *d
     for (int c = 0; c < 4; ++c) {
         int len = or_sequence(u.m_from, u.m_to, u.r, c, seq);
         if (len < 0) return -1;
-        seq_cost sc = cost_sequence(u.D, u.h, u.m_from, u.r, seq, len, shard0, N, L, Bintra,
-                                    Binter);
-        unsigned __int128 key = (unsigned __int128)sc.intra * Binter +
-                                (unsigned __int128)sc.inter * Bintra;
+        seq_cost sc = cost_sequence(u.D, u.h, u.m_from, u.r, seq, len, shard0, N, topo);
+        unsigned __int128 key = class_key(&sc, topo, w);
         if (best_c < 0 || key < best_key) {
             best_c = c;
             best_key = key;
@@ -912,10 +1014,16 @@ static int edge_cost_dir(const or_op *src, const or_strategy *si, const or_op *d
     return 0;
 }
 
+int or_edge_cost_topo(const or_op *src, const or_strategy *si, const or_op *dst, int slot,
+                      const or_strategy *sj, int64_t N, const or_topology *topo, or_record *rec) {
+    return edge_cost_dir(src, si, dst, slot, sj, N, topo, 0, rec);
+}
+
 int or_edge_cost(const or_op *src, const or_strategy *si, const or_op *dst, int slot,
                  const or_strategy *sj, int64_t N, int64_t L, uint64_t Bintra, uint64_t Binter,
                  or_record *rec) {
-    return edge_cost_dir(src, si, dst, slot, sj, N, L, Bintra, Binter, 0, rec);
+    const or_topology topo = two_class(N, L, Bintra, Binter);
+    return edge_cost_dir(src, si, dst, slot, sj, N, &topo, 0, rec);
 }
 
 /* The backward direction of the same pair: the gradient moves from the
@@ -923,7 +1031,28 @@ int or_edge_cost(const or_op *src, const or_strategy *si, const or_op *dst, int 
 int or_edge_cost_reverse(const or_op *src, const or_strategy *si, const or_op *dst, int slot,
                          const or_strategy *sj, int64_t N, int64_t L, uint64_t Bintra,
                          uint64_t Binter, or_record *rec) {
-    return edge_cost_dir(src, si, dst, slot, sj, N, L, Bintra, Binter, 1, rec);
+    const or_topology topo = two_class(N, L, Bintra, Binter);
+    return edge_cost_dir(src, si, dst, slot, sj, N, &topo, 1, rec);
+}
+
+/* Row-major table of one edge under a topology: out[i * nd + j]. */
+int64_t or_edge_table_topo(const or_op *src, const or_strategy *ss, int64_t ns, const or_op *dst,
+                           int slot, const or_strategy *sd, int64_t nd, int64_t N,
+                           const or_topology *topo, or_record *out) {
+    for (int64_t i = 0; i < ns; ++i)
+        for (int64_t j = 0; j < nd; ++j)
+            if (edge_cost_dir(src, &ss[i], dst, slot, &sd[j], N, topo, 0, &out[i * nd + j]))
+                return -1;
+    return ns * nd;
+}
+
+/* Selected entries (i[k], j[k]) of one edge table under a topology. */
+int64_t or_edge_entries_topo(const or_op *src, const or_strategy *ss, const or_op *dst, int slot,
+                             const or_strategy *sd, const int64_t *ii, const int64_t *jj,
+                             int64_t n, int64_t N, const or_topology *topo, or_record *out) {
+    for (int64_t k = 0; k < n; ++k)
+        if (edge_cost_dir(src, &ss[ii[k]], dst, slot, &sd[jj[k]], N, topo, 0, &out[k])) return -1;
+    return n;
 }
 
 /* Backward table of one edge, consumer-major: out[j * ns + i]. */

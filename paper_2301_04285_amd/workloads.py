@@ -102,6 +102,27 @@ class Cluster:
         return self.nodes * self.devices_per_node
 
 
+@dataclass(frozen=True)
+class Topology:
+    """A hierarchy of link classes (an extension of the paper's two classes):
+    blocks of ``domains[c]`` consecutive device ranks, non-decreasing, the last
+    one all devices.  Class 0 links join the devices of one domains[0] block (a
+    node), class c >= 1 links join the domains[c-1] blocks of one domains[c]
+    block, at ``bw[c]`` bytes/s each."""
+    domains: Tuple[int, ...]
+    bw: Tuple[int, ...]
+
+    @property
+    def devices(self) -> int:
+        return self.domains[-1]
+
+    @staticmethod
+    def of(cluster: Cluster) -> "Topology":
+        """The paper's two classes: nodes of L devices inside the cluster."""
+        return Topology((cluster.devices_per_node, cluster.devices),
+                        (cluster.bw_intra, cluster.bw_inter))
+
+
 @dataclass
 class Workload:
     name: str
@@ -295,6 +316,15 @@ ALL_CONFIGS = (1, 2, 3, 4, 5)
 # Physical meshes of the configurations that name one (innermost dimension
 # first: the 8 devices of a node, then the node grid).
 CONFIG_MESHES = {4: (8, 4, 2), 5: (8, 4, 4)}
+
+
+# Three link classes for the configurations with a 3-D mesh: 8 devices of a
+# node (600 GB/s), 4 nodes of a group (the configuration's inter-node
+# bandwidth, 50 GB/s for the wide MLP), and the groups above them at a quarter
+# of that (a 4:1 oversubscribed tier).  The bandwidths of the upper tier are a
+# choice: the workload list names the meshes, not their links.
+CONFIG_TOPOLOGIES = {4: Topology((8, 32, 64), (600 * GB, 50 * GB, 12 * GB + GB // 2)),
+                     5: Topology((8, 32, 128), (600 * GB, 100 * GB, 25 * GB))}
 
 
 def physical_mesh(index: int, cluster: Cluster) -> Tuple[int, ...]:
