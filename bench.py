@@ -19,7 +19,9 @@ single-threaded and on all host cores, on the first layers of the same graph.
 result equal to the full evaluation;
 `bandwidth_sweep` builds the tables at four inter-node bandwidths in
 one pass (candidates costed once per entry, one selection and store per
-point); `value` and `roofline` always come from the full evaluation.
+point); `link_classes` builds them under three link classes (8-device nodes,
+4-node groups, the groups above them); `value` and `roofline` always come from
+the two-class full evaluation.
 `roofline.traffic` is the edge kernel's HBM bytes per launch from the
 committed rocprofv3 counter summary (null once the kernel sources differ from
 the ones the counters were taken with).
@@ -127,6 +129,10 @@ def main() -> int:
                     help="also time taps_edge_costs_sweep at this many inter-node bandwidths "
                          "(the wide-MLP workload's 12.5-100 GB/s points, the benchmark's cluster "
                          "last) and report it under bandwidth_sweep (0 = skip)")
+    ap.add_argument("--link-classes", type=int, default=1,
+                    help="also time the build under the workload's hierarchy of link classes "
+                         "(taps_node_costs_topology, taps_edge_costs_topology) and report it "
+                         "under link_classes (0 = skip)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES bytes (to scale HBM "
                          "traffic counters), then exit")
@@ -165,23 +171,28 @@ def main() -> int:
     strategies = int(tabs.op_offsets[-1])
     log(f"[bench] {strategies} strategies, {entries} edge entries")
 
-    def step(ev=None, shared=False, edge_out=None, points=None):
+    def step(ev=None, shared=False, edge_out=None, points=None, topology=None):
         offs, strat = taps.taps_enumerate_strategies(g, cl, stream=stream, out=tabs.strategies)
-        taps.taps_node_costs(g, cl, strat, offs, out=tabs.node, stream=stream)
+        if topology is None:
+            taps.taps_node_costs(g, cl, strat, offs, out=tabs.node, stream=stream)
+        else:
+            taps.taps_node_costs_topology(g, topology, strat, offs, out=tabs.node, stream=stream)
         if ev is not None:
             ev[0].record(stream)
             taps.taps_set_edge_kernel_events(ev[2], ev[3])
         if points:
             taps.taps_edge_costs_sweep(g, points, strat, offs, out=edge_out, stream=stream)
+        elif topology is not None:
+            taps.taps_edge_costs_topology(g, topology, strat, offs, out=edge_out, stream=stream)
         else:
             taps.taps_edge_costs(g, cl, strat, offs, out=edge_out or tabs.edge, stream=stream,
                                  shared=shared)
         if ev is not None:
             ev[1].record(stream)
 
-    def timed(shared=False, edge_out=None, points=None):
+    def timed(shared=False, edge_out=None, points=None, topology=None):
         for _ in range(args.warmup):
-            step(shared=shared, edge_out=edge_out, points=points)
+            step(shared=shared, edge_out=edge_out, points=points, topology=topology)
         torch.cuda.synchronize()
         # per step: the whole edge call, and the edge-table kernel alone (recorded by
         # the library on the same stream right around that launch)
@@ -193,7 +204,7 @@ def main() -> int:
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         for k in range(args.steps):
-            step(events[k], shared=shared, edge_out=edge_out, points=points)
+            step(events[k], shared=shared, edge_out=edge_out, points=points, topology=topology)
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
         edge_ms = float(np.mean([ev[0].elapsed_time(ev[1]) for ev in events]))
@@ -268,6 +279,19 @@ def main() -> int:
             "hbm_write_frac": k * bytes_per_launch / (w_kernel * 1e-3) / 1e9 / HBM_PEAK_GBPS,
             "equal_to_single_point": equal}
         del outs
+    if args.link_classes and args.config in W.CONFIG_TOPOLOGIES:
+        # the same build under a hierarchy of link classes (taps_*_costs_topology)
+        topo = W.CONFIG_TOPOLOGIES[args.config]
+        other = taps.alloc_table(entries, device="cuda")
+        h_step, h_edge, h_kernel = timed(edge_out=other, topology=topo)
+        log(f"[bench] link classes {topo.domains}: {h_step:.3f} ms/step, edge call {h_edge:.3f} ms, "
+            f"edge kernel {h_kernel:.3f} ms")
+        out["link_classes"] = {
+            "domains": list(topo.domains), "bw_GBps": [b / 1e9 for b in topo.bw],
+            "ms_per_step": h_step, "edge_call_ms": h_edge, "edge_kernel_ms": h_kernel,
+            "edge_entries_per_s": entries / (h_step * 1e-3),
+            "hbm_write_frac": bytes_per_launch / (h_kernel * 1e-3) / 1e9 / HBM_PEAK_GBPS}
+        del other
     if args.cpu_layers > 0 and args.config == 5:
         log(f"[bench] CPU oracle baseline on {args.cpu_layers} layers")
         out["cpu_baseline"] = cpu_baseline(w, cl, args.cpu_layers)

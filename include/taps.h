@@ -145,6 +145,20 @@ typedef struct {
     uint32_t dims[TAPS_MAX_LEVELS];
 } taps_mesh;
 
+/* A hierarchy of link classes, an extension of the paper's two (intra- and
+ * inter-node, Eq. 11-14): blocks of domain[0] <= domain[1] <= ... <=
+ * domain[n_classes - 1] = N consecutive device ranks (a node, a group of
+ * nodes, ...).  Class 0 links join the devices of one domain[0] block; class
+ * c >= 1 links join the domain[c-1] blocks of one domain[c] block, bw[c]
+ * bytes per second each.  The paper's cluster is {2, {L, N}, {B_intra,
+ * B_inter}}. */
+#define TAPS_MAX_CLASSES 4
+typedef struct {
+    uint32_t n_classes;                 /* 1 .. TAPS_MAX_CLASSES */
+    uint32_t domain[TAPS_MAX_CLASSES];  /* powers of two, non-decreasing, the last N */
+    uint64_t bw[TAPS_MAX_CLASSES];      /* bytes per second, > 0 */
+} taps_topology;
+
 /* Device arrays of one table, one element per record. */
 typedef struct {
     double *t;
@@ -248,6 +262,32 @@ taps_status taps_edge_costs_shared(const taps_graph *graph, const taps_cluster *
  *                 consumer strategy j.
  * Other arguments and errors as taps_edge_costs. */
 taps_status taps_edge_costs_backward(const taps_graph *graph, const taps_cluster *cluster,
+                                     const taps_strategy *strategies, const uint64_t *op_offsets,
+                                     uint64_t *edge_offsets, taps_table out, uint64_t capacity,
+                                     void *stream);
+
+/* The node and edge tables under a hierarchy of link classes (an extension
+ * of Eq. 11-14).  A collective belongs to the smallest block size that holds
+ * each of its groups (class c: the first domain[c] whose Algorithm 2 / 3
+ * inter-block count is zero); it pays bw[c] divided by ct, the number of its
+ * groups that share the uplink of one domain[c-1] block (Algorithm 2 / 3 and
+ * the AllToAll paragraph with "node" read as that block; an AllToAll's uplink
+ * carries k(p-k)/p of the shard per group, k = members in one block).  Fields:
+ * t = sum over classes of (link volume x ct) / (N bw[c]); intra = the class-0
+ * volume; inter = the sum over the other classes of link volume x ct; vol and
+ * meta as before ("inter-node" read as "leaving a domain[0] block").
+ * Candidates compare exactly by sum_c x_c lcm(bw) / bw[c].  With the domains
+ * (L, N) the tables equal those of taps_node_costs / taps_edge_costs.
+ *   topology  host; TAPS_ERR_TOPOLOGY unless n_classes is 1..TAPS_MAX_CLASSES,
+ *             every domain is a power of two, non-decreasing, the last one
+ *             N <= 2^TAPS_MAX_LEVELS, every bw > 0 and lcm(bw) / bw[c] < 2^30
+ *             for every c (bandwidths in round ratios).
+ *   strategies from taps_enumerate_strategies(_mesh) on N devices.
+ * Other arguments, layouts and errors as taps_node_costs / taps_edge_costs. */
+taps_status taps_node_costs_topology(const taps_graph *graph, const taps_topology *topology,
+                                     const taps_strategy *strategies, const uint64_t *op_offsets,
+                                     taps_table out, void *stream);
+taps_status taps_edge_costs_topology(const taps_graph *graph, const taps_topology *topology,
                                      const taps_strategy *strategies, const uint64_t *op_offsets,
                                      uint64_t *edge_offsets, taps_table out, uint64_t capacity,
                                      void *stream);

@@ -354,7 +354,7 @@ taps_status share_edges(const taps_graph *g, const uint64_t *op_offsets,
 taps_status edge_costs(const taps_graph *graph, const taps_cluster *clusters, uint32_t n_points,
                        const taps_strategy *strategies, const uint64_t *op_offsets,
                        uint64_t *edge_offsets, const taps_table *outs, uint64_t capacity,
-                       void *stream_, bool share, bool reverse) {
+                       void *stream_, bool share, bool reverse, const taps_hier *hier = nullptr) {
     g_last_error.clear();
     if (!clusters) return fail(TAPS_ERR_ARG, "cluster is NULL");
     if (n_points == 0 || n_points > TAPS_MAX_SWEEP)
@@ -475,7 +475,9 @@ taps_status edge_costs(const taps_graph *graph, const taps_cluster *clusters, ui
     const hipEvent_t before = g_kernel_before, after = g_kernel_after;
     g_kernel_before = g_kernel_after = nullptr;
     if (err == hipSuccess && before) err = hipEventRecord(before, stream);
-    if (err == hipSuccess && n_points == 1) {
+    if (err == hipSuccess && hier) {
+        err = taps_launch_edge_costs_h(d_params, d_segs, n_segs, d_desc, lp, *hier, outs[0], stream);
+    } else if (err == hipSuccess && n_points == 1) {
         err = taps_launch_edge_costs(d_params, d_segs, n_segs, d_desc, lp, outs[0], stream);
     } else if (err == hipSuccess) {
         taps_sweep sw;
@@ -496,6 +498,65 @@ taps_status edge_costs(const taps_graph *graph, const taps_cluster *clusters, ui
                                       at<uint64_t>(dev, ch[6]), outs[k], stream);
     if (err == hipSuccess && after) err = hipEventRecord(after, stream);
     if (err != hipSuccess) return hip_fail(err, "edge costs");
+    return TAPS_OK;
+}
+
+// A hierarchy of link classes: the per-level class and boundary tables and
+// the exact-order weights of the kernels, and a cluster with the same device
+// count and innermost block (for the per-edge set-up that the two models
+// share).
+taps_status check_topology(const taps_topology *t, taps_hier *H, taps_cluster *cl) {
+    if (!t) return fail(TAPS_ERR_ARG, "topology is NULL");
+    if (t->n_classes < 1 || t->n_classes > TAPS_MAX_CLASSES)
+        return fail(TAPS_ERR_TOPOLOGY, "%u link classes, 1 to %u allowed", t->n_classes,
+                    (unsigned)TAPS_MAX_CLASSES);
+    const uint32_t C = t->n_classes;
+    for (uint32_t c = 0; c < C; ++c) {
+        if (!pow2(t->domain[c]) || (c && t->domain[c] < t->domain[c - 1]))
+            return fail(TAPS_ERR_TOPOLOGY, "domain %u (%u devices) must be a power of two, "
+                        "not below the previous one", c, t->domain[c]);
+        if (t->bw[c] == 0) return fail(TAPS_ERR_TOPOLOGY, "bandwidth of class %u is zero", c);
+    }
+    const uint64_t N = t->domain[C - 1];
+    if (N > (1ull << TAPS_MAX_LEVELS))
+        return fail(TAPS_ERR_TOPOLOGY, "%llu devices exceed the limit of %u", (unsigned long long)N,
+                    1u << TAPS_MAX_LEVELS);
+    // exact-order weights lcm(bw) / bw[c], each below 2^30
+    unsigned __int128 lcm = 1;
+    for (uint32_t c = 0; c < C; ++c) {
+        const uint64_t g = std::gcd((uint64_t)(lcm % t->bw[c]), t->bw[c]);
+        const unsigned __int128 q = lcm / g;
+        if (q >> 64) return fail(TAPS_ERR_TOPOLOGY, "bandwidths not in round ratios");
+        lcm = q * t->bw[c];
+    }
+    std::memset(H, 0, sizeof(*H));
+    H->n_classes = C;
+    for (uint32_t c = 0; c < C; ++c) {
+        const unsigned __int128 w = lcm / t->bw[c];
+        if (w >> 30)
+            return fail(TAPS_ERR_TOPOLOGY, "bandwidths not in round ratios (lcm / bw[%u] >= 2^30)",
+                        c);
+        H->w[c] = (uint64_t)w;
+        H->inv_n_bw[c] = 1.0 / ((double)N * (double)t->bw[c]);
+    }
+    // class of a collective with top level l: the boundaries log2(domain[c]) <= l (c < C - 1);
+    // its ct counts the uplinks of a block of the largest of them
+    for (uint32_t l = 0; l < TAPS_MAX_LEVELS; ++l) {
+        uint32_t cls = 0, beta = 0;
+        for (uint32_t c = 0; c + 1 < C; ++c) {
+            const uint32_t b = log2u(t->domain[c]);
+            if (b <= l) {
+                ++cls;
+                beta = b;
+            }
+        }
+        H->cls_of_top |= cls << (4u * l);
+        H->beta_of_top |= beta << (4u * l);
+    }
+    cl->nodes = (uint32_t)(N / t->domain[0]);
+    cl->devices_per_node = t->domain[0];
+    cl->bw_intra = t->bw[0];
+    cl->bw_inter = t->bw[C - 1];
     return TAPS_OK;
 }
 
@@ -676,6 +737,53 @@ taps_status taps_node_costs(const taps_graph *graph, const taps_cluster *cluster
                                      d_desc, total, lp, out, stream);
     if (err != hipSuccess) return hip_fail(err, "node costs");
     return TAPS_OK;
+}
+
+taps_status taps_node_costs_topology(const taps_graph *graph, const taps_topology *topology,
+                                     const taps_strategy *strategies, const uint64_t *op_offsets,
+                                     taps_table out, void *stream_) {
+    g_last_error.clear();
+    taps_hier H;
+    taps_cluster cl;
+    taps_status st = check_topology(topology, &H, &cl);
+    if (st == TAPS_OK) st = check_graph(graph, false);
+    if (st == TAPS_OK) st = check_offsets(graph, op_offsets);
+    if (st != TAPS_OK) return st;
+    const uint32_t n_ops = graph->n_ops;
+    const uint64_t total = op_offsets[n_ops];
+    if (total == 0) return TAPS_OK;
+    if (!strategies) return fail(TAPS_ERR_ARG, "strategies is NULL");
+    if (!out.t || !out.vol || !out.intra || !out.inter || !out.meta)
+        return fail(TAPS_ERR_ARG, "a table array is NULL");
+    hipStream_t stream = (hipStream_t)stream_;
+    scratch sc(stream);
+    std::vector<chunk> ch{{graph->ops, sizeof(taps_op) * n_ops, 0},
+                          {op_offsets, sizeof(uint64_t) * (n_ops + 1), 0}};
+    void *dev = nullptr;
+    if ((st = upload(ch, &dev, stream)) != TAPS_OK) return st;
+    sc.adopt(dev);
+    taps_desc *d_desc = nullptr;
+    if ((st = sc.alloc((void **)&d_desc, sizeof(taps_desc) * total)) != TAPS_OK) return st;
+    hipError_t err = taps_launch_describe(strategies, total, d_desc, stream);
+    if (err == hipSuccess)
+        err = taps_launch_node_costs_h(at<taps_op>(dev, ch[0]), n_ops, at<uint64_t>(dev, ch[1]),
+                                       d_desc, total, log2u(topology->domain[H.n_classes - 1]), H,
+                                       out, stream);
+    if (err != hipSuccess) return hip_fail(err, "node costs");
+    return TAPS_OK;
+}
+
+taps_status taps_edge_costs_topology(const taps_graph *graph, const taps_topology *topology,
+                                     const taps_strategy *strategies, const uint64_t *op_offsets,
+                                     uint64_t *edge_offsets, taps_table out, uint64_t capacity,
+                                     void *stream) {
+    g_last_error.clear();
+    taps_hier H;
+    taps_cluster cl;
+    const taps_status st = check_topology(topology, &H, &cl);
+    if (st != TAPS_OK) return st;
+    return edge_costs(graph, &cl, 1, strategies, op_offsets, edge_offsets, &out, capacity, stream,
+                      false, false, &H);
 }
 
 taps_status taps_memory_costs(const taps_graph *graph, const taps_strategy *strategies,

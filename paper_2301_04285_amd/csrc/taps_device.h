@@ -31,6 +31,7 @@
 #define TAPS_D_MAX_RANK 8
 #define TAPS_D_MAX_LEVELS 8
 #define TAPS_D_NONE 0xFFu
+#define TAPS_D_MAX_CLASSES 4
 
 // A strategy on binary levels: per op axis the lowest level of its run and
 // the run's width (0 = not split), 4 bits each; per level the op axis that
@@ -489,11 +490,28 @@ __host__ __device__ inline bool taps_hopeless(const taps_fac &c, const taps_limi
     return lim.on && c.vol >= lim.vol && taps_key64(c, K) >= lim.key;
 }
 
-struct taps_run {
-    taps_fac c;
+template <class Fac>
+struct taps_run_t {
+    Fac c;
     uint32_t n_a2a;   // AllToAlls issued
     bool ok;          // false if the loop did not settle (cannot happen)
     bool stopped;     // stopped early: cannot beat the limit it was given
+};
+using taps_run = taps_run_t<taps_fac>;
+
+// The paper's two link classes (Eq. 11-14 with Algorithm 3): the cost of one
+// AllGather and of the AllToAlls of one closure, and the early stop of a later
+// candidate.  Algorithm 1 and "rearrange" below are written over such a model.
+struct taps_two_class {
+    using fac = taps_fac;
+    uint32_t lam;
+    const taps_keys *K;
+    const taps_limit *lim;
+    __host__ __device__ void gather(fac &c, uint32_t top, const taps_ax &a, uint32_t e,
+                                    uint32_t unused) const;
+    __host__ __device__ void a2a(fac &c, uint32_t x, const taps_lv &L, uint32_t e,
+                                 uint32_t unused) const;
+    __host__ __device__ bool hopeless(const fac &c) const;
 };
 
 // Running state of one sequence: axes held at their producer position (ats)
@@ -503,10 +521,25 @@ struct taps_state {
     uint32_t ats, atd, blk, unused, e;
 };
 
-__host__ __device__ inline void taps_gather(const taps_row &P, const taps_lv &L, taps_state &s,
-                                            taps_fac &c, uint32_t top) {
+__host__ __device__ inline void taps_two_class::gather(fac &c, uint32_t top, const taps_ax &a,
+                                                      uint32_t e, uint32_t unused) const {
+    taps_cost(c, top, a, lam, e, unused);
+}
+
+__host__ __device__ inline void taps_two_class::a2a(fac &c, uint32_t x, const taps_lv &L,
+                                                   uint32_t e, uint32_t unused) const {
+    taps_a2a_batch(c, x, L, lam, e, unused);
+}
+
+__host__ __device__ inline bool taps_two_class::hopeless(const fac &c) const {
+    return taps_hopeless(c, *lim, *K);
+}
+
+template <class Cm>
+__host__ __device__ inline void taps_gather(const taps_lv &L, taps_state &s, typename Cm::fac &c,
+                                            uint32_t top, const Cm &M) {
     const taps_ax a = taps_axis(L, top);
-    taps_cost(c, top, a, P.lam, s.e, s.unused);
+    M.gather(c, top, a, s.e, s.unused);
     s.ats &= ~(1u << top);
     s.unused |= a.lv;
     s.e += a.w;
@@ -539,9 +572,12 @@ __host__ __device__ inline uint32_t taps_slice(const taps_lv &L, taps_state &s) 
 //   * once no axis is held at a producer position only slices remain (no
 //     held axis blocks a target), and slices cost nothing: the sequence's
 //     cost is final there.
-__host__ __device__ inline taps_run taps_alg1(const taps_row &P, const taps_col &Q,
-                                              const taps_lv &L) {
-    taps_fac c;
+template <class Cm>
+__host__ __device__ inline taps_run_t<typename Cm::fac> taps_alg1_t(const taps_row &P,
+                                                                    const taps_col &Q,
+                                                                    const taps_lv &L,
+                                                                    const Cm &M) {
+    typename Cm::fac c;
     taps_fac_zero(c);
     taps_state s;
     s.ats = L.src & ~L.home;
@@ -568,7 +604,7 @@ __host__ __device__ inline taps_run taps_alg1(const taps_row &P, const taps_col 
         if (moved) {
             s.atd |= moved;
             n_a2a += taps_popc(moved);
-            taps_a2a_batch(c, moved, L, P.lam, s.e, s.unused);
+            M.a2a(c, moved, L, s.e, s.unused);
         }
         if (sl) taps_slice(L, s);
         // nothing held at a producer position: only slices remain, and they cost nothing
@@ -581,21 +617,27 @@ __host__ __device__ inline taps_run taps_alg1(const taps_row &P, const taps_col 
             while (x) {
                 const uint32_t top = taps_rank_level(P, taps_ctz(x));
                 x &= x - 1u;
-                taps_gather(P, L, s, c, top);
+                taps_gather(L, s, c, top, M);
             }
         } else {
             const uint32_t top = taps_first_src(P, s.ats);
             s.blk &= ~taps_blocked(P, Q, L, 1u << top);
-            taps_gather(P, L, s, c, top);
+            taps_gather(L, s, c, top, M);
         }
         if (s.ats == 0) break;
     }
-    taps_run r;
+    taps_run_t<typename Cm::fac> r;
     r.c = c;
     r.n_a2a = n_a2a;
     r.ok = ok;
     r.stopped = false;
     return r;
+}
+
+__host__ __device__ inline taps_run taps_alg1(const taps_row &P, const taps_col &Q,
+                                              const taps_lv &L) {
+    const taps_two_class M{P.lam, nullptr, nullptr};
+    return taps_alg1_t(P, Q, L, M);
 }
 
 // Algorithm 1 without AllToAll ("rearrange" in Table 2).  Without AllToAll
@@ -613,10 +655,12 @@ __host__ __device__ inline taps_run taps_alg1(const taps_row &P, const taps_col 
 // Step 2 is step 3 on positions no consumer axis targets (nothing is freed
 // for anyone there), so both run as one loop over the held axes: the
 // untargeted ones in producer order, then the targeted ones.
-__host__ __device__ inline taps_run taps_rearrange(const taps_row &P, const taps_col &Q,
-                                                   const taps_lv &L, const taps_limit &lim,
-                                                   const taps_keys &K) {
-    taps_fac c;
+template <class Cm>
+__host__ __device__ inline taps_run_t<typename Cm::fac> taps_rearrange_t(const taps_row &P,
+                                                                         const taps_col &Q,
+                                                                         const taps_lv &L,
+                                                                         const Cm &M) {
+    typename Cm::fac c;
     taps_fac_zero(c);
     taps_state s;
     s.ats = L.src & ~L.home;
@@ -630,7 +674,7 @@ __host__ __device__ inline taps_run taps_rearrange(const taps_row &P, const taps
     uint32_t x = (uint32_t)P.to_rank[s.ats & ~L.tgtsrc] |
                  ((uint32_t)P.to_rank[s.ats & L.tgtsrc] << 8);
     while (x) {
-        if (taps_hopeless(c, lim, K)) {
+        if (M.hopeless(c)) {
             stopped = true;
             break;
         }
@@ -638,7 +682,7 @@ __host__ __device__ inline taps_run taps_rearrange(const taps_row &P, const taps
         x &= x - 1u;
         const uint32_t b = 1u << top;
         const taps_ax a = taps_axis(L, top);
-        taps_cost(c, top, a, P.lam, s.e, s.unused);
+        M.gather(c, top, a, s.e, s.unused);
         const uint32_t freed_for = taps_blocked(P, Q, L, b);   // the axis targeting that position
         s.ats &= ~b;
         s.blk &= ~freed_for;
@@ -656,12 +700,19 @@ __host__ __device__ inline taps_run taps_rearrange(const taps_row &P, const taps
             s.e -= taps_popc(lv);
         }
     }
-    taps_run r;
+    taps_run_t<typename Cm::fac> r;
     r.c = c;
     r.n_a2a = 0;
     r.ok = true;
     r.stopped = stopped;
     return r;
+}
+
+__host__ __device__ inline taps_run taps_rearrange(const taps_row &P, const taps_col &Q,
+                                                   const taps_lv &L, const taps_limit &lim,
+                                                   const taps_keys &K) {
+    const taps_two_class M{P.lam, &K, &lim};
+    return taps_rearrange_t(P, Q, L, M);
 }
 
 // "remove" (Table 2): gather every held axis not at its target, lowest
@@ -972,4 +1023,217 @@ __host__ __device__ inline void taps_make_col(taps_col &Q, const taps_desc &D, u
         Q.chi[d] = lo + w;
         Q.cr[d] = taps_levels(lo, w);
     }
+}
+
+// ---------------------------------------------------------------------------
+// Link-class hierarchies (an extension of the paper's two classes).
+//
+// Blocks of 2^beta_0 <= 2^beta_1 <= ... consecutive ranks (a node, a group of
+// nodes, ...; the last class spans all devices).  A collective belongs to
+// the smallest block that holds each of its groups: with top level t that is
+// class c = the number of boundaries beta <= t; it pays bw[c] divided by the
+// number of groups sharing the uplink of one block of the largest boundary
+// beta <= t (Algorithm 2 / 3 and the AllToAll paragraph with "node" read as
+// that block).  With one boundary (beta = lam) this is the two-class model.
+// Every collective is costed on its own (no closed forms over the node
+// boundary); volumes are the same factor units as above, accumulated per
+// class, and candidates compare by the exact key sum_c x_c w_c with
+// w_c = lcm(bw) / bw_c.
+// ---------------------------------------------------------------------------
+struct taps_hier {
+    uint32_t n_classes;     // 1 .. TAPS_D_MAX_CLASSES
+    uint32_t cls_of_top;    // nibble t: class of a collective whose top level is t
+    uint32_t beta_of_top;   // nibble t: the largest boundary <= t (0 for class 0)
+    uint32_t pad;
+    uint64_t w[TAPS_D_MAX_CLASSES];        // exact-order weights, each below 2^30
+    double inv_n_bw[TAPS_D_MAX_CLASSES];   // 1 / (N bw[c])
+};
+
+// One candidate in factor units, per link class (x0: inside the innermost block).
+struct taps_fach {
+    uint32_t vol, x0, x1, x2, x3;
+    uint32_t counts;   // collectives | inter-block collectives << 8 | sum of ct << 16
+};
+
+__host__ __device__ inline void taps_fac_zero(taps_fach &c) {
+    c.vol = c.x0 = c.x1 = c.x2 = c.x3 = 0;
+    c.counts = 0;
+}
+
+// x_cls += v (selects, no indexed register arrays)
+__host__ __device__ inline void taps_fach_add(taps_fach &c, uint32_t cls, uint32_t v) {
+    c.x0 += cls == 0 ? v : 0u;
+    c.x1 += cls == 1 ? v : 0u;
+    c.x2 += cls == 2 ? v : 0u;
+    c.x3 += cls == 3 ? v : 0u;
+}
+
+__host__ __device__ inline uint64_t taps_fach_key(const taps_fach &c, const taps_hier &H) {
+    return (uint64_t)c.x0 * H.w[0] + (uint64_t)c.x1 * H.w[1] + (uint64_t)c.x2 * H.w[2] +
+           (uint64_t)c.x3 * H.w[3];
+}
+
+// The shared uplinks of a collective of width w at lowest level lo whose
+// class is cls under the boundary beta: 2^lct groups, with the free levels
+// below min(lo, beta) letting replicas share one transfer (Algorithm 3).
+__host__ __device__ inline uint32_t taps_hier_lct(uint32_t lo, uint32_t beta, uint32_t unused) {
+    const uint32_t m = lo < beta ? lo : beta;
+    return m - taps_popc(unused & taps_below(m));
+}
+
+struct taps_hier_model {
+    using fac = taps_fach;
+    const taps_hier *H;
+    uint64_t lim_key;   // a later candidate stops once its key and volume reach these
+    uint32_t lim_vol;
+    bool lim_on;
+
+    // AllGather (Eq. 9) of the axis with top level `top`.
+    __host__ __device__ void gather(fac &c, uint32_t top, const taps_ax &a, uint32_t e,
+                                    uint32_t unused) const {
+        const uint32_t V = ((1u << a.w) - 1u) << (e + 8u);
+        const uint32_t cls = taps_nib(H->cls_of_top, top);
+        const uint32_t lct = cls ? taps_hier_lct(a.lo, taps_nib(H->beta_of_top, top), unused) : 0u;
+        c.vol += V;
+        taps_fach_add(c, cls, V << lct);
+        c.counts += cls ? 0x101u + ((1u << lct) << 16) : 1u;
+    }
+
+    // AllToAlls (Eq. 10, Eq. 14) of every axis whose top is in x, at one state:
+    // k = 2^kap members of a group inside one block of the boundary beta, the
+    // uplink carries k (p - k) / p of the shard per group.
+    __host__ __device__ void a2a(fac &c, uint32_t x, const taps_lv &L, uint32_t e,
+                                 uint32_t unused) const {
+        const uint32_t sh = e + 8u;
+        for (uint32_t m = x; m; m &= m - 1u) {
+            const uint32_t top = taps_ctz(m);
+            const taps_ax a = taps_axis(L, top);
+            const uint32_t V = (1u << sh) - (1u << (sh - a.w));
+            const uint32_t cls = taps_nib(H->cls_of_top, top);
+            c.vol += V;
+            if (!cls) {
+                c.x0 += V;
+                c.counts += 1u;
+                continue;
+            }
+            const uint32_t beta = taps_nib(H->beta_of_top, top);
+            const uint32_t kap = beta > a.lo ? beta - a.lo : 0u;
+            const uint32_t link = ((1u << a.w) - (1u << kap)) << (kap + sh - a.w);
+            const uint32_t lct = taps_hier_lct(a.lo, beta, unused);
+            taps_fach_add(c, cls, link << lct);
+            c.counts += 0x101u + ((1u << lct) << 16);
+        }
+    }
+
+    __host__ __device__ bool hopeless(const fac &c) const {
+        return lim_on && c.vol >= lim_vol && taps_fach_key(c, *H) >= lim_key;
+    }
+};
+
+// "remove" (Table 2): every held axis not at its target gathered in producer
+// order (dimensions ascending, each from its top level down), one by one.
+__host__ __device__ inline taps_fach taps_remove_h(const taps_row &P, const taps_lv &L,
+                                                   const taps_hier_model &M) {
+    taps_fach c;
+    taps_fac_zero(c);
+    uint32_t e = P.e0, unused = P.full & ~P.pru;
+    for (uint32_t x = P.to_rank[L.src & ~L.home]; x; x &= x - 1u) {
+        const uint32_t top = taps_rank_level(P, taps_ctz(x));
+        const taps_ax a = taps_axis(L, top);
+        M.gather(c, top, a, e, unused);
+        unused |= a.lv;
+        e += a.w;
+    }
+    return c;
+}
+
+struct taps_pickh {
+    taps_fach best;
+    uint32_t vmin, cand;
+    bool ok;
+};
+
+// The cheapest of Algorithm 1, the same without AllToAll, and "remove" under
+// the link classes of H (ties to the lower index); vmin the smallest volume.
+__host__ __device__ inline taps_pickh taps_edge_select_h(const taps_row &P, const taps_col &Q,
+                                                         const taps_hier &H) {
+    taps_lv L;
+    taps_unify(P, Q, L);
+    taps_hier_model M{&H, 0, 0, false};
+    const taps_run_t<taps_fach> r0 = taps_alg1_t(P, Q, L, M);
+    taps_pickh k;
+    k.best = r0.c;
+    k.cand = 0;
+    k.vmin = r0.c.vol;
+    k.ok = r0.ok;
+    uint64_t best_key = taps_fach_key(r0.c, H);
+    if (r0.n_a2a) {   // without AllToAll the sequence would be the same
+        M.lim_on = true;
+        M.lim_key = best_key;
+        M.lim_vol = k.vmin;
+        const taps_run_t<taps_fach> r1 = taps_rearrange_t(P, Q, L, M);
+        if (!r1.stopped) {
+            const uint64_t k1 = taps_fach_key(r1.c, H);
+            if (k1 < best_key) {
+                k.best = r1.c;
+                k.cand = 1;
+                best_key = k1;
+            }
+            k.vmin = r1.c.vol < k.vmin ? r1.c.vol : k.vmin;
+        }
+        M.lim_on = false;
+    }
+    const taps_fach c2 = taps_remove_h(P, L, M);
+    if (taps_fach_key(c2, H) < best_key) {
+        k.best = c2;
+        k.cand = 2;
+    }
+    k.vmin = c2.vol < k.vmin ? c2.vol : k.vmin;
+    return k;
+}
+
+__host__ __device__ inline taps_entry_out taps_entry_finish_h(const taps_pickh &k,
+                                                              const taps_scaler &S,
+                                                              const taps_hier &H) {
+    taps_entry_out o;
+    const double unit = (double)S.tbytes * (1.0 / 256.0);
+    o.vol = taps_scale(S, k.vmin);
+    o.intra = taps_scale(S, k.best.x0);
+    o.inter = taps_scale(S, k.best.x1) + taps_scale(S, k.best.x2) + taps_scale(S, k.best.x3);
+    o.t = (double)k.best.x0 * (unit * H.inv_n_bw[0]) + (double)k.best.x1 * (unit * H.inv_n_bw[1]) +
+          (double)k.best.x2 * (unit * H.inv_n_bw[2]) + (double)k.best.x3 * (unit * H.inv_n_bw[3]);
+    const uint32_t n = k.best.counts;
+    o.meta = k.cand | ((n & 0xFFu) << 2) | (((n >> 8) & 0xFFu) << 7) | ((n >> 16) << 12);
+    o.ok = k.ok;
+    return o;
+}
+
+// Intra-op AllReduce (Eq. 5-8) of a tensor missing the levels `missing`,
+// under link classes: nb volumes per class.
+struct taps_acch {
+    uint64_t vol, x0, x1, x2, x3;
+    uint32_t n_coll, n_inter, sum_ct;
+};
+
+__host__ __device__ inline void taps_allreduce_h(taps_acch &c, uint32_t missing, uint64_t bytes,
+                                                 const taps_hier &H) {
+    if (!missing) return;
+    const uint32_t lg = taps_popc(missing);
+    const uint64_t V = ((bytes << lg) - bytes) << 1;   // 2 (g - 1) |tensor| bytes, in nb
+    const uint32_t top = taps_msb(missing);
+    const uint32_t cls = taps_nib(H.cls_of_top, top);
+    c.vol += V;
+    c.n_coll += 1;
+    if (!cls) {
+        c.x0 += V;
+        return;
+    }
+    const uint32_t beta = taps_nib(H.beta_of_top, top);
+    const uint32_t lct = beta - taps_popc(missing & taps_below(beta));
+    const uint64_t X = V << lct;
+    c.x1 += cls == 1 ? X : 0u;
+    c.x2 += cls == 2 ? X : 0u;
+    c.x3 += cls == 3 ? X : 0u;
+    c.n_inter += 1;
+    c.sum_ct += 1u << lct;
 }

@@ -102,6 +102,13 @@ hipError_t taps_launch_edge_costs_sweep(const taps_edge_params *params, const ta
                                         uint64_t n_rows, const taps_desc *desc,
                                         const taps_launch &lp, const taps_sweep &sw,
                                         hipStream_t stream);
+// Link-class hierarchies: the edge and node tables under the classes of H.
+hipError_t taps_launch_edge_costs_h(const taps_edge_params *params, const taps_row_ref *rows,
+                                    uint64_t n_rows, const taps_desc *desc, const taps_launch &lp,
+                                    const taps_hier &H, taps_table out, hipStream_t stream);
+hipError_t taps_launch_node_costs_h(const taps_op *ops, uint32_t n_ops, const uint64_t *offsets,
+                                    const taps_desc *desc, uint64_t total, uint32_t n,
+                                    const taps_hier &H, taps_table out, hipStream_t stream);
 hipError_t taps_launch_copy_tables(const taps_copy_task *tasks, uint32_t n_tasks,
                                    const uint64_t *dst_list, taps_table out, hipStream_t stream);
 // For each pair p: flags[p] = 0 if strategies[first_a .. +count) equals

@@ -422,6 +422,73 @@ __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_co
     }
 }
 
+// Link-class hierarchies: as k_edge_costs, each entry selected and scaled
+// under the classes of H.
+__global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_costs_h(
+    const taps_edge_params *__restrict__ params, const taps_row_ref *__restrict__ rows,
+    uint32_t n_segs, const taps_desc *__restrict__ desc, taps_launch lp, taps_hier H,
+    taps_table out) {
+    __shared__ uint8_t rank_tab[TAPS_ROWS_PER_BLOCK][256];
+    const uint32_t lane = threadIdx.x % TAPS_TILE_COLS;
+    const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x / TAPS_TILE_COLS);
+    const uint32_t r = blockIdx.x * TAPS_ROWS_PER_BLOCK + wave;
+    const bool live = r < n_segs;
+    const taps_row_ref ref = rows[live ? r : 0u];
+    const taps_edge_params E = params[ref.edge];
+    const taps_desc Dp = desc[ref.strategy];
+    const uint32_t i = ref.strategy - E.src_base;
+    taps_row P;
+    taps_make_row(P, Dp, E.paxes, E.rank, lp.n, lp.lam);
+    taps_fill_rank_table(P, rank_tab[wave], lane, TAPS_TILE_COLS);
+    __syncthreads();
+    if (!live) return;
+    P.to_rank = rank_tab[wave];
+    const uint64_t row_out = E.out_offset + (uint64_t)i * E.nd;
+    const taps_desc *col = desc + E.dst_base;
+    const uint32_t c0 = ref.first_col;
+    const uint32_t c1 = E.nd - c0 < TAPS_TILE_COLS * TAPS_SEG_TILES ? E.nd
+                                                                       : c0 + TAPS_TILE_COLS * TAPS_SEG_TILES;
+    for (uint32_t j = c0 + lane; j < c1; j += TAPS_TILE_COLS) {
+        taps_col Q;
+        taps_make_col(Q, col[j], E.caxes, E.rank);
+        const taps_entry_out o = taps_entry_finish_h(taps_edge_select_h(P, Q, H), E.scale, H);
+        store_entry(out, row_out, j, o, o.ok ? o.meta : 0xFFFFFFFFu);
+    }
+}
+
+__global__ __launch_bounds__(256) void k_node_costs_h(const taps_op *__restrict__ ops,
+                                                      uint32_t n_ops,
+                                                      const uint64_t *__restrict__ offsets,
+                                                      const taps_desc *__restrict__ desc,
+                                                      uint64_t total, uint32_t n, taps_hier H,
+                                                      taps_table out) {
+    const uint64_t idx = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= total) return;
+    const taps_op &op = ops[find_owner(offsets, n_ops, idx)];
+    const taps_desc D = desc[idx];
+    const uint32_t full = taps_low_mask(n);
+    taps_acch c = {0, 0, 0, 0, 0, 0, 0, 0};
+    auto tensor = [&](const taps_tensor &t) {
+        uint32_t used = 0;
+        uint64_t bytes = op.dtype_bytes;
+        for (uint32_t d = 0; d < t.rank && d < TAPS_MAX_RANK; ++d) {
+            const uint32_t a = t.axis[d] & 7u;
+            used |= taps_levels(taps_nib(D.lo, a), taps_nib(D.width, a));
+            bytes *= (uint64_t)op.axis_len[a];
+        }
+        taps_allreduce_h(c, full & ~used, bytes, H);
+    };
+    tensor(op.out);
+    for (uint32_t k = 0; k < op.n_in && k < TAPS_MAX_INPUTS; ++k) tensor(op.in[k]);
+    for (uint32_t k = 0; k < op.n_w && k < TAPS_MAX_WEIGHTS; ++k) tensor(op.w[k]);
+    out.t[idx] = (double)c.x0 * H.inv_n_bw[0] + (double)c.x1 * H.inv_n_bw[1] +
+                 (double)c.x2 * H.inv_n_bw[2] + (double)c.x3 * H.inv_n_bw[3];
+    out.vol[idx] = c.vol;
+    out.intra[idx] = c.x0;
+    out.inter[idx] = c.x1 + c.x2 + c.x3;
+    out.meta[idx] = (c.n_coll << 2) | (c.n_inter << 7) | (c.sum_ct << 12);
+}
+
 // Shared tables: each task holds `count` (<= TAPS_COPY_CHUNK) consecutive
 // entries of a computed table, staged once in LDS and stored into every table
 // that shares it, at the same offset; blockIdx.y picks the array.  The tables
@@ -570,6 +637,25 @@ hipError_t taps_launch_edge_costs_sweep(const taps_edge_params *params, const ta
     hipLaunchKernelGGL(k_edge_costs_sweep, dim3(blocks_for(n_segs, TAPS_ROWS_PER_BLOCK)),
                        dim3(TAPS_TILE_COLS * TAPS_ROWS_PER_BLOCK), 0, stream, params, segs,
                        (uint32_t)n_segs, desc, lp, sw);
+    return hipGetLastError();
+}
+
+hipError_t taps_launch_edge_costs_h(const taps_edge_params *params, const taps_row_ref *rows,
+                                    uint64_t n_rows, const taps_desc *desc, const taps_launch &lp,
+                                    const taps_hier &H, taps_table out, hipStream_t stream) {
+    if (n_rows == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_edge_costs_h, dim3(blocks_for(n_rows, TAPS_ROWS_PER_BLOCK)),
+                       dim3(TAPS_TILE_COLS * TAPS_ROWS_PER_BLOCK), 0, stream, params, rows,
+                       (uint32_t)n_rows, desc, lp, H, out);
+    return hipGetLastError();
+}
+
+hipError_t taps_launch_node_costs_h(const taps_op *ops, uint32_t n_ops, const uint64_t *offsets,
+                                    const taps_desc *desc, uint64_t total, uint32_t n,
+                                    const taps_hier &H, taps_table out, hipStream_t stream) {
+    if (total == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_node_costs_h, dim3(blocks_for(total, 256)), dim3(256), 0, stream, ops,
+                       n_ops, offsets, desc, total, n, H, out);
     return hipGetLastError();
 }
 

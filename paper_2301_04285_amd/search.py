@@ -35,7 +35,8 @@ from typing import Dict, List, Optional, Sequence
 
 import numpy as np
 
-__all__ = ["Plan", "solve", "plan_cost", "compare", "compare_mesh", "host_tables"]
+__all__ = ["Plan", "solve", "plan_cost", "compare", "compare_mesh", "compare_topology",
+           "host_tables"]
 
 
 @dataclass
@@ -264,6 +265,30 @@ def compare_mesh(graph, cluster, mesh, time_limit: float = 600.0, device="cuda")
     return out
 
 
+def compare_topology(graph, cluster, topology, time_limit: float = 600.0, device="cuda") -> Dict:
+    """Searching with the link classes of ``topology`` against searching with the
+    cluster's two classes and against the volume-based search, every plan priced
+    with the topology's time."""
+    import torch
+    from . import taps
+    h = taps.build_tables(graph, cluster, device=device, topology=topology)
+    torch.cuda.synchronize()
+    nh, eh = host_tables(graph, h, "t")
+    del h
+    two = taps.build_tables(graph, cluster, device=device)
+    torch.cuda.synchronize()
+    n2, e2 = host_tables(graph, two, "t")
+    nv, ev = host_tables(graph, two, "vol")
+    del two
+    plans = {"classes": solve(graph, nh, eh, time_limit), "two_classes": solve(graph, n2, e2, time_limit),
+             "volume": solve(graph, nv, ev, time_limit)}
+    t = {k: plan_cost(graph, nh, eh, p.choice) for k, p in plans.items()}
+    return {"domains": list(topology.domains), "bw_GBps": [b / 1e9 for b in topology.bw],
+            "t_s": t, "reduction_vs_two_classes": 1.0 - t["classes"] / t["two_classes"],
+            "reduction_vs_volume": 1.0 - t["classes"] / t["volume"],
+            "solve_s": {k: p.solve_s for k, p in plans.items()}}
+
+
 def experiment_workloads():
     """(name, graph, cluster) of every comparison: the five configurations (the
     transformer ones cut to one layer, as the paper searches one layer of a stack of
@@ -303,6 +328,10 @@ def main() -> int:
     ap.add_argument("--mesh-space", action="store_true",
                     help="instead: TAPS over every device matrix against TAPS over the strategies "
                          "of the workload's fixed physical mesh (taps_enumerate_strategies_mesh)")
+    ap.add_argument("--link-classes", action="store_true",
+                    help="instead: on the workloads with a three-level mesh, search with its link "
+                         "classes against searching with two classes and by volume, all plans "
+                         "priced with the link classes")
     ap.add_argument("--memory-budget-gb", type=float, default=0.0,
                     help="device-memory constraint (Eq. 18) in GB: the chosen strategies' weight "
                          "and output shards per device (taps_memory_costs) must fit (0 = none)")
@@ -328,6 +357,16 @@ def main() -> int:
             continue
         if args.mesh_space:
             r = compare_mesh(g, cl, mesh, args.time_limit)
+            print(json.dumps({"workload": name, **r}), flush=True)
+            continue
+        if args.link_classes:
+            from . import workloads as W
+            topo = next((t for t in W.CONFIG_TOPOLOGIES.values() if t.devices == cl.devices and
+                         t.domains[0] == cl.devices_per_node), None)
+            if topo is None or len(mesh) < 3:
+                continue
+            topo = W.Topology(topo.domains, (cl.bw_intra, cl.bw_inter, cl.bw_inter // 4))
+            r = compare_topology(g, cl, topo, args.time_limit)
             print(json.dumps({"workload": name, **r}), flush=True)
             continue
         tabs = taps.build_tables(g, cl)

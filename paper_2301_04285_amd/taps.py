@@ -45,6 +45,14 @@ class Mesh(C.Structure):
     _fields_ = [("n_dims", C.c_uint32), ("dims", C.c_uint32 * MAX_LEVELS)]
 
 
+MAX_CLASSES = 4
+
+
+class TopologyS(C.Structure):
+    _fields_ = [("n_classes", C.c_uint32), ("domain", C.c_uint32 * MAX_CLASSES),
+                ("bw", C.c_uint64 * MAX_CLASSES)]
+
+
 class Tensor(C.Structure):
     _fields_ = [("rank", C.c_uint8), ("axis", C.c_uint8 * MAX_RANK)]
 
@@ -90,6 +98,12 @@ def load():
         L.taps_enumerate_strategies_mesh.restype = C.c_int
         L.taps_enumerate_strategies_mesh.argtypes = [P(GraphS), P(Cluster), P(Mesh), P(C.c_uint64),
                                                      C.c_void_p, C.c_uint64, C.c_void_p]
+        L.taps_node_costs_topology.restype = C.c_int
+        L.taps_node_costs_topology.argtypes = [P(GraphS), P(TopologyS), C.c_void_p, P(C.c_uint64),
+                                               Table, C.c_void_p]
+        L.taps_edge_costs_topology.restype = C.c_int
+        L.taps_edge_costs_topology.argtypes = [P(GraphS), P(TopologyS), C.c_void_p, P(C.c_uint64),
+                                               P(C.c_uint64), Table, C.c_uint64, C.c_void_p]
         L.taps_node_costs.restype = C.c_int
         L.taps_node_costs.argtypes = [P(GraphS), P(Cluster), C.c_void_p, P(C.c_uint64), Table,
                                       C.c_void_p]
@@ -285,6 +299,54 @@ def taps_node_costs(graph, cluster, strategies, op_offsets, out=None, stream=Non
     return {k: v[:total] for k, v in out.items()}
 
 
+def pack_topology(topo) -> TopologyS:
+    """workloads.Topology (block sizes and bandwidths per link class) -> the ABI struct."""
+    if not 1 <= len(topo.domains) == len(topo.bw) <= MAX_CLASSES:
+        raise ValueError(f"1 to {MAX_CLASSES} link classes, one bandwidth each")
+    return TopologyS(len(topo.domains), (C.c_uint32 * MAX_CLASSES)(*topo.domains),
+                     (C.c_uint64 * MAX_CLASSES)(*topo.bw))
+
+
+def taps_node_costs_topology(graph, topology, strategies, op_offsets, out=None, stream=None):
+    """Node table under a hierarchy of link classes (taps_node_costs_topology)."""
+    g = _graph(graph)
+    tp = pack_topology(topology)
+    offs = np.ascontiguousarray(op_offsets, dtype=np.uint64)
+    total = int(offs[-1])
+    if out is None:
+        out = alloc_table(total, device=strategies.device)
+    st = load().taps_node_costs_topology(C.byref(g.struct), C.byref(tp),
+                                         C.c_void_p(strategies.data_ptr()), _u64_array(offs),
+                                         _table(out), _stream(stream))
+    _check(st, "taps_node_costs_topology")
+    return {k: v[:total] for k, v in out.items()}
+
+
+def taps_edge_costs_topology(graph, topology, strategies, op_offsets, out=None, stream=None,
+                             size_only=False):
+    """Edge tables under a hierarchy of link classes (taps_edge_costs_topology):
+    (edge_offsets, dict of device tensors or None for a size query)."""
+    g = _graph(graph)
+    tp = pack_topology(topology)
+    offs = np.ascontiguousarray(op_offsets, dtype=np.uint64)
+    eoffs = np.zeros(g.n_edges + 1, dtype=np.uint64)
+    L = load()
+    sptr = C.c_void_p(strategies.data_ptr()) if strategies is not None else None
+    if out is None or size_only:
+        st = L.taps_edge_costs_topology(C.byref(g.struct), C.byref(tp), sptr, _u64_array(offs),
+                                        _u64_array(eoffs), _table(None), 0, _stream(stream))
+        _check(st, "taps_edge_costs_topology")
+        if size_only:
+            return eoffs, None
+        out = alloc_table(int(eoffs[-1]), device=strategies.device)
+    cap = min(int(v.numel()) for v in out.values())
+    st = L.taps_edge_costs_topology(C.byref(g.struct), C.byref(tp), sptr, _u64_array(offs),
+                                    _u64_array(eoffs), _table(out), cap, _stream(stream))
+    _check(st, "taps_edge_costs_topology")
+    total = int(eoffs[-1])
+    return eoffs, {k: v[:total] for k, v in out.items()}
+
+
 def taps_edge_costs(graph, cluster, strategies, op_offsets, out=None, stream=None,
                     size_only=False, shared=False, backward=False):
     """(edge_offsets numpy uint64 [n_edges+1], edge table dict of device
@@ -424,16 +486,25 @@ def _torch():
 
 
 def build_tables(graph, cluster, device="cuda", stream=None, out: Optional[Tables] = None,
-                 shared: bool = False, mesh=None) -> Tables:
+                 shared: bool = False, mesh=None, topology=None) -> Tables:
     """Enumeration, node table and edge table of one graph on one cluster.
     ``out``: tables of an earlier build of the same graph to fill again;
     ``shared``: identical edge tables computed once (taps_edge_costs_shared);
     ``mesh``: the strategy space of a fixed device mesh (sizes, innermost
-    first) instead of every device matrix."""
+    first) instead of every device matrix; ``topology``: the link classes of a
+    workloads.Topology on the cluster's devices instead of its two."""
     g = _graph(graph)
     offs, strat = taps_enumerate_strategies(g, cluster, device=device, stream=stream,
                                             out=out.strategies if out is not None else None,
                                             mesh=mesh)
+    if topology is not None:
+        if shared:
+            raise ValueError("shared tables are built for two link classes only")
+        node = taps_node_costs_topology(g, topology, strat, offs, stream=stream,
+                                        out=out.node if out is not None else None)
+        eoffs, edge = taps_edge_costs_topology(g, topology, strat, offs, stream=stream,
+                                               out=out.edge if out is not None else None)
+        return Tables(offs, strat, node, eoffs, edge)
     node = taps_node_costs(g, cluster, strat, offs, stream=stream,
                            out=out.node if out is not None else None)
     eoffs, edge = taps_edge_costs(g, cluster, strat, offs, stream=stream,

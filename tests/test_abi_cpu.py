@@ -19,7 +19,8 @@ def lib():
 def test_exports_every_declared_symbol(lib):
     declared = T.declared_symbols()
     assert declared == sorted(["taps_enumerate_strategies", "taps_enumerate_strategies_mesh",
-                               "taps_node_costs", "taps_edge_costs",
+                               "taps_node_costs", "taps_edge_costs", "taps_node_costs_topology",
+                               "taps_edge_costs_topology",
                                "taps_edge_costs_shared", "taps_edge_costs_backward",
                                "taps_edge_costs_sweep", "taps_memory_costs",
                                "taps_set_edge_kernel_events", "taps_status_str",
@@ -109,6 +110,30 @@ def test_mesh_validation(lib, mesh):
     assert (offs == 7).all()   # nothing written
     assert lib.taps_enumerate_strategies_mesh(C.byref(g.struct), C.byref(cl), None,
                                               T._u64_array(offs), None, 0, None) == T.ERR_ARG
+
+
+@pytest.mark.parametrize("domains,bw", [
+    ((8, 4, 16), (600, 100, 25)),          # not non-decreasing
+    ((8, 24), (600, 100)),                 # not a power of two
+    ((8, 512), (600, 100)),                # more than 256 devices
+    ((8, 32, 128), (600, 0, 25)),          # a zero bandwidth
+    ((8, 32, 128), (600, 100, 600000007)), # ratios too fine for exact keys
+    ((), ()),                              # no class
+    ((1, 2, 4, 8, 16), (5, 4, 3, 2, 1)),   # five classes
+])
+def test_topology_validation(lib, domains, bw):
+    g = T.pack_graph(W.mlp2())
+    n = len(domains)
+    tp = T.TopologyS(n, (C.c_uint32 * 4)(*domains[:4]), (C.c_uint64 * 4)(*[b * W.GB for b in bw[:4]]))
+    offs = np.array([0, 9, 13, 22], np.uint64)
+    eo = np.full(3, 5, np.uint64)
+    assert lib.taps_edge_costs_topology(C.byref(g.struct), C.byref(tp), None, T._u64_array(offs),
+                                        T._u64_array(eo), T._table(None), 0, None) == T.ERR_TOPOLOGY
+    assert T.last_error() != "" and (eo == 5).all()
+    assert lib.taps_node_costs_topology(C.byref(g.struct), C.byref(tp), None, T._u64_array(offs),
+                                        T.Table(1, 1, 1, 1, 1), None) == T.ERR_TOPOLOGY
+    assert lib.taps_edge_costs_topology(C.byref(g.struct), None, None, T._u64_array(offs),
+                                        T._u64_array(eo), T._table(None), 0, None) == T.ERR_ARG
 
 
 def _op(**kw):

@@ -257,6 +257,78 @@ def test_fixed_mesh_spaces(T):
     assert done >= 8
 
 
+def _topology_check(T, graph, cluster, topo, name, sample=None):
+    """Tables under link classes against the oracle: every entry, or `sample`
+    seeded entries per edge."""
+    import torch
+    say(f"[gpu] build {name} under {topo}")
+    tabs = T.build_tables(graph, cluster, topology=topo)
+    torch.cuda.synchronize()
+    strats = check_strategies(T, graph, cluster, tabs.op_offsets, tabs.strategies)
+    node = _host(tabs.node)
+    for k, op in enumerate(graph.ops):
+        a, b = int(tabs.op_offsets[k]), int(tabs.op_offsets[k + 1])
+        assert_records({f: v[a:b] for f, v in node.items()},
+                       O.node_table_topo(op, strats[k], topo), f"{name} node {k}")
+    rng = np.random.default_rng(99)
+    for x, e in enumerate(graph.edges):
+        a, b = int(tabs.edge_offsets[x]), int(tabs.edge_offsets[x + 1])
+        src, dst = graph.ops[e.src], graph.ops[e.dst]
+        if sample is None:
+            got = {f: _np(v[a:b]) for f, v in tabs.edge.items()}
+            ref = O.edge_table_topo(src, strats[e.src], dst, e.slot, strats[e.dst], topo)
+        else:
+            nd = len(strats[e.dst])
+            loc = np.unique(np.concatenate([[0, b - a - 1], rng.integers(0, b - a, sample)]))
+            glob = torch.from_numpy(loc + a).to(tabs.edge["t"].device)
+            got = {f: _np(_signed(v).index_select(0, glob).view(v.dtype))
+                   for f, v in tabs.edge.items()}
+            ref = O.edge_entries_topo(src, strats[e.src], dst, e.slot, strats[e.dst], loc // nd,
+                                      loc % nd, topo)
+        assert_records(got, ref, f"{name} edge {x}")
+    return tabs
+
+
+def _random_topology(rng, n):
+    k = rng.randint(1, 4)
+    sizes = sorted(rng.randint(0, n) for _ in range(k - 1)) + [n]
+    bw = [rng.choice([600, 400, 100, 50, 25, 12]) * W.GB for _ in range(k)]
+    return W.Topology(tuple(1 << e for e in sizes), tuple(bw))
+
+
+def test_link_class_tables(T):
+    """taps_node_costs_topology / taps_edge_costs_topology against the oracle: the
+    three-class topologies of the wide MLP and (one layer, then the whole graph on
+    samples) the 96-layer GPT, random graphs under random topologies, and the
+    two-class topology, which must give exactly the tables of taps_edge_costs."""
+    import torch
+    for k in (4, 5):
+        w = W.config(k)
+        cl = w.clusters[0][1]
+        g = w.graph if k == 4 else W.leading_ops(w.graph, 28)
+        _topology_check(T, g, cl, W.CONFIG_TOPOLOGIES[k], f"{w.name}")
+    w = W.config(5)
+    _topology_check(T, w.graph, w.clusters[0][1], W.CONFIG_TOPOLOGIES[5], w.name, sample=40)
+    rng = random.Random(5150)
+    done = 0
+    for k, (g, cl) in enumerate(_random_cases(5150, 24)):
+        topo = _random_topology(rng, cl.devices.bit_length() - 1)
+        try:
+            _topology_check(T, g, cl, topo, f"random {k} N={cl.devices}")
+        except T.TapsError as ex:
+            assert ex.status in (T.ERR_NO_STRATEGY, T.ERR_TOPOLOGY)
+            continue
+        done += 1
+    assert done >= 12
+    for cfg in (1, 2, 4):
+        w = W.config(cfg)
+        cl = w.clusters[0][1]
+        a = T.build_tables(w.graph, cl)
+        b = T.build_tables(w.graph, cl, topology=W.Topology.of(cl))
+        torch.cuda.synchronize()
+        assert _same_tables(a.edge, b.edge) and _same_tables(a.node, b.node), w.name
+
+
 def test_empty_graph_and_no_edges(T):
     cl = W.Cluster(2, 2, 10, 1)
     tabs = T.build_tables(W.Graph(), cl)

@@ -225,3 +225,16 @@ def test_fixed_mesh_space_search(oracle_lib):
         assert _close(plan.objective, _exhaustive(w.graph, node, edge))
         assert plan.objective >= t_free * (1 - 1e-12)
         assert _close(plan.objective, t_free) == same
+
+
+def test_link_class_tables_search(oracle_lib):
+    """The ILP on tables under three link classes reaches the exhaustive optimum
+    of those tables (the 2-layer MLP on 2 x 2 devices as blocks of 1, 2, 4)."""
+    w = W.config(1)
+    cl = w.clusters[0][1]
+    topo = W.Topology((1, 2, 4), (400 * W.GB, 100 * W.GB, 25 * W.GB))
+    tab = oracle_lib.build_tables(w.graph, cl, topology=topo)
+    node = [np.asarray(v["t"], dtype=np.float64) for v in tab.node]
+    edge = [np.asarray(m["t"], dtype=np.float64) for m in tab.edge]
+    plan = S.solve(w.graph, node, edge)
+    assert _close(plan.objective, _exhaustive(w.graph, node, edge))
