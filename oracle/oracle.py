@@ -69,14 +69,15 @@ MAX_CLASSES = 4
 
 class OrTopology(C.Structure):
     _fields_ = [("n_classes", C.c_int32), ("pad_", C.c_int32),
-                ("domain", C.c_int64 * MAX_CLASSES), ("bw", C.c_uint64 * MAX_CLASSES)]
+                ("domain", C.c_int64 * MAX_CLASSES), ("bw", C.c_uint64 * MAX_CLASSES),
+                ("bw_a2a", C.c_uint64)]
 
 
 def make_topology(topo) -> OrTopology:
     """workloads.Topology -> the oracle's struct."""
     assert 1 <= len(topo.domains) == len(topo.bw) <= MAX_CLASSES
     return OrTopology(len(topo.domains), 0, (C.c_int64 * MAX_CLASSES)(*topo.domains),
-                      (C.c_uint64 * MAX_CLASSES)(*topo.bw))
+                      (C.c_uint64 * MAX_CLASSES)(*topo.bw), topo.bw_a2a)
 
 
 RECORD_DTYPE = np.dtype([("t", "<f8"), ("vol", "<u8"), ("intra", "<u8"), ("inter", "<u8"),

@@ -58,7 +58,9 @@
  *        belongs to the smallest domain whose Algorithm 2 / 3 count is zero
  *        (its group fits inside one block), takes that class's bandwidth and
  *        the count of the next smaller domain as its ct; with the domains
- *        (L, N) this is the paper's two-class model.
+ *        (L, N) this is the paper's two-class model.  An AllToAll inside one
+ *        domain[0] block may take its own bandwidth (peer to peer over every
+ *        link of the block, where a ring uses one).
  */
 #include <stdint.h>
 #include <stdlib.h>
@@ -123,6 +125,7 @@ typedef struct {
     int32_t pad_;
     int64_t domain[OR_MAX_CLASSES];
     uint64_t bw[OR_MAX_CLASSES];
+    uint64_t bw_a2a;   /* an AllToAll inside one domain[0] block: bytes/s (0: bw[0]) */
 } or_topology;
 
 static or_topology two_class(int64_t N, int64_t L, uint64_t Bintra, uint64_t Binter) {
@@ -793,7 +796,8 @@ int or_sequence(const int32_t *Mfrom, const int32_t *Mto, int r, int cand, or_re
 typedef struct {
     double t;
     uint64_t vol, intra, inter;
-    uint64_t x[OR_MAX_CLASSES];   /* per link class: link volume x ct (x[0] = intra) */
+    uint64_t x[OR_MAX_CLASSES];   /* per link class: link volume x ct (x[0]: intra, rings) */
+    uint64_t x_a2a;               /* intra AllToAll volume when it has its own bandwidth */
     uint32_t n_coll, n_inter, sum_ct;
 } seq_cost;
 
@@ -842,7 +846,7 @@ static seq_cost cost_sequence(const int64_t *D, int h, const int32_t *Mfrom, int
             V = (uint64_t)(p - 1) * shard / (uint64_t)p;     /* Eq. 10 */
             if (ct == 0) {
                 link = V;
-                cost = ((double)V / (double)N) / Bintra;
+                cost = ((double)V / (double)N) / (topo->bw_a2a ? (double)topo->bw_a2a : Bintra);
             } else {                                          /* Eq. 14, p > k */
                 link = (uint64_t)k_in * (uint64_t)(p - k_in) * shard / (uint64_t)p;
                 double factor = (double)(k_in * (p - k_in)) / (double)(p - 1);
@@ -859,7 +863,10 @@ static seq_cost cost_sequence(const int64_t *D, int h, const int32_t *Mfrom, int
         c.n_coll += 1;
         if (ct == 0) {
             c.intra += link;
-            c.x[0] += link;
+            if (op->kind == OR_ALLTOALL && topo->bw_a2a)
+                c.x_a2a += link;
+            else
+                c.x[0] += link;
         } else {
             c.inter += link * (uint64_t)ct;
             c.x[cls] += link * (uint64_t)ct;
@@ -944,34 +951,43 @@ static uint64_t gcd_u64(uint64_t a, uint64_t b) {
     return a;
 }
 
-/* Exact order of sum_c x[c] / bw[c] (reading R-j) as integer keys: with two
- * classes x[0] bw[1] + x[1] bw[0] (reading R-h's intra/(N B_intra) +
- * inter/(N B_inter)); with more, sum_c x[c] w[c] with w[c] = lcm(bw) / bw[c],
- * which must stay below 2^32 (returns -1 otherwise). */
-static int class_weights(const or_topology *topo, uint64_t *w) {
-    if (topo->n_classes == 2) {
+/* Exact order of sum_c x[c] / bw[c] (+ x_a2a / bw_a2a; reading R-j) as
+ * integer keys: with two classes x[0] bw[1] + x[1] bw[0] (reading R-h's
+ * intra/(N B_intra) + inter/(N B_inter)); otherwise sum_c x[c] w[c] with
+ * w[c] = lcm(bw) / bw[c], which must stay below 2^32 (returns -1 otherwise). */
+static int class_weights(const or_topology *topo, uint64_t *w, uint64_t *w_a2a) {
+    *w_a2a = 0;
+    if (topo->n_classes == 2 && !topo->bw_a2a) {
         w[0] = topo->bw[1];
         w[1] = topo->bw[0];
         return 0;
     }
     unsigned __int128 lcm = 1;
-    for (int c = 0; c < topo->n_classes; ++c) {
-        if (topo->bw[c] == 0) return -1;
-        const uint64_t g = gcd_u64((uint64_t)(lcm % topo->bw[c]), topo->bw[c]);
+    for (int c = 0; c <= topo->n_classes; ++c) {
+        const uint64_t b = c < topo->n_classes ? topo->bw[c] : topo->bw_a2a;
+        if (c == topo->n_classes && !b) break;
+        if (b == 0) return -1;
+        const uint64_t g = gcd_u64((uint64_t)(lcm % b), b);
         const unsigned __int128 q = lcm / g;
         if (q >> 64) return -1;
-        lcm = q * topo->bw[c];
+        lcm = q * b;
     }
-    for (int c = 0; c < topo->n_classes; ++c) {
-        unsigned __int128 q = lcm / topo->bw[c];
+    for (int c = 0; c <= topo->n_classes; ++c) {
+        const uint64_t b = c < topo->n_classes ? topo->bw[c] : topo->bw_a2a;
+        if (!b) break;
+        unsigned __int128 q = lcm / b;
         if (q >> 32) return -1;
-        w[c] = (uint64_t)q;
+        if (c < topo->n_classes)
+            w[c] = (uint64_t)q;
+        else
+            *w_a2a = (uint64_t)q;
     }
     return 0;
 }
 
-static unsigned __int128 class_key(const seq_cost *sc, const or_topology *topo, const uint64_t *w) {
-    unsigned __int128 key = 0;
+static unsigned __int128 class_key(const seq_cost *sc, const or_topology *topo, const uint64_t *w,
+                                   uint64_t w_a2a) {
+    unsigned __int128 key = (unsigned __int128)sc->x_a2a * w_a2a;
     for (int c = 0; c < topo->n_classes; ++c) key += (unsigned __int128)sc->x[c] * w[c];
     return key;
 }
@@ -984,9 +1000,9 @@ static int edge_cost_dir(const or_op *src, const or_strategy *si, const or_op *d
                          or_record *rec) {
     or_unified u;
     uint64_t shard0;
-    uint64_t w[OR_MAX_CLASSES];
+    uint64_t w[OR_MAX_CLASSES], w_a2a;
     memset(rec, 0, sizeof *rec);
-    if (class_weights(topo, w)) return -1;
+    if (class_weights(topo, w, &w_a2a)) return -1;
     if (edge_problem_dir(src, si, dst, slot, sj, N, reverse, &u, &shard0)) return -1;
     or_redop seq[OR_MAX_SEQ];
     seq_cost best;
@@ -998,7 +1014,7 @@ static int edge_cost_dir(const or_op *src, const or_strategy *si, const or_op *d
         int len = or_sequence(u.m_from, u.m_to, u.r, c, seq);
         if (len < 0) return -1;
         seq_cost sc = cost_sequence(u.D, u.h, u.m_from, u.r, seq, len, shard0, N, topo);
-        unsigned __int128 key = class_key(&sc, topo, w);
+        unsigned __int128 key = class_key(&sc, topo, w, w_a2a);
         if (best_c < 0 || key < best_key) {
             best_c = c;
             best_key = key;

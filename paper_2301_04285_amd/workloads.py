@@ -108,9 +108,12 @@ class Topology:
     blocks of ``domains[c]`` consecutive device ranks, non-decreasing, the last
     one all devices.  Class 0 links join the devices of one domains[0] block (a
     node), class c >= 1 links join the domains[c-1] blocks of one domains[c]
-    block, at ``bw[c]`` bytes/s each."""
+    block, at ``bw[c]`` bytes/s each.  ``bw_a2a``: an AllToAll inside one
+    domains[0] block moves at this rate (peer to peer over every link of the
+    block, where a ring uses one); 0: bw[0]."""
     domains: Tuple[int, ...]
     bw: Tuple[int, ...]
+    bw_a2a: int = 0
 
     @property
     def devices(self) -> int:

@@ -23,11 +23,13 @@ from paper_2301_04285_amd import workloads as W
 
 
 def _random_topology(rng, n):
-    """Non-decreasing block sizes (powers of two up to 2^n) and bandwidths."""
+    """Non-decreasing block sizes (powers of two up to 2^n) and bandwidths, and
+    half the time an in-block AllToAll bandwidth of its own."""
     k = rng.randint(1, 4)
     sizes = sorted(rng.randint(0, n) for _ in range(k - 1)) + [n]
     bw = [rng.choice([600, 400, 100, 50, 25, 12]) * W.GB for _ in range(k)]
-    return W.Topology(tuple(1 << e for e in sizes), tuple(bw))
+    a2a = rng.choice([0, 0, 1200 * W.GB, 7 * 150 * W.GB, 50 * W.GB])
+    return W.Topology(tuple(1 << e for e in sizes), tuple(bw), a2a)
 
 
 def _matrix(s, n_axes):
@@ -146,7 +148,8 @@ def _candidate_costs(oracle_lib, g, e, si, sj, topo):
             vol += V
             if c == 0:
                 intra += link
-                t += Fraction(link, N * topo.bw[0])
+                a2a = o.kind == oracle_lib.ALLTOALL and topo.bw_a2a
+                t += Fraction(link, N * (topo.bw_a2a if a2a else topo.bw[0]))
             else:
                 inter += link * ct
                 n_inter += 1
@@ -209,3 +212,24 @@ def test_cost_non_increasing_in_each_bandwidth(oracle_lib):
         faster = oracle_lib.build_tables(g, cl, topology=W.Topology(base.domains, tuple(bw)))
         for a, b in zip(ref.edge + ref.node, faster.edge + faster.node):
             assert (b["t"] <= a["t"] * (1 + 1e-12)).all()
+
+
+def test_alltoall_bandwidth(oracle_lib):
+    """An in-block AllToAll bandwidth equal to bw[0] changes nothing; a faster one
+    lowers t exactly where the chosen sequence has an in-block AllToAll."""
+    g = W.gpt(1, 64, 4, 32, 4, 2)
+    cl = W.Cluster(4, 4, 1, 1)
+    base = W.Topology((4, 8, 16), (600 * W.GB, 100 * W.GB, 25 * W.GB))
+    same = W.Topology(base.domains, base.bw, base.bw[0])
+    fast = W.Topology(base.domains, base.bw, 7 * base.bw[0])
+    a = oracle_lib.build_tables(g, cl, topology=base)
+    b = oracle_lib.build_tables(g, cl, topology=same)
+    c = oracle_lib.build_tables(g, cl, topology=fast)
+    lower = 0
+    for x, y, z in zip(a.edge, b.edge, c.edge):
+        assert x.tobytes() == y.tobytes()
+        assert (z["t"] <= x["t"] * (1 + 1e-12)).all()
+        lower += int((z["t"] < x["t"] * (1 - 1e-12)).sum())
+    for x, z in zip(a.node, c.node):   # AllReduces are rings
+        assert x.tobytes() == z.tobytes()
+    assert lower > 0
