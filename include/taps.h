@@ -151,12 +151,15 @@ typedef struct {
  * nodes, ...).  Class 0 links join the devices of one domain[0] block; class
  * c >= 1 links join the domain[c-1] blocks of one domain[c] block, bw[c]
  * bytes per second each.  The paper's cluster is {2, {L, N}, {B_intra,
- * B_inter}}. */
+ * B_inter}, 0}. */
 #define TAPS_MAX_CLASSES 4
 typedef struct {
     uint32_t n_classes;                 /* 1 .. TAPS_MAX_CLASSES */
     uint32_t domain[TAPS_MAX_CLASSES];  /* powers of two, non-decreasing, the last N */
     uint64_t bw[TAPS_MAX_CLASSES];      /* bytes per second, > 0 */
+    uint64_t bw_a2a;                    /* bytes per second of an AllToAll inside one domain[0]
+                                           block (peer to peer over every link of the block,
+                                           where a ring uses one); 0: bw[0] */
 } taps_topology;
 
 /* Device arrays of one table, one element per record. */
@@ -276,12 +279,14 @@ taps_status taps_edge_costs_backward(const taps_graph *graph, const taps_cluster
  * t = sum over classes of (link volume x ct) / (N bw[c]); intra = the class-0
  * volume; inter = the sum over the other classes of link volume x ct; vol and
  * meta as before ("inter-node" read as "leaving a domain[0] block").
- * Candidates compare exactly by sum_c x_c lcm(bw) / bw[c].  With the domains
- * (L, N) the tables equal those of taps_node_costs / taps_edge_costs.
+ * Candidates compare exactly by sum_c x_c lcm(bw) / bw[c] (bw_a2a, if set,
+ * prices the in-block AllToAll volume, which stays in intra).  With the
+ * domains (L, N) and bw_a2a 0 the tables equal those of taps_node_costs /
+ * taps_edge_costs.
  *   topology  host; TAPS_ERR_TOPOLOGY unless n_classes is 1..TAPS_MAX_CLASSES,
  *             every domain is a power of two, non-decreasing, the last one
  *             N <= 2^TAPS_MAX_LEVELS, every bw > 0 and lcm(bw) / bw[c] < 2^30
- *             for every c (bandwidths in round ratios).
+ *             for every c, bw_a2a included (bandwidths in round ratios).
  *   strategies from taps_enumerate_strategies(_mesh) on N devices.
  * Other arguments, layouts and errors as taps_node_costs / taps_edge_costs. */
 taps_status taps_node_costs_topology(const taps_graph *graph, const taps_topology *topology,

@@ -521,23 +521,31 @@ taps_status check_topology(const taps_topology *t, taps_hier *H, taps_cluster *c
     if (N > (1ull << TAPS_MAX_LEVELS))
         return fail(TAPS_ERR_TOPOLOGY, "%llu devices exceed the limit of %u", (unsigned long long)N,
                     1u << TAPS_MAX_LEVELS);
-    // exact-order weights lcm(bw) / bw[c], each below 2^30
+    // exact-order weights lcm(bw) / bw[c] (and the in-block AllToAll's), each below 2^30
+    const uint32_t nb = C + (t->bw_a2a ? 1u : 0u);
+    auto bw_of = [&](uint32_t c) { return c < C ? t->bw[c] : t->bw_a2a; };
     unsigned __int128 lcm = 1;
-    for (uint32_t c = 0; c < C; ++c) {
-        const uint64_t g = std::gcd((uint64_t)(lcm % t->bw[c]), t->bw[c]);
+    for (uint32_t c = 0; c < nb; ++c) {
+        const uint64_t g = std::gcd((uint64_t)(lcm % bw_of(c)), bw_of(c));
         const unsigned __int128 q = lcm / g;
         if (q >> 64) return fail(TAPS_ERR_TOPOLOGY, "bandwidths not in round ratios");
-        lcm = q * t->bw[c];
+        lcm = q * bw_of(c);
     }
     std::memset(H, 0, sizeof(*H));
     H->n_classes = C;
-    for (uint32_t c = 0; c < C; ++c) {
-        const unsigned __int128 w = lcm / t->bw[c];
+    for (uint32_t c = 0; c < nb; ++c) {
+        const unsigned __int128 w = lcm / bw_of(c);
         if (w >> 30)
-            return fail(TAPS_ERR_TOPOLOGY, "bandwidths not in round ratios (lcm / bw[%u] >= 2^30)",
-                        c);
-        H->w[c] = (uint64_t)w;
-        H->inv_n_bw[c] = 1.0 / ((double)N * (double)t->bw[c]);
+            return fail(TAPS_ERR_TOPOLOGY, "bandwidths not in round ratios (lcm / bw >= 2^30)");
+        const double inv = 1.0 / ((double)N * (double)bw_of(c));
+        if (c < C) {
+            H->w[c] = (uint64_t)w;
+            H->inv_n_bw[c] = inv;
+        } else {
+            H->w_a2a = (uint64_t)w;
+            H->inv_n_bw_a2a = inv;
+            H->a2a_own = 1;
+        }
     }
     // class of a collective with top level l: the boundaries log2(domain[c]) <= l (c < C - 1);
     // its ct counts the uplinks of a block of the largest of them

@@ -1047,16 +1047,21 @@ struct taps_hier {
     uint32_t pad;
     uint64_t w[TAPS_D_MAX_CLASSES];        // exact-order weights, each below 2^30
     double inv_n_bw[TAPS_D_MAX_CLASSES];   // 1 / (N bw[c])
+    uint64_t w_a2a;          // weight of the in-block AllToAll volume (0: priced as class 0)
+    double inv_n_bw_a2a;     // 1 / (N bw_a2a)
+    uint32_t a2a_own;        // 1: in-block AllToAlls go to xa at their own bandwidth
+    uint32_t pad2;
 };
 
 // One candidate in factor units, per link class (x0: inside the innermost block).
 struct taps_fach {
     uint32_t vol, x0, x1, x2, x3;
+    uint32_t xa;       // in-block AllToAll volume priced at its own bandwidth
     uint32_t counts;   // collectives | inter-block collectives << 8 | sum of ct << 16
 };
 
 __host__ __device__ inline void taps_fac_zero(taps_fach &c) {
-    c.vol = c.x0 = c.x1 = c.x2 = c.x3 = 0;
+    c.vol = c.x0 = c.x1 = c.x2 = c.x3 = c.xa = 0;
     c.counts = 0;
 }
 
@@ -1070,7 +1075,7 @@ __host__ __device__ inline void taps_fach_add(taps_fach &c, uint32_t cls, uint32
 
 __host__ __device__ inline uint64_t taps_fach_key(const taps_fach &c, const taps_hier &H) {
     return (uint64_t)c.x0 * H.w[0] + (uint64_t)c.x1 * H.w[1] + (uint64_t)c.x2 * H.w[2] +
-           (uint64_t)c.x3 * H.w[3];
+           (uint64_t)c.x3 * H.w[3] + (uint64_t)c.xa * H.w_a2a;
 }
 
 // The shared uplinks of a collective of width w at lowest level lo whose
@@ -1112,7 +1117,8 @@ struct taps_hier_model {
             const uint32_t cls = taps_nib(H->cls_of_top, top);
             c.vol += V;
             if (!cls) {
-                c.x0 += V;
+                c.x0 += H->a2a_own ? 0u : V;
+                c.xa += H->a2a_own ? V : 0u;
                 c.counts += 1u;
                 continue;
             }
@@ -1198,10 +1204,11 @@ __host__ __device__ inline taps_entry_out taps_entry_finish_h(const taps_pickh &
     taps_entry_out o;
     const double unit = (double)S.tbytes * (1.0 / 256.0);
     o.vol = taps_scale(S, k.vmin);
-    o.intra = taps_scale(S, k.best.x0);
+    o.intra = taps_scale(S, k.best.x0) + taps_scale(S, k.best.xa);
     o.inter = taps_scale(S, k.best.x1) + taps_scale(S, k.best.x2) + taps_scale(S, k.best.x3);
     o.t = (double)k.best.x0 * (unit * H.inv_n_bw[0]) + (double)k.best.x1 * (unit * H.inv_n_bw[1]) +
-          (double)k.best.x2 * (unit * H.inv_n_bw[2]) + (double)k.best.x3 * (unit * H.inv_n_bw[3]);
+          (double)k.best.x2 * (unit * H.inv_n_bw[2]) + (double)k.best.x3 * (unit * H.inv_n_bw[3]) +
+          (double)k.best.xa * (unit * H.inv_n_bw_a2a);
     const uint32_t n = k.best.counts;
     o.meta = k.cand | ((n & 0xFFu) << 2) | (((n >> 8) & 0xFFu) << 7) | ((n >> 16) << 12);
     o.ok = k.ok;

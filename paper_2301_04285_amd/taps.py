@@ -50,7 +50,7 @@ MAX_CLASSES = 4
 
 class TopologyS(C.Structure):
     _fields_ = [("n_classes", C.c_uint32), ("domain", C.c_uint32 * MAX_CLASSES),
-                ("bw", C.c_uint64 * MAX_CLASSES)]
+                ("bw", C.c_uint64 * MAX_CLASSES), ("bw_a2a", C.c_uint64)]
 
 
 class Tensor(C.Structure):
@@ -304,7 +304,7 @@ def pack_topology(topo) -> TopologyS:
     if not 1 <= len(topo.domains) == len(topo.bw) <= MAX_CLASSES:
         raise ValueError(f"1 to {MAX_CLASSES} link classes, one bandwidth each")
     return TopologyS(len(topo.domains), (C.c_uint32 * MAX_CLASSES)(*topo.domains),
-                     (C.c_uint64 * MAX_CLASSES)(*topo.bw))
+                     (C.c_uint64 * MAX_CLASSES)(*topo.bw), getattr(topo, "bw_a2a", 0))
 
 
 def taps_node_costs_topology(graph, topology, strategies, op_offsets, out=None, stream=None):

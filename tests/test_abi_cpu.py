@@ -124,7 +124,8 @@ def test_mesh_validation(lib, mesh):
 def test_topology_validation(lib, domains, bw):
     g = T.pack_graph(W.mlp2())
     n = len(domains)
-    tp = T.TopologyS(n, (C.c_uint32 * 4)(*domains[:4]), (C.c_uint64 * 4)(*[b * W.GB for b in bw[:4]]))
+    tp = T.TopologyS(n, (C.c_uint32 * 4)(*domains[:4]), (C.c_uint64 * 4)(*[b * W.GB for b in bw[:4]]),
+                     0)
     offs = np.array([0, 9, 13, 22], np.uint64)
     eo = np.full(3, 5, np.uint64)
     assert lib.taps_edge_costs_topology(C.byref(g.struct), C.byref(tp), None, T._u64_array(offs),

@@ -293,7 +293,8 @@ def _random_topology(rng, n):
     k = rng.randint(1, 4)
     sizes = sorted(rng.randint(0, n) for _ in range(k - 1)) + [n]
     bw = [rng.choice([600, 400, 100, 50, 25, 12]) * W.GB for _ in range(k)]
-    return W.Topology(tuple(1 << e for e in sizes), tuple(bw))
+    a2a = rng.choice([0, 0, 1200 * W.GB, 7 * 150 * W.GB, 50 * W.GB])
+    return W.Topology(tuple(1 << e for e in sizes), tuple(bw), a2a)
 
 
 def test_link_class_tables(T):
@@ -306,7 +307,10 @@ def test_link_class_tables(T):
         w = W.config(k)
         cl = w.clusters[0][1]
         g = w.graph if k == 4 else W.leading_ops(w.graph, 28)
-        _topology_check(T, g, cl, W.CONFIG_TOPOLOGIES[k], f"{w.name}")
+        topo = W.CONFIG_TOPOLOGIES[k]
+        _topology_check(T, g, cl, topo, f"{w.name}")
+        # in-node AllToAlls over all seven links of an 8-device node
+        _topology_check(T, g, cl, W.Topology(topo.domains, topo.bw, 7 * 150 * W.GB), f"{w.name}")
     w = W.config(5)
     _topology_check(T, w.graph, w.clusters[0][1], W.CONFIG_TOPOLOGIES[5], w.name, sample=40)
     rng = random.Random(5150)
