@@ -5,8 +5,10 @@ One step = one pass of the whole hot path on the 96-layer GPT-style graph
 16 nodes x 8 devices (600 GB/s inside a node, 100 GB/s between nodes):
 enumerate every strategy of every operator, compute the node (intra-op)
 table and the edge (redistribution) table -- 599,136 strategies and
-98,668,128 edge entries, left resident in HBM.  The graph description is
-packed into the C structs once, outside the timed region.
+98,668,128 edge entries, left resident in HBM -- through one call of
+taps_build_tables (sized on the host, queued without a synchronisation, so
+consecutive steps overlap the host's work with the GPU's).  The graph
+description is packed into the C structs once, outside the timed region.
 
 Prints one JSON line.  `value` is edge entries per second of whole steps;
 `roofline` relates the edge-table kernel (which dominates the step), timed
@@ -166,12 +168,23 @@ def main() -> int:
 
     stream = torch.cuda.current_stream()
     tabs = taps.build_tables(g, cl, stream=stream)    # allocates the outputs once
+    # the separate calls (enumerate, node, edge) give the same tables: checked below
+    # for the shared-table and sweep legs, which run on them
     torch.cuda.synchronize()
     entries = int(tabs.edge_offsets[-1])
     strategies = int(tabs.op_offsets[-1])
     log(f"[bench] {strategies} strategies, {entries} edge entries")
 
     def step(ev=None, shared=False, edge_out=None, points=None, topology=None):
+        if not shared and edge_out is None and not points and topology is None:
+            # the headline build: one call, sized on the host, nothing synchronised
+            if ev is not None:
+                ev[0].record(stream)
+                taps.taps_set_edge_kernel_events(ev[2], ev[3])
+            taps.taps_build_tables(g, cl, out=tabs, stream=stream)
+            if ev is not None:
+                ev[1].record(stream)
+            return
         offs, strat = taps.taps_enumerate_strategies(g, cl, stream=stream, out=tabs.strategies)
         if topology is None:
             taps.taps_node_costs(g, cl, strat, offs, out=tabs.node, stream=stream)
@@ -211,9 +224,9 @@ def main() -> int:
         kernel_ms = float(np.mean([ev[2].elapsed_time(ev[3]) for ev in events]))
         return wall * 1e3 / args.steps, edge_ms, kernel_ms
 
-    ms_per_step, edge_ms, kernel_ms = timed()
-    log(f"[bench] {args.steps} steps: {ms_per_step:.3f} ms/step, edge call {edge_ms:.3f} ms, "
-        f"edge kernel {kernel_ms:.3f} ms")
+    ms_per_step, build_gpu_ms, kernel_ms = timed()
+    log(f"[bench] {args.steps} steps: {ms_per_step:.3f} ms/step, build on the GPU "
+        f"{build_gpu_ms:.3f} ms, edge kernel {kernel_ms:.3f} ms")
 
     bytes_per_launch = BYTES_PER_ENTRY * entries
     achieved = bytes_per_launch / (kernel_ms * 1e-3) / 1e9
@@ -235,9 +248,9 @@ def main() -> int:
                    "modeled_devices": cl.devices, "devices_per_node": cl.devices_per_node,
                    "bw_intra_GBps": cl.bw_intra / 1e9, "bw_inter_GBps": cl.bw_inter / 1e9},
         "build_ms": ms_per_step,
-        "edge_call_ms": edge_ms,
+        "build_gpu_ms": build_gpu_ms,
         "edge_kernel_ms": kernel_ms,
-        "edge_entries_per_s": entries / (edge_ms * 1e-3),
+        "edge_entries_per_s": entries / (kernel_ms * 1e-3),
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBPS,
                      "traffic": measured_traffic() if args.config == 5 else None},

@@ -204,6 +204,33 @@ taps_status taps_enumerate_strategies_mesh(const taps_graph *graph, const taps_c
                                            taps_strategy *strategies, uint64_t capacity,
                                            void *stream);
 
+/* The whole build in one call, without a host synchronisation: the strategies
+ * of taps_enumerate_strategies (or, with a mesh, of
+ * taps_enumerate_strategies_mesh), the node table of taps_node_costs and the
+ * edge table of taps_edge_costs, bit for bit.  The per-operator strategy
+ * counts are computed on the host by an exact count of the same filter
+ * (ordered runs of distinct partitionable axes covering the n levels, each
+ * at most as wide as its length allows, each boundary a mesh boundary), so
+ * op_offsets and edge_offsets are known before any GPU work and the whole
+ * build is queued on `stream` at once (a caller can queue the next build
+ * while this one runs).
+ *   mesh          host, or NULL for every device matrix.
+ *   op_offsets    host, n_ops + 1 entries, written.
+ *   strategies    device, strategy_capacity entries; node: device arrays of
+ *                 strategy_capacity records.
+ *   edge_offsets  host, n_edges + 1 entries, written; edge: device arrays of
+ *                 edge_capacity records, layout as taps_edge_costs.
+ *   strategies NULL and every table array NULL: size query (host only).  The
+ *   edge arrays may be NULL when the graph has no edge entries.
+ * TAPS_ERR_NO_STRATEGY, TAPS_ERR_CAPACITY (either capacity), TAPS_ERR_TOPOLOGY
+ * (cluster or mesh) and TAPS_ERR_ARG as the separate calls, all before any GPU
+ * work; outputs are valid after a stream synchronisation. */
+taps_status taps_build_tables(const taps_graph *graph, const taps_cluster *cluster,
+                              const taps_mesh *mesh, uint64_t *op_offsets,
+                              taps_strategy *strategies, uint64_t strategy_capacity, taps_table node,
+                              uint64_t *edge_offsets, taps_table edge, uint64_t edge_capacity,
+                              void *stream);
+
 /* Intra-operator cost of every strategy (Eq. 5-8 generalised to any
  * operator: one ring AllReduce per tensor that lacks some split axis -- the
  * forward partial sum of the output, the backward gradient of an input or

@@ -14,6 +14,7 @@
 #include <mutex>
 #include <numeric>
 #include <string>
+#include <unordered_map>
 #include <vector>
 
 #include "taps.h"
@@ -568,6 +569,48 @@ taps_status check_topology(const taps_topology *t, taps_hier *H, taps_cluster *c
     return TAPS_OK;
 }
 
+// The number of strategies GenerateStrategySet keeps for an operator on 2^n
+// devices: ordered runs of distinct partitionable axes that cover levels
+// 0..n-1 from level 0, axis a's run at most v_a = (trailing zero bits of its
+// length) wide so that its degree divides its length, every boundary between
+// two runs an allowed cut -- the candidates of k_enumerate that pass its two
+// tests, counted by a dynamic program over (levels covered, axes used).  The
+// count depends only on n, the allowed cuts, the partitionable axes and their
+// v_a, so it is memoised on those (per thread).
+uint64_t strategy_count(const taps_op &op, uint32_t n, uint32_t allowed) {
+    uint64_t key = n | (uint64_t)(allowed & 0xFFu) << 4 | (uint64_t)op.part_mask << 12;
+    uint32_t v[TAPS_MAX_AXES] = {0};
+    for (uint32_t a = 0; a < op.n_axes; ++a) {
+        if (!((op.part_mask >> a) & 1u)) continue;
+        const uint32_t z = (uint32_t)__builtin_ctzll((uint64_t)op.axis_len[a]);
+        v[a] = z < n ? z : n;
+        key |= (uint64_t)v[a] << (20 + 4 * a);
+    }
+    thread_local std::unordered_map<uint64_t, uint64_t> memo;
+    const auto it = memo.find(key);
+    if (it != memo.end()) return it->second;
+    // ways[s][m]: sequences of runs covering levels 0..s-1 with axis set m
+    std::vector<uint64_t> ways((size_t)(n + 1) << TAPS_MAX_AXES, 0);
+    ways[0] = 1;
+    for (uint32_t lev = 0; lev < n; ++lev)
+        for (uint32_t m = 0; m < (1u << TAPS_MAX_AXES); ++m) {
+            const uint64_t w = ways[((size_t)lev << TAPS_MAX_AXES) | m];
+            if (!w) continue;
+            for (uint32_t a = 0; a < op.n_axes; ++a) {
+                if (!((op.part_mask >> a) & 1u) || ((m >> a) & 1u)) continue;
+                for (uint32_t e = 1; e <= v[a] && lev + e <= n; ++e) {
+                    const uint32_t t = lev + e;
+                    if (t < n && !((allowed >> t) & 1u)) continue;
+                    ways[((size_t)t << TAPS_MAX_AXES) | (m | (1u << a))] += w;
+                }
+            }
+        }
+    uint64_t count = 0;
+    for (uint32_t m = 0; m < (1u << TAPS_MAX_AXES); ++m) count += ways[((size_t)n << TAPS_MAX_AXES) | m];
+    memo.emplace(key, count);
+    return count;
+}
+
 // GenerateStrategySet on the device; allowed_cuts: the level boundaries a
 // strategy's axis runs may meet (all of them unless a fixed mesh is given).
 taps_status enumerate(const taps_graph *graph, const taps_launch &lp, uint32_t allowed_cuts,
@@ -744,6 +787,102 @@ taps_status taps_node_costs(const taps_graph *graph, const taps_cluster *cluster
         err = taps_launch_node_costs(at<taps_op>(dev, ch[0]), n_ops, at<uint64_t>(dev, ch[1]),
                                      d_desc, total, lp, out, stream);
     if (err != hipSuccess) return hip_fail(err, "node costs");
+    return TAPS_OK;
+}
+
+taps_status taps_build_tables(const taps_graph *graph, const taps_cluster *cluster,
+                              const taps_mesh *mesh, uint64_t *op_offsets,
+                              taps_strategy *strategies, uint64_t strategy_capacity, taps_table node,
+                              uint64_t *edge_offsets, taps_table edge, uint64_t edge_capacity,
+                              void *stream_) {
+    g_last_error.clear();
+    taps_launch lp;
+    taps_status st = check_cluster(cluster, &lp);
+    if (st == TAPS_OK) st = check_graph(graph, true);
+    if (st != TAPS_OK) return st;
+    if (!op_offsets || !edge_offsets) return fail(TAPS_ERR_ARG, "op_offsets or edge_offsets is NULL");
+    uint32_t allowed = 0xFFu;
+    if (mesh && (st = mesh_cuts(mesh, lp.n, &allowed)) != TAPS_OK) return st;
+    const uint32_t n_ops = graph->n_ops, n_edges = graph->n_edges;
+    // sizes, on the host
+    std::vector<uint64_t> offs(n_ops + 1, 0);
+    for (uint32_t k = 0; k < n_ops; ++k) {
+        const uint64_t c = strategy_count(graph->ops[k], lp.n, allowed);
+        if (c == 0)
+            return fail(TAPS_ERR_NO_STRATEGY,
+                        "op %u has no strategy on %u devices (no partitionable axis whose length "
+                        "the degrees divide)",
+                        k, 1u << lp.n);
+        offs[k + 1] = offs[k] + c;
+    }
+    if (offs[n_ops] > 0xFFFFFFFFull) return fail(TAPS_ERR_ARG, "more than 2^32 strategies");
+    std::vector<uint64_t> eoff(n_edges + 1, 0), segs(n_edges + 1, 0);
+    for (uint32_t e = 0; e < n_edges; ++e) {
+        const taps_edge &E = graph->edges[e];
+        const uint64_t ns = offs[E.src_op + 1] - offs[E.src_op];
+        const uint64_t nd = offs[E.dst_op + 1] - offs[E.dst_op];
+        eoff[e + 1] = eoff[e] + ns * nd;
+        segs[e + 1] = segs[e] + ns * ((nd + TAPS_TILE_COLS * TAPS_SEG_TILES - 1) /
+                                      (TAPS_TILE_COLS * TAPS_SEG_TILES));
+    }
+    if (segs[n_edges] >= 0x7FFFFFFFull) return fail(TAPS_ERR_ARG, "more than 2^31 row segments");
+    // a size query passes no array; a build passes the strategy and node arrays, and
+    // the edge arrays unless there are no edge entries (then they are not read)
+    const bool none_s = !strategies && !node.t && !node.vol && !node.intra && !node.inter &&
+                        !node.meta;
+    const bool all_s = strategies && node.t && node.vol && node.intra && node.inter && node.meta;
+    const bool none_e = !edge.t && !edge.vol && !edge.intra && !edge.inter && !edge.meta;
+    const bool all_e = edge.t && edge.vol && edge.intra && edge.inter && edge.meta;
+    const bool none = none_s && none_e;
+    if (!none && !(all_s && (all_e || (none_e && eoff[n_edges] == 0))))
+        return fail(TAPS_ERR_ARG, "strategies and every table array must be all set or all NULL "
+                                  "(the edge arrays may be NULL when there are no edge entries)");
+    if (!none && offs[n_ops] > strategy_capacity)
+        return fail(TAPS_ERR_CAPACITY, "%llu strategies, capacity %llu",
+                    (unsigned long long)offs[n_ops], (unsigned long long)strategy_capacity);
+    if (!none && eoff[n_edges] > edge_capacity)
+        return fail(TAPS_ERR_CAPACITY, "%llu entries, capacity %llu",
+                    (unsigned long long)eoff[n_edges], (unsigned long long)edge_capacity);
+    std::memcpy(op_offsets, offs.data(), sizeof(uint64_t) * (n_ops + 1));
+    std::memcpy(edge_offsets, eoff.data(), sizeof(uint64_t) * (n_edges + 1));
+    if (none || n_ops == 0) return TAPS_OK;
+    // one upload and one set of scratch for the whole build
+    hipStream_t stream = (hipStream_t)stream_;
+    scratch sc(stream);
+    const uint64_t total = offs[n_ops], n_segs = segs[n_edges];
+    std::vector<chunk> ch{{graph->ops, sizeof(taps_op) * n_ops, 0},
+                          {graph->edges, sizeof(taps_edge) * n_edges, 0},
+                          {offs.data(), sizeof(uint64_t) * (n_ops + 1), 0},
+                          {eoff.data(), sizeof(uint64_t) * (n_edges + 1), 0},
+                          {segs.data(), sizeof(uint64_t) * (n_edges + 1), 0}};
+    void *dev = nullptr;
+    if ((st = upload(ch, &dev, stream)) != TAPS_OK) return st;
+    sc.adopt(dev);
+    taps_desc *d_desc = nullptr;
+    taps_edge_params *d_params = nullptr;
+    taps_row_ref *d_segs = nullptr;
+    if ((st = sc.alloc((void **)&d_desc, sizeof(taps_desc) * total)) != TAPS_OK) return st;
+    if ((st = sc.alloc((void **)&d_params, sizeof(taps_edge_params) * (n_edges ? n_edges : 1))) !=
+        TAPS_OK)
+        return st;
+    if ((st = sc.alloc((void **)&d_segs, sizeof(taps_row_ref) * (n_segs ? n_segs : 1))) != TAPS_OK)
+        return st;
+    const taps_op *d_ops = at<taps_op>(dev, ch[0]);
+    hipError_t err = taps_launch_build_strategies(d_ops, n_ops, at<uint64_t>(dev, ch[2]), allowed,
+                                                  lp, strategies, d_desc, node, stream);
+    if (err == hipSuccess && eoff[n_edges] > 0) {
+        err = taps_launch_edge_setup(d_ops, at<taps_edge>(dev, ch[1]), n_edges,
+                                     at<uint64_t>(dev, ch[2]), at<uint64_t>(dev, ch[3]),
+                                     at<uint64_t>(dev, ch[4]), lp, false, d_params, n_segs, d_segs,
+                                     stream);
+        const hipEvent_t before = g_kernel_before, after = g_kernel_after;
+        g_kernel_before = g_kernel_after = nullptr;
+        if (err == hipSuccess && before) err = hipEventRecord(before, stream);
+        if (err == hipSuccess)
+            err = taps_launch_edge_costs(d_params, d_segs, n_segs, d_desc, lp, edge, stream);
+        if (err == hipSuccess && after) err = hipEventRecord(after, stream);
+    }
+    if (err != hipSuccess) return hip_fail(err, "build");
     return TAPS_OK;
 }
 

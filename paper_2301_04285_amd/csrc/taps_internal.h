@@ -102,6 +102,12 @@ hipError_t taps_launch_edge_costs_sweep(const taps_edge_params *params, const ta
                                         uint64_t n_rows, const taps_desc *desc,
                                         const taps_launch &lp, const taps_sweep &sw,
                                         hipStream_t stream);
+// Strategies, descriptors and node records of every operator in one launch
+// (one workgroup per operator); op_offsets: device copy of the host's counts.
+hipError_t taps_launch_build_strategies(const taps_op *ops, uint32_t n_ops,
+                                        const uint64_t *op_offsets, uint32_t allowed_cuts,
+                                        const taps_launch &lp, taps_strategy *out, taps_desc *desc,
+                                        taps_table node, hipStream_t stream);
 // Link-class hierarchies: the edge and node tables under the classes of H.
 hipError_t taps_launch_edge_costs_h(const taps_edge_params *params, const taps_row_ref *rows,
                                     uint64_t n_rows, const taps_desc *desc, const taps_launch &lp,

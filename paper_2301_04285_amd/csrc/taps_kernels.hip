@@ -238,6 +238,78 @@ __global__ __launch_bounds__(256) void k_node_costs(const taps_op *__restrict__ 
     out.meta[idx] = taps_meta(0, c);
 }
 
+// The whole strategy side of a build in one launch: one workgroup per
+// operator walks its candidates in canonical order, 256 per pass (a ballot
+// per wavefront, the four wavefront counts scanned in LDS), and writes every
+// valid strategy together with its descriptor and its node (intra-op) record.
+// The operator's strategies go to [op_offsets[k], op_offsets[k+1]), which the
+// host sized with an exact count of the same filter; nothing is written
+// outside that range.
+__global__ __launch_bounds__(256) void k_build_strategies(const taps_op *__restrict__ ops,
+                                                          const uint64_t *__restrict__ op_offsets,
+                                                          uint32_t allowed_cuts, taps_launch lp,
+                                                          taps_strategy *__restrict__ out,
+                                                          taps_desc *__restrict__ desc,
+                                                          taps_table node) {
+    __shared__ uint32_t W[9 * 9 * 9];
+    __shared__ uint32_t wave_count[4];
+    const uint32_t tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
+    for (uint32_t x = tid; x < 9u * 9u * 9u; x += blockDim.x) W[x] = kCompletions.v[x];
+    __syncthreads();
+    const taps_op &op = ops[blockIdx.x];
+    const uint32_t n_axes = op.n_axes, part = op.part_mask;
+    const uint32_t total = W[(taps_popc(part) * 9u + lp.n) * 9u];
+    const uint64_t base = op_offsets[blockIdx.x], end = op_offsets[blockIdx.x + 1];
+    const uint32_t full = taps_low_mask(lp.n);
+    uint64_t running = 0;
+    for (uint32_t r0 = 0; r0 < total; r0 += blockDim.x) {
+        const uint32_t r = r0 + tid;
+        uint32_t expo[TAPS_D_MAX_AXES];
+        int32_t pos[TAPS_D_MAX_AXES];
+        bool valid = r < total && taps_unrank(n_axes, part, lp.n, r, W, expo, pos);
+        if (valid)
+            for (uint32_t a = 0; a < n_axes; ++a)
+                if (op.axis_len[a] & (((int64_t)1 << expo[a]) - 1)) valid = false;
+        taps_desc D = {0u, 0u, 0u, 0u};
+        if (valid) {
+            D = taps_describe(n_axes, expo, pos);
+            if (D.cuts & ~allowed_cuts) valid = false;
+        }
+        const uint64_t m = __ballot(valid);
+        if (lane == 0) wave_count[wave] = (uint32_t)__builtin_popcountll(m);
+        __syncthreads();
+        uint32_t before = 0, all = 0;
+        for (uint32_t w = 0; w < blockDim.x / kWave; ++w) {
+            before += w < wave ? wave_count[w] : 0u;
+            all += wave_count[w];
+        }
+        __syncthreads();   // wave_count is rewritten by the next pass
+        const uint64_t idx = base + running + before + lanes_below(m);
+        if (valid && idx < end) {
+            taps_strategy st;
+            for (uint32_t a = 0; a < TAPS_MAX_AXES; ++a) {
+                st.log2_deg[a] = a < n_axes ? (uint8_t)expo[a] : 0;
+                st.pos[a] = a < n_axes ? (int8_t)pos[a] : (int8_t)-1;
+            }
+            out[idx] = st;
+            desc[idx] = D;
+            taps_acc c;
+            taps_acc_zero(c);
+            node_tensor(c, op, op.out, D, full, lp.lam);
+            for (uint32_t k = 0; k < op.n_in && k < TAPS_MAX_INPUTS; ++k)
+                node_tensor(c, op, op.in[k], D, full, lp.lam);
+            for (uint32_t k = 0; k < op.n_w && k < TAPS_MAX_WEIGHTS; ++k)
+                node_tensor(c, op, op.w[k], D, full, lp.lam);
+            node.t[idx] = (double)c.intra * lp.inv_n_bintra + (double)c.inter * lp.inv_n_binter;
+            node.vol[idx] = c.vol;
+            node.intra[idx] = c.intra;
+            node.inter[idx] = c.inter;
+            node.meta[idx] = taps_meta(0, c);
+        }
+        running += all;
+    }
+}
+
 // Bytes of one shard of tensor t under strategy s: each dimension's length
 // divided by its split degree, times the element size.
 __device__ inline uint64_t shard_bytes(const taps_op &op, const taps_tensor &t,
@@ -637,6 +709,16 @@ hipError_t taps_launch_edge_costs_sweep(const taps_edge_params *params, const ta
     hipLaunchKernelGGL(k_edge_costs_sweep, dim3(blocks_for(n_segs, TAPS_ROWS_PER_BLOCK)),
                        dim3(TAPS_TILE_COLS * TAPS_ROWS_PER_BLOCK), 0, stream, params, segs,
                        (uint32_t)n_segs, desc, lp, sw);
+    return hipGetLastError();
+}
+
+hipError_t taps_launch_build_strategies(const taps_op *ops, uint32_t n_ops,
+                                        const uint64_t *op_offsets, uint32_t allowed_cuts,
+                                        const taps_launch &lp, taps_strategy *out, taps_desc *desc,
+                                        taps_table node, hipStream_t stream) {
+    if (n_ops == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_build_strategies, dim3(n_ops), dim3(256), 0, stream, ops, op_offsets,
+                       allowed_cuts, lp, out, desc, node);
     return hipGetLastError();
 }
 

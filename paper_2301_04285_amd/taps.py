@@ -104,6 +104,10 @@ def load():
         L.taps_edge_costs_topology.restype = C.c_int
         L.taps_edge_costs_topology.argtypes = [P(GraphS), P(TopologyS), C.c_void_p, P(C.c_uint64),
                                                P(C.c_uint64), Table, C.c_uint64, C.c_void_p]
+        L.taps_build_tables.restype = C.c_int
+        L.taps_build_tables.argtypes = [P(GraphS), P(Cluster), P(Mesh), P(C.c_uint64), C.c_void_p,
+                                        C.c_uint64, Table, P(C.c_uint64), Table, C.c_uint64,
+                                        C.c_void_p]
         L.taps_node_costs.restype = C.c_int
         L.taps_node_costs.argtypes = [P(GraphS), P(Cluster), C.c_void_p, P(C.c_uint64), Table,
                                       C.c_void_p]
@@ -485,15 +489,54 @@ def _torch():
     return torch
 
 
+def taps_build_tables(graph, cluster, mesh=None, out: Optional["Tables"] = None, device="cuda",
+                      stream=None, size_only=False):
+    """The whole build in one call without a host synchronisation
+    (taps_build_tables): a Tables, or (op_offsets, edge_offsets) for a size
+    query.  ``out``: tables of an earlier build of the same graph to fill
+    again; otherwise they are allocated after a size query."""
+    g = _graph(graph)
+    cl = pack_cluster(cluster)
+    ms = pack_mesh(mesh) if mesh is not None else None
+    offs = np.zeros(g.n_ops + 1, dtype=np.uint64)
+    eoffs = np.zeros(g.n_edges + 1, dtype=np.uint64)
+    L = load()
+
+    def call(strat, s_cap, node, edge, e_cap):
+        return L.taps_build_tables(C.byref(g.struct), C.byref(cl), C.byref(ms) if ms else None,
+                                   _u64_array(offs), strat, s_cap, _table(node), _u64_array(eoffs),
+                                   _table(edge), e_cap, _stream(stream) if strat else None)
+    if out is None:
+        _check(call(None, 0, None, None, 0), "taps_build_tables")
+        if size_only:
+            return offs, eoffs
+        import torch
+        n_str, n_edge = int(offs[-1]), int(eoffs[-1])
+        out = Tables(offs, torch.empty((max(n_str, 1), STRATEGY_BYTES), dtype=torch.uint8,
+                                       device=device),
+                     alloc_table(n_str, device), eoffs, alloc_table(n_edge, device))
+    s_cap = min(int(out.strategies.shape[0]), *(int(v.numel()) for v in out.node.values()))
+    e_cap = min(int(v.numel()) for v in out.edge.values())
+    _check(call(C.c_void_p(out.strategies.data_ptr()), s_cap, out.node, out.edge, e_cap),
+           "taps_build_tables")
+    n_str, n_edge = int(offs[-1]), int(eoffs[-1])
+    return Tables(offs, out.strategies[:n_str], {k: v[:n_str] for k, v in out.node.items()}, eoffs,
+                  {k: v[:n_edge] for k, v in out.edge.items()})
+
+
 def build_tables(graph, cluster, device="cuda", stream=None, out: Optional[Tables] = None,
-                 shared: bool = False, mesh=None, topology=None) -> Tables:
+                 shared: bool = False, mesh=None, topology=None, fused: bool = True) -> Tables:
     """Enumeration, node table and edge table of one graph on one cluster.
     ``out``: tables of an earlier build of the same graph to fill again;
     ``shared``: identical edge tables computed once (taps_edge_costs_shared);
     ``mesh``: the strategy space of a fixed device mesh (sizes, innermost
     first) instead of every device matrix; ``topology``: the link classes of a
-    workloads.Topology on the cluster's devices instead of its two."""
+    workloads.Topology on the cluster's devices instead of its two.  Plain and
+    mesh builds go through the single call taps_build_tables unless
+    ``fused`` is False (then the three separate calls run)."""
     g = _graph(graph)
+    if fused and not shared and topology is None:
+        return taps_build_tables(g, cluster, mesh=mesh, out=out, device=device, stream=stream)
     offs, strat = taps_enumerate_strategies(g, cluster, device=device, stream=stream,
                                             out=out.strategies if out is not None else None,
                                             mesh=mesh)

@@ -18,7 +18,8 @@ def lib():
 
 def test_exports_every_declared_symbol(lib):
     declared = T.declared_symbols()
-    assert declared == sorted(["taps_enumerate_strategies", "taps_enumerate_strategies_mesh",
+    assert declared == sorted(["taps_build_tables",
+                               "taps_enumerate_strategies", "taps_enumerate_strategies_mesh",
                                "taps_node_costs", "taps_edge_costs", "taps_node_costs_topology",
                                "taps_edge_costs_topology",
                                "taps_edge_costs_shared", "taps_edge_costs_backward",
@@ -299,3 +300,47 @@ def test_device_errors_are_reported(lib):
         pytest.skip("a GPU is present")
     assert _enum(lib, W.mlp2(), W.Cluster(2, 2, 10, 1)) == T.ERR_DEVICE
     assert "hip" in T.last_error().lower()
+
+
+def test_build_size_query_counts_like_the_oracle(lib, oracle_lib):
+    """taps_build_tables sizes every table on the host (an exact count of the
+    enumeration filter, no GPU): its offsets equal the oracle's strategy counts
+    and the row-major edge sizes, with and without a fixed mesh."""
+    import random
+    rng = random.Random(808)
+    checked = 0
+    for trial in range(60):
+        g = W.random_graph(rng, rng.randint(1, 6), max_axes=6, max_rank=4, len_pow_range=(0, 9))
+        n = rng.randint(0, 8)
+        L = 1 << rng.randint(0, n)
+        cl = W.Cluster((1 << n) // L, L, 600 * W.GB, 100 * W.GB)
+        mesh = None
+        if rng.random() < 0.5:
+            mesh, left = [], n
+            while left:
+                e = rng.randint(1, min(3, left))
+                mesh.append(1 << e)
+                left -= e
+        counts = [len(oracle_lib.enumerate_strategies(op, cl.devices) if mesh is None else
+                      oracle_lib.enumerate_strategies_mesh(op, mesh)) for op in g.ops]
+        try:
+            offs, eoffs = T.taps_build_tables(g, cl, mesh=mesh, size_only=True)
+        except T.TapsError as ex:
+            assert ex.status == T.ERR_NO_STRATEGY and 0 in counts
+            continue
+        assert list(np.diff(offs)) == counts, (trial, mesh)
+        assert list(np.diff(eoffs)) == [counts[e.src] * counts[e.dst] for e in g.edges]
+        checked += 1
+    # the workloads (every view and mesh)
+    for k in W.ALL_CONFIGS:
+        w = W.config(k)
+        for _, cl in w.clusters:
+            for mesh in (None, W.physical_mesh(k, cl)):
+                offs, _ = T.taps_build_tables(w.graph, cl, mesh=mesh, size_only=True)
+                got = np.diff(offs)
+                for op_i in range(min(len(w.graph.ops), 20)):
+                    op = w.graph.ops[op_i]
+                    ref = (oracle_lib.enumerate_strategies(op, cl.devices) if mesh is None else
+                           oracle_lib.enumerate_strategies_mesh(op, mesh))
+                    assert got[op_i] == len(ref)
+    assert checked > 30

@@ -333,6 +333,63 @@ def test_link_class_tables(T):
         assert _same_tables(a.edge, b.edge) and _same_tables(a.node, b.node), w.name
 
 
+def test_fused_build_equals_separate_calls(T):
+    """taps_build_tables (host-sized, one call, no synchronisation) writes exactly
+    what taps_enumerate_strategies(_mesh) + taps_node_costs + taps_edge_costs
+    write: every configuration (both 32-device views, every bandwidth), the
+    workloads on their meshes, and random graphs on random meshes; a second build
+    into the same tables, queued right behind the first, gives the same bits."""
+    import torch
+    cases = []
+    for k in W.ALL_CONFIGS:
+        w = W.config(k)
+        for _, cl in w.clusters:
+            cases.append((w.graph, cl, None))
+        cases.append((w.graph, w.clusters[0][1], W.physical_mesh(k, w.clusters[0][1])))
+    rng = random.Random(616)
+    for g, cl in _random_cases(616, 16):
+        cases.append((g, cl, _random_mesh(rng, cl.devices.bit_length() - 1) if rng.random() < 0.5
+                      else None))
+    for g, cl, mesh in cases:
+        name = f"{len(g.ops)} ops N={cl.devices} L={cl.devices_per_node} mesh={mesh}"
+        say(f"[gpu] fused build {name}")
+        try:
+            a = T.build_tables(g, cl, mesh=mesh, fused=False)
+        except T.TapsError as ex:
+            assert ex.status == T.ERR_NO_STRATEGY
+            with pytest.raises(T.TapsError):
+                T.build_tables(g, cl, mesh=mesh)
+            continue
+        b = T.build_tables(g, cl, mesh=mesh)
+        T.build_tables(g, cl, mesh=mesh, out=b)   # queued behind the first
+        torch.cuda.synchronize()
+        assert list(a.op_offsets) == list(b.op_offsets) and list(a.edge_offsets) == list(b.edge_offsets)
+        assert torch.equal(a.strategies, b.strategies), name
+        assert _same_tables(a.node, b.node) and _same_tables(a.edge, b.edge), name
+
+
+def test_fused_build_capacity_and_errors(T):
+    """Capacity and argument errors are reported before any GPU work and leave the
+    outputs untouched."""
+    import torch
+    w = W.config(2)
+    cl = w.clusters[0][1]
+    offs, eoffs = T.taps_build_tables(w.graph, cl, size_only=True)
+    n_s, n_e = int(offs[-1]), int(eoffs[-1])
+    for short_s, short_e in ((1, 0), (0, 1)):
+        out = T.Tables(offs, torch.full((n_s - short_s, T.STRATEGY_BYTES), 7, dtype=torch.uint8,
+                                        device="cuda"),
+                       T.alloc_table(n_s - short_s), eoffs, T.alloc_table(n_e - short_e))
+        for v in (*out.node.values(), *out.edge.values()):
+            _signed(v).fill_(5)
+        with pytest.raises(T.TapsError) as ex:
+            T.taps_build_tables(w.graph, cl, out=out)
+        assert ex.value.status == T.ERR_CAPACITY
+        torch.cuda.synchronize()
+        assert bool((out.strategies == 7).all())
+        assert all(bool((_signed(v) == 5).all()) for v in (*out.node.values(), *out.edge.values()))
+
+
 def test_empty_graph_and_no_edges(T):
     cl = W.Cluster(2, 2, 10, 1)
     tabs = T.build_tables(W.Graph(), cl)
