@@ -245,14 +245,16 @@ __global__ __launch_bounds__(256) void k_node_costs(const taps_op *__restrict__ 
 // The operator's strategies go to [op_offsets[k], op_offsets[k+1]), which the
 // host sized with an exact count of the same filter; nothing is written
 // outside that range.
-__global__ __launch_bounds__(256) void k_build_strategies(const taps_op *__restrict__ ops,
+constexpr uint32_t kBuildThreads = 256;   // candidates per pass of k_build_strategies (1024: slower)
+
+__global__ __launch_bounds__(kBuildThreads) void k_build_strategies(const taps_op *__restrict__ ops,
                                                           const uint64_t *__restrict__ op_offsets,
                                                           uint32_t allowed_cuts, taps_launch lp,
                                                           taps_strategy *__restrict__ out,
                                                           taps_desc *__restrict__ desc,
                                                           taps_table node) {
     __shared__ uint32_t W[9 * 9 * 9];
-    __shared__ uint32_t wave_count[4];
+    __shared__ uint32_t wave_count[kBuildThreads / kWave];
     const uint32_t tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
     for (uint32_t x = tid; x < 9u * 9u * 9u; x += blockDim.x) W[x] = kCompletions.v[x];
     __syncthreads();
@@ -717,8 +719,8 @@ hipError_t taps_launch_build_strategies(const taps_op *ops, uint32_t n_ops,
                                         const taps_launch &lp, taps_strategy *out, taps_desc *desc,
                                         taps_table node, hipStream_t stream) {
     if (n_ops == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_build_strategies, dim3(n_ops), dim3(256), 0, stream, ops, op_offsets,
-                       allowed_cuts, lp, out, desc, node);
+    hipLaunchKernelGGL(k_build_strategies, dim3(n_ops), dim3(kBuildThreads), 0, stream, ops,
+                       op_offsets, allowed_cuts, lp, out, desc, node);
     return hipGetLastError();
 }
 

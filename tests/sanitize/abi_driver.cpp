@@ -135,9 +135,62 @@ int main() {
     expect(taps_set_edge_kernel_events((void *)256, nullptr), TAPS_ERR_ARG, "one event");
     expect(taps_set_edge_kernel_events(nullptr, nullptr), TAPS_OK, "no events");
 
+    // the single-call build sizes everything on the host: a size query needs no GPU
+    std::vector<uint64_t> bo(ops.size() + 1, 0), beo(edges.size() + 1, 0);
+    expect(taps_build_tables(&g, &cl, nullptr, bo.data(), nullptr, 0, none, beo.data(), none, 0,
+                             nullptr),
+           TAPS_OK, "build size query");
+    if (bo != offs || beo[1] != 81 || beo[2] != 162) ++failures;
+    taps_mesh mesh = {2, {2, 2}};
+    expect(taps_build_tables(&g, &cl, &mesh, bo.data(), nullptr, 0, none, beo.data(), none, 0,
+                           nullptr),
+           TAPS_OK, "build size query on a mesh");
+    if (bo != offs) ++failures;
+    mesh = {1, {4}};   // one axis split 4 ways: 3 strategies per matmul
+    expect(taps_build_tables(&g, &cl, &mesh, bo.data(), nullptr, 0, none, beo.data(), none, 0,
+                             nullptr),
+           TAPS_OK, "build size query on a 1-D mesh");
+    if (bo[1] != 3 || bo[3] != 9 || beo[2] != 18) ++failures;
+    for (taps_mesh badm : {taps_mesh{2, {4, 2}}, taps_mesh{1, {3}}, taps_mesh{9, {2}}})
+        expect(taps_build_tables(&g, &cl, &badm, bo.data(), nullptr, 0, none, beo.data(), none, 0,
+                                 nullptr),
+               TAPS_ERR_TOPOLOGY, "bad mesh");
+    std::vector<uint64_t> bsent(bo.size(), 77);
+    expect(taps_build_tables(&g, &cl, nullptr, bsent.data(), (taps_strategy *)256, 26, fake,
+                             beo.data(), fake, 1000, nullptr),
+           TAPS_ERR_CAPACITY, "build strategy capacity");
+    expect(taps_build_tables(&g, &cl, nullptr, bsent.data(), (taps_strategy *)256, 27, fake,
+                             beo.data(), fake, 161, nullptr),
+           TAPS_ERR_CAPACITY, "build edge capacity");
+    expect(taps_build_tables(&g, &cl, nullptr, bsent.data(), (taps_strategy *)256, 27, partial,
+                             beo.data(), fake, 162, nullptr),
+           TAPS_ERR_ARG, "build partial table");
+    for (uint64_t v : bsent)
+        if (v != 77) ++failures;
+    std::vector<taps_op> tiny = {matmul(1, 1, 1)};   // nothing divides: no strategy on 4 devices
+    taps_graph gt = {1, 0, tiny.data(), nullptr};
+    expect(taps_build_tables(&gt, &cl, nullptr, bo.data(), nullptr, 0, none, beo.data(), none, 0,
+                             nullptr),
+           TAPS_ERR_NO_STRATEGY, "build without a strategy");
+    // link classes: validation before any GPU work
+    taps_topology topo = {3, {2, 2, 4}, {400000000000ull, 100000000000ull, 25000000000ull}, 0};
+    expect(taps_edge_costs_topology(&g, &topo, nullptr, offs.data(), eo.data(), none, 0, nullptr),
+           TAPS_OK, "topology size query");
+    topo.domain[1] = 1;
+    expect(taps_edge_costs_topology(&g, &topo, nullptr, offs.data(), eo.data(), none, 0, nullptr),
+           TAPS_ERR_TOPOLOGY, "decreasing domains");
+    topo = {2, {2, 4}, {400000000000ull, 100000000000ull}, 7};
+    expect(taps_edge_costs_topology(&g, &topo, nullptr, offs.data(), eo.data(), none, 0, nullptr),
+           TAPS_ERR_TOPOLOGY, "AllToAll bandwidth in no round ratio");
+    expect(taps_node_costs_topology(&g, nullptr, nullptr, offs.data(), fake, nullptr), TAPS_ERR_ARG,
+           "null topology");
+
     // the device is reached: without a GPU every such call reports it
     expect(taps_enumerate_strategies(&g, &cl, offs.data(), nullptr, 0, nullptr), TAPS_ERR_DEVICE,
            "enumerate without a device");
+    expect(taps_build_tables(&g, &cl, nullptr, bo.data(), (taps_strategy *)256, 27, fake,
+                             beo.data(), fake, 162, nullptr),
+           TAPS_ERR_DEVICE, "build without a device");
     std::printf("abi driver: %d failures\n", failures);
     return failures ? 1 : 0;
 }

@@ -95,6 +95,35 @@ int main(void) {
                 return 6;
             checked += 1;
         }
+        /* fixed meshes and link classes */
+        if (n > 0) {
+            int64_t mesh[OR_MAX_DEV];
+            int k = 0, rest = n;
+            while (rest > 0) {
+                const int e = 1 + (int)rnd((uint32_t)(rest < 3 ? rest : 3));
+                mesh[k++] = (int64_t)1 << e;
+                rest -= e;
+            }
+            if (or_enumerate_mesh(&src, mesh, k, (int)rnd(2), ss, CAP) < 0) return 8;
+        }
+        if (ms && md) {
+            or_topology topo;
+            memset(&topo, 0, sizeof topo);
+            topo.n_classes = 1 + (int)rnd(OR_MAX_CLASSES);
+            int64_t size = 1;
+            for (int c = 0; c < topo.n_classes; ++c) {
+                if (c == topo.n_classes - 1) size = N;
+                else while (size < N && rnd(2)) size *= 2;
+                topo.domain[c] = size;
+                topo.bw[c] = 1000000000ull * (1 + rnd(4)) * 25;
+            }
+            topo.bw_a2a = rnd(2) ? 0 : 150000000000ull;
+            if (or_edge_table_topo(&src, ss, ms, &dst, 0, sd, md, N, &topo, tab) != ms * md ||
+                or_node_table_topo(&src, ss, ms, N, &topo, rec) != ms) {
+                fprintf(stderr, "topology tables failed\n");
+                return 9;
+            }
+        }
         /* collective group counts on a random device matrix and map */
         int64_t D[OR_MAX_DEV];
         int h = 0, left = n;
