@@ -222,14 +222,22 @@ taps_status taps_enumerate_strategies_mesh(const taps_graph *graph, const taps_c
  *                 edge_capacity records, layout as taps_edge_costs.
  *   strategies NULL and every table array NULL: size query (host only).  The
  *   edge arrays may be NULL when the graph has no edge entries.
+ *   flags         0, or TAPS_BUILD_SHARED: edges described alike (as for
+ *                 taps_edge_costs_shared) share one computed table, copied to
+ *                 the others; the strategies here are the library's own, so the
+ *                 grouping needs no device comparison and the call still does
+ *                 not synchronise.  The tables are the same either way.
  * TAPS_ERR_NO_STRATEGY, TAPS_ERR_CAPACITY (either capacity), TAPS_ERR_TOPOLOGY
- * (cluster or mesh) and TAPS_ERR_ARG as the separate calls, all before any GPU
- * work; outputs are valid after a stream synchronisation. */
+ * (cluster or mesh) and TAPS_ERR_ARG (also for unknown flags) as the separate
+ * calls, all before any GPU work; outputs are valid after a stream
+ * synchronisation.  The events of taps_set_edge_kernel_events bracket the
+ * edge-table kernel and, when shared, the copies after it. */
+#define TAPS_BUILD_SHARED 1u
 taps_status taps_build_tables(const taps_graph *graph, const taps_cluster *cluster,
                               const taps_mesh *mesh, uint64_t *op_offsets,
                               taps_strategy *strategies, uint64_t strategy_capacity, taps_table node,
                               uint64_t *edge_offsets, taps_table edge, uint64_t edge_capacity,
-                              void *stream);
+                              uint32_t flags, void *stream);
 
 /* Intra-operator cost of every strategy (Eq. 5-8 generalised to any
  * operator: one ring AllReduce per tensor that lacks some split axis -- the

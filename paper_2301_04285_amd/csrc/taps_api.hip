@@ -349,6 +349,35 @@ taps_status share_edges(const taps_graph *g, const uint64_t *op_offsets,
     return TAPS_OK;
 }
 
+// Copy tasks of shared tables: every TAPS_COPY_CHUNK entries of a computed
+// table (rep[e] == e with members) go to at most TAPS_COPY_DSTS of the tables
+// that share it per task.
+void plan_copies(const std::vector<uint64_t> &eoff, const std::vector<uint32_t> &rep,
+                 std::vector<taps_copy_task> &copies, std::vector<uint64_t> &dst_list) {
+    const uint32_t n_edges = (uint32_t)rep.size();
+    std::vector<std::vector<uint32_t>> members(n_edges);
+    for (uint32_t e = 0; e < n_edges; ++e)
+        if (rep[e] != e) members[rep[e]].push_back(e);
+    for (uint32_t r = 0; r < n_edges; ++r) {
+        if (members[r].empty()) continue;
+        const uint32_t begin = (uint32_t)dst_list.size();
+        for (uint32_t m : members[r]) dst_list.push_back(eoff[m]);
+        const uint64_t size = eoff[r + 1] - eoff[r];
+        const uint32_t n_dst = (uint32_t)members[r].size();
+        for (uint64_t k = 0; k < size; k += TAPS_COPY_CHUNK)
+            for (uint32_t m = 0; m < n_dst; m += TAPS_COPY_DSTS) {
+                taps_copy_task c;
+                c.src = eoff[r] + k;
+                c.offset = k;
+                c.count = (uint32_t)(size - k < TAPS_COPY_CHUNK ? size - k : TAPS_COPY_CHUNK);
+                c.dst_begin = begin + m;
+                c.n_dst = n_dst - m < TAPS_COPY_DSTS ? n_dst - m : TAPS_COPY_DSTS;
+                c.pad = 0;
+                copies.push_back(c);
+            }
+    }
+}
+
 // Edge tables of one graph at n_points bandwidth points (clusters that differ
 // only in their bandwidths), table k in outs[k]; outs NULL or every table's
 // arrays NULL: size query.
@@ -423,29 +452,7 @@ taps_status edge_costs(const taps_graph *graph, const taps_cluster *clusters, ui
     // shared tables: every chunk of a computed table is stored into each table sharing it
     std::vector<uint64_t> dst_list;
     std::vector<taps_copy_task> copies;
-    {
-        std::vector<std::vector<uint32_t>> members(n_edges);
-        for (uint32_t e = 0; e < n_edges; ++e)
-            if (rep[e] != e) members[rep[e]].push_back(e);
-        for (uint32_t r = 0; r < n_edges; ++r) {
-            if (members[r].empty()) continue;
-            const uint32_t begin = (uint32_t)dst_list.size();
-            for (uint32_t m : members[r]) dst_list.push_back(eoff[m]);
-            const uint64_t size = eoff[r + 1] - eoff[r];
-            const uint32_t n_dst = (uint32_t)members[r].size();
-            for (uint64_t k = 0; k < size; k += TAPS_COPY_CHUNK)
-                for (uint32_t m = 0; m < n_dst; m += TAPS_COPY_DSTS) {
-                    taps_copy_task c;
-                    c.src = eoff[r] + k;
-                    c.offset = k;
-                    c.count = (uint32_t)(size - k < TAPS_COPY_CHUNK ? size - k : TAPS_COPY_CHUNK);
-                    c.dst_begin = begin + m;
-                    c.n_dst = n_dst - m < TAPS_COPY_DSTS ? n_dst - m : TAPS_COPY_DSTS;
-                    c.pad = 0;
-                    copies.push_back(c);
-                }
-        }
-    }
+    plan_copies(eoff, rep, copies, dst_list);
     if (copies.size() > 0x7FFFFFFFull) return fail(TAPS_ERR_ARG, "too many table copies");
     scratch sc(stream);
     const uint64_t total = op_offsets[n_ops];
@@ -794,8 +801,9 @@ taps_status taps_build_tables(const taps_graph *graph, const taps_cluster *clust
                               const taps_mesh *mesh, uint64_t *op_offsets,
                               taps_strategy *strategies, uint64_t strategy_capacity, taps_table node,
                               uint64_t *edge_offsets, taps_table edge, uint64_t edge_capacity,
-                              void *stream_) {
+                              uint32_t flags, void *stream_) {
     g_last_error.clear();
+    if (flags & ~TAPS_BUILD_SHARED) return fail(TAPS_ERR_ARG, "unknown flags 0x%x", flags);
     taps_launch lp;
     taps_status st = check_cluster(cluster, &lp);
     if (st == TAPS_OK) st = check_graph(graph, true);
@@ -816,16 +824,32 @@ taps_status taps_build_tables(const taps_graph *graph, const taps_cluster *clust
         offs[k + 1] = offs[k] + c;
     }
     if (offs[n_ops] > 0xFFFFFFFFull) return fail(TAPS_ERR_ARG, "more than 2^32 strategies");
+    // shared tables: edges described alike share one table -- their operators'
+    // strategies are the same function of the same descriptions here, so no
+    // device comparison is needed
+    std::vector<uint32_t> rep(n_edges);
+    std::iota(rep.begin(), rep.end(), 0u);
+    if (flags & TAPS_BUILD_SHARED) {
+        std::map<std::vector<int64_t>, uint32_t> first;
+        for (uint32_t e = 0; e < n_edges; ++e) rep[e] = first.emplace(edge_key(graph, e), e).first->second;
+    }
     std::vector<uint64_t> eoff(n_edges + 1, 0), segs(n_edges + 1, 0);
+    uint64_t all_segs = 0;
     for (uint32_t e = 0; e < n_edges; ++e) {
         const taps_edge &E = graph->edges[e];
         const uint64_t ns = offs[E.src_op + 1] - offs[E.src_op];
         const uint64_t nd = offs[E.dst_op + 1] - offs[E.dst_op];
+        const uint64_t per_row = (nd + TAPS_TILE_COLS * TAPS_SEG_TILES - 1) /
+                                 (TAPS_TILE_COLS * TAPS_SEG_TILES);
         eoff[e + 1] = eoff[e] + ns * nd;
-        segs[e + 1] = segs[e] + ns * ((nd + TAPS_TILE_COLS * TAPS_SEG_TILES - 1) /
-                                      (TAPS_TILE_COLS * TAPS_SEG_TILES));
+        segs[e + 1] = segs[e] + (rep[e] == e ? ns * per_row : 0);
+        all_segs += ns * per_row;
     }
-    if (segs[n_edges] >= 0x7FFFFFFFull) return fail(TAPS_ERR_ARG, "more than 2^31 row segments");
+    if (all_segs >= 0x7FFFFFFFull) return fail(TAPS_ERR_ARG, "more than 2^31 row segments");
+    std::vector<uint64_t> dst_list;
+    std::vector<taps_copy_task> copies;
+    plan_copies(eoff, rep, copies, dst_list);
+    if (copies.size() > 0x7FFFFFFFull) return fail(TAPS_ERR_ARG, "too many table copies");
     // a size query passes no array; a build passes the strategy and node arrays, and
     // the edge arrays unless there are no edge entries (then they are not read)
     const bool none_s = !strategies && !node.t && !node.vol && !node.intra && !node.inter &&
@@ -854,7 +878,9 @@ taps_status taps_build_tables(const taps_graph *graph, const taps_cluster *clust
                           {graph->edges, sizeof(taps_edge) * n_edges, 0},
                           {offs.data(), sizeof(uint64_t) * (n_ops + 1), 0},
                           {eoff.data(), sizeof(uint64_t) * (n_edges + 1), 0},
-                          {segs.data(), sizeof(uint64_t) * (n_edges + 1), 0}};
+                          {segs.data(), sizeof(uint64_t) * (n_edges + 1), 0},
+                          {copies.data(), sizeof(taps_copy_task) * copies.size(), 0},
+                          {dst_list.data(), sizeof(uint64_t) * dst_list.size(), 0}};
     void *dev = nullptr;
     if ((st = upload(ch, &dev, stream)) != TAPS_OK) return st;
     sc.adopt(dev);
@@ -880,6 +906,9 @@ taps_status taps_build_tables(const taps_graph *graph, const taps_cluster *clust
         if (err == hipSuccess && before) err = hipEventRecord(before, stream);
         if (err == hipSuccess)
             err = taps_launch_edge_costs(d_params, d_segs, n_segs, d_desc, lp, edge, stream);
+        if (err == hipSuccess)
+            err = taps_launch_copy_tables(at<taps_copy_task>(dev, ch[5]), (uint32_t)copies.size(),
+                                          at<uint64_t>(dev, ch[6]), edge, stream);
         if (err == hipSuccess && after) err = hipEventRecord(after, stream);
     }
     if (err != hipSuccess) return hip_fail(err, "build");

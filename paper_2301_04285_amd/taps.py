@@ -107,7 +107,7 @@ def load():
         L.taps_build_tables.restype = C.c_int
         L.taps_build_tables.argtypes = [P(GraphS), P(Cluster), P(Mesh), P(C.c_uint64), C.c_void_p,
                                         C.c_uint64, Table, P(C.c_uint64), Table, C.c_uint64,
-                                        C.c_void_p]
+                                        C.c_uint32, C.c_void_p]
         L.taps_node_costs.restype = C.c_int
         L.taps_node_costs.argtypes = [P(GraphS), P(Cluster), C.c_void_p, P(C.c_uint64), Table,
                                       C.c_void_p]
@@ -489,12 +489,16 @@ def _torch():
     return torch
 
 
+BUILD_SHARED = 1
+
+
 def taps_build_tables(graph, cluster, mesh=None, out: Optional["Tables"] = None, device="cuda",
-                      stream=None, size_only=False):
+                      stream=None, size_only=False, shared=False):
     """The whole build in one call without a host synchronisation
     (taps_build_tables): a Tables, or (op_offsets, edge_offsets) for a size
     query.  ``out``: tables of an earlier build of the same graph to fill
-    again; otherwise they are allocated after a size query."""
+    again; otherwise they are allocated after a size query.  ``shared``:
+    identical edge tables computed once (TAPS_BUILD_SHARED)."""
     g = _graph(graph)
     cl = pack_cluster(cluster)
     ms = pack_mesh(mesh) if mesh is not None else None
@@ -505,7 +509,8 @@ def taps_build_tables(graph, cluster, mesh=None, out: Optional["Tables"] = None,
     def call(strat, s_cap, node, edge, e_cap):
         return L.taps_build_tables(C.byref(g.struct), C.byref(cl), C.byref(ms) if ms else None,
                                    _u64_array(offs), strat, s_cap, _table(node), _u64_array(eoffs),
-                                   _table(edge), e_cap, _stream(stream) if strat else None)
+                                   _table(edge), e_cap, BUILD_SHARED if shared else 0,
+                                   _stream(stream) if strat else None)
     if out is None:
         _check(call(None, 0, None, None, 0), "taps_build_tables")
         if size_only:
@@ -531,12 +536,13 @@ def build_tables(graph, cluster, device="cuda", stream=None, out: Optional[Table
     ``shared``: identical edge tables computed once (taps_edge_costs_shared);
     ``mesh``: the strategy space of a fixed device mesh (sizes, innermost
     first) instead of every device matrix; ``topology``: the link classes of a
-    workloads.Topology on the cluster's devices instead of its two.  Plain and
-    mesh builds go through the single call taps_build_tables unless
-    ``fused`` is False (then the three separate calls run)."""
+    workloads.Topology on the cluster's devices instead of its two.  Builds
+    with two link classes go through the single call taps_build_tables unless
+    ``fused`` is False (then the separate calls run)."""
     g = _graph(graph)
-    if fused and not shared and topology is None:
-        return taps_build_tables(g, cluster, mesh=mesh, out=out, device=device, stream=stream)
+    if fused and topology is None:
+        return taps_build_tables(g, cluster, mesh=mesh, out=out, device=device, stream=stream,
+                                 shared=shared)
     offs, strat = taps_enumerate_strategies(g, cluster, device=device, stream=stream,
                                             out=out.strategies if out is not None else None,
                                             mesh=mesh)

@@ -137,39 +137,45 @@ int main() {
 
     // the single-call build sizes everything on the host: a size query needs no GPU
     std::vector<uint64_t> bo(ops.size() + 1, 0), beo(edges.size() + 1, 0);
-    expect(taps_build_tables(&g, &cl, nullptr, bo.data(), nullptr, 0, none, beo.data(), none, 0,
+    expect(taps_build_tables(&g, &cl, nullptr, bo.data(), nullptr, 0, none, beo.data(), none, 0, 0,
                              nullptr),
            TAPS_OK, "build size query");
     if (bo != offs || beo[1] != 81 || beo[2] != 162) ++failures;
+    expect(taps_build_tables(&g, &cl, nullptr, bo.data(), nullptr, 0, none, beo.data(), none, 0,
+                             TAPS_BUILD_SHARED, nullptr),
+           TAPS_OK, "shared build size query");
+    expect(taps_build_tables(&g, &cl, nullptr, bo.data(), nullptr, 0, none, beo.data(), none, 0, 6,
+                             nullptr),
+           TAPS_ERR_ARG, "unknown build flags");
     taps_mesh mesh = {2, {2, 2}};
-    expect(taps_build_tables(&g, &cl, &mesh, bo.data(), nullptr, 0, none, beo.data(), none, 0,
-                           nullptr),
+    expect(taps_build_tables(&g, &cl, &mesh, bo.data(), nullptr, 0, none, beo.data(), none, 0, 0,
+                             nullptr),
            TAPS_OK, "build size query on a mesh");
     if (bo != offs) ++failures;
     mesh = {1, {4}};   // one axis split 4 ways: 3 strategies per matmul
-    expect(taps_build_tables(&g, &cl, &mesh, bo.data(), nullptr, 0, none, beo.data(), none, 0,
+    expect(taps_build_tables(&g, &cl, &mesh, bo.data(), nullptr, 0, none, beo.data(), none, 0, 0,
                              nullptr),
            TAPS_OK, "build size query on a 1-D mesh");
     if (bo[1] != 3 || bo[3] != 9 || beo[2] != 18) ++failures;
     for (taps_mesh badm : {taps_mesh{2, {4, 2}}, taps_mesh{1, {3}}, taps_mesh{9, {2}}})
-        expect(taps_build_tables(&g, &cl, &badm, bo.data(), nullptr, 0, none, beo.data(), none, 0,
-                                 nullptr),
+        expect(taps_build_tables(&g, &cl, &badm, bo.data(), nullptr, 0, none, beo.data(), none, 0, 0,
+                             nullptr),
                TAPS_ERR_TOPOLOGY, "bad mesh");
     std::vector<uint64_t> bsent(bo.size(), 77);
     expect(taps_build_tables(&g, &cl, nullptr, bsent.data(), (taps_strategy *)256, 26, fake,
-                             beo.data(), fake, 1000, nullptr),
+                             beo.data(), fake, 1000, 0, nullptr),
            TAPS_ERR_CAPACITY, "build strategy capacity");
     expect(taps_build_tables(&g, &cl, nullptr, bsent.data(), (taps_strategy *)256, 27, fake,
-                             beo.data(), fake, 161, nullptr),
+                             beo.data(), fake, 161, 0, nullptr),
            TAPS_ERR_CAPACITY, "build edge capacity");
     expect(taps_build_tables(&g, &cl, nullptr, bsent.data(), (taps_strategy *)256, 27, partial,
-                             beo.data(), fake, 162, nullptr),
+                             beo.data(), fake, 162, 0, nullptr),
            TAPS_ERR_ARG, "build partial table");
     for (uint64_t v : bsent)
         if (v != 77) ++failures;
     std::vector<taps_op> tiny = {matmul(1, 1, 1)};   // nothing divides: no strategy on 4 devices
     taps_graph gt = {1, 0, tiny.data(), nullptr};
-    expect(taps_build_tables(&gt, &cl, nullptr, bo.data(), nullptr, 0, none, beo.data(), none, 0,
+    expect(taps_build_tables(&gt, &cl, nullptr, bo.data(), nullptr, 0, none, beo.data(), none, 0, 0,
                              nullptr),
            TAPS_ERR_NO_STRATEGY, "build without a strategy");
     // link classes: validation before any GPU work
@@ -189,7 +195,7 @@ int main() {
     expect(taps_enumerate_strategies(&g, &cl, offs.data(), nullptr, 0, nullptr), TAPS_ERR_DEVICE,
            "enumerate without a device");
     expect(taps_build_tables(&g, &cl, nullptr, bo.data(), (taps_strategy *)256, 27, fake,
-                             beo.data(), fake, 162, nullptr),
+                             beo.data(), fake, 162, 0, nullptr),
            TAPS_ERR_DEVICE, "build without a device");
     std::printf("abi driver: %d failures\n", failures);
     return failures ? 1 : 0;

@@ -336,9 +336,10 @@ def test_link_class_tables(T):
 def test_fused_build_equals_separate_calls(T):
     """taps_build_tables (host-sized, one call, no synchronisation) writes exactly
     what taps_enumerate_strategies(_mesh) + taps_node_costs + taps_edge_costs
-    write: every configuration (both 32-device views, every bandwidth), the
-    workloads on their meshes, and random graphs on random meshes; a second build
-    into the same tables, queued right behind the first, gives the same bits."""
+    write, with and without TAPS_BUILD_SHARED: every configuration (both
+    32-device views, every bandwidth), the workloads on their meshes, and random
+    graphs on random meshes; a second build into the same tables, queued right
+    behind the first, gives the same bits."""
     import torch
     cases = []
     for k in W.ALL_CONFIGS:
@@ -362,10 +363,12 @@ def test_fused_build_equals_separate_calls(T):
             continue
         b = T.build_tables(g, cl, mesh=mesh)
         T.build_tables(g, cl, mesh=mesh, out=b)   # queued behind the first
+        c = T.build_tables(g, cl, mesh=mesh, shared=True)   # identical tables computed once
         torch.cuda.synchronize()
         assert list(a.op_offsets) == list(b.op_offsets) and list(a.edge_offsets) == list(b.edge_offsets)
         assert torch.equal(a.strategies, b.strategies), name
         assert _same_tables(a.node, b.node) and _same_tables(a.edge, b.edge), name
+        assert _same_tables(a.edge, c.edge) and _same_tables(a.node, c.node), name
 
 
 def test_fused_build_capacity_and_errors(T):
