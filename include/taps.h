@@ -54,8 +54,9 @@
  *     pointer of the caller after the call returns.
  *   - Kernels are asynchronous on `stream` (a hipStream_t; NULL = the null
  *     stream): the tables are complete once that stream has been
- *     synchronised.  taps_enumerate_strategies synchronises `stream` once to
- *     read the per-operator counts back.
+ *     synchronised.  Every size (strategies per operator, entries per edge)
+ *     is computed on the host, so only taps_edge_costs_shared synchronises
+ *     (to read back a device comparison of strategy ranges).
  *   - Calls on distinct outputs may run concurrently from several threads.
  *
  * Errors
@@ -181,8 +182,13 @@ typedef struct {
  *               descending -- the order of Table 3).  NULL: only op_offsets
  *               is written (size query).
  * Strategies whose degree does not divide its axis are left out; with N = 1
- * the single strategy splits nothing.  TAPS_ERR_NO_STRATEGY if an operator
- * has none, TAPS_ERR_CAPACITY if op_offsets[n_ops] > capacity. */
+ * the single strategy splits nothing.  The counts come from an exact count of
+ * that filter on the host (ordered runs of distinct partitionable axes over
+ * the n levels, each at most as wide as its length allows); the strategies
+ * themselves are enumerated on the device, one workgroup per operator, and
+ * the call does not synchronise.  TAPS_ERR_NO_STRATEGY if an operator has
+ * none, TAPS_ERR_CAPACITY if op_offsets[n_ops] > capacity (op_offsets is
+ * still written, the strategies are not). */
 taps_status taps_enumerate_strategies(const taps_graph *graph, const taps_cluster *cluster,
                                       uint64_t *op_offsets, taps_strategy *strategies,
                                       uint64_t capacity, void *stream);

@@ -42,24 +42,6 @@ taps_status hip_fail(hipError_t err, const char *what) {
 
 bool pow2(uint64_t v) { return v && !(v & (v - 1)); }
 
-// Strategies of an operator with p partitionable axes on 2^n devices before
-// the divisibility filter: sum_{i=1}^{min(p,n)} i! C(p,i) C(n-1,i-1); one
-// (nothing split) for n = 0.  Sizes the enumeration grid.
-uint64_t candidate_count(uint32_t p, uint32_t n) {
-    if (n == 0) return 1;
-    auto binom = [](uint64_t a, uint64_t b) {
-        uint64_t r = 1;
-        for (uint64_t x = 1; x <= b; ++x) r = r * (a - b + x) / x;
-        return b > a ? 0 : r;
-    };
-    uint64_t tot = 0, fact = 1;
-    for (uint32_t i = 1; i <= p && i <= n; ++i) {
-        fact *= i;
-        tot += fact * binom(p, i) * binom(n - 1, i - 1);
-    }
-    return tot;
-}
-
 uint32_t log2u(uint64_t v) {
     uint32_t k = 0;
     while ((1ull << k) < v) ++k;
@@ -580,8 +562,8 @@ taps_status check_topology(const taps_topology *t, taps_hier *H, taps_cluster *c
 // devices: ordered runs of distinct partitionable axes that cover levels
 // 0..n-1 from level 0, axis a's run at most v_a = (trailing zero bits of its
 // length) wide so that its degree divides its length, every boundary between
-// two runs an allowed cut -- the candidates of k_enumerate that pass its two
-// tests, counted by a dynamic program over (levels covered, axes used).  The
+// two runs an allowed cut -- the candidates of k_build_strategies that pass its
+// two tests, counted by a dynamic program over (levels covered, axes used).  The
 // count depends only on n, the allowed cuts, the partitionable axes and their
 // v_a, so it is memoised on those (per thread).
 uint64_t strategy_count(const taps_op &op, uint32_t n, uint32_t allowed) {
@@ -618,72 +600,52 @@ uint64_t strategy_count(const taps_op &op, uint32_t n, uint32_t allowed) {
     return count;
 }
 
-// GenerateStrategySet on the device; allowed_cuts: the level boundaries a
-// strategy's axis runs may meet (all of them unless a fixed mesh is given).
-taps_status enumerate(const taps_graph *graph, const taps_launch &lp, uint32_t allowed_cuts,
-                      uint64_t *op_offsets, taps_strategy *strategies, uint64_t capacity,
-                      void *stream_) {
-    taps_status st = TAPS_OK;
-    hipStream_t stream = (hipStream_t)stream_;
+// Per-operator strategy counts and offsets (host); TAPS_ERR_NO_STRATEGY if an
+// operator has none.
+taps_status count_strategies(const taps_graph *graph, uint32_t n, uint32_t allowed,
+                             std::vector<uint64_t> &offs) {
     const uint32_t n_ops = graph->n_ops;
-    if (n_ops == 0) {
-        op_offsets[0] = 0;
-        return TAPS_OK;
-    }
-    // launch geometry: the operator's candidates before the divisibility
-    // filter (the closed-form count) cut into chunks of one wavefront
-    std::vector<uint32_t> first_chunk(n_ops + 1, 0);
-    uint64_t n_chunks64 = 0;
+    offs.assign(n_ops + 1, 0);
     for (uint32_t k = 0; k < n_ops; ++k) {
-        const uint64_t cand = candidate_count(__builtin_popcount(graph->ops[k].part_mask), lp.n);
-        first_chunk[k] = (uint32_t)n_chunks64;
-        n_chunks64 += (cand + TAPS_ENUM_CHUNK - 1) / TAPS_ENUM_CHUNK;
-        if (n_chunks64 > 0x7FFFFFFFull) return fail(TAPS_ERR_ARG, "too many candidates");
-    }
-    first_chunk[n_ops] = (uint32_t)n_chunks64;
-    const uint32_t n_chunks = (uint32_t)n_chunks64;
-    scratch sc(stream);
-    std::vector<chunk> ch{{graph->ops, sizeof(taps_op) * n_ops, 0},
-                          {first_chunk.data(), sizeof(uint32_t) * (n_ops + 1), 0}};
-    void *dev = nullptr;
-    if ((st = upload(ch, &dev, stream)) != TAPS_OK) return st;
-    sc.adopt(dev);
-    const taps_op *d_ops = at<taps_op>(dev, ch[0]);
-    uint32_t *d_counts = nullptr;
-    uint64_t *d_base = nullptr, *d_scan = nullptr;
-    if ((st = sc.alloc((void **)&d_counts, sizeof(uint32_t) * (n_chunks ? n_chunks : 1))) != TAPS_OK)
-        return st;
-    if ((st = sc.alloc((void **)&d_base, sizeof(uint64_t) * (n_chunks ? n_chunks : 1))) != TAPS_OK)
-        return st;
-    if ((st = sc.alloc((void **)&d_scan, sizeof(uint64_t) * (n_ops + 2))) != TAPS_OK) return st;
-    // count pass, prefix sums and (for a real call) the emit pass back to back on the
-    // device; the emit pass writes nothing unless every operator has a strategy and
-    // they fit the capacity.  One read-back returns the offsets.
-    const uint32_t *d_first = at<uint32_t>(dev, ch[1]);
-    hipError_t err = taps_launch_enumerate(d_ops, lp.n, n_ops, n_chunks, d_first, d_base,
-                                           d_scan + n_ops + 1, allowed_cuts, d_counts, nullptr, stream);
-    if (err == hipSuccess)
-        err = taps_launch_chunk_scan(d_counts, n_chunks, d_first, n_ops,
-                                     strategies ? capacity : UINT64_MAX, d_base, d_scan, stream);
-    if (err == hipSuccess && strategies)
-        err = taps_launch_enumerate(d_ops, lp.n, n_ops, n_chunks, d_first, d_base,
-                                    d_scan + n_ops + 1, allowed_cuts, nullptr, strategies, stream);
-    std::vector<uint64_t> offs(n_ops + 2, 0);
-    if (err == hipSuccess)
-        err = hipMemcpyAsync(offs.data(), d_scan, sizeof(uint64_t) * (n_ops + 2),
-                             hipMemcpyDeviceToHost, stream);
-    if (err == hipSuccess) err = wait_stream(stream);
-    if (err != hipSuccess) return hip_fail(err, "enumerate");
-    for (uint32_t k = 0; k < n_ops; ++k)
-        if (offs[k + 1] == offs[k])
+        const uint64_t c = strategy_count(graph->ops[k], n, allowed);
+        if (c == 0)
             return fail(TAPS_ERR_NO_STRATEGY,
                         "op %u has no strategy on %u devices (no partitionable axis whose length "
                         "the degrees divide)",
-                        k, 1u << lp.n);
+                        k, 1u << n);
+        offs[k + 1] = offs[k] + c;
+    }
+    if (offs[n_ops] > 0xFFFFFFFFull) return fail(TAPS_ERR_ARG, "more than 2^32 strategies");
+    return TAPS_OK;
+}
+
+// GenerateStrategySet: sizes on the host, strategies on the device (no
+// synchronisation); allowed_cuts: the level boundaries a strategy's axis runs
+// may meet (all of them unless a fixed mesh is given).
+taps_status enumerate(const taps_graph *graph, const taps_launch &lp, uint32_t allowed_cuts,
+                      uint64_t *op_offsets, taps_strategy *strategies, uint64_t capacity,
+                      void *stream_) {
+    std::vector<uint64_t> offs;
+    taps_status st = count_strategies(graph, lp.n, allowed_cuts, offs);
+    if (st != TAPS_OK) return st;
+    const uint32_t n_ops = graph->n_ops;
     std::memcpy(op_offsets, offs.data(), sizeof(uint64_t) * (n_ops + 1));
-    if (strategies && offs[n_ops] > capacity)
+    if (!strategies || n_ops == 0) return TAPS_OK;
+    if (offs[n_ops] > capacity)
         return fail(TAPS_ERR_CAPACITY, "%llu strategies, capacity %llu",
                     (unsigned long long)offs[n_ops], (unsigned long long)capacity);
+    hipStream_t stream = (hipStream_t)stream_;
+    scratch sc(stream);
+    std::vector<chunk> ch{{graph->ops, sizeof(taps_op) * n_ops, 0},
+                          {offs.data(), sizeof(uint64_t) * (n_ops + 1), 0}};
+    void *dev = nullptr;
+    if ((st = upload(ch, &dev, stream)) != TAPS_OK) return st;
+    sc.adopt(dev);
+    const taps_table no_node = {nullptr, nullptr, nullptr, nullptr, nullptr};
+    const hipError_t err =
+        taps_launch_build_strategies(at<taps_op>(dev, ch[0]), n_ops, at<uint64_t>(dev, ch[1]),
+                                     allowed_cuts, lp, strategies, nullptr, no_node, stream);
+    if (err != hipSuccess) return hip_fail(err, "enumerate");
     return TAPS_OK;
 }
 
@@ -813,17 +775,8 @@ taps_status taps_build_tables(const taps_graph *graph, const taps_cluster *clust
     if (mesh && (st = mesh_cuts(mesh, lp.n, &allowed)) != TAPS_OK) return st;
     const uint32_t n_ops = graph->n_ops, n_edges = graph->n_edges;
     // sizes, on the host
-    std::vector<uint64_t> offs(n_ops + 1, 0);
-    for (uint32_t k = 0; k < n_ops; ++k) {
-        const uint64_t c = strategy_count(graph->ops[k], lp.n, allowed);
-        if (c == 0)
-            return fail(TAPS_ERR_NO_STRATEGY,
-                        "op %u has no strategy on %u devices (no partitionable axis whose length "
-                        "the degrees divide)",
-                        k, 1u << lp.n);
-        offs[k + 1] = offs[k] + c;
-    }
-    if (offs[n_ops] > 0xFFFFFFFFull) return fail(TAPS_ERR_ARG, "more than 2^32 strategies");
+    std::vector<uint64_t> offs;
+    if ((st = count_strategies(graph, lp.n, allowed, offs)) != TAPS_OK) return st;
     // shared tables: edges described alike share one table -- their operators'
     // strategies are the same function of the same descriptions here, so no
     // device comparison is needed

@@ -58,18 +58,6 @@ struct taps_row_ref {
     uint32_t pad;
 };
 
-#define TAPS_ENUM_CHUNK 64   // candidates per enumeration wavefront
-
-// first_chunk: n_ops + 1 entries, operator k owns chunks [first_chunk[k], first_chunk[k+1]).
-hipError_t taps_launch_enumerate(const taps_op *ops, uint32_t n, uint32_t n_ops,
-                                 uint32_t n_chunks, const uint32_t *first_chunk,
-                                 const uint64_t *base, const uint64_t *valid_flag,
-                                 uint32_t allowed_cuts, uint32_t *counts, taps_strategy *out,
-                                 hipStream_t stream);
-// scan: n_ops + 2 entries (operator offsets, total, valid flag); base: n_chunks.
-hipError_t taps_launch_chunk_scan(const uint32_t *counts, uint32_t n_chunks,
-                                  const uint32_t *first_chunk, uint32_t n_ops, uint64_t capacity,
-                                  uint64_t *base, uint64_t *scan, hipStream_t stream);
 hipError_t taps_launch_describe(const taps_strategy *s, uint64_t total, taps_desc *desc,
                                 hipStream_t stream);
 hipError_t taps_launch_node_costs(const taps_op *ops, uint32_t n_ops, const uint64_t *offsets,
@@ -102,8 +90,9 @@ hipError_t taps_launch_edge_costs_sweep(const taps_edge_params *params, const ta
                                         uint64_t n_rows, const taps_desc *desc,
                                         const taps_launch &lp, const taps_sweep &sw,
                                         hipStream_t stream);
-// Strategies, descriptors and node records of every operator in one launch
-// (one workgroup per operator); op_offsets: device copy of the host's counts.
+// Strategies of every operator in one launch (one workgroup per operator),
+// with their descriptors and node records unless desc / node.t are NULL;
+// op_offsets: device copy of the host's counts.
 hipError_t taps_launch_build_strategies(const taps_op *ops, uint32_t n_ops,
                                         const uint64_t *op_offsets, uint32_t allowed_cuts,
                                         const taps_launch &lp, taps_strategy *out, taps_desc *desc,

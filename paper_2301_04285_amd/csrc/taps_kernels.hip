@@ -1,7 +1,8 @@
 // taps_kernels.hip -- gfx950 kernels of the TAPS cost tables.
 //
-//   k_enumerate   one wavefront per 64 candidates of one operator:
-//                 GenerateStrategySet in canonical order, ballot compaction
+//   k_build_strategies  one workgroup per operator: GenerateStrategySet in
+//                 canonical order at host-counted offsets (ballots, LDS scan),
+//                 optionally each strategy's descriptor and node record
 //   k_describe    one thread per strategy: level runs, owners and cuts
 //   k_node_costs  one thread per strategy: the intra-op AllReduces
 //   k_memory_costs one thread per strategy: weight and output shard bytes
@@ -22,7 +23,6 @@
 namespace {
 
 constexpr uint32_t kWave = 64;
-static_assert(TAPS_ENUM_CHUNK == kWave, "one enumeration chunk per wavefront");
 
 // Completion counts w(k, s, z) for k, s, z in 0..8 (see taps_completions),
 // evaluated by the compiler.
@@ -51,128 +51,6 @@ __device__ inline void store_entry(const taps_table &out, uint64_t row, uint32_t
 __device__ inline uint32_t lanes_below(uint64_t mask) {
     return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
                                      __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
-}
-
-// The operator owning chunk c: largest k < n_ops with first_chunk[k] <= c
-// (operators without chunks share their successor's first chunk).
-__device__ inline uint32_t find_chunk_owner(const uint32_t *first_chunk, uint32_t n_ops,
-                                            uint32_t c) {
-    uint32_t lo = 0, hi = n_ops;
-    while (hi - lo > 1) {
-        const uint32_t mid = (lo + hi) >> 1;
-        if (first_chunk[mid] <= c)
-            lo = mid;
-        else
-            hi = mid;
-    }
-    return lo;
-}
-
-// One wavefront per chunk of 64 consecutive candidates of one operator.
-// Operator k owns chunks first_chunk[k] .. first_chunk[k+1]-1, its candidates
-// in order, 64 per chunk.
-// Count pass (out == nullptr): counts[c] = valid candidates of the chunk.
-// Emit pass: valid candidates go to out[base[c] + rank among the chunk's],
-// only if the scan found the enumeration valid (scan[n_ops + 1] == 1).
-// allowed_cuts: level boundaries a strategy's axis runs may meet (bit c: the
-// boundary between levels c-1 and c); all of them without a fixed mesh.
-__global__ __launch_bounds__(kWave) void k_enumerate(const taps_op *__restrict__ ops, uint32_t n,
-                                                     uint32_t n_ops,
-                                                     const uint32_t *__restrict__ first_chunk,
-                                                     const uint64_t *__restrict__ base,
-                                                     const uint64_t *__restrict__ valid_flag,
-                                                     uint32_t allowed_cuts,
-                                                     uint32_t *__restrict__ counts,
-                                                     taps_strategy *__restrict__ out) {
-    __shared__ uint32_t W[9 * 9 * 9];
-    if (out && *valid_flag != 1u) return;   // uniform: nothing is written on an error
-    const uint32_t lane = threadIdx.x;
-    for (uint32_t x = lane; x < 9u * 9u * 9u; x += kWave) W[x] = kCompletions.v[x];
-    __syncthreads();
-    const uint32_t c = blockIdx.x;
-    const uint32_t k = find_chunk_owner(first_chunk, n_ops, c);
-    const taps_op &op = ops[k];
-    const uint32_t n_axes = op.n_axes, part = op.part_mask;
-    const uint32_t total = W[(taps_popc(part) * 9u + n) * 9u];
-    const uint32_t r = (c - first_chunk[k]) * kWave + lane;
-    uint32_t expo[TAPS_D_MAX_AXES];
-    int32_t pos[TAPS_D_MAX_AXES];
-    bool valid = r < total && taps_unrank(n_axes, part, n, r, W, expo, pos);
-    if (valid)
-        for (uint32_t a = 0; a < n_axes; ++a)
-            if (op.axis_len[a] & (((int64_t)1 << expo[a]) - 1)) valid = false;
-    // a fixed mesh admits only boundaries between axis runs that are mesh boundaries
-    if (valid && (taps_describe(n_axes, expo, pos).cuts & ~allowed_cuts)) valid = false;
-    const uint64_t m = __ballot(valid);
-    if (counts && lane == 0) counts[c] = (uint32_t)__builtin_popcountll(m);
-    if (out && valid) {
-        taps_strategy st;
-        for (uint32_t a = 0; a < TAPS_MAX_AXES; ++a) {
-            st.log2_deg[a] = a < n_axes ? (uint8_t)expo[a] : 0;
-            st.pos[a] = a < n_axes ? (int8_t)pos[a] : (int8_t)-1;
-        }
-        out[base[c] + lanes_below(m)] = st;
-    }
-}
-
-// One workgroup: exclusive prefix sums of the chunk counts (base[c], the
-// first strategy of chunk c), the operator offsets scan[k] = base of the
-// operator's first chunk (scan[n_ops] = total), and scan[n_ops + 1] = 1 if
-// every operator has a strategy and the total fits `capacity`, else 0.
-__global__ __launch_bounds__(1024) void k_chunk_scan(const uint32_t *__restrict__ counts,
-                                                     uint32_t n_chunks,
-                                                     const uint32_t *__restrict__ first_chunk,
-                                                     uint32_t n_ops, uint64_t capacity,
-                                                     uint64_t *__restrict__ base,
-                                                     uint64_t *__restrict__ scan) {
-    __shared__ uint32_t wsum[16];
-    __shared__ uint32_t bad;
-    const uint32_t t = threadIdx.x, lane = t % kWave, wave = t / kWave;
-    if (t == 0) bad = 0;
-    uint64_t carry = 0;
-    // tiles of 1024 consecutive chunks: wavefront scans, then a scan of the 16
-    // wavefront sums
-    for (uint32_t tile = 0; tile < n_chunks; tile += 1024u) {
-        const uint32_t c = tile + t;
-        const uint32_t own = c < n_chunks ? counts[c] : 0u;
-        uint32_t v = own;
-#pragma unroll
-        for (uint32_t d = 1; d < kWave; d <<= 1) {
-            const uint32_t y = __shfl_up(v, d, kWave);
-            if (lane >= d) v += y;
-        }
-        if (lane == kWave - 1) wsum[wave] = v;
-        __syncthreads();
-        if (wave == 0) {
-            uint32_t w = lane < 16u ? wsum[lane] : 0u;
-#pragma unroll
-            for (uint32_t d = 1; d < 16u; d <<= 1) {
-                const uint32_t y = __shfl_up(w, d, kWave);
-                if (lane >= d) w += y;
-            }
-            if (lane < 16u) wsum[lane] = w;
-        }
-        __syncthreads();
-        const uint32_t before = wave ? wsum[wave - 1] : 0u;
-        if (c < n_chunks) base[c] = carry + before + v - own;
-        carry += wsum[15];
-        __syncthreads();   // wsum is rewritten by the next tile
-    }
-    __threadfence_block();
-    __syncthreads();
-    const uint64_t total = carry;
-    for (uint32_t k = t; k < n_ops; k += 1024u) {
-        const uint32_t f = first_chunk[k], f1 = first_chunk[k + 1];
-        const uint64_t start = f < n_chunks ? base[f] : total;
-        const uint64_t end = f1 < n_chunks ? base[f1] : total;
-        scan[k] = start;
-        if (end == start) bad = 1;   // an operator without a strategy
-    }
-    __syncthreads();
-    if (t == 0) {
-        scan[n_ops] = total;
-        scan[n_ops + 1] = (!bad && total <= capacity) ? 1u : 0u;
-    }
 }
 
 __global__ __launch_bounds__(256) void k_describe(const taps_strategy *__restrict__ s,
@@ -238,10 +116,11 @@ __global__ __launch_bounds__(256) void k_node_costs(const taps_op *__restrict__ 
     out.meta[idx] = taps_meta(0, c);
 }
 
-// The whole strategy side of a build in one launch: one workgroup per
-// operator walks its candidates in canonical order, 256 per pass (a ballot
-// per wavefront, the four wavefront counts scanned in LDS), and writes every
-// valid strategy together with its descriptor and its node (intra-op) record.
+// GenerateStrategySet, and the whole strategy side of a single-call build, in
+// one launch: one workgroup per operator walks its candidates in canonical
+// order, 256 per pass (a ballot per wavefront, the four wavefront counts
+// scanned in LDS), and writes every valid strategy together with, when asked
+// (desc and node.t not NULL), its descriptor and its node (intra-op) record.
 // The operator's strategies go to [op_offsets[k], op_offsets[k+1]), which the
 // host sized with an exact count of the same filter; nothing is written
 // outside that range.
@@ -294,19 +173,22 @@ __global__ __launch_bounds__(kBuildThreads) void k_build_strategies(const taps_o
                 st.pos[a] = a < n_axes ? (int8_t)pos[a] : (int8_t)-1;
             }
             out[idx] = st;
-            desc[idx] = D;
-            taps_acc c;
-            taps_acc_zero(c);
-            node_tensor(c, op, op.out, D, full, lp.lam);
-            for (uint32_t k = 0; k < op.n_in && k < TAPS_MAX_INPUTS; ++k)
-                node_tensor(c, op, op.in[k], D, full, lp.lam);
-            for (uint32_t k = 0; k < op.n_w && k < TAPS_MAX_WEIGHTS; ++k)
-                node_tensor(c, op, op.w[k], D, full, lp.lam);
-            node.t[idx] = (double)c.intra * lp.inv_n_bintra + (double)c.inter * lp.inv_n_binter;
-            node.vol[idx] = c.vol;
-            node.intra[idx] = c.intra;
-            node.inter[idx] = c.inter;
-            node.meta[idx] = taps_meta(0, c);
+            if (desc) desc[idx] = D;   // uniform: descriptors and node records are optional
+            if (node.t) {
+                taps_acc c;
+                taps_acc_zero(c);
+                node_tensor(c, op, op.out, D, full, lp.lam);
+                for (uint32_t k = 0; k < op.n_in && k < TAPS_MAX_INPUTS; ++k)
+                    node_tensor(c, op, op.in[k], D, full, lp.lam);
+                for (uint32_t k = 0; k < op.n_w && k < TAPS_MAX_WEIGHTS; ++k)
+                    node_tensor(c, op, op.w[k], D, full, lp.lam);
+                node.t[idx] =
+                    (double)c.intra * lp.inv_n_bintra + (double)c.inter * lp.inv_n_binter;
+                node.vol[idx] = c.vol;
+                node.intra[idx] = c.intra;
+                node.inter[idx] = c.inter;
+                node.meta[idx] = taps_meta(0, c);
+            }
         }
         running += all;
     }
@@ -631,25 +513,6 @@ __global__ __launch_bounds__(256) void k_same_ranges(const taps_strategy *__rest
 inline uint32_t blocks_for(uint64_t n, uint32_t per) { return (uint32_t)((n + per - 1) / per); }
 
 }  // namespace
-
-hipError_t taps_launch_enumerate(const taps_op *ops, uint32_t n, uint32_t n_ops,
-                                 uint32_t n_chunks, const uint32_t *first_chunk,
-                                 const uint64_t *base, const uint64_t *valid_flag,
-                                 uint32_t allowed_cuts, uint32_t *counts, taps_strategy *out,
-                                 hipStream_t stream) {
-    if (n_chunks == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_enumerate, dim3(n_chunks), dim3(kWave), 0, stream, ops, n, n_ops,
-                       first_chunk, base, valid_flag, allowed_cuts, counts, out);
-    return hipGetLastError();
-}
-
-hipError_t taps_launch_chunk_scan(const uint32_t *counts, uint32_t n_chunks,
-                                  const uint32_t *first_chunk, uint32_t n_ops, uint64_t capacity,
-                                  uint64_t *base, uint64_t *scan, hipStream_t stream) {
-    hipLaunchKernelGGL(k_chunk_scan, dim3(1), dim3(1024), 0, stream, counts, n_chunks,
-                       first_chunk, n_ops, capacity, base, scan);
-    return hipGetLastError();
-}
 
 hipError_t taps_launch_describe(const taps_strategy *s, uint64_t total, taps_desc *desc,
                                 hipStream_t stream) {

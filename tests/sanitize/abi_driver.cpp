@@ -192,8 +192,10 @@ int main() {
            "null topology");
 
     // the device is reached: without a GPU every such call reports it
-    expect(taps_enumerate_strategies(&g, &cl, offs.data(), nullptr, 0, nullptr), TAPS_ERR_DEVICE,
-           "enumerate without a device");
+    expect(taps_enumerate_strategies(&g, &cl, offs.data(), nullptr, 0, nullptr), TAPS_OK,
+           "enumeration size query (host only)");
+    expect(taps_enumerate_strategies(&g, &cl, offs.data(), (taps_strategy *)256, 27, nullptr),
+           TAPS_ERR_DEVICE, "enumerate without a device");
     expect(taps_build_tables(&g, &cl, nullptr, bo.data(), (taps_strategy *)256, 27, fake,
                              beo.data(), fake, 162, 0, nullptr),
            TAPS_ERR_DEVICE, "build without a device");

@@ -298,7 +298,15 @@ def test_device_errors_are_reported(lib):
     import torch
     if torch.cuda.is_available():
         pytest.skip("a GPU is present")
-    assert _enum(lib, W.mlp2(), W.Cluster(2, 2, 10, 1)) == T.ERR_DEVICE
+    g = T.pack_graph(W.mlp2())
+    cl = T.pack_cluster(W.Cluster(2, 2, 10, 1))
+    offs = np.zeros(4, np.uint64)
+    # the size query is computed on the host; writing the strategies needs the device
+    assert lib.taps_enumerate_strategies(C.byref(g.struct), C.byref(cl), T._u64_array(offs),
+                                         None, 0, None) == T.OK
+    assert list(offs) == [0, 9, 13, 22]
+    assert lib.taps_enumerate_strategies(C.byref(g.struct), C.byref(cl), T._u64_array(offs),
+                                         C.c_void_p(256), 22, None) == T.ERR_DEVICE
     assert "hip" in T.last_error().lower()
 
 
