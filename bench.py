@@ -24,9 +24,10 @@ one pass (candidates costed once per entry, one selection and store per
 point); `link_classes` builds them under three link classes (8-device nodes,
 4-node groups, the groups above them); `value` and `roofline` always come from
 the two-class full evaluation.
-`roofline.traffic` is the edge kernel's HBM bytes per launch from the
-committed rocprofv3 counter summary (null once the kernel sources differ from
-the ones the counters were taken with).
+`roofline.traffic` is the edge kernel's HBM bytes per launch and
+`roofline.valu` its VALU instruction count, lane utilisation and issue rate,
+both from the committed rocprofv3 counter summary (null once the kernel
+sources differ from the ones the counters were taken with).
 """
 from __future__ import annotations
 
@@ -54,23 +55,38 @@ def log(msg: str) -> None:
     print(msg, file=sys.stderr, flush=True)
 
 
-def measured_traffic():
-    """HBM bytes per launch of the edge kernel from the committed counter summary,
-    or None when the kernel sources changed since the counters were taken."""
+def counter_summary():
+    """Figures of the edge kernel from the committed counter summary (HBM bytes
+    per launch, VALU figures), or None when the kernel sources changed since the
+    counters were taken."""
     import hashlib
     try:
         text = open(COUNTERS).read()
     except OSError:
         return None
     fields = dict(line.split(": ", 1) for line in text.splitlines()
-                  if line.startswith(("traffic_bytes_per_launch: ", "kernel_sources_sha256: ")))
+                  if ": " in line and line.split(": ", 1)[0].replace("_", "").isalnum()
+                  and not line.startswith((" ", "|", "#", "*")))
     h = hashlib.sha256()
     for f in KERNEL_SOURCES:
         with open(f, "rb") as fh:
             h.update(fh.read())
     if fields.get("kernel_sources_sha256", "").strip() != h.hexdigest():
         return None
-    return int(fields["traffic_bytes_per_launch"])
+    return fields
+
+
+def measured_traffic(fields):
+    return int(fields["traffic_bytes_per_launch"]) if fields else None
+
+
+def measured_valu(fields):
+    if not fields or "valu_instructions_per_64_entries" not in fields:
+        return None
+    return {"instructions_per_64_entries": float(fields["valu_instructions_per_64_entries"]),
+            "lane_utilisation": float(fields["valu_lane_utilisation"]),
+            "issue_per_simd_cycle": float(fields["valu_issue_per_simd_cycle"]),
+            "source": os.path.relpath(COUNTERS, ROOT)}
 
 
 def cpu_baseline(workload, cluster, layers: int) -> dict:
@@ -232,6 +248,7 @@ def main() -> int:
         f"{build_gpu_ms:.3f} ms, edge kernel {kernel_ms:.3f} ms")
 
     bytes_per_launch = BYTES_PER_ENTRY * entries
+    counters = counter_summary()
     achieved = bytes_per_launch / (kernel_ms * 1e-3) / 1e9
     out = {
         "metric": "edge-cost entries/sec on 1 GPU (full cost-table build: enumerate + node + edge)",
@@ -256,7 +273,9 @@ def main() -> int:
         "edge_entries_per_s": entries / (kernel_ms * 1e-3),
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBPS,
-                     "traffic": measured_traffic() if args.config == 5 else None},
+                     "traffic": measured_traffic(counters) if args.config == 5 else None,
+                     # the co-limit: VALU issue (rocprofv3 counters of the same kernel)
+                     "valu": measured_valu(counters) if args.config == 5 else None},
     }
     if args.shared:
         # identical edge tables computed once (taps_edge_costs_shared), into a second
