@@ -125,7 +125,14 @@ def cpu_baseline(workload, cluster, layers: int) -> dict:
     cores = min(16, len(os.sched_getaffinity(0)))
     entries_mt, dt_mt = run(cores)
     assert entries_mt == entries
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), "")
+    except OSError:
+        pass
     return {"value": entries / dt, "unit": "edge entries/s", "cores": 1, "kind": "oracle",
+            "cpu_model": model,
             "sample": f"first {layers} of 96 layers: {len(keep)} ops, {len(edges)} edges, "
                       f"{entries} edge entries, enumeration + node + edge tables in {dt:.2f} s "
                       f"on one core",
