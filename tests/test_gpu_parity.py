@@ -393,6 +393,44 @@ def test_fused_build_capacity_and_errors(T):
         assert all(bool((_signed(v) == 5).all()) for v in (*out.node.values(), *out.edge.values()))
 
 
+def test_link_class_degenerate_topologies(T):
+    """Link classes at their edges: one class (every collective inside the one
+    block), an innermost block of one device (every collective leaves it), block
+    sizes repeated (empty classes), four classes on the largest mesh, and the
+    in-node AllToAll bandwidth with one device per node (no in-node AllToAll)."""
+    g = W.gpt(1, 64, 4, 32, 4, 2)
+    cl16 = W.Cluster(2, 8, 600 * W.GB, 100 * W.GB)
+    for topo in (W.Topology((16,), (300 * W.GB,)),
+                 W.Topology((1, 16), (600 * W.GB, 100 * W.GB)),
+                 W.Topology((2, 2, 8, 16), (600 * W.GB, 400 * W.GB, 100 * W.GB, 25 * W.GB)),
+                 W.Topology((1, 4, 16), (600 * W.GB, 100 * W.GB, 50 * W.GB), 1200 * W.GB)):
+        _topology_check(T, g, cl16, topo, f"gpt1 under {topo.domains}")
+    g = W.gpt(1, 64, 2, 128, 2, 2)
+    cl256 = W.Cluster(32, 8, 600 * W.GB, 100 * W.GB)
+    _topology_check(T, g, cl256, W.Topology((8, 32, 128, 256), (600 * W.GB, 200 * W.GB, 50 * W.GB,
+                                                                   25 * W.GB), 700 * W.GB),
+                    "gpt1-s128 on 256 devices, four classes")
+    one = W.Cluster(1, 1, 10, 1)
+    _topology_check(T, W.gpt(1, 64, 4, 32, 4, 2), one, W.Topology((1,), (10,)), "one device")
+
+
+def test_fused_build_degenerate(T):
+    """The single-call build on one device, on 256 devices (batch x sequence split
+    256 ways), on an empty graph and on operators without edges, against the
+    oracle."""
+    import torch
+    full_check(T, W.gpt(1, 64, 4, 32, 4, 2), W.Cluster(1, 1, 10, 1), "fused one device")
+    full_check(T, W.gpt(1, 64, 2, 128, 2, 2), W.Cluster(32, 8, 300, 7), "fused 256 devices")
+    full_check(T, W.gpt(1, 64, 2, 128, 2, 2), W.Cluster(32, 8, 300, 7), "fused 256 devices on a mesh",
+               mesh=[8, 4, 4, 2])
+    tabs = T.build_tables(W.Graph(), W.Cluster(2, 2, 10, 1))
+    torch.cuda.synchronize()
+    assert list(tabs.op_offsets) == [0] and list(tabs.edge_offsets) == [0]
+    g = W.Graph([W.matmul("a", 8, 8, 8, 2), W.matmul("b", 16, 8, 4, 4)], [])
+    tabs = full_check(T, g, W.Cluster(2, 2, 10, 1), "fused, no edges")
+    assert list(tabs.edge_offsets) == [0]
+
+
 def test_empty_graph_and_no_edges(T):
     cl = W.Cluster(2, 2, 10, 1)
     tabs = T.build_tables(W.Graph(), cl)
