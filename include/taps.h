@@ -49,9 +49,15 @@
  * Memory and streams
  *   - Graph, cluster and offset arrays are host memory owned by the caller
  *     and read only during the call.  Strategy and table arrays are device
- *     memory (HIP) owned by the caller.  The library allocates and frees its
- *     own device scratch in stream order on the given stream and keeps no
- *     pointer of the caller after the call returns.
+ *     memory (HIP) owned by the caller.  The library keeps one device scratch
+ *     block per (device, stream), reused by the next call on that stream
+ *     (stream order makes the reuse safe) and grown in stream order when a
+ *     call needs more; at most 16 such blocks are kept (the least recently
+ *     used idle one is freed).  Host arrays a call uploads are copied into
+ *     one of at most 8 pinned staging buffers (1 MiB or more each, kept until
+ *     the process ends) and from there to the device in stream order.  Calls
+ *     on one stream from several threads are queued one after the other.  No
+ *     pointer of the caller is kept after the call returns.
  *   - Kernels are asynchronous on `stream` (a hipStream_t; NULL = the null
  *     stream): the tables are complete once that stream has been
  *     synchronised.  Every size (strategies per operator, entries per edge)

@@ -10,6 +10,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <list>
 #include <map>
 #include <mutex>
 #include <numeric>
@@ -148,16 +149,27 @@ taps_status check_offsets(const taps_graph *g, const uint64_t *op_offsets) {
     return TAPS_OK;
 }
 
-// Pinned staging for host-to-device uploads: the next upload waits for the
-// previous copy out of the buffer to finish before overwriting it.
-struct staging {
-    std::mutex mu;
+// Pinned staging for host-to-device uploads: a small pool of buffers, each
+// with the event recorded after the copy out of it.  An upload takes a buffer
+// whose copy has completed (or a new one), so calls on different streams or
+// threads, and a call queued behind a long-running build, do not wait for
+// each other's copies; only when every buffer of a full pool is still in
+// flight does an upload wait, for the oldest.
+struct staging_buffer {
     char *host = nullptr;
     size_t cap = 0;
     hipEvent_t done = nullptr;
     bool pending = false;
+    uint64_t last_use = 0;
 };
-staging g_stage;
+struct staging_pool {
+    std::mutex mu;
+    std::vector<staging_buffer> bufs;
+    uint64_t clock = 0;
+};
+staging_pool g_stage;
+constexpr size_t kStagingBuffers = 8;
+constexpr size_t kStagingMin = size_t(1) << 20;
 
 struct chunk {
     const void *src;
@@ -199,82 +211,216 @@ void retain_pool() {
     done[dev] = true;
 }
 
-// Uploads the chunks into one stream-ordered device allocation; *dev
-// receives its base (free it with hipFreeAsync on the same stream).
-taps_status upload(std::vector<chunk> &chunks, void **dev, hipStream_t stream) {
+template <class T>
+T *at(void *base, const chunk &c) {
+    return reinterpret_cast<T *>(static_cast<char *>(base) + c.offset);
+}
+
+// Device scratch: one block per (device, stream), kept for the next call on
+// the same stream -- stream order makes the reuse safe, and a call then
+// neither allocates nor frees (a stream-ordered free blocks the host until the
+// stream has drained, which would keep the host from queueing the next build
+// while the current one runs).  A call holds its block's lock from start to
+// end, so calls on one stream from several threads queue one after the other;
+// calls on different streams use different blocks.  A call carves its arrays
+// from the block; what does not fit goes to allocations of its own, freed in
+// stream order when it returns, and the block is grown past the call's whole
+// need (to a power of two) at the start of the next call on that stream.  At
+// most kMaxBlocks blocks are kept; beyond that the least recently used idle
+// one is freed.
+struct stream_block {
+    int device = 0;
+    hipStream_t stream = nullptr;
+    std::mutex mu;
+    char *ptr = nullptr;
+    size_t cap = 0;
+    size_t want = 0;       // largest need seen on this stream
+    uint64_t last_use = 0;
+};
+std::mutex g_blocks_mu;
+std::list<stream_block> g_blocks;   // stable addresses
+uint64_t g_blocks_clock = 0;
+constexpr size_t kMaxBlocks = 16;
+
+stream_block *find_block(hipStream_t stream) {
+    int device = 0;
+    (void)hipGetDevice(&device);
+    std::lock_guard<std::mutex> lock(g_blocks_mu);
+    for (stream_block &b : g_blocks)
+        if (b.device == device && b.stream == stream) {
+            b.last_use = ++g_blocks_clock;
+            return &b;
+        }
+    if (g_blocks.size() >= kMaxBlocks) {   // free the least recently used idle block
+        auto victim = g_blocks.end();
+        for (auto it = g_blocks.begin(); it != g_blocks.end(); ++it) {
+            if (!it->mu.try_lock()) continue;
+            it->mu.unlock();
+            if (victim == g_blocks.end() || it->last_use < victim->last_use) victim = it;
+        }
+        if (victim != g_blocks.end()) {
+            // its stream may be gone: a device-wide free, which waits for the work using it
+            if (victim->ptr) {
+                int cur = 0;
+                (void)hipGetDevice(&cur);
+                (void)hipSetDevice(victim->device);
+                (void)hipFree(victim->ptr);
+                (void)hipSetDevice(cur);
+            }
+            g_blocks.erase(victim);
+        }
+    }
+    g_blocks.emplace_back();
+    stream_block &b = g_blocks.back();
+    b.device = device;
+    b.stream = stream;
+    b.last_use = ++g_blocks_clock;
+    return &b;
+}
+
+struct scratch {
+    hipStream_t stream;
+    stream_block *blk;
+    std::unique_lock<std::mutex> lock;
+    size_t used = 0;                // bytes of the block this call has taken
+    size_t need = 0;                // what the call asked for in all
+    std::vector<void *> own;        // allocations beyond the block, freed on return
+    explicit scratch(hipStream_t s) : stream(s), blk(find_block(s)), lock(blk->mu) {
+        if (blk->want > blk->cap) {   // grow past the largest need seen (nothing uses the block yet)
+            // a power of two, so that a stream whose calls vary in size regrows rarely
+            size_t cap = size_t(1) << 20;
+            while (cap < blk->want) cap *= 2;
+            retain_pool();
+            if (blk->ptr) (void)hipFreeAsync(blk->ptr, stream);
+            blk->ptr = nullptr;
+            blk->cap = 0;
+            void *p = nullptr;
+            if (hipMallocAsync(&p, cap, stream) == hipSuccess) {
+                blk->ptr = (char *)p;
+                blk->cap = cap;
+            }
+        }
+    }
+    ~scratch() {
+        for (void *p : own) (void)hipFreeAsync(p, stream);
+        if (need > blk->want) blk->want = need;
+    }
+    taps_status alloc(void **p, size_t bytes) {
+        const size_t size = align256(bytes ? bytes : 256);
+        need += size;
+        if (blk->ptr && used + size <= blk->cap) {
+            *p = blk->ptr + used;
+            used += size;
+            return TAPS_OK;
+        }
+        retain_pool();
+        hipError_t err = hipMallocAsync(p, size, stream);
+        if (err != hipSuccess) return hip_fail(err, "hipMallocAsync");
+        own.push_back(*p);
+        return TAPS_OK;
+    }
+};
+
+// Uploads the chunks into one array of the call's scratch; *dev receives its
+// base.
+taps_status upload(scratch &sc, std::vector<chunk> &chunks, void **dev) {
+    const hipStream_t stream = sc.stream;
     size_t total = 0;
     for (chunk &c : chunks) {
         c.offset = total;
         total += align256(c.bytes);
     }
     if (total == 0) total = 256;
-    retain_pool();
-    hipError_t err = hipMallocAsync(dev, total, stream);
-    if (err != hipSuccess) return hip_fail(err, "hipMallocAsync");
+    taps_status st = sc.alloc(dev, total);
+    if (st != TAPS_OK) return st;
+    hipError_t err = hipSuccess;
     std::lock_guard<std::mutex> lock(g_stage.mu);
-    if (g_stage.pending) {
-        err = hipEventSynchronize(g_stage.done);
-        if (err != hipSuccess) return hip_fail(err, "hipEventSynchronize");
-        g_stage.pending = false;
+    // a buffer whose last copy is done: free, or completed in the meantime
+    staging_buffer *b = nullptr;
+    for (staging_buffer &x : g_stage.bufs) {
+        if (x.pending && hipEventQuery(x.done) == hipSuccess) x.pending = false;
+        if (!x.pending && (!b || x.cap > b->cap)) b = &x;
     }
-    if (!g_stage.done) {
-        err = hipEventCreateWithFlags(&g_stage.done, hipEventDisableTiming);
+    if (!b && g_stage.bufs.size() < kStagingBuffers) {
+        g_stage.bufs.emplace_back();
+        b = &g_stage.bufs.back();
+    }
+    if (!b) {   // every buffer in flight: wait for the least recently used one
+        b = &g_stage.bufs[0];
+        for (staging_buffer &x : g_stage.bufs)
+            if (x.last_use < b->last_use) b = &x;
+        err = hipEventSynchronize(b->done);
+        if (err != hipSuccess) return hip_fail(err, "hipEventSynchronize");
+        b->pending = false;
+    }
+    if (!b->done) {
+        err = hipEventCreateWithFlags(&b->done, hipEventDisableTiming);
         if (err != hipSuccess) return hip_fail(err, "hipEventCreate");
     }
-    if (g_stage.cap < total) {
-        if (g_stage.host) (void)hipHostFree(g_stage.host);
-        g_stage.host = nullptr;
-        g_stage.cap = 0;
-        err = hipHostMalloc((void **)&g_stage.host, total, hipHostMallocDefault);
+    if (b->cap < total) {
+        // hipHostFree waits for the device to go idle: grow to a power of two
+        // (at least kStagingMin) so that a buffer is replaced at most a few times
+        size_t cap = kStagingMin;
+        while (cap < total) cap *= 2;
+        if (b->host) (void)hipHostFree(b->host);
+        b->host = nullptr;
+        b->cap = 0;
+        err = hipHostMalloc((void **)&b->host, cap, hipHostMallocDefault);
         if (err != hipSuccess) return hip_fail(err, "hipHostMalloc");
-        g_stage.cap = total;
+        b->cap = cap;
     }
     for (const chunk &c : chunks)
-        if (c.bytes) std::memcpy(g_stage.host + c.offset, c.src, c.bytes);
-    err = hipMemcpyAsync(*dev, g_stage.host, total, hipMemcpyHostToDevice, stream);
+        if (c.bytes) std::memcpy(b->host + c.offset, c.src, c.bytes);
+    err = hipMemcpyAsync(*dev, b->host, total, hipMemcpyHostToDevice, stream);
     if (err != hipSuccess) return hip_fail(err, "hipMemcpyAsync");
-    err = hipEventRecord(g_stage.done, stream);
+    err = hipEventRecord(b->done, stream);
     if (err != hipSuccess) return hip_fail(err, "hipEventRecord");
-    g_stage.pending = true;
+    b->pending = true;
+    b->last_use = ++g_stage.clock;
     return TAPS_OK;
 }
-
-template <class T>
-T *at(void *base, const chunk &c) {
-    return reinterpret_cast<T *>(static_cast<char *>(base) + c.offset);
-}
-
-// Stream-ordered scratch that is released on every exit path.
-struct scratch {
-    hipStream_t stream;
-    std::vector<void *> ptrs;
-    explicit scratch(hipStream_t s) : stream(s) {}
-    ~scratch() {
-        for (void *p : ptrs) (void)hipFreeAsync(p, stream);
-    }
-    taps_status alloc(void **p, size_t bytes) {
-        hipError_t err = hipMallocAsync(p, bytes ? bytes : 256, stream);
-        if (err != hipSuccess) return hip_fail(err, "hipMallocAsync");
-        ptrs.push_back(*p);
-        return TAPS_OK;
-    }
-    void adopt(void *p) { ptrs.push_back(p); }
-};
 
 // Edges whose tables are identical: the same producer description (axes,
 // lengths, partitionable axes, element size, output tensor), the same
 // consumer description (axes, lengths, partitionable axes, the input tensor
 // the edge feeds) -- and, checked on the device, the same strategies.
-std::vector<int64_t> edge_key(const taps_graph *g, uint32_t e) {
+struct edge_sig {
+    int64_t v[7 + 2 * TAPS_MAX_AXES + 2 * TAPS_MAX_RANK];   // zero-padded
+    bool operator==(const edge_sig &o) const { return std::memcmp(v, o.v, sizeof v) == 0; }
+};
+struct edge_sig_hash {
+    size_t operator()(const edge_sig &k) const {   // FNV-1a over the words
+        uint64_t h = 1469598103934665603ull;
+        for (int64_t x : k.v) h = (h ^ (uint64_t)x) * 1099511628211ull;
+        return (size_t)h;
+    }
+};
+edge_sig edge_key(const taps_graph *g, uint32_t e) {
     const taps_edge &E = g->edges[e];
     const taps_op &s = g->ops[E.src_op], &d = g->ops[E.dst_op];
-    std::vector<int64_t> k{s.n_axes, s.part_mask, s.dtype_bytes, s.out.rank,
-                           d.n_axes, d.part_mask, d.in[E.dst_slot].rank};
-    for (uint32_t a = 0; a < s.n_axes; ++a) k.push_back(s.axis_len[a]);
-    for (uint32_t a = 0; a < d.n_axes; ++a) k.push_back(d.axis_len[a]);
-    for (uint32_t r = 0; r < s.out.rank; ++r) k.push_back(s.out.axis[r]);
-    for (uint32_t r = 0; r < d.in[E.dst_slot].rank; ++r) k.push_back(d.in[E.dst_slot].axis[r]);
+    edge_sig k;
+    std::memset(&k, 0, sizeof k);
+    int n = 0;
+    for (int64_t x : {(int64_t)s.n_axes, (int64_t)s.part_mask, (int64_t)s.dtype_bytes,
+                      (int64_t)s.out.rank, (int64_t)d.n_axes, (int64_t)d.part_mask,
+                      (int64_t)d.in[E.dst_slot].rank})
+        k.v[n++] = x;
+    for (uint32_t a = 0; a < TAPS_MAX_AXES; ++a) k.v[n++] = a < s.n_axes ? s.axis_len[a] : 0;
+    for (uint32_t a = 0; a < TAPS_MAX_AXES; ++a) k.v[n++] = a < d.n_axes ? d.axis_len[a] : 0;
+    for (uint32_t r = 0; r < TAPS_MAX_RANK; ++r) k.v[n++] = r < s.out.rank ? s.out.axis[r] : 0;
+    for (uint32_t r = 0; r < TAPS_MAX_RANK; ++r)
+        k.v[n++] = r < d.in[E.dst_slot].rank ? d.in[E.dst_slot].axis[r] : 0;
     return k;
+}
+
+// group[e] = the first edge whose key equals edge e's.
+std::vector<uint32_t> group_edges(const taps_graph *g) {
+    std::unordered_map<edge_sig, uint32_t, edge_sig_hash> first;
+    first.reserve(2 * (size_t)g->n_edges + 1);
+    std::vector<uint32_t> group(g->n_edges);
+    for (uint32_t e = 0; e < g->n_edges; ++e)
+        group[e] = first.emplace(edge_key(g, e), e).first->second;
+    return group;
 }
 
 // rep[e]: the edge whose table edge e shares (itself if none).  One
@@ -283,7 +429,7 @@ taps_status share_edges(const taps_graph *g, const uint64_t *op_offsets,
                         const taps_strategy *strategies, hipStream_t stream,
                         std::vector<uint32_t> &rep) {
     const uint32_t n_edges = g->n_edges;
-    std::map<std::vector<int64_t>, uint32_t> first;
+    const std::vector<uint32_t> group = group_edges(g);
     std::map<std::pair<uint32_t, uint32_t>, uint32_t> pair_index;   // (op, rep op) -> pair
     std::vector<uint64_t> pairs;
     auto count = [&](uint32_t op) { return op_offsets[op + 1] - op_offsets[op]; };
@@ -299,8 +445,7 @@ taps_status share_edges(const taps_graph *g, const uint64_t *op_offsets,
     };
     std::vector<int64_t> src_pair(n_edges, -2), dst_pair(n_edges, -2);
     for (uint32_t e = 0; e < n_edges; ++e) {
-        auto it = first.emplace(edge_key(g, e), e).first;
-        rep[e] = it->second;
+        rep[e] = group[e];
         if (rep[e] == e) continue;
         const taps_edge &E = g->edges[e], &R = g->edges[rep[e]];
         src_pair[e] = want(E.src_op, R.src_op);
@@ -447,8 +592,7 @@ taps_status edge_costs(const taps_graph *graph, const taps_cluster *clusters, ui
                           {copies.data(), sizeof(taps_copy_task) * copies.size(), 0},
                           {dst_list.data(), sizeof(uint64_t) * dst_list.size(), 0}};
     void *dev = nullptr;
-    if ((st = upload(ch, &dev, stream)) != TAPS_OK) return st;
-    sc.adopt(dev);
+    if ((st = upload(sc, ch, &dev)) != TAPS_OK) return st;
     taps_desc *d_desc = nullptr;
     taps_edge_params *d_params = nullptr;
     taps_row_ref *d_segs = nullptr;
@@ -639,8 +783,7 @@ taps_status enumerate(const taps_graph *graph, const taps_launch &lp, uint32_t a
     std::vector<chunk> ch{{graph->ops, sizeof(taps_op) * n_ops, 0},
                           {offs.data(), sizeof(uint64_t) * (n_ops + 1), 0}};
     void *dev = nullptr;
-    if ((st = upload(ch, &dev, stream)) != TAPS_OK) return st;
-    sc.adopt(dev);
+    if ((st = upload(sc, ch, &dev)) != TAPS_OK) return st;
     const taps_table no_node = {nullptr, nullptr, nullptr, nullptr, nullptr};
     const hipError_t err =
         taps_launch_build_strategies(at<taps_op>(dev, ch[0]), n_ops, at<uint64_t>(dev, ch[1]),
@@ -747,8 +890,7 @@ taps_status taps_node_costs(const taps_graph *graph, const taps_cluster *cluster
     std::vector<chunk> ch{{graph->ops, sizeof(taps_op) * n_ops, 0},
                           {op_offsets, sizeof(uint64_t) * (n_ops + 1), 0}};
     void *dev = nullptr;
-    if ((st = upload(ch, &dev, stream)) != TAPS_OK) return st;
-    sc.adopt(dev);
+    if ((st = upload(sc, ch, &dev)) != TAPS_OK) return st;
     taps_desc *d_desc = nullptr;
     if ((st = sc.alloc((void **)&d_desc, sizeof(taps_desc) * total)) != TAPS_OK) return st;
     hipError_t err = taps_launch_describe(strategies, total, d_desc, stream);
@@ -783,8 +925,7 @@ taps_status taps_build_tables(const taps_graph *graph, const taps_cluster *clust
     std::vector<uint32_t> rep(n_edges);
     std::iota(rep.begin(), rep.end(), 0u);
     if (flags & TAPS_BUILD_SHARED) {
-        std::map<std::vector<int64_t>, uint32_t> first;
-        for (uint32_t e = 0; e < n_edges; ++e) rep[e] = first.emplace(edge_key(graph, e), e).first->second;
+        rep = group_edges(graph);
     }
     std::vector<uint64_t> eoff(n_edges + 1, 0), segs(n_edges + 1, 0);
     uint64_t all_segs = 0;
@@ -835,8 +976,7 @@ taps_status taps_build_tables(const taps_graph *graph, const taps_cluster *clust
                           {copies.data(), sizeof(taps_copy_task) * copies.size(), 0},
                           {dst_list.data(), sizeof(uint64_t) * dst_list.size(), 0}};
     void *dev = nullptr;
-    if ((st = upload(ch, &dev, stream)) != TAPS_OK) return st;
-    sc.adopt(dev);
+    if ((st = upload(sc, ch, &dev)) != TAPS_OK) return st;
     taps_desc *d_desc = nullptr;
     taps_edge_params *d_params = nullptr;
     taps_row_ref *d_segs = nullptr;
@@ -889,8 +1029,7 @@ taps_status taps_node_costs_topology(const taps_graph *graph, const taps_topolog
     std::vector<chunk> ch{{graph->ops, sizeof(taps_op) * n_ops, 0},
                           {op_offsets, sizeof(uint64_t) * (n_ops + 1), 0}};
     void *dev = nullptr;
-    if ((st = upload(ch, &dev, stream)) != TAPS_OK) return st;
-    sc.adopt(dev);
+    if ((st = upload(sc, ch, &dev)) != TAPS_OK) return st;
     taps_desc *d_desc = nullptr;
     if ((st = sc.alloc((void **)&d_desc, sizeof(taps_desc) * total)) != TAPS_OK) return st;
     hipError_t err = taps_launch_describe(strategies, total, d_desc, stream);
@@ -931,8 +1070,7 @@ taps_status taps_memory_costs(const taps_graph *graph, const taps_strategy *stra
     std::vector<chunk> ch{{graph->ops, sizeof(taps_op) * n_ops, 0},
                           {op_offsets, sizeof(uint64_t) * (n_ops + 1), 0}};
     void *dev = nullptr;
-    if ((st = upload(ch, &dev, stream)) != TAPS_OK) return st;
-    sc.adopt(dev);
+    if ((st = upload(sc, ch, &dev)) != TAPS_OK) return st;
     const hipError_t err = taps_launch_memory_costs(at<taps_op>(dev, ch[0]), n_ops,
                                                     at<uint64_t>(dev, ch[1]), strategies, total,
                                                     memory, stream);

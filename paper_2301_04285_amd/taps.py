@@ -529,6 +529,35 @@ def taps_build_tables(graph, cluster, mesh=None, out: Optional["Tables"] = None,
                   {k: v[:n_edge] for k, v in out.edge.items()})
 
 
+class PreparedBuild:
+    """taps_build_tables with every argument packed once, for callers that
+    rebuild the same tables repeatedly (a serving loop, a benchmark): each call
+    only queues the build on the stream.  `out` (a Tables of a build of the same
+    graph) receives the tables; it must stay alive while the object is used."""
+
+    def __init__(self, graph, cluster, out: "Tables", mesh=None, shared=False, stream=None):
+        self._g = _graph(graph)
+        self._cl = pack_cluster(cluster)
+        self._ms = pack_mesh(mesh) if mesh is not None else None
+        self._offs = np.zeros(self._g.n_ops + 1, dtype=np.uint64)
+        self._eoffs = np.zeros(self._g.n_edges + 1, dtype=np.uint64)
+        self._out = out
+        s_cap = min(int(out.strategies.shape[0]), *(int(v.numel()) for v in out.node.values()))
+        e_cap = min(int(v.numel()) for v in out.edge.values())
+        L = load()
+        self._fn = L.taps_build_tables
+        self._args = (C.byref(self._g.struct), C.byref(self._cl),
+                      C.byref(self._ms) if self._ms else None, _u64_array(self._offs),
+                      C.c_void_p(out.strategies.data_ptr()), s_cap, _table(out.node),
+                      _u64_array(self._eoffs), _table(out.edge), e_cap,
+                      BUILD_SHARED if shared else 0, _stream(stream))
+
+    def __call__(self) -> None:
+        st = self._fn(*self._args)
+        if st != OK:
+            _check(st, "taps_build_tables")
+
+
 def build_tables(graph, cluster, device="cuda", stream=None, out: Optional[Tables] = None,
                  shared: bool = False, mesh=None, topology=None, fused: bool = True) -> Tables:
     """Enumeration, node table and edge table of one graph on one cluster.

@@ -371,6 +371,29 @@ def test_fused_build_equals_separate_calls(T):
         assert _same_tables(a.edge, c.edge) and _same_tables(a.node, c.node), name
 
 
+def test_prepared_build_repeats_the_build(T):
+    """PreparedBuild (arguments packed once) fills the tables it was given with
+    what taps_build_tables writes, full and shared, on every call: three calls in
+    a row into cleared tables."""
+    import torch
+    for k in (2, 4):
+        w = W.config(k)
+        cl = w.clusters[-1][1]
+        a = T.build_tables(w.graph, cl)
+        for shared in (False, True):
+            say(f"[gpu] prepared build {w.name} shared={shared}")
+            b = T.taps_build_tables(w.graph, cl)
+            run = T.PreparedBuild(w.graph, cl, b, shared=shared)
+            for _ in range(3):
+                for v in (*b.node.values(), *b.edge.values()):
+                    _signed(v).fill_(-1)
+                b.strategies.fill_(0)
+                run()
+                torch.cuda.synchronize()
+                assert torch.equal(a.strategies, b.strategies), w.name
+                assert _same_tables(a.node, b.node) and _same_tables(a.edge, b.edge), w.name
+
+
 def test_fused_build_capacity_and_errors(T):
     """Capacity and argument errors are reported before any GPU work and leave the
     outputs untouched."""
