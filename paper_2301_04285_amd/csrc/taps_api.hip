@@ -236,6 +236,7 @@ struct stream_block {
     size_t cap = 0;
     size_t want = 0;       // largest need seen on this stream
     uint64_t last_use = 0;
+    uint32_t users = 0;    // calls holding or waiting for mu (under g_blocks_mu)
 };
 std::mutex g_blocks_mu;
 std::list<stream_block> g_blocks;   // stable addresses
@@ -249,13 +250,15 @@ stream_block *find_block(hipStream_t stream) {
     for (stream_block &b : g_blocks)
         if (b.device == device && b.stream == stream) {
             b.last_use = ++g_blocks_clock;
+            ++b.users;
             return &b;
         }
     if (g_blocks.size() >= kMaxBlocks) {   // free the least recently used idle block
+        // idle: no call holds its lock or is about to take it, so nothing else
+        // can reach it while the list lock is held
         auto victim = g_blocks.end();
         for (auto it = g_blocks.begin(); it != g_blocks.end(); ++it) {
-            if (!it->mu.try_lock()) continue;
-            it->mu.unlock();
+            if (it->users) continue;
             if (victim == g_blocks.end() || it->last_use < victim->last_use) victim = it;
         }
         if (victim != g_blocks.end()) {
@@ -275,7 +278,13 @@ stream_block *find_block(hipStream_t stream) {
     b.device = device;
     b.stream = stream;
     b.last_use = ++g_blocks_clock;
+    b.users = 1;
     return &b;
+}
+
+void release_block(stream_block *b) {
+    std::lock_guard<std::mutex> lock(g_blocks_mu);
+    --b->users;
 }
 
 struct scratch {
@@ -304,6 +313,8 @@ struct scratch {
     ~scratch() {
         for (void *p : own) (void)hipFreeAsync(p, stream);
         if (need > blk->want) blk->want = need;
+        lock.unlock();   // before the block may become idle (and be freed)
+        release_block(blk);
     }
     taps_status alloc(void **p, size_t bytes) {
         const size_t size = align256(bytes ? bytes : 256);

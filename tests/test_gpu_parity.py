@@ -394,6 +394,74 @@ def test_prepared_build_repeats_the_build(T):
                 assert _same_tables(a.node, b.node) and _same_tables(a.edge, b.edge), w.name
 
 
+def test_concurrent_builds_streams_and_staging(T):
+    """Single-call builds (full and shared) from 7 threads at once on 5 streams
+    (two pairs of threads share a stream); one build on each of 20 streams in
+    turn (more streams than the library keeps scratch blocks for); and 12
+    builds queued on one stream behind a bounded spin kernel (more uploads in
+    flight than there are staging buffers).  Every table equals the same build
+    made alone."""
+    import threading
+    import torch
+    cases = [(W.config(k).graph, W.config(k).clusters[0][1]) for k in (2, 3, 4)]
+    refs = [T.build_tables(g, cl) for g, cl in cases]
+    torch.cuda.synchronize()
+
+    def same(c, got):
+        ref = refs[c]
+        return (list(got.op_offsets) == list(ref.op_offsets) and
+                torch.equal(got.strategies, ref.strategies) and
+                _same_tables(got.node, ref.node) and _same_tables(got.edge, ref.edge))
+
+    streams = [torch.cuda.Stream() for _ in range(5)]
+    results, errors = {}, []
+
+    def work(t):
+        try:
+            s = streams[t % len(streams)]
+            outs = []
+            with torch.cuda.stream(s):
+                for k in range(6):
+                    c = (t + k) % len(cases)
+                    outs.append((c, T.build_tables(*cases[c], stream=s, shared=k % 2 == 1)))
+            s.synchronize()
+            results[t] = outs
+        except Exception as ex:   # reported below, in the test's thread
+            errors.append(f"thread {t}: {ex!r}")
+
+    say("[gpu] concurrent builds: 7 threads on 5 streams")
+    threads = [threading.Thread(target=work, args=(t,)) for t in range(7)]
+    for th in threads:
+        th.start()
+    for th in threads:
+        th.join(timeout=60)
+    assert not errors, errors
+    assert sorted(results) == list(range(7))
+    for t, outs in results.items():
+        for k, (c, got) in enumerate(outs):
+            assert same(c, got), f"thread {t} build {k} (case {c})"
+
+    say("[gpu] one build on each of 20 streams")
+    outs = []
+    for k in range(20):
+        s = torch.cuda.Stream()
+        with torch.cuda.stream(s):
+            outs.append((k % len(cases), s, T.build_tables(*cases[k % len(cases)], stream=s)))
+    torch.cuda.synchronize()
+    for k, (c, _, got) in enumerate(outs):
+        assert same(c, got), f"stream {k} (case {c})"
+
+    say("[gpu] 12 builds queued behind a spin kernel on one stream")
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        torch.cuda._sleep(20_000_000)
+        outs = [(k % len(cases), T.build_tables(*cases[k % len(cases)], stream=s))
+                for k in range(12)]
+    s.synchronize()
+    for k, (c, got) in enumerate(outs):
+        assert same(c, got), f"queued build {k} (case {c})"
+
+
 def test_fused_build_capacity_and_errors(T):
     """Capacity and argument errors are reported before any GPU work and leave the
     outputs untouched."""
