@@ -516,6 +516,66 @@ void plan_copies(const std::vector<uint64_t> &eoff, const std::vector<uint32_t> 
     }
 }
 
+// Row segments of every computed table (rep[e] == e; rows are the source
+// side's strategies, columns the target side's): each row cut into segments
+// of `cols` columns and its remainder.  Ordered, the launch takes every
+// full-length segment first (edges in order, a row's segments together) and
+// the remainders last, longest first, so that it ends on its shortest
+// segments; otherwise each row's segments, remainder included, run together.
+// Returns the number of segments.
+uint64_t plan_segments(const taps_graph *graph, const uint64_t *op_offsets, bool reverse,
+                       const std::vector<uint32_t> &rep, uint32_t cols, bool ordered,
+                       std::vector<taps_seg_group> &groups) {
+    struct remainder {
+        uint32_t edge, rows, first_col, cols;
+    };
+    std::vector<remainder> rems;
+    groups.clear();
+    uint64_t start = 0;
+    for (uint32_t e = 0; e < graph->n_edges; ++e) {
+        if (rep[e] != e) continue;
+        const taps_edge &E = graph->edges[e];
+        const uint64_t np = op_offsets[E.src_op + 1] - op_offsets[E.src_op];
+        const uint64_t nc = op_offsets[E.dst_op + 1] - op_offsets[E.dst_op];
+        const uint64_t ns = reverse ? nc : np, nd = reverse ? np : nc;
+        if (ns == 0 || nd == 0) continue;
+        if (!ordered) {
+            const uint64_t per_row = (nd + cols - 1) / cols;
+            groups.push_back({start, e, (uint32_t)per_row, 0u, cols});
+            start += ns * per_row;
+            continue;
+        }
+        const uint64_t full = nd / cols, left = nd % cols;
+        if (full) {
+            groups.push_back({start, e, (uint32_t)full, 0u, cols});
+            start += ns * full;
+        }
+        if (left) rems.push_back({e, (uint32_t)ns, (uint32_t)(full * cols), (uint32_t)left});
+    }
+    std::stable_sort(rems.begin(), rems.end(),
+                     [](const remainder &a, const remainder &b) { return a.cols > b.cols; });
+    for (const remainder &r : rems) {
+        groups.push_back({start, r.edge, 1u, r.first_col, r.cols});
+        start += r.rows;
+    }
+    return start;
+}
+
+// The segments of a launch: one table, long segments (remainders last) when
+// there are enough of them to fill the GPU many times over, else short ones;
+// several tables (the bandwidth sweep), short ones in row order.
+uint64_t plan_launch(const taps_graph *graph, const uint64_t *op_offsets, bool reverse,
+                     const std::vector<uint32_t> &rep, bool one_table,
+                     std::vector<taps_seg_group> &groups) {
+    if (one_table) {
+        const uint64_t n = plan_segments(graph, op_offsets, reverse, rep,
+                                         TAPS_TILE_COLS * TAPS_SEG_TILES_LONG, true, groups);
+        if (n >= TAPS_LONG_SEGS_MIN) return n;
+    }
+    return plan_segments(graph, op_offsets, reverse, rep, TAPS_TILE_COLS * TAPS_SEG_TILES_SHORT,
+                         one_table, groups);
+}
+
 // Edge tables of one graph at n_points bandwidth points (clusters that differ
 // only in their bandwidths), table k in outs[k]; outs NULL or every table's
 // arrays NULL: size query.
@@ -552,8 +612,7 @@ taps_status edge_costs(const taps_graph *graph, const taps_cluster *clusters, ui
         const uint64_t nc = op_offsets[E.dst_op + 1] - op_offsets[E.dst_op];
         const uint64_t ns = reverse ? nc : np, nd = reverse ? np : nc;   // rows, columns
         eoff[e + 1] = eoff[e] + ns * nd;
-        all_segs += ns * ((nd + TAPS_TILE_COLS * TAPS_SEG_TILES - 1) /
-                          (TAPS_TILE_COLS * TAPS_SEG_TILES));
+        all_segs += ns * ((nd + TAPS_TILE_COLS - 1) / TAPS_TILE_COLS);
     }
     bool none = true, all = outs != nullptr;
     for (uint32_t k = 0; outs && k < n_points; ++k) {
@@ -577,16 +636,8 @@ taps_status edge_costs(const taps_graph *graph, const taps_cluster *clusters, ui
     if (share && (st = share_edges(graph, op_offsets, strategies, stream, rep)) != TAPS_OK)
         return st;
     // row segments of every computed table (shared tables: the first of each group)
-    std::vector<uint64_t> segs(n_edges + 1, 0);
-    for (uint32_t e = 0; e < n_edges; ++e) {
-        const taps_edge &E = graph->edges[e];
-        const uint64_t np = op_offsets[E.src_op + 1] - op_offsets[E.src_op];
-        const uint64_t nc = op_offsets[E.dst_op + 1] - op_offsets[E.dst_op];
-        const uint64_t ns = reverse ? nc : np, nd = reverse ? np : nc;
-        const uint64_t per_row = (nd + TAPS_TILE_COLS * TAPS_SEG_TILES - 1) /
-                                 (TAPS_TILE_COLS * TAPS_SEG_TILES);
-        segs[e + 1] = segs[e] + (rep[e] == e ? ns * per_row : 0);
-    }
+    std::vector<taps_seg_group> groups;
+    const uint64_t n_segs = plan_launch(graph, op_offsets, reverse, rep, n_points == 1, groups);
     // shared tables: every chunk of a computed table is stored into each table sharing it
     std::vector<uint64_t> dst_list;
     std::vector<taps_copy_task> copies;
@@ -594,12 +645,11 @@ taps_status edge_costs(const taps_graph *graph, const taps_cluster *clusters, ui
     if (copies.size() > 0x7FFFFFFFull) return fail(TAPS_ERR_ARG, "too many table copies");
     scratch sc(stream);
     const uint64_t total = op_offsets[n_ops];
-    const uint64_t n_segs = segs[n_edges];
     std::vector<chunk> ch{{graph->ops, sizeof(taps_op) * n_ops, 0},
                           {graph->edges, sizeof(taps_edge) * n_edges, 0},
                           {op_offsets, sizeof(uint64_t) * (n_ops + 1), 0},
                           {eoff.data(), sizeof(uint64_t) * (n_edges + 1), 0},
-                          {segs.data(), sizeof(uint64_t) * (n_edges + 1), 0},
+                          {groups.data(), sizeof(taps_seg_group) * groups.size(), 0},
                           {copies.data(), sizeof(taps_copy_task) * copies.size(), 0},
                           {dst_list.data(), sizeof(uint64_t) * dst_list.size(), 0}};
     void *dev = nullptr;
@@ -614,8 +664,8 @@ taps_status edge_costs(const taps_graph *graph, const taps_cluster *clusters, ui
     if (err == hipSuccess)
         err = taps_launch_edge_setup(at<taps_op>(dev, ch[0]), at<taps_edge>(dev, ch[1]), n_edges,
                                      at<uint64_t>(dev, ch[2]), at<uint64_t>(dev, ch[3]),
-                                     at<uint64_t>(dev, ch[4]), lp, reverse, d_params, n_segs,
-                                     d_segs, stream);
+                                     at<taps_seg_group>(dev, ch[4]), (uint32_t)groups.size(), lp,
+                                     reverse, d_params, n_segs, d_segs, stream);
     // the edge-table kernel launches (entries > 0): use the events, if any, once
     const hipEvent_t before = g_kernel_before, after = g_kernel_after;
     g_kernel_before = g_kernel_after = nullptr;
@@ -938,17 +988,14 @@ taps_status taps_build_tables(const taps_graph *graph, const taps_cluster *clust
     if (flags & TAPS_BUILD_SHARED) {
         rep = group_edges(graph);
     }
-    std::vector<uint64_t> eoff(n_edges + 1, 0), segs(n_edges + 1, 0);
+    std::vector<uint64_t> eoff(n_edges + 1, 0);
     uint64_t all_segs = 0;
     for (uint32_t e = 0; e < n_edges; ++e) {
         const taps_edge &E = graph->edges[e];
         const uint64_t ns = offs[E.src_op + 1] - offs[E.src_op];
         const uint64_t nd = offs[E.dst_op + 1] - offs[E.dst_op];
-        const uint64_t per_row = (nd + TAPS_TILE_COLS * TAPS_SEG_TILES - 1) /
-                                 (TAPS_TILE_COLS * TAPS_SEG_TILES);
         eoff[e + 1] = eoff[e] + ns * nd;
-        segs[e + 1] = segs[e] + (rep[e] == e ? ns * per_row : 0);
-        all_segs += ns * per_row;
+        all_segs += ns * ((nd + TAPS_TILE_COLS - 1) / TAPS_TILE_COLS);
     }
     if (all_segs >= 0x7FFFFFFFull) return fail(TAPS_ERR_ARG, "more than 2^31 row segments");
     std::vector<uint64_t> dst_list;
@@ -978,12 +1025,14 @@ taps_status taps_build_tables(const taps_graph *graph, const taps_cluster *clust
     // one upload and one set of scratch for the whole build
     hipStream_t stream = (hipStream_t)stream_;
     scratch sc(stream);
-    const uint64_t total = offs[n_ops], n_segs = segs[n_edges];
+    std::vector<taps_seg_group> groups;
+    const uint64_t total = offs[n_ops];
+    const uint64_t n_segs = plan_launch(graph, offs.data(), false, rep, true, groups);
     std::vector<chunk> ch{{graph->ops, sizeof(taps_op) * n_ops, 0},
                           {graph->edges, sizeof(taps_edge) * n_edges, 0},
                           {offs.data(), sizeof(uint64_t) * (n_ops + 1), 0},
                           {eoff.data(), sizeof(uint64_t) * (n_edges + 1), 0},
-                          {segs.data(), sizeof(uint64_t) * (n_edges + 1), 0},
+                          {groups.data(), sizeof(taps_seg_group) * groups.size(), 0},
                           {copies.data(), sizeof(taps_copy_task) * copies.size(), 0},
                           {dst_list.data(), sizeof(uint64_t) * dst_list.size(), 0}};
     void *dev = nullptr;
@@ -1003,8 +1052,8 @@ taps_status taps_build_tables(const taps_graph *graph, const taps_cluster *clust
     if (err == hipSuccess && eoff[n_edges] > 0) {
         err = taps_launch_edge_setup(d_ops, at<taps_edge>(dev, ch[1]), n_edges,
                                      at<uint64_t>(dev, ch[2]), at<uint64_t>(dev, ch[3]),
-                                     at<uint64_t>(dev, ch[4]), lp, false, d_params, n_segs, d_segs,
-                                     stream);
+                                     at<taps_seg_group>(dev, ch[4]), (uint32_t)groups.size(), lp,
+                                     false, d_params, n_segs, d_segs, stream);
         const hipEvent_t before = g_kernel_before, after = g_kernel_after;
         g_kernel_before = g_kernel_after = nullptr;
         if (err == hipSuccess && before) err = hipEventRecord(before, stream);

@@ -21,7 +21,6 @@ struct taps_launch {
 // Per-edge constants of the edge-table kernel.
 struct taps_edge_params {
     uint64_t out_offset;   // first entry of the edge's table
-    uint64_t seg_begin;    // first row segment of the edge (segments of all edges, in order)
     taps_scaler scale;     // tbytes and the per-unit seconds of the edge tensor
     uint32_t src_base;     // first strategy of the source side (producer; consumer for
     uint32_t dst_base;     //   the backward tables) and of the target side
@@ -42,20 +41,41 @@ struct taps_copy_task {
 #define TAPS_COPY_CHUNK 2048    // entries per copy task (8 per thread of 256)
 #define TAPS_COPY_DSTS 6        // tables one copy task writes (4-6 measured best, 16 is 20 % slower)
 
-// One wavefront per row segment: producer strategy i of one edge and up to
-// TAPS_SEG_TILES tiles of 64 consecutive consumer strategies, walked 64 at a
-// time.  A workgroup holds TAPS_ROWS_PER_BLOCK segments.
+// One wavefront per row segment: producer strategy i of one edge and the
+// consumer strategies [first_col, last_col) of its row, walked 64 at a time.
+// A workgroup holds TAPS_ROWS_PER_BLOCK segments.  A segment builds its
+// producer side once (about 0.15 ms of the 96-layer GPT's launch at two
+// tiles per segment); TAPS_SEG_TILES_LONG tiles amortise that in launches of
+// many segments, and launching the full-length segments before the shorter
+// remainders keeps the longer segments from stretching the end of the launch
+// (1, 2, 4, 8, 16 and 32 tiles measured).  Launches with few segments use
+// TAPS_SEG_TILES_SHORT.  The bandwidth sweep, bound by its four sets of
+// stores per entry, keeps short segments in row order: a row's remainder
+// written long after its full-length segments leaves the 128-byte lines they
+// share to reach HBM in two partial writes.
 #define TAPS_TILE_COLS 64
-#define TAPS_SEG_TILES 2
+#define TAPS_SEG_TILES_LONG 8
+#define TAPS_SEG_TILES_SHORT 2
+#define TAPS_LONG_SEGS_MIN 32768   // long segments only when there are at least this many
 #define TAPS_ROWS_PER_BLOCK 2
 
-// Segment r of the flat segment list: its edge, the global index of its
-// producer strategy and its first consumer strategy.
+// A run of row segments of one edge: every row of the edge's table cut into
+// per_row segments of `cols` consumer strategies from first_col, the last
+// one ending at the row's end at the latest.  Segment r of a launch belongs
+// to the last group whose start is at most r: row (r - start) / per_row,
+// first consumer first_col + ((r - start) % per_row) * cols.
+struct taps_seg_group {
+    uint64_t start;
+    uint32_t edge, per_row, first_col, cols;
+};
+
+// Segment r of a launch: its edge, the global index of its producer strategy
+// and its consumer strategies [first_col, last_col).
 struct taps_row_ref {
     uint32_t edge;
     uint32_t strategy;
     uint32_t first_col;
-    uint32_t pad;
+    uint32_t last_col;
 };
 
 hipError_t taps_launch_describe(const taps_strategy *s, uint64_t total, taps_desc *desc,
@@ -66,9 +86,9 @@ hipError_t taps_launch_node_costs(const taps_op *ops, uint32_t n_ops, const uint
 // reverse: the backward tables (source side = the consumer's input map).
 hipError_t taps_launch_edge_setup(const taps_op *ops, const taps_edge *edges, uint32_t n_edges,
                                   const uint64_t *op_offsets, const uint64_t *edge_offsets,
-                                  const uint64_t *seg_begin, const taps_launch &lp,
-                                  bool reverse, taps_edge_params *params, uint64_t n_segs,
-                                  taps_row_ref *segs, hipStream_t stream);
+                                  const taps_seg_group *groups, uint32_t n_groups,
+                                  const taps_launch &lp, bool reverse, taps_edge_params *params,
+                                  uint64_t n_segs, taps_row_ref *segs, hipStream_t stream);
 hipError_t taps_launch_edge_costs(const taps_edge_params *params, const taps_row_ref *rows,
                                   uint64_t n_rows, const taps_desc *desc, const taps_launch &lp,
                                   taps_table out, hipStream_t stream);

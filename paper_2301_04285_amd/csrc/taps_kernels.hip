@@ -8,10 +8,11 @@
 //   k_memory_costs one thread per strategy: weight and output shard bytes
 //   k_edge_setup  one thread per edge: per-edge constants
 //   k_row_map     one thread per row segment: its edge, producer strategy
-//                 and first consumer strategy
+//                 and first consumer strategy (every edge's full-length
+//                 segments first, the rows' remainders last, longest first)
 //   k_edge_costs  one wavefront per row segment (one producer strategy,
-//                 uniform: its descriptor sits in scalar registers; up to
-//                 TAPS_SEG_TILES tiles of 64 consumer strategies, one per lane, the
+//                 uniform: its descriptor sits in scalar registers; 2 or 8
+//                 tiles of 64 consumer strategies, one per lane, the
 //                 next 64 prefetched), TAPS_ROWS_PER_BLOCK segments per workgroup; five
 //                 coalesced SoA stores per entry
 //   k_edge_costs_sweep  as k_edge_costs for several bandwidth points: the
@@ -226,7 +227,6 @@ __global__ __launch_bounds__(256) void k_edge_setup(const taps_op *__restrict__ 
                                                     uint32_t n_edges,
                                                     const uint64_t *__restrict__ op_offsets,
                                                     const uint64_t *__restrict__ edge_offsets,
-                                                    const uint64_t *__restrict__ seg_begin,
                                                     taps_launch lp, uint32_t reverse,
                                                     taps_edge_params *__restrict__ params) {
     const uint32_t e = blockIdx.x * blockDim.x + threadIdx.x;
@@ -238,7 +238,6 @@ __global__ __launch_bounds__(256) void k_edge_setup(const taps_op *__restrict__ 
     const taps_tensor &Tc = dst.in[E.dst_slot];
     taps_edge_params p;
     p.out_offset = edge_offsets[e];
-    p.seg_begin = seg_begin[e];
     uint64_t bytes = src.dtype_bytes;
     uint32_t pa = 0, ca = 0;
     for (uint32_t d = 0; d < T.rank && d < TAPS_MAX_RANK; ++d) {
@@ -261,23 +260,29 @@ __global__ __launch_bounds__(256) void k_edge_setup(const taps_op *__restrict__ 
     params[e] = p;
 }
 
-__global__ __launch_bounds__(256) void k_row_map(const uint64_t *__restrict__ seg_begin,
-                                                 const uint64_t *__restrict__ op_offsets,
-                                                 const taps_edge *__restrict__ edges,
+__global__ __launch_bounds__(256) void k_row_map(const taps_seg_group *__restrict__ groups,
+                                                 uint32_t n_groups,
                                                  const taps_edge_params *__restrict__ params,
-                                                 uint32_t n_edges, uint64_t n_segs,
-                                                 taps_row_ref *__restrict__ segs) {
+                                                 uint64_t n_segs, taps_row_ref *__restrict__ segs) {
     const uint64_t r = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (r >= n_segs) return;
-    const uint32_t e = find_owner(seg_begin, n_edges, r);
-    const uint32_t nd = params[e].nd;
-    const uint64_t per_row = (nd + TAPS_TILE_COLS * TAPS_SEG_TILES - 1) / (TAPS_TILE_COLS * TAPS_SEG_TILES);
-    const uint64_t k = r - seg_begin[e];
+    // the last group starting at or before r (groups[0].start == 0)
+    uint32_t lo = 0, hi = n_groups - 1;
+    while (lo < hi) {
+        const uint32_t mid = (lo + hi + 1) / 2;
+        if (groups[mid].start <= r)
+            lo = mid;
+        else
+            hi = mid - 1;
+    }
+    const taps_seg_group G = groups[lo];
+    const uint64_t k = r - G.start;
     taps_row_ref ref;
-    ref.edge = e;
-    ref.strategy = (uint32_t)(params[e].src_base + k / per_row);
-    ref.first_col = (uint32_t)(k % per_row) * (TAPS_TILE_COLS * TAPS_SEG_TILES);
-    ref.pad = 0;
+    ref.edge = G.edge;
+    ref.strategy = (uint32_t)(params[G.edge].src_base + k / G.per_row);
+    ref.first_col = G.first_col + (uint32_t)(k % G.per_row) * G.cols;
+    const uint32_t nd = params[G.edge].nd;
+    ref.last_col = nd - ref.first_col < G.cols ? nd : ref.first_col + G.cols;
     segs[r] = ref;
 }
 
@@ -307,8 +312,7 @@ __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_co
     const uint64_t row_out = E.out_offset + (uint64_t)i * E.nd;
     const taps_desc *col = desc + E.dst_base;
     const uint32_t c0 = ref.first_col;
-    const uint32_t c1 = E.nd - c0 < TAPS_TILE_COLS * TAPS_SEG_TILES ? E.nd
-                                                                       : c0 + TAPS_TILE_COLS * TAPS_SEG_TILES;
+    const uint32_t c1 = ref.last_col;
     // consumer descriptors one tile ahead
     taps_desc next = col[c0 + lane < c1 ? c0 + lane : c0];
     for (uint32_t j0 = c0; j0 < c1; j0 += TAPS_TILE_COLS) {
@@ -352,8 +356,7 @@ __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_co
     const uint64_t row_out = E.out_offset + (uint64_t)i * E.nd;
     const taps_desc *col = desc + E.dst_base;
     const uint32_t c0 = ref.first_col;
-    const uint32_t c1 = E.nd - c0 < TAPS_TILE_COLS * TAPS_SEG_TILES ? E.nd
-                                                                       : c0 + TAPS_TILE_COLS * TAPS_SEG_TILES;
+    const uint32_t c1 = ref.last_col;
     taps_desc next = col[c0 + lane < c1 ? c0 + lane : c0];
     for (uint32_t j0 = c0; j0 < c1; j0 += TAPS_TILE_COLS) {
         const taps_desc cur = next;
@@ -402,8 +405,7 @@ __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_co
     const uint64_t row_out = E.out_offset + (uint64_t)i * E.nd;
     const taps_desc *col = desc + E.dst_base;
     const uint32_t c0 = ref.first_col;
-    const uint32_t c1 = E.nd - c0 < TAPS_TILE_COLS * TAPS_SEG_TILES ? E.nd
-                                                                       : c0 + TAPS_TILE_COLS * TAPS_SEG_TILES;
+    const uint32_t c1 = ref.last_col;
     for (uint32_t j = c0 + lane; j < c1; j += TAPS_TILE_COLS) {
         taps_col Q;
         taps_make_col(Q, col[j], E.caxes, E.rank);
@@ -542,17 +544,16 @@ hipError_t taps_launch_memory_costs(const taps_op *ops, uint32_t n_ops, const ui
 
 hipError_t taps_launch_edge_setup(const taps_op *ops, const taps_edge *edges, uint32_t n_edges,
                                   const uint64_t *op_offsets, const uint64_t *edge_offsets,
-                                  const uint64_t *seg_begin, const taps_launch &lp,
-                                  bool reverse, taps_edge_params *params, uint64_t n_segs,
-                                  taps_row_ref *segs, hipStream_t stream) {
+                                  const taps_seg_group *groups, uint32_t n_groups,
+                                  const taps_launch &lp, bool reverse, taps_edge_params *params,
+                                  uint64_t n_segs, taps_row_ref *segs, hipStream_t stream) {
     if (n_edges == 0) return hipSuccess;
     hipLaunchKernelGGL(k_edge_setup, dim3(blocks_for(n_edges, 256)), dim3(256), 0, stream, ops,
-                       edges, n_edges, op_offsets, edge_offsets, seg_begin, lp,
-                       reverse ? 1u : 0u, params);
+                       edges, n_edges, op_offsets, edge_offsets, lp, reverse ? 1u : 0u, params);
     hipError_t err = hipGetLastError();
-    if (err != hipSuccess || n_segs == 0) return err;
-    hipLaunchKernelGGL(k_row_map, dim3(blocks_for(n_segs, 256)), dim3(256), 0, stream, seg_begin,
-                       op_offsets, edges, params, n_edges, n_segs, segs);
+    if (err != hipSuccess || n_segs == 0 || n_groups == 0) return err;
+    hipLaunchKernelGGL(k_row_map, dim3(blocks_for(n_segs, 256)), dim3(256), 0, stream, groups,
+                       n_groups, params, n_segs, segs);
     return hipGetLastError();
 }
 
