@@ -516,6 +516,16 @@ void plan_copies(const std::vector<uint64_t> &eoff, const std::vector<uint32_t> 
     }
 }
 
+// The largest rank of the tensors the edges carry (the producers' outputs).
+uint32_t max_edge_rank(const taps_graph *graph) {
+    uint32_t r = 0;
+    for (uint32_t e = 0; e < graph->n_edges; ++e) {
+        const uint32_t k = graph->ops[graph->edges[e].src_op].out.rank;
+        r = k > r ? k : r;
+    }
+    return r;
+}
+
 // Row segments of every computed table (rep[e] == e; rows are the source
 // side's strategies, columns the target side's): each row cut into segments
 // of `cols` columns and its remainder.  Ordered, the launch takes every
@@ -671,9 +681,11 @@ taps_status edge_costs(const taps_graph *graph, const taps_cluster *clusters, ui
     g_kernel_before = g_kernel_after = nullptr;
     if (err == hipSuccess && before) err = hipEventRecord(before, stream);
     if (err == hipSuccess && hier) {
-        err = taps_launch_edge_costs_h(d_params, d_segs, n_segs, d_desc, lp, *hier, outs[0], stream);
+        err = taps_launch_edge_costs_h(d_params, d_segs, n_segs, d_desc, lp, max_edge_rank(graph),
+                                       *hier, outs[0], stream);
     } else if (err == hipSuccess && n_points == 1) {
-        err = taps_launch_edge_costs(d_params, d_segs, n_segs, d_desc, lp, outs[0], stream);
+        err = taps_launch_edge_costs(d_params, d_segs, n_segs, d_desc, lp, max_edge_rank(graph),
+                                     outs[0], stream);
     } else if (err == hipSuccess) {
         taps_sweep sw;
         std::memset(&sw, 0, sizeof(sw));
@@ -686,7 +698,8 @@ taps_status edge_costs(const taps_graph *graph, const taps_cluster *clusters, ui
             sw.inv_n_binter[k] = lps[k].inv_n_binter;
             sw.out[k] = outs[k];
         }
-        err = taps_launch_edge_costs_sweep(d_params, d_segs, n_segs, d_desc, lp, sw, stream);
+        err = taps_launch_edge_costs_sweep(d_params, d_segs, n_segs, d_desc, lp,
+                                           max_edge_rank(graph), sw, stream);
     }
     for (uint32_t k = 0; k < n_points && err == hipSuccess; ++k)
         err = taps_launch_copy_tables(at<taps_copy_task>(dev, ch[5]), (uint32_t)copies.size(),
@@ -1058,7 +1071,8 @@ taps_status taps_build_tables(const taps_graph *graph, const taps_cluster *clust
         g_kernel_before = g_kernel_after = nullptr;
         if (err == hipSuccess && before) err = hipEventRecord(before, stream);
         if (err == hipSuccess)
-            err = taps_launch_edge_costs(d_params, d_segs, n_segs, d_desc, lp, edge, stream);
+            err = taps_launch_edge_costs(d_params, d_segs, n_segs, d_desc, lp,
+                                         max_edge_rank(graph), edge, stream);
         if (err == hipSuccess)
             err = taps_launch_copy_tables(at<taps_copy_task>(dev, ch[5]), (uint32_t)copies.size(),
                                           at<uint64_t>(dev, ch[6]), edge, stream);

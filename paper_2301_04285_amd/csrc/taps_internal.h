@@ -89,9 +89,13 @@ hipError_t taps_launch_edge_setup(const taps_op *ops, const taps_edge *edges, ui
                                   const taps_seg_group *groups, uint32_t n_groups,
                                   const taps_launch &lp, bool reverse, taps_edge_params *params,
                                   uint64_t n_segs, taps_row_ref *segs, hipStream_t stream);
+// max_rank: the largest tensor rank of the launch's edges; up to
+// TAPS_LOW_RANK the kernels are compiled for that many dimensions (fewer
+// registers for the producer side, shorter per-dimension loops).
+#define TAPS_LOW_RANK 4
 hipError_t taps_launch_edge_costs(const taps_edge_params *params, const taps_row_ref *rows,
                                   uint64_t n_rows, const taps_desc *desc, const taps_launch &lp,
-                                  taps_table out, hipStream_t stream);
+                                  uint32_t max_rank, taps_table out, hipStream_t stream);
 hipError_t taps_launch_memory_costs(const taps_op *ops, uint32_t n_ops, const uint64_t *offsets,
                                    const taps_strategy *s, uint64_t total, uint64_t *memory,
                                    hipStream_t stream);
@@ -108,8 +112,8 @@ struct taps_sweep {
 };
 hipError_t taps_launch_edge_costs_sweep(const taps_edge_params *params, const taps_row_ref *rows,
                                         uint64_t n_rows, const taps_desc *desc,
-                                        const taps_launch &lp, const taps_sweep &sw,
-                                        hipStream_t stream);
+                                        const taps_launch &lp, uint32_t max_rank,
+                                        const taps_sweep &sw, hipStream_t stream);
 // Strategies of every operator in one launch (one workgroup per operator),
 // with their descriptors and node records unless desc / node.t are NULL;
 // op_offsets: device copy of the host's counts.
@@ -120,7 +124,8 @@ hipError_t taps_launch_build_strategies(const taps_op *ops, uint32_t n_ops,
 // Link-class hierarchies: the edge and node tables under the classes of H.
 hipError_t taps_launch_edge_costs_h(const taps_edge_params *params, const taps_row_ref *rows,
                                     uint64_t n_rows, const taps_desc *desc, const taps_launch &lp,
-                                    const taps_hier &H, taps_table out, hipStream_t stream);
+                                    uint32_t max_rank, const taps_hier &H, taps_table out,
+                                    hipStream_t stream);
 hipError_t taps_launch_node_costs_h(const taps_op *ops, uint32_t n_ops, const uint64_t *offsets,
                                     const taps_desc *desc, uint64_t total, uint32_t n,
                                     const taps_hier &H, taps_table out, hipStream_t stream);

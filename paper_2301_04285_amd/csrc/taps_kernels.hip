@@ -286,6 +286,7 @@ __global__ __launch_bounds__(256) void k_row_map(const taps_seg_group *__restric
     segs[r] = ref;
 }
 
+template <uint32_t R>
 __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_costs(
     const taps_edge_params *__restrict__ params, const taps_row_ref *__restrict__ rows,
     uint32_t n_segs, const taps_desc *__restrict__ desc, taps_launch lp, taps_table out) {
@@ -296,6 +297,7 @@ __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_co
     const bool live = r < n_segs;
     const taps_row_ref ref = rows[live ? r : 0u];
     const taps_edge_params E = params[ref.edge];
+    __builtin_assume(E.rank <= R);   // the launch's tensors have rank R at most
     const taps_desc Dp = desc[ref.strategy];
     const uint32_t i = ref.strategy - E.src_base;
     taps_row P;
@@ -331,6 +333,7 @@ __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_co
 
 // Several bandwidth points: the candidates of each entry are costed once and
 // selected, scaled and stored once per point.
+template <uint32_t R>
 __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_costs_sweep(
     const taps_edge_params *__restrict__ params, const taps_row_ref *__restrict__ rows,
     uint32_t n_segs, const taps_desc *__restrict__ desc, taps_launch lp, taps_sweep sw) {
@@ -341,6 +344,7 @@ __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_co
     const bool live = r < n_segs;
     const taps_row_ref ref = rows[live ? r : 0u];
     const taps_edge_params E = params[ref.edge];
+    __builtin_assume(E.rank <= R);   // the launch's tensors have rank R at most
     const taps_desc Dp = desc[ref.strategy];
     const uint32_t i = ref.strategy - E.src_base;
     taps_row P;
@@ -383,6 +387,7 @@ __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_co
 
 // Link-class hierarchies: as k_edge_costs, each entry selected and scaled
 // under the classes of H.
+template <uint32_t R>
 __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_costs_h(
     const taps_edge_params *__restrict__ params, const taps_row_ref *__restrict__ rows,
     uint32_t n_segs, const taps_desc *__restrict__ desc, taps_launch lp, taps_hier H,
@@ -394,6 +399,7 @@ __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_co
     const bool live = r < n_segs;
     const taps_row_ref ref = rows[live ? r : 0u];
     const taps_edge_params E = params[ref.edge];
+    __builtin_assume(E.rank <= R);   // the launch's tensors have rank R at most
     const taps_desc Dp = desc[ref.strategy];
     const uint32_t i = ref.strategy - E.src_base;
     taps_row P;
@@ -559,22 +565,30 @@ hipError_t taps_launch_edge_setup(const taps_op *ops, const taps_edge *edges, ui
 
 hipError_t taps_launch_edge_costs(const taps_edge_params *params, const taps_row_ref *segs,
                                   uint64_t n_segs, const taps_desc *desc, const taps_launch &lp,
-                                  taps_table out, hipStream_t stream) {
+                                  uint32_t max_rank, taps_table out, hipStream_t stream) {
     if (n_segs == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_edge_costs, dim3(blocks_for(n_segs, TAPS_ROWS_PER_BLOCK)),
-                       dim3(TAPS_TILE_COLS * TAPS_ROWS_PER_BLOCK), 0, stream, params, segs,
-                       (uint32_t)n_segs, desc, lp, out);
+    const dim3 grid(blocks_for(n_segs, TAPS_ROWS_PER_BLOCK)), block(TAPS_TILE_COLS * TAPS_ROWS_PER_BLOCK);
+    if (max_rank <= TAPS_LOW_RANK)
+        hipLaunchKernelGGL(k_edge_costs<TAPS_LOW_RANK>, grid, block, 0, stream, params, segs,
+                           (uint32_t)n_segs, desc, lp, out);
+    else
+        hipLaunchKernelGGL(k_edge_costs<TAPS_D_MAX_RANK>, grid, block, 0, stream, params, segs,
+                           (uint32_t)n_segs, desc, lp, out);
     return hipGetLastError();
 }
 
 hipError_t taps_launch_edge_costs_sweep(const taps_edge_params *params, const taps_row_ref *segs,
                                         uint64_t n_segs, const taps_desc *desc,
-                                        const taps_launch &lp, const taps_sweep &sw,
-                                        hipStream_t stream) {
+                                        const taps_launch &lp, uint32_t max_rank,
+                                        const taps_sweep &sw, hipStream_t stream) {
     if (n_segs == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_edge_costs_sweep, dim3(blocks_for(n_segs, TAPS_ROWS_PER_BLOCK)),
-                       dim3(TAPS_TILE_COLS * TAPS_ROWS_PER_BLOCK), 0, stream, params, segs,
-                       (uint32_t)n_segs, desc, lp, sw);
+    const dim3 grid(blocks_for(n_segs, TAPS_ROWS_PER_BLOCK)), block(TAPS_TILE_COLS * TAPS_ROWS_PER_BLOCK);
+    if (max_rank <= TAPS_LOW_RANK)
+        hipLaunchKernelGGL(k_edge_costs_sweep<TAPS_LOW_RANK>, grid, block, 0, stream, params, segs,
+                           (uint32_t)n_segs, desc, lp, sw);
+    else
+        hipLaunchKernelGGL(k_edge_costs_sweep<TAPS_D_MAX_RANK>, grid, block, 0, stream, params,
+                           segs, (uint32_t)n_segs, desc, lp, sw);
     return hipGetLastError();
 }
 
@@ -590,11 +604,16 @@ hipError_t taps_launch_build_strategies(const taps_op *ops, uint32_t n_ops,
 
 hipError_t taps_launch_edge_costs_h(const taps_edge_params *params, const taps_row_ref *rows,
                                     uint64_t n_rows, const taps_desc *desc, const taps_launch &lp,
-                                    const taps_hier &H, taps_table out, hipStream_t stream) {
+                                    uint32_t max_rank, const taps_hier &H, taps_table out,
+                                    hipStream_t stream) {
     if (n_rows == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_edge_costs_h, dim3(blocks_for(n_rows, TAPS_ROWS_PER_BLOCK)),
-                       dim3(TAPS_TILE_COLS * TAPS_ROWS_PER_BLOCK), 0, stream, params, rows,
-                       (uint32_t)n_rows, desc, lp, H, out);
+    const dim3 grid(blocks_for(n_rows, TAPS_ROWS_PER_BLOCK)), block(TAPS_TILE_COLS * TAPS_ROWS_PER_BLOCK);
+    if (max_rank <= TAPS_LOW_RANK)
+        hipLaunchKernelGGL(k_edge_costs_h<TAPS_LOW_RANK>, grid, block, 0, stream, params, rows,
+                           (uint32_t)n_rows, desc, lp, H, out);
+    else
+        hipLaunchKernelGGL(k_edge_costs_h<TAPS_D_MAX_RANK>, grid, block, 0, stream, params, rows,
+                           (uint32_t)n_rows, desc, lp, H, out);
     return hipGetLastError();
 }
 

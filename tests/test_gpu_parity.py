@@ -208,6 +208,53 @@ def test_random_graphs_and_meshes(T):
     assert done >= 20
 
 
+def _within_tensor_limit(g):
+    """Every tensor of g within the library's 2^40-byte bound."""
+    for op in g.ops:
+        for t in (op.out, *op.ins, *op.ws):
+            size = op.dtype_bytes
+            for a in t:
+                size *= op.axis_len[a]
+            if size > 1 << 40:
+                return False
+    return True
+
+
+def test_high_rank_tensors(T):
+    """Edges carrying tensors of rank 5 to 8 (the launches that cannot use the
+    kernels compiled for rank 4 at most), beside edges of low rank in the same
+    graph: the two-class tables entry by entry, the bandwidth sweep and the
+    link-class tables, against the oracle."""
+    from paper_2301_04285_amd.taps import TapsError
+    rng = random.Random(4285)
+    done, top_rank = 0, 0
+    while done < 10:
+        g = W.random_graph(rng, rng.randint(2, 5), max_axes=8, max_rank=8, len_pow_range=(1, 6))
+        n = rng.randint(1, 6)
+        L = 1 << rng.randint(0, n)
+        cl = W.Cluster((1 << n) // L, L, rng.choice([600, 200]) * W.GB,
+                       rng.choice([100, 25]) * W.GB)
+        rank = max((len(g.ops[e.src].out) for e in g.edges), default=0)
+        if rank <= 4 or not _within_tensor_limit(g) or _entries(g, cl.devices) > 300_000:
+            continue
+        name = f"rank {rank} graph {done} N={cl.devices} L={cl.devices_per_node}"
+        try:
+            full_check(T, g, cl, name)
+        except TapsError as ex:
+            assert ex.status == T.ERR_NO_STRATEGY
+            continue
+        if done % 2 == 0:
+            sweep_check(T, g, [cl, W.Cluster(cl.nodes, cl.devices_per_node, 50 * W.GB, 50 * W.GB)],
+                        name)
+        else:
+            domains = (cl.devices_per_node, cl.devices) if cl.nodes > 1 else (cl.devices,)
+            bws = (cl.bw_intra, cl.bw_inter)[:len(domains)]
+            _topology_check(T, g, cl, W.Topology(domains, bws), name)
+        top_rank = max(top_rank, rank)
+        done += 1
+    assert top_rank == 8
+
+
 def test_degenerate_clusters(T):
     g = W.gpt(1, 64, 4, 32, 4, 2)
     for cl in (W.Cluster(1, 1, 10, 1),        # one device: one whole strategy per op
