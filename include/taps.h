@@ -55,7 +55,7 @@
  *     call needs more; at most 16 such blocks are kept (the least recently
  *     used idle one is freed).  Host arrays a call uploads are copied into
  *     one of at most 8 pinned staging buffers (1 MiB or more each, kept until
- *     the process ends) and from there to the device in stream order.  Calls
+ *     the process ends) and read from there by a kernel in stream order.  Calls
  *     on one stream from several threads are queued one after the other.  No
  *     pointer of the caller is kept after the call returns.
  *   - Kernels are asynchronous on `stream` (a hipStream_t; NULL = the null

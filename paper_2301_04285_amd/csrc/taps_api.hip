@@ -149,14 +149,17 @@ taps_status check_offsets(const taps_graph *g, const uint64_t *op_offsets) {
     return TAPS_OK;
 }
 
-// Pinned staging for host-to-device uploads: a small pool of buffers, each
-// with the event recorded after the copy out of it.  An upload takes a buffer
-// whose copy has completed (or a new one), so calls on different streams or
-// threads, and a call queued behind a long-running build, do not wait for
-// each other's copies; only when every buffer of a full pool is still in
-// flight does an upload wait, for the oldest.
+// Pinned staging for host-to-device uploads: a small pool of fine-grained
+// host buffers, each with the event recorded after the kernel that reads it
+// (k_pull: no copy engine, so the build's kernels follow on the same queue
+// without a hand-over).  An upload takes a buffer whose upload has completed
+// (or a new one), so calls on different streams or threads, and a call queued
+// behind a long-running build, do not wait for each other's uploads; only
+// when every buffer of a full pool is still in flight does an upload wait,
+// for the oldest.
 struct staging_buffer {
     char *host = nullptr;
+    void *dev = nullptr;   // the same memory as the device addresses it
     size_t cap = 0;
     hipEvent_t done = nullptr;
     bool pending = false;
@@ -375,15 +378,24 @@ taps_status upload(scratch &sc, std::vector<chunk> &chunks, void **dev) {
         while (cap < total) cap *= 2;
         if (b->host) (void)hipHostFree(b->host);
         b->host = nullptr;
+        b->dev = nullptr;
         b->cap = 0;
-        err = hipHostMalloc((void **)&b->host, cap, hipHostMallocDefault);
+        // fine-grained: the upload kernel reads the host's latest writes
+        err = hipHostMalloc((void **)&b->host, cap, hipHostMallocCoherent);
         if (err != hipSuccess) return hip_fail(err, "hipHostMalloc");
         b->cap = cap;
+        err = hipHostGetDevicePointer(&b->dev, b->host, 0);
+        if (err != hipSuccess) {
+            (void)hipHostFree(b->host);
+            b->host = nullptr;
+            b->cap = 0;
+            return hip_fail(err, "hipHostGetDevicePointer");
+        }
     }
     for (const chunk &c : chunks)
         if (c.bytes) std::memcpy(b->host + c.offset, c.src, c.bytes);
-    err = hipMemcpyAsync(*dev, b->host, total, hipMemcpyHostToDevice, stream);
-    if (err != hipSuccess) return hip_fail(err, "hipMemcpyAsync");
+    err = taps_launch_pull(b->dev, *dev, total, stream);
+    if (err != hipSuccess) return hip_fail(err, "upload");
     err = hipEventRecord(b->done, stream);
     if (err != hipSuccess) return hip_fail(err, "hipEventRecord");
     b->pending = true;

@@ -129,6 +129,9 @@ hipError_t taps_launch_edge_costs_h(const taps_edge_params *params, const taps_r
 hipError_t taps_launch_node_costs_h(const taps_op *ops, uint32_t n_ops, const uint64_t *offsets,
                                     const taps_desc *desc, uint64_t total, uint32_t n,
                                     const taps_hier &H, taps_table out, hipStream_t stream);
+// Copies `bytes` (a multiple of 16, below 2^36) from src, fine-grained pinned
+// host memory mapped for the device, to device memory at dst.
+hipError_t taps_launch_pull(const void *src, void *dst, uint64_t bytes, hipStream_t stream);
 hipError_t taps_launch_copy_tables(const taps_copy_task *tasks, uint32_t n_tasks,
                                    const uint64_t *dst_list, taps_table out, hipStream_t stream);
 // For each pair p: flags[p] = 0 if strategies[first_a .. +count) equals

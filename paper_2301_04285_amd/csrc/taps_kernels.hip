@@ -19,6 +19,7 @@
 //                 candidates once per entry, one selection and store per point
 //   k_copy_tables shared tables: one workgroup per chunk of a computed
 //                 table, written to every table that shares it
+//   k_pull        a call's upload, read from pinned host memory
 #include "taps_internal.h"
 
 namespace {
@@ -488,6 +489,15 @@ __device__ inline void copy_range(T *base, const taps_copy_task &c,
     }
 }
 
+// An upload without the copy engine: the plan is read straight from
+// fine-grained pinned host memory, 16 bytes per thread and step, so the
+// build's kernels follow it on the same queue with no hand-over.
+__global__ __launch_bounds__(256) void k_pull(const uint4 *__restrict__ src,
+                                              uint4 *__restrict__ dst, uint32_t n16) {
+    for (uint32_t k = blockIdx.x * 256u + threadIdx.x; k < n16; k += gridDim.x * 256u)
+        dst[k] = src[k];
+}
+
 __global__ __launch_bounds__(256) void k_copy_tables(const taps_copy_task *__restrict__ tasks,
                                                      const uint64_t *__restrict__ dst_list,
                                                      taps_table out) {
@@ -623,6 +633,15 @@ hipError_t taps_launch_node_costs_h(const taps_op *ops, uint32_t n_ops, const ui
     if (total == 0) return hipSuccess;
     hipLaunchKernelGGL(k_node_costs_h, dim3(blocks_for(total, 256)), dim3(256), 0, stream, ops,
                        n_ops, offsets, desc, total, n, H, out);
+    return hipGetLastError();
+}
+
+hipError_t taps_launch_pull(const void *src, void *dst, uint64_t bytes, hipStream_t stream) {
+    const uint64_t n16 = bytes / 16;
+    if (n16 == 0) return hipSuccess;
+    const uint64_t blocks = (n16 + 255) / 256 < 256 ? (n16 + 255) / 256 : 256;
+    hipLaunchKernelGGL(k_pull, dim3((uint32_t)blocks), dim3(256), 0, stream, (const uint4 *)src,
+                       (uint4 *)dst, (uint32_t)n16);
     return hipGetLastError();
 }
 
