@@ -287,7 +287,9 @@ __global__ __launch_bounds__(256) void k_row_map(const taps_seg_group *__restric
     segs[r] = ref;
 }
 
-template <uint32_t R>
+// R: the launch's tensors have rank R at most; Narrow: both reduced
+// bandwidths are below 2^32 (64-bit keys), so the other order is not compiled.
+template <uint32_t R, bool Narrow>
 __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_costs(
     const taps_edge_params *__restrict__ params, const taps_row_ref *__restrict__ rows,
     uint32_t n_segs, const taps_desc *__restrict__ desc, taps_launch lp, taps_table out) {
@@ -310,7 +312,7 @@ __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_co
     taps_keys K;
     K.b_inter_red = lp.b_inter_red;
     K.b_intra_red = lp.b_intra_red;
-    K.narrow = lp.narrow != 0;
+    K.narrow = Narrow;
     // the row's records start here; lane j writes entry j
     const uint64_t row_out = E.out_offset + (uint64_t)i * E.nd;
     const taps_desc *col = desc + E.dst_base;
@@ -578,12 +580,19 @@ hipError_t taps_launch_edge_costs(const taps_edge_params *params, const taps_row
                                   uint32_t max_rank, taps_table out, hipStream_t stream) {
     if (n_segs == 0) return hipSuccess;
     const dim3 grid(blocks_for(n_segs, TAPS_ROWS_PER_BLOCK)), block(TAPS_TILE_COLS * TAPS_ROWS_PER_BLOCK);
-    if (max_rank <= TAPS_LOW_RANK)
-        hipLaunchKernelGGL(k_edge_costs<TAPS_LOW_RANK>, grid, block, 0, stream, params, segs,
-                           (uint32_t)n_segs, desc, lp, out);
+    const bool low = max_rank <= TAPS_LOW_RANK, narrow = lp.narrow != 0;
+    if (low && narrow)
+        hipLaunchKernelGGL((k_edge_costs<TAPS_LOW_RANK, true>), grid, block, 0, stream, params,
+                           segs, (uint32_t)n_segs, desc, lp, out);
+    else if (low)
+        hipLaunchKernelGGL((k_edge_costs<TAPS_LOW_RANK, false>), grid, block, 0, stream, params,
+                           segs, (uint32_t)n_segs, desc, lp, out);
+    else if (narrow)
+        hipLaunchKernelGGL((k_edge_costs<TAPS_D_MAX_RANK, true>), grid, block, 0, stream, params,
+                           segs, (uint32_t)n_segs, desc, lp, out);
     else
-        hipLaunchKernelGGL(k_edge_costs<TAPS_D_MAX_RANK>, grid, block, 0, stream, params, segs,
-                           (uint32_t)n_segs, desc, lp, out);
+        hipLaunchKernelGGL((k_edge_costs<TAPS_D_MAX_RANK, false>), grid, block, 0, stream, params,
+                           segs, (uint32_t)n_segs, desc, lp, out);
     return hipGetLastError();
 }
 

@@ -223,8 +223,9 @@ def _within_tensor_limit(g):
 def test_high_rank_tensors(T):
     """Edges carrying tensors of rank 5 to 8 (the launches that cannot use the
     kernels compiled for rank 4 at most), beside edges of low rank in the same
-    graph: the two-class tables entry by entry, the bandwidth sweep and the
-    link-class tables, against the oracle."""
+    graph: the two-class tables entry by entry, the bandwidth sweep (with a
+    point whose exact order needs 128-bit keys) and the link-class tables,
+    against the oracle."""
     from paper_2301_04285_amd.taps import TapsError
     rng = random.Random(4285)
     done, top_rank = 0, 0
@@ -244,7 +245,8 @@ def test_high_rank_tensors(T):
             assert ex.status == T.ERR_NO_STRATEGY
             continue
         if done % 2 == 0:
-            sweep_check(T, g, [cl, W.Cluster(cl.nodes, cl.devices_per_node, 50 * W.GB, 50 * W.GB)],
+            # the second point's reduced bandwidths exceed 2^32 (128-bit keys)
+            sweep_check(T, g, [cl, W.Cluster(cl.nodes, cl.devices_per_node, (1 << 40) + 1, 3)],
                         name)
         else:
             domains = (cl.devices_per_node, cl.devices) if cl.nodes > 1 else (cl.devices,)
