@@ -386,8 +386,9 @@ taps_status taps_edge_costs_sweep(const taps_graph *graph, const taps_cluster *c
 /* Profiling aid, not part of the method: `before` and `after` are HIP events
  * (hipEvent_t, created by the caller, passed as plain pointers) that the
  * calling thread's next taps_edge_costs, taps_edge_costs_shared,
- * taps_edge_costs_backward or taps_edge_costs_sweep call that launches the
- * edge-table kernel records on its stream immediately before and after that
+ * taps_edge_costs_backward, taps_edge_costs_sweep, taps_edge_costs_topology
+ * or taps_build_tables call that launches the edge-table kernel records on
+ * its stream immediately before and after that
  * kernel (and, for shared tables, the copies after it), so that
  * the caller can time the kernel alone.  The setting is thread-local,
  * used once and then cleared; two NULLs clear it.  The events stay owned by
