@@ -511,6 +511,25 @@ def test_concurrent_builds_streams_and_staging(T):
         assert same(c, got), f"queued build {k} (case {c})"
 
 
+def test_plan_larger_than_a_staging_buffer(T):
+    """A 600-layer GPT on 2 devices: 8,400 operators and 10,798 edges, a plan of
+    about 1.9 MB (more than a staging buffer holds at first, so one is replaced
+    by a larger one, and the stream's scratch block grows), against the oracle;
+    the shared-table build equals it, and a small build after it (on the grown
+    buffers) still equals its own reference."""
+    import torch
+    g = W.gpt(600, 64, 2, 32, 2, 2)
+    cl = W.Cluster(1, 2, 100 * W.GB, 10 * W.GB)
+    small = W.config(2)
+    ref_small = T.build_tables(small.graph, small.clusters[0][1])
+    tabs = full_check(T, g, cl, "gpt 600 layers on 2 devices")
+    shared = T.build_tables(g, cl, shared=True)
+    again = T.build_tables(small.graph, small.clusters[0][1])
+    torch.cuda.synchronize()
+    assert _same_tables(tabs.edge, shared.edge) and _same_tables(tabs.node, shared.node)
+    assert _same_tables(ref_small.edge, again.edge) and _same_tables(ref_small.node, again.node)
+
+
 def test_fused_build_capacity_and_errors(T):
     """Capacity and argument errors are reported before any GPU work and leave the
     outputs untouched."""
