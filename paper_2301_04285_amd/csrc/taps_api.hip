@@ -830,6 +830,60 @@ uint64_t strategy_count(const taps_op &op, uint32_t n, uint32_t allowed) {
     return count;
 }
 
+// Strategies among each chunk of TAPS_BUILD_CHUNK candidate ranks of an
+// operator, found with the device's own unranking and filter, memoised on
+// what decides them (devices, allowed cuts, axes, partitionable axes and the
+// trailing zero bits of their lengths).
+const std::vector<uint32_t> &chunk_counts(const taps_op &op, uint32_t n, uint32_t allowed) {
+    static const taps_completion_table W = taps_make_completions();
+    uint64_t key = n | (uint64_t)(allowed & 0xFFu) << 4 | (uint64_t)op.part_mask << 12 |
+                   (uint64_t)op.n_axes << 20;
+    for (uint32_t a = 0; a < op.n_axes; ++a) {
+        if (!((op.part_mask >> a) & 1u)) continue;
+        const uint32_t z = (uint32_t)__builtin_ctzll((uint64_t)op.axis_len[a]);
+        key |= (uint64_t)(z < n ? z : n) << (24 + 4 * a);
+    }
+    thread_local std::unordered_map<uint64_t, std::vector<uint32_t>> memo;
+    const auto it = memo.find(key);
+    if (it != memo.end()) return it->second;
+    const uint32_t total = W.v[(taps_popc(op.part_mask) * 9u + n) * 9u];
+    std::vector<uint32_t> counts((total + TAPS_BUILD_CHUNK - 1) / TAPS_BUILD_CHUNK, 0);
+    for (uint32_t r = 0; r < total; ++r) {
+        uint32_t expo[TAPS_D_MAX_AXES];
+        int32_t pos[TAPS_D_MAX_AXES];
+        if (!taps_unrank(op.n_axes, op.part_mask, n, r, W.v, expo, pos)) continue;
+        bool valid = true;
+        for (uint32_t a = 0; a < op.n_axes; ++a)
+            if (op.axis_len[a] & (((int64_t)1 << expo[a]) - 1)) valid = false;
+        if (valid && (taps_describe(op.n_axes, expo, pos).cuts & ~allowed)) valid = false;
+        counts[r / TAPS_BUILD_CHUNK] += valid ? 1u : 0u;
+    }
+    return memo.emplace(key, std::move(counts)).first->second;
+}
+
+// The workgroups of k_build_strategies: every chunk of candidate ranks that
+// holds a strategy, at the operator's offset plus the strategies of the
+// chunks before it.  The chunks' counts must add up to the exact count.
+taps_status plan_build(const taps_graph *graph, uint32_t n, uint32_t allowed,
+                       const std::vector<uint64_t> &offs, std::vector<taps_build_chunk> &chunks) {
+    chunks.clear();
+    for (uint32_t k = 0; k < graph->n_ops; ++k) {
+        const std::vector<uint32_t> &cc = chunk_counts(graph->ops[k], n, allowed);
+        uint64_t base = offs[k];
+        for (uint32_t c = 0; c < cc.size(); ++c) {
+            if (!cc[c]) continue;
+            chunks.push_back({base, k, c * (uint32_t)TAPS_BUILD_CHUNK, cc[c], 0u});
+            base += cc[c];
+        }
+        if (base != offs[k + 1])
+            return fail(TAPS_ERR_ARG, "op %u: %llu strategies by chunks, %llu counted", k,
+                        (unsigned long long)(base - offs[k]),
+                        (unsigned long long)(offs[k + 1] - offs[k]));
+    }
+    if (chunks.size() > 0x7FFFFFFFull) return fail(TAPS_ERR_ARG, "too many strategy chunks");
+    return TAPS_OK;
+}
+
 // Per-operator strategy counts and offsets (host); TAPS_ERR_NO_STRATEGY if an
 // operator has none.
 taps_status count_strategies(const taps_graph *graph, uint32_t n, uint32_t allowed,
@@ -864,16 +918,18 @@ taps_status enumerate(const taps_graph *graph, const taps_launch &lp, uint32_t a
     if (offs[n_ops] > capacity)
         return fail(TAPS_ERR_CAPACITY, "%llu strategies, capacity %llu",
                     (unsigned long long)offs[n_ops], (unsigned long long)capacity);
+    std::vector<taps_build_chunk> chunks;
+    if ((st = plan_build(graph, lp.n, allowed_cuts, offs, chunks)) != TAPS_OK) return st;
     hipStream_t stream = (hipStream_t)stream_;
     scratch sc(stream);
     std::vector<chunk> ch{{graph->ops, sizeof(taps_op) * n_ops, 0},
-                          {offs.data(), sizeof(uint64_t) * (n_ops + 1), 0}};
+                          {chunks.data(), sizeof(taps_build_chunk) * chunks.size(), 0}};
     void *dev = nullptr;
     if ((st = upload(sc, ch, &dev)) != TAPS_OK) return st;
     const taps_table no_node = {nullptr, nullptr, nullptr, nullptr, nullptr};
-    const hipError_t err =
-        taps_launch_build_strategies(at<taps_op>(dev, ch[0]), n_ops, at<uint64_t>(dev, ch[1]),
-                                     allowed_cuts, lp, strategies, nullptr, no_node, stream);
+    const hipError_t err = taps_launch_build_strategies(
+        at<taps_op>(dev, ch[0]), at<taps_build_chunk>(dev, ch[1]), (uint32_t)chunks.size(),
+        allowed_cuts, lp, strategies, nullptr, no_node, stream);
     if (err != hipSuccess) return hip_fail(err, "enumerate");
     return TAPS_OK;
 }
@@ -1049,6 +1105,8 @@ taps_status taps_build_tables(const taps_graph *graph, const taps_cluster *clust
     if (none || n_ops == 0) return TAPS_OK;
     // one upload and one set of scratch for the whole build
     hipStream_t stream = (hipStream_t)stream_;
+    std::vector<taps_build_chunk> bchunks;
+    if ((st = plan_build(graph, lp.n, allowed, offs, bchunks)) != TAPS_OK) return st;
     scratch sc(stream);
     std::vector<taps_seg_group> groups;
     const uint64_t total = offs[n_ops];
@@ -1059,7 +1117,8 @@ taps_status taps_build_tables(const taps_graph *graph, const taps_cluster *clust
                           {eoff.data(), sizeof(uint64_t) * (n_edges + 1), 0},
                           {groups.data(), sizeof(taps_seg_group) * groups.size(), 0},
                           {copies.data(), sizeof(taps_copy_task) * copies.size(), 0},
-                          {dst_list.data(), sizeof(uint64_t) * dst_list.size(), 0}};
+                          {dst_list.data(), sizeof(uint64_t) * dst_list.size(), 0},
+                          {bchunks.data(), sizeof(taps_build_chunk) * bchunks.size(), 0}};
     void *dev = nullptr;
     if ((st = upload(sc, ch, &dev)) != TAPS_OK) return st;
     taps_desc *d_desc = nullptr;
@@ -1072,8 +1131,9 @@ taps_status taps_build_tables(const taps_graph *graph, const taps_cluster *clust
     if ((st = sc.alloc((void **)&d_segs, sizeof(taps_row_ref) * (n_segs ? n_segs : 1))) != TAPS_OK)
         return st;
     const taps_op *d_ops = at<taps_op>(dev, ch[0]);
-    hipError_t err = taps_launch_build_strategies(d_ops, n_ops, at<uint64_t>(dev, ch[2]), allowed,
-                                                  lp, strategies, d_desc, node, stream);
+    hipError_t err = taps_launch_build_strategies(d_ops, at<taps_build_chunk>(dev, ch[7]),
+                                                  (uint32_t)bchunks.size(), allowed, lp, strategies,
+                                                  d_desc, node, stream);
     if (err == hipSuccess && eoff[n_edges] > 0) {
         err = taps_launch_edge_setup(d_ops, at<taps_edge>(dev, ch[1]), n_edges,
                                      at<uint64_t>(dev, ch[2]), at<uint64_t>(dev, ch[3]),

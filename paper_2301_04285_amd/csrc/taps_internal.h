@@ -114,11 +114,19 @@ hipError_t taps_launch_edge_costs_sweep(const taps_edge_params *params, const ta
                                         uint64_t n_rows, const taps_desc *desc,
                                         const taps_launch &lp, uint32_t max_rank,
                                         const taps_sweep &sw, hipStream_t stream);
-// Strategies of every operator in one launch (one workgroup per operator),
-// with their descriptors and node records unless desc / node.t are NULL;
-// op_offsets: device copy of the host's counts.
-hipError_t taps_launch_build_strategies(const taps_op *ops, uint32_t n_ops,
-                                        const uint64_t *op_offsets, uint32_t allowed_cuts,
+// One workgroup of k_build_strategies: candidate ranks [first, first +
+// TAPS_BUILD_CHUNK) of operator `op`, of which `count` pass the filter; they
+// are strategies base, base + 1, ... in rank order.
+#define TAPS_BUILD_CHUNK 256
+struct taps_build_chunk {
+    uint64_t base;
+    uint32_t op, first, count, pad;
+};
+// Strategies of every operator in one launch (one workgroup per chunk of
+// candidate ranks that holds a strategy), with their descriptors and node
+// records unless desc / node.t are NULL.
+hipError_t taps_launch_build_strategies(const taps_op *ops, const taps_build_chunk *chunks,
+                                        uint32_t n_chunks, uint32_t allowed_cuts,
                                         const taps_launch &lp, taps_strategy *out, taps_desc *desc,
                                         taps_table node, hipStream_t stream);
 // Link-class hierarchies: the edge and node tables under the classes of H.

@@ -1,8 +1,9 @@
 // taps_kernels.hip -- gfx950 kernels of the TAPS cost tables.
 //
-//   k_build_strategies  one workgroup per operator: GenerateStrategySet in
-//                 canonical order at host-counted offsets (ballots, LDS scan),
-//                 optionally each strategy's descriptor and node record
+//   k_build_strategies  one workgroup per chunk of 256 candidate ranks of an
+//                 operator: GenerateStrategySet in canonical order at
+//                 host-counted offsets (ballot, LDS scan), optionally each
+//                 strategy's descriptor and node record
 //   k_describe    one thread per strategy: level runs, owners and cuts
 //   k_node_costs  one thread per strategy: the intra-op AllReduces
 //   k_memory_costs one thread per strategy: weight and output shard bytes
@@ -123,13 +124,12 @@ __global__ __launch_bounds__(256) void k_node_costs(const taps_op *__restrict__ 
 // order, 256 per pass (a ballot per wavefront, the four wavefront counts
 // scanned in LDS), and writes every valid strategy together with, when asked
 // (desc and node.t not NULL), its descriptor and its node (intra-op) record.
-// The operator's strategies go to [op_offsets[k], op_offsets[k+1]), which the
-// host sized with an exact count of the same filter; nothing is written
-// outside that range.
-constexpr uint32_t kBuildThreads = 256;   // candidates per pass of k_build_strategies (1024: slower)
+// A chunk's strategies go to [base, base + count), counted on the host with
+// the same unranking and filter; nothing is written outside that range.
+constexpr uint32_t kBuildThreads = TAPS_BUILD_CHUNK;
 
 __global__ __launch_bounds__(kBuildThreads) void k_build_strategies(const taps_op *__restrict__ ops,
-                                                          const uint64_t *__restrict__ op_offsets,
+                                                          const taps_build_chunk *__restrict__ chunks,
                                                           uint32_t allowed_cuts, taps_launch lp,
                                                           taps_strategy *__restrict__ out,
                                                           taps_desc *__restrict__ desc,
@@ -139,60 +139,52 @@ __global__ __launch_bounds__(kBuildThreads) void k_build_strategies(const taps_o
     const uint32_t tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
     for (uint32_t x = tid; x < 9u * 9u * 9u; x += blockDim.x) W[x] = kCompletions.v[x];
     __syncthreads();
-    const taps_op &op = ops[blockIdx.x];
+    const taps_build_chunk ck = chunks[blockIdx.x];
+    const taps_op &op = ops[ck.op];
     const uint32_t n_axes = op.n_axes, part = op.part_mask;
     const uint32_t total = W[(taps_popc(part) * 9u + lp.n) * 9u];
-    const uint64_t base = op_offsets[blockIdx.x], end = op_offsets[blockIdx.x + 1];
     const uint32_t full = taps_low_mask(lp.n);
-    uint64_t running = 0;
-    for (uint32_t r0 = 0; r0 < total; r0 += blockDim.x) {
-        const uint32_t r = r0 + tid;
-        uint32_t expo[TAPS_D_MAX_AXES];
-        int32_t pos[TAPS_D_MAX_AXES];
-        bool valid = r < total && taps_unrank(n_axes, part, lp.n, r, W, expo, pos);
-        if (valid)
-            for (uint32_t a = 0; a < n_axes; ++a)
-                if (op.axis_len[a] & (((int64_t)1 << expo[a]) - 1)) valid = false;
-        taps_desc D = {0u, 0u, 0u, 0u};
-        if (valid) {
-            D = taps_describe(n_axes, expo, pos);
-            if (D.cuts & ~allowed_cuts) valid = false;
+    const uint32_t r = ck.first + tid;
+    uint32_t expo[TAPS_D_MAX_AXES];
+    int32_t pos[TAPS_D_MAX_AXES];
+    bool valid = r < total && taps_unrank(n_axes, part, lp.n, r, W, expo, pos);
+    if (valid)
+        for (uint32_t a = 0; a < n_axes; ++a)
+            if (op.axis_len[a] & (((int64_t)1 << expo[a]) - 1)) valid = false;
+    taps_desc D = {0u, 0u, 0u, 0u};
+    if (valid) {
+        D = taps_describe(n_axes, expo, pos);
+        if (D.cuts & ~allowed_cuts) valid = false;
+    }
+    const uint64_t m = __ballot(valid);
+    if (lane == 0) wave_count[wave] = (uint32_t)__builtin_popcountll(m);
+    __syncthreads();
+    uint32_t before = 0;
+    for (uint32_t w = 0; w < wave; ++w) before += wave_count[w];
+    const uint32_t k = before + lanes_below(m);
+    if (valid && k < ck.count) {
+        const uint64_t idx = ck.base + k;
+        taps_strategy st;
+        for (uint32_t a = 0; a < TAPS_MAX_AXES; ++a) {
+            st.log2_deg[a] = a < n_axes ? (uint8_t)expo[a] : 0;
+            st.pos[a] = a < n_axes ? (int8_t)pos[a] : (int8_t)-1;
         }
-        const uint64_t m = __ballot(valid);
-        if (lane == 0) wave_count[wave] = (uint32_t)__builtin_popcountll(m);
-        __syncthreads();
-        uint32_t before = 0, all = 0;
-        for (uint32_t w = 0; w < blockDim.x / kWave; ++w) {
-            before += w < wave ? wave_count[w] : 0u;
-            all += wave_count[w];
+        out[idx] = st;
+        if (desc) desc[idx] = D;   // uniform: descriptors and node records are optional
+        if (node.t) {
+            taps_acc c;
+            taps_acc_zero(c);
+            node_tensor(c, op, op.out, D, full, lp.lam);
+            for (uint32_t q = 0; q < op.n_in && q < TAPS_MAX_INPUTS; ++q)
+                node_tensor(c, op, op.in[q], D, full, lp.lam);
+            for (uint32_t q = 0; q < op.n_w && q < TAPS_MAX_WEIGHTS; ++q)
+                node_tensor(c, op, op.w[q], D, full, lp.lam);
+            node.t[idx] = (double)c.intra * lp.inv_n_bintra + (double)c.inter * lp.inv_n_binter;
+            node.vol[idx] = c.vol;
+            node.intra[idx] = c.intra;
+            node.inter[idx] = c.inter;
+            node.meta[idx] = taps_meta(0, c);
         }
-        __syncthreads();   // wave_count is rewritten by the next pass
-        const uint64_t idx = base + running + before + lanes_below(m);
-        if (valid && idx < end) {
-            taps_strategy st;
-            for (uint32_t a = 0; a < TAPS_MAX_AXES; ++a) {
-                st.log2_deg[a] = a < n_axes ? (uint8_t)expo[a] : 0;
-                st.pos[a] = a < n_axes ? (int8_t)pos[a] : (int8_t)-1;
-            }
-            out[idx] = st;
-            if (desc) desc[idx] = D;   // uniform: descriptors and node records are optional
-            if (node.t) {
-                taps_acc c;
-                taps_acc_zero(c);
-                node_tensor(c, op, op.out, D, full, lp.lam);
-                for (uint32_t k = 0; k < op.n_in && k < TAPS_MAX_INPUTS; ++k)
-                    node_tensor(c, op, op.in[k], D, full, lp.lam);
-                for (uint32_t k = 0; k < op.n_w && k < TAPS_MAX_WEIGHTS; ++k)
-                    node_tensor(c, op, op.w[k], D, full, lp.lam);
-                node.t[idx] =
-                    (double)c.intra * lp.inv_n_bintra + (double)c.inter * lp.inv_n_binter;
-                node.vol[idx] = c.vol;
-                node.intra[idx] = c.intra;
-                node.inter[idx] = c.inter;
-                node.meta[idx] = taps_meta(0, c);
-            }
-        }
-        running += all;
     }
 }
 
@@ -611,13 +603,13 @@ hipError_t taps_launch_edge_costs_sweep(const taps_edge_params *params, const ta
     return hipGetLastError();
 }
 
-hipError_t taps_launch_build_strategies(const taps_op *ops, uint32_t n_ops,
-                                        const uint64_t *op_offsets, uint32_t allowed_cuts,
+hipError_t taps_launch_build_strategies(const taps_op *ops, const taps_build_chunk *chunks,
+                                        uint32_t n_chunks, uint32_t allowed_cuts,
                                         const taps_launch &lp, taps_strategy *out, taps_desc *desc,
                                         taps_table node, hipStream_t stream) {
-    if (n_ops == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_build_strategies, dim3(n_ops), dim3(kBuildThreads), 0, stream, ops,
-                       op_offsets, allowed_cuts, lp, out, desc, node);
+    if (n_chunks == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_build_strategies, dim3(n_chunks), dim3(kBuildThreads), 0, stream, ops,
+                       chunks, allowed_cuts, lp, out, desc, node);
     return hipGetLastError();
 }
 
