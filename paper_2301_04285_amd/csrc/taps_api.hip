@@ -683,11 +683,13 @@ taps_status edge_costs(const taps_graph *graph, const taps_cluster *clusters, ui
     if ((st = sc.alloc((void **)&d_params, sizeof(taps_edge_params) * n_edges)) != TAPS_OK) return st;
     if ((st = sc.alloc((void **)&d_segs, sizeof(taps_row_ref) * n_segs)) != TAPS_OK) return st;
     hipError_t err = taps_launch_describe(strategies, total, d_desc, stream);
-    if (err == hipSuccess)
-        err = taps_launch_edge_setup(at<taps_op>(dev, ch[0]), at<taps_edge>(dev, ch[1]), n_edges,
-                                     at<uint64_t>(dev, ch[2]), at<uint64_t>(dev, ch[3]),
-                                     at<taps_seg_group>(dev, ch[4]), (uint32_t)groups.size(), lp,
-                                     reverse, d_params, n_segs, d_segs, stream);
+    if (err == hipSuccess) {
+        const taps_plan_args pa{at<taps_op>(dev, ch[0]), at<taps_edge>(dev, ch[1]),
+                                at<uint64_t>(dev, ch[2]), at<uint64_t>(dev, ch[3]),
+                                at<taps_seg_group>(dev, ch[4]), d_params, d_segs, n_segs,
+                                n_edges, (uint32_t)groups.size(), reverse ? 1u : 0u, 0u};
+        err = taps_launch_edge_setup(pa, lp, stream);
+    }
     // the edge-table kernel launches (entries > 0): use the events, if any, once
     const hipEvent_t before = g_kernel_before, after = g_kernel_after;
     g_kernel_before = g_kernel_after = nullptr;
@@ -1130,15 +1132,17 @@ taps_status taps_build_tables(const taps_graph *graph, const taps_cluster *clust
         return st;
     if ((st = sc.alloc((void **)&d_segs, sizeof(taps_row_ref) * (n_segs ? n_segs : 1))) != TAPS_OK)
         return st;
-    const taps_op *d_ops = at<taps_op>(dev, ch[0]);
-    hipError_t err = taps_launch_build_strategies(d_ops, at<taps_build_chunk>(dev, ch[7]),
-                                                  (uint32_t)bchunks.size(), allowed, lp, strategies,
-                                                  d_desc, node, stream);
-    if (err == hipSuccess && eoff[n_edges] > 0) {
-        err = taps_launch_edge_setup(d_ops, at<taps_edge>(dev, ch[1]), n_edges,
-                                     at<uint64_t>(dev, ch[2]), at<uint64_t>(dev, ch[3]),
-                                     at<taps_seg_group>(dev, ch[4]), (uint32_t)groups.size(), lp,
-                                     false, d_params, n_segs, d_segs, stream);
+    // the strategies, and the edge plan when there are edge entries, in one launch
+    const bool edges_on = eoff[n_edges] > 0;
+    const taps_plan_args pa{at<taps_op>(dev, ch[0]), at<taps_edge>(dev, ch[1]),
+                            at<uint64_t>(dev, ch[2]), at<uint64_t>(dev, ch[3]),
+                            at<taps_seg_group>(dev, ch[4]), d_params, d_segs,
+                            edges_on ? n_segs : 0u, edges_on ? n_edges : 0u,
+                            edges_on ? (uint32_t)groups.size() : 0u, 0u, 0u};
+    hipError_t err = taps_launch_build_front(at<taps_build_chunk>(dev, ch[7]),
+                                             (uint32_t)bchunks.size(), allowed, lp, strategies,
+                                             d_desc, node, pa, stream);
+    if (err == hipSuccess && edges_on) {
         const hipEvent_t before = g_kernel_before, after = g_kernel_after;
         g_kernel_before = g_kernel_after = nullptr;
         if (err == hipSuccess && before) err = hipEventRecord(before, stream);

@@ -83,12 +83,22 @@ hipError_t taps_launch_describe(const taps_strategy *s, uint64_t total, taps_des
 hipError_t taps_launch_node_costs(const taps_op *ops, uint32_t n_ops, const uint64_t *offsets,
                                   const taps_desc *desc, uint64_t total, const taps_launch &lp,
                                   taps_table out, hipStream_t stream);
-// reverse: the backward tables (source side = the consumer's input map).
-hipError_t taps_launch_edge_setup(const taps_op *ops, const taps_edge *edges, uint32_t n_edges,
-                                  const uint64_t *op_offsets, const uint64_t *edge_offsets,
-                                  const taps_seg_group *groups, uint32_t n_groups,
-                                  const taps_launch &lp, bool reverse, taps_edge_params *params,
-                                  uint64_t n_segs, taps_row_ref *segs, hipStream_t stream);
+// The edge plan of a launch (device arrays): per-edge constants into params
+// and the row segments of the groups into segs; reverse: the backward tables
+// (source side = the consumer's input map).
+struct taps_plan_args {
+    const taps_op *ops;
+    const taps_edge *edges;
+    const uint64_t *op_offsets;
+    const uint64_t *edge_offsets;
+    const taps_seg_group *groups;
+    taps_edge_params *params;
+    taps_row_ref *segs;
+    uint64_t n_segs;
+    uint32_t n_edges, n_groups, reverse, pad;
+};
+hipError_t taps_launch_edge_setup(const taps_plan_args &pa, const taps_launch &lp,
+                                  hipStream_t stream);
 // max_rank: the largest tensor rank of the launch's edges; up to
 // TAPS_LOW_RANK the kernels are compiled for that many dimensions (fewer
 // registers for the producer side, shorter per-dimension loops).
@@ -129,6 +139,12 @@ hipError_t taps_launch_build_strategies(const taps_op *ops, const taps_build_chu
                                         uint32_t n_chunks, uint32_t allowed_cuts,
                                         const taps_launch &lp, taps_strategy *out, taps_desc *desc,
                                         taps_table node, hipStream_t stream);
+// taps_launch_build_strategies and taps_launch_edge_setup as one launch (the
+// plan needs only the host-counted strategy offsets).
+hipError_t taps_launch_build_front(const taps_build_chunk *chunks, uint32_t n_chunks,
+                                   uint32_t allowed_cuts, const taps_launch &lp, taps_strategy *out,
+                                   taps_desc *desc, taps_table node, const taps_plan_args &pa,
+                                   hipStream_t stream);
 // Link-class hierarchies: the edge and node tables under the classes of H.
 hipError_t taps_launch_edge_costs_h(const taps_edge_params *params, const taps_row_ref *rows,
                                     uint64_t n_rows, const taps_desc *desc, const taps_launch &lp,

@@ -7,10 +7,11 @@
 //   k_describe    one thread per strategy: level runs, owners and cuts
 //   k_node_costs  one thread per strategy: the intra-op AllReduces
 //   k_memory_costs one thread per strategy: weight and output shard bytes
-//   k_edge_setup  one thread per edge: per-edge constants
-//   k_row_map     one thread per row segment: its edge, producer strategy
-//                 and first consumer strategy (every edge's full-length
-//                 segments first, the rows' remainders last, longest first)
+//   k_edge_plan   one thread per edge (its constants), then one thread per
+//                 row segment (its edge, producer strategy and consumer
+//                 range: every edge's full-length segments first, the rows'
+//                 remainders last, longest first)
+//   k_build_front k_build_strategies and k_edge_plan in one launch
 //   k_edge_costs  one wavefront per row segment (one producer strategy,
 //                 uniform: its descriptor sits in scalar registers; 2 or 8
 //                 tiles of 64 consumer strategies, one per lane, the
@@ -128,18 +129,16 @@ __global__ __launch_bounds__(256) void k_node_costs(const taps_op *__restrict__ 
 // the same unranking and filter; nothing is written outside that range.
 constexpr uint32_t kBuildThreads = TAPS_BUILD_CHUNK;
 
-__global__ __launch_bounds__(kBuildThreads) void k_build_strategies(const taps_op *__restrict__ ops,
-                                                          const taps_build_chunk *__restrict__ chunks,
-                                                          uint32_t allowed_cuts, taps_launch lp,
-                                                          taps_strategy *__restrict__ out,
-                                                          taps_desc *__restrict__ desc,
-                                                          taps_table node) {
+// The strategies of one chunk of candidate ranks (a whole workgroup).
+__device__ inline void build_chunk(const taps_build_chunk &ck, const taps_op *__restrict__ ops,
+                                   uint32_t allowed_cuts, const taps_launch &lp,
+                                   taps_strategy *__restrict__ out, taps_desc *__restrict__ desc,
+                                   const taps_table &node) {
     __shared__ uint32_t W[9 * 9 * 9];
     __shared__ uint32_t wave_count[kBuildThreads / kWave];
     const uint32_t tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
     for (uint32_t x = tid; x < 9u * 9u * 9u; x += blockDim.x) W[x] = kCompletions.v[x];
     __syncthreads();
-    const taps_build_chunk ck = chunks[blockIdx.x];
     const taps_op &op = ops[ck.op];
     const uint32_t n_axes = op.n_axes, part = op.part_mask;
     const uint32_t total = W[(taps_popc(part) * 9u + lp.n) * 9u];
@@ -188,6 +187,13 @@ __global__ __launch_bounds__(kBuildThreads) void k_build_strategies(const taps_o
     }
 }
 
+__global__ __launch_bounds__(kBuildThreads) void k_build_strategies(
+    const taps_op *__restrict__ ops, const taps_build_chunk *__restrict__ chunks,
+    uint32_t allowed_cuts, taps_launch lp, taps_strategy *__restrict__ out,
+    taps_desc *__restrict__ desc, taps_table node) {
+    build_chunk(chunks[blockIdx.x], ops, allowed_cuts, lp, out, desc, node);
+}
+
 // Bytes of one shard of tensor t under strategy s: each dimension's length
 // divided by its split degree, times the element size.
 __device__ inline uint64_t shard_bytes(const taps_op &op, const taps_tensor &t,
@@ -215,68 +221,94 @@ __global__ __launch_bounds__(256) void k_memory_costs(const taps_op *__restrict_
     memory[idx] = m;
 }
 
-__global__ __launch_bounds__(256) void k_edge_setup(const taps_op *__restrict__ ops,
-                                                    const taps_edge *__restrict__ edges,
-                                                    uint32_t n_edges,
-                                                    const uint64_t *__restrict__ op_offsets,
-                                                    const uint64_t *__restrict__ edge_offsets,
-                                                    taps_launch lp, uint32_t reverse,
-                                                    taps_edge_params *__restrict__ params) {
-    const uint32_t e = blockIdx.x * blockDim.x + threadIdx.x;
-    if (e >= n_edges) return;
-    const taps_edge E = edges[e];
-    const taps_op &src = ops[E.src_op];
-    const taps_op &dst = ops[E.dst_op];
+// Per-edge constants of edge e.
+__device__ inline void edge_setup_one(uint32_t e, const taps_plan_args &pa, const taps_launch &lp) {
+    const taps_edge E = pa.edges[e];
+    const taps_op &src = pa.ops[E.src_op];
+    const taps_op &dst = pa.ops[E.dst_op];
     const taps_tensor &T = src.out;
     const taps_tensor &Tc = dst.in[E.dst_slot];
     taps_edge_params p;
-    p.out_offset = edge_offsets[e];
+    p.out_offset = pa.edge_offsets[e];
     uint64_t bytes = src.dtype_bytes;
-    uint32_t pa = 0, ca = 0;
+    uint32_t pax = 0, cax = 0;
     for (uint32_t d = 0; d < T.rank && d < TAPS_MAX_RANK; ++d) {
         bytes *= (uint64_t)src.axis_len[T.axis[d] & 7u];
-        pa |= (uint32_t)(T.axis[d] & 7u) << (4u * d);
-        ca |= (uint32_t)(Tc.axis[d] & 7u) << (4u * d);
+        pax |= (uint32_t)(T.axis[d] & 7u) << (4u * d);
+        cax |= (uint32_t)(Tc.axis[d] & 7u) << (4u * d);
     }
     p.scale = taps_make_scaler(bytes, lp.inv_n_bintra, lp.inv_n_binter);
     // the source side of the redistribution: the producer's output map, or for
     // the backward tables the consumer's input map (the gradient moves back)
-    const uint32_t from = reverse ? E.dst_op : E.src_op, to = reverse ? E.src_op : E.dst_op;
-    p.src_base = (uint32_t)op_offsets[from];
-    p.dst_base = (uint32_t)op_offsets[to];
-    p.ns = (uint32_t)(op_offsets[from + 1] - op_offsets[from]);
-    p.nd = (uint32_t)(op_offsets[to + 1] - op_offsets[to]);
+    const uint32_t from = pa.reverse ? E.dst_op : E.src_op, to = pa.reverse ? E.src_op : E.dst_op;
+    p.src_base = (uint32_t)pa.op_offsets[from];
+    p.dst_base = (uint32_t)pa.op_offsets[to];
+    p.ns = (uint32_t)(pa.op_offsets[from + 1] - pa.op_offsets[from]);
+    p.nd = (uint32_t)(pa.op_offsets[to + 1] - pa.op_offsets[to]);
     p.rank = T.rank;
-    p.paxes = reverse ? ca : pa;
-    p.caxes = reverse ? pa : ca;
+    p.paxes = pa.reverse ? cax : pax;
+    p.caxes = pa.reverse ? pax : cax;
     p.pad = 0;
-    params[e] = p;
+    pa.params[e] = p;
 }
 
-__global__ __launch_bounds__(256) void k_row_map(const taps_seg_group *__restrict__ groups,
-                                                 uint32_t n_groups,
-                                                 const taps_edge_params *__restrict__ params,
-                                                 uint64_t n_segs, taps_row_ref *__restrict__ segs) {
-    const uint64_t r = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (r >= n_segs) return;
+// Row segment r: its edge, producer strategy and consumer range (from the
+// strategy offsets, so it does not wait for the edge constants).
+__device__ inline void row_map_one(uint64_t r, const taps_plan_args &pa) {
     // the last group starting at or before r (groups[0].start == 0)
-    uint32_t lo = 0, hi = n_groups - 1;
+    uint32_t lo = 0, hi = pa.n_groups - 1;
     while (lo < hi) {
         const uint32_t mid = (lo + hi + 1) / 2;
-        if (groups[mid].start <= r)
+        if (pa.groups[mid].start <= r)
             lo = mid;
         else
             hi = mid - 1;
     }
-    const taps_seg_group G = groups[lo];
+    const taps_seg_group G = pa.groups[lo];
+    const taps_edge E = pa.edges[G.edge];
+    const uint32_t from = pa.reverse ? E.dst_op : E.src_op, to = pa.reverse ? E.src_op : E.dst_op;
+    const uint32_t nd = (uint32_t)(pa.op_offsets[to + 1] - pa.op_offsets[to]);
     const uint64_t k = r - G.start;
     taps_row_ref ref;
     ref.edge = G.edge;
-    ref.strategy = (uint32_t)(params[G.edge].src_base + k / G.per_row);
+    ref.strategy = (uint32_t)(pa.op_offsets[from] + k / G.per_row);
     ref.first_col = G.first_col + (uint32_t)(k % G.per_row) * G.cols;
-    const uint32_t nd = params[G.edge].nd;
     ref.last_col = nd - ref.first_col < G.cols ? nd : ref.first_col + G.cols;
-    segs[r] = ref;
+    pa.segs[r] = ref;
+}
+
+// The edge plan in one launch: blocks [0, setup_blocks) set up the edges, the
+// rest map the row segments.
+__global__ __launch_bounds__(256) void k_edge_plan(taps_plan_args pa, taps_launch lp,
+                                                   uint32_t setup_blocks) {
+    if (blockIdx.x < setup_blocks) {
+        const uint32_t e = blockIdx.x * blockDim.x + threadIdx.x;
+        if (e < pa.n_edges) edge_setup_one(e, pa, lp);
+    } else {
+        const uint64_t r = (uint64_t)(blockIdx.x - setup_blocks) * blockDim.x + threadIdx.x;
+        if (r < pa.n_segs) row_map_one(r, pa);
+    }
+}
+
+// The front of a single-call build: the strategy chunks, then the edge plan
+// (the edge setup and the row map need only the strategy offsets, which the
+// host counted), in one launch.
+__global__ __launch_bounds__(kBuildThreads) void k_build_front(
+    const taps_build_chunk *__restrict__ chunks, uint32_t n_chunks, uint32_t allowed_cuts,
+    taps_launch lp, taps_strategy *__restrict__ out, taps_desc *__restrict__ desc,
+    taps_table node, taps_plan_args pa, uint32_t setup_blocks) {
+    if (blockIdx.x < n_chunks) {
+        build_chunk(chunks[blockIdx.x], pa.ops, allowed_cuts, lp, out, desc, node);
+        return;
+    }
+    const uint32_t b = blockIdx.x - n_chunks;
+    if (b < setup_blocks) {
+        const uint32_t e = b * blockDim.x + threadIdx.x;
+        if (e < pa.n_edges) edge_setup_one(e, pa, lp);
+    } else {
+        const uint64_t r = (uint64_t)(b - setup_blocks) * blockDim.x + threadIdx.x;
+        if (r < pa.n_segs) row_map_one(r, pa);
+    }
 }
 
 // R: the launch's tensors have rank R at most; Narrow: both reduced
@@ -552,18 +584,13 @@ hipError_t taps_launch_memory_costs(const taps_op *ops, uint32_t n_ops, const ui
     return hipGetLastError();
 }
 
-hipError_t taps_launch_edge_setup(const taps_op *ops, const taps_edge *edges, uint32_t n_edges,
-                                  const uint64_t *op_offsets, const uint64_t *edge_offsets,
-                                  const taps_seg_group *groups, uint32_t n_groups,
-                                  const taps_launch &lp, bool reverse, taps_edge_params *params,
-                                  uint64_t n_segs, taps_row_ref *segs, hipStream_t stream) {
-    if (n_edges == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_edge_setup, dim3(blocks_for(n_edges, 256)), dim3(256), 0, stream, ops,
-                       edges, n_edges, op_offsets, edge_offsets, lp, reverse ? 1u : 0u, params);
-    hipError_t err = hipGetLastError();
-    if (err != hipSuccess || n_segs == 0 || n_groups == 0) return err;
-    hipLaunchKernelGGL(k_row_map, dim3(blocks_for(n_segs, 256)), dim3(256), 0, stream, groups,
-                       n_groups, params, n_segs, segs);
+hipError_t taps_launch_edge_setup(const taps_plan_args &pa, const taps_launch &lp,
+                                  hipStream_t stream) {
+    if (pa.n_edges == 0) return hipSuccess;
+    const uint32_t setup_blocks = blocks_for(pa.n_edges, 256);
+    const uint64_t map_blocks = pa.n_groups ? blocks_for(pa.n_segs, 256) : 0;
+    hipLaunchKernelGGL(k_edge_plan, dim3((uint32_t)(setup_blocks + map_blocks)), dim3(256), 0,
+                       stream, pa, lp, setup_blocks);
     return hipGetLastError();
 }
 
@@ -610,6 +637,19 @@ hipError_t taps_launch_build_strategies(const taps_op *ops, const taps_build_chu
     if (n_chunks == 0) return hipSuccess;
     hipLaunchKernelGGL(k_build_strategies, dim3(n_chunks), dim3(kBuildThreads), 0, stream, ops,
                        chunks, allowed_cuts, lp, out, desc, node);
+    return hipGetLastError();
+}
+
+hipError_t taps_launch_build_front(const taps_build_chunk *chunks, uint32_t n_chunks,
+                                   uint32_t allowed_cuts, const taps_launch &lp, taps_strategy *out,
+                                   taps_desc *desc, taps_table node, const taps_plan_args &pa,
+                                   hipStream_t stream) {
+    const uint32_t setup_blocks = pa.n_edges ? blocks_for(pa.n_edges, 256) : 0;
+    const uint64_t map_blocks = pa.n_groups ? blocks_for(pa.n_segs, 256) : 0;
+    const uint64_t blocks = n_chunks + setup_blocks + map_blocks;
+    if (blocks == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_build_front, dim3((uint32_t)blocks), dim3(kBuildThreads), 0, stream,
+                       chunks, n_chunks, allowed_cuts, lp, out, desc, node, pa, setup_blocks);
     return hipGetLastError();
 }
 
