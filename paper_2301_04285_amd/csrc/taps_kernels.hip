@@ -360,7 +360,7 @@ __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_co
 
 // Several bandwidth points: the candidates of each entry are costed once and
 // selected, scaled and stored once per point.
-template <uint32_t R>
+template <uint32_t R, bool Narrow>
 __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_costs_sweep(
     const taps_edge_params *__restrict__ params, const taps_row_ref *__restrict__ rows,
     uint32_t n_segs, const taps_desc *__restrict__ desc, taps_launch lp, taps_sweep sw) {
@@ -402,7 +402,7 @@ __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_co
                 taps_keys K;
                 K.b_inter_red = sw.b_inter_red[k];
                 K.b_intra_red = sw.b_intra_red[k];
-                K.narrow = sw.narrow[k] != 0;
+                K.narrow = Narrow || sw.narrow[k] != 0;   // Narrow: 64-bit keys at every point
                 const taps_scaler S = taps_make_scaler(E.scale.tbytes, sw.inv_n_bintra[k],
                                                        sw.inv_n_binter[k]);
                 const taps_entry_out o = taps_entry_finish(taps_pick_for(cands, K), S);
@@ -621,12 +621,21 @@ hipError_t taps_launch_edge_costs_sweep(const taps_edge_params *params, const ta
                                         const taps_sweep &sw, hipStream_t stream) {
     if (n_segs == 0) return hipSuccess;
     const dim3 grid(blocks_for(n_segs, TAPS_ROWS_PER_BLOCK)), block(TAPS_TILE_COLS * TAPS_ROWS_PER_BLOCK);
-    if (max_rank <= TAPS_LOW_RANK)
-        hipLaunchKernelGGL(k_edge_costs_sweep<TAPS_LOW_RANK>, grid, block, 0, stream, params, segs,
-                           (uint32_t)n_segs, desc, lp, sw);
+    bool narrow = true;
+    for (uint32_t k = 0; k < sw.count; ++k) narrow = narrow && sw.narrow[k] != 0;
+    const bool low = max_rank <= TAPS_LOW_RANK;
+    if (low && narrow)
+        hipLaunchKernelGGL((k_edge_costs_sweep<TAPS_LOW_RANK, true>), grid, block, 0, stream,
+                           params, segs, (uint32_t)n_segs, desc, lp, sw);
+    else if (low)
+        hipLaunchKernelGGL((k_edge_costs_sweep<TAPS_LOW_RANK, false>), grid, block, 0, stream,
+                           params, segs, (uint32_t)n_segs, desc, lp, sw);
+    else if (narrow)
+        hipLaunchKernelGGL((k_edge_costs_sweep<TAPS_D_MAX_RANK, true>), grid, block, 0, stream,
+                           params, segs, (uint32_t)n_segs, desc, lp, sw);
     else
-        hipLaunchKernelGGL(k_edge_costs_sweep<TAPS_D_MAX_RANK>, grid, block, 0, stream, params,
-                           segs, (uint32_t)n_segs, desc, lp, sw);
+        hipLaunchKernelGGL((k_edge_costs_sweep<TAPS_D_MAX_RANK, false>), grid, block, 0, stream,
+                           params, segs, (uint32_t)n_segs, desc, lp, sw);
     return hipGetLastError();
 }
 
