@@ -1065,17 +1065,24 @@ __host__ __device__ inline void taps_fac_zero(taps_fach &c) {
     c.counts = 0;
 }
 
-// x_cls += v (selects, no indexed register arrays)
+// x_cls += v (selects, no indexed register arrays).  C: the hierarchy's
+// number of classes (every class index is below it, so x_C .. x_3 stay 0 and
+// are not touched).
+template <uint32_t C = TAPS_D_MAX_CLASSES>
 __host__ __device__ inline void taps_fach_add(taps_fach &c, uint32_t cls, uint32_t v) {
     c.x0 += cls == 0 ? v : 0u;
-    c.x1 += cls == 1 ? v : 0u;
-    c.x2 += cls == 2 ? v : 0u;
-    c.x3 += cls == 3 ? v : 0u;
+    if (C > 1) c.x1 += cls == 1 ? v : 0u;
+    if (C > 2) c.x2 += cls == 2 ? v : 0u;
+    if (C > 3) c.x3 += cls == 3 ? v : 0u;
 }
 
+template <uint32_t C = TAPS_D_MAX_CLASSES>
 __host__ __device__ inline uint64_t taps_fach_key(const taps_fach &c, const taps_hier &H) {
-    return (uint64_t)c.x0 * H.w[0] + (uint64_t)c.x1 * H.w[1] + (uint64_t)c.x2 * H.w[2] +
-           (uint64_t)c.x3 * H.w[3] + (uint64_t)c.xa * H.w_a2a;
+    uint64_t k = (uint64_t)c.x0 * H.w[0];
+    if (C > 1) k += (uint64_t)c.x1 * H.w[1];
+    if (C > 2) k += (uint64_t)c.x2 * H.w[2];
+    if (C > 3) k += (uint64_t)c.x3 * H.w[3];
+    return k + (uint64_t)c.xa * H.w_a2a;
 }
 
 // The shared uplinks of a collective of width w at lowest level lo whose
@@ -1086,7 +1093,8 @@ __host__ __device__ inline uint32_t taps_hier_lct(uint32_t lo, uint32_t beta, ui
     return m - taps_popc(unused & taps_below(m));
 }
 
-struct taps_hier_model {
+template <uint32_t C>
+struct taps_hier_model_t {
     using fac = taps_fach;
     const taps_hier *H;
     uint64_t lim_key;   // a later candidate stops once its key and volume reach these
@@ -1100,7 +1108,7 @@ struct taps_hier_model {
         const uint32_t cls = taps_nib(H->cls_of_top, top);
         const uint32_t lct = cls ? taps_hier_lct(a.lo, taps_nib(H->beta_of_top, top), unused) : 0u;
         c.vol += V;
-        taps_fach_add(c, cls, V << lct);
+        taps_fach_add<C>(c, cls, V << lct);
         c.counts += cls ? 0x101u + ((1u << lct) << 16) : 1u;
     }
 
@@ -1126,20 +1134,22 @@ struct taps_hier_model {
             const uint32_t kap = beta > a.lo ? beta - a.lo : 0u;
             const uint32_t link = ((1u << a.w) - (1u << kap)) << (kap + sh - a.w);
             const uint32_t lct = taps_hier_lct(a.lo, beta, unused);
-            taps_fach_add(c, cls, link << lct);
+            taps_fach_add<C>(c, cls, link << lct);
             c.counts += 0x101u + ((1u << lct) << 16);
         }
     }
 
     __host__ __device__ bool hopeless(const fac &c) const {
-        return lim_on && c.vol >= lim_vol && taps_fach_key(c, *H) >= lim_key;
+        return lim_on && c.vol >= lim_vol && taps_fach_key<C>(c, *H) >= lim_key;
     }
 };
+using taps_hier_model = taps_hier_model_t<TAPS_D_MAX_CLASSES>;
 
 // "remove" (Table 2): every held axis not at its target gathered in producer
 // order (dimensions ascending, each from its top level down), one by one.
+template <class Mh>
 __host__ __device__ inline taps_fach taps_remove_h(const taps_row &P, const taps_lv &L,
-                                                   const taps_hier_model &M) {
+                                                   const Mh &M) {
     taps_fach c;
     taps_fac_zero(c);
     uint32_t e = P.e0, unused = P.full & ~P.pru;
@@ -1161,25 +1171,26 @@ struct taps_pickh {
 
 // The cheapest of Algorithm 1, the same without AllToAll, and "remove" under
 // the link classes of H (ties to the lower index); vmin the smallest volume.
+template <uint32_t C = TAPS_D_MAX_CLASSES>
 __host__ __device__ inline taps_pickh taps_edge_select_h(const taps_row &P, const taps_col &Q,
                                                          const taps_hier &H) {
     taps_lv L;
     taps_unify(P, Q, L);
-    taps_hier_model M{&H, 0, 0, false};
+    taps_hier_model_t<C> M{&H, 0, 0, false};
     const taps_run_t<taps_fach> r0 = taps_alg1_t(P, Q, L, M);
     taps_pickh k;
     k.best = r0.c;
     k.cand = 0;
     k.vmin = r0.c.vol;
     k.ok = r0.ok;
-    uint64_t best_key = taps_fach_key(r0.c, H);
+    uint64_t best_key = taps_fach_key<C>(r0.c, H);
     if (r0.n_a2a) {   // without AllToAll the sequence would be the same
         M.lim_on = true;
         M.lim_key = best_key;
         M.lim_vol = k.vmin;
         const taps_run_t<taps_fach> r1 = taps_rearrange_t(P, Q, L, M);
         if (!r1.stopped) {
-            const uint64_t k1 = taps_fach_key(r1.c, H);
+            const uint64_t k1 = taps_fach_key<C>(r1.c, H);
             if (k1 < best_key) {
                 k.best = r1.c;
                 k.cand = 1;
@@ -1190,7 +1201,7 @@ __host__ __device__ inline taps_pickh taps_edge_select_h(const taps_row &P, cons
         M.lim_on = false;
     }
     const taps_fach c2 = taps_remove_h(P, L, M);
-    if (taps_fach_key(c2, H) < best_key) {
+    if (taps_fach_key<C>(c2, H) < best_key) {
         k.best = c2;
         k.cand = 2;
     }

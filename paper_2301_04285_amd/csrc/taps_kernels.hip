@@ -414,7 +414,8 @@ __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_co
 
 // Link-class hierarchies: as k_edge_costs, each entry selected and scaled
 // under the classes of H.
-template <uint32_t R>
+// C: the hierarchy's number of classes.
+template <uint32_t R, uint32_t C>
 __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_costs_h(
     const taps_edge_params *__restrict__ params, const taps_row_ref *__restrict__ rows,
     uint32_t n_segs, const taps_desc *__restrict__ desc, taps_launch lp, taps_hier H,
@@ -442,7 +443,7 @@ __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_co
     for (uint32_t j = c0 + lane; j < c1; j += TAPS_TILE_COLS) {
         taps_col Q;
         taps_make_col(Q, col[j], E.caxes, E.rank);
-        const taps_entry_out o = taps_entry_finish_h(taps_edge_select_h(P, Q, H), E.scale, H);
+        const taps_entry_out o = taps_entry_finish_h(taps_edge_select_h<C>(P, Q, H), E.scale, H);
         store_entry(out, row_out, j, o, o.ok ? o.meta : 0xFFFFFFFFu);
     }
 }
@@ -668,12 +669,21 @@ hipError_t taps_launch_edge_costs_h(const taps_edge_params *params, const taps_r
                                     hipStream_t stream) {
     if (n_rows == 0) return hipSuccess;
     const dim3 grid(blocks_for(n_rows, TAPS_ROWS_PER_BLOCK)), block(TAPS_TILE_COLS * TAPS_ROWS_PER_BLOCK);
-    if (max_rank <= TAPS_LOW_RANK)
-        hipLaunchKernelGGL(k_edge_costs_h<TAPS_LOW_RANK>, grid, block, 0, stream, params, rows,
-                           (uint32_t)n_rows, desc, lp, H, out);
-    else
-        hipLaunchKernelGGL(k_edge_costs_h<TAPS_D_MAX_RANK>, grid, block, 0, stream, params, rows,
-                           (uint32_t)n_rows, desc, lp, H, out);
+    const bool low = max_rank <= TAPS_LOW_RANK;
+#define TAPS_H_LAUNCH(RR, CC)                                                                    \
+    hipLaunchKernelGGL((k_edge_costs_h<RR, CC>), grid, block, 0, stream, params, rows,            \
+                       (uint32_t)n_rows, desc, lp, H, out)
+    switch (H.n_classes * 2 + (low ? 0 : 1)) {
+    case 2: TAPS_H_LAUNCH(TAPS_LOW_RANK, 1); break;
+    case 3: TAPS_H_LAUNCH(TAPS_D_MAX_RANK, 1); break;
+    case 4: TAPS_H_LAUNCH(TAPS_LOW_RANK, 2); break;
+    case 5: TAPS_H_LAUNCH(TAPS_D_MAX_RANK, 2); break;
+    case 6: TAPS_H_LAUNCH(TAPS_LOW_RANK, 3); break;
+    case 7: TAPS_H_LAUNCH(TAPS_D_MAX_RANK, 3); break;
+    case 8: TAPS_H_LAUNCH(TAPS_LOW_RANK, 4); break;
+    default: TAPS_H_LAUNCH(TAPS_D_MAX_RANK, 4); break;
+    }
+#undef TAPS_H_LAUNCH
     return hipGetLastError();
 }
 
