@@ -191,8 +191,10 @@ typedef struct {
  * the single strategy splits nothing.  The counts come from an exact count of
  * that filter on the host (ordered runs of distinct partitionable axes over
  * the n levels, each at most as wide as its length allows); the strategies
- * themselves are enumerated on the device, one workgroup per operator, and
- * the call does not synchronise.  TAPS_ERR_NO_STRATEGY if an operator has
+ * themselves are enumerated on the device, one workgroup per chunk of 256
+ * candidate ranks of an operator, each writing at the offset the host counted
+ * for that chunk (the same unranking and filter, checked against the exact
+ * count), and the call does not synchronise.  TAPS_ERR_NO_STRATEGY if an operator has
  * none, TAPS_ERR_CAPACITY if op_offsets[n_ops] > capacity (op_offsets is
  * still written, the strategies are not). */
 taps_status taps_enumerate_strategies(const taps_graph *graph, const taps_cluster *cluster,

@@ -121,12 +121,15 @@ __global__ __launch_bounds__(256) void k_node_costs(const taps_op *__restrict__ 
 }
 
 // GenerateStrategySet, and the whole strategy side of a single-call build, in
-// one launch: one workgroup per operator walks its candidates in canonical
-// order, 256 per pass (a ballot per wavefront, the four wavefront counts
-// scanned in LDS), and writes every valid strategy together with, when asked
-// (desc and node.t not NULL), its descriptor and its node (intra-op) record.
-// A chunk's strategies go to [base, base + count), counted on the host with
-// the same unranking and filter; nothing is written outside that range.
+// one launch: one workgroup per chunk of 256 consecutive candidate ranks of
+// one operator (only chunks that hold a strategy are launched) tests its
+// candidates in canonical order (a ballot per wavefront, the four wavefront
+// counts scanned in LDS) and writes every valid strategy together with, when
+// asked (desc and node.t not NULL), its descriptor and its node (intra-op)
+// record.  A chunk's strategies go to [base, base + count), where the host
+// counted them with the same unranking and filter (plan_build checks the
+// chunks' counts against the exact per-operator count); nothing is written
+// outside that range.
 constexpr uint32_t kBuildThreads = TAPS_BUILD_CHUNK;
 
 // The strategies of one chunk of candidate ranks (a whole workgroup).
