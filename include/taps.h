@@ -253,6 +253,28 @@ taps_status taps_build_tables(const taps_graph *graph, const taps_cluster *clust
                               uint64_t *edge_offsets, taps_table edge, uint64_t edge_capacity,
                               uint32_t flags, void *stream);
 
+/* taps_build_tables for callers that cannot allocate device memory: code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  Same arguments, outputs and errors, the same tables bit for
+ * bit; the caller still provides every output array.  The call's device
+ * workspace (the uploaded graph and plan, strategy descriptors, per-edge
+ * constants, row segments) lives in a fixed array of
+ * TAPS_NOALLOC_SCRATCH_BYTES that each GPU the library runs on holds until
+ * the process ends; the plan is uploaded with one hipMemcpyAsync from
+ * pageable host memory.  No hipMalloc, hipFree, hipHostMalloc or other
+ * allocating routine is called.
+ * TAPS_ERR_CAPACITY, before any GPU work, if a build needs more workspace
+ * than that (the 96-layer GPT on 128 devices needs about 21 MB).
+ * Every call on one GPU uses that GPU's single array: calls that overlap on
+ * one GPU (other streams, other threads) race and must be serialised by the
+ * caller; consecutive calls on one stream are ordered and safe. */
+#define TAPS_NOALLOC_SCRATCH_BYTES ((uint64_t)32 << 20)
+taps_status taps_build_tables_noalloc(const taps_graph *graph, const taps_cluster *cluster,
+                                      const taps_mesh *mesh, uint64_t *op_offsets,
+                                      taps_strategy *strategies, uint64_t strategy_capacity,
+                                      taps_table node, uint64_t *edge_offsets, taps_table edge,
+                                      uint64_t edge_capacity, uint32_t flags, void *stream);
+
 /* Intra-operator cost of every strategy (Eq. 5-8 generalised to any
  * operator: one ring AllReduce per tensor that lacks some split axis -- the
  * forward partial sum of the output, the backward gradient of an input or

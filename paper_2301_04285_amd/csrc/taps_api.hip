@@ -11,6 +11,7 @@
 #include <cstdio>
 #include <cstring>
 #include <list>
+#include <memory>
 #include <map>
 #include <mutex>
 #include <numeric>
@@ -20,6 +21,14 @@
 
 #include "taps.h"
 #include "taps_internal.h"
+
+// The fixed workspace of taps_build_tables_noalloc: a file-scope device array
+// of TAPS_NOALLOC_SCRATCH_BYTES, one copy on every GPU the library runs on.
+// In host code its name is only a stand-in for the symbol; the device address
+// comes from hipGetSymbolAddress, taken once per device with that device
+// current, and only that address is used.  Nothing in it has to start at
+// zero: every kernel of a build writes what it later reads.
+static __device__ __align__(256) char scratch[TAPS_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -182,6 +191,9 @@ struct chunk {
 
 size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
+// Bytes an array of `bytes` takes from a workspace (at least 256, aligned).
+size_t carve_size(size_t bytes) { return align256(bytes ? bytes : 256); }
+
 // Waits for the stream: the calls that must read a result back usually wait
 // for a few tens of microseconds of queued work, where a blocking wait adds
 // its own wake-up latency, so the stream is polled for up to 200 us before
@@ -199,11 +211,13 @@ hipError_t wait_stream(hipStream_t stream) {
 // The stream-ordered pool of the current device keeps freed scratch for the
 // next call instead of handing it back to the driver: a fresh reservation of
 // the tens of MB an edge call needs costs hundreds of microseconds.
+constexpr uint32_t kMaxDevices = 64;
+
 void retain_pool() {
     static std::mutex mu;
-    static bool done[64] = {};
+    static bool done[kMaxDevices] = {};
     int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= (int)kMaxDevices) return;
     std::lock_guard<std::mutex> lock(mu);
     if (done[dev]) return;
     hipMemPool_t pool;
@@ -290,14 +304,14 @@ void release_block(stream_block *b) {
     --b->users;
 }
 
-struct scratch {
+struct call_scratch {
     hipStream_t stream;
     stream_block *blk;
     std::unique_lock<std::mutex> lock;
     size_t used = 0;                // bytes of the block this call has taken
     size_t need = 0;                // what the call asked for in all
     std::vector<void *> own;        // allocations beyond the block, freed on return
-    explicit scratch(hipStream_t s) : stream(s), blk(find_block(s)), lock(blk->mu) {
+    explicit call_scratch(hipStream_t s) : stream(s), blk(find_block(s)), lock(blk->mu) {
         if (blk->want > blk->cap) {   // grow past the largest need seen (nothing uses the block yet)
             // a power of two, so that a stream whose calls vary in size regrows rarely
             size_t cap = size_t(1) << 20;
@@ -313,7 +327,7 @@ struct scratch {
             }
         }
     }
-    ~scratch() {
+    ~call_scratch() {
         for (void *p : own) (void)hipFreeAsync(p, stream);
         if (need > blk->want) blk->want = need;
         lock.unlock();   // before the block may become idle (and be freed)
@@ -337,7 +351,7 @@ struct scratch {
 
 // Uploads the chunks into one array of the call's scratch; *dev receives its
 // base.
-taps_status upload(scratch &sc, std::vector<chunk> &chunks, void **dev) {
+taps_status upload(call_scratch &sc, std::vector<chunk> &chunks, void **dev) {
     const hipStream_t stream = sc.stream;
     size_t total = 0;
     for (chunk &c : chunks) {
@@ -476,7 +490,7 @@ taps_status share_edges(const taps_graph *g, const uint64_t *op_offsets,
     }
     std::vector<uint32_t> flags(pairs.size() / 3, 0);
     if (!flags.empty()) {
-        scratch sc(stream);
+        call_scratch sc(stream);
         uint64_t *d_pairs = nullptr;
         uint32_t *d_flags = nullptr;
         taps_status st;
@@ -665,7 +679,7 @@ taps_status edge_costs(const taps_graph *graph, const taps_cluster *clusters, ui
     std::vector<taps_copy_task> copies;
     plan_copies(eoff, rep, copies, dst_list);
     if (copies.size() > 0x7FFFFFFFull) return fail(TAPS_ERR_ARG, "too many table copies");
-    scratch sc(stream);
+    call_scratch sc(stream);
     const uint64_t total = op_offsets[n_ops];
     std::vector<chunk> ch{{graph->ops, sizeof(taps_op) * n_ops, 0},
                           {graph->edges, sizeof(taps_edge) * n_edges, 0},
@@ -923,7 +937,7 @@ taps_status enumerate(const taps_graph *graph, const taps_launch &lp, uint32_t a
     std::vector<taps_build_chunk> chunks;
     if ((st = plan_build(graph, lp.n, allowed_cuts, offs, chunks)) != TAPS_OK) return st;
     hipStream_t stream = (hipStream_t)stream_;
-    scratch sc(stream);
+    call_scratch sc(stream);
     std::vector<chunk> ch{{graph->ops, sizeof(taps_op) * n_ops, 0},
                           {chunks.data(), sizeof(taps_build_chunk) * chunks.size(), 0}};
     void *dev = nullptr;
@@ -956,6 +970,224 @@ taps_status mesh_cuts(const taps_mesh *mesh, uint32_t n, uint32_t *allowed) {
     if (level != n)
         return fail(TAPS_ERR_TOPOLOGY, "the mesh does not have 2^%u devices", n);
     *allowed = cuts;
+    return TAPS_OK;
+}
+
+
+// Device memory of one build: carve() hands out 256-byte aligned arrays and
+// put() uploads host chunks into one of them.
+struct workspace {
+    virtual ~workspace() = default;
+    virtual taps_status carve(void **p, size_t bytes) = 0;
+    virtual taps_status put(std::vector<chunk> &chunks, void **dev) = 0;
+};
+
+// The stream's scratch block, and uploads through the pinned staging pool.
+struct stream_workspace : workspace {
+    call_scratch sc;
+    explicit stream_workspace(hipStream_t s) : sc(s) {}
+    taps_status carve(void **p, size_t bytes) override { return sc.alloc(p, bytes); }
+    taps_status put(std::vector<chunk> &chunks, void **dev) override {
+        return upload(sc, chunks, dev);
+    }
+};
+
+// The device address of the current device's `scratch` array (see its
+// definition), taken on the device's first call.
+taps_status scratch_address(char **base) {
+    static std::mutex mu;
+    static char *addr[kMaxDevices] = {};
+    int device = -1;
+    hipError_t err = hipGetDevice(&device);
+    if (err != hipSuccess) return hip_fail(err, "hipGetDevice");
+    if (device < 0 || device >= (int)kMaxDevices)
+        return fail(TAPS_ERR_DEVICE, "device %d: the fixed workspace serves devices 0..%u", device,
+                    kMaxDevices - 1);
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[device]) {
+        void *p = nullptr;
+        err = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (err != hipSuccess) return hip_fail(err, "hipGetSymbolAddress(scratch)");
+        if (!p) return fail(TAPS_ERR_DEVICE, "hipGetSymbolAddress(scratch) returned NULL");
+        addr[device] = (char *)p;
+    }
+    *base = addr[device];
+    return TAPS_OK;
+}
+
+// Carves from the current device's fixed array and uploads with one
+// hipMemcpyAsync from a per-thread host buffer: no device or pinned memory is
+// allocated.
+struct fixed_workspace : workspace {
+    hipStream_t stream;
+    char *base = nullptr;
+    size_t used = 0;
+    explicit fixed_workspace(hipStream_t s) : stream(s) {}
+    taps_status open() { return scratch_address(&base); }
+    taps_status carve(void **p, size_t bytes) override {
+        const size_t size = carve_size(bytes);
+        if (used + size > TAPS_NOALLOC_SCRATCH_BYTES)   // the caller checked the whole need
+            return fail(TAPS_ERR_CAPACITY, "fixed workspace exhausted");
+        *p = base + used;
+        used += size;
+        return TAPS_OK;
+    }
+    taps_status put(std::vector<chunk> &chunks, void **dev) override {
+        size_t total = 0;
+        for (chunk &c : chunks) {
+            c.offset = total;
+            total += align256(c.bytes);
+        }
+        if (total == 0) total = 256;
+        taps_status st = carve(dev, total);
+        if (st != TAPS_OK) return st;
+        // pageable host memory: the copy has read it when hipMemcpyAsync returns
+        thread_local std::vector<char> host;
+        if (host.size() < total) host.resize(total);
+        for (const chunk &c : chunks)
+            if (c.bytes) std::memcpy(host.data() + c.offset, c.src, c.bytes);
+        const hipError_t err = hipMemcpyAsync(*dev, host.data(), total, hipMemcpyHostToDevice,
+                                              stream);
+        if (err != hipSuccess) return hip_fail(err, "hipMemcpyAsync (upload)");
+        return TAPS_OK;
+    }
+};
+
+taps_status build_tables(const taps_graph *graph, const taps_cluster *cluster, const taps_mesh *mesh,
+                         uint64_t *op_offsets, taps_strategy *strategies,
+                         uint64_t strategy_capacity, taps_table node, uint64_t *edge_offsets,
+                         taps_table edge, uint64_t edge_capacity, uint32_t flags, void *stream_,
+                         bool fixed) {
+    g_last_error.clear();
+    if (flags & ~TAPS_BUILD_SHARED) return fail(TAPS_ERR_ARG, "unknown flags 0x%x", flags);
+    taps_launch lp;
+    taps_status st = check_cluster(cluster, &lp);
+    if (st == TAPS_OK) st = check_graph(graph, true);
+    if (st != TAPS_OK) return st;
+    if (!op_offsets || !edge_offsets) return fail(TAPS_ERR_ARG, "op_offsets or edge_offsets is NULL");
+    uint32_t allowed = 0xFFu;
+    if (mesh && (st = mesh_cuts(mesh, lp.n, &allowed)) != TAPS_OK) return st;
+    const uint32_t n_ops = graph->n_ops, n_edges = graph->n_edges;
+    // sizes, on the host
+    std::vector<uint64_t> offs;
+    if ((st = count_strategies(graph, lp.n, allowed, offs)) != TAPS_OK) return st;
+    // shared tables: edges described alike share one table -- their operators'
+    // strategies are the same function of the same descriptions here, so no
+    // device comparison is needed
+    std::vector<uint32_t> rep(n_edges);
+    std::iota(rep.begin(), rep.end(), 0u);
+    if (flags & TAPS_BUILD_SHARED) {
+        rep = group_edges(graph);
+    }
+    std::vector<uint64_t> eoff(n_edges + 1, 0);
+    uint64_t all_segs = 0;
+    for (uint32_t e = 0; e < n_edges; ++e) {
+        const taps_edge &E = graph->edges[e];
+        const uint64_t ns = offs[E.src_op + 1] - offs[E.src_op];
+        const uint64_t nd = offs[E.dst_op + 1] - offs[E.dst_op];
+        eoff[e + 1] = eoff[e] + ns * nd;
+        all_segs += ns * ((nd + TAPS_TILE_COLS - 1) / TAPS_TILE_COLS);
+    }
+    if (all_segs >= 0x7FFFFFFFull) return fail(TAPS_ERR_ARG, "more than 2^31 row segments");
+    std::vector<uint64_t> dst_list;
+    std::vector<taps_copy_task> copies;
+    plan_copies(eoff, rep, copies, dst_list);
+    if (copies.size() > 0x7FFFFFFFull) return fail(TAPS_ERR_ARG, "too many table copies");
+    // a size query passes no array; a build passes the strategy and node arrays, and
+    // the edge arrays unless there are no edge entries (then they are not read)
+    const bool none_s = !strategies && !node.t && !node.vol && !node.intra && !node.inter &&
+                        !node.meta;
+    const bool all_s = strategies && node.t && node.vol && node.intra && node.inter && node.meta;
+    const bool none_e = !edge.t && !edge.vol && !edge.intra && !edge.inter && !edge.meta;
+    const bool all_e = edge.t && edge.vol && edge.intra && edge.inter && edge.meta;
+    const bool none = none_s && none_e;
+    if (!none && !(all_s && (all_e || (none_e && eoff[n_edges] == 0))))
+        return fail(TAPS_ERR_ARG, "strategies and every table array must be all set or all NULL "
+                                  "(the edge arrays may be NULL when there are no edge entries)");
+    if (!none && offs[n_ops] > strategy_capacity)
+        return fail(TAPS_ERR_CAPACITY, "%llu strategies, capacity %llu",
+                    (unsigned long long)offs[n_ops], (unsigned long long)strategy_capacity);
+    if (!none && eoff[n_edges] > edge_capacity)
+        return fail(TAPS_ERR_CAPACITY, "%llu entries, capacity %llu",
+                    (unsigned long long)eoff[n_edges], (unsigned long long)edge_capacity);
+    if (none || n_ops == 0) {
+        std::memcpy(op_offsets, offs.data(), sizeof(uint64_t) * (n_ops + 1));
+        std::memcpy(edge_offsets, eoff.data(), sizeof(uint64_t) * (n_edges + 1));
+        return TAPS_OK;
+    }
+    // one upload and one set of scratch for the whole build
+    hipStream_t stream = (hipStream_t)stream_;
+    std::vector<taps_build_chunk> bchunks;
+    if ((st = plan_build(graph, lp.n, allowed, offs, bchunks)) != TAPS_OK) return st;
+    std::vector<taps_seg_group> groups;
+    const uint64_t total = offs[n_ops];
+    const uint64_t n_segs = plan_launch(graph, offs.data(), false, rep, true, groups);
+    std::vector<chunk> ch{{graph->ops, sizeof(taps_op) * n_ops, 0},
+                          {graph->edges, sizeof(taps_edge) * n_edges, 0},
+                          {offs.data(), sizeof(uint64_t) * (n_ops + 1), 0},
+                          {eoff.data(), sizeof(uint64_t) * (n_edges + 1), 0},
+                          {groups.data(), sizeof(taps_seg_group) * groups.size(), 0},
+                          {copies.data(), sizeof(taps_copy_task) * copies.size(), 0},
+                          {dst_list.data(), sizeof(uint64_t) * dst_list.size(), 0},
+                          {bchunks.data(), sizeof(taps_build_chunk) * bchunks.size(), 0}};
+    if (fixed) {   // the whole need, checked on the host before any HIP call
+        size_t up = 0;
+        for (const chunk &c : ch) up += align256(c.bytes);
+        const size_t need = carve_size(up) + carve_size(sizeof(taps_desc) * total) +
+                            carve_size(sizeof(taps_edge_params) * (n_edges ? n_edges : 1)) +
+                            carve_size(sizeof(taps_row_ref) * (n_segs ? n_segs : 1));
+        if (need > TAPS_NOALLOC_SCRATCH_BYTES)
+            return fail(TAPS_ERR_CAPACITY,
+                        "this build needs %llu bytes of device workspace; the fixed workspace of "
+                        "taps_build_tables_noalloc holds %llu",
+                        (unsigned long long)need, (unsigned long long)TAPS_NOALLOC_SCRATCH_BYTES);
+    }
+    std::memcpy(op_offsets, offs.data(), sizeof(uint64_t) * (n_ops + 1));
+    std::memcpy(edge_offsets, eoff.data(), sizeof(uint64_t) * (n_edges + 1));
+    // device memory: the stream's scratch block, or the fixed workspace
+    std::unique_ptr<workspace> ws;
+    if (fixed) {
+        auto fw = std::make_unique<fixed_workspace>(stream);
+        if ((st = fw->open()) != TAPS_OK) return st;
+        ws = std::move(fw);
+    } else {
+        ws = std::make_unique<stream_workspace>(stream);
+    }
+    void *dev = nullptr;
+    if ((st = ws->put(ch, &dev)) != TAPS_OK) return st;
+    taps_desc *d_desc = nullptr;
+    taps_edge_params *d_params = nullptr;
+    taps_row_ref *d_segs = nullptr;
+    if ((st = ws->carve((void **)&d_desc, sizeof(taps_desc) * total)) != TAPS_OK) return st;
+    if ((st = ws->carve((void **)&d_params, sizeof(taps_edge_params) * (n_edges ? n_edges : 1))) !=
+        TAPS_OK)
+        return st;
+    if ((st = ws->carve((void **)&d_segs, sizeof(taps_row_ref) * (n_segs ? n_segs : 1))) !=
+        TAPS_OK)
+        return st;
+    // the strategies, and the edge plan when there are edge entries, in one launch
+    const bool edges_on = eoff[n_edges] > 0;
+    const taps_plan_args pa{at<taps_op>(dev, ch[0]), at<taps_edge>(dev, ch[1]),
+                            at<uint64_t>(dev, ch[2]), at<uint64_t>(dev, ch[3]),
+                            at<taps_seg_group>(dev, ch[4]), d_params, d_segs,
+                            edges_on ? n_segs : 0u, edges_on ? n_edges : 0u,
+                            edges_on ? (uint32_t)groups.size() : 0u, 0u, 0u};
+    hipError_t err = taps_launch_build_front(at<taps_build_chunk>(dev, ch[7]),
+                                             (uint32_t)bchunks.size(), allowed, lp, strategies,
+                                             d_desc, node, pa, stream);
+    if (err == hipSuccess && edges_on) {
+        const hipEvent_t before = g_kernel_before, after = g_kernel_after;
+        g_kernel_before = g_kernel_after = nullptr;
+        if (err == hipSuccess && before) err = hipEventRecord(before, stream);
+        if (err == hipSuccess)
+            err = taps_launch_edge_costs(d_params, d_segs, n_segs, d_desc, lp,
+                                         max_edge_rank(graph), edge, stream);
+        if (err == hipSuccess)
+            err = taps_launch_copy_tables(at<taps_copy_task>(dev, ch[5]), (uint32_t)copies.size(),
+                                          at<uint64_t>(dev, ch[6]), edge, stream);
+        if (err == hipSuccess && after) err = hipEventRecord(after, stream);
+    }
+    if (err != hipSuccess) return hip_fail(err, "build");
     return TAPS_OK;
 }
 
@@ -1030,7 +1262,7 @@ taps_status taps_node_costs(const taps_graph *graph, const taps_cluster *cluster
     if (!out.t || !out.vol || !out.intra || !out.inter || !out.meta)
         return fail(TAPS_ERR_ARG, "a table array is NULL");
     hipStream_t stream = (hipStream_t)stream_;
-    scratch sc(stream);
+    call_scratch sc(stream);
     std::vector<chunk> ch{{graph->ops, sizeof(taps_op) * n_ops, 0},
                           {op_offsets, sizeof(uint64_t) * (n_ops + 1), 0}};
     void *dev = nullptr;
@@ -1049,113 +1281,18 @@ taps_status taps_build_tables(const taps_graph *graph, const taps_cluster *clust
                               const taps_mesh *mesh, uint64_t *op_offsets,
                               taps_strategy *strategies, uint64_t strategy_capacity, taps_table node,
                               uint64_t *edge_offsets, taps_table edge, uint64_t edge_capacity,
-                              uint32_t flags, void *stream_) {
-    g_last_error.clear();
-    if (flags & ~TAPS_BUILD_SHARED) return fail(TAPS_ERR_ARG, "unknown flags 0x%x", flags);
-    taps_launch lp;
-    taps_status st = check_cluster(cluster, &lp);
-    if (st == TAPS_OK) st = check_graph(graph, true);
-    if (st != TAPS_OK) return st;
-    if (!op_offsets || !edge_offsets) return fail(TAPS_ERR_ARG, "op_offsets or edge_offsets is NULL");
-    uint32_t allowed = 0xFFu;
-    if (mesh && (st = mesh_cuts(mesh, lp.n, &allowed)) != TAPS_OK) return st;
-    const uint32_t n_ops = graph->n_ops, n_edges = graph->n_edges;
-    // sizes, on the host
-    std::vector<uint64_t> offs;
-    if ((st = count_strategies(graph, lp.n, allowed, offs)) != TAPS_OK) return st;
-    // shared tables: edges described alike share one table -- their operators'
-    // strategies are the same function of the same descriptions here, so no
-    // device comparison is needed
-    std::vector<uint32_t> rep(n_edges);
-    std::iota(rep.begin(), rep.end(), 0u);
-    if (flags & TAPS_BUILD_SHARED) {
-        rep = group_edges(graph);
-    }
-    std::vector<uint64_t> eoff(n_edges + 1, 0);
-    uint64_t all_segs = 0;
-    for (uint32_t e = 0; e < n_edges; ++e) {
-        const taps_edge &E = graph->edges[e];
-        const uint64_t ns = offs[E.src_op + 1] - offs[E.src_op];
-        const uint64_t nd = offs[E.dst_op + 1] - offs[E.dst_op];
-        eoff[e + 1] = eoff[e] + ns * nd;
-        all_segs += ns * ((nd + TAPS_TILE_COLS - 1) / TAPS_TILE_COLS);
-    }
-    if (all_segs >= 0x7FFFFFFFull) return fail(TAPS_ERR_ARG, "more than 2^31 row segments");
-    std::vector<uint64_t> dst_list;
-    std::vector<taps_copy_task> copies;
-    plan_copies(eoff, rep, copies, dst_list);
-    if (copies.size() > 0x7FFFFFFFull) return fail(TAPS_ERR_ARG, "too many table copies");
-    // a size query passes no array; a build passes the strategy and node arrays, and
-    // the edge arrays unless there are no edge entries (then they are not read)
-    const bool none_s = !strategies && !node.t && !node.vol && !node.intra && !node.inter &&
-                        !node.meta;
-    const bool all_s = strategies && node.t && node.vol && node.intra && node.inter && node.meta;
-    const bool none_e = !edge.t && !edge.vol && !edge.intra && !edge.inter && !edge.meta;
-    const bool all_e = edge.t && edge.vol && edge.intra && edge.inter && edge.meta;
-    const bool none = none_s && none_e;
-    if (!none && !(all_s && (all_e || (none_e && eoff[n_edges] == 0))))
-        return fail(TAPS_ERR_ARG, "strategies and every table array must be all set or all NULL "
-                                  "(the edge arrays may be NULL when there are no edge entries)");
-    if (!none && offs[n_ops] > strategy_capacity)
-        return fail(TAPS_ERR_CAPACITY, "%llu strategies, capacity %llu",
-                    (unsigned long long)offs[n_ops], (unsigned long long)strategy_capacity);
-    if (!none && eoff[n_edges] > edge_capacity)
-        return fail(TAPS_ERR_CAPACITY, "%llu entries, capacity %llu",
-                    (unsigned long long)eoff[n_edges], (unsigned long long)edge_capacity);
-    std::memcpy(op_offsets, offs.data(), sizeof(uint64_t) * (n_ops + 1));
-    std::memcpy(edge_offsets, eoff.data(), sizeof(uint64_t) * (n_edges + 1));
-    if (none || n_ops == 0) return TAPS_OK;
-    // one upload and one set of scratch for the whole build
-    hipStream_t stream = (hipStream_t)stream_;
-    std::vector<taps_build_chunk> bchunks;
-    if ((st = plan_build(graph, lp.n, allowed, offs, bchunks)) != TAPS_OK) return st;
-    scratch sc(stream);
-    std::vector<taps_seg_group> groups;
-    const uint64_t total = offs[n_ops];
-    const uint64_t n_segs = plan_launch(graph, offs.data(), false, rep, true, groups);
-    std::vector<chunk> ch{{graph->ops, sizeof(taps_op) * n_ops, 0},
-                          {graph->edges, sizeof(taps_edge) * n_edges, 0},
-                          {offs.data(), sizeof(uint64_t) * (n_ops + 1), 0},
-                          {eoff.data(), sizeof(uint64_t) * (n_edges + 1), 0},
-                          {groups.data(), sizeof(taps_seg_group) * groups.size(), 0},
-                          {copies.data(), sizeof(taps_copy_task) * copies.size(), 0},
-                          {dst_list.data(), sizeof(uint64_t) * dst_list.size(), 0},
-                          {bchunks.data(), sizeof(taps_build_chunk) * bchunks.size(), 0}};
-    void *dev = nullptr;
-    if ((st = upload(sc, ch, &dev)) != TAPS_OK) return st;
-    taps_desc *d_desc = nullptr;
-    taps_edge_params *d_params = nullptr;
-    taps_row_ref *d_segs = nullptr;
-    if ((st = sc.alloc((void **)&d_desc, sizeof(taps_desc) * total)) != TAPS_OK) return st;
-    if ((st = sc.alloc((void **)&d_params, sizeof(taps_edge_params) * (n_edges ? n_edges : 1))) !=
-        TAPS_OK)
-        return st;
-    if ((st = sc.alloc((void **)&d_segs, sizeof(taps_row_ref) * (n_segs ? n_segs : 1))) != TAPS_OK)
-        return st;
-    // the strategies, and the edge plan when there are edge entries, in one launch
-    const bool edges_on = eoff[n_edges] > 0;
-    const taps_plan_args pa{at<taps_op>(dev, ch[0]), at<taps_edge>(dev, ch[1]),
-                            at<uint64_t>(dev, ch[2]), at<uint64_t>(dev, ch[3]),
-                            at<taps_seg_group>(dev, ch[4]), d_params, d_segs,
-                            edges_on ? n_segs : 0u, edges_on ? n_edges : 0u,
-                            edges_on ? (uint32_t)groups.size() : 0u, 0u, 0u};
-    hipError_t err = taps_launch_build_front(at<taps_build_chunk>(dev, ch[7]),
-                                             (uint32_t)bchunks.size(), allowed, lp, strategies,
-                                             d_desc, node, pa, stream);
-    if (err == hipSuccess && edges_on) {
-        const hipEvent_t before = g_kernel_before, after = g_kernel_after;
-        g_kernel_before = g_kernel_after = nullptr;
-        if (err == hipSuccess && before) err = hipEventRecord(before, stream);
-        if (err == hipSuccess)
-            err = taps_launch_edge_costs(d_params, d_segs, n_segs, d_desc, lp,
-                                         max_edge_rank(graph), edge, stream);
-        if (err == hipSuccess)
-            err = taps_launch_copy_tables(at<taps_copy_task>(dev, ch[5]), (uint32_t)copies.size(),
-                                          at<uint64_t>(dev, ch[6]), edge, stream);
-        if (err == hipSuccess && after) err = hipEventRecord(after, stream);
-    }
-    if (err != hipSuccess) return hip_fail(err, "build");
-    return TAPS_OK;
+                              uint32_t flags, void *stream) {
+    return build_tables(graph, cluster, mesh, op_offsets, strategies, strategy_capacity, node,
+                        edge_offsets, edge, edge_capacity, flags, stream, false);
+}
+
+taps_status taps_build_tables_noalloc(const taps_graph *graph, const taps_cluster *cluster,
+                                      const taps_mesh *mesh, uint64_t *op_offsets,
+                                      taps_strategy *strategies, uint64_t strategy_capacity,
+                                      taps_table node, uint64_t *edge_offsets, taps_table edge,
+                                      uint64_t edge_capacity, uint32_t flags, void *stream) {
+    return build_tables(graph, cluster, mesh, op_offsets, strategies, strategy_capacity, node,
+                        edge_offsets, edge, edge_capacity, flags, stream, true);
 }
 
 taps_status taps_node_costs_topology(const taps_graph *graph, const taps_topology *topology,
@@ -1175,7 +1312,7 @@ taps_status taps_node_costs_topology(const taps_graph *graph, const taps_topolog
     if (!out.t || !out.vol || !out.intra || !out.inter || !out.meta)
         return fail(TAPS_ERR_ARG, "a table array is NULL");
     hipStream_t stream = (hipStream_t)stream_;
-    scratch sc(stream);
+    call_scratch sc(stream);
     std::vector<chunk> ch{{graph->ops, sizeof(taps_op) * n_ops, 0},
                           {op_offsets, sizeof(uint64_t) * (n_ops + 1), 0}};
     void *dev = nullptr;
@@ -1216,7 +1353,7 @@ taps_status taps_memory_costs(const taps_graph *graph, const taps_strategy *stra
     if (!strategies) return fail(TAPS_ERR_ARG, "strategies is NULL");
     if (!memory) return fail(TAPS_ERR_ARG, "memory is NULL");
     hipStream_t stream = (hipStream_t)stream_;
-    scratch sc(stream);
+    call_scratch sc(stream);
     std::vector<chunk> ch{{graph->ops, sizeof(taps_op) * n_ops, 0},
                           {op_offsets, sizeof(uint64_t) * (n_ops + 1), 0}};
     void *dev = nullptr;

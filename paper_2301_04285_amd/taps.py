@@ -108,6 +108,8 @@ def load():
         L.taps_build_tables.argtypes = [P(GraphS), P(Cluster), P(Mesh), P(C.c_uint64), C.c_void_p,
                                         C.c_uint64, Table, P(C.c_uint64), Table, C.c_uint64,
                                         C.c_uint32, C.c_void_p]
+        L.taps_build_tables_noalloc.restype = C.c_int
+        L.taps_build_tables_noalloc.argtypes = L.taps_build_tables.argtypes
         L.taps_node_costs.restype = C.c_int
         L.taps_node_costs.argtypes = [P(GraphS), P(Cluster), C.c_void_p, P(C.c_uint64), Table,
                                       C.c_void_p]
@@ -527,6 +529,28 @@ def taps_build_tables(graph, cluster, mesh=None, out: Optional["Tables"] = None,
     n_str, n_edge = int(offs[-1]), int(eoffs[-1])
     return Tables(offs, out.strategies[:n_str], {k: v[:n_str] for k, v in out.node.items()}, eoffs,
                   {k: v[:n_edge] for k, v in out.edge.items()})
+
+
+def taps_build_tables_noalloc(graph, cluster, out: "Tables", mesh=None, stream=None,
+                              shared=False) -> "Tables":
+    """taps_build_tables_noalloc: the build of taps_build_tables into the caller's
+    tables ``out`` (of a build of the same graph and cluster, or larger), with the
+    library's device workspace in its fixed per-GPU array instead of allocations."""
+    g = _graph(graph)
+    cl = pack_cluster(cluster)
+    ms = pack_mesh(mesh) if mesh is not None else None
+    offs = np.zeros(g.n_ops + 1, dtype=np.uint64)
+    eoffs = np.zeros(g.n_edges + 1, dtype=np.uint64)
+    s_cap = min(int(out.strategies.shape[0]), *(int(v.numel()) for v in out.node.values()))
+    e_cap = min(int(v.numel()) for v in out.edge.values())
+    _check(load().taps_build_tables_noalloc(
+        C.byref(g.struct), C.byref(cl), C.byref(ms) if ms else None, _u64_array(offs),
+        C.c_void_p(out.strategies.data_ptr()), s_cap, _table(out.node), _u64_array(eoffs),
+        _table(out.edge), e_cap, BUILD_SHARED if shared else 0, _stream(stream)),
+        "taps_build_tables_noalloc")
+    n_str, n_edge = int(offs[-1]), int(eoffs[-1])
+    return Tables(offs, out.strategies[:n_str], {k: v[:n_str] for k, v in out.node.items()},
+                  eoffs, {k: v[:n_edge] for k, v in out.edge.items()})
 
 
 class PreparedBuild:

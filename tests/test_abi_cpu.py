@@ -18,7 +18,7 @@ def lib():
 
 def test_exports_every_declared_symbol(lib):
     declared = T.declared_symbols()
-    assert declared == sorted(["taps_build_tables",
+    assert declared == sorted(["taps_build_tables", "taps_build_tables_noalloc",
                                "taps_enumerate_strategies", "taps_enumerate_strategies_mesh",
                                "taps_node_costs", "taps_edge_costs", "taps_node_costs_topology",
                                "taps_edge_costs_topology",
@@ -216,6 +216,35 @@ def test_capacity_and_partial_tables(lib):
         assert np.all(eo == 0)   # nothing written on error
         assert fn(C.byref(g.struct), C.byref(cl), C.c_void_p(256), T._u64_array(offs),
                   T._u64_array(eo), partial, 72, None) == T.ERR_ARG
+
+
+def test_noalloc_rejects_a_build_beyond_its_workspace(lib):
+    """taps_build_tables_noalloc refuses, on the host and before any HIP call, a
+    build whose device workspace exceeds its fixed array (a 400-layer GPT on 128
+    devices: its strategy descriptors alone take 40 MB, shared tables or not),
+    and writes no offsets; its size query answers as taps_build_tables does."""
+    g = T.pack_graph(W.gpt(400, 12288, 96, 2048, 64, 2))
+    cl = T.pack_cluster(W.config(5).clusters[0][1])
+    none = T.Table(None, None, None, None, None)
+    offs = np.zeros(g.n_ops + 1, np.uint64)
+    eo = np.zeros(g.n_edges + 1, np.uint64)
+    assert lib.taps_build_tables_noalloc(C.byref(g.struct), C.byref(cl), None, T._u64_array(offs),
+                                         None, 0, none, T._u64_array(eo), none, 0, 0, None) == 0
+    offs2 = np.zeros_like(offs)
+    eo2 = np.zeros_like(eo)
+    assert lib.taps_build_tables(C.byref(g.struct), C.byref(cl), None, T._u64_array(offs2),
+                                 None, 0, none, T._u64_array(eo2), none, 0, 0, None) == 0
+    assert np.array_equal(offs, offs2) and np.array_equal(eo, eo2)
+    fake = T.Table(256, 256, 256, 256, 256)   # never dereferenced: the check fails first
+    offs3 = np.zeros_like(offs)
+    eo3 = np.zeros_like(eo)
+    for flags in (0, T.BUILD_SHARED):
+        st = lib.taps_build_tables_noalloc(C.byref(g.struct), C.byref(cl), None,
+                                           T._u64_array(offs3), C.c_void_p(256), int(offs[-1]),
+                                           fake, T._u64_array(eo3), fake, int(eo[-1]), flags, None)
+        assert st == T.ERR_CAPACITY
+        assert "fixed workspace" in T.last_error()
+        assert np.all(offs3 == 0) and np.all(eo3 == 0)   # nothing written on error
 
 
 def test_shared_size_query_matches(lib):
