@@ -172,6 +172,50 @@ def test_largest_config_sampled(T):
     assert checked > 90_000
 
 
+def test_largest_config_full_oracle(T):
+    """Every one of the 96-layer GPT's 98,668,128 edge entries against the
+    oracle, built by the benchmark's call (taps_build_tables: long row segments,
+    the rows' remainders launched last).  The oracle's edge tables are computed
+    by a pool of host threads (its calls release the interpreter lock) and each
+    is compared with the GPU's slice as it arrives."""
+    import os
+    from concurrent.futures import ThreadPoolExecutor
+
+    import torch
+    w = W.config(5)
+    name, cl = w.clusters[0]
+    g = w.graph
+    say(f"[gpu] build {w.name}/{name} for the full oracle comparison")
+    tabs = T.build_tables(g, cl)
+    torch.cuda.synchronize()
+    total = int(tabs.edge_offsets[-1])
+    assert total == 98_668_128
+    edge = _host(tabs.edge)
+    del tabs
+    strats = [O.enumerate_strategies(op, cl.devices) for op in g.ops]
+    eoff = [0]
+    for e in g.edges:
+        eoff.append(eoff[-1] + len(strats[e.src]) * len(strats[e.dst]))
+    assert eoff[-1] == total
+
+    def one(x):
+        e = g.edges[x]
+        ref = O.edge_table(g.ops[e.src], strats[e.src], g.ops[e.dst], e.slot, strats[e.dst], cl)
+        a, b = eoff[x], eoff[x + 1]
+        assert_records({f: v[a:b] for f, v in edge.items()}, ref, f"edge {x}")
+        return b - a
+
+    threads = max(1, min(16, len(os.sched_getaffinity(0))))
+    compared = 0
+    with ThreadPoolExecutor(threads) as pool:
+        for k, n in enumerate(pool.map(one, range(len(g.edges)))):
+            compared += n
+            if k % 200 == 199:
+                say(f"[gpu] {k + 1} of {len(g.edges)} edges equal to the oracle ({compared} entries)")
+    say(f"[gpu] all {compared} edge entries equal to the oracle ({threads} host threads)")
+    assert compared == 98_668_128
+
+
 def _entries(g, N):
     counts = [len(O.enumerate_strategies(op, N)) for op in g.ops]
     return sum(counts[e.src] * counts[e.dst] for e in g.edges)
