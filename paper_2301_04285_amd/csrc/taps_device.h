@@ -55,6 +55,18 @@ __host__ __device__ inline uint32_t taps_low_mask(uint32_t k) { return k >= 32u 
 // Bits 0..k-1 for k < 32.
 __host__ __device__ inline uint32_t taps_below(uint32_t k) { return (1u << k) - 1u; }
 
+// w one-bits starting at bit o, ((1 << w) - 1) << o, for w, o < 32 and w + o <= 32:
+// one v_bfm_b32 on the device.
+__host__ __device__ inline uint32_t taps_bfm(uint32_t w, uint32_t o) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    uint32_t r;
+    __asm__("v_bfm_b32 %0, %1, %2" : "=v"(r) : "v"(w), "v"(o));
+    return r;
+#else
+    return ((1u << w) - 1u) << o;
+#endif
+}
+
 // Levels lo .. lo+w-1 (lo + w <= 8).
 __host__ __device__ inline uint32_t taps_levels(uint32_t lo, uint32_t w) {
     return taps_below(lo + w) & ~taps_below(lo);
@@ -245,11 +257,6 @@ __host__ __device__ inline void taps_allreduce(taps_acc &c, uint32_t missing, ui
 // candidates of one entry does not need tbytes at all.
 // ---------------------------------------------------------------------------
 
-// m shifted towards higher levels by d (d may be negative; d in [-8, 8]).
-__host__ __device__ inline uint32_t taps_shift(uint32_t m, int32_t d) {
-    return (m << 16) >> (16 - d);
-}
-
 __host__ __device__ inline uint32_t taps_msb(uint32_t v) { return 31u - (uint32_t)__builtin_clz(v); }
 
 // Producer side of one table row (uniform across a wavefront).
@@ -284,7 +291,11 @@ struct taps_lv {
     uint32_t tgtsrc;        // producer positions the consumer map also uses
     uint32_t st;            // top of the axis holding levels lam - 1 and lam (0 if none)
     uint32_t lo_s;          // its lowest level
-    int32_t dl[TAPS_D_MAX_RANK];
+    // Positions: producer level l of dimension d and consumer level l + dl[d]
+    // hold the same bit of d.  sh[d] = 8 + dl[d], so that a producer mask m of
+    // d moves to the consumer side as (m << sh[d]) >> 8 (no signed shifts).
+    uint32_t sh[TAPS_D_MAX_RANK];
+    uint32_t pt[TAPS_D_MAX_RANK];   // producer levels of d whose position the consumer splits too
 };
 
 // One candidate sequence, in factor units.
@@ -310,16 +321,18 @@ __host__ __device__ inline uint32_t taps_fill(const taps_lv &L, uint32_t x) {
 // of a dimension both maps split forces the cut at the same bit of that
 // dimension on the other side.  Then the axes and their positions.
 __host__ __device__ inline void taps_unify(const taps_row &P, const taps_col &Q, taps_lv &L) {
-    uint32_t pwin[TAPS_D_MAX_RANK], cwin[TAPS_D_MAX_RANK];
+    uint32_t pwin[TAPS_D_MAX_RANK], cwin[TAPS_D_MAX_RANK], back[TAPS_D_MAX_RANK];
     uint32_t cru = 0, home = 0, tgt = 0;
 #pragma unroll
     for (uint32_t d = 0; d < TAPS_D_MAX_RANK; ++d) {
         pwin[d] = cwin[d] = 0;
-        L.dl[d] = 0;
+        L.sh[d] = back[d] = 8u;
+        L.pt[d] = 0;
         if (d >= P.rank) continue;
         const bool both = P.pw[d] && Q.cw[d];
-        const int32_t dl = both ? (int32_t)Q.chi[d] - (int32_t)P.phi[d] : 0;
-        L.dl[d] = dl;
+        const uint32_t sh = both ? Q.chi[d] + 8u - P.phi[d] : 8u;   // 8 + dl, in 0 .. 16
+        L.sh[d] = sh;
+        back[d] = 16u - sh;
         const uint32_t m = P.pw[d] < Q.cw[d] ? P.pw[d] : Q.cw[d];
         if (m >= 2) {
             const uint32_t win = taps_low_mask(m - 1);
@@ -327,18 +340,26 @@ __host__ __device__ inline void taps_unify(const taps_row &P, const taps_col &Q,
             cwin[d] = win << (Q.chi[d] - m + 1);
         }
         cru |= Q.cr[d];
-        if (both && dl == 0) home |= P.pr[d] & Q.cr[d];
-        if (both) tgt |= P.pr[d] & taps_shift(Q.cr[d], -dl);
+        if (both && sh == 8u) home |= P.pr[d] & Q.cr[d];
+        // producer levels whose consumer level (l + dl) the consumer splits in d
+        const uint32_t pt = both ? P.pr[d] & ((Q.cr[d] << (16u - sh)) >> 8) : 0u;
+        L.pt[d] = pt;
+        tgt |= pt;
     }
+    // least fixpoint: each pass moves the cuts inside every window to the other
+    // side (at most 7 cuts exist, so at most 8 passes)
     uint32_t C = (P.pcuts | Q.ccuts) & P.full & ~1u;
     for (uint32_t it = 0; it < TAPS_D_MAX_LEVELS; ++it) {
-        const uint32_t before = C;
+        uint32_t acc = 0;
 #pragma unroll
         for (uint32_t d = 0; d < TAPS_D_MAX_RANK; ++d) {
             if (d >= P.rank) break;
-            C |= taps_shift(C & pwin[d], L.dl[d]) | taps_shift(C & cwin[d], -L.dl[d]);
+            acc = ((C & pwin[d]) << L.sh[d]) | acc;
+            acc = ((C & cwin[d]) << back[d]) | acc;
         }
-        if (C == before) break;
+        const uint32_t next = C | (acc >> 8);
+        if (next == C) break;
+        C = next;
     }
     const uint32_t starts = (C | 1u) & P.full;
     L.tp = P.n ? ((starts >> 1) | (1u << (P.n - 1))) & P.full : 0u;
@@ -357,15 +378,15 @@ __host__ __device__ inline void taps_unify(const taps_row &P, const taps_col &Q,
 }
 
 // Consumer tops whose target position an axis in ats (producer tops) holds.
-__host__ __device__ inline uint32_t taps_blocked(const taps_row &P, const taps_col &Q,
-                                                 const taps_lv &L, uint32_t ats) {
-    uint32_t b = 0;
+__host__ __device__ inline uint32_t taps_blocked(const taps_row &P, const taps_lv &L,
+                                                 uint32_t ats) {
+    uint32_t acc = 0;
 #pragma unroll
     for (uint32_t d = 0; d < TAPS_D_MAX_RANK; ++d) {
         if (d >= P.rank) break;
-        b |= taps_shift(ats & P.pr[d], L.dl[d]) & Q.cr[d];
+        acc = ((ats & L.pt[d]) << L.sh[d]) | acc;
     }
-    return b;
+    return acc >> 8;
 }
 
 // The level holding producer-order rank k.
@@ -386,9 +407,9 @@ struct taps_ax {
 
 __host__ __device__ inline taps_ax taps_axis(const taps_lv &L, uint32_t top) {
     taps_ax a;
-    a.lo = taps_msb(((L.tp & taps_below(top)) << 1) | 1u);
+    a.lo = taps_msb(((L.tp & taps_bfm(top, 0u)) << 1) | 1u);
     a.w = top + 1u - a.lo;
-    a.lv = taps_below(top + 1u) & ~taps_below(a.lo);
+    a.lv = taps_bfm(a.w, a.lo);
     return a;
 }
 
@@ -398,15 +419,18 @@ __host__ __device__ inline taps_ax taps_axis(const taps_lv &L, uint32_t top) {
 // inter-node transfer.
 __host__ __device__ inline void taps_cost(taps_fac &c, uint32_t top, const taps_ax &a,
                                           uint32_t lam, uint32_t e, uint32_t unused) {
-    const uint32_t V = ((1u << a.w) - 1u) << (e + 8u);
-    const bool in_node = top < lam;   // the whole group inside one node
+    const uint32_t V = taps_bfm(a.w, e + 8u);
+    // all ones when the whole group lies inside one node (top < lam)
+    const uint32_t in_node = (uint32_t)((int32_t)(top - lam) >> 31);
     const uint32_t m = a.lo < lam ? a.lo : lam;
-    const uint32_t lct = m - taps_popc(unused & taps_below(m));
+    // groups of replicas inside a node share one transfer: the levels below m
+    // that some dimension uses count
+    const uint32_t lct = taps_popc(taps_bfm(m, 0u) & ~unused);
     c.vol += V;
-    c.intra += in_node ? V : 0u;
-    c.inter += in_node ? 0u : V << lct;
+    c.intra += V & in_node;
+    c.inter += (V << lct) & ~in_node;
     // collectives (bits 0-7), inter-node ones (8-15), sum of their ct (16-31)
-    c.counts += in_node ? 1u : 0x101u + ((1u << lct) << 16);
+    c.counts += 1u + ((0x100u + (1u << (lct + 16u))) & ~in_node);
 }
 
 // AllToAlls (Eq. 10, Eq. 14) of every axis whose top is in x, all issued at
@@ -421,19 +445,19 @@ __host__ __device__ inline void taps_a2a_batch(taps_fac &c, uint32_t x, const ta
     const uint32_t sh = e + 8u;
     const uint32_t low = taps_below(lam);
     const uint32_t whole = 1u << sh;
-    uint32_t sum_in = 0, sum_out = 0;
+    uint32_t sum = 0, sum_in = 0;
     for (uint32_t m = x & ~L.st; m; m &= m - 1u) {
         const uint32_t t = taps_ctz(m);
-        const uint32_t lo = taps_msb(((L.tp & taps_below(t)) << 1) | 1u);
-        const uint32_t V = whole - (1u << (sh + lo - t - 1u));   // width t + 1 - lo
-        sum_in += t < lam ? V : 0u;
-        sum_out += t < lam ? 0u : V;
+        const uint32_t lo = taps_msb(((L.tp & taps_bfm(t, 0u)) << 1) | 1u);
+        const uint32_t V = whole - (whole >> (t + 1u - lo));   // (p - 1) / p of the shard, p = 2^width
+        sum += V;
+        sum_in += V & (uint32_t)((int32_t)(t - lam) >> 31);   // the group inside one node
     }
     const uint32_t n_in = taps_popc(x & low), n_out = taps_popc(x & ~low & ~L.st);
-    const uint32_t lct = lam - taps_popc(unused & low);
-    c.vol += sum_in + sum_out;
+    const uint32_t lct = taps_popc(low & ~unused);
+    c.vol += sum;
     c.intra += sum_in;
-    c.inter += sum_out << lct;
+    c.inter += (sum - sum_in) << lct;
     c.counts += n_in + (n_out << 8) + n_out + ((n_out << lct) << 16);
     if (x & L.st) {
         const uint32_t t = taps_ctz(L.st), lo = L.lo_s;
@@ -582,7 +606,7 @@ __host__ __device__ inline taps_run_t<typename Cm::fac> taps_alg1_t(const taps_r
     taps_state s;
     s.ats = L.src & ~L.home;
     s.atd = L.home;
-    s.blk = taps_blocked(P, Q, L, s.ats);
+    s.blk = taps_blocked(P, L, s.ats);
     s.unused = P.full & ~P.pru;
     s.e = P.e0;
     uint32_t n_a2a = 0;
@@ -598,7 +622,7 @@ __host__ __device__ inline taps_run_t<typename Cm::fac> taps_alg1_t(const taps_r
             const uint32_t mv = L.dst & s.ats & ~s.blk;
             if (!mv) break;
             moved |= mv;
-            s.blk &= ~taps_blocked(P, Q, L, mv);
+            s.blk &= ~taps_blocked(P, L, mv);
             s.ats &= ~mv;
         }
         if (moved) {
@@ -621,7 +645,7 @@ __host__ __device__ inline taps_run_t<typename Cm::fac> taps_alg1_t(const taps_r
             }
         } else {
             const uint32_t top = taps_first_src(P, s.ats);
-            s.blk &= ~taps_blocked(P, Q, L, 1u << top);
+            s.blk &= ~taps_blocked(P, L, 1u << top);
             taps_gather(L, s, c, top, M);
         }
         if (s.ats == 0) break;
@@ -665,7 +689,7 @@ __host__ __device__ inline taps_run_t<typename Cm::fac> taps_rearrange_t(const t
     taps_state s;
     s.ats = L.src & ~L.home;
     s.atd = L.home;
-    s.blk = taps_blocked(P, Q, L, s.ats);
+    s.blk = taps_blocked(P, L, s.ats);
     s.unused = P.full & ~P.pru;
     s.e = P.e0;
     bool stopped = false;
@@ -683,15 +707,15 @@ __host__ __device__ inline taps_run_t<typename Cm::fac> taps_rearrange_t(const t
         const uint32_t b = 1u << top;
         const taps_ax a = taps_axis(L, top);
         M.gather(c, top, a, s.e, s.unused);
-        const uint32_t freed_for = taps_blocked(P, Q, L, b);   // the axis targeting that position
+        const uint32_t freed_for = taps_blocked(P, L, b);   // the axis targeting that position
         s.ats &= ~b;
         s.blk &= ~freed_for;
-        if (L.dst & b & ~s.blk) {
-            s.atd |= b;   // sliced back into its own target: shard and free levels as before
-        } else {
-            s.unused |= a.lv;
-            s.e += a.w;
-        }
+        // sliced back into its own target if that is free (shard and free levels
+        // as before), else kept whole: all ones then
+        const uint32_t keep = (((L.dst & ~s.blk) >> top) & 1u) - 1u;
+        s.atd |= b & ~keep;
+        s.unused |= a.lv & keep;
+        s.e += a.w & keep;
         const uint32_t sf = freed_for & ~(s.ats | s.atd);   // sliced into the freed position
         if (sf) {
             const uint32_t lv = taps_fill(L, sf);
@@ -736,38 +760,38 @@ __host__ __device__ inline taps_fac taps_remove(const taps_row &P, const taps_lv
     const uint32_t lo_s = L.lo_s;
     const uint32_t S = L.st && P.dstr < TAPS_D_MAX_RANK ? taps_fill(L, L.st) : 0u;
     const uint32_t GA = G & ~low & ~S, GB = G & low & ~S;
-    const uint32_t TA = L.tp & GA, TB = L.tp & GB;
+    const uint32_t TA = L.tp & GA, TAB = L.tp & (GA | GB);
     taps_fac c;
-    c.vol = ((1u << taps_popc(G)) - 1u) << (P.e0 + 8u);
+    c.vol = taps_bfm(taps_popc(G), P.e0 + 8u);
     c.intra = c.inter = 0;
     c.counts = 0;
     uint32_t sh = P.e0 + 8u;
     uint32_t unused = P.full & ~P.pru;
+    // levels below lam some dimension still uses: the inter-node group count of
+    // the axes above the node boundary (they leave these levels alone)
+    uint32_t lctA = taps_popc(low & ~unused);
 #pragma unroll
     for (uint32_t d = 0; d < TAPS_D_MAX_RANK; ++d) {
         if (d >= P.rank) break;
         const uint32_t pd = P.pr[d];
         const uint32_t WA = taps_popc(GA & pd), WB = taps_popc(GB & pd);
-        const uint32_t nA = taps_popc(TA & pd), nB = taps_popc(TB & pd);
-        const uint32_t lctA = lam - taps_popc(unused & low);
+        const uint32_t nAB = taps_popc(TAB & pd), nA = taps_popc(TA & pd);
         uint32_t WS = 0;
         if (d == P.dstr) {   // uniform: the only dimension that can hold the straddler
             WS = taps_popc(G & S);
             if (WS) {
-                const uint32_t lctS = lo_s - taps_popc(unused & taps_below(lo_s));
-                const uint32_t VS = ((1u << WS) - 1u) << (sh + WA);
-                c.inter += VS << lctS;
+                const uint32_t lctS = taps_popc(taps_bfm(lo_s, 0u) & ~unused);
+                c.inter += taps_bfm(WS, sh + WA) << lctS;
                 c.counts += 0x101u + ((1u << lctS) << 16);
             }
         }
-        const uint32_t VA = ((1u << WA) - 1u) << sh;
-        const uint32_t VB = ((1u << WB) - 1u) << (sh + WA + WS);
-        c.intra += VB;
-        c.inter += VA << lctA;
-        c.counts += (nA + nB) + (nA << 8) + ((nA << lctA) << 16);
+        c.intra += taps_bfm(WB, sh + WA + WS);
+        c.inter += taps_bfm(WA, sh) << lctA;
+        c.counts += nAB + (nA << 8) + ((nA << lctA) << 16);
+        sh += WA + WB + WS;
         const uint32_t Gd = G & pd;
-        sh += taps_popc(Gd);
         unused |= Gd;
+        lctA -= taps_popc(Gd & low);
     }
     return c;
 }
