@@ -31,6 +31,9 @@ constexpr uint32_t kWave = 64;
 // Completion counts w(k, s, z) for k, s, z in 0..8 (see taps_completions),
 // evaluated by the compiler.
 __constant__ taps_completion_table kCompletions = taps_make_completions();
+// Widths of unified axes by their tops (taps_make_widths), copied to LDS by the
+// edge kernels.
+__constant__ taps_width_table kWidths = taps_make_widths();
 
 template <typename T>
 __device__ inline T *at_byte(T *base, uint32_t offset) {
@@ -321,6 +324,7 @@ __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_co
     const taps_edge_params *__restrict__ params, const taps_row_ref *__restrict__ rows,
     uint32_t n_segs, const taps_desc *__restrict__ desc, taps_launch lp, taps_table out) {
     __shared__ uint8_t rank_tab[TAPS_ROWS_PER_BLOCK][256];
+    __shared__ uint32_t width_tab[256];
     const uint32_t lane = threadIdx.x % TAPS_TILE_COLS;
     const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x / TAPS_TILE_COLS);
     const uint32_t r = blockIdx.x * TAPS_ROWS_PER_BLOCK + wave;
@@ -333,9 +337,11 @@ __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_co
     taps_row P;
     taps_make_row(P, Dp, E.paxes, E.rank, lp.n, lp.lam);
     taps_fill_rank_table(P, rank_tab[wave], lane, TAPS_TILE_COLS);
+    for (uint32_t x = threadIdx.x; x < 256u; x += blockDim.x) width_tab[x] = kWidths.v[x];
     __syncthreads();
     if (!live) return;
     P.to_rank = rank_tab[wave];
+    P.widths = width_tab;
     taps_keys K;
     K.b_inter_red = lp.b_inter_red;
     K.b_intra_red = lp.b_intra_red;
@@ -368,6 +374,7 @@ __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_co
     const taps_edge_params *__restrict__ params, const taps_row_ref *__restrict__ rows,
     uint32_t n_segs, const taps_desc *__restrict__ desc, taps_launch lp, taps_sweep sw) {
     __shared__ uint8_t rank_tab[TAPS_ROWS_PER_BLOCK][256];
+    __shared__ uint32_t width_tab[256];
     const uint32_t lane = threadIdx.x % TAPS_TILE_COLS;
     const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x / TAPS_TILE_COLS);
     const uint32_t r = blockIdx.x * TAPS_ROWS_PER_BLOCK + wave;
@@ -380,9 +387,11 @@ __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_co
     taps_row P;
     taps_make_row(P, Dp, E.paxes, E.rank, lp.n, lp.lam);
     taps_fill_rank_table(P, rank_tab[wave], lane, TAPS_TILE_COLS);
+    for (uint32_t x = threadIdx.x; x < 256u; x += blockDim.x) width_tab[x] = kWidths.v[x];
     __syncthreads();
     if (!live) return;
     P.to_rank = rank_tab[wave];
+    P.widths = width_tab;
     taps_keys any;
     any.b_inter_red = sw.b_inter_red[0];
     any.b_intra_red = sw.b_intra_red[0];
@@ -424,6 +433,7 @@ __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_co
     uint32_t n_segs, const taps_desc *__restrict__ desc, taps_launch lp, taps_hier H,
     taps_table out) {
     __shared__ uint8_t rank_tab[TAPS_ROWS_PER_BLOCK][256];
+    __shared__ uint32_t width_tab[256];
     const uint32_t lane = threadIdx.x % TAPS_TILE_COLS;
     const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x / TAPS_TILE_COLS);
     const uint32_t r = blockIdx.x * TAPS_ROWS_PER_BLOCK + wave;
@@ -436,9 +446,11 @@ __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_co
     taps_row P;
     taps_make_row(P, Dp, E.paxes, E.rank, lp.n, lp.lam);
     taps_fill_rank_table(P, rank_tab[wave], lane, TAPS_TILE_COLS);
+    for (uint32_t x = threadIdx.x; x < 256u; x += blockDim.x) width_tab[x] = kWidths.v[x];
     __syncthreads();
     if (!live) return;
     P.to_rank = rank_tab[wave];
+    P.widths = width_tab;
     const uint64_t row_out = E.out_offset + (uint64_t)i * E.nd;
     const taps_desc *col = desc + E.dst_base;
     const uint32_t c0 = ref.first_col;
