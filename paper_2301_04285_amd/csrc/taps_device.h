@@ -367,22 +367,23 @@ __host__ __device__ inline void taps_unify(const taps_row &P, const taps_col &Q,
         L.sh[d] = back[d] = 8u;
         L.pt[d] = 0;
         if (d >= P.rank) continue;
-        const bool both = P.pw[d] && Q.cw[d];
-        const uint32_t sh = both ? Q.chi[d] + 8u - P.phi[d] : 8u;   // 8 + dl, in 0 .. 16
+        // When either side leaves d whole its run mask is 0, and so is every
+        // mask below: no case split on which sides split d.
+        const uint32_t sh = Q.chi[d] + 8u - P.phi[d];   // 8 + dl, in 0 .. 16
         L.sh[d] = sh;
         back[d] = 16u - sh;
-        const uint32_t m = P.pw[d] < Q.cw[d] ? P.pw[d] : Q.cw[d];
-        if (m >= 2) {
-            const uint32_t win = taps_low_mask(m - 1);
-            pwin[d] = win << (P.phi[d] - m + 1);
-            cwin[d] = win << (Q.chi[d] - m + 1);
-        }
-        cru |= Q.cr[d];
-        if (both && sh == 8u) home |= P.pr[d] & Q.cr[d];
-        // producer levels whose consumer level (l + dl) the consumer splits in d
-        const uint32_t pt = both ? P.pr[d] & ((Q.cr[d] << (16u - sh)) >> 8) : 0u;
+        // producer levels whose consumer level (l + dl) the consumer splits in
+        // d: the top min(pw, cw) levels of the producer's run
+        const uint32_t pt = P.pr[d] & ((Q.cr[d] << (16u - sh)) >> 8);
         L.pt[d] = pt;
         tgt |= pt;
+        cru |= Q.cr[d];
+        // the cut positions inside that part (all its levels but the lowest),
+        // on each side
+        pwin[d] = pt & (pt - 1u);
+        cwin[d] = (pwin[d] << sh) >> 8;
+        // at the same position on both sides when dl = 0
+        home |= pt & (uint32_t)((int32_t)((sh ^ 8u) - 1u) >> 31);
     }
     // least fixpoint: each pass moves the cuts inside every window to the other
     // side (at most 7 cuts exist, so at most 8 passes)
@@ -634,6 +635,31 @@ __host__ __device__ inline uint32_t taps_slice(const taps_lv &L, taps_state &s) 
 //   * once no axis is held at a producer position only slices remain (no
 //     held axis blocks a target), and slices cost nothing: the sequence's
 //     cost is final there.
+// One pass of the printed inner loop: InferSlice, then InferAll2All until
+// nothing moves (the AllToAlls of one closure share one state and are costed
+// together), then, if the first InferSlice sliced, the slices the AllToAlls
+// made possible (a slice frees no position, so a third round finds nothing).
+template <class Cm>
+__host__ __device__ inline void taps_alg1_pass(const taps_row &P, const taps_lv &L, taps_state &s,
+                                               typename Cm::fac &c, uint32_t &n_a2a,
+                                               const Cm &M) {
+    const uint32_t sl = taps_slice(L, s);
+    uint32_t moved = 0;
+    for (;;) {
+        const uint32_t mv = L.dst & s.ats & ~s.blk;
+        if (!mv) break;
+        moved |= mv;
+        s.blk &= ~taps_blocked(P, L, mv);
+        s.ats &= ~mv;
+    }
+    if (moved) {
+        s.atd |= moved;
+        n_a2a += taps_popc(moved);
+        M.a2a(c, moved, L, s.e, s.unused);
+    }
+    if (sl) taps_slice(L, s);
+}
+
 template <class Cm>
 __host__ __device__ inline taps_run_t<typename Cm::fac> taps_alg1_t(const taps_row &P,
                                                                     const taps_col &Q,
@@ -648,50 +674,39 @@ __host__ __device__ inline taps_run_t<typename Cm::fac> taps_alg1_t(const taps_r
     s.unused = P.full & ~P.pru;
     s.e = P.e0;
     uint32_t n_a2a = 0;
-    bool ok = true;
-    for (uint32_t guard = 0;; ++guard) {
-        if (guard > 4 * TAPS_D_MAX_LEVELS) {
-            ok = false;
-            break;
+    taps_alg1_pass(P, L, s, c, n_a2a, M);
+    // Nothing held at a producer position: only slices remain, and they cost
+    // nothing.  Otherwise InferAllGather first gathers the held axes at
+    // positions no consumer axis targets.  Such a gather frees no position
+    // anyone wants, and the axis cannot be sliced back (its target is still
+    // blocked, else it would have moved), so the passes between these gathers
+    // only perform the slices left pending by the last AllToAlls: they run back
+    // to back in producer order, the first alone before the pending slices.
+    uint32_t ug = s.ats & ~L.tgtsrc;
+    if (ug) {
+        if (L.dst & ~(s.ats | s.atd) & ~s.blk) {
+            taps_gather(L, s, c, taps_first_src(P, ug), M);
+            taps_slice(L, s);
+            ug = s.ats & ~L.tgtsrc;
         }
-        const uint32_t sl = taps_slice(L, s);
-        uint32_t moved = 0;
-        for (;;) {
-            const uint32_t mv = L.dst & s.ats & ~s.blk;
-            if (!mv) break;
-            moved |= mv;
-            s.blk &= ~taps_blocked(P, L, mv);
-            s.ats &= ~mv;
-        }
-        if (moved) {
-            s.atd |= moved;
-            n_a2a += taps_popc(moved);
-            M.a2a(c, moved, L, s.e, s.unused);
-        }
-        if (sl) taps_slice(L, s);
-        // nothing held at a producer position: only slices remain, and they cost nothing
-        if (s.ats == 0) break;
-        // InferAllGather / AllGatherFirstUndoneDim
-        uint32_t ug = s.ats & ~L.tgtsrc;
-        if (ug) {
-            if (L.dst & ~(s.ats | s.atd) & ~s.blk) ug = 1u << taps_first_src(P, ug);
-            uint32_t x = P.to_rank[ug];
-            while (x) {
-                const uint32_t top = taps_rank_level(P, taps_ctz(x));
-                x &= x - 1u;
-                taps_gather(L, s, c, top, M);
-            }
-        } else {
-            const uint32_t top = taps_first_src(P, s.ats);
-            s.blk &= ~taps_blocked(P, L, 1u << top);
-            taps_gather(L, s, c, top, M);
-        }
-        if (s.ats == 0) break;
+        for (uint32_t x = P.to_rank[ug]; x; x &= x - 1u)
+            taps_gather(L, s, c, taps_rank_level(P, taps_ctz(x)), M);
+    }
+    // Held axes now sit only at targeted positions (the held set only shrinks):
+    // AllGatherFirstUndoneDim gathers the first in producer order, which frees
+    // its position for the axis targeting it, and a pass follows.  Each round
+    // gathers one held axis, so at most |held| rounds run.
+    while (s.ats) {
+        const uint32_t top = taps_first_src(P, s.ats);
+        s.blk &= ~taps_blocked(P, L, 1u << top);
+        taps_gather(L, s, c, top, M);
+        if (!s.ats) break;
+        taps_alg1_pass(P, L, s, c, n_a2a, M);
     }
     taps_run_t<typename Cm::fac> r;
     r.c = c;
     r.n_a2a = n_a2a;
-    r.ok = ok;
+    r.ok = true;
     r.stopped = false;
     return r;
 }
