@@ -24,10 +24,15 @@ one pass (candidates costed once per entry, one selection and store per
 point); `link_classes` builds them under three link classes (8-device nodes,
 4-node groups, the groups above them); `value` and `roofline` always come from
 the two-class full evaluation.
-`roofline.traffic` is the edge kernel's HBM bytes per launch and
-`roofline.valu` its VALU instruction count, lane utilisation and issue rate,
-both from the committed rocprofv3 counter summary (null once the kernel
-sources differ from the ones the counters were taken with).
+`roofline.traffic` is the edge kernel's HBM bytes per launch, from the
+committed rocprofv3 counter summary (null once the kernel sources differ from
+the ones the counters were taken with).  The kernel's binding limit is VALU
+issue, not HBM: `roofline.valu` gives its wavefront VALU instructions per
+launch (same counter summary) divided by the measured kernel time, against
+the issue ceiling a calibration kernel of plain 32-bit integer VALU
+instructions measures on this GPU (libtaps_calibrate.so).
+`cpu_baseline` runs the oracle over the whole graph on the host's cores
+(the box's share: 16), and single-threaded over its first layers.
 """
 from __future__ import annotations
 
@@ -80,31 +85,79 @@ def measured_traffic(fields):
     return int(fields["traffic_bytes_per_launch"]) if fields else None
 
 
-def measured_valu(fields):
-    if not fields or "valu_instructions_per_64_entries" not in fields:
+def valu_ceiling() -> dict:
+    """Issue rates (wavefront VALU instructions per second, whole GPU) of the
+    calibration kernels: plain 32-bit adds and xors on vector operands (the
+    fastest class on gfx950) and 3-operand / bit-field operations."""
+    import ctypes as C
+    lib = C.CDLL(os.path.join(ROOT, "paper_2301_04285_amd", "libtaps_calibrate.so"))
+    lib.taps_calibrate_valu.restype = C.c_int
+    lib.taps_calibrate_valu.argtypes = [C.c_int, C.c_uint32, C.POINTER(C.c_float),
+                                        C.POINTER(C.c_double), C.POINTER(C.c_uint32)]
+    out = {}
+    for kind, name in ((0, "add_xor"), (1, "bfe_lshl_or")):
+        ms, n, simds = C.c_float(), C.c_double(), C.c_uint32()
+        rc = lib.taps_calibrate_valu(kind, 2000, C.byref(ms), C.byref(n), C.byref(simds))
+        if rc != 0:
+            raise RuntimeError(f"taps_calibrate_valu({kind}) failed: {rc}")
+        rate = n.value / (ms.value * 1e-3)
+        out[name] = {"instr_per_s": rate, "per_simd_per_cycle_at_2p4GHz":
+                     rate / simds.value / 2.4e9, "ms": ms.value}
+    return out
+
+
+def measured_valu(fields, kernel_ms: float, ceiling):
+    """The edge kernel's VALU issue rate against the calibrated ceiling."""
+    if not fields or "valu_instructions_per_launch" not in fields:
         return None
-    return {"instructions_per_64_entries": float(fields["valu_instructions_per_64_entries"]),
-            "lane_utilisation": float(fields["valu_lane_utilisation"]),
-            "issue_per_simd_cycle": float(fields["valu_issue_per_simd_cycle"]),
-            "source": os.path.relpath(COUNTERS, ROOT)}
+    instr = float(fields["valu_instructions_per_launch"])
+    rate = instr / (kernel_ms * 1e-3)
+    out = {"instructions_per_launch": instr,
+           "instructions_per_64_entries": float(fields["valu_instructions_per_64_entries"]),
+           "lane_utilisation": float(fields["valu_lane_utilisation"]),
+           "achieved": rate, "unit": "wavefront VALU instructions/s",
+           "source": os.path.relpath(COUNTERS, ROOT)}
+    if ceiling:
+        out["peak"] = ceiling["add_xor"]["instr_per_s"]
+        out["frac"] = rate / out["peak"]
+        out["peak_source"] = ("calibration kernel: 8 independent chains of v_add_u32/v_xor_b32 "
+                              "per thread, 8 wavefronts per SIMD (libtaps_calibrate.so)")
+        out["slow_class_peak"] = ceiling["bfe_lshl_or"]["instr_per_s"]
+    return out
+
+
+def cpu_model() -> str:
+    """The host CPU's model name as lscpu reports it, else /proc/cpuinfo's."""
+    import subprocess
+    try:
+        text = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for ln in text.splitlines():
+            if ln.strip().startswith("Model name:"):
+                return ln.split(":", 1)[1].strip()
+    except (OSError, subprocess.SubprocessError):
+        pass
+    try:
+        with open("/proc/cpuinfo") as f:
+            return next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), "")
+    except OSError:
+        return ""
 
 
 def cpu_baseline(workload, cluster, layers: int) -> dict:
-    """The oracle as it stands on the ops and edges of the graph's first `layers`
-    transformer layers: single-threaded (`value`), and the same sample with its
-    edge tables spread over the host's cores (`all_cores`; each oracle call is
-    one edge table, run from a thread pool; the calls release the interpreter
-    lock)."""
+    """The oracle as it stands: every strategy, node table and edge table of the
+    whole graph with its edge tables spread over the host's cores (`value`; each
+    oracle call is one edge table, run from a thread pool, and releases the
+    interpreter lock), and single-threaded over the graph's first `layers`
+    transformer layers (`single_core`)."""
     from concurrent.futures import ThreadPoolExecutor
 
     from oracle import oracle as O
 
     g = workload.graph
     ops_per_layer = 14
-    keep = set(range(layers * ops_per_layer))
-    edges = [e for e in g.edges if e.src in keep and e.dst in keep]
 
-    def run(threads: int):
+    def run(keep, threads: int):
+        edges = [e for e in g.edges if e.src in keep and e.dst in keep]
         t0 = time.perf_counter()
         strats = {k: O.enumerate_strategies(g.ops[k], cluster.devices) for k in sorted(keep)}
         for k in sorted(keep):
@@ -119,24 +172,24 @@ def cpu_baseline(workload, cluster, layers: int) -> dict:
         else:
             with ThreadPoolExecutor(threads) as pool:
                 entries = sum(pool.map(one, edges))
-        return entries, time.perf_counter() - t0
+        return entries, len(edges), time.perf_counter() - t0
 
-    entries, dt = run(1)
-    cores = min(16, len(os.sched_getaffinity(0)))
-    entries_mt, dt_mt = run(cores)
-    assert entries_mt == entries
-    model = ""
-    try:
-        with open("/proc/cpuinfo") as f:
-            model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), "")
-    except OSError:
-        pass
-    return {"value": entries / dt, "unit": "edge entries/s", "cores": 1, "kind": "oracle",
-            "cpu_model": model,
-            "sample": f"first {layers} of 96 layers: {len(keep)} ops, {len(edges)} edges, "
-                      f"{entries} edge entries, enumeration + node + edge tables in {dt:.2f} s "
-                      f"on one core",
-            "all_cores": {"value": entries / dt_mt, "cores": cores, "seconds": dt_mt}}
+    # the machine's CPU share is 16 cores for one GPU, whatever the affinity mask shows
+    cores = max(1, min(16, len(os.sched_getaffinity(0))))
+    everything = set(range(len(g.ops)))
+    entries, n_edges, dt = run(everything, cores)
+    sample = set(range(min(len(g.ops), layers * ops_per_layer)))
+    s_entries, s_edges, s_dt = run(sample, 1)
+    return {"value": entries / dt, "unit": "edge entries/s", "cores": cores, "kind": "oracle",
+            "cpu_model": cpu_model(), "affinity_cpus": len(os.sched_getaffinity(0)),
+            "sample": f"the whole graph: {len(g.ops)} ops, {n_edges} edges, {entries} edge "
+                      f"entries, enumeration + node + edge tables in {dt:.2f} s on {cores} "
+                      f"threads",
+            "seconds": dt,
+            "single_core": {"value": s_entries / s_dt, "cores": 1, "seconds": s_dt,
+                            "sample": f"first {layers} of 96 layers: {len(sample)} ops, {s_edges} "
+                                      f"edges, {s_entries} edge entries",
+                            "whole_graph_seconds_extrapolated": entries / (s_entries / s_dt)}}
 
 
 def main() -> int:
@@ -145,8 +198,9 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=5, help="workload 1..5 (default: 5, the largest)")
-    ap.add_argument("--cpu-layers", type=int, default=12,
-                    help="layers of the graph the CPU oracle baseline covers (0 = skip)")
+    ap.add_argument("--cpu-layers", type=int, default=2,
+                    help="layers of the graph the single-threaded CPU oracle baseline covers; "
+                         "the multi-threaded one covers the whole graph (0 = skip both)")
     ap.add_argument("--shared", type=int, default=1,
                     help="also time taps_edge_costs_shared (identical tables computed once) "
                          "and report it under shared_tables (0 = skip)")
@@ -261,6 +315,10 @@ def main() -> int:
 
     bytes_per_launch = BYTES_PER_ENTRY * entries
     counters = counter_summary()
+    ceiling = valu_ceiling()
+    log(f"[bench] VALU ceiling: {ceiling['add_xor']['instr_per_s']:.4g} instr/s "
+        f"({ceiling['add_xor']['per_simd_per_cycle_at_2p4GHz']:.3f} per SIMD per cycle), "
+        f"slow class {ceiling['bfe_lshl_or']['instr_per_s']:.4g}")
     achieved = bytes_per_launch / (kernel_ms * 1e-3) / 1e9
     out = {
         "metric": "edge-cost entries/sec on 1 GPU (full cost-table build: enumerate + node + edge)",
@@ -286,8 +344,11 @@ def main() -> int:
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBPS,
                      "traffic": measured_traffic(counters) if args.config == 5 else None,
-                     # the co-limit: VALU issue (rocprofv3 counters of the same kernel)
-                     "valu": measured_valu(counters) if args.config == 5 else None},
+                     # the binding limit: VALU issue (rocprofv3 counters of the same
+                     # kernel against the calibrated issue ceiling)
+                     "limiter": "valu_issue",
+                     "valu": measured_valu(counters, kernel_ms, ceiling)
+                     if args.config == 5 else None},
     }
     if args.shared:
         # identical edge tables computed once (taps_edge_costs_shared), into a second
@@ -341,7 +402,8 @@ def main() -> int:
             "hbm_write_frac": bytes_per_launch / (h_kernel * 1e-3) / 1e9 / HBM_PEAK_GBPS}
         del other
     if args.cpu_layers > 0 and args.config == 5:
-        log(f"[bench] CPU oracle baseline on {args.cpu_layers} layers")
+        log(f"[bench] CPU oracle baseline: the whole graph on the host's cores, "
+            f"{args.cpu_layers} layers on one core")
         out["cpu_baseline"] = cpu_baseline(w, cl, args.cpu_layers)
     print(json.dumps(out), flush=True)
     return 0

@@ -16,6 +16,9 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libtaps.so")
 SOURCES = ["taps_api.hip", "taps_kernels.hip"]
+# VALU issue-rate calibration for the benchmark's roofline (not the cost-table path)
+CALIB_LIB = os.path.join(HERE, "libtaps_calibrate.so")
+CALIB_SOURCES = ["taps_calibrate.hip"]
 ARCH = "gfx950"
 
 
@@ -26,7 +29,7 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found (ROCm is required to build libtaps.so)")
 
 
-def command(out: str = LIB) -> list:
+def command(out: str = LIB, sources=None) -> list:
     return [
         hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
         # the fp64 cost expression must not be contracted into FMAs
@@ -34,21 +37,27 @@ def command(out: str = LIB) -> list:
         # keep the compiler from forming packed fp32 instructions
         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
         "-I", INCLUDE, "-I", CSRC,
-        *[os.path.join(CSRC, s) for s in SOURCES],
+        *[os.path.join(CSRC, s) for s in (sources or SOURCES)],
         "-o", out,
     ]
 
 
-def build(verbose: bool = False) -> str:
-    tmp = LIB + ".tmp"
-    cmd = command(tmp)
+def _build_one(lib: str, sources, verbose: bool) -> None:
+    tmp = lib + ".tmp"
+    cmd = command(tmp, sources)
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         sys.stderr.write(res.stdout + res.stderr)
-        raise RuntimeError("building libtaps.so failed")
-    os.replace(tmp, LIB)
+        raise RuntimeError(f"building {os.path.basename(lib)} failed")
+    os.replace(tmp, lib)
+
+
+def build(verbose: bool = False) -> str:
+    """Builds libtaps.so and the calibration library; returns libtaps.so's path."""
+    _build_one(LIB, SOURCES, verbose)
+    _build_one(CALIB_LIB, CALIB_SOURCES, verbose)
     return LIB
 
 

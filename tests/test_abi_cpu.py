@@ -34,6 +34,27 @@ def test_exports_every_declared_symbol(lib):
         assert getattr(lib, name) is not None
 
 
+def test_calibration_library_exports_its_header():
+    """libtaps_calibrate.so (the benchmark's VALU issue ceiling) exports what
+    include/taps_calibrate.h declares, and rejects bad arguments on the host."""
+    import os
+    import re
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    header = open(os.path.join(root, "include", "taps_calibrate.h")).read()
+    declared = re.findall(r"^int (taps_\w+)\(", header, flags=re.M)
+    assert declared == ["taps_calibrate_valu"]
+    path = os.path.join(root, "paper_2301_04285_amd", "libtaps_calibrate.so")
+    out = subprocess.run(["nm", "-D", "--defined-only", path], capture_output=True, text=True,
+                         check=True).stdout
+    assert "taps_calibrate_valu" in {ln.split()[-1] for ln in out.splitlines() if ln.strip()}
+    cal = C.CDLL(path)
+    cal.taps_calibrate_valu.restype = C.c_int
+    ms, n, simds = C.c_float(), C.c_double(), C.c_uint32()
+    assert cal.taps_calibrate_valu(2, 10, C.byref(ms), C.byref(n), C.byref(simds)) == 1
+    assert cal.taps_calibrate_valu(0, 0, C.byref(ms), C.byref(n), C.byref(simds)) == 1
+    assert cal.taps_calibrate_valu(0, 10, None, C.byref(n), C.byref(simds)) == 1
+
+
 def test_kernel_events_need_both_or_neither(lib):
     import ctypes as C
     assert lib.taps_set_edge_kernel_events(C.c_void_p(0x1000), None) == T.ERR_ARG

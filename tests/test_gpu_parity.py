@@ -753,8 +753,23 @@ def _same_tables(a, b):
 
 
 @pytest.mark.gpu
+def oracle_check_edges(graph, cluster, tabs, name):
+    """Every edge record of `tabs` (and its strategies) against the oracle."""
+    strats = [O.enumerate_strategies(op, cluster.devices) for op in graph.ops]
+    assert list(np.diff(tabs.op_offsets)) == [len(x) for x in strats], name
+    edge = _host(tabs.edge)
+    for x, e in enumerate(graph.edges):
+        a, b = int(tabs.edge_offsets[x]), int(tabs.edge_offsets[x + 1])
+        ref = O.edge_table(graph.ops[e.src], strats[e.src], graph.ops[e.dst], e.slot,
+                           strats[e.dst], cluster)
+        assert_records({f: v[a:b] for f, v in edge.items()}, ref, f"{name} edge {x}")
+    return int(tabs.edge_offsets[-1])
+
+
 def test_shared_tables_equal_full_evaluation(T):
-    """taps_edge_costs_shared writes exactly the tables of taps_edge_costs."""
+    """taps_edge_costs_shared, and the single-call build with TAPS_BUILD_SHARED,
+    write exactly the tables of taps_edge_costs, and every entry of both equals
+    the oracle's."""
     import torch
     cases = [(W.config(2).graph, W.config(2).clusters[0][1]),
              (W.config(4).graph, W.config(4).clusters[0][1]),
@@ -776,12 +791,20 @@ def test_shared_tables_equal_full_evaluation(T):
             continue
         cases.append((rep, W.Cluster(2, 4, 600 * W.GB, 50 * W.GB)))
     assert len(cases) >= 6
-    for g, cl in cases:
+    checked = 0
+    for k, (g, cl) in enumerate(cases):
         a = T.build_tables(g, cl)
-        b = T.build_tables(g, cl, shared=True)
+        b = T.build_tables(g, cl, shared=True)                 # single call, shared
+        c = T.build_tables(g, cl, shared=True, fused=False)    # taps_edge_costs_shared
         torch.cuda.synchronize()
         assert np.array_equal(a.edge_offsets, b.edge_offsets)
+        assert np.array_equal(a.edge_offsets, c.edge_offsets)
         assert _same_tables(a.edge, b.edge)
+        assert _same_tables(a.edge, c.edge)
+        say(f"[gpu] shared tables case {k}: oracle comparison")
+        checked += oracle_check_edges(g, cl, b, f"shared case {k} (single call)")
+        checked += oracle_check_edges(g, cl, c, f"shared case {k} (separate calls)")
+    say(f"[gpu] {checked} shared-table entries equal to the oracle")
 
 
 @pytest.mark.gpu
