@@ -335,66 +335,72 @@ static int64_t tensor_elems(const or_op *op, const or_tensor *t) {
 }
 
 /* ---------------------------------------------------------------------------
- * Algorithm 2: number of inter-node communication groups inside a node for an
- * AllReduce of a tensor with map M over the axes M does not use.
- * Reading R-d: when an unused axis straddles the node boundary, the in-node
- * factor is multiplied into device_in (the printed line overwrites it, which
- * would forget the factors of earlier axes).
+ * Where the devices of one node sit in the device matrix (the rank layout of
+ * reading R-a: axis 0 fastest, node = rank / L).  Axis k advances the rank
+ * in steps of stride_k = D[0] ... D[k-1]; every size is a power of two, so
+ * the ranks of one node (L consecutive ranks, or all N when N < L) take
+ * in_node(k) = min(D[k], max(1, L / stride_k)) distinct coordinates of axis
+ * k, the same ones on every node.
  * ------------------------------------------------------------------------- */
-int64_t or_allreduce_ct(const int64_t *D, int h, const int32_t *M, int r, int64_t L) {
-    int64_t remain_devices = L;
-    int64_t total_devices = 1;
-    for (int k = 0; k < h; ++k) total_devices *= D[k];
-    int64_t parallel_degree = total_devices;
-    int64_t device_in = 1;
-    for (int d = 0; d < r; ++d)
-        if (M[d] >= 0) parallel_degree /= D[M[d]];
-    for (int k = 0; k < h; ++k) {
-        if (!map_uses(M, r, k) && remain_devices > 1) {
-            if (remain_devices > D[k])
-                device_in = device_in * D[k];
-            else
-                device_in = device_in * remain_devices;
-        }
-        remain_devices = remain_devices / D[k];
-    }
-    if (device_in >= parallel_degree) return 0;
-    if (device_in > 1) return L / device_in;
-    return L;
+static int64_t axis_stride(const int64_t *D, int k) {
+    int64_t s = 1;
+    for (int j = 0; j < k; ++j) s *= D[j];
+    return s;
+}
+
+static int64_t in_node(const int64_t *D, int k, int64_t L) {
+    const int64_t per_node = L / axis_stride(D, k);
+    return per_node <= 1 ? 1 : (per_node < D[k] ? per_node : D[k]);
+}
+
+static int64_t devices_per_node(const int64_t *D, int h, int64_t L) {
+    const int64_t N = axis_stride(D, h);
+    return N < L ? N : L;
 }
 
 /* ---------------------------------------------------------------------------
- * Algorithm 3: inter-node communication groups inside a node for an
- * AllGather (or AllToAll) along device axis g of a tensor with map M.
- * Reading R-e: the loop runs over the axes inside g (the printed bound mixes
- * the dimension index with the axis index), and an axis no dimension uses
- * lets groups share results only for its part that lies inside one node.
- * *k_in receives the number of group members inside one node (the k of the
- * AllToAll paragraph).
+ * Algorithm 2 (inter-node groups of the AllReduce of a tensor with map M over
+ * the axes M does not use), from the layout above.  A group is the set of
+ * devices that agree on every axis M uses; it has prod D[k] members over the
+ * unused axes k, prod in_node(k) of them on one node.  If that is all of
+ * them, the group never leaves its node: 0.  Otherwise every group that
+ * touches a node crosses to other nodes, and the node's devices belong to
+ * devices_per_node / (members on the node) such groups: the count of groups
+ * sharing the node's uplink (Eq. 11-12).  Multiplying the in-node parts of
+ * all unused axes is reading R-d.
+ * ------------------------------------------------------------------------- */
+int64_t or_allreduce_ct(const int64_t *D, int h, const int32_t *M, int r, int64_t L) {
+    int64_t members = 1, on_node = 1;
+    for (int k = 0; k < h; ++k) {
+        if (map_uses(M, r, k)) continue;
+        members *= D[k];
+        on_node *= in_node(D, k, L);
+    }
+    if (on_node == members) return 0;
+    return devices_per_node(D, h, L) / on_node;
+}
+
+/* ---------------------------------------------------------------------------
+ * Algorithm 3 (inter-node groups of an AllGather, or AllToAll, along axis g of
+ * a tensor with map M), from the same layout.  A group is the D[g] devices
+ * that differ only along g, in_node(g) of them on one node (*k_in, the k of
+ * the AllToAll paragraph).  If that is all of them the group stays inside its
+ * node: 0.  Otherwise the node's devices belong to devices_per_node /
+ * in_node(g) groups, and groups that hold the same data -- they differ only
+ * along axes M does not use -- share one inter-node transfer, but only among
+ * the groups on the same node, i.e. through the in-node part of each such
+ * axis (reading R-e): the count is the groups on a node divided by the
+ * product of in_node(k) over the unused axes k other than g.
  * ------------------------------------------------------------------------- */
 int64_t or_gather_ct(const int64_t *D, int h, const int32_t *M, int r, int g, int64_t L,
                      int64_t *k_in) {
-    (void)h;
-    int64_t parallel_degree = D[g];
-    int64_t temp_device_num = 1;
-    int64_t repeat_num = 1;
-    for (int k = 0; k < g; ++k) {
-        int64_t inside_node = temp_device_num >= L ? 1
-                            : (D[k] < L / temp_device_num ? D[k] : L / temp_device_num);
-        temp_device_num *= D[k];
-        if (!map_uses(M, r, k)) repeat_num *= inside_node;
-    }
-    if (temp_device_num >= L) {
-        *k_in = 1;
-        return L / repeat_num;
-    }
-    int64_t remain_devices = L / temp_device_num;
-    if (remain_devices >= parallel_degree) {
-        *k_in = parallel_degree;
-        return 0;
-    }
-    *k_in = remain_devices;
-    return temp_device_num / repeat_num;
+    const int64_t members_on_node = in_node(D, g, L);
+    *k_in = members_on_node;
+    if (members_on_node == D[g]) return 0;
+    int64_t replicas = 1;
+    for (int k = 0; k < h; ++k)
+        if (k != g && !map_uses(M, r, k)) replicas *= in_node(D, k, L);
+    return devices_per_node(D, h, L) / members_on_node / replicas;
 }
 
 /* ---------------------------------------------------------------------------
@@ -720,28 +726,40 @@ static int maps_equal(const int32_t *a, const int32_t *b, int r) {
     return 1;
 }
 
-/* Algorithm 1 (use_a2a = 1: all three optimisations, "replace"); with
- * use_a2a = 0 it is the "rearrange" sequence of Table 2. */
+/* Slices and AllToAlls as far as they go (the inner part of Algorithm 1, with
+ * readings R-g): slice every dimension whose target axis is free, then move
+ * by AllToAll every target axis another dimension holds until none is left
+ * (with use_a2a); repeat while the slices found something.  The AllToAlls of
+ * the last round may free targets whose slices then wait for the next
+ * settle. */
+static int settle(int32_t *M, const int32_t *Mto, int r, int use_a2a, or_redop *seq, int *len) {
+    for (;;) {
+        const int sliced = infer_slice(M, Mto, r, seq, len);
+        if (sliced < 0) return -1;
+        for (int moved = use_a2a; moved;) {
+            moved = infer_all2all(M, Mto, r, seq, len);
+            if (moved < 0) return -1;
+        }
+        if (!sliced) return 0;
+    }
+}
+
+/* Algorithm 1 ("replace"; without AllToAll, use_a2a = 0, the "rearrange"
+ * sequence of Table 2): until the map reaches the target, settle it, then
+ * gather one dimension -- the first one split now but whole in the target,
+ * else the first one split by an axis that is not its target one (a no-op
+ * when there is none, reading R-g).  Every round gathers or settles at least
+ * one dimension, so 4r + 8 rounds bound it. */
 static int optimized_redistribution(const int32_t *Mfrom, const int32_t *Mto, int r, int use_a2a,
                                     or_redop *seq) {
     int32_t M[OR_MAX_SUB];
     memcpy(M, Mfrom, sizeof(int32_t) * (size_t)r);
     int len = 0;
-    for (int guard = 0; !maps_equal(M, Mto, r); ++guard) {
-        if (guard > 4 * r + 8) return -1;
-        int s_flag = 1;
-        while (s_flag) {
-            s_flag = infer_slice(M, Mto, r, seq, &len);
-            if (s_flag < 0) return -1;
-            int a2a_flag = use_a2a;
-            while (a2a_flag) {
-                a2a_flag = infer_all2all(M, Mto, r, seq, &len);
-                if (a2a_flag < 0) return -1;
-            }
-        }
-        int ag_flag = infer_allgather(M, Mto, r, seq, &len);
-        if (ag_flag < 0) return -1;
-        if (!ag_flag && allgather_first_undone_dim(M, Mto, r, seq, &len) < 0) return -1;
+    for (int round = 0; !maps_equal(M, Mto, r); ++round) {
+        if (round > 4 * r + 8 || settle(M, Mto, r, use_a2a, seq, &len) < 0) return -1;
+        const int gathered = infer_allgather(M, Mto, r, seq, &len);
+        if (gathered < 0) return -1;
+        if (!gathered && allgather_first_undone_dim(M, Mto, r, seq, &len) < 0) return -1;
     }
     return len;
 }
