@@ -640,10 +640,9 @@ __host__ __device__ inline uint32_t taps_slice(const taps_lv &L, taps_state &s) 
 // together), then, if the first InferSlice sliced, the slices the AllToAlls
 // made possible (a slice frees no position, so a third round finds nothing).
 template <class Cm>
-__host__ __device__ inline void taps_alg1_pass(const taps_row &P, const taps_lv &L, taps_state &s,
-                                               typename Cm::fac &c, uint32_t &n_a2a,
-                                               const Cm &M) {
-    const uint32_t sl = taps_slice(L, s);
+__host__ __device__ inline void taps_alg1_settle(const taps_row &P, const taps_lv &L,
+                                                 taps_state &s, typename Cm::fac &c,
+                                                 uint32_t &n_a2a, const Cm &M, uint32_t sl) {
     uint32_t moved = 0;
     for (;;) {
         const uint32_t mv = L.dst & s.ats & ~s.blk;
@@ -661,20 +660,43 @@ __host__ __device__ inline void taps_alg1_pass(const taps_row &P, const taps_lv 
 }
 
 template <class Cm>
+__host__ __device__ inline void taps_alg1_pass(const taps_row &P, const taps_lv &L, taps_state &s,
+                                               typename Cm::fac &c, uint32_t &n_a2a,
+                                               const Cm &M) {
+    const uint32_t sl = taps_slice(L, s);
+    taps_alg1_settle(P, L, s, c, n_a2a, M, sl);
+}
+
+// The common start of the sequences: every axis not at its target held at its
+// producer position, the home axes placed, and the first InferSlice done
+// (slice = what it sliced).  Algorithm 1 and "rearrange" both begin here.
+struct taps_start {
+    taps_state s;
+    uint32_t slice;
+};
+
+__host__ __device__ inline taps_start taps_begin(const taps_row &P, const taps_lv &L) {
+    taps_start b;
+    b.s.ats = L.src & ~L.home;
+    b.s.atd = L.home;
+    b.s.blk = taps_blocked(P, L, b.s.ats);
+    b.s.unused = P.full & ~P.pru;
+    b.s.e = P.e0;
+    b.slice = taps_slice(L, b.s);
+    return b;
+}
+
+template <class Cm>
 __host__ __device__ inline taps_run_t<typename Cm::fac> taps_alg1_t(const taps_row &P,
                                                                     const taps_col &Q,
                                                                     const taps_lv &L,
-                                                                    const Cm &M) {
+                                                                    const Cm &M,
+                                                                    const taps_start &b) {
     typename Cm::fac c;
     taps_fac_zero(c);
-    taps_state s;
-    s.ats = L.src & ~L.home;
-    s.atd = L.home;
-    s.blk = taps_blocked(P, L, s.ats);
-    s.unused = P.full & ~P.pru;
-    s.e = P.e0;
+    taps_state s = b.s;
     uint32_t n_a2a = 0;
-    taps_alg1_pass(P, L, s, c, n_a2a, M);
+    taps_alg1_settle(P, L, s, c, n_a2a, M, b.slice);
     // Nothing held at a producer position: only slices remain, and they cost
     // nothing.  Otherwise InferAllGather first gathers the held axes at
     // positions no consumer axis targets.  Such a gather frees no position
@@ -712,9 +734,14 @@ __host__ __device__ inline taps_run_t<typename Cm::fac> taps_alg1_t(const taps_r
 }
 
 __host__ __device__ inline taps_run taps_alg1(const taps_row &P, const taps_col &Q,
-                                              const taps_lv &L) {
+                                              const taps_lv &L, const taps_start &b) {
     const taps_two_class M{P.lam, nullptr, nullptr};
-    return taps_alg1_t(P, Q, L, M);
+    return taps_alg1_t(P, Q, L, M, b);
+}
+
+__host__ __device__ inline taps_run taps_alg1(const taps_row &P, const taps_col &Q,
+                                              const taps_lv &L) {
+    return taps_alg1(P, Q, L, taps_begin(P, L));
 }
 
 // Algorithm 1 without AllToAll ("rearrange" in Table 2).  Without AllToAll
@@ -736,17 +763,12 @@ template <class Cm>
 __host__ __device__ inline taps_run_t<typename Cm::fac> taps_rearrange_t(const taps_row &P,
                                                                          const taps_col &Q,
                                                                          const taps_lv &L,
-                                                                         const Cm &M) {
+                                                                         const Cm &M,
+                                                                         const taps_start &b) {
     typename Cm::fac c;
     taps_fac_zero(c);
-    taps_state s;
-    s.ats = L.src & ~L.home;
-    s.atd = L.home;
-    s.blk = taps_blocked(P, L, s.ats);
-    s.unused = P.full & ~P.pru;
-    s.e = P.e0;
+    taps_state s = b.s;   // InferSlice once
     bool stopped = false;
-    taps_slice(L, s);
     // producer ranks of the untargeted held axes in bits 0-7, of the targeted ones in bits 8-15
     uint32_t x = (uint32_t)P.to_rank[s.ats & ~L.tgtsrc] |
                  ((uint32_t)P.to_rank[s.ats & L.tgtsrc] << 8);
@@ -789,7 +811,14 @@ __host__ __device__ inline taps_run taps_rearrange(const taps_row &P, const taps
                                                    const taps_lv &L, const taps_limit &lim,
                                                    const taps_keys &K) {
     const taps_two_class M{P.lam, &K, &lim};
-    return taps_rearrange_t(P, Q, L, M);
+    return taps_rearrange_t(P, Q, L, M, taps_begin(P, L));
+}
+
+__host__ __device__ inline taps_run taps_rearrange(const taps_row &P, const taps_col &Q,
+                                                   const taps_lv &L, const taps_limit &lim,
+                                                   const taps_keys &K, const taps_start &b) {
+    const taps_two_class M{P.lam, &K, &lim};
+    return taps_rearrange_t(P, Q, L, M, b);
 }
 
 // "remove" (Table 2): gather every held axis not at its target, lowest
@@ -900,7 +929,8 @@ __host__ __device__ inline taps_pick taps_edge_select(const taps_row &P, const t
                                                       const taps_keys &K) {
     taps_lv L;
     taps_unify(P, Q, L);
-    const taps_run r0 = taps_alg1(P, Q, L);
+    const taps_start b = taps_begin(P, L);
+    const taps_run r0 = taps_alg1(P, Q, L, b);
     taps_pick k;
     k.best = r0.c;
     k.cand = 0;
@@ -913,7 +943,7 @@ __host__ __device__ inline taps_pick taps_edge_select(const taps_row &P, const t
     lim.vol = k.vmin;
     lim.intra = lim.inter = 0;
     if (r0.n_a2a) {   // without AllToAll the sequence would be the same
-        const taps_run r1 = taps_rearrange(P, Q, L, lim, K);
+        const taps_run r1 = taps_rearrange(P, Q, L, lim, K, b);
         k.ok = k.ok && r1.ok;
         if (!r1.stopped) {
             if (taps_less(r1.c, k.best, K)) {
@@ -950,7 +980,8 @@ __host__ __device__ inline taps_cands taps_edge_candidates(const taps_row &P, co
                                                            const taps_keys &any) {
     taps_lv L;
     taps_unify(P, Q, L);
-    const taps_run r0 = taps_alg1(P, Q, L);
+    const taps_start b = taps_begin(P, L);
+    const taps_run r0 = taps_alg1(P, Q, L, b);
     taps_cands k;
     k.c[0] = r0.c;
     k.ok = r0.ok;
@@ -965,7 +996,7 @@ __host__ __device__ inline taps_cands taps_edge_candidates(const taps_row &P, co
         lim.vol = r0.c.vol;
         lim.intra = r0.c.intra;
         lim.inter = r0.c.inter;
-        const taps_run r1 = taps_rearrange(P, Q, L, lim, any);
+        const taps_run r1 = taps_rearrange(P, Q, L, lim, any, b);
         k.ok = k.ok && r1.ok;
         if (r1.stopped) {
             k.has_rearrange = false;
@@ -1255,7 +1286,8 @@ __host__ __device__ inline taps_pickh taps_edge_select_h(const taps_row &P, cons
     taps_lv L;
     taps_unify(P, Q, L);
     taps_hier_model_t<C> M{&H, 0, 0, false};
-    const taps_run_t<taps_fach> r0 = taps_alg1_t(P, Q, L, M);
+    const taps_start b = taps_begin(P, L);
+    const taps_run_t<taps_fach> r0 = taps_alg1_t(P, Q, L, M, b);
     taps_pickh k;
     k.best = r0.c;
     k.cand = 0;
@@ -1266,7 +1298,7 @@ __host__ __device__ inline taps_pickh taps_edge_select_h(const taps_row &P, cons
         M.lim_on = true;
         M.lim_key = best_key;
         M.lim_vol = k.vmin;
-        const taps_run_t<taps_fach> r1 = taps_rearrange_t(P, Q, L, M);
+        const taps_run_t<taps_fach> r1 = taps_rearrange_t(P, Q, L, M, b);
         if (!r1.stopped) {
             const uint64_t k1 = taps_fach_key<C>(r1.c, H);
             if (k1 < best_key) {
