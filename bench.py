@@ -14,8 +14,7 @@ Prints one JSON line.  `value` is edge entries per second of whole steps;
 `roofline` relates the edge-table kernel (which dominates the step), timed
 with HIP events the library records right around its launch on the same
 stream, to MI355X's 8 TB/s HBM: each entry writes 36 bytes (t 8, vol 8,
-intra 8, inter 8, meta 4).  `cpu_baseline` times the CPU oracle,
-single-threaded and on all host cores, on the first layers of the same graph.
+intra 8, inter 8, meta 4).
 `shared_tables` times the same build with identical edge tables computed once
 (the paper searches one layer of a stack of identical layers) and checks the
 result equal to the full evaluation;
@@ -31,8 +30,8 @@ issue, not HBM: `roofline.valu` gives its wavefront VALU instructions per
 launch (same counter summary) divided by the measured kernel time, against
 the issue ceiling a calibration kernel of plain 32-bit integer VALU
 instructions measures on this GPU (libtaps_calibrate.so).
-`cpu_baseline` runs the oracle over the whole graph on the host's cores
-(the box's share: 16), and single-threaded over its first layers.
+`cpu_baseline` runs the CPU oracle over the whole graph on the host's cores
+(one GPU's share of the host: 16), and single-threaded over its first layers.
 """
 from __future__ import annotations
 
@@ -126,21 +125,32 @@ def measured_valu(fields, kernel_ms: float, ceiling):
     return out
 
 
-def cpu_model() -> str:
-    """The host CPU's model name as lscpu reports it, else /proc/cpuinfo's."""
+def cpu_info() -> dict:
+    """The host CPU as lscpu reports it (model name, family / model / stepping,
+    sockets, cores, threads, online CPUs, hypervisor), else /proc/cpuinfo's
+    model name."""
     import subprocess
+    keys = {"Model name": "model_name", "CPU family": "family", "Model": "model",
+            "Stepping": "stepping", "Socket(s)": "sockets", "Core(s) per socket": "cores_per_socket",
+            "Thread(s) per core": "threads_per_core", "CPU(s)": "online_cpus",
+            "Hypervisor vendor": "hypervisor", "CPU max MHz": "max_mhz"}
+    out = {}
     try:
         text = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
         for ln in text.splitlines():
-            if ln.strip().startswith("Model name:"):
-                return ln.split(":", 1)[1].strip()
+            k, _, v = ln.partition(":")
+            if k.strip() in keys and keys[k.strip()] not in out:
+                out[keys[k.strip()]] = v.strip()
     except (OSError, subprocess.SubprocessError):
         pass
-    try:
-        with open("/proc/cpuinfo") as f:
-            return next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), "")
-    except OSError:
-        return ""
+    if "model_name" not in out:
+        try:
+            with open("/proc/cpuinfo") as f:
+                out["model_name"] = next((ln.split(":", 1)[1].strip() for ln in f
+                                          if ln.startswith("model name")), "")
+        except OSError:
+            out["model_name"] = ""
+    return out
 
 
 def cpu_baseline(workload, cluster, layers: int) -> dict:
@@ -174,14 +184,16 @@ def cpu_baseline(workload, cluster, layers: int) -> dict:
                 entries = sum(pool.map(one, edges))
         return entries, len(edges), time.perf_counter() - t0
 
-    # the machine's CPU share is 16 cores for one GPU, whatever the affinity mask shows
+    # one GPU's share of the machine's host is 16 cores, whatever the affinity mask
+    # shows; host_cpus and affinity_cpus are reported beside it
     cores = max(1, min(16, len(os.sched_getaffinity(0))))
     everything = set(range(len(g.ops)))
     entries, n_edges, dt = run(everything, cores)
     sample = set(range(min(len(g.ops), layers * ops_per_layer)))
     s_entries, s_edges, s_dt = run(sample, 1)
     return {"value": entries / dt, "unit": "edge entries/s", "cores": cores, "kind": "oracle",
-            "cpu_model": cpu_model(), "affinity_cpus": len(os.sched_getaffinity(0)),
+            "cpu": cpu_info(), "host_cpus": os.cpu_count(),
+            "affinity_cpus": len(os.sched_getaffinity(0)),
             "sample": f"the whole graph: {len(g.ops)} ops, {n_edges} edges, {entries} edge "
                       f"entries, enumeration + node + edge tables in {dt:.2f} s on {cores} "
                       f"threads",
