@@ -419,6 +419,18 @@ taps_status taps_edge_costs_sweep(const taps_graph *graph, const taps_cluster *c
  * the caller.  TAPS_ERR_ARG if exactly one of them is NULL. */
 taps_status taps_set_edge_kernel_events(void *before, void *after);
 
+/* Launch-shape setting, not part of the method: single-table edge launches
+ * (taps_edge_costs, taps_edge_costs_shared, taps_edge_costs_backward,
+ * taps_edge_costs_topology, taps_build_tables) whose tables hold at least
+ * `min_segments` row segments of eight 64-entry tiles run those long segments
+ * (each edge's full-length segments first, the rows' remainders last, longest
+ * first); smaller launches, and the bandwidth sweep, run segments of at most two
+ * tiles in row order.  Both shapes write the same tables; the setting only moves
+ * the size at which the launch changes shape (default 32768; 0 or 1: every
+ * launch with at least one segment runs long ones).  Process-wide, read when a
+ * launch is planned; returns the previous value.  Never fails. */
+uint64_t taps_set_long_segments_min(uint64_t min_segments);
+
 /* Static name of a status code. */
 const char *taps_status_str(taps_status status);
 

@@ -6,6 +6,7 @@
 // computed on the GPU.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <chrono>
 #include <cstdarg>
 #include <cstdio>
@@ -600,13 +601,15 @@ uint64_t plan_segments(const taps_graph *graph, const uint64_t *op_offsets, bool
 // The segments of a launch: one table, long segments (remainders last) when
 // there are enough of them to fill the GPU many times over, else short ones;
 // several tables (the bandwidth sweep), short ones in row order.
+std::atomic<uint64_t> g_long_segs_min{TAPS_LONG_SEGS_MIN};
+
 uint64_t plan_launch(const taps_graph *graph, const uint64_t *op_offsets, bool reverse,
                      const std::vector<uint32_t> &rep, bool one_table,
                      std::vector<taps_seg_group> &groups) {
     if (one_table) {
         const uint64_t n = plan_segments(graph, op_offsets, reverse, rep,
                                          TAPS_TILE_COLS * TAPS_SEG_TILES_LONG, true, groups);
-        if (n >= TAPS_LONG_SEGS_MIN) return n;
+        if (n >= g_long_segs_min.load(std::memory_order_relaxed)) return n;
     }
     return plan_segments(graph, op_offsets, reverse, rep, TAPS_TILE_COLS * TAPS_SEG_TILES_SHORT,
                          one_table, groups);
@@ -1209,6 +1212,10 @@ const char *taps_status_str(taps_status s) {
 }
 
 const char *taps_last_error(void) { return g_last_error.c_str(); }
+
+uint64_t taps_set_long_segments_min(uint64_t min_segments) {
+    return g_long_segs_min.exchange(min_segments);
+}
 
 taps_status taps_set_edge_kernel_events(void *before, void *after) {
     g_last_error.clear();

@@ -129,6 +129,8 @@ def load():
                                         C.c_void_p]
         L.taps_set_edge_kernel_events.restype = C.c_int
         L.taps_set_edge_kernel_events.argtypes = [C.c_void_p, C.c_void_p]
+        L.taps_set_long_segments_min.restype = C.c_uint64
+        L.taps_set_long_segments_min.argtypes = [C.c_uint64]
         L.taps_status_str.restype = C.c_char_p
         L.taps_status_str.argtypes = [C.c_int]
         L.taps_last_error.restype = C.c_char_p
@@ -141,7 +143,7 @@ def declared_symbols() -> List[str]:
     """Entry points declared in include/taps.h."""
     with open(HEADER) as f:
         text = f.read()
-    return sorted(set(re.findall(r"^\s*(?:taps_status|const char \*)\s*(taps_\w+)\s*\(", text,
+    return sorted(set(re.findall(r"^\s*(?:taps_status|const char \*|uint64_t)\s*(taps_\w+)\s*\(", text,
                                  flags=re.M)))
 
 
@@ -429,6 +431,13 @@ def taps_edge_costs_sweep(graph, clusters, strategies, op_offsets, out=None, str
     _check(st, "taps_edge_costs_sweep")
     total = int(eoffs[-1])
     return eoffs, [{k: v[:total] for k, v in o.items()} for o in out]
+
+
+def taps_set_long_segments_min(min_segments: int) -> int:
+    """Single-table edge launches with at least ``min_segments`` row segments
+    run long (eight-tile) segments, remainders last; returns the previous
+    threshold.  The tables are the same either way."""
+    return int(load().taps_set_long_segments_min(int(min_segments)))
 
 
 def taps_set_edge_kernel_events(before, after) -> None:

@@ -24,7 +24,8 @@ def test_exports_every_declared_symbol(lib):
                                "taps_edge_costs_topology",
                                "taps_edge_costs_shared", "taps_edge_costs_backward",
                                "taps_edge_costs_sweep", "taps_memory_costs",
-                               "taps_set_edge_kernel_events", "taps_status_str",
+                               "taps_set_edge_kernel_events", "taps_set_long_segments_min",
+                               "taps_status_str",
                                "taps_last_error"])
     out = subprocess.run(["nm", "-D", "--defined-only", T.LIB_PATH], capture_output=True,
                          text=True, check=True).stdout
@@ -61,6 +62,13 @@ def test_kernel_events_need_both_or_neither(lib):
     assert "both" in T.last_error()
     assert lib.taps_set_edge_kernel_events(None, C.c_void_p(0x1000)) == T.ERR_ARG
     assert lib.taps_set_edge_kernel_events(None, None) == 0
+
+
+def test_long_segment_threshold_setting(lib):
+    # the launch-shape threshold: returns the previous value, default 32768
+    prev = T.taps_set_long_segments_min(5)
+    assert prev == 32768
+    assert T.taps_set_long_segments_min(prev) == 5
 
 
 def test_status_strings(lib):

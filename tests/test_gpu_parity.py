@@ -120,6 +120,27 @@ def test_full_tables_config3_both_views(T):
         full_check(T, w.graph, cl, f"{w.name}/{name}")
 
 
+def test_long_segments_on_small_configs(T):
+    """The long-segment launch shape (eight-tile row segments, each edge's
+    full-length ones first, the rows' remainders last, longest first), which
+    only launches of at least 32,768 segments take by default, forced on
+    configurations 1-4 and random graphs and compared with the oracle in full."""
+    prev = T.taps_set_long_segments_min(1)
+    try:
+        for cfg in (1, 2, 3, 4):
+            w = W.config(cfg)
+            for name, cl in w.clusters:
+                full_check(T, w.graph, cl, f"long segments {w.name}/{name}")
+        from paper_2301_04285_amd.taps import TapsError
+        for k, (g, cl) in enumerate(_random_cases(7, 12)):
+            try:
+                full_check(T, g, cl, f"long segments random {k}")
+            except TapsError as ex:
+                assert ex.status == T.ERR_NO_STRATEGY
+    finally:
+        T.taps_set_long_segments_min(prev)
+
+
 def test_largest_config_sampled(T):
     """The 96-layer GPT on 16 x 8 devices, built whole in HBM."""
     import torch
@@ -752,7 +773,6 @@ def _same_tables(a, b):
     return all(torch.equal(a[f], b[f]) for f in ("t", "vol", "intra", "inter", "meta"))
 
 
-@pytest.mark.gpu
 def oracle_check_edges(graph, cluster, tabs, name):
     """Every edge record of `tabs` (and its strategies) against the oracle."""
     strats = [O.enumerate_strategies(op, cluster.devices) for op in graph.ops]
