@@ -80,6 +80,29 @@ __host__ __device__ inline uint32_t taps_bfm(uint32_t w, uint32_t o) {
 #endif
 }
 
+// The low w bits, (1 << w) - 1 for w < 32: taps_bfm(w, 0) with the offset as
+// an inline constant (no register holding the zero).
+__host__ __device__ inline uint32_t taps_low(uint32_t w) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    uint32_t r;
+    __asm__("v_bfm_b32 %0, %1, 0" : "=v"(r) : "v"(w));
+    return r;
+#else
+    return (1u << w) - 1u;
+#endif
+}
+
+// 1 << k for k < 16: taps_shl16(1, k) with the one as an inline constant.
+__host__ __device__ inline uint32_t taps_bit16(uint32_t k) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    uint32_t r;
+    __asm__("v_lshlrev_b16_e64 %0, %1, 1" : "=v"(r) : "v"(k));
+    return r;
+#else
+    return (1u << k) & 0xFFFFu;
+#endif
+}
+
 // Levels lo .. lo+w-1 (lo + w <= 8).
 __host__ __device__ inline uint32_t taps_levels(uint32_t lo, uint32_t w) {
     return taps_below(lo + w) & ~taps_below(lo);
@@ -295,6 +318,65 @@ __host__ __device__ constexpr taps_width_table taps_make_widths() {
     return t;
 }
 
+// AllToAll shard fractions by tops mask: byte t of (lo, hi) is 2^(8 - w_t) for
+// every top t of the mask (w_t the width of the axis with top t, as in
+// taps_make_widths), 0 for the other levels; bytes 0-3 in lo, 4-7 in hi.
+struct taps_a2a_table {
+    uint32_t lo[256], hi[256];
+};
+
+__host__ __device__ constexpr taps_a2a_table taps_make_a2a() {
+    taps_a2a_table t{};
+    for (uint32_t m = 0; m < 256u; ++m) {
+        uint32_t lo = 0, bytes[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+        for (uint32_t l = 0; l < 8u; ++l)
+            if ((m >> l) & 1u) {
+                bytes[l] = 1u << (8u - (l + 1u - lo));
+                lo = l + 1u;
+            }
+        t.lo[m] = bytes[0] | (bytes[1] << 8) | (bytes[2] << 16) | (bytes[3] << 24);
+        t.hi[m] = bytes[4] | (bytes[5] << 8) | (bytes[6] << 16) | (bytes[7] << 24);
+    }
+    return t;
+}
+
+// Bit masks as byte vectors: byte t of (lo, hi) is bit t of the mask.
+struct taps_expand_table {
+    uint32_t lo[256], hi[256];
+};
+
+__host__ __device__ constexpr taps_expand_table taps_make_expand() {
+    taps_expand_table t{};
+    for (uint32_t m = 0; m < 256u; ++m) {
+        t.lo[m] = t.hi[m] = 0;
+        for (uint32_t l = 0; l < 4u; ++l) {
+            t.lo[m] |= ((m >> l) & 1u) << (8u * l);
+            t.hi[m] |= ((m >> (l + 4u)) & 1u) << (8u * l);
+        }
+    }
+    return t;
+}
+
+// Sum of the four byte products of a and b, plus c: one v_dot4_u32_u8.
+__host__ __device__ inline uint32_t taps_dot4(uint32_t a, uint32_t b, uint32_t c) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    return __builtin_amdgcn_udot4(a, b, c, false);
+#else
+    for (uint32_t k = 0; k < 32u; k += 8u) c += ((a >> k) & 0xFFu) * ((b >> k) & 0xFFu);
+    return c;
+#endif
+}
+
+struct taps_pair {
+    uint32_t lo, hi;
+};
+
+// Per tops mask, in LDS: the shard fractions of every axis (x, y: taps_make_a2a)
+// and of the axes inside one node (z, w: the same bytes below lam, 0 above).
+struct taps_a2a_row {
+    uint32_t all_lo, all_hi, in_lo, in_hi;
+};
+
 // Producer side of one table row (uniform across a wavefront).
 struct taps_row {
     uint32_t rank, n, lam, full;
@@ -310,7 +392,9 @@ struct taps_row {
     // to_rank[x] is the level mask x with level l moved to bit rank(l).
     uint32_t order;
     const uint8_t *to_rank;
-    const uint32_t *widths;   // taps_make_widths()
+    const uint32_t *widths;      // taps_make_widths()
+    const taps_a2a_row *a2a;     // by tops mask (taps_make_a2a, split at lam)
+    const taps_pair *expand;     // by mask (taps_make_expand)
 };
 
 // Consumer side of one table column.
@@ -465,12 +549,12 @@ __host__ __device__ inline void taps_cost(taps_fac &c, uint32_t top, const taps_
     const uint32_t m = a.lo < lam ? a.lo : lam;
     // groups of replicas inside a node share one transfer: the levels below m
     // that some dimension uses count
-    const uint32_t lct = taps_popc(taps_bfm(m, 0u) & ~unused);
+    const uint32_t lct = taps_popc(taps_low(m) & ~unused);
     c.vol += V;
     c.intra += V & in_node;
     c.inter += (V << lct) & ~in_node;
     // collectives (bits 0-7), inter-node ones (8-15), sum of their ct (16-31)
-    c.counts += 1u + ((0x100u + (taps_shl16(1u, lct) << 16)) & ~in_node);
+    c.counts += 1u + ((0x100u + (taps_bit16(lct) << 16)) & ~in_node);
 }
 
 // AllToAlls (Eq. 10, Eq. 14) of every axis whose top is in x, all issued at
@@ -481,18 +565,23 @@ __host__ __device__ inline void taps_cost(taps_fac &c, uint32_t top, const taps_
 // inside the node; the straddling axis (at most one) keeps its group
 // members inside a node out of the inter-node link.
 __host__ __device__ inline void taps_a2a_batch(taps_fac &c, uint32_t x, const taps_lv &L,
-                                               uint32_t lam, uint32_t e, uint32_t unused) {
+                                               uint32_t lam, uint32_t e, uint32_t unused,
+                                               const taps_a2a_row *a2a, const taps_pair *expand) {
     const uint32_t sh = e + 8u;
     const uint32_t low = taps_below(lam);
-    const uint32_t whole = 1u << sh;
-    uint32_t sum = 0, sum_in = 0;
-    for (uint32_t m = x & ~L.st; m; m &= m - 1u) {
-        const uint32_t t = taps_ctz(m);
-        const uint32_t V = whole - (whole >> ((L.wt >> (4u * t)) & 15u));   // (p - 1) / p of the shard, p = 2^width
-        sum += V;
-        sum_in += V & (uint32_t)((int32_t)(t - lam) >> 31);   // the group inside one node
-    }
-    const uint32_t n_in = taps_popc(x & low), n_out = taps_popc(x & ~low & ~L.st);
+    // Axis t keeps 2^-w_t of the shard: V_t = 2^sh - 2^(sh - w_t), and over the
+    // axes of m, sum V_t = |m| 2^sh - 2^e sum 2^(8 - w_t) (w_t <= 8 <= sh, so
+    // every term is whole).  The bytes 2^(8 - w_t) of the tops come from a
+    // table by tops mask, m's bits as bytes from another; two byte dot products
+    // sum them, all axes and the in-node ones (tops below lam).
+    const uint32_t m = x & ~L.st;
+    const taps_a2a_row W = a2a[L.tp];
+    const taps_pair X = expand[m];
+    const uint32_t f_all = taps_dot4(W.all_hi, X.hi, taps_dot4(W.all_lo, X.lo, 0u));
+    const uint32_t f_in = taps_dot4(W.in_hi, X.hi, taps_dot4(W.in_lo, X.lo, 0u));
+    const uint32_t n_in = taps_popc(m & low), n_out = taps_popc(m & ~low);
+    const uint32_t sum = ((n_in + n_out) << sh) - (f_all << e);
+    const uint32_t sum_in = (n_in << sh) - (f_in << e);
     const uint32_t lct = taps_popc(low & ~unused);
     c.vol += sum;
     c.intra += sum_in;
@@ -501,7 +590,7 @@ __host__ __device__ inline void taps_a2a_batch(taps_fac &c, uint32_t x, const ta
     if (x & L.st) {
         const uint32_t t = taps_ctz(L.st), lo = L.lo_s;
         const uint32_t w = t + 1u - lo, kap = lam - lo;
-        const uint32_t V = whole - (1u << (sh - w));
+        const uint32_t V = (1u << sh) - (1u << (sh - w));
         const uint32_t link = ((1u << w) - (1u << kap)) << (kap + sh - w);
         const uint32_t lcts = lo - taps_popc(unused & taps_below(lo));
         c.vol += V;
@@ -570,6 +659,8 @@ struct taps_two_class {
     uint32_t lam;
     const taps_keys *K;
     const taps_limit *lim;
+    const taps_a2a_row *a2a_rows;   // the row's AllToAll tables (taps_row)
+    const taps_pair *expand;
     __host__ __device__ void gather(fac &c, uint32_t top, const taps_ax &a, uint32_t e,
                                     uint32_t unused) const;
     __host__ __device__ void a2a(fac &c, uint32_t x, const taps_lv &L, uint32_t e,
@@ -591,7 +682,7 @@ __host__ __device__ inline void taps_two_class::gather(fac &c, uint32_t top, con
 
 __host__ __device__ inline void taps_two_class::a2a(fac &c, uint32_t x, const taps_lv &L,
                                                    uint32_t e, uint32_t unused) const {
-    taps_a2a_batch(c, x, L, lam, e, unused);
+    taps_a2a_batch(c, x, L, lam, e, unused, a2a_rows, expand);
 }
 
 __host__ __device__ inline bool taps_two_class::hopeless(const fac &c) const {
@@ -735,7 +826,7 @@ __host__ __device__ inline taps_run_t<typename Cm::fac> taps_alg1_t(const taps_r
 
 __host__ __device__ inline taps_run taps_alg1(const taps_row &P, const taps_col &Q,
                                               const taps_lv &L, const taps_start &b) {
-    const taps_two_class M{P.lam, nullptr, nullptr};
+    const taps_two_class M{P.lam, nullptr, nullptr, P.a2a, P.expand};
     return taps_alg1_t(P, Q, L, M, b);
 }
 
@@ -779,7 +870,7 @@ __host__ __device__ inline taps_run_t<typename Cm::fac> taps_rearrange_t(const t
         }
         const uint32_t top = taps_rank_level(P, taps_ctz(x) & 7u);
         x &= x - 1u;
-        const uint32_t b = taps_shl16(1u, top);
+        const uint32_t b = taps_bit16(top);
         const taps_ax a = taps_axis(L, top);
         M.gather(c, top, a, s.e, s.unused);
         const uint32_t freed_for = taps_blocked(P, L, b);   // the axis targeting that position
@@ -810,14 +901,14 @@ __host__ __device__ inline taps_run_t<typename Cm::fac> taps_rearrange_t(const t
 __host__ __device__ inline taps_run taps_rearrange(const taps_row &P, const taps_col &Q,
                                                    const taps_lv &L, const taps_limit &lim,
                                                    const taps_keys &K) {
-    const taps_two_class M{P.lam, &K, &lim};
+    const taps_two_class M{P.lam, &K, &lim, P.a2a, P.expand};
     return taps_rearrange_t(P, Q, L, M, taps_begin(P, L));
 }
 
 __host__ __device__ inline taps_run taps_rearrange(const taps_row &P, const taps_col &Q,
                                                    const taps_lv &L, const taps_limit &lim,
                                                    const taps_keys &K, const taps_start &b) {
-    const taps_two_class M{P.lam, &K, &lim};
+    const taps_two_class M{P.lam, &K, &lim, P.a2a, P.expand};
     return taps_rearrange_t(P, Q, L, M, b);
 }
 
@@ -862,7 +953,7 @@ __host__ __device__ inline taps_fac taps_remove(const taps_row &P, const taps_lv
         if (d == P.dstr) {   // uniform: the only dimension that can hold the straddler
             WS = taps_popc(G & S);
             if (WS) {
-                const uint32_t lctS = taps_popc(taps_bfm(lo_s, 0u) & ~unused);
+                const uint32_t lctS = taps_popc(taps_low(lo_s) & ~unused);
                 c.inter += taps_bfm(WS, sh + WA) << lctS;
                 c.counts += 0x101u + ((1u << lctS) << 16);
             }
@@ -1099,6 +1190,8 @@ __host__ __device__ inline void taps_make_row(taps_row &P, const taps_desc &D, u
         for (uint32_t t = 0; t < P.pw[d]; ++t) P.order |= (P.phi[d] - 1u - t) << (4u * k++);
     P.to_rank = nullptr;
     P.widths = nullptr;
+    P.a2a = nullptr;
+    P.expand = nullptr;
 }
 
 // to_rank table of a row: tab[x] = level mask x permuted into producer order.

@@ -34,6 +34,22 @@ __constant__ taps_completion_table kCompletions = taps_make_completions();
 // Widths of unified axes by their tops (taps_make_widths), copied to LDS by the
 // edge kernels.
 __constant__ taps_width_table kWidths = taps_make_widths();
+// AllToAll shard fractions by tops mask and masks as bytes (taps_make_a2a,
+// taps_make_expand), copied to LDS by the two-class edge kernels.
+__constant__ taps_a2a_table kA2a = taps_make_a2a();
+__constant__ taps_expand_table kExpand = taps_make_expand();
+
+// The per-workgroup LDS tables of the two-class AllToAll costing: the shard
+// fractions split at the node boundary lam (bytes below lam: in-node tops).
+__device__ inline void fill_a2a_tables(taps_a2a_row *a2a, taps_pair *expand, uint32_t lam) {
+    const uint32_t in_lo = lam >= 4u ? ~0u : (1u << (8u * lam)) - 1u;
+    const uint32_t in_hi = lam <= 4u ? 0u : lam >= 8u ? ~0u : (1u << (8u * (lam - 4u))) - 1u;
+    for (uint32_t x = threadIdx.x; x < 256u; x += blockDim.x) {
+        const uint32_t lo = kA2a.lo[x], hi = kA2a.hi[x];
+        a2a[x] = taps_a2a_row{lo, hi, lo & in_lo, hi & in_hi};
+        expand[x] = taps_pair{kExpand.lo[x], kExpand.hi[x]};
+    }
+}
 
 template <typename T>
 __device__ inline T *at_byte(T *base, uint32_t offset) {
@@ -325,6 +341,8 @@ __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_co
     uint32_t n_segs, const taps_desc *__restrict__ desc, taps_launch lp, taps_table out) {
     __shared__ uint8_t rank_tab[TAPS_ROWS_PER_BLOCK][256];
     __shared__ uint32_t width_tab[256];
+    __shared__ taps_a2a_row a2a_tab[256];
+    __shared__ taps_pair expand_tab[256];
     const uint32_t lane = threadIdx.x % TAPS_TILE_COLS;
     const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x / TAPS_TILE_COLS);
     const uint32_t r = blockIdx.x * TAPS_ROWS_PER_BLOCK + wave;
@@ -337,11 +355,14 @@ __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_co
     taps_row P;
     taps_make_row(P, Dp, E.paxes, E.rank, lp.n, lp.lam);
     taps_fill_rank_table(P, rank_tab[wave], lane, TAPS_TILE_COLS);
+    fill_a2a_tables(a2a_tab, expand_tab, lp.lam);
     for (uint32_t x = threadIdx.x; x < 256u; x += blockDim.x) width_tab[x] = kWidths.v[x];
     __syncthreads();
     if (!live) return;
     P.to_rank = rank_tab[wave];
     P.widths = width_tab;
+    P.a2a = a2a_tab;
+    P.expand = expand_tab;
     taps_keys K;
     K.b_inter_red = lp.b_inter_red;
     K.b_intra_red = lp.b_intra_red;
@@ -375,6 +396,8 @@ __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_co
     uint32_t n_segs, const taps_desc *__restrict__ desc, taps_launch lp, taps_sweep sw) {
     __shared__ uint8_t rank_tab[TAPS_ROWS_PER_BLOCK][256];
     __shared__ uint32_t width_tab[256];
+    __shared__ taps_a2a_row a2a_tab[256];
+    __shared__ taps_pair expand_tab[256];
     const uint32_t lane = threadIdx.x % TAPS_TILE_COLS;
     const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x / TAPS_TILE_COLS);
     const uint32_t r = blockIdx.x * TAPS_ROWS_PER_BLOCK + wave;
@@ -387,11 +410,14 @@ __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_co
     taps_row P;
     taps_make_row(P, Dp, E.paxes, E.rank, lp.n, lp.lam);
     taps_fill_rank_table(P, rank_tab[wave], lane, TAPS_TILE_COLS);
+    fill_a2a_tables(a2a_tab, expand_tab, lp.lam);
     for (uint32_t x = threadIdx.x; x < 256u; x += blockDim.x) width_tab[x] = kWidths.v[x];
     __syncthreads();
     if (!live) return;
     P.to_rank = rank_tab[wave];
     P.widths = width_tab;
+    P.a2a = a2a_tab;
+    P.expand = expand_tab;
     taps_keys any;
     any.b_inter_red = sw.b_inter_red[0];
     any.b_intra_red = sw.b_intra_red[0];
