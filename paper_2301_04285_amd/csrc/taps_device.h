@@ -420,15 +420,20 @@ struct taps_lv {
     uint32_t pt[TAPS_D_MAX_RANK];   // producer levels of d whose position the consumer splits too
 };
 
-// One candidate sequence, in factor units.
+// One candidate sequence, in factor units, and the sum of the inter-node
+// group counts (Algorithm 3's ct) of its collectives.  The number of
+// collectives and of inter-node ones is the same for every candidate (each
+// axis held off its target is moved once, by an AllToAll or an AllGather, and
+// its collective crosses nodes exactly when its top is at or above lam), so
+// it is counted once per entry (taps_collectives).
 struct taps_fac {
     uint32_t vol, intra, inter;
-    uint32_t counts;   // collectives | inter-node collectives << 8 | sum of ct << 16
+    uint32_t ct;
 };
 
 __host__ __device__ inline void taps_fac_zero(taps_fac &c) {
     c.vol = c.intra = c.inter = 0;
-    c.counts = 0;
+    c.ct = 0;
 }
 
 // All levels of the axes whose tops are in x.
@@ -553,8 +558,7 @@ __host__ __device__ inline void taps_cost(taps_fac &c, uint32_t top, const taps_
     c.vol += V;
     c.intra += V & in_node;
     c.inter += (V << lct) & ~in_node;
-    // collectives (bits 0-7), inter-node ones (8-15), sum of their ct (16-31)
-    c.counts += 1u + ((0x100u + (taps_bit16(lct) << 16)) & ~in_node);
+    c.ct += taps_bit16(lct) & ~in_node;
 }
 
 // AllToAlls (Eq. 10, Eq. 14) of every axis whose top is in x, all issued at
@@ -586,7 +590,7 @@ __host__ __device__ inline void taps_a2a_batch(taps_fac &c, uint32_t x, const ta
     c.vol += sum;
     c.intra += sum_in;
     c.inter += (sum - sum_in) << lct;
-    c.counts += n_in + (n_out << 8) + n_out + ((n_out << lct) << 16);
+    c.ct += n_out << lct;
     if (x & L.st) {
         const uint32_t t = taps_ctz(L.st), lo = L.lo_s;
         const uint32_t w = t + 1u - lo, kap = lam - lo;
@@ -595,7 +599,7 @@ __host__ __device__ inline void taps_a2a_batch(taps_fac &c, uint32_t x, const ta
         const uint32_t lcts = lo - taps_popc(unused & taps_below(lo));
         c.vol += V;
         c.inter += link << lcts;
-        c.counts += 0x101u + ((1u << lcts) << 16);
+        c.ct += 1u << lcts;
     }
 }
 
@@ -933,11 +937,11 @@ __host__ __device__ inline taps_fac taps_remove(const taps_row &P, const taps_lv
     const uint32_t lo_s = L.lo_s;
     const uint32_t S = L.st && P.dstr < TAPS_D_MAX_RANK ? taps_fill(L, L.st) : 0u;
     const uint32_t GA = G & ~low & ~S, GB = G & low & ~S;
-    const uint32_t TA = L.tp & GA, TAB = L.tp & (GA | GB);
+    const uint32_t TA = L.tp & GA;
     taps_fac c;
     c.vol = taps_bfm(taps_popc(G), P.e0 + 8u);
     c.intra = c.inter = 0;
-    c.counts = 0;
+    c.ct = 0;
     uint32_t sh = P.e0 + 8u;
     uint32_t unused = P.full & ~P.pru;
     // levels below lam some dimension still uses: the inter-node group count of
@@ -948,19 +952,19 @@ __host__ __device__ inline taps_fac taps_remove(const taps_row &P, const taps_lv
         if (d >= P.rank) break;
         const uint32_t pd = P.pr[d];
         const uint32_t WA = taps_popc(GA & pd), WB = taps_popc(GB & pd);
-        const uint32_t nAB = taps_popc(TAB & pd), nA = taps_popc(TA & pd);
+        const uint32_t nA = taps_popc(TA & pd);
         uint32_t WS = 0;
         if (d == P.dstr) {   // uniform: the only dimension that can hold the straddler
             WS = taps_popc(G & S);
             if (WS) {
                 const uint32_t lctS = taps_popc(taps_low(lo_s) & ~unused);
                 c.inter += taps_bfm(WS, sh + WA) << lctS;
-                c.counts += 0x101u + ((1u << lctS) << 16);
+                c.ct += 1u << lctS;
             }
         }
         c.intra += taps_bfm(WB, sh + WA + WS);
         c.inter += taps_bfm(WA, sh) << lctA;
-        c.counts += nAB + (nA << 8) + ((nA << lctA) << 16);
+        c.ct += nA << lctA;
         sh += WA + WB + WS;
         const uint32_t Gd = G & pd;
         unused |= Gd;
@@ -1001,8 +1005,17 @@ struct taps_pick {
     taps_fac best;
     uint32_t vmin;   // smallest volume among the candidates
     uint32_t cand;   // 0 Algorithm 1, 1 without AllToAll, 2 remove
+    uint32_t coll;   // taps_collectives
     bool ok;
 };
+
+// Collectives of every candidate of an entry (bits 0-7) and the inter-node
+// ones among them (bits 8-15): one per axis held off its target, inter-node
+// when its top is at or above lam.
+__host__ __device__ inline uint32_t taps_collectives(const taps_lv &L, uint32_t lam) {
+    const uint32_t x = L.src & ~L.home;
+    return taps_popc(x) | (taps_popc(x & ~taps_below(lam)) << 8);
+}
 
 struct taps_entry_out {
     double t;
@@ -1026,6 +1039,7 @@ __host__ __device__ inline taps_pick taps_edge_select(const taps_row &P, const t
     k.best = r0.c;
     k.cand = 0;
     k.vmin = r0.c.vol;
+    k.coll = taps_collectives(L, P.lam);
     k.ok = r0.ok;
     taps_limit lim;
     lim.on = K.narrow;
@@ -1063,6 +1077,7 @@ __host__ __device__ inline taps_pick taps_edge_select(const taps_row &P, const t
 struct taps_cands {
     taps_fac c[3];   // replace, rearrange, remove
     uint32_t vmin;   // smallest volume among them
+    uint32_t coll;   // taps_collectives
     bool has_rearrange;
     bool ok;
 };
@@ -1077,6 +1092,7 @@ __host__ __device__ inline taps_cands taps_edge_candidates(const taps_row &P, co
     k.c[0] = r0.c;
     k.ok = r0.ok;
     k.vmin = r0.c.vol;
+    k.coll = taps_collectives(L, P.lam);
     k.has_rearrange = r0.n_a2a != 0;   // without AllToAll the sequence would be the same
     taps_fac_zero(k.c[1]);
     if (k.has_rearrange) {
@@ -1130,6 +1146,7 @@ __host__ __device__ inline taps_pick taps_pick_for(const taps_cands &k, const ta
         }
     }
     p.vmin = k.vmin;
+    p.coll = k.coll;
     p.ok = k.ok;
     return p;
 }
@@ -1141,8 +1158,7 @@ __host__ __device__ inline taps_entry_out taps_entry_finish(const taps_pick &k,
     o.intra = taps_scale(S, k.best.intra);
     o.inter = taps_scale(S, k.best.inter);
     o.t = (double)k.best.intra * S.a_intra + (double)k.best.inter * S.a_inter;
-    const uint32_t n = k.best.counts;
-    o.meta = k.cand | ((n & 0xFFu) << 2) | (((n >> 8) & 0xFFu) << 7) | ((n >> 16) << 12);
+    o.meta = k.cand | ((k.coll & 0xFFu) << 2) | ((k.coll >> 8) << 7) | (k.best.ct << 12);
     o.ok = k.ok;
     return o;
 }
