@@ -478,9 +478,10 @@ __host__ __device__ inline void taps_unify(const taps_row &P, const taps_col &Q,
     // side (at most 7 cuts exist, so at most 8 passes)
     uint32_t C = (P.pcuts | Q.ccuts) & P.full & ~1u;
     for (uint32_t it = 0; it < TAPS_D_MAX_LEVELS; ++it) {
-        uint32_t acc = 0;
+        // dimension 0 unconditionally (its windows are 0 without one)
+        uint32_t acc = ((C & pwin[0]) << L.sh[0]) | ((C & cwin[0]) << back[0]);
 #pragma unroll
-        for (uint32_t d = 0; d < TAPS_D_MAX_RANK; ++d) {
+        for (uint32_t d = 1; d < TAPS_D_MAX_RANK; ++d) {
             if (d >= P.rank) break;
             acc = ((C & pwin[d]) << L.sh[d]) | acc;
             acc = ((C & cwin[d]) << back[d]) | acc;
@@ -509,9 +510,10 @@ __host__ __device__ inline void taps_unify(const taps_row &P, const taps_col &Q,
 // Consumer tops whose target position an axis in ats (producer tops) holds.
 __host__ __device__ inline uint32_t taps_blocked(const taps_row &P, const taps_lv &L,
                                                  uint32_t ats) {
-    uint32_t acc = 0;
+    // dimension 0 unconditionally: without one, pt[0] is 0 and so is its term
+    uint32_t acc = (ats & L.pt[0]) << L.sh[0];
 #pragma unroll
-    for (uint32_t d = 0; d < TAPS_D_MAX_RANK; ++d) {
+    for (uint32_t d = 1; d < TAPS_D_MAX_RANK; ++d) {
         if (d >= P.rank) break;
         acc = ((ats & L.pt[d]) << L.sh[d]) | acc;
     }
@@ -551,10 +553,9 @@ __host__ __device__ inline void taps_cost(taps_fac &c, uint32_t top, const taps_
     const uint32_t V = taps_bfm(a.w, e + 8u);
     // all ones when the whole group lies inside one node (top < lam)
     const uint32_t in_node = (uint32_t)((int32_t)(top - lam) >> 31);
-    const uint32_t m = a.lo < lam ? a.lo : lam;
-    // groups of replicas inside a node share one transfer: the levels below m
-    // that some dimension uses count
-    const uint32_t lct = taps_popc(taps_low(m) & ~unused);
+    // groups of replicas inside a node share one transfer: the levels below
+    // min(lo, lam) that some dimension uses count
+    const uint32_t lct = taps_popc(taps_low(a.lo) & taps_below(lam) & ~unused);
     c.vol += V;
     c.intra += V & in_node;
     c.inter += (V << lct) & ~in_node;
@@ -738,15 +739,21 @@ template <class Cm>
 __host__ __device__ inline void taps_alg1_settle(const taps_row &P, const taps_lv &L,
                                                  taps_state &s, typename Cm::fac &c,
                                                  uint32_t &n_a2a, const Cm &M, uint32_t sl) {
-    uint32_t moved = 0;
-    for (;;) {
-        const uint32_t mv = L.dst & s.ats & ~s.blk;
-        if (!mv) break;
-        moved |= mv;
-        s.blk &= ~taps_blocked(P, L, mv);
-        s.ats &= ~mv;
+    // The closure as a frontier: the held axes with a target whose target is
+    // free move first; each move frees the target its position blocked (each
+    // target is blocked by at most one held axis), and exactly the held axes
+    // with a target among those move next.
+    const uint32_t A = L.dst & s.ats;
+    uint32_t F = A & ~s.blk, moved = 0, freed = 0;
+    while (F) {
+        moved |= F;
+        const uint32_t fr = taps_blocked(P, L, F);
+        freed |= fr;
+        F = fr & A;
     }
     if (moved) {
+        s.ats &= ~moved;
+        s.blk &= ~freed;
         s.atd |= moved;
         n_a2a += taps_popc(moved);
         M.a2a(c, moved, L, s.e, s.unused);
