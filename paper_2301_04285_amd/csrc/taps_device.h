@@ -525,6 +525,25 @@ __host__ __device__ inline uint32_t taps_rank_level(const taps_row &P, uint32_t 
     return (P.order >> (4u * k)) & 15u;
 }
 
+// The level holding producer-order rank k mod 8 (k < 16): v_bfe_u32 reads
+// the low five bits of its offset, so 4k needs no reduction on the device.
+__host__ __device__ inline uint32_t taps_rank_level_mod8(const taps_row &P, uint32_t k) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    return __builtin_amdgcn_ubfe(P.order, 4u * k, 4u);
+#else
+    return (P.order >> (4u * (k & 7u))) & 15u;
+#endif
+}
+
+// All ones when bit k of x is set, else 0 (k < 32): one v_bfe_i32 on the device.
+__host__ __device__ inline uint32_t taps_bit_mask(uint32_t x, uint32_t k) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    return (uint32_t)__builtin_amdgcn_sbfe((int32_t)x, k, 1u);
+#else
+    return 0u - ((x >> k) & 1u);
+#endif
+}
+
 // The axis of x (non-empty, producer levels) at the lowest producer position.
 __host__ __device__ inline uint32_t taps_first_src(const taps_row &P, uint32_t x) {
     return taps_rank_level(P, taps_ctz(P.to_rank[x]));
@@ -544,13 +563,13 @@ __host__ __device__ inline taps_ax taps_axis(const taps_lv &L, uint32_t top) {
     return a;
 }
 
-// An AllGather (Eq. 9) of the axis with top level `top`, shard tbytes * 2^e,
-// with the inter-node group count of Algorithm 3: groups holding the same
-// data inside a node (replicas along levels no dimension uses) share one
-// inter-node transfer.
+// An AllGather (Eq. 9) of the axis with top level `top`, shard 2^sh factor
+// units (taps_state), with the inter-node group count of Algorithm 3: groups
+// holding the same data inside a node (replicas along levels no dimension
+// uses) share one inter-node transfer.
 __host__ __device__ inline void taps_cost(taps_fac &c, uint32_t top, const taps_ax &a,
-                                          uint32_t lam, uint32_t e, uint32_t unused) {
-    const uint32_t V = taps_bfm(a.w, e + 8u);
+                                          uint32_t lam, uint32_t sh, uint32_t unused) {
+    const uint32_t V = taps_bfm(a.w, sh);
     // all ones when the whole group lies inside one node (top < lam)
     const uint32_t in_node = (uint32_t)((int32_t)(top - lam) >> 31);
     // groups of replicas inside a node share one transfer: the levels below
@@ -563,20 +582,19 @@ __host__ __device__ inline void taps_cost(taps_fac &c, uint32_t top, const taps_
 }
 
 // AllToAlls (Eq. 10, Eq. 14) of every axis whose top is in x, all issued at
-// one state (shard tbytes * 2^e, free levels `unused`): an AllToAll changes
+// one state (shard 2^sh factor units, free levels `unused`): an AllToAll changes
 // neither, so the axes of one closure are costed together.  An axis wholly
 // above the node boundary sends V over the inter-node link with the group
 // count of Algorithm 3 that all such axes share; an in-node axis costs V
 // inside the node; the straddling axis (at most one) keeps its group
 // members inside a node out of the inter-node link.
 __host__ __device__ inline void taps_a2a_batch(taps_fac &c, uint32_t x, const taps_lv &L,
-                                               uint32_t lam, uint32_t e, uint32_t unused,
+                                               uint32_t lam, uint32_t sh, uint32_t unused,
                                                const taps_a2a_row *a2a, const taps_pair *expand) {
-    const uint32_t sh = e + 8u;
     const uint32_t low = taps_below(lam);
     // Axis t keeps 2^-w_t of the shard: V_t = 2^sh - 2^(sh - w_t), and over the
-    // axes of m, sum V_t = |m| 2^sh - 2^e sum 2^(8 - w_t) (w_t <= 8 <= sh, so
-    // every term is whole).  The bytes 2^(8 - w_t) of the tops come from a
+    // axes of m, sum V_t = |m| 2^sh - 2^(sh - 8) sum 2^(8 - w_t) (w_t <= 8 <= sh,
+    // so every term is whole).  The bytes 2^(8 - w_t) of the tops come from a
     // table by tops mask, m's bits as bytes from another; two byte dot products
     // sum them, all axes and the in-node ones (tops below lam).
     const uint32_t m = x & ~L.st;
@@ -585,6 +603,7 @@ __host__ __device__ inline void taps_a2a_batch(taps_fac &c, uint32_t x, const ta
     const uint32_t f_all = taps_dot4(W.all_hi, X.hi, taps_dot4(W.all_lo, X.lo, 0u));
     const uint32_t f_in = taps_dot4(W.in_hi, X.hi, taps_dot4(W.in_lo, X.lo, 0u));
     const uint32_t n_in = taps_popc(m & low), n_out = taps_popc(m & ~low);
+    const uint32_t e = sh - 8u;
     const uint32_t sum = ((n_in + n_out) << sh) - (f_all << e);
     const uint32_t sum_in = (n_in << sh) - (f_in << e);
     const uint32_t lct = taps_popc(low & ~unused);
@@ -666,28 +685,29 @@ struct taps_two_class {
     const taps_limit *lim;
     const taps_a2a_row *a2a_rows;   // the row's AllToAll tables (taps_row)
     const taps_pair *expand;
-    __host__ __device__ void gather(fac &c, uint32_t top, const taps_ax &a, uint32_t e,
+    __host__ __device__ void gather(fac &c, uint32_t top, const taps_ax &a, uint32_t sh,
                                     uint32_t unused) const;
-    __host__ __device__ void a2a(fac &c, uint32_t x, const taps_lv &L, uint32_t e,
+    __host__ __device__ void a2a(fac &c, uint32_t x, const taps_lv &L, uint32_t sh,
                                  uint32_t unused) const;
     __host__ __device__ bool hopeless(const fac &c) const;
 };
 
 // Running state of one sequence: axes held at their producer position (ats)
 // and at their target (atd), consumer tops whose target an at-src axis holds
-// (blk), free levels (unused) and the shard exponent e (shard = tbytes 2^e).
+// (blk), free levels (unused) and the shard as a shift, sh = e + 8 for a shard
+// of tbytes 2^e (taps_row's e0 at the start): 2^sh factor units.
 struct taps_state {
-    uint32_t ats, atd, blk, unused, e;
+    uint32_t ats, atd, blk, unused, sh;
 };
 
 __host__ __device__ inline void taps_two_class::gather(fac &c, uint32_t top, const taps_ax &a,
-                                                      uint32_t e, uint32_t unused) const {
-    taps_cost(c, top, a, lam, e, unused);
+                                                      uint32_t sh, uint32_t unused) const {
+    taps_cost(c, top, a, lam, sh, unused);
 }
 
 __host__ __device__ inline void taps_two_class::a2a(fac &c, uint32_t x, const taps_lv &L,
-                                                   uint32_t e, uint32_t unused) const {
-    taps_a2a_batch(c, x, L, lam, e, unused, a2a_rows, expand);
+                                                   uint32_t sh, uint32_t unused) const {
+    taps_a2a_batch(c, x, L, lam, sh, unused, a2a_rows, expand);
 }
 
 __host__ __device__ inline bool taps_two_class::hopeless(const fac &c) const {
@@ -698,10 +718,10 @@ template <class Cm>
 __host__ __device__ inline void taps_gather(const taps_lv &L, taps_state &s, typename Cm::fac &c,
                                             uint32_t top, const Cm &M) {
     const taps_ax a = taps_axis(L, top);
-    M.gather(c, top, a, s.e, s.unused);
+    M.gather(c, top, a, s.sh, s.unused);
     s.ats &= ~(1u << top);
     s.unused |= a.lv;
-    s.e += a.w;
+    s.sh += a.w;
 }
 
 // Every free target position whose axis no dimension uses is sliced.
@@ -711,7 +731,7 @@ __host__ __device__ inline uint32_t taps_slice(const taps_lv &L, taps_state &s) 
         const uint32_t lv = taps_fill(L, sl);
         s.atd |= sl;
         s.unused &= ~lv;
-        s.e -= taps_popc(lv);
+        s.sh -= taps_popc(lv);
     }
     return sl;
 }
@@ -756,7 +776,7 @@ __host__ __device__ inline void taps_alg1_settle(const taps_row &P, const taps_l
         s.blk &= ~freed;
         s.atd |= moved;
         n_a2a += taps_popc(moved);
-        M.a2a(c, moved, L, s.e, s.unused);
+        M.a2a(c, moved, L, s.sh, s.unused);
     }
     if (sl) taps_slice(L, s);
 }
@@ -783,7 +803,7 @@ __host__ __device__ inline taps_start taps_begin(const taps_row &P, const taps_l
     b.s.atd = L.home;
     b.s.blk = taps_blocked(P, L, b.s.ats);
     b.s.unused = P.full & ~P.pru;
-    b.s.e = P.e0;
+    b.s.sh = P.e0 + 8u;
     b.slice = taps_slice(L, b.s);
     return b;
 }
@@ -879,26 +899,26 @@ __host__ __device__ inline taps_run_t<typename Cm::fac> taps_rearrange_t(const t
             stopped = true;
             break;
         }
-        const uint32_t top = taps_rank_level(P, taps_ctz(x) & 7u);
+        const uint32_t top = taps_rank_level_mod8(P, taps_ctz(x));
         x &= x - 1u;
         const uint32_t b = taps_bit16(top);
         const taps_ax a = taps_axis(L, top);
-        M.gather(c, top, a, s.e, s.unused);
+        M.gather(c, top, a, s.sh, s.unused);
         const uint32_t freed_for = taps_blocked(P, L, b);   // the axis targeting that position
         s.ats &= ~b;
         s.blk &= ~freed_for;
         // sliced back into its own target if that is free (shard and free levels
-        // as before), else kept whole: all ones then
-        const uint32_t keep = (((L.dst & ~s.blk) >> top) & 1u) - 1u;
-        s.atd |= b & ~keep;
-        s.unused |= a.lv & keep;
-        s.e += a.w & keep;
+        // as before: all ones then), else kept whole
+        const uint32_t back = taps_bit_mask(L.dst & ~s.blk, top);
+        s.atd |= b & back;
+        s.unused |= a.lv & ~back;
+        s.sh += a.w & ~back;
         const uint32_t sf = freed_for & ~(s.ats | s.atd);   // sliced into the freed position
         if (sf) {
             const uint32_t lv = taps_fill(L, sf);
             s.atd |= sf;
             s.unused &= ~lv;
-            s.e -= taps_popc(lv);
+            s.sh -= taps_popc(lv);
         }
     }
     taps_run_t<typename Cm::fac> r;
@@ -1327,9 +1347,9 @@ struct taps_hier_model_t {
     bool lim_on;
 
     // AllGather (Eq. 9) of the axis with top level `top`.
-    __host__ __device__ void gather(fac &c, uint32_t top, const taps_ax &a, uint32_t e,
+    __host__ __device__ void gather(fac &c, uint32_t top, const taps_ax &a, uint32_t sh,
                                     uint32_t unused) const {
-        const uint32_t V = ((1u << a.w) - 1u) << (e + 8u);
+        const uint32_t V = ((1u << a.w) - 1u) << sh;
         const uint32_t cls = taps_nib(H->cls_of_top, top);
         const uint32_t lct = cls ? taps_hier_lct(a.lo, taps_nib(H->beta_of_top, top), unused) : 0u;
         c.vol += V;
@@ -1340,9 +1360,8 @@ struct taps_hier_model_t {
     // AllToAlls (Eq. 10, Eq. 14) of every axis whose top is in x, at one state:
     // k = 2^kap members of a group inside one block of the boundary beta, the
     // uplink carries k (p - k) / p of the shard per group.
-    __host__ __device__ void a2a(fac &c, uint32_t x, const taps_lv &L, uint32_t e,
+    __host__ __device__ void a2a(fac &c, uint32_t x, const taps_lv &L, uint32_t sh,
                                  uint32_t unused) const {
-        const uint32_t sh = e + 8u;
         for (uint32_t m = x; m; m &= m - 1u) {
             const uint32_t top = taps_ctz(m);
             const taps_ax a = taps_axis(L, top);
@@ -1377,13 +1396,13 @@ __host__ __device__ inline taps_fach taps_remove_h(const taps_row &P, const taps
                                                    const Mh &M) {
     taps_fach c;
     taps_fac_zero(c);
-    uint32_t e = P.e0, unused = P.full & ~P.pru;
+    uint32_t sh = P.e0 + 8u, unused = P.full & ~P.pru;
     for (uint32_t x = P.to_rank[L.src & ~L.home]; x; x &= x - 1u) {
         const uint32_t top = taps_rank_level(P, taps_ctz(x));
         const taps_ax a = taps_axis(L, top);
-        M.gather(c, top, a, e, unused);
+        M.gather(c, top, a, sh, unused);
         unused |= a.lv;
-        e += a.w;
+        sh += a.w;
     }
     return c;
 }
