@@ -387,6 +387,7 @@ struct taps_row {
     uint32_t pru;                   // levels the producer map uses
     uint32_t e0;                    // n - |pru|
     uint32_t dstr;                  // dimension whose run holds levels lam - 1 and lam (8: none)
+    uint32_t split;                 // bit d: the producer splits dimension d (pr[d] != 0)
     // Producer positions in order (dimension ascending, then bit ascending,
     // i.e. level descending): rank r holds level nibble r of `order`;
     // to_rank[x] is the level mask x with level l moved to bit rank(l).
@@ -456,6 +457,7 @@ __host__ __device__ inline void taps_unify(const taps_row &P, const taps_col &Q,
         L.sh[d] = back[d] = 8u;
         L.pt[d] = 0;
         if (d >= P.rank) continue;
+        cru |= Q.cr[d];
         // When either side leaves d whole its run mask is 0, and so is every
         // mask below: no case split on which sides split d.
         const uint32_t sh = Q.chi[d] + 8u - P.phi[d];   // 8 + dl, in 0 .. 16
@@ -466,7 +468,6 @@ __host__ __device__ inline void taps_unify(const taps_row &P, const taps_col &Q,
         const uint32_t pt = P.pr[d] & ((Q.cr[d] << (16u - sh)) >> 8);
         L.pt[d] = pt;
         tgt |= pt;
-        cru |= Q.cr[d];
         // the cut positions inside that part (all its levels but the lowest),
         // on each side
         pwin[d] = pt & (pt - 1u);
@@ -976,18 +977,17 @@ __host__ __device__ inline taps_fac taps_remove(const taps_row &P, const taps_lv
     uint32_t lctA = taps_popc(low & ~unused);
 #pragma unroll
     for (uint32_t d = 0; d < TAPS_D_MAX_RANK; ++d) {
-        if (d >= P.rank) break;
+        if (!((P.split >> d) & 1u)) continue;   // nothing of G in a dimension left whole
         const uint32_t pd = P.pr[d];
         const uint32_t WA = taps_popc(GA & pd), WB = taps_popc(GB & pd);
         const uint32_t nA = taps_popc(TA & pd);
         uint32_t WS = 0;
         if (d == P.dstr) {   // uniform: the only dimension that can hold the straddler
+            // without one (WS = 0) both terms are 0
             WS = taps_popc(G & S);
-            if (WS) {
-                const uint32_t lctS = taps_popc(taps_low(lo_s) & ~unused);
-                c.inter += taps_bfm(WS, sh + WA) << lctS;
-                c.ct += 1u << lctS;
-            }
+            const uint32_t lctS = taps_popc(taps_low(lo_s) & ~unused);
+            c.inter += taps_bfm(WS, sh + WA) << lctS;
+            c.ct += (WS < 1u ? WS : 1u) << lctS;
         }
         c.intra += taps_bfm(WB, sh + WA + WS);
         c.inter += taps_bfm(WA, sh) << lctA;
@@ -1218,6 +1218,9 @@ __host__ __device__ inline void taps_make_row(taps_row &P, const taps_desc &D, u
         used += w;
     }
     P.e0 = n - used;
+    P.split = 0;
+#pragma unroll
+    for (uint32_t d = 0; d < TAPS_D_MAX_RANK; ++d) P.split |= (P.pr[d] ? 1u : 0u) << d;
     P.dstr = TAPS_D_MAX_RANK;
     if (lam >= 1u && lam < n) {
         const uint32_t two = 3u << (lam - 1u);
