@@ -799,6 +799,8 @@ taps_status check_topology(const taps_topology *t, taps_hier *H, taps_cluster *c
         }
         H->cls_of_top |= cls << (4u * l);
         H->beta_of_top |= beta << (4u * l);
+        H->levels_of_cls[cls] |= 1u << l;
+        H->beta_of_cls[cls] = beta;
     }
     cl->nodes = (uint32_t)(N / t->domain[0]);
     cl->devices_per_node = t->domain[0];

@@ -396,6 +396,9 @@ struct taps_row {
     const uint32_t *widths;      // taps_make_widths()
     const taps_a2a_row *a2a;     // by tops mask (taps_make_a2a, split at lam)
     const taps_pair *expand;     // by mask (taps_make_expand)
+    // by tops mask, TAPS_D_MAX_CLASSES entries each: taps_make_a2a's bytes of
+    // the tops in link class c (hierarchies of link classes)
+    const taps_pair *a2a_cls;
 };
 
 // Consumer side of one table column.
@@ -1238,6 +1241,7 @@ __host__ __device__ inline void taps_make_row(taps_row &P, const taps_desc &D, u
     P.widths = nullptr;
     P.a2a = nullptr;
     P.expand = nullptr;
+    P.a2a_cls = nullptr;
 }
 
 // to_rank table of a row: tab[x] = level mask x permuted into producer order.
@@ -1299,18 +1303,23 @@ struct taps_hier {
     double inv_n_bw_a2a;     // 1 / (N bw_a2a)
     uint32_t a2a_own;        // 1: in-block AllToAlls go to xa at their own bandwidth
     uint32_t pad2;
+    uint32_t levels_of_cls[TAPS_D_MAX_CLASSES];   // bit l: cls_of_top's nibble l is c
+    uint32_t beta_of_cls[TAPS_D_MAX_CLASSES];     // the boundary of class c (0 for class 0)
 };
 
 // One candidate in factor units, per link class (x0: inside the innermost block).
+// ct: the sum of the inter-block group counts of its collectives (the number
+// of collectives and of inter-block ones is the same for every candidate, as
+// for taps_fac: taps_collectives_h).
 struct taps_fach {
     uint32_t vol, x0, x1, x2, x3;
-    uint32_t xa;       // in-block AllToAll volume priced at its own bandwidth
-    uint32_t counts;   // collectives | inter-block collectives << 8 | sum of ct << 16
+    uint32_t xa;   // in-block AllToAll volume priced at its own bandwidth
+    uint32_t ct;
 };
 
 __host__ __device__ inline void taps_fac_zero(taps_fach &c) {
     c.vol = c.x0 = c.x1 = c.x2 = c.x3 = c.xa = 0;
-    c.counts = 0;
+    c.ct = 0;
 }
 
 // x_cls += v (selects, no indexed register arrays).  C: the hierarchy's
@@ -1348,6 +1357,8 @@ struct taps_hier_model_t {
     uint64_t lim_key;   // a later candidate stops once its key and volume reach these
     uint32_t lim_vol;
     bool lim_on;
+    const taps_pair *a2a_cls;   // the row's AllToAll tables by class (taps_row)
+    const taps_pair *expand;
 
     // AllGather (Eq. 9) of the axis with top level `top`.
     __host__ __device__ void gather(fac &c, uint32_t top, const taps_ax &a, uint32_t sh,
@@ -1357,32 +1368,64 @@ struct taps_hier_model_t {
         const uint32_t lct = cls ? taps_hier_lct(a.lo, taps_nib(H->beta_of_top, top), unused) : 0u;
         c.vol += V;
         taps_fach_add<C>(c, cls, V << lct);
-        c.counts += cls ? 0x101u + ((1u << lct) << 16) : 1u;
+        c.ct += cls ? 1u << lct : 0u;
     }
 
     // AllToAlls (Eq. 10, Eq. 14) of every axis whose top is in x, at one state:
     // k = 2^kap members of a group inside one block of the boundary beta, the
     // uplink carries k (p - k) / p of the shard per group.
+    //
+    // An axis whose levels all lie at or above its class's boundary (kap = 0)
+    // sends its whole V = 2^sh - 2^(sh - w) over its class's link, with the
+    // group count the free levels below the boundary give every such axis of
+    // the class: per class, sum V = n 2^sh - 2^(sh - 8) sum 2^(8 - w), the last
+    // sum one byte dot product per half against a table of the row's tops
+    // split by class (as taps_a2a_batch).  Only the lowest axis of a class can
+    // reach below its boundary (when the level under the boundary is not a
+    // top); those axes (at most one per class) are costed one by one.
     __host__ __device__ void a2a(fac &c, uint32_t x, const taps_lv &L, uint32_t sh,
                                  uint32_t unused) const {
-        for (uint32_t m = x; m; m &= m - 1u) {
-            const uint32_t top = taps_ctz(m);
+        uint32_t cross = 0;
+#pragma unroll
+        for (uint32_t k = 1; k < C; ++k) {
+            const uint32_t b = H->beta_of_cls[k];   // uniform
+            if (b == 0) continue;                   // nothing reaches below level 0
+            const uint32_t low_top = L.tp & H->levels_of_cls[k];
+            cross |= (low_top & (0u - low_top)) & (((L.tp >> (b - 1u)) & 1u) - 1u);
+        }
+        const uint32_t m = x & ~cross;
+        const taps_pair X = expand[m];
+        const taps_pair *W = a2a_cls + (size_t)L.tp * TAPS_D_MAX_CLASSES;
+        const uint32_t e = sh - 8u;
+#pragma unroll
+        for (uint32_t k = 0; k < C; ++k) {
+            const uint32_t mk = m & H->levels_of_cls[k];
+            const uint32_t nk = taps_popc(mk);
+            const uint32_t f = taps_dot4(W[k].hi, X.hi, taps_dot4(W[k].lo, X.lo, 0u));
+            const uint32_t sum = (nk << sh) - (f << e);
+            c.vol += sum;
+            if (k == 0) {
+                c.x0 += H->a2a_own ? 0u : sum;
+                c.xa += H->a2a_own ? sum : 0u;
+                continue;
+            }
+            const uint32_t b = H->beta_of_cls[k];
+            const uint32_t lct = b - taps_popc(unused & taps_below(b));
+            taps_fach_add<C>(c, k, sum << lct);
+            c.ct += nk << lct;
+        }
+        for (uint32_t r = x & cross; r; r &= r - 1u) {
+            const uint32_t top = taps_ctz(r);
             const taps_ax a = taps_axis(L, top);
             const uint32_t V = (1u << sh) - (1u << (sh - a.w));
             const uint32_t cls = taps_nib(H->cls_of_top, top);
-            c.vol += V;
-            if (!cls) {
-                c.x0 += H->a2a_own ? 0u : V;
-                c.xa += H->a2a_own ? V : 0u;
-                c.counts += 1u;
-                continue;
-            }
             const uint32_t beta = taps_nib(H->beta_of_top, top);
-            const uint32_t kap = beta > a.lo ? beta - a.lo : 0u;
+            const uint32_t kap = beta - a.lo;   // lo < beta for a crossing axis
             const uint32_t link = ((1u << a.w) - (1u << kap)) << (kap + sh - a.w);
             const uint32_t lct = taps_hier_lct(a.lo, beta, unused);
+            c.vol += V;
             taps_fach_add<C>(c, cls, link << lct);
-            c.counts += 0x101u + ((1u << lct) << 16);
+            c.ct += 1u << lct;
         }
     }
 
@@ -1413,8 +1456,17 @@ __host__ __device__ inline taps_fach taps_remove_h(const taps_row &P, const taps
 struct taps_pickh {
     taps_fach best;
     uint32_t vmin, cand;
+    uint32_t coll;   // taps_collectives_h
     bool ok;
 };
+
+// Collectives of every candidate of an entry (bits 0-7) and the inter-block
+// ones among them (bits 8-15): one per axis held off its target, inter-block
+// when its top is in a class above 0.
+__host__ __device__ inline uint32_t taps_collectives_h(const taps_lv &L, const taps_hier &H) {
+    const uint32_t x = L.src & ~L.home;
+    return taps_popc(x) | (taps_popc(x & ~H.levels_of_cls[0]) << 8);
+}
 
 // The cheapest of Algorithm 1, the same without AllToAll, and "remove" under
 // the link classes of H (ties to the lower index); vmin the smallest volume.
@@ -1423,13 +1475,14 @@ __host__ __device__ inline taps_pickh taps_edge_select_h(const taps_row &P, cons
                                                          const taps_hier &H) {
     taps_lv L;
     taps_unify(P, Q, L);
-    taps_hier_model_t<C> M{&H, 0, 0, false};
+    taps_hier_model_t<C> M{&H, 0, 0, false, P.a2a_cls, P.expand};
     const taps_start b = taps_begin(P, L);
     const taps_run_t<taps_fach> r0 = taps_alg1_t(P, Q, L, M, b);
     taps_pickh k;
     k.best = r0.c;
     k.cand = 0;
     k.vmin = r0.c.vol;
+    k.coll = taps_collectives_h(L, H);
     k.ok = r0.ok;
     uint64_t best_key = taps_fach_key<C>(r0.c, H);
     if (r0.n_a2a) {   // without AllToAll the sequence would be the same
@@ -1468,8 +1521,7 @@ __host__ __device__ inline taps_entry_out taps_entry_finish_h(const taps_pickh &
     o.t = (double)k.best.x0 * (unit * H.inv_n_bw[0]) + (double)k.best.x1 * (unit * H.inv_n_bw[1]) +
           (double)k.best.x2 * (unit * H.inv_n_bw[2]) + (double)k.best.x3 * (unit * H.inv_n_bw[3]) +
           (double)k.best.xa * (unit * H.inv_n_bw_a2a);
-    const uint32_t n = k.best.counts;
-    o.meta = k.cand | ((n & 0xFFu) << 2) | (((n >> 8) & 0xFFu) << 7) | ((n >> 16) << 12);
+    o.meta = k.cand | ((k.coll & 0xFFu) << 2) | ((k.coll >> 8) << 7) | (k.best.ct << 12);
     o.ok = k.ok;
     return o;
 }

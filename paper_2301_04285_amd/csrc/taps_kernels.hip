@@ -51,6 +51,27 @@ __device__ inline void fill_a2a_tables(taps_a2a_row *a2a, taps_pair *expand, uin
     }
 }
 
+// The per-workgroup LDS tables of the link-class AllToAll costing: per tops
+// mask, the shard-fraction bytes of the tops in each class (a level's byte
+// kept where the level's class is c).
+__device__ inline void fill_a2a_class_tables(taps_pair *a2a_cls, taps_pair *expand,
+                                             const taps_hier &H) {
+    uint32_t lo_mask[TAPS_D_MAX_CLASSES], hi_mask[TAPS_D_MAX_CLASSES];
+#pragma unroll
+    for (uint32_t c = 0; c < TAPS_D_MAX_CLASSES; ++c) {
+        const uint32_t m = c < H.n_classes ? H.levels_of_cls[c] & 0xFFu : 0u;
+        lo_mask[c] = kExpand.lo[m] * 0xFFu;
+        hi_mask[c] = kExpand.hi[m] * 0xFFu;
+    }
+    for (uint32_t x = threadIdx.x; x < 256u; x += blockDim.x) {
+        const uint32_t lo = kA2a.lo[x], hi = kA2a.hi[x];
+#pragma unroll
+        for (uint32_t c = 0; c < TAPS_D_MAX_CLASSES; ++c)
+            a2a_cls[x * TAPS_D_MAX_CLASSES + c] = taps_pair{lo & lo_mask[c], hi & hi_mask[c]};
+        expand[x] = taps_pair{kExpand.lo[x], kExpand.hi[x]};
+    }
+}
+
 template <typename T>
 __device__ inline T *at_byte(T *base, uint32_t offset) {
     return (T *)((char *)base + offset);
@@ -460,6 +481,8 @@ __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_co
     taps_table out) {
     __shared__ uint8_t rank_tab[TAPS_ROWS_PER_BLOCK][256];
     __shared__ uint32_t width_tab[256];
+    __shared__ taps_pair a2a_cls_tab[256 * TAPS_D_MAX_CLASSES];
+    __shared__ taps_pair expand_tab[256];
     const uint32_t lane = threadIdx.x % TAPS_TILE_COLS;
     const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x / TAPS_TILE_COLS);
     const uint32_t r = blockIdx.x * TAPS_ROWS_PER_BLOCK + wave;
@@ -473,10 +496,13 @@ __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_co
     taps_make_row(P, Dp, E.paxes, E.rank, lp.n, lp.lam);
     taps_fill_rank_table(P, rank_tab[wave], lane, TAPS_TILE_COLS);
     for (uint32_t x = threadIdx.x; x < 256u; x += blockDim.x) width_tab[x] = kWidths.v[x];
+    fill_a2a_class_tables(a2a_cls_tab, expand_tab, H);
     __syncthreads();
     if (!live) return;
     P.to_rank = rank_tab[wave];
     P.widths = width_tab;
+    P.a2a_cls = a2a_cls_tab;
+    P.expand = expand_tab;
     const uint64_t row_out = E.out_offset + (uint64_t)i * E.nd;
     const taps_desc *col = desc + E.dst_base;
     const uint32_t c0 = ref.first_col;
