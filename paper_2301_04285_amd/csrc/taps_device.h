@@ -403,7 +403,9 @@ struct taps_row {
 
 // Consumer side of one table column.
 struct taps_col {
-    uint32_t cr[TAPS_D_MAX_RANK], chi[TAPS_D_MAX_RANK], cw[TAPS_D_MAX_RANK];
+    uint32_t cr[TAPS_D_MAX_RANK];    // level run of dimension d (0 if whole)
+    uint32_t clo[TAPS_D_MAX_RANK];   // its lowest level
+    uint32_t cw[TAPS_D_MAX_RANK];    // its width
     uint32_t ccuts;
 };
 
@@ -463,7 +465,8 @@ __host__ __device__ inline void taps_unify(const taps_row &P, const taps_col &Q,
         cru |= Q.cr[d];
         // When either side leaves d whole its run mask is 0, and so is every
         // mask below: no case split on which sides split d.
-        const uint32_t sh = Q.chi[d] + 8u - P.phi[d];   // 8 + dl, in 0 .. 16
+        // 8 + dl, in 0 .. 16 (dl: consumer top + 1 minus the producer's)
+        const uint32_t sh = Q.clo[d] + Q.cw[d] + (8u - P.phi[d]);
         L.sh[d] = sh;
         back[d] = 16u - sh;
         // producer levels whose consumer level (l + dl) the consumer splits in
@@ -476,7 +479,7 @@ __host__ __device__ inline void taps_unify(const taps_row &P, const taps_col &Q,
         pwin[d] = pt & (pt - 1u);
         cwin[d] = (pwin[d] << sh) >> 8;
         // at the same position on both sides when dl = 0
-        home |= pt & (uint32_t)((int32_t)((sh ^ 8u) - 1u) >> 31);
+        home |= sh == 8u ? pt : 0u;
     }
     // least fixpoint: each pass moves the cuts inside every window to the other
     // side (at most 7 cuts exist, so at most 8 passes)
@@ -1264,16 +1267,18 @@ __host__ __device__ inline void taps_fill_rank_table(const taps_row &P, uint8_t 
     }
 }
 
+// Dimensions d >= rank are left as they come (nothing reads them).
 __host__ __device__ inline void taps_make_col(taps_col &Q, const taps_desc &D, uint32_t axes,
                                               uint32_t rank) {
+    (void)rank;
     Q.ccuts = D.cuts;
 #pragma unroll
     for (uint32_t d = 0; d < TAPS_D_MAX_RANK; ++d) {
         const uint32_t a = taps_nib(axes, d);
-        const uint32_t lo = taps_nib(D.lo, a), w = d < rank ? taps_nib(D.width, a) : 0u;
+        const uint32_t lo = taps_nib(D.lo, a), w = taps_nib(D.width, a);
         Q.cw[d] = w;
-        Q.chi[d] = lo + w;
-        Q.cr[d] = taps_levels(lo, w);
+        Q.clo[d] = lo;
+        Q.cr[d] = taps_bfm(w, lo);
     }
 }
 
