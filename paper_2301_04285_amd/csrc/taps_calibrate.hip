@@ -2,8 +2,9 @@
 // support for the benchmark's roofline, not part of the cost-table path).
 //
 // Each kernel runs 8 independent dependency chains of one 32-bit integer
-// VALU instruction per thread, 8 wavefronts per SIMD (the edge kernel's
-// occupancy), so the issue rate, not the latency, bounds it.  The instruction
+// VALU instruction per thread, 8 wavefronts per SIMD (the most a SIMD holds;
+// the edge kernel runs 7, as many as its scalar registers allow, and held to
+// 8 it ran no faster), so the issue rate, not the latency, bounds it.  The instruction
 // count per launch is exact (inline assembly, 16 instructions per block); the
 // caller divides it by the measured time.
 //   kind 0: v_add_u32 / v_xor_b32 with vector operands -- on gfx950 the class
