@@ -52,7 +52,8 @@ BYTES_PER_ENTRY = 36
 # sources they were taken with
 COUNTERS = os.path.join(ROOT, "profiles", "edge_costs_gpt96L_16x8_counters.md")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2301_04285_amd", "csrc", f)
-                  for f in ("taps_device.h", "taps_kernels.hip", "taps_internal.h")]
+                  for f in ("taps_device.h", "taps_kernels.hip", "taps_internal.h")] + \
+                 [os.path.join(ROOT, "paper_2301_04285_amd", "build.py")]   # the compile flags
 
 
 def log(msg: str) -> None:
