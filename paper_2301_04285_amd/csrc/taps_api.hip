@@ -600,7 +600,7 @@ uint64_t plan_segments(const taps_graph *graph, const uint64_t *op_offsets, bool
 
 // The segments of a launch: one table, long segments (remainders last) when
 // there are enough of them to fill the GPU many times over, else short ones;
-// several tables (the bandwidth sweep), short ones in row order.
+// several tables (the bandwidth sweep), one tile each in row order.
 std::atomic<uint64_t> g_long_segs_min{TAPS_LONG_SEGS_MIN};
 
 uint64_t plan_launch(const taps_graph *graph, const uint64_t *op_offsets, bool reverse,
@@ -611,7 +611,8 @@ uint64_t plan_launch(const taps_graph *graph, const uint64_t *op_offsets, bool r
                                          TAPS_TILE_COLS * TAPS_SEG_TILES_LONG, true, groups);
         if (n >= g_long_segs_min.load(std::memory_order_relaxed)) return n;
     }
-    return plan_segments(graph, op_offsets, reverse, rep, TAPS_TILE_COLS * TAPS_SEG_TILES_SHORT,
+    return plan_segments(graph, op_offsets, reverse, rep,
+                         TAPS_TILE_COLS * (one_table ? TAPS_SEG_TILES_SHORT : TAPS_SEG_TILES_SWEEP),
                          one_table, groups);
 }
 

@@ -50,12 +50,15 @@ struct taps_copy_task {
 // remainders keeps the longer segments from stretching the end of the launch
 // (1, 2, 4, 8, 16 and 32 tiles measured).  Launches with few segments use
 // TAPS_SEG_TILES_SHORT.  The bandwidth sweep, bound by its four sets of
-// stores per entry, keeps short segments in row order: a row's remainder
-// written long after its full-length segments leaves the 128-byte lines they
-// share to reach HBM in two partial writes.
+// stores per entry, keeps segments of TAPS_SEG_TILES_SWEEP tiles in row order:
+// a row's remainder written long after its full-length segments leaves the
+// 128-byte lines they share to reach HBM in two partial writes, and one tile
+// per wavefront stores fastest (5.48 ms with two tiles, 5.17-5.26 with one, on
+// the 96-layer GPT at four points).
 #define TAPS_TILE_COLS 64
 #define TAPS_SEG_TILES_LONG 8
 #define TAPS_SEG_TILES_SHORT 2
+#define TAPS_SEG_TILES_SWEEP 1
 #define TAPS_LONG_SEGS_MIN 32768   // long segments only when there are at least this many
 #define TAPS_ROWS_PER_BLOCK 2
 
