@@ -424,10 +424,10 @@ taps_status taps_set_edge_kernel_events(void *before, void *after);
  * taps_edge_costs_topology, taps_build_tables) whose tables hold at least
  * `min_segments` row segments of eight 64-entry tiles run those long segments
  * (each edge's full-length segments first, the rows' remainders last, longest
- * first); smaller launches run segments of at most two tiles in row order, and
- * the bandwidth sweep segments of one tile in row order.  Every shape writes the
- * same tables; the setting only moves the size at which a single-table launch
- * changes shape (default 32768; 0 or 1: every launch with at least one segment
+ * first); smaller launches run segments of at most two tiles in row order (the
+ * bandwidth sweep runs aligned 64-entry windows of its tables instead).  Every
+ * shape writes the same tables; the setting only moves the size at which a
+ * single-table launch changes shape (default 32768; 0 or 1: every launch with at least one segment
  * runs long ones).  Process-wide, read when a
  * launch is planned; returns the previous value.  Never fails. */
 uint64_t taps_set_long_segments_min(uint64_t min_segments);

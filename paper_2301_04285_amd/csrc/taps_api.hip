@@ -598,9 +598,9 @@ uint64_t plan_segments(const taps_graph *graph, const uint64_t *op_offsets, bool
     return start;
 }
 
-// The segments of a launch: one table, long segments (remainders last) when
-// there are enough of them to fill the GPU many times over, else short ones;
-// several tables (the bandwidth sweep), one tile each in row order.
+// The segments of a one-table launch: long segments (remainders last) when
+// there are enough of them to fill the GPU many times over, else short ones in
+// row order.
 std::atomic<uint64_t> g_long_segs_min{TAPS_LONG_SEGS_MIN};
 
 uint64_t plan_launch(const taps_graph *graph, const uint64_t *op_offsets, bool reverse,
@@ -611,8 +611,7 @@ uint64_t plan_launch(const taps_graph *graph, const uint64_t *op_offsets, bool r
                                          TAPS_TILE_COLS * TAPS_SEG_TILES_LONG, true, groups);
         if (n >= g_long_segs_min.load(std::memory_order_relaxed)) return n;
     }
-    return plan_segments(graph, op_offsets, reverse, rep,
-                         TAPS_TILE_COLS * (one_table ? TAPS_SEG_TILES_SHORT : TAPS_SEG_TILES_SWEEP),
+    return plan_segments(graph, op_offsets, reverse, rep, TAPS_TILE_COLS * TAPS_SEG_TILES_SHORT,
                          one_table, groups);
 }
 
@@ -676,8 +675,10 @@ taps_status edge_costs(const taps_graph *graph, const taps_cluster *clusters, ui
     if (share && (st = share_edges(graph, op_offsets, strategies, stream, rep)) != TAPS_OK)
         return st;
     // row segments of every computed table (shared tables: the first of each group)
+    // (the bandwidth sweep runs over aligned windows of the tables instead)
     std::vector<taps_seg_group> groups;
-    const uint64_t n_segs = plan_launch(graph, op_offsets, reverse, rep, n_points == 1, groups);
+    const uint64_t n_segs =
+        n_points == 1 ? plan_launch(graph, op_offsets, reverse, rep, true, groups) : 0;
     // shared tables: every chunk of a computed table is stored into each table sharing it
     std::vector<uint64_t> dst_list;
     std::vector<taps_copy_task> copies;
@@ -700,6 +701,12 @@ taps_status edge_costs(const taps_graph *graph, const taps_cluster *clusters, ui
     if ((st = sc.alloc((void **)&d_desc, sizeof(taps_desc) * total)) != TAPS_OK) return st;
     if ((st = sc.alloc((void **)&d_params, sizeof(taps_edge_params) * n_edges)) != TAPS_OK) return st;
     if ((st = sc.alloc((void **)&d_segs, sizeof(taps_row_ref) * n_segs)) != TAPS_OK) return st;
+    // the bandwidth sweep runs over aligned 64-entry windows: each window's edge
+    uint32_t *d_win = nullptr;
+    const uint64_t n_windows = (eoff[n_edges] + TAPS_TILE_COLS - 1) / TAPS_TILE_COLS;
+    if (n_points > 1 && !hier &&
+        (st = sc.alloc((void **)&d_win, sizeof(uint32_t) * n_windows)) != TAPS_OK)
+        return st;
     hipError_t err = taps_launch_describe(strategies, total, d_desc, stream);
     if (err == hipSuccess) {
         const taps_plan_args pa{at<taps_op>(dev, ch[0]), at<taps_edge>(dev, ch[1]),
@@ -730,8 +737,9 @@ taps_status edge_costs(const taps_graph *graph, const taps_cluster *clusters, ui
             sw.inv_n_binter[k] = lps[k].inv_n_binter;
             sw.out[k] = outs[k];
         }
-        err = taps_launch_edge_costs_sweep(d_params, d_segs, n_segs, d_desc, lp,
-                                           max_edge_rank(graph), sw, stream);
+        err = taps_launch_edge_costs_sweep_win(d_params, n_edges, at<uint64_t>(dev, ch[3]),
+                                               eoff[n_edges], d_win, d_desc, lp,
+                                               max_edge_rank(graph), sw, stream);
     }
     for (uint32_t k = 0; k < n_points && err == hipSuccess; ++k)
         err = taps_launch_copy_tables(at<taps_copy_task>(dev, ch[5]), (uint32_t)copies.size(),

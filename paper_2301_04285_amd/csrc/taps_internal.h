@@ -50,15 +50,11 @@ struct taps_copy_task {
 // remainders keeps the longer segments from stretching the end of the launch
 // (1, 2, 4, 8, 16 and 32 tiles measured).  Launches with few segments use
 // TAPS_SEG_TILES_SHORT.  The bandwidth sweep, bound by its four sets of
-// stores per entry, keeps segments of TAPS_SEG_TILES_SWEEP tiles in row order:
-// a row's remainder written long after its full-length segments leaves the
-// 128-byte lines they share to reach HBM in two partial writes, and one tile
-// per wavefront stores fastest (5.48 ms with two tiles, 5.17-5.26 with one, on
-// the 96-layer GPT at four points).
+// stores per entry, does not use segments: it runs one wavefront per aligned
+// 64-entry window of the tables (k_edge_costs_sweep_win).
 #define TAPS_TILE_COLS 64
 #define TAPS_SEG_TILES_LONG 8
 #define TAPS_SEG_TILES_SHORT 2
-#define TAPS_SEG_TILES_SWEEP 1
 #define TAPS_LONG_SEGS_MIN 32768   // long segments only when there are at least this many
 #define TAPS_ROWS_PER_BLOCK 2
 
@@ -123,10 +119,14 @@ struct taps_sweep {
     double inv_n_binter[TAPS_MAX_SWEEP];
     taps_table out[TAPS_MAX_SWEEP];
 };
-hipError_t taps_launch_edge_costs_sweep(const taps_edge_params *params, const taps_row_ref *rows,
-                                        uint64_t n_rows, const taps_desc *desc,
-                                        const taps_launch &lp, uint32_t max_rank,
-                                        const taps_sweep &sw, hipStream_t stream);
+// The sweep over aligned 64-entry windows of the concatenated tables (eoff:
+// device, n_edges + 1 entry offsets; win_edge: device scratch of one uint32
+// per window, ceil(total / 64)).
+hipError_t taps_launch_edge_costs_sweep_win(const taps_edge_params *params, uint32_t n_edges,
+                                            const uint64_t *eoff, uint64_t total,
+                                            uint32_t *win_edge, const taps_desc *desc,
+                                            const taps_launch &lp, uint32_t max_rank,
+                                            const taps_sweep &sw, hipStream_t stream);
 // One workgroup of k_build_strategies: candidate ranks [first, first +
 // TAPS_BUILD_CHUNK) of operator `op`, of which `count` pass the filter; they
 // are strategies base, base + 1, ... in rank order.
