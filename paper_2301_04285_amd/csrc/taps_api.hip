@@ -703,7 +703,8 @@ taps_status edge_costs(const taps_graph *graph, const taps_cluster *clusters, ui
     if ((st = sc.alloc((void **)&d_segs, sizeof(taps_row_ref) * n_segs)) != TAPS_OK) return st;
     // the bandwidth sweep runs over aligned 64-entry windows: each window's edge
     uint32_t *d_win = nullptr;
-    const uint64_t n_windows = (eoff[n_edges] + TAPS_TILE_COLS - 1) / TAPS_TILE_COLS;
+    const uint64_t n_windows = (eoff[n_edges] + TAPS_TILE_COLS * TAPS_WIN_TILES - 1) /
+                               (TAPS_TILE_COLS * TAPS_WIN_TILES);
     if (n_points > 1 && !hier &&
         (st = sc.alloc((void **)&d_win, sizeof(uint32_t) * n_windows)) != TAPS_OK)
         return st;

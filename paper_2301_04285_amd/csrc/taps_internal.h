@@ -50,11 +50,14 @@ struct taps_copy_task {
 // remainders keeps the longer segments from stretching the end of the launch
 // (1, 2, 4, 8, 16 and 32 tiles measured).  Launches with few segments use
 // TAPS_SEG_TILES_SHORT.  The bandwidth sweep, bound by its four sets of
-// stores per entry, does not use segments: it runs one wavefront per aligned
-// 64-entry window of the tables (k_edge_costs_sweep_win).
+// stores per entry, does not use segments: it runs one wavefront per window of
+// TAPS_WIN_TILES aligned 64-entry tiles of the tables (k_edge_costs_sweep_win).
 #define TAPS_TILE_COLS 64
 #define TAPS_SEG_TILES_LONG 8
 #define TAPS_SEG_TILES_SHORT 2
+#ifndef TAPS_WIN_TILES
+#define TAPS_WIN_TILES 2
+#endif
 #define TAPS_LONG_SEGS_MIN 32768   // long segments only when there are at least this many
 #define TAPS_ROWS_PER_BLOCK 2
 
@@ -119,9 +122,9 @@ struct taps_sweep {
     double inv_n_binter[TAPS_MAX_SWEEP];
     taps_table out[TAPS_MAX_SWEEP];
 };
-// The sweep over aligned 64-entry windows of the concatenated tables (eoff:
-// device, n_edges + 1 entry offsets; win_edge: device scratch of one uint32
-// per window, ceil(total / 64)).
+// The sweep over aligned windows of TAPS_WIN_TILES 64-entry tiles of the
+// concatenated tables (eoff: device, n_edges + 1 entry offsets; win_edge:
+// device scratch of one uint32 per window, ceil(total / (64 TAPS_WIN_TILES))).
 hipError_t taps_launch_edge_costs_sweep_win(const taps_edge_params *params, uint32_t n_edges,
                                             const uint64_t *eoff, uint64_t total,
                                             uint32_t *win_edge, const taps_desc *desc,

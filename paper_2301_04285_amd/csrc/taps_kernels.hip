@@ -415,18 +415,19 @@ __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_co
 // Several bandwidth points: the candidates of each entry are costed once and
 // selected, scaled and stored once per point.
 //
-// The sweep runs over aligned windows: wavefront w handles the 64 entries
-// [64 w, 64 w + 64) of the concatenated tables (lane l entry 64 w + l), so
-// every store covers whole 128-byte lines (store-only kernels of the sweep's
-// four tables: 5.75 TB/s this way against 2.7-3.4 TB/s for row segments that
-// start inside a line).  A window that crosses rows (or edges) is taken row by
-// row: the wavefront builds each row's producer side in turn and the lanes of
-// that row compute their entries.  win_edge[w] is the edge holding entry 64 w.
+// The sweep runs over aligned windows: wavefront w handles the entries
+// [64 T w, 64 T (w + 1)) of the concatenated tables (T = TAPS_WIN_TILES), one
+// 64-entry tile at a time (lane l entry 64 t + l of the tile), so every store
+// covers whole 128-byte lines (store-only kernels of the sweep's four tables:
+// 5.75 TB/s this way against 2.7-3.4 TB/s for row segments that start inside a
+// line).  A tile that crosses rows (or edges) is taken row by row; the
+// wavefront builds a row's producer side once and keeps it while the row
+// continues into the next tile.  win_edge[w] is the edge holding entry 64 T w.
 __global__ void k_window_edges(const uint64_t *__restrict__ eoff, uint32_t n_edges,
                                uint64_t n_windows, uint32_t *__restrict__ win_edge) {
     const uint64_t w = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (w >= n_windows) return;
-    const uint64_t g = w * TAPS_TILE_COLS;
+    const uint64_t g = w * (TAPS_TILE_COLS * TAPS_WIN_TILES);
     // the last edge e with eoff[e] <= g (edges without entries share an offset
     // with the next one, so this is the edge that holds g)
     uint32_t lo = 0, hi = n_edges;   // eoff[lo] <= g < eoff[hi]
@@ -457,56 +458,68 @@ __global__ __launch_bounds__(TAPS_TILE_COLS *TAPS_ROWS_PER_BLOCK) void k_edge_co
     any.b_inter_red = sw.b_inter_red[0];
     any.b_intra_red = sw.b_intra_red[0];
     any.narrow = sw.narrow[0] != 0;
-    const uint64_t g0 = w * TAPS_TILE_COLS;
-    const uint32_t n_here = (uint32_t)(total - g0 < TAPS_TILE_COLS ? total - g0 : TAPS_TILE_COLS);
+    // the window: TAPS_WIN_TILES aligned tiles of 64 entries, [g_begin, g_end)
+    const uint64_t g_begin = w * (TAPS_TILE_COLS * TAPS_WIN_TILES);
+    const uint64_t g_end = total - g_begin < TAPS_TILE_COLS * TAPS_WIN_TILES
+                               ? total : g_begin + TAPS_TILE_COLS * TAPS_WIN_TILES;
     uint32_t e = win_edge[w];
     taps_edge_params E = params[e];
-    uint64_t local = g0 - E.out_offset;   // below ns * nd
+    const uint64_t local = g_begin - E.out_offset;   // below ns * nd
     uint32_t i = (uint32_t)(local / E.nd), j0 = (uint32_t)(local % E.nd);
-    uint32_t done = 0;   // lanes below this are handled
-    while (done < n_here) {   // uniform: one row of one edge per pass
-        __builtin_assume(E.rank <= R);
-        const uint32_t len = n_here - done < E.nd - j0 ? n_here - done : E.nd - j0;
-        if (len == 0) break;   // (cannot happen: entries remain only in edges that hold them)
-        taps_row P;
-        taps_make_row(P, desc[E.src_base + i], E.paxes, E.rank, lp.n, lp.lam);
-        // the row's producer-order table, written and read by this wavefront only
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        taps_fill_rank_table(P, rank_tab[wave], lane, TAPS_TILE_COLS);
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-        P.to_rank = rank_tab[wave];
-        P.widths = width_tab;
-        P.a2a = a2a_tab;
-        P.expand = expand_tab;
-        if (lane >= done && lane < done + len) {
-            const uint32_t j = j0 + (lane - done);
-            taps_col Q;
-            taps_make_col(Q, desc[E.dst_base + j], E.caxes, E.rank);
-            const taps_cands cands = taps_edge_candidates(P, Q, any);
-            for (uint32_t k = 0; k < sw.count; ++k) {
-                taps_keys K;
-                K.b_inter_red = sw.b_inter_red[k];
-                K.b_intra_red = sw.b_intra_red[k];
-                K.narrow = Narrow || sw.narrow[k] != 0;   // Narrow: 64-bit keys at every point
-                const taps_scaler S = taps_make_scaler(E.scale.tbytes, sw.inv_n_bintra[k],
-                                                       sw.inv_n_binter[k]);
-                const taps_entry_out o = taps_entry_finish(taps_pick_for(cands, K), S);
-                store_entry(sw.out[k], g0, lane, o, o.ok ? o.meta : 0xFFFFFFFFu);
+    taps_row P;
+    bool built = false;   // P (and this wavefront's rank table) hold row i of edge e
+    for (uint64_t g0 = g_begin; g0 < g_end; g0 += TAPS_TILE_COLS) {
+        const uint32_t n_here = (uint32_t)(g_end - g0 < TAPS_TILE_COLS ? g_end - g0 : TAPS_TILE_COLS);
+        uint32_t done = 0;   // lanes below this are handled
+        while (done < n_here) {   // uniform: one row of one edge per pass
+            __builtin_assume(E.rank <= R);
+            const uint32_t len = n_here - done < E.nd - j0 ? n_here - done : E.nd - j0;
+            if (len == 0) break;   // (cannot happen: entries remain only in edges that hold them)
+            if (!built) {
+                taps_make_row(P, desc[E.src_base + i], E.paxes, E.rank, lp.n, lp.lam);
+                // the row's producer-order table, written and read by this wavefront only
+                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+                __builtin_amdgcn_wave_barrier();
+                taps_fill_rank_table(P, rank_tab[wave], lane, TAPS_TILE_COLS);
+                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+                __builtin_amdgcn_wave_barrier();
+                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+                P.to_rank = rank_tab[wave];
+                P.widths = width_tab;
+                P.a2a = a2a_tab;
+                P.expand = expand_tab;
+                built = true;
             }
-        }
-        done += len;
-        j0 += len;
-        if (done < n_here && j0 == E.nd) {   // next row, or the next edge with entries
-            j0 = 0;
-            if (++i == E.ns) {
-                i = 0;
-                do {
-                    ++e;
-                    E = params[e];
-                } while (e + 1u < n_edges && (uint64_t)E.ns * E.nd == 0u);
+            if (lane >= done && lane < done + len) {
+                const uint32_t j = j0 + (lane - done);
+                taps_col Q;
+                taps_make_col(Q, desc[E.dst_base + j], E.caxes, E.rank);
+                const taps_cands cands = taps_edge_candidates(P, Q, any);
+                for (uint32_t k = 0; k < sw.count; ++k) {
+                    taps_keys K;
+                    K.b_inter_red = sw.b_inter_red[k];
+                    K.b_intra_red = sw.b_intra_red[k];
+                    K.narrow = Narrow || sw.narrow[k] != 0;   // Narrow: 64-bit keys at every point
+                    const taps_scaler S = taps_make_scaler(E.scale.tbytes, sw.inv_n_bintra[k],
+                                                           sw.inv_n_binter[k]);
+                    const taps_entry_out o = taps_entry_finish(taps_pick_for(cands, K), S);
+                    store_entry(sw.out[k], g0, lane, o, o.ok ? o.meta : 0xFFFFFFFFu);
+                }
+            }
+            done += len;
+            j0 += len;
+            // the row is done and entries remain in the window: the next row, or
+            // the first row of the next edge with entries
+            if (j0 == E.nd && g0 + done < g_end) {
+                j0 = 0;
+                built = false;
+                if (++i == E.ns) {
+                    i = 0;
+                    do {
+                        ++e;
+                        E = params[e];
+                    } while (e + 1u < n_edges && (uint64_t)E.ns * E.nd == 0u);
+                }
             }
         }
     }
@@ -730,7 +743,8 @@ hipError_t taps_launch_edge_costs_sweep_win(const taps_edge_params *params, uint
                                             const taps_launch &lp, uint32_t max_rank,
                                             const taps_sweep &sw, hipStream_t stream) {
     if (total == 0) return hipSuccess;
-    const uint64_t n_windows = (total + TAPS_TILE_COLS - 1) / TAPS_TILE_COLS;
+    const uint64_t span = TAPS_TILE_COLS * TAPS_WIN_TILES;
+    const uint64_t n_windows = (total + span - 1) / span;
     hipLaunchKernelGGL(k_window_edges, dim3(blocks_for(n_windows, 256)), dim3(256), 0, stream, eoff,
                        n_edges, n_windows, win_edge);
     const hipError_t err = hipGetLastError();
