@@ -50,3 +50,25 @@ def test_library_host_code_under_sanitizers(tmp_path):
                     os.path.join(HERE, "sanitize", "abi_driver.cpp"), "-o", exe],
                    check=True, capture_output=True, timeout=600)
     assert "0 failures" in _run(exe)
+
+
+def test_batched_alltoall_closed_forms(tmp_path):
+    """The edge kernels' closed-form AllToAll costing (byte dot products over
+    shard-fraction tables) against axis-by-axis costing from the definitions,
+    on every closure of every tops mask (two classes) and on random
+    hierarchies of link classes; host build of the device header, under the
+    sanitizers."""
+    hipcc = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
+    if not os.path.exists(hipcc):
+        pytest.skip("hipcc not available")
+    exe = str(tmp_path / "closed_forms")
+    subprocess.run([hipcc, "-x", "hip", "--offload-arch=gfx950", "-O1", "-g", "-std=c++17",
+                    "-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+                    "-Xarch_host", "-fno-sanitize-recover=undefined",
+                    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+                    "-I", os.path.join(ROOT, "include"), "-I", CSRC,
+                    os.path.join(HERE, "sanitize", "closed_forms.cpp"), "-o", exe],
+                   check=True, capture_output=True, timeout=600)
+    out = _run(exe)
+    assert " 0 mismatches" in out, out
+    assert int(out.split()[0]) > 150_000
