@@ -99,7 +99,7 @@ int main() {
                         const uint32_t unused = rnd() & full;
                         taps_fac got;
                         taps_fac_zero(got);
-                        taps_a2a_batch(got, x, L, lam, sh, unused, rows, expand);
+                        taps_a2a_batch(got, x, L, lam, taps_below(lam), sh, unused, rows, expand);
                         const taps_fac want = two_class_reference(tp, x, lam, sh, unused, n);
                         ++closures;
                         if (!same(got, want)) {
