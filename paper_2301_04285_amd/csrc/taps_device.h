@@ -433,6 +433,7 @@ struct taps_row {
     uint32_t dstr;                  // dimension whose run holds levels lam - 1 and lam (8: none)
     uint32_t split;                 // bit d: the producer splits dimension d (pr[d] != 0)
     uint32_t vlam, vlow;            // lam and taps_below(lam) for the per-lane arithmetic (taps_vcopy)
+    uint32_t vpr[TAPS_D_MAX_RANK];  // pr, likewise
     // Producer positions in order (dimension ascending, then bit ascending,
     // i.e. level descending): rank r holds level nibble r of `order`;
     // to_rank[x] is the level mask x with level l moved to bit rank(l).
@@ -517,7 +518,7 @@ __host__ __device__ inline void taps_unify(const taps_row &P, const taps_col &Q,
         // producer levels whose consumer level (l + dl) the consumer splits in
         // d: the top min(pw, cw) levels of the producer's run (the run moved
         // down by dl: (cr << 8) >> sh)
-        const uint32_t pt = P.pr[d] & (Q.cr8[d] >> sh);
+        const uint32_t pt = P.vpr[d] & (Q.cr8[d] >> sh);
         L.pt[d] = pt;
         tgt |= pt;
         // the cut positions inside that part (all its levels but the lowest),
@@ -561,21 +562,29 @@ __host__ __device__ inline void taps_unify(const taps_row &P, const taps_col &Q,
 }
 
 // Consumer tops whose target position an axis in ats (producer tops) holds.
+// Each term lies in bits 8-15 (16-bit shifts; pt[d] is 0 where sh[d] is 16 or
+// d >= rank), and two dimensions at a time join the sum in one three-way or.
 __host__ __device__ inline uint32_t taps_blocked(const taps_row &P, const taps_lv &L,
                                                  uint32_t ats) {
     // dimension 0 unconditionally: without one, pt[0] is 0 and so is its term
-    uint32_t acc = (ats & L.pt[0]) << L.sh[0];
+    uint32_t acc = taps_shl16(ats & L.pt[0], L.sh[0]);
 #pragma unroll
-    for (uint32_t d = 1; d < TAPS_D_MAX_RANK; ++d) {
+    for (uint32_t d = 1; d < TAPS_D_MAX_RANK; d += 2) {
         if (d >= P.rank) break;
-        acc = ((ats & L.pt[d]) << L.sh[d]) | acc;
+        const uint32_t t = taps_shl16(ats & L.pt[d], L.sh[d]);
+        const uint32_t u = d + 1u < TAPS_D_MAX_RANK ? taps_shl16(ats & L.pt[d + 1u], L.sh[d + 1u]) : 0u;
+        acc = taps_or3(t, u, acc);
     }
     return acc >> 8;
 }
 
 // The level holding producer-order rank k.
 __host__ __device__ inline uint32_t taps_rank_level(const taps_row &P, uint32_t k) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    return __builtin_amdgcn_ubfe(P.order, taps_x4(k), 4u);
+#else
     return (P.order >> (4u * k)) & 15u;
+#endif
 }
 
 // The level holding producer-order rank k mod 8 (k < 16): v_bfe_u32 reads
@@ -1036,7 +1045,7 @@ __host__ __device__ inline taps_fac taps_remove(const taps_row &P, const taps_lv
 #pragma unroll
     for (uint32_t d = 0; d < TAPS_D_MAX_RANK; ++d) {
         if (!((P.split >> d) & 1u)) continue;   // nothing of G in a dimension left whole
-        const uint32_t pd = P.pr[d];
+        const uint32_t pd = P.vpr[d];
         const uint32_t WA = taps_popc(GA & pd), WB = taps_popc(GB & pd);
         const uint32_t nA = taps_popc(TA & pd);
         uint32_t WS = 0;
@@ -1278,6 +1287,8 @@ __host__ __device__ inline void taps_make_row(taps_row &P, const taps_desc &D, u
     P.e0 = n - used;
     P.vlam = taps_vcopy(lam);
     P.vlow = taps_vcopy(taps_below(lam));
+#pragma unroll
+    for (uint32_t d = 0; d < TAPS_D_MAX_RANK; ++d) P.vpr[d] = taps_vcopy(P.pr[d]);
     P.split = 0;
 #pragma unroll
     for (uint32_t d = 0; d < TAPS_D_MAX_RANK; ++d) P.split |= (P.pr[d] ? 1u : 0u) << d;
