@@ -92,16 +92,26 @@ __host__ __device__ inline uint32_t taps_low(uint32_t w) {
 #endif
 }
 
-// 4 k for k < 16 (a nibble's bit offset): one v_lshlrev_b16 with the shift as
-// an inline constant.
-__host__ __device__ inline uint32_t taps_x4(uint32_t k) {
+// x << K for a result below 2^16, the shift an inline constant.
+template <uint32_t K>
+__host__ __device__ inline uint32_t taps_shl16c(uint32_t x) {
 #if defined(__HIP_DEVICE_COMPILE__)
     uint32_t r;
-    __asm__("v_lshlrev_b16 %0, 2, %1" : "=v"(r) : "v"(k));
+    __asm__("v_lshlrev_b16 %0, %2, %1" : "=v"(r) : "v"(x), "i"(K));
     return r;
 #else
-    return (k << 2) & 0xFFFFu;
+    return (x << K) & 0xFFFFu;
 #endif
+}
+
+// 4 k for k < 16 (a nibble's bit offset).
+__host__ __device__ inline uint32_t taps_x4(uint32_t k) { return taps_shl16c<2>(k); }
+
+// Entry i (< 2^16 / sizeof(T)) of a small table: the byte offset by a 16-bit shift.
+template <uint32_t LogSize, typename T>
+__host__ __device__ inline const T &taps_entry(const T *tab, uint32_t i) {
+    static_assert(sizeof(T) == (1u << LogSize), "entry size");
+    return *(const T *)((const char *)tab + taps_shl16c<LogSize>(i));
 }
 
 // A uniform value copied into a vector register: the per-lane arithmetic then
@@ -546,7 +556,7 @@ __host__ __device__ inline void taps_unify(const taps_row &P, const taps_col &Q,
     }
     const uint32_t starts = (C | 1u) & P.full;
     L.tp = P.n ? ((starts >> 1) | (1u << (P.n - 1))) & P.full : 0u;
-    L.wt = P.widths[L.tp];
+    L.wt = taps_entry<2>(P.widths, L.tp);
     L.p1 = ~(starts >> 1) & P.full;
     L.p2 = L.p1 & (L.p1 >> 1);
     L.p4 = L.p2 & (L.p2 >> 2);
@@ -666,8 +676,8 @@ __host__ __device__ inline void taps_a2a_batch(taps_fac &c, uint32_t x, const ta
     // table by tops mask, m's bits as bytes from another; two byte dot products
     // sum them, all axes and the in-node ones (tops below lam).
     const uint32_t m = x & ~L.st;
-    const taps_a2a_row W = a2a[L.tp];
-    const taps_pair X = expand[m];
+    const taps_a2a_row W = taps_entry<4>(a2a, L.tp);
+    const taps_pair X = taps_entry<3>(expand, m);
     const uint32_t f_all = taps_dot4(W.all_hi, X.hi, taps_dot4(W.all_lo, X.lo, 0u));
     const uint32_t f_in = taps_dot4(W.in_hi, X.hi, taps_dot4(W.in_lo, X.lo, 0u));
     const uint32_t n_in = taps_popc(m & low), n_out = taps_popc(m & ~low);
@@ -788,7 +798,7 @@ __host__ __device__ inline void taps_gather(const taps_lv &L, taps_state &s, typ
                                             uint32_t top, const Cm &M) {
     const taps_ax a = taps_axis(L, top);
     M.gather(c, top, a, s.sh, s.unused);
-    s.ats &= ~(1u << top);
+    s.ats &= ~taps_bit16(top);
     s.unused |= a.lv;
     s.sh += a.w;
 }
@@ -911,7 +921,7 @@ __host__ __device__ inline taps_run_t<typename Cm::fac> taps_alg1_t(const taps_r
     // gathers one held axis, so at most |held| rounds run.
     while (s.ats) {
         const uint32_t top = taps_first_src(P, s.ats);
-        s.blk &= ~taps_blocked(P, L, 1u << top);
+        s.blk &= ~taps_blocked(P, L, taps_bit16(top));
         taps_gather(L, s, c, top, M);
         if (!s.ats) break;
         taps_alg1_pass(P, L, s, c, n_a2a, M);
@@ -979,7 +989,7 @@ __host__ __device__ inline taps_run_t<typename Cm::fac> taps_rearrange_t(const t
         // sliced back into its own target if that is free (shard and free levels
         // as before: all ones then), else kept whole
         const uint32_t back = taps_bit_mask(L.dst & ~s.blk, top);
-        s.atd |= b & back;
+        s.atd = taps_and_or(b, back, s.atd);
         s.unused |= a.lv & ~back;
         s.sh += a.w & ~back;
         const uint32_t sf = freed_for & ~(s.ats | s.atd);   // sliced into the freed position
