@@ -748,7 +748,7 @@ __host__ __device__ inline bool taps_hopeless(const taps_fac &c, const taps_limi
 template <class Fac>
 struct taps_run_t {
     Fac c;
-    uint32_t n_a2a;   // AllToAlls issued
+    uint32_t a2a_tops;   // tops of the axes moved by an AllToAll (0: none)
     bool ok;          // false if the loop did not settle (cannot happen)
     bool stopped;     // stopped early: cannot beat the limit it was given
 };
@@ -837,7 +837,7 @@ __host__ __device__ inline uint32_t taps_slice(const taps_lv &L, taps_state &s) 
 template <class Cm>
 __host__ __device__ inline void taps_alg1_settle(const taps_row &P, const taps_lv &L,
                                                  taps_state &s, typename Cm::fac &c,
-                                                 uint32_t &n_a2a, const Cm &M, uint32_t sl) {
+                                                 uint32_t &a2a_tops, const Cm &M, uint32_t sl) {
     // The closure as a frontier: the held axes with a target whose target is
     // free move first; each move frees the target its position blocked (each
     // target is blocked by at most one held axis), and exactly the held axes
@@ -854,7 +854,7 @@ __host__ __device__ inline void taps_alg1_settle(const taps_row &P, const taps_l
         s.ats &= ~moved;
         s.blk &= ~freed;
         s.atd |= moved;
-        n_a2a += taps_popc(moved);
+        a2a_tops |= moved;
         M.a2a(c, moved, L, s.sh, s.unused);
     }
     if (sl) taps_slice(L, s);
@@ -862,10 +862,10 @@ __host__ __device__ inline void taps_alg1_settle(const taps_row &P, const taps_l
 
 template <class Cm>
 __host__ __device__ inline void taps_alg1_pass(const taps_row &P, const taps_lv &L, taps_state &s,
-                                               typename Cm::fac &c, uint32_t &n_a2a,
+                                               typename Cm::fac &c, uint32_t &a2a_tops,
                                                const Cm &M) {
     const uint32_t sl = taps_slice(L, s);
-    taps_alg1_settle(P, L, s, c, n_a2a, M, sl);
+    taps_alg1_settle(P, L, s, c, a2a_tops, M, sl);
 }
 
 // The common start of the sequences: every axis not at its target held at its
@@ -896,8 +896,8 @@ __host__ __device__ inline taps_run_t<typename Cm::fac> taps_alg1_t(const taps_r
     typename Cm::fac c;
     taps_fac_zero(c);
     taps_state s = b.s;
-    uint32_t n_a2a = 0;
-    taps_alg1_settle(P, L, s, c, n_a2a, M, b.slice);
+    uint32_t a2a_tops = 0;
+    taps_alg1_settle(P, L, s, c, a2a_tops, M, b.slice);
     // Nothing held at a producer position: only slices remain, and they cost
     // nothing.  Otherwise InferAllGather first gathers the held axes at
     // positions no consumer axis targets.  Such a gather frees no position
@@ -924,11 +924,11 @@ __host__ __device__ inline taps_run_t<typename Cm::fac> taps_alg1_t(const taps_r
         s.blk &= ~taps_blocked(P, L, taps_bit16(top));
         taps_gather(L, s, c, top, M);
         if (!s.ats) break;
-        taps_alg1_pass(P, L, s, c, n_a2a, M);
+        taps_alg1_pass(P, L, s, c, a2a_tops, M);
     }
     taps_run_t<typename Cm::fac> r;
     r.c = c;
-    r.n_a2a = n_a2a;
+    r.a2a_tops = a2a_tops;
     r.ok = true;
     r.stopped = false;
     return r;
@@ -1002,7 +1002,7 @@ __host__ __device__ inline taps_run_t<typename Cm::fac> taps_rearrange_t(const t
     }
     taps_run_t<typename Cm::fac> r;
     r.c = c;
-    r.n_a2a = 0;
+    r.a2a_tops = 0;
     r.ok = true;
     r.stopped = stopped;
     return r;
@@ -1058,10 +1058,11 @@ __host__ __device__ inline taps_fac taps_remove(const taps_row &P, const taps_lv
         const uint32_t pd = P.vpr[d];
         const uint32_t WA = taps_popc(GA & pd), WB = taps_popc(GB & pd);
         const uint32_t nA = taps_popc(TA & pd);
-        uint32_t WS = 0;
+        uint32_t WS = 0, WL = WB;   // WL: gathered levels of d below lam
         if (d == P.dstr) {   // uniform: the only dimension that can hold the straddler
             // without one (WS = 0) both terms are 0
             WS = taps_popc(G & S);
+            WL += taps_popc(G & S & low);
             const uint32_t lctS = taps_popc(taps_low(lo_s) & ~unused);
             c.inter += taps_bfm(WS, sh + WA) << lctS;
             c.ct += (WS < 1u ? WS : 1u) << lctS;
@@ -1070,9 +1071,8 @@ __host__ __device__ inline taps_fac taps_remove(const taps_row &P, const taps_lv
         c.inter += taps_bfm(WA, sh) << lctA;
         c.ct += nA << lctA;
         sh += WA + WB + WS;
-        const uint32_t Gd = G & pd;
-        unused |= Gd;
-        lctA -= taps_popc(Gd & low);
+        unused |= G & pd;
+        lctA -= WL;
     }
     return c;
 }
@@ -1151,7 +1151,7 @@ __host__ __device__ inline taps_pick taps_edge_select(const taps_row &P, const t
     lim.key = taps_key64(k.best, K);
     lim.vol = k.vmin;
     lim.intra = lim.inter = 0;
-    if (r0.n_a2a) {   // without AllToAll the sequence would be the same
+    if (r0.a2a_tops) {   // without AllToAll the sequence would be the same
         const taps_run r1 = taps_rearrange(P, Q, L, lim, K, b);
         k.ok = k.ok && r1.ok;
         if (!r1.stopped) {
@@ -1197,7 +1197,7 @@ __host__ __device__ inline taps_cands taps_edge_candidates(const taps_row &P, co
     k.ok = r0.ok;
     k.vmin = r0.c.vol;
     k.coll = taps_collectives(L, P.lam);
-    k.has_rearrange = r0.n_a2a != 0;   // without AllToAll the sequence would be the same
+    k.has_rearrange = r0.a2a_tops != 0;   // without AllToAll the sequence would be the same
     taps_fac_zero(k.c[1]);
     if (k.has_rearrange) {
         taps_limit lim;
@@ -1565,7 +1565,7 @@ __host__ __device__ inline taps_pickh taps_edge_select_h(const taps_row &P, cons
     k.coll = taps_collectives_h(L, H);
     k.ok = r0.ok;
     uint64_t best_key = taps_fach_key<C>(r0.c, H);
-    if (r0.n_a2a) {   // without AllToAll the sequence would be the same
+    if (r0.a2a_tops) {   // without AllToAll the sequence would be the same
         M.lim_on = true;
         M.lim_key = best_key;
         M.lim_vol = k.vmin;
