@@ -85,25 +85,65 @@ def measured_traffic(fields):
     return int(fields["traffic_bytes_per_launch"]) if fields else None
 
 
+# calibration kinds of the fast class (taps_calibrate_valu_name): v_bitop3_b32,
+# v_lshlrev_b16, v_lshrrev_b32, v_and_b32 -- the highest issue rates measured
+FAST_KINDS = (2, 5, 7, 10)
+
+
 def valu_ceiling() -> dict:
     """Issue rates (wavefront VALU instructions per second, whole GPU) of the
-    calibration kernels: plain 32-bit adds and xors on vector operands (the
-    fastest class on gfx950) and 3-operand / bit-field operations."""
+    calibration kernels: plain 32-bit adds and xors on vector operands,
+    3-operand / bit-field operations (the slow class), and the fastest of the
+    single-instruction fast-class kernels (the ceiling the edge kernel is
+    measured against)."""
     import ctypes as C
     lib = C.CDLL(os.path.join(ROOT, "paper_2301_04285_amd", "libtaps_calibrate.so"))
     lib.taps_calibrate_valu.restype = C.c_int
     lib.taps_calibrate_valu.argtypes = [C.c_int, C.c_uint32, C.POINTER(C.c_float),
                                         C.POINTER(C.c_double), C.POINTER(C.c_uint32)]
-    out = {}
-    for kind, name in ((0, "add_xor"), (1, "bfe_lshl_or")):
+    lib.taps_calibrate_valu_name.restype = C.c_char_p
+
+    def rate(kind):
+        ms, n, simds = C.c_float(), C.c_double(), C.c_uint32()
+        rc = lib.taps_calibrate_valu(kind, 2000, C.byref(ms), C.byref(n), C.byref(simds))
+        if rc != 0:
+            raise RuntimeError(f"taps_calibrate_valu({kind}) failed: {rc}")
+        r = n.value / (ms.value * 1e-3)
+        return {"instr_per_s": r, "per_simd_per_cycle_at_2p4GHz": r / simds.value / 2.4e9,
+                "ms": ms.value, "instructions": lib.taps_calibrate_valu_name(kind).decode()}
+
+    rate(0)   # warm-up
+    out = {"add_xor": rate(0), "bfe_lshl_or": rate(1)}
+    out["fastest"] = max((rate(k) for k in FAST_KINDS), key=lambda r: r["instr_per_s"])
+    return out
+
+
+def valu_classes() -> int:
+    """Issue rate of every instruction kind of the calibration library, relative
+    to the first (v_add_u32 / v_xor_b32), as one JSON line per kind."""
+    import ctypes as C
+    import torch
+    torch.cuda.init()
+    lib = C.CDLL(os.path.join(ROOT, "paper_2301_04285_amd", "libtaps_calibrate.so"))
+    lib.taps_calibrate_valu.restype = C.c_int
+    lib.taps_calibrate_valu.argtypes = [C.c_int, C.c_uint32, C.POINTER(C.c_float),
+                                        C.POINTER(C.c_double), C.POINTER(C.c_uint32)]
+    lib.taps_calibrate_valu_name.restype = C.c_char_p
+    base = None
+    ms, n, simds = C.c_float(), C.c_double(), C.c_uint32()
+    lib.taps_calibrate_valu(0, 2000, C.byref(ms), C.byref(n), C.byref(simds))   # warm-up
+    for kind in range(lib.taps_calibrate_valu_kinds()):
         ms, n, simds = C.c_float(), C.c_double(), C.c_uint32()
         rc = lib.taps_calibrate_valu(kind, 2000, C.byref(ms), C.byref(n), C.byref(simds))
         if rc != 0:
             raise RuntimeError(f"taps_calibrate_valu({kind}) failed: {rc}")
         rate = n.value / (ms.value * 1e-3)
-        out[name] = {"instr_per_s": rate, "per_simd_per_cycle_at_2p4GHz":
-                     rate / simds.value / 2.4e9, "ms": ms.value}
-    return out
+        base = base or rate
+        print(json.dumps({"kind": kind, "instructions": lib.taps_calibrate_valu_name(kind).decode(),
+                          "instr_per_s": rate, "cycles_per_instr_per_simd_at_2p4GHz":
+                          simds.value * 2.4e9 / rate, "relative_rate": rate / base,
+                          "ms": ms.value}), flush=True)
+    return 0
 
 
 def measured_valu(fields, kernel_ms: float, ceiling):
@@ -118,10 +158,12 @@ def measured_valu(fields, kernel_ms: float, ceiling):
            "achieved": rate, "unit": "wavefront VALU instructions/s",
            "source": os.path.relpath(COUNTERS, ROOT)}
     if ceiling:
-        out["peak"] = ceiling["add_xor"]["instr_per_s"]
+        out["peak"] = ceiling["fastest"]["instr_per_s"]
         out["frac"] = rate / out["peak"]
-        out["peak_source"] = ("calibration kernel: 8 independent chains of v_add_u32/v_xor_b32 "
-                              "per thread, 8 wavefronts per SIMD (libtaps_calibrate.so)")
+        out["peak_source"] = ("calibration kernels: 8 independent chains of one instruction per "
+                              "thread, 8 wavefronts per SIMD (libtaps_calibrate.so); the fastest "
+                              "fast-class kernel, " + ceiling["fastest"]["instructions"])
+        out["add_xor_peak"] = ceiling["add_xor"]["instr_per_s"]
         out["slow_class_peak"] = ceiling["bfe_lshl_or"]["instr_per_s"]
     return out
 
@@ -225,10 +267,15 @@ def main() -> int:
                     help="also time the build under the workload's hierarchy of link classes "
                          "(taps_node_costs_topology, taps_edge_costs_topology) and report it "
                          "under link_classes (0 = skip)")
+    ap.add_argument("--valu-classes", action="store_true",
+                    help="only time every instruction kind of libtaps_calibrate.so (issue rates "
+                         "per class), print one JSON line per kind, then exit")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES bytes (to scale HBM "
                          "traffic counters), then exit")
     args = ap.parse_args()
+    if args.valu_classes:
+        return valu_classes()
     if args.copy_calibration:
         import torch
         src = torch.ones(args.copy_calibration // 4, dtype=torch.int32, device="cuda")
@@ -329,8 +376,10 @@ def main() -> int:
     bytes_per_launch = BYTES_PER_ENTRY * entries
     counters = counter_summary()
     ceiling = valu_ceiling()
-    log(f"[bench] VALU ceiling: {ceiling['add_xor']['instr_per_s']:.4g} instr/s "
-        f"({ceiling['add_xor']['per_simd_per_cycle_at_2p4GHz']:.3f} per SIMD per cycle), "
+    log(f"[bench] VALU ceiling: {ceiling['fastest']['instr_per_s']:.4g} instr/s "
+        f"({ceiling['fastest']['instructions']}, "
+        f"{ceiling['fastest']['per_simd_per_cycle_at_2p4GHz']:.3f} per SIMD per cycle), "
+        f"add/xor {ceiling['add_xor']['instr_per_s']:.4g}, "
         f"slow class {ceiling['bfe_lshl_or']['instr_per_s']:.4g}")
     achieved = bytes_per_launch / (kernel_ms * 1e-3) / 1e9
     out = {

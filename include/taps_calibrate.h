@@ -11,13 +11,21 @@
 extern "C" {
 #endif
 
+/* Number of instruction kinds taps_calibrate_valu times (0 .. count - 1). */
+int taps_calibrate_valu_kinds(void);
+
+/* The instruction(s) of a kind, a static string; NULL for a kind out of range. */
+const char *taps_calibrate_valu_name(int kind);
+
 /* Times a kernel of 8 independent dependency chains of one 32-bit integer
  * VALU instruction class per thread, at 8 wavefronts per SIMD on every CU of
  * the current device, `iters` loop iterations of 128 instructions each (the
  * best of three launches on the null stream; the call synchronises).
  *   kind  0: v_add_u32 / v_xor_b32 on vector operands (the highest-rate class
  *            on gfx950); 1: v_bfe_u32 / v_lshl_or_b32 (3-operand and
- *            bit-field operations).
+ *            bit-field operations); 2 and up: one instruction each
+ *            (taps_calibrate_valu_name), the classes the edge kernels'
+ *            choice of instructions rests on.
  *   ms                 out: the launch's duration in milliseconds.
  *   wave_instructions  out: wavefront instructions the launch issued.
  *   simds              out: SIMDs of the device (4 per CU).

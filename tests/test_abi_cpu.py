@@ -42,16 +42,25 @@ def test_calibration_library_exports_its_header():
     import re
     root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
     header = open(os.path.join(root, "include", "taps_calibrate.h")).read()
-    declared = re.findall(r"^int (taps_\w+)\(", header, flags=re.M)
-    assert declared == ["taps_calibrate_valu"]
+    declared = re.findall(r"^(?:int |const char \*)(taps_\w+)\(", header, flags=re.M)
+    assert declared == ["taps_calibrate_valu_kinds", "taps_calibrate_valu_name",
+                        "taps_calibrate_valu"]
     path = os.path.join(root, "paper_2301_04285_amd", "libtaps_calibrate.so")
     out = subprocess.run(["nm", "-D", "--defined-only", path], capture_output=True, text=True,
                          check=True).stdout
-    assert "taps_calibrate_valu" in {ln.split()[-1] for ln in out.splitlines() if ln.strip()}
+    exported = {ln.split()[-1] for ln in out.splitlines() if ln.strip()}
+    assert set(declared) <= exported
     cal = C.CDLL(path)
     cal.taps_calibrate_valu.restype = C.c_int
+    cal.taps_calibrate_valu_name.restype = C.c_char_p
+    kinds = cal.taps_calibrate_valu_kinds()
+    assert kinds == 13
+    names = [cal.taps_calibrate_valu_name(k).decode() for k in range(kinds)]
+    assert names[0] == "v_add_u32 / v_xor_b32" and len(set(names)) == kinds
+    assert cal.taps_calibrate_valu_name(kinds) is None and cal.taps_calibrate_valu_name(-1) is None
     ms, n, simds = C.c_float(), C.c_double(), C.c_uint32()
-    assert cal.taps_calibrate_valu(2, 10, C.byref(ms), C.byref(n), C.byref(simds)) == 1
+    assert cal.taps_calibrate_valu(kinds, 10, C.byref(ms), C.byref(n), C.byref(simds)) == 1
+    assert cal.taps_calibrate_valu(-1, 10, C.byref(ms), C.byref(n), C.byref(simds)) == 1
     assert cal.taps_calibrate_valu(0, 0, C.byref(ms), C.byref(n), C.byref(simds)) == 1
     assert cal.taps_calibrate_valu(0, 10, None, C.byref(n), C.byref(simds)) == 1
 
