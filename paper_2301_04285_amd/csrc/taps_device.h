@@ -107,6 +107,15 @@ __host__ __device__ inline uint32_t taps_shl16c(uint32_t x) {
 // 4 k for k < 16 (a nibble's bit offset).
 __host__ __device__ inline uint32_t taps_x4(uint32_t k) { return taps_shl16c<2>(k); }
 
+// Nibble k (< 8) of v, k per lane: one bit-field extract at a 16-bit-shifted offset.
+__host__ __device__ inline uint32_t taps_nib_at(uint32_t v, uint32_t k) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    return __builtin_amdgcn_ubfe(v, taps_x4(k), 4u);
+#else
+    return (v >> (4u * k)) & 15u;
+#endif
+}
+
 // Entry i (< 2^16 / sizeof(T)) of a small table: the byte offset by a 16-bit shift.
 template <uint32_t LogSize, typename T>
 __host__ __device__ inline const T &taps_entry(const T *tab, uint32_t i) {
@@ -1443,12 +1452,12 @@ struct taps_hier_model_t {
     // AllGather (Eq. 9) of the axis with top level `top`.
     __host__ __device__ void gather(fac &c, uint32_t top, const taps_ax &a, uint32_t sh,
                                     uint32_t unused) const {
-        const uint32_t V = ((1u << a.w) - 1u) << sh;
-        const uint32_t cls = taps_nib(H->cls_of_top, top);
-        const uint32_t lct = cls ? taps_hier_lct(a.lo, taps_nib(H->beta_of_top, top), unused) : 0u;
+        const uint32_t V = taps_bfm(a.w, sh);
+        const uint32_t cls = taps_nib_at(H->cls_of_top, top);
+        const uint32_t lct = cls ? taps_hier_lct(a.lo, taps_nib_at(H->beta_of_top, top), unused) : 0u;
         c.vol += V;
         taps_fach_add<C>(c, cls, V << lct);
-        c.ct += cls ? 1u << lct : 0u;
+        c.ct += cls ? taps_bit16(lct) : 0u;
     }
 
     // AllToAlls (Eq. 10, Eq. 14) of every axis whose top is in x, at one state:
@@ -1474,8 +1483,9 @@ struct taps_hier_model_t {
             cross |= (low_top & (0u - low_top)) & (((L.tp >> (b - 1u)) & 1u) - 1u);
         }
         const uint32_t m = x & ~cross;
-        const taps_pair X = expand[m];
-        const taps_pair *W = a2a_cls + (size_t)L.tp * TAPS_D_MAX_CLASSES;
+        const taps_pair X = taps_entry<3>(expand, m);
+        static_assert(sizeof(taps_pair) * TAPS_D_MAX_CLASSES == 32u, "class table row");
+        const taps_pair *W = (const taps_pair *)((const char *)a2a_cls + taps_shl16c<5>(L.tp));
         const uint32_t e = sh - 8u;
 #pragma unroll
         for (uint32_t k = 0; k < C; ++k) {
@@ -1498,8 +1508,8 @@ struct taps_hier_model_t {
             const uint32_t top = taps_ctz(r);
             const taps_ax a = taps_axis(L, top);
             const uint32_t V = (1u << sh) - (1u << (sh - a.w));
-            const uint32_t cls = taps_nib(H->cls_of_top, top);
-            const uint32_t beta = taps_nib(H->beta_of_top, top);
+            const uint32_t cls = taps_nib_at(H->cls_of_top, top);
+            const uint32_t beta = taps_nib_at(H->beta_of_top, top);
             const uint32_t kap = beta - a.lo;   // lo < beta for a crossing axis
             const uint32_t link = ((1u << a.w) - (1u << kap)) << (kap + sh - a.w);
             const uint32_t lct = taps_hier_lct(a.lo, beta, unused);
@@ -1510,7 +1520,7 @@ struct taps_hier_model_t {
     }
 
     __host__ __device__ bool hopeless(const fac &c) const {
-        return lim_on && c.vol >= lim_vol && taps_fach_key<C>(c, *H) >= lim_key;
+        return lim_on && ((c.vol >= lim_vol) & (taps_fach_key<C>(c, *H) >= lim_key));
     }
 };
 using taps_hier_model = taps_hier_model_t<TAPS_D_MAX_CLASSES>;
