@@ -125,7 +125,9 @@ __host__ __device__ inline const T &taps_entry(const T *tab, uint32_t i) {
 
 // A uniform value copied into a vector register: the per-lane arithmetic then
 // reads it from there (gfx950 issues a simple 32-bit operation with a scalar
-// register operand at about half the rate of one with vector operands).
+// register operand at about half the rate of one with vector operands).  x
+// must be the same in every lane of the wavefront (it is read from a scalar
+// register): taps_make_row, its only caller, runs on one row per wavefront.
 __host__ __device__ inline uint32_t taps_vcopy(uint32_t x) {
 #if defined(__HIP_DEVICE_COMPILE__)
     uint32_t r;
