@@ -944,6 +944,8 @@ def test_sweep_tables(T):
     sweep_check(T, w.graph, [cl for _, cl in w.clusters], w.name)
     w = W.config(2)
     sweep_check(T, w.graph, [W.Cluster(2, 8, 400 * W.GB, b * W.GB) for b in (50, 6, 400)], w.name)
+    # one point: the single-table launch (row segments, not windows)
+    sweep_check(T, w.graph, [W.Cluster(2, 8, 400 * W.GB, 50 * W.GB)], w.name + " one point")
     rng = random.Random(5151)
     n = 0
     while n < 10:
